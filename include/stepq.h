@@ -1,0 +1,184 @@
+/*
+ * stepq.h -- C ABI of the MI355X (gfx950) quantized gated-Delta decode step.
+ *
+ * The library keeps a pool of recurrent states S in R^{d_k x d_v}, one per
+ * (request slot, value head), stored as mixed-precision integer codes with
+ * per-tile key-row and value-column scales, and advances the active ones by
+ * one decode step in a single fused kernel launch.
+ *
+ * What one decode step computes (paper: Eq. 1 with the GDN gate D = alpha I,
+ * Eq. 3, Eq. 4, Section 4.3 and Appendix C, Table C2, with frozen scales):
+ *   S^_ij = r_i c_j q_ij / q_{b_i}                 reconstruction, q_b = 2^(b-1)-1
+ *   X     = alpha S^ + beta k (v - alpha S^T k)^T   gated Delta update
+ *   o     = X^T q                                  readout, taken before requantization
+ *   q'_ij = clip(round(X_ij q_{b_i} / (r_i c_j)), -q_{b_i}, q_{b_i})   round = ties-to-even
+ * and q' replaces q in place; r and c are left unchanged.
+ *
+ * Conventions for every call:
+ *  - Pointers named *_dev, and every array argument of the device calls, are
+ *    device memory of the current HIP device; the descriptor's tables and the
+ *    setup calls' arrays are host memory.  The caller owns all of it.
+ *  - `stream` is a hipStream_t (NULL = the null stream).  Device calls only
+ *    enqueue work on it and return; inputs must stay alive, and outputs must
+ *    not be read, until the stream has reached the work.
+ *  - A pool must not be used from two streams at once.  In one decode step
+ *    the slot ids must be distinct and in [0, n_slots): each (slot, head)
+ *    tile is rewritten in place by exactly one workgroup.  With the
+ *    environment variable STEPQ_DEBUG=1 this is checked on the host (a
+ *    synchronising copy of the ids) and violations return STEPQ_E_INVALID.
+ *  - Nothing is thrown across the ABI.  Invalid arguments return
+ *    STEPQ_E_INVALID before anything is enqueued; a failing HIP call returns
+ *    STEPQ_E_HIP.  stepq_last_error() describes the last failure of the
+ *    calling thread.
+ *
+ * ---------------------------------------------------------------------------
+ * Pool layout (what stepq_pool_device_ptr() points at)
+ *
+ * The pool is n_slots slot records of slot_bytes each, back to back.  A slot
+ * record is the tile records of value heads 0 .. n_v_heads-1 in order.  The
+ * tile record of head h, whose key rows have widths row_bits[h][0 .. d_k-1]
+ * (each 8, 4 or 2; the same for every slot, the paper's fixed precision map):
+ *
+ *  - Physical row order: the 8-bit rows in increasing logical row index,
+ *    then the 4-bit rows, then the 2-bit rows.  n8, n4, n2 = row counts.
+ *  - Row groups: each group holds 8/b physical rows of one width b -- one
+ *    8-bit row, two 4-bit rows or four 2-bit rows -- filled in physical
+ *    order.  A width's last group may have empty slots.  Groups are ordered
+ *    8-bit, 4-bit, 2-bit: G = n8 + ceil(n4/2) + ceil(n2/4).
+ *  - Codes region: G groups of d_v bytes each.  Byte j of a group holds
+ *    column j of all its rows: the row in slot s (0-based, in physical
+ *    order) occupies bits [s*b, s*b + b) as a b-bit two's-complement integer
+ *    in [-q_b, q_b]; empty slots are 0.  The region is zero-padded to a
+ *    multiple of 128 bytes.
+ *  - Then r: d_k fp32 row scales in physical row order; then c: d_v fp32
+ *    column scales.  The record is zero-padded to a multiple of 128 bytes.
+ *
+ * So a 6-bit tile (64 rows @8 + 64 rows @4, d = 128) is 12,288 code bytes +
+ * 1,024 scale bytes = 13,312 bytes, read once and its codes written once per
+ * decode step.  The code-carrying part of every group is one 128-byte line at
+ * d_v = 128, so a wavefront's dword load covers two whole lines.
+ */
+#ifndef STEPQ_H
+#define STEPQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    STEPQ_OK = 0,
+    STEPQ_E_INVALID = 1,      /* bad argument; nothing was enqueued */
+    STEPQ_E_UNSUPPORTED = 2,  /* well-formed but outside what the library implements */
+    STEPQ_E_NOMEM = 3,        /* device allocation failed */
+    STEPQ_E_HIP = 4           /* a HIP runtime call failed */
+} stepq_status;
+
+typedef enum {
+    STEPQ_F32 = 0,            /* activations as float */
+    STEPQ_BF16 = 1            /* activations as bfloat16 (upper half of a float) */
+} stepq_dtype;
+
+typedef struct stepq_pool stepq_pool;   /* opaque */
+
+typedef struct {
+    int32_t n_slots;          /* >= 1 */
+    int32_t n_v_heads;        /* Hv >= 1 */
+    int32_t n_qk_heads;       /* Hqk >= 1, Hv % Hqk == 0; value head h reads q/k head h / (Hv/Hqk) */
+    int32_t d_k;              /* key rows per tile, 1 .. 128 */
+    int32_t d_v;              /* value columns per tile, 64 or 128 */
+    const uint8_t *row_bits;  /* host [Hv][d_k], each 2, 4 or 8; copied by stepq_pool_create */
+} stepq_pool_desc;
+
+/* Size of the pool described by desc (layout above).  Either output may be
+ * NULL.  Host only, no device work. */
+stepq_status stepq_pool_bytes(const stepq_pool_desc *desc, size_t *pool_bytes, size_t *slot_bytes);
+
+/* Create a pool.  device_mem: caller-owned device memory of at least
+ * stepq_pool_bytes() bytes, 256-byte aligned, whose contents become the
+ * pool; or NULL, in which case the library allocates (and later frees) it.
+ * The pool contents are undefined until written by stepq_pool_load or
+ * stepq_pool_import.  Allocates the small per-head layout tables on the
+ * current device.  Blocks until they are copied. */
+stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, size_t device_mem_bytes,
+                               stepq_pool **out);
+
+/* Release the pool object, its layout tables and (only if the library
+ * allocated it) the pool memory.  Synchronises the device first.  NULL ok. */
+void stepq_pool_destroy(stepq_pool *pool);
+
+/* Raw pool memory (layout above), for saving, restoring or inspecting it. */
+void *stepq_pool_device_ptr(const stepq_pool *pool);
+
+/* Quantize and pack full-precision states into slots (the boundary pack after
+ * prefill).  For i < n: slot slot_ids[i] receives
+ *   q_hj = clip(round(state[i][h][j][:] q_b / (r c)), -q_b, q_b)
+ * with scales r (logical row order) and c stored alongside.
+ *   slot_ids [n] int32, state [n][Hv][d_k][d_v] fp32 (logical row order),
+ *   r [n][Hv][d_k] fp32 > 0, c [n][Hv][d_v] fp32 > 0.
+ * The rounding is taken in fp32. */
+stepq_status stepq_pool_load(stepq_pool *pool, const int32_t *slot_ids, int32_t n, const float *state,
+                             const float *r, const float *c, void *stream);
+
+/* One fused decode step for `batch` active requests (the update written out
+ * at the top of this header).  For b < batch, tile (slot_ids[b], h) reads
+ *   q[b][h/(Hv/Hqk)][:], k[b][h/(Hv/Hqk)][:]  (d_k each),  v[b][h][:] (d_v),
+ *   alpha[b][h], beta[b][h]
+ * in act_dtype (arrays [batch][Hqk][d_k], [batch][Hv][d_v], [batch][Hv]),
+ * writes o[b][h][:] (fp32, [batch][Hv][d_v]) and rewrites its codes in
+ * place.  All arithmetic is fp32.  batch == 0 is a no-op. */
+stepq_status stepq_decode_step(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
+                               const void *k, const void *v, const void *alpha, const void *beta,
+                               stepq_dtype act_dtype, float *o, void *stream);
+
+/* Reconstruct S^_ij = r_i c_j q_ij / q_{b_i} (Section 4.3) for n slots into
+ * out [n][Hv][d_k][d_v] fp32, logical row order.  Computed in fp32. */
+stepq_status stepq_pool_dequant(const stepq_pool *pool, const int32_t *slot_ids, int32_t n, float *out,
+                                void *stream);
+
+/* Unpack n slots to raw codes [n][Hv][d_k][d_v] int8 (logical row order) and
+ * scales r [n][Hv][d_k] (logical order), c [n][Hv][d_v].  Bit-exact. */
+stepq_status stepq_pool_export(const stepq_pool *pool, const int32_t *slot_ids, int32_t n, int8_t *codes,
+                               float *r, float *c, void *stream);
+
+/* Pack raw codes and scales (shapes as in stepq_pool_export) into n slots.
+ * Codes must lie in [-q_b, q_b] of their row; out-of-range fields are
+ * written modulo 2^b.  Bit-exact inverse of stepq_pool_export. */
+stepq_status stepq_pool_import(stepq_pool *pool, const int32_t *slot_ids, int32_t n, const int8_t *codes,
+                               const float *r, const float *c, void *stream);
+
+/* Last failure message of the calling thread ("" if none). */
+const char *stepq_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * CPU setup step (offline; host arrays, runs on the calling thread plus up to
+ * n_threads-1 helpers; n_threads <= 0 means all hardware threads).
+ */
+
+/* Fit per-tile scales to full-precision states (Section 4.3): row factors
+ *   m_i = (1/d_v) sum_j |S_ij|,   r_i = m_i^{1/2} w_i^{-1/2}
+ * and absmax column factors c_j = max_i |S_ij| / r_i, so r_i c_j >= |S_ij|
+ * (c is rounded upward to fp32 to keep that bound).  Both are floored at
+ * 2^-60 (the positive numerical floor of Appendix C.1).  Sums in double.
+ *   state [n_tiles][d_k][d_v], row_weight [n_tiles][d_k] (NULL: w = 1),
+ *   r [n_tiles][d_k], c [n_tiles][d_v] (outputs). */
+stepq_status stepq_setup_fit(int64_t n_tiles, int32_t d_k, int32_t d_v, const float *state,
+                             const float *row_weight, float *r, float *c, int32_t n_threads);
+
+/* Lifetime-aware bit allocation over key rows (Section 3.2, Eq. 6) with two
+ * candidate widths lo < hi and an average budget lo <= budget <= hi.
+ * gates [T][B][H] are calibration retention gates; each head's mean log
+ * retention l_h = mean over (t, b) of log gates (Appendix A.3) orders its
+ * rows.  With one distortion profile shared by all rows, Eq. 6 gives the wide
+ * code to the floor(N (budget-lo)/(hi-lo)) rows of largest l (ties by head,
+ * then row).  Output row_bits [H][d_k]. */
+stepq_status stepq_setup_lifetime_bits(const double *gates, int32_t T, int32_t B, int32_t H, int32_t d_k,
+                                       double budget, int32_t lo, int32_t hi, uint8_t *row_bits);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STEPQ_H */

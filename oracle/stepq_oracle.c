@@ -1,0 +1,351 @@
+/*
+ * Reference oracle for the quantized gated-Delta decode step.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and the
+ * cpu_baseline leg of bench.py may load or call this library.  It shares no
+ * code, header, table or helper with the HIP path: the pool layout below is
+ * re-derived here from its written definition in include/stepq.h.
+ *
+ * Everything is plain loops in double precision, in the order the paper
+ * states the computation.  OpenMP is used only across independent tiles.
+ *
+ * Notation (paper, Section 2): a tile is one (request, value head) state
+ * S in R^{d_k x d_v}; key rows i, value columns j.  Row i holds a b_i-bit
+ * signed integer code per entry with q_b = 2^(b-1) - 1 (Eq. 3).  The
+ * dual-axis representation (Section 4.3) reconstructs
+ *     S^_ij = r_i * c_j * z_ij ,   z_ij = q_ij / q_{b_i}
+ * i.e. the level set is normalised so that |S^_ij| <= r_i c_j at every
+ * width (this is the reading that makes "r_i c_j >= |S_ij|" the no-clip
+ * condition of a symmetric absmax fit).
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <string.h>
+#include <stdlib.h>
+
+static double qb_of(int b) { return (double)((1 << (b - 1)) - 1); }
+
+/* ------------------------------------------------------------------------
+ * Scale fit used by the setup step (Section 4.3, "Row factors"; the column
+ * factor in its absmax form).
+ *   m_i = (1/d_v) sum_j |S_ij|
+ *   r_i = m_i^{1/2} w_i^{-1/2}
+ *   c_j = max_i |S_ij| / r_i            (so that r_i c_j >= |S_ij|)
+ * A positive floor of 2^-60 keeps both factors strictly positive
+ * (Appendix C.1 asks for a positive numerical floor).  The results are
+ * rounded once to fp32, the storage precision of the scales.
+ * w == NULL means w_i = 1.
+ */
+void orc_fit_absmax(int n_tiles, int dk, int dv, const float *S, const double *w,
+                    float *r_out, float *c_out)
+{
+    const double floor_ = ldexp(1.0, -60);
+    #pragma omp parallel for schedule(static)
+    for (int t = 0; t < n_tiles; ++t) {
+        const float *St = S + (size_t)t * dk * dv;
+        double *r = (double *)malloc(sizeof(double) * dk);
+        for (int i = 0; i < dk; ++i) {
+            double m = 0.0;
+            for (int j = 0; j < dv; ++j) m += fabs((double)St[(size_t)i * dv + j]);
+            m /= (double)dv;
+            double wi = w ? w[(size_t)t * dk + i] : 1.0;
+            double ri = sqrt(m / wi);
+            if (ri < floor_) ri = floor_;
+            r_out[(size_t)t * dk + i] = (float)ri;
+            r[i] = (double)r_out[(size_t)t * dk + i];   /* the column fit sees the stored r */
+        }
+        for (int j = 0; j < dv; ++j) {
+            double cj = 0.0;
+            for (int i = 0; i < dk; ++i) {
+                double a = fabs((double)St[(size_t)i * dv + j]) / r[i];
+                if (a > cj) cj = a;
+            }
+            if (cj < floor_) cj = floor_;
+            /* stored rounded upward so that r_i c_j >= |S_ij| survives the
+               rounding to fp32 */
+            float cf = (float)cj;
+            if ((double)cf < cj) cf = nextafterf(cf, INFINITY);
+            c_out[(size_t)t * dv + j] = cf;
+        }
+        free(r);
+    }
+}
+
+/* ------------------------------------------------------------------------
+ * Quantizer (Eq. 3, applied to the dual-axis representation of Section 4.3):
+ *   q_ij = clip(round(X_ij * q_b / (r_i c_j)), -q_b, q_b)
+ * round = nearest, ties to even (nearbyint under the default rounding mode).
+ * bits: [n_tiles][dk].  y (optional) receives the unrounded X q_b/(r c).
+ */
+void orc_quantize(int n_tiles, int dk, int dv, const double *X, const float *r, const float *c,
+                  const uint8_t *bits, int8_t *codes, double *y)
+{
+    #pragma omp parallel for schedule(static)
+    for (int t = 0; t < n_tiles; ++t) {
+        for (int i = 0; i < dk; ++i) {
+            double qb = qb_of(bits[(size_t)t * dk + i]);
+            double ri = (double)r[(size_t)t * dk + i];
+            for (int j = 0; j < dv; ++j) {
+                size_t e = ((size_t)t * dk + i) * dv + j;
+                double s = X[e] * qb / (ri * (double)c[(size_t)t * dv + j]);
+                if (y) y[e] = s;
+                double n = nearbyint(s);
+                if (n > qb) n = qb;
+                if (n < -qb) n = -qb;
+                codes[e] = (int8_t)n;
+            }
+        }
+    }
+}
+
+/* Reconstruction (Section 4.3): S^_ij = r_i c_j q_ij / q_{b_i}. */
+void orc_dequant(int n_tiles, int dk, int dv, const int8_t *codes, const float *r, const float *c,
+                 const uint8_t *bits, double *S)
+{
+    #pragma omp parallel for schedule(static)
+    for (int t = 0; t < n_tiles; ++t)
+        for (int i = 0; i < dk; ++i) {
+            double qb = qb_of(bits[(size_t)t * dk + i]);
+            for (int j = 0; j < dv; ++j) {
+                size_t e = ((size_t)t * dk + i) * dv + j;
+                S[e] = (double)r[(size_t)t * dk + i] * (double)c[(size_t)t * dv + j] * (double)codes[e] / qb;
+            }
+        }
+}
+
+/* ------------------------------------------------------------------------
+ * Gated Delta update on a real-valued state, GDN gate D = alpha I
+ * (Eq. 1, first form, and the readout of Eq. 4 taken from X before any
+ * requantization):
+ *   R = alpha S                       retained state
+ *   e_j = v_j - sum_i k_i R_ij        residual of the retrieval k^T R
+ *   X_ij = R_ij + beta k_i e_j
+ *   o_j = sum_i X_ij q_i              (X^T q)
+ */
+static void update_tile(int dk, int dv, const double *S, const double *q, const double *k,
+                        const double *v, double alpha, double beta, double *X, double *o)
+{
+    for (int i = 0; i < dk; ++i)
+        for (int j = 0; j < dv; ++j) X[(size_t)i * dv + j] = alpha * S[(size_t)i * dv + j];
+    for (int j = 0; j < dv; ++j) {
+        double kr = 0.0;
+        for (int i = 0; i < dk; ++i) kr += k[i] * X[(size_t)i * dv + j];
+        double e = v[j] - kr;
+        for (int i = 0; i < dk; ++i) X[(size_t)i * dv + j] += beta * k[i] * e;
+    }
+    for (int j = 0; j < dv; ++j) {
+        double acc = 0.0;
+        for (int i = 0; i < dk; ++i) acc += X[(size_t)i * dv + j] * q[i];
+        o[j] = acc;
+    }
+}
+
+void orc_update_fp(int n_tiles, int dk, int dv, const double *S, const double *q, const double *k,
+                   const double *v, const double *alpha, const double *beta, double *X, double *o)
+{
+    #pragma omp parallel for schedule(static)
+    for (int t = 0; t < n_tiles; ++t)
+        update_tile(dk, dv, S + (size_t)t * dk * dv, q + (size_t)t * dk, k + (size_t)t * dk,
+                    v + (size_t)t * dv, alpha[t], beta[t], X + (size_t)t * dk * dv, o + (size_t)t * dv);
+}
+
+/* ------------------------------------------------------------------------
+ * One decode step on a quantized tile (Appendix C, Table C2, with frozen
+ * scales):  reconstruct S^ (step 1), X = alpha S^ + beta k (v - alpha k^T S^)
+ * (step 2), emit o = X^T q before requantization (step 3), requantize X on
+ * the same r, c and per-row widths (Eq. 3) as the new codes.
+ * y (optional) receives X q_b/(r c) before rounding.
+ */
+void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const float *r,
+                     const float *c, const uint8_t *bits, const double *q, const double *k,
+                     const double *v, const double *alpha, const double *beta,
+                     int8_t *codes_out, double *o, double *y)
+{
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int t = 0; t < n_tiles; ++t) {
+        size_t nel = (size_t)dk * dv;
+        double *Sh = (double *)malloc(sizeof(double) * nel);
+        double *X = (double *)malloc(sizeof(double) * nel);
+        const int8_t *ci = codes_in + (size_t)t * nel;
+        const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
+        const uint8_t *bt = bits + (size_t)t * dk;
+        for (int i = 0; i < dk; ++i) {
+            double qb = qb_of(bt[i]);
+            for (int j = 0; j < dv; ++j)
+                Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / qb;
+        }
+        update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
+                    alpha[t], beta[t], X, o + (size_t)t * dv);
+        for (int i = 0; i < dk; ++i) {
+            double qb = qb_of(bt[i]);
+            for (int j = 0; j < dv; ++j) {
+                double s = X[(size_t)i * dv + j] * qb / ((double)rt[i] * (double)ct[j]);
+                if (y) y[(size_t)t * nel + (size_t)i * dv + j] = s;
+                double n = nearbyint(s);
+                if (n > qb) n = qb;
+                if (n < -qb) n = -qb;
+                codes_out[(size_t)t * nel + (size_t)i * dv + j] = (int8_t)n;
+            }
+        }
+        free(Sh);
+        free(X);
+    }
+}
+
+/* ------------------------------------------------------------------------
+ * Pool layout, re-derived from its definition in include/stepq.h:
+ *  - physical key-row order: the 8-bit rows in increasing logical index,
+ *    then the 4-bit rows, then the 2-bit rows;
+ *  - row groups of 8/b physical rows of one width (1, 2 or 4 rows); a last
+ *    partial group of a width is completed with empty slots;
+ *  - each group is d_v bytes; byte j holds column j, slot s of the group at
+ *    bits [s*b, s*b+b) as b-bit two's complement, empty slots zero;
+ *  - codes region padded with zeros to a multiple of 128 bytes, followed by
+ *    r (d_k fp32, physical row order) and c (d_v fp32), the whole tile
+ *    record padded with zeros to a multiple of 128 bytes.
+ */
+static size_t round128(size_t x) { return (x + 127) & ~(size_t)127; }
+
+static void class_counts(int dk, const uint8_t *bits, int *n8, int *n4, int *n2)
+{
+    *n8 = *n4 = *n2 = 0;
+    for (int i = 0; i < dk; ++i) {
+        if (bits[i] == 8) ++*n8;
+        else if (bits[i] == 4) ++*n4;
+        else if (bits[i] == 2) ++*n2;
+    }
+}
+
+static size_t codes_region(int dk, int dv, const uint8_t *bits)
+{
+    int n8, n4, n2;
+    class_counts(dk, bits, &n8, &n4, &n2);
+    size_t groups = (size_t)n8 + (size_t)(n4 + 1) / 2 + (size_t)(n2 + 3) / 4;
+    return round128(groups * (size_t)dv);
+}
+
+size_t orc_tile_bytes(int dk, int dv, const uint8_t *bits)
+{
+    return round128(codes_region(dk, dv, bits) + 4u * (size_t)dk + 4u * (size_t)dv);
+}
+
+/* logical row of each physical row, and the (group, slot) position of each
+ * logical row inside the codes region */
+static void row_positions(int dk, const uint8_t *bits, int *phys_to_log, int *group, int *slot)
+{
+    int n8, n4, n2;
+    class_counts(dk, bits, &n8, &n4, &n2);
+    int p = 0;
+    static const int order[3] = {8, 4, 2};
+    for (int cl = 0; cl < 3; ++cl)
+        for (int i = 0; i < dk; ++i)
+            if (bits[i] == order[cl]) phys_to_log[p++] = i;
+    int g4 = n8, g2 = n8 + (n4 + 1) / 2;
+    for (int pp = 0; pp < dk; ++pp) {
+        int i = phys_to_log[pp];
+        if (pp < n8) { group[i] = pp; slot[i] = 0; }
+        else if (pp < n8 + n4) { int k = pp - n8; group[i] = g4 + k / 2; slot[i] = k % 2; }
+        else { int k = pp - n8 - n4; group[i] = g2 + k / 4; slot[i] = k % 4; }
+    }
+}
+
+/* codes: [dk][dv] logical order; r: [dk] logical order; c: [dv] */
+void orc_pack_tile(int dk, int dv, const uint8_t *bits, const int8_t *codes, const float *r,
+                   const float *c, uint8_t *rec)
+{
+    size_t creg = codes_region(dk, dv, bits);
+    size_t tb = orc_tile_bytes(dk, dv, bits);
+    memset(rec, 0, tb);
+    int *p2l = (int *)malloc(sizeof(int) * dk * 3);
+    int *grp = p2l + dk, *slt = p2l + 2 * dk;
+    row_positions(dk, bits, p2l, grp, slt);
+    for (int i = 0; i < dk; ++i) {
+        int b = bits[i];
+        unsigned mask = (1u << b) - 1u;
+        for (int j = 0; j < dv; ++j) {
+            unsigned field = ((unsigned)(int)codes[(size_t)i * dv + j]) & mask;
+            rec[(size_t)grp[i] * dv + j] |= (uint8_t)(field << (slt[i] * b));
+        }
+    }
+    float *rr = (float *)(rec + creg);
+    float *cc = rr + dk;
+    for (int p = 0; p < dk; ++p) rr[p] = r[p2l[p]];
+    for (int j = 0; j < dv; ++j) cc[j] = c[j];
+    free(p2l);
+}
+
+void orc_unpack_tile(int dk, int dv, const uint8_t *bits, const uint8_t *rec, int8_t *codes,
+                     float *r, float *c)
+{
+    size_t creg = codes_region(dk, dv, bits);
+    int *p2l = (int *)malloc(sizeof(int) * dk * 3);
+    int *grp = p2l + dk, *slt = p2l + 2 * dk;
+    row_positions(dk, bits, p2l, grp, slt);
+    for (int i = 0; i < dk; ++i) {
+        int b = bits[i];
+        for (int j = 0; j < dv; ++j) {
+            unsigned byte = rec[(size_t)grp[i] * dv + j];
+            int field = (int)((byte >> (slt[i] * b)) & ((1u << b) - 1u));
+            if (field >= (1 << (b - 1))) field -= (1 << b);    /* two's complement */
+            codes[(size_t)i * dv + j] = (int8_t)field;
+        }
+    }
+    const float *rr = (const float *)(rec + creg);
+    const float *cc = rr + dk;
+    for (int p = 0; p < dk; ++p) r[p2l[p]] = rr[p];
+    for (int j = 0; j < dv; ++j) c[j] = cc[j];
+    free(p2l);
+}
+
+/* Whole-pool image: n_slots records, each the head tiles in order.
+ * bits: [Hv][dk]; codes: [n_slots][Hv][dk][dv]; r: [n_slots][Hv][dk];
+ * c: [n_slots][Hv][dv]. */
+size_t orc_slot_bytes(int Hv, int dk, int dv, const uint8_t *bits)
+{
+    size_t s = 0;
+    for (int h = 0; h < Hv; ++h) s += orc_tile_bytes(dk, dv, bits + (size_t)h * dk);
+    return s;
+}
+
+void orc_pack_pool(int n_slots, int Hv, int dk, int dv, const uint8_t *bits, const int8_t *codes,
+                   const float *r, const float *c, uint8_t *pool)
+{
+    size_t sb = orc_slot_bytes(Hv, dk, dv, bits);
+    #pragma omp parallel for schedule(static)
+    for (int s = 0; s < n_slots; ++s) {
+        size_t off = (size_t)s * sb;
+        for (int h = 0; h < Hv; ++h) {
+            size_t t = (size_t)s * Hv + h;
+            orc_pack_tile(dk, dv, bits + (size_t)h * dk, codes + t * dk * dv, r + t * dk, c + t * dv,
+                          pool + off);
+            off += orc_tile_bytes(dk, dv, bits + (size_t)h * dk);
+        }
+    }
+}
+
+void orc_unpack_pool(int n_slots, int Hv, int dk, int dv, const uint8_t *bits, const uint8_t *pool,
+                     int8_t *codes, float *r, float *c)
+{
+    size_t sb = orc_slot_bytes(Hv, dk, dv, bits);
+    #pragma omp parallel for schedule(static)
+    for (int s = 0; s < n_slots; ++s) {
+        size_t off = (size_t)s * sb;
+        for (int h = 0; h < Hv; ++h) {
+            size_t t = (size_t)s * Hv + h;
+            orc_unpack_tile(dk, dv, bits + (size_t)h * dk, pool + off, codes + t * dk * dv, r + t * dk,
+                            c + t * dv);
+            off += orc_tile_bytes(dk, dv, bits + (size_t)h * dk);
+        }
+    }
+}
+
+int orc_max_threads(void)
+{
+#ifdef _OPENMP
+    extern int omp_get_max_threads(void);
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

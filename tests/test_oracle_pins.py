@@ -1,0 +1,403 @@
+"""Pins for the fp64 oracle against what the paper and the mathematics fix.
+
+Each test targets a mistake the oracle could plausibly contain (a dropped
+term, a wrong sign, a transposed operand, a wrong level set or tie rule)
+and checks it against something other than the oracle itself: a closed
+form, an identity the paper proves, a different algebraic form of the same
+equation, brute-force enumeration, or an integer the paper prints.
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_accounting.json")))
+
+
+def _unit(rng, n, d):
+    x = rng.standard_normal((n, d))
+    return x / np.linalg.norm(x, axis=1, keepdims=True)
+
+
+def _case(seed=0, n=3, dk=16, dv=12):
+    rng = np.random.default_rng(seed)
+    S = rng.standard_normal((n, dk, dv)) * 0.3
+    q, k = _unit(rng, n, dk), _unit(rng, n, dk)
+    v = rng.standard_normal((n, dv))
+    alpha = rng.uniform(0.5, 1.0, n)
+    beta = rng.uniform(0.0, 1.0, n)
+    return rng, S, q, k, v, alpha, beta
+
+
+# ---------------------------------------------------------------- update (Eq. 1, 2, 4)
+def test_update_matches_affine_form():
+    """Eq. 1 (first form, in the oracle) equals the affine form of Eq. 2,
+    S_t = A S + B with A = (I - beta k k^T) alpha, B = beta k v^T, written
+    here independently; the readout is y = X^T q (Eq. 4)."""
+    _, S, q, k, v, alpha, beta = _case()
+    X, o = oracle.update_fp(S, q, k, v, alpha, beta)
+    for t in range(S.shape[0]):
+        dk = S.shape[1]
+        A = (np.eye(dk) - beta[t] * np.outer(k[t], k[t])) * alpha[t]
+        Bm = beta[t] * np.outer(k[t], v[t])
+        Xr = A @ S[t] + Bm
+        np.testing.assert_allclose(X[t], Xr, rtol=0, atol=1e-13)
+        np.testing.assert_allclose(o[t], Xr.T @ q[t], rtol=0, atol=1e-13)
+
+
+def test_identity_gate_zero_write():
+    """alpha = 1, beta = 0: the state is unchanged exactly and o = S^T q."""
+    _, S, q, k, v, _, _ = _case(1)
+    n = S.shape[0]
+    X, o = oracle.update_fp(S, q, k, v, np.ones(n), np.zeros(n))
+    assert np.array_equal(X, S)
+    for t in range(n):
+        np.testing.assert_allclose(o[t], S[t].T @ q[t], rtol=0, atol=1e-14)
+
+
+def test_full_write_recalls_value():
+    """alpha = 1, beta = 1, |k| = 1: the retrieval of the new state along k is
+    the written value, X^T k = v (the Delta rule's defining property)."""
+    _, S, q, k, v, _, _ = _case(2)
+    n = S.shape[0]
+    X, o = oracle.update_fp(S, q, k, v, np.ones(n), np.ones(n))
+    for t in range(n):
+        np.testing.assert_allclose(X[t].T @ k[t], v[t], rtol=0, atol=1e-12)
+    # reading with q := k returns v as well
+    X2, o2 = oracle.update_fp(S, k, k, v, np.ones(n), np.ones(n))
+    np.testing.assert_allclose(o2, v, rtol=0, atol=1e-12)
+
+
+def test_directional_contraction_identity():
+    """Appendix B.1, Eq. self_correction:
+    ||alpha (I - beta k k^T) E||_F^2 = alpha^2 [ ||E||^2 - beta (2 - beta |k|^2) ||k^T E||^2 ].
+    With v = 0 the oracle's update maps E to alpha (I - beta k k^T) E."""
+    rng = np.random.default_rng(3)
+    n, dk, dv = 4, 10, 7
+    E = rng.standard_normal((n, dk, dv))
+    k = rng.standard_normal((n, dk)) * 0.4        # not unit: exercises the |k|^2 term
+    q = rng.standard_normal((n, dk))
+    alpha = rng.uniform(0.2, 1.0, n)
+    beta = rng.uniform(0.0, 1.0, n)
+    X, _ = oracle.update_fp(E, q, k, np.zeros((n, dv)), alpha, beta)
+    for t in range(n):
+        lhs = np.sum(X[t] ** 2)
+        kE = k[t] @ E[t]
+        rhs = alpha[t] ** 2 * (np.sum(E[t] ** 2) - beta[t] * (2 - beta[t] * k[t] @ k[t]) * kE @ kE)
+        assert lhs == pytest.approx(rhs, rel=1e-12)
+
+
+def test_row_readout_sensitivity():
+    """Appendix B.3 / Eq. kda_sensitivity with d_i = alpha: a unit-norm error
+    confined to key row i is read at the next step with squared norm g_i^2,
+    g = A^T q = alpha (q - beta k (k^T q))."""
+    rng = np.random.default_rng(4)
+    dk, dv = 9, 6
+    q, k = _unit(rng, 1, dk)[0], _unit(rng, 1, dk)[0]
+    alpha, beta = 0.9, 0.6
+    g = alpha * (q - beta * k * (k @ q))
+    for i in range(dk):
+        E = np.zeros((1, dk, dv))
+        row = rng.standard_normal(dv)
+        E[0, i] = row / np.linalg.norm(row)
+        _, o = oracle.update_fp(E, q[None], k[None], np.zeros((1, dv)), [alpha], [beta])
+        assert np.sum(o ** 2) == pytest.approx(g[i] ** 2, rel=1e-12, abs=1e-15)
+
+
+# ---------------------------------------------------------------- quantizer (Eq. 3)
+@pytest.mark.parametrize("b", [2, 4, 8])
+def test_quantize_dequantize_idempotent(b):
+    """Every code of every width survives dequantize -> quantize unchanged."""
+    qb = 2 ** (b - 1) - 1
+    rng = np.random.default_rng(b)
+    dk, dv = 3, 2 * qb + 1
+    codes = np.tile(np.arange(-qb, qb + 1, dtype=np.int8), (dk, 1))[None]
+    r = rng.uniform(0.01, 2, (1, dk)).astype(np.float32)
+    c = rng.uniform(0.01, 2, (1, dv)).astype(np.float32)
+    bits = np.full((1, dk), b, np.uint8)
+    S = oracle.dequant(codes, r, c, bits)
+    assert np.array_equal(oracle.quantize(S, r, c, bits), codes)
+    # the level set: S^ = r c q / q_b, so the extreme codes sit exactly at +-r c
+    np.testing.assert_allclose(np.abs(S[0, :, 0]), r[0].astype(np.float64) * np.float64(c[0, 0]), rtol=1e-15)
+
+
+def test_bruteforce_2x2_nearest_level():
+    """On 2x2 tiles the oracle's codes minimise sum_i w_i^2 (X - X^)^2 over
+    all joint code choices (enumerated for b <= 4) and are the per-entry
+    nearest level for b = 8 (enumerating all 255 levels)."""
+    rng = np.random.default_rng(5)
+    for trial in range(40):
+        bits = rng.choice([2, 4, 8], size=2).astype(np.uint8)
+        r = rng.uniform(0.05, 1.0, 2).astype(np.float32)
+        c = rng.uniform(0.05, 1.0, 2).astype(np.float32)
+        X = rng.standard_normal((2, 2)) * 0.6
+        w = rng.uniform(0.5, 2.0, 2)
+        got = oracle.quantize(X[None], r[None], c[None], bits[None])[0]
+        levels = [np.arange(-(2 ** (int(b) - 1) - 1), 2 ** (int(b) - 1)) for b in bits]
+        if max(bits) <= 4:
+            best, best_err = None, np.inf
+            for z in itertools.product(levels[0], levels[0], levels[1], levels[1]):
+                Z = np.array(z, dtype=np.float64).reshape(2, 2)
+                qb = np.array([2 ** (int(b) - 1) - 1 for b in bits], np.float64)
+                Xh = r[:, None].astype(np.float64) * c[None, :].astype(np.float64) * Z / qb[:, None]
+                err = np.sum(w[:, None] ** 2 * (X - Xh) ** 2)
+                if err < best_err:
+                    best, best_err = Z, err
+            assert np.array_equal(got, best.astype(np.int8))
+        for i in range(2):
+            qb = 2 ** (int(bits[i]) - 1) - 1
+            for j in range(2):
+                cand = float(r[i]) * float(c[j]) * levels[i] / qb
+                assert got[i, j] == levels[i][np.argmin(np.abs(X[i, j] - cand))]
+
+
+def test_quantizer_error_bound_and_clip():
+    """|X^ - X| <= r c / (2 q_b) where X is in range; out of range clips to
+    +-q_b (symmetric: -2^(b-1) is never produced)."""
+    rng = np.random.default_rng(6)
+    n, dk, dv = 4, 8, 8
+    bits = rng.choice([2, 4, 8], size=(n, dk)).astype(np.uint8)
+    r = rng.uniform(0.1, 1, (n, dk)).astype(np.float32)
+    c = rng.uniform(0.1, 1, (n, dv)).astype(np.float32)
+    X = rng.standard_normal((n, dk, dv)) * 1.5
+    codes, y = oracle.quantize(X, r, c, bits, want_y=True)
+    Xh = oracle.dequant(codes, r, c, bits)
+    qb = (2.0 ** (bits.astype(np.int64) - 1) - 1)[:, :, None]
+    rc = r.astype(np.float64)[:, :, None] * c.astype(np.float64)[:, None, :]
+    inside = np.abs(y) <= qb
+    assert np.all(np.abs(Xh - X)[inside] <= (rc / (2 * qb))[np.broadcast_to(inside, X.shape)] * (1 + 1e-12))
+    assert np.all(codes[~inside] == np.sign(y[~inside]) * np.broadcast_to(qb, y.shape)[~inside])
+    assert codes.min() >= -127
+
+
+def test_ties_round_to_even():
+    """Exact half-way values (power-of-two scales make X q_b/(r c) exact)
+    round to the even neighbour."""
+    b = 4                     # q_b = 7
+    r = np.full((1, 1), 0.5, np.float32)
+    c = np.full((1, 6), 2.0, np.float32)
+    halfs = np.array([0.5, 1.5, 2.5, -0.5, -1.5, -6.5])
+    X = (halfs / 7.0 * 1.0)[None, None, :]   # r c = 1
+    codes, y = oracle.quantize(X, r, c, np.array([[b]], np.uint8), want_y=True)
+    assert np.array_equal(y[0, 0], halfs)
+    assert codes[0, 0].tolist() == [0, 2, 2, 0, -2, -6]
+
+
+# ---------------------------------------------------------------- decode step (Table C2)
+def test_decode_step_is_dequant_update_quantize():
+    """The quantized step reads o from X before requantization (Eq. 4) and
+    stores Q(X) (Eq. 3) on the frozen scales."""
+    rng, S, q, k, v, alpha, beta = _case(7, n=3, dk=12, dv=10)
+    bits = rng.choice([2, 4, 8], size=(3, 12)).astype(np.uint8)
+    r, c = oracle.fit_absmax(S.astype(np.float32))
+    codes = oracle.quantize(S, r, c, bits)
+    new, o = oracle.decode_step(codes, r, c, bits, q, k, v, alpha, beta)
+    X, o_ref = oracle.update_fp(oracle.dequant(codes, r, c, bits), q, k, v, alpha, beta)
+    np.testing.assert_allclose(o, o_ref, rtol=0, atol=1e-14)
+    assert np.array_equal(new, oracle.quantize(X, r, c, bits))
+    # identity gate, no write: codes unchanged
+    same, _ = oracle.decode_step(codes, r, c, bits, q, k, v, np.ones(3), np.zeros(3))
+    assert np.array_equal(same, codes)
+
+
+def test_error_propagation_proposition():
+    """Proposition 1: with E_t = S^_t - S_t and eps_t = Q(X_t) - X_t,
+    E_t = A_t E_{t-1} + eps_t and y^_t - y_t = E_{t-1}^T A_t^T q_t, and
+    ||A_t||_2 <= 1 when |k| <= 1, 0 <= beta <= 1, 0 <= alpha <= 1."""
+    rng = np.random.default_rng(8)
+    n, dk, dv, T = 2, 16, 16, 6
+    S = rng.standard_normal((n, dk, dv)) * 0.1
+    bits = rng.choice([4, 8], size=(n, dk)).astype(np.uint8)
+    r, c = oracle.fit_absmax(S.astype(np.float32))
+    r = r * np.float32(3.0)                   # head-room so the trajectory rarely clips
+    codes = oracle.quantize(S, r, c, bits)
+    S_ref = S.copy()
+    E_prev = oracle.dequant(codes, r, c, bits) - S_ref
+    for t in range(T):
+        q, k = _unit(rng, n, dk), _unit(rng, n, dk) * 0.9
+        v = rng.standard_normal((n, dv)) * 0.1
+        alpha, beta = rng.uniform(0.8, 1.0, n), rng.uniform(0, 1, n)
+        Sh_prev = oracle.dequant(codes, r, c, bits)
+        X, yhat = oracle.update_fp(Sh_prev, q, k, v, alpha, beta)
+        codes, o_q = oracle.decode_step(codes, r, c, bits, q, k, v, alpha, beta)
+        np.testing.assert_allclose(o_q, yhat, rtol=0, atol=1e-14)
+        S_ref, y = oracle.update_fp(S_ref, q, k, v, alpha, beta)
+        Sh = oracle.dequant(codes, r, c, bits)
+        E = Sh - S_ref
+        eps = Sh - X
+        for b in range(n):
+            A = (np.eye(dk) - beta[b] * np.outer(k[b], k[b])) * alpha[b]
+            np.testing.assert_allclose(E[b], A @ E_prev[b] + eps[b], rtol=0, atol=1e-13)
+            np.testing.assert_allclose(yhat[b] - y[b], E_prev[b].T @ A.T @ q[b], rtol=0, atol=1e-13)
+            assert np.linalg.norm(A, 2) <= 1 + 1e-12
+        E_prev = E
+
+
+# ---------------------------------------------------------------- setup fit (Section 4.3)
+def test_fit_absmax_bounds():
+    """r_i = (m_i / w_i)^{1/2} with m_i the row mean |S|; r_i c_j >= |S_ij|
+    everywhere, with equality (to fp32 rounding) at each column's arg-max."""
+    rng = np.random.default_rng(9)
+    S = (rng.standard_normal((3, 16, 12)) * np.exp(rng.standard_normal((3, 16, 1)))).astype(np.float32)
+    w = rng.uniform(0.5, 2.0, (3, 16))
+    r, c = oracle.fit_absmax(S, w)
+    m = np.abs(S.astype(np.float64)).mean(axis=2)
+    np.testing.assert_allclose(r.astype(np.float64) ** 2 * w, m, rtol=3e-7)
+    rc = r.astype(np.float64)[:, :, None] * c.astype(np.float64)[:, None, :]
+    assert np.all(rc >= np.abs(S))
+    ratio = (np.abs(S) / rc).max(axis=1)
+    np.testing.assert_allclose(ratio, 1.0, rtol=3e-7)
+    # codes of the fitted state never clip, and each column reaches +-q_b
+    bits = np.full((3, 16), 8, np.uint8)
+    codes, y = oracle.quantize(S.astype(np.float64), r, c, bits, want_y=True)
+    assert np.abs(y).max() <= 127.0
+    assert np.all(np.abs(codes).max(axis=1) == 127)
+
+
+def test_fit_zero_rows_use_floor():
+    S = np.zeros((1, 4, 4), np.float32)
+    S[0, 1, 2] = 0.25
+    r, c = oracle.fit_absmax(S)
+    assert r[0, 0] == np.float32(2.0 ** -60) and r[0, 1] > 0
+    assert np.all(c > 0)
+
+
+# ---------------------------------------------------------------- bit allocation (Eq. 6)
+def test_mean_log_retention_closed_form():
+    g = np.full((4, 3, 2), 0.9)
+    g[..., 1] = 0.5
+    np.testing.assert_allclose(oracle.mean_log_retention(g), [math.log(0.9), math.log(0.5)], rtol=1e-15)
+    # half-life tau = log 2 / (-l) (Appendix B.4)
+    assert math.log(2) / -math.log(0.5) == pytest.approx(1.0)
+
+
+def test_lifetime_allocation_bruteforce():
+    """The ranked allocation minimises sum_u L_u d(b_u) subject to the
+    average-width budget (Eq. 6), checked by enumerating every assignment of
+    {4, 8} to 2 rows x 4 heads with a shared distortion profile d(4) > d(8)."""
+    rng = np.random.default_rng(10)
+    for trial in range(5):
+        H, dk, T, B = 4, 2, 6, 3
+        gates = rng.uniform(0.6, 1.0, (T, B, H))
+        bits = oracle.lifetime_bitmap(gates, dk, budget=6.0)
+        ell = oracle.mean_log_retention(gates)
+        Lw = np.array([oracle.lifetime_weight(e, 64) for e in ell])
+        d = {4: 1.0, 8: 1.0 / 16}
+        units = [(h, i) for h in range(H) for i in range(dk)]
+        best = np.inf
+        for choice in itertools.product([4, 8], repeat=len(units)):
+            if sum(choice) > 6.0 * len(units):
+                continue
+            best = min(best, sum(Lw[h] * d[b] for (h, i), b in zip(units, choice)))
+        got = sum(Lw[h] * d[int(bits[h, i])] for h, i in units)
+        assert got == pytest.approx(best, rel=1e-12)
+        assert bits.astype(float).mean() == 6.0
+
+
+# ---------------------------------------------------------------- layout (include/stepq.h)
+@pytest.mark.parametrize("b", [2, 4, 8])
+def test_pack_single_field(b):
+    """Each field lands in byte j of its row group at bit offset slot*b as a
+    b-bit two's-complement integer, rows of one width in logical order."""
+    dk, dv = 8, 128
+    bits = np.full((1, dk), b, np.uint8)
+    qb = 2 ** (b - 1) - 1
+    rows_per_group = 8 // b
+    for code in range(-qb, qb + 1):
+        for i in (0, dk - 1, 3):
+            j = (i * 37 + 5) % dv
+            codes = np.zeros((1, 1, dk, dv), np.int8)
+            codes[0, 0, i, j] = code
+            r = np.zeros((1, 1, dk), np.float32)
+            c = np.zeros((1, 1, dv), np.float32)
+            img = oracle.pack_pool(codes, r, c, bits)
+            g, s = i // rows_per_group, i % rows_per_group
+            expect = ((code & ((1 << b) - 1)) << (s * b)) & 0xFF
+            assert img[g * dv + j] == expect
+            assert np.count_nonzero(img) == (1 if code != 0 else 0)
+
+
+def test_pack_roundtrip_and_sizes():
+    rng = np.random.default_rng(11)
+    for dk, dv in [(64, 64), (128, 128), (32, 64)]:
+        Hv, n = 3, 2
+        bits = rng.choice([2, 4, 8], size=(Hv, dk)).astype(np.uint8)
+        qb = (2 ** (bits.astype(np.int64) - 1) - 1)
+        codes = rng.integers(-qb[None, :, :, None], qb[None, :, :, None] + 1, size=(n, Hv, dk, dv)).astype(np.int8)
+        r = rng.uniform(0, 1, (n, Hv, dk)).astype(np.float32)
+        c = rng.uniform(0, 1, (n, Hv, dv)).astype(np.float32)
+        img = oracle.pack_pool(codes, r, c, bits)
+        c2, r2, cc2 = oracle.unpack_pool(img, n, bits, dv)
+        assert np.array_equal(c2, codes) and np.array_equal(r2, r) and np.array_equal(cc2, c)
+        for h in range(Hv):
+            n8, n4, n2 = [(bits[h] == w).sum() for w in (8, 4, 2)]
+            groups = n8 + (n4 + 1) // 2 + (n2 + 3) // 4
+            creg = -(-groups * dv // 128) * 128
+            assert oracle.tile_bytes(bits[h], dv) == -(-(creg + 4 * dk + 4 * dv) // 128) * 128
+        assert img.size == n * oracle.slot_bytes(bits, dv)
+
+
+def test_six_bit_tile_bytes():
+    """64 rows @8 + 64 rows @4 at d=128: 12,288 code bytes + 1,024 scale bytes."""
+    bits = np.array([8] * 64 + [4] * 64, np.uint8)
+    assert oracle.tile_bytes(bits, 128) == 13312
+    bits = np.array([8] * 32 + [4] * 32 + [2] * 64, np.uint8)
+    assert oracle.tile_bytes(bits, 128) == 8192 + 1024
+
+
+# ---------------------------------------------------------------- the paper's printed accounting
+def _gib(x):
+    return x / 2 ** 30
+
+
+def test_qwen_packed_bytes():
+    g = GOLD
+    assert oracle.packed_bytes_qwen6() == g["qwen6_packed_bytes"]["value"]
+    assert oracle.packed_bytes_qwen6(pivot_scale_slots=True) == g["qwen6_compact_bytes_with_pivot_scale_slots"]["value"]
+    fp32 = 4 * g["qwen_elements_per_request"]["value"]
+    assert fp32 == g["qwen_state_bytes_fp32"]["value"]
+    assert round(fp32 / oracle.packed_bytes_qwen6(), 2) == g["qwen6_ratio"]["value"]
+    assert round(100 * (1 - oracle.packed_bytes_qwen6() / fp32), 2) == g["qwen6_reduction_pct"]["value"]
+    assert round(oracle.compact_bits_qwen(6), 4) == g["b_qwen6"]["value"]
+
+
+def test_kda_compact_sizes():
+    g = GOLD
+    N = g["kda_elements_per_request"]["value"]
+    assert N == 20 * 32 * 128 * 128
+    for bud, key_b, key_mib, key_ratio in [(6, "b_kda6", "kda6_mib", "kda6_ratio"), (4, "b_kda4", "kda4_mib", "kda4_ratio")]:
+        b = oracle.compact_bits_kda(bud)
+        assert round(b, 2) == g[key_b]["value"]
+        mib = b * N / 8 / 2 ** 20
+        assert mib == pytest.approx(g[key_mib]["value"], abs=1e-9)
+        assert round(g["kda_fp32_mib"]["value"] / mib, 2) == g[key_ratio]["value"]
+
+
+def test_serving_capacity_model():
+    g = GOLD
+    K = g["qwen_kv_bytes_per_token"]["value"]
+    conv = g["qwen_conv_state_bytes"]["value"]
+    S32 = g["qwen_state_bytes_fp32"]["value"] + conv
+    Sq = g["qwen6_compact_bytes_with_pivot_scale_slots"]["value"] + conv
+    assert Sq / 2 ** 20 == 31.4375
+    # reserved state pool at B = 64 (weights and KV excluded)
+    assert round(_gib(oracle.serving_memory(64, 0, 0, S32, K)), 2) == g["reserved_pool_fp32_b64_gib"]["value"]
+    assert round(_gib(oracle.serving_memory(64, 0, 0, Sq, K)), 2) == g["reserved_pool_stepq_b64_gib"]["value"]
+    # total serving memory at B = 512 with W4 weights, 128 + 1024 tokens
+    W4 = g["qwen_weights_w4_bytes"]["value"]
+    assert round(_gib(oracle.serving_memory(512, 1152, W4, S32, K)), 2) == g["qwen_total_w4_b512_fp32_gib"]["value"]
+    assert round(_gib(oracle.serving_memory(512, 1152, W4, Sq, K)), 2) == g["qwen_total_w4_b512_stepq_gib"]["value"]
+    # KDA recurrent-state pool at B = 512
+    kda32 = g["kda_fp32_mib"]["value"] * 2 ** 20
+    kda6 = g["kda6_mib"]["value"] * 2 ** 20
+    assert round(_gib(oracle.serving_memory(512, 0, 0, kda32, 0)), 2) == g["kda_state_b512_fp32_gib"]["value"]
+    assert round(_gib(oracle.serving_memory(512, 0, 0, kda6, 0)), 2) == g["kda_state_b512_stepq_gib"]["value"]
+    # the FP32 pool first exceeds the BF16 weights at B = 70
+    Wb = g["qwen_weights_bf16_bytes"]["value"]
+    first = next(B for B in range(1, 1000) if (5 * B + 1) * S32 > Wb)
+    assert first == g["fp32_pool_exceeds_bf16_weights_at_b"]["value"]
