@@ -1,0 +1,215 @@
+"""Decode-step throughput of the quantized gated-Delta state pool on one MI355X.
+
+Default workload: a 2048-slot pool, 512 active requests x 32 heads,
+d_k = d_v = 128, 6-bit mixed {4,8} codes with fp32 row/column scales, bf16
+activations.  One "step" is one fused decode launch over all 16,384 active
+(request, head) tiles.  By default successive steps rotate over four
+disjoint 512-slot subsets of the pool (832 MiB cycle), so a step's 208 MiB
+of state is not still resident in the 256 MB last-level cache from the
+previous one; --resident keeps one subset (reported as cache-resident).
+
+Prints one JSON line (rank 0):
+  value      state-updates/s (tiles advanced per second) over the timed steps
+  roofline   the decode kernel's algorithmic state bytes per launch (codes
+             read + codes written + scales read) / its mean launch duration
+             from HIP events around every launch, against the 8 TB/s HBM peak
+  cpu_baseline  the fp64 oracle on the host cores on a bounded sample
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "state-updates/s and achieved HBM GB/s (% of peak), B=512 heads=32 dk=dv=128"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode_pool_b512.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_38169_amd", "csrc", "stepq_kernels.hip")
+
+
+def kernel_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def state_bytes_per_tile(bits_row, d_k, d_v) -> int:
+    """Algorithmic bytes one tile update moves: its codes read and written
+    once, its fp32 row and column scales read once."""
+    import numpy as np
+    n8 = int(np.sum(bits_row == 8)); n4 = int(np.sum(bits_row == 4)); n2 = int(np.sum(bits_row == 2))
+    code_bytes = (8 * n8 + 4 * n4 + 2 * n2) * d_v // 8
+    return 2 * code_bytes + 4 * (d_k + d_v)
+
+
+def cpu_baseline(w, bits, seconds: float):
+    """The fp64 oracle on the host: decode steps on a sample of tiles of the
+    same workload until ~seconds have elapsed."""
+    import numpy as np
+    import oracle
+    from paper_2609_38169_amd import workloads as W
+    rows = np.arange(16)                                  # 16 requests x 32 heads = 512 tiles
+    slots = [int(s) for s in W.active_slots(w)[rows]]
+    S = W.initial_state(w, 0, slots).numpy().reshape(-1, w.d_k, w.d_v)
+    n = S.shape[0]
+    tb = np.broadcast_to(bits[None], (len(rows),) + bits.shape).reshape(n, w.d_k)
+    r, c = oracle.fit_absmax(S)
+    codes = oracle.quantize(S.astype(np.float64), r, c, tb)
+    g = w.n_v_heads // w.n_qk_heads
+    hq = np.arange(w.n_v_heads) // g
+    done, t0, step = 0, time.perf_counter(), 0
+    elapsed = 0.0
+    while elapsed < seconds:
+        inp = W.step_inputs(w, 0, step)
+        q = inp["q"][rows].double().numpy()[:, hq].reshape(n, w.d_k)
+        k = inp["k"][rows].double().numpy()[:, hq].reshape(n, w.d_k)
+        v = inp["v"][rows].double().numpy().reshape(n, w.d_v)
+        a = inp["alpha"][rows].double().numpy().reshape(n)
+        b = inp["beta"][rows].double().numpy().reshape(n)
+        ts = time.perf_counter()
+        codes, _ = oracle.decode_step(codes, r, c, tb, q, k, v, a, b)
+        elapsed += time.perf_counter() - ts
+        done += n
+        step += 1
+    return {"value": done / elapsed, "unit": "state-updates/s", "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": f"{step} decode steps x {n} tiles (16 requests x {w.n_v_heads} heads) of {w.name}, "
+                      f"{elapsed:.1f} s of oracle time (input draws excluded)"}
+
+
+def traffic_entry(launch_bytes):
+    """HBM traffic per launch from committed rocprofv3 counter summaries, if
+    they were taken on the current kernel source."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_sha") != kernel_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=128)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--resident", action="store_true", help="no slot rotation (cache-resident number)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-ref", action="store_true", help="also time a plain device copy of the same bytes")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (each (request, head) tile is "
+              "independent; see the sharding note in DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2609_38169_amd import stepq, workloads as W
+    from paper_2609_38169_amd.pools import build_pool, row_bits
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    w = W.workload(2)
+    bits = row_bits(w)
+    t_setup = time.perf_counter()
+    pool = build_pool(w, device=dev, bits=bits)
+    subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
+    n_inp = min(w.steps, args.steps + args.warmup)
+    inputs = [W.step_inputs(w, 0, t, device=dev) for t in range(n_inp)]
+    o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+
+    def launch(i):
+        inp = inputs[i % n_inp]
+        pool.step(subsets[i % len(subsets)], inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o)
+
+    for i in range(args.warmup):
+        launch(i)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * K)]
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for i in range(K):
+        ev[2 * i].record(stream)
+        launch(args.warmup + i)
+        ev[2 * i + 1].record(stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    per_launch_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(K)]
+    kern_ms = float(np.mean(per_launch_ms))
+
+    tiles = w.tiles_per_step
+    per_tile = [state_bytes_per_tile(bits[h], w.d_k, w.d_v) for h in range(w.n_v_heads)]
+    launch_bytes = w.batch * sum(per_tile)
+    act_bytes = w.batch * (2 * w.n_qk_heads * w.d_k * 2 + w.n_v_heads * w.d_v * 2 + 2 * w.n_v_heads * 2
+                           + w.n_v_heads * w.d_v * 4 + 4)
+    achieved = launch_bytes / (kern_ms * 1e-3) / 1e9
+    value = tiles * K / (total_ms * 1e-3)
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "state-updates/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
+                               f"d_k=d_v={w.d_k}, 6-bit mixed {{4,8}}, fp32 scales, bf16 activations",
+                   "slot_rotation": 1 if args.resident else len(subsets),
+                   "cache_resident": bool(args.resident)},
+        "GBps_state": launch_bytes * K / (total_ms * 1e-3) / 1e9,
+        "pct_hbm_peak": 100.0 * launch_bytes * K / (total_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic_entry(launch_bytes),
+            "kernel": "decode_kernel<128, bf16>",
+            "kernel_ms_mean": kern_ms,
+            "kernel_ms_min": float(np.min(per_launch_ms)),
+            "bytes_per_launch": launch_bytes,
+            "activation_bytes_per_launch": act_bytes,
+            "kernel_sha": kernel_hash(),
+        },
+        "setup_s": setup_s,
+    }
+    if args.copy_ref:
+        src = torch.empty(launch_bytes // 2, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record(stream)
+        for _ in range(20):
+            dst.copy_(src)
+        c1.record(stream)
+        torch.cuda.synchronize()
+        line["copy_ref_GBps"] = 2 * src.numel() * 20 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w, bits, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

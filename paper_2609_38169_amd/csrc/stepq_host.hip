@@ -1,0 +1,324 @@
+// Host side of libstepq: the C ABI declared in include/stepq.h.
+// Argument checking, the per-head layout tables, launches.
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "stepq.h"
+#include "stepq_internal.h"
+
+using stepq::HeadInfo;
+
+struct stepq_pool {
+    int32_t n_slots, Hv, Hqk, dk, dv;
+    std::vector<uint8_t> bits;        // [Hv][dk]
+    std::vector<HeadInfo> heads;      // [Hv]
+    std::vector<uint8_t> perm;        // [Hv][dk] physical -> logical
+    size_t slot_bytes = 0, pool_bytes = 0;
+    uint8_t *mem = nullptr;
+    bool owns_mem = false;
+    HeadInfo *d_heads = nullptr;
+    uint8_t *d_perm = nullptr;
+    int device = 0;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+stepq_status fail(stepq_status s, const std::string &msg)
+{
+    g_err = msg;
+    return s;
+}
+
+stepq_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(STEPQ_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t round128(size_t x) { return (x + 127) & ~static_cast<size_t>(127); }
+
+// Validate a descriptor and derive the layout tables (include/stepq.h).
+stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads, std::vector<uint8_t> *perm,
+                          size_t *slot_bytes)
+{
+    if (!d) return fail(STEPQ_E_INVALID, "descriptor is NULL");
+    if (d->n_slots < 1 || d->n_v_heads < 1 || d->n_qk_heads < 1)
+        return fail(STEPQ_E_INVALID, "n_slots, n_v_heads and n_qk_heads must be >= 1");
+    if (d->n_v_heads % d->n_qk_heads != 0)
+        return fail(STEPQ_E_INVALID, "n_v_heads must be a multiple of n_qk_heads");
+    if (d->d_k < 1 || d->d_k > stepq::kMaxDk) return fail(STEPQ_E_UNSUPPORTED, "d_k must be in 1..128");
+    if (d->d_v != 64 && d->d_v != 128) return fail(STEPQ_E_UNSUPPORTED, "d_v must be 64 or 128");
+    if (!d->row_bits) return fail(STEPQ_E_INVALID, "row_bits is NULL");
+    const int Hv = d->n_v_heads, dk = d->d_k, dv = d->d_v;
+    heads->assign(Hv, HeadInfo{});
+    perm->assign(static_cast<size_t>(Hv) * dk, 0);
+    size_t off = 0;
+    for (int h = 0; h < Hv; ++h) {
+        const uint8_t *b = d->row_bits + static_cast<size_t>(h) * dk;
+        int n8 = 0, n4 = 0, n2 = 0;
+        for (int i = 0; i < dk; ++i) {
+            if (b[i] == 8) ++n8;
+            else if (b[i] == 4) ++n4;
+            else if (b[i] == 2) ++n2;
+            else return fail(STEPQ_E_INVALID, "row_bits entries must be 2, 4 or 8");
+        }
+        int p = 0;
+        for (int width : {8, 4, 2})
+            for (int i = 0; i < dk; ++i)
+                if (b[i] == width) (*perm)[static_cast<size_t>(h) * dk + p++] = static_cast<uint8_t>(i);
+        HeadInfo &hi = (*heads)[h];
+        hi.n8 = static_cast<uint16_t>(n8);
+        hi.n4 = static_cast<uint16_t>(n4);
+        hi.n2 = static_cast<uint16_t>(n2);
+        hi.g8 = static_cast<uint16_t>(n8);
+        hi.g4 = static_cast<uint16_t>((n4 + 1) / 2);
+        hi.g2 = static_cast<uint16_t>((n2 + 3) / 4);
+        hi.groups = static_cast<uint32_t>(hi.g8 + hi.g4 + hi.g2);
+        const size_t creg = round128(static_cast<size_t>(hi.groups) * dv);
+        const size_t tb = round128(creg + 4u * static_cast<size_t>(dk) + 4u * static_cast<size_t>(dv));
+        hi.r_off = static_cast<uint32_t>(creg);
+        hi.tile_bytes = static_cast<uint32_t>(tb);
+        hi.tile_off = static_cast<uint32_t>(off);
+        off += tb;
+    }
+    *slot_bytes = off;
+    return STEPQ_OK;
+}
+
+stepq::PoolView view(const stepq_pool *p)
+{
+    stepq::PoolView v;
+    v.base = p->mem;
+    v.slot_bytes = p->slot_bytes;
+    v.heads = p->d_heads;
+    v.perm = p->d_perm;
+    v.n_slots = p->n_slots;
+    v.Hv = p->Hv;
+    v.Hqk = p->Hqk;
+    v.dk = p->dk;
+    v.dv = p->dv;
+    return v;
+}
+
+bool debug_checks()
+{
+    const char *e = std::getenv("STEPQ_DEBUG");
+    return e && e[0] == '1';
+}
+
+stepq_status check_device(const stepq_pool *p)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != p->device) return fail(STEPQ_E_INVALID, "the pool lives on another device than the current one");
+    return STEPQ_OK;
+}
+
+// STEPQ_DEBUG=1: slot ids distinct and in range (synchronising host copy).
+stepq_status check_slots(const stepq_pool *p, const int32_t *ids, int32_t n, hipStream_t s)
+{
+    if (!debug_checks() || n == 0) return STEPQ_OK;
+    std::vector<int32_t> h(n);
+    hipError_t e = hipStreamSynchronize(s);
+    if (e == hipSuccess) e = hipMemcpy(h.data(), ids, sizeof(int32_t) * n, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "slot id check");
+    std::vector<uint8_t> seen(p->n_slots, 0);
+    for (int32_t i = 0; i < n; ++i) {
+        if (h[i] < 0 || h[i] >= p->n_slots) return fail(STEPQ_E_INVALID, "slot id out of range");
+        if (seen[h[i]]) return fail(STEPQ_E_INVALID, "slot id repeated within one call");
+        seen[h[i]] = 1;
+    }
+    return STEPQ_OK;
+}
+
+stepq_status common_checks(const stepq_pool *p, const int32_t *ids, int32_t n)
+{
+    if (!p) return fail(STEPQ_E_INVALID, "pool is NULL");
+    if (n < 0) return fail(STEPQ_E_INVALID, "negative count");
+    if (n > p->n_slots) return fail(STEPQ_E_INVALID, "more slots requested than the pool holds");
+    if (n > 0 && !ids) return fail(STEPQ_E_INVALID, "slot_ids is NULL");
+    return check_device(p);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *stepq_last_error(void) { return g_err.c_str(); }
+
+stepq_status stepq_pool_bytes(const stepq_pool_desc *desc, size_t *pool_bytes, size_t *slot_bytes)
+{
+    std::vector<HeadInfo> heads;
+    std::vector<uint8_t> perm;
+    size_t sb = 0;
+    stepq_status st = build_layout(desc, &heads, &perm, &sb);
+    if (st != STEPQ_OK) return st;
+    if (pool_bytes) *pool_bytes = sb * static_cast<size_t>(desc->n_slots);
+    if (slot_bytes) *slot_bytes = sb;
+    return STEPQ_OK;
+}
+
+stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, size_t device_mem_bytes,
+                               stepq_pool **out)
+{
+    if (!out) return fail(STEPQ_E_INVALID, "out is NULL");
+    *out = nullptr;
+    auto *p = new stepq_pool;
+    stepq_status st = build_layout(desc, &p->heads, &p->perm, &p->slot_bytes);
+    if (st != STEPQ_OK) {
+        delete p;
+        return st;
+    }
+    p->n_slots = desc->n_slots;
+    p->Hv = desc->n_v_heads;
+    p->Hqk = desc->n_qk_heads;
+    p->dk = desc->d_k;
+    p->dv = desc->d_v;
+    p->bits.assign(desc->row_bits, desc->row_bits + static_cast<size_t>(p->Hv) * p->dk);
+    p->pool_bytes = p->slot_bytes * static_cast<size_t>(p->n_slots);
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) {
+        delete p;
+        return hip_fail(e, "hipGetDevice");
+    }
+    if (device_mem) {
+        if (reinterpret_cast<uintptr_t>(device_mem) % 256 != 0) {
+            delete p;
+            return fail(STEPQ_E_INVALID, "device_mem must be 256-byte aligned");
+        }
+        if (device_mem_bytes < p->pool_bytes) {
+            delete p;
+            return fail(STEPQ_E_INVALID, "device_mem is smaller than stepq_pool_bytes()");
+        }
+        p->mem = static_cast<uint8_t *>(device_mem);
+    } else {
+        e = hipMalloc(reinterpret_cast<void **>(&p->mem), p->pool_bytes);
+        if (e != hipSuccess) {
+            delete p;
+            return fail(STEPQ_E_NOMEM, std::string("pool allocation: ") + hipGetErrorString(e));
+        }
+        p->owns_mem = true;
+    }
+    e = hipMalloc(reinterpret_cast<void **>(&p->d_heads), sizeof(HeadInfo) * p->heads.size());
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&p->d_perm), p->perm.size());
+    if (e == hipSuccess)
+        e = hipMemcpy(p->d_heads, p->heads.data(), sizeof(HeadInfo) * p->heads.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(p->d_perm, p->perm.data(), p->perm.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        stepq_pool_destroy(p);
+        return fail(STEPQ_E_NOMEM, std::string("layout tables: ") + hipGetErrorString(e));
+    }
+    *out = p;
+    return STEPQ_OK;
+}
+
+void stepq_pool_destroy(stepq_pool *p)
+{
+    if (!p) return;
+    (void)hipDeviceSynchronize();
+    if (p->owns_mem && p->mem) (void)hipFree(p->mem);
+    if (p->d_heads) (void)hipFree(p->d_heads);
+    if (p->d_perm) (void)hipFree(p->d_perm);
+    delete p;
+}
+
+void *stepq_pool_device_ptr(const stepq_pool *p) { return p ? p->mem : nullptr; }
+
+stepq_status stepq_decode_step(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q, const void *k,
+                               const void *v, const void *alpha, const void *beta, stepq_dtype act_dtype, float *o,
+                               void *stream)
+{
+    stepq_status st = common_checks(p, slot_ids, batch);
+    if (st != STEPQ_OK) return st;
+    if (act_dtype != STEPQ_F32 && act_dtype != STEPQ_BF16) return fail(STEPQ_E_INVALID, "unknown activation dtype");
+    if (batch == 0) return STEPQ_OK;
+    if (!q || !k || !v || !alpha || !beta || !o) return fail(STEPQ_E_INVALID, "NULL activation or output pointer");
+    auto s = static_cast<hipStream_t>(stream);
+    st = check_slots(p, slot_ids, batch, s);
+    if (st != STEPQ_OK) return st;
+    stepq::DecodeArgs a;
+    a.pool = view(p);
+    a.slot_ids = slot_ids;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.alpha = alpha;
+    a.beta = beta;
+    a.o = o;
+    a.batch = batch;
+    hipError_t e = stepq::launch_decode(a, act_dtype == STEPQ_BF16, s);
+    return e == hipSuccess ? STEPQ_OK : hip_fail(e, "decode launch");
+}
+
+static stepq_status tile_op(const stepq_pool *p, const int32_t *ids, int32_t n, stepq::TileArgs &a,
+                            stepq::TileOp op, void *stream)
+{
+    auto s = static_cast<hipStream_t>(stream);
+    stepq_status st = check_slots(p, ids, n, s);
+    if (st != STEPQ_OK) return st;
+    a.pool = view(p);
+    a.slot_ids = ids;
+    a.n = n;
+    hipError_t e = stepq::launch_tile_op(a, op, s);
+    return e == hipSuccess ? STEPQ_OK : hip_fail(e, "tile kernel launch");
+}
+
+stepq_status stepq_pool_load(stepq_pool *p, const int32_t *slot_ids, int32_t n, const float *state, const float *r,
+                             const float *c, void *stream)
+{
+    stepq_status st = common_checks(p, slot_ids, n);
+    if (st != STEPQ_OK) return st;
+    if (n == 0) return STEPQ_OK;
+    if (!state || !r || !c) return fail(STEPQ_E_INVALID, "NULL state or scale pointer");
+    stepq::TileArgs a{};
+    a.state = state;
+    a.r_in = r;
+    a.c_in = c;
+    return tile_op(p, slot_ids, n, a, stepq::TileOp::Load, stream);
+}
+
+stepq_status stepq_pool_import(stepq_pool *p, const int32_t *slot_ids, int32_t n, const int8_t *codes,
+                               const float *r, const float *c, void *stream)
+{
+    stepq_status st = common_checks(p, slot_ids, n);
+    if (st != STEPQ_OK) return st;
+    if (n == 0) return STEPQ_OK;
+    if (!codes || !r || !c) return fail(STEPQ_E_INVALID, "NULL codes or scale pointer");
+    stepq::TileArgs a{};
+    a.codes_in = codes;
+    a.r_in = r;
+    a.c_in = c;
+    return tile_op(p, slot_ids, n, a, stepq::TileOp::Import, stream);
+}
+
+stepq_status stepq_pool_export(const stepq_pool *p, const int32_t *slot_ids, int32_t n, int8_t *codes, float *r,
+                               float *c, void *stream)
+{
+    stepq_status st = common_checks(p, slot_ids, n);
+    if (st != STEPQ_OK) return st;
+    if (n == 0) return STEPQ_OK;
+    if (!codes || !r || !c) return fail(STEPQ_E_INVALID, "NULL output pointer");
+    stepq::TileArgs a{};
+    a.codes_out = codes;
+    a.r_out = r;
+    a.c_out = c;
+    return tile_op(p, slot_ids, n, a, stepq::TileOp::Export, stream);
+}
+
+stepq_status stepq_pool_dequant(const stepq_pool *p, const int32_t *slot_ids, int32_t n, float *out, void *stream)
+{
+    stepq_status st = common_checks(p, slot_ids, n);
+    if (st != STEPQ_OK) return st;
+    if (n == 0) return STEPQ_OK;
+    if (!out) return fail(STEPQ_E_INVALID, "NULL output pointer");
+    stepq::TileArgs a{};
+    a.deq_out = out;
+    return tile_op(p, slot_ids, n, a, stepq::TileOp::Dequant, stream);
+}
+
+}  // extern "C"

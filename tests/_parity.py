@@ -1,0 +1,132 @@
+"""Test-side helpers: drive the oracle and the HIP path on the same seeded
+draws and compare them to the tolerances of the decode step.
+
+Protocol (lockstep, re-anchored from the oracle): the oracle runs its own
+trajectory from its own quantization of the initial state.  Before each
+step the checked GPU slots are overwritten (stepq_pool_import) with the
+oracle's previous codes and scales, the GPU step runs at full size, and its
+exported codes and outputs for those slots are compared with the oracle's
+next step.  Every oracle input comes from the workload draws or from the
+oracle itself, never from the GPU.
+
+Tolerances:
+  codes   bit-exact, except at most 1e-4 of the entries of a step may differ
+          by exactly one level, and only where the oracle's unrounded value
+          lies within TIE_WINDOW of a rounding boundary (a tie that fp32 and
+          fp64 may break differently);
+  outputs |o_gpu - o_oracle| <= 1e-5 + 1e-3 |o_oracle| element-wise.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2609_38169_amd import workloads as W
+
+CODE_MISMATCH_FRAC = 1e-4
+TIE_WINDOW = 2e-3          # code units; fp32 error of the code-space update is ~1e-5
+O_ABS, O_REL = 1e-5, 1e-3
+
+
+def bits_for(w: W.Workload, layer: int = 0) -> np.ndarray:
+    """Bit map from the oracle's own setup (lifetime ranking) or the draw."""
+    if w.bits == "lifetime48":
+        return oracle.lifetime_bitmap(W.calibration_gates(w, layer).numpy(), w.d_k, budget=6.0)
+    return W.bit_map_draw(w, layer).numpy()
+
+
+def oracle_inputs(w: W.Workload, inp: dict, rows: np.ndarray):
+    """Per-tile fp64 activations for batch rows ``rows`` (all heads), exact
+    widenings of the stored dtype; q/k expanded over grouped heads."""
+    g = w.n_v_heads // w.n_qk_heads
+    hq = np.arange(w.n_v_heads) // g
+    rows_t = torch.as_tensor(rows, dtype=torch.long, device=inp["q"].device)
+    q = inp["q"].index_select(0, rows_t).double().cpu().numpy()[:, hq, :]
+    k = inp["k"].index_select(0, rows_t).double().cpu().numpy()[:, hq, :]
+    v = inp["v"].index_select(0, rows_t).double().cpu().numpy()
+    a = inp["alpha"].index_select(0, rows_t).double().cpu().numpy()
+    b = inp["beta"].index_select(0, rows_t).double().cpu().numpy()
+    n = len(rows) * w.n_v_heads
+    return (q.reshape(n, w.d_k), k.reshape(n, w.d_k), v.reshape(n, w.d_v), a.reshape(n), b.reshape(n))
+
+
+def compare_codes(gpu: np.ndarray, orc: np.ndarray, y: np.ndarray, what: str = "codes"):
+    """Apply the code tolerance; returns the number of tie mismatches."""
+    diff = gpu.astype(np.int16) - orc.astype(np.int16)
+    bad = np.nonzero(diff)
+    n_bad = bad[0].size
+    if n_bad == 0:
+        return 0
+    assert np.all(np.abs(diff[bad]) == 1), f"{what}: a code differs by more than one level"
+    frac = np.abs(y[bad]) - np.floor(np.abs(y[bad]))
+    near_tie = np.abs(frac - 0.5) <= TIE_WINDOW
+    assert np.all(near_tie), (f"{what}: {int((~near_tie).sum())} mismatches away from a rounding tie, e.g. "
+                              f"y={y[bad][~near_tie][:4]}")
+    assert n_bad <= CODE_MISMATCH_FRAC * gpu.size, f"{what}: {n_bad} of {gpu.size} codes differ"
+    return n_bad
+
+
+def compare_out(gpu: np.ndarray, orc: np.ndarray, what: str = "o"):
+    err = np.abs(gpu.astype(np.float64) - orc)
+    lim = O_ABS + O_REL * np.abs(orc)
+    worst = np.argmax(err - lim)
+    assert np.all(err <= lim), (f"{what}: |diff| {err.flat[worst]:.3g} > {lim.flat[worst]:.3g} "
+                                f"(oracle {orc.flat[worst]:.6g}); {int((err > lim).sum())} entries out")
+
+
+class Lockstep:
+    """One workload layer: a GPU pool plus the oracle's trajectory on
+    ``check_rows`` (batch rows whose slots are compared each step)."""
+
+    def __init__(self, w: W.Workload, pool, slots: torch.Tensor, bits: np.ndarray, check_rows: np.ndarray,
+                 S0_check: np.ndarray, layer: int = 0):
+        self.w, self.pool, self.slots, self.bits, self.layer = w, pool, slots, bits, layer
+        self.rows = np.asarray(check_rows)
+        n = len(self.rows) * w.n_v_heads
+        self.tile_bits = np.broadcast_to(bits[None], (len(self.rows),) + bits.shape).reshape(n, w.d_k)
+        S = S0_check.reshape(n, w.d_k, w.d_v)
+        self.r, self.c = oracle.fit_absmax(S)
+        self.codes = oracle.quantize(S.astype(np.float64), self.r, self.c, self.tile_bits)
+        dev = pool.device
+        self.ids = slots.index_select(0, torch.as_tensor(self.rows, dtype=torch.long, device=slots.device)).to(dev)
+        self.n_tiles = n
+        self.mismatches = 0
+        self.saturated = 0.0
+
+    def shaped(self, a, tail):
+        return a.reshape((len(self.rows), self.w.n_v_heads) + tail)
+
+    def anchor(self):
+        """Write the oracle's current state into the checked GPU slots."""
+        w, dev = self.w, self.pool.device
+        self.pool.import_(self.ids,
+                          torch.from_numpy(np.ascontiguousarray(self.shaped(self.codes, (w.d_k, w.d_v)))).to(dev),
+                          torch.from_numpy(np.ascontiguousarray(self.shaped(self.r, (w.d_k,)))).to(dev),
+                          torch.from_numpy(np.ascontiguousarray(self.shaped(self.c, (w.d_v,)))).to(dev))
+
+    def export(self):
+        w, dev = self.w, self.pool.device
+        n = len(self.rows)
+        codes = torch.empty((n, w.n_v_heads, w.d_k, w.d_v), dtype=torch.int8, device=dev)
+        r = torch.empty((n, w.n_v_heads, w.d_k), dtype=torch.float32, device=dev)
+        c = torch.empty((n, w.n_v_heads, w.d_v), dtype=torch.float32, device=dev)
+        self.pool.export(self.ids, codes, r, c)
+        torch.cuda.synchronize()
+        return codes.cpu().numpy().reshape(self.n_tiles, w.d_k, w.d_v), r.cpu().numpy(), c.cpu().numpy()
+
+    def check_step(self, inp: dict, o_gpu: torch.Tensor, step: int):
+        """Oracle step on its own state, compare with the GPU's result."""
+        w = self.w
+        q, k, v, a, b = oracle_inputs(w, inp, self.rows)
+        new, o, y = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True)
+        g_codes, g_r, g_c = self.export()
+        assert np.array_equal(g_r.reshape(self.r.shape), self.r), "row scales changed"
+        assert np.array_equal(g_c.reshape(self.c.shape), self.c), "column scales changed"
+        self.mismatches += compare_codes(g_codes, new, y, f"layer {self.layer} step {step} codes")
+        rows_t = torch.as_tensor(self.rows, dtype=torch.long, device=o_gpu.device)
+        og = o_gpu.index_select(0, rows_t).cpu().numpy().reshape(self.n_tiles, w.d_v)
+        compare_out(og, o, f"layer {self.layer} step {step} o")
+        qb = (2 ** (self.tile_bits.astype(np.int32) - 1) - 1)[:, :, None]
+        self.saturated = float(np.mean(np.abs(new) == qb))
+        self.codes = new
