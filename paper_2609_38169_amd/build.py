@@ -1,34 +1,67 @@
-"""Build libstepq.so in-tree with hipcc for gfx950."""
+"""Build libstepq.so in-tree for gfx950.
+
+Each source is compiled on its own (the .hip files with hipcc for gfx950,
+the host-only setup code with g++) and the objects are linked by hipcc.
+Mixing a `-x c++` source into one hipcc command makes hipcc drop
+--offload-arch and fall back to its default target, so the link step is
+followed by a check that the library's device bundle is gfx950 and only
+gfx950.
+"""
 from __future__ import annotations
 
 import os
+import re
 import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
+BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libstepq.so")
-SOURCES = ["stepq_host.hip", "stepq_kernels.hip", "stepq_setup.cpp"]
+HIP_SOURCES = ["stepq_host.hip", "stepq_kernels.hip"]
+CXX_SOURCES = ["stepq_setup.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
 
-FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+INCLUDES = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+HIP_FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     # packed fp32 VALU forms stay off: scalar fp32 only on the device
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
-    "-I", os.path.join(ROOT, "include"), "-I", CSRC,
 ]
+CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-pthread"]
+
+
+def device_targets(path: str) -> list[str]:
+    """Offload targets named in a built library's device bundle."""
+    data = open(path, "rb").read()
+    return sorted(set(t.decode() for t in re.findall(rb"hipv4-amdgcn-amd-amdhsa--(gfx[0-9a-f]+)", data)))
 
 
 def build(extra_flags: list[str] | None = None, out: str = LIB, verbose: bool = False) -> str:
-    hip = [os.path.join(CSRC, s) for s in SOURCES if s.endswith(".hip")]
-    cpp = [os.path.join(CSRC, s) for s in SOURCES if s.endswith(".cpp")]
-    srcs = hip + ["-x", "c++"] + cpp      # plain host C++ last
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    objs = []
+
+    def run(cmd):
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.check_call(cmd, cwd=CSRC)
+
+    for s in HIP_SOURCES:
+        o = os.path.join(BUILD_DIR, s + ".o")
+        run([HIPCC] + HIP_FLAGS + (extra_flags or []) + INCLUDES + ["-c", os.path.join(CSRC, s), "-o", o])
+        objs.append(o)
+    for s in CXX_SOURCES:
+        o = os.path.join(BUILD_DIR, s + ".o")
+        run(["g++"] + CXX_FLAGS + INCLUDES + ["-c", os.path.join(CSRC, s), "-o", o])
+        objs.append(o)
     tmp = out + ".tmp"
-    cmd = [HIPCC] + FLAGS + (extra_flags or []) + ["-o", tmp] + srcs
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.check_call(cmd, cwd=CSRC)
+    run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-pthread", "-o", tmp] + objs)
+    targets = device_targets(tmp)
+    if targets != [ARCH]:
+        os.remove(tmp)
+        raise RuntimeError(f"libstepq device bundle targets {targets}, expected only {ARCH}")
     os.replace(tmp, out)
     return out
 

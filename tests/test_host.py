@@ -120,3 +120,10 @@ def test_workload_draws_are_seeded():
     assert sorted(torch.cat(W.rotation_slots(W.workload(2))).tolist()) == list(range(2048))
     bits = W.bit_map_draw(W.workload(3)).numpy()
     assert all(sorted(np.bincount(row, minlength=9)[[2, 4, 8]]) == [32, 32, 64] for row in bits)
+
+
+def test_library_device_code_is_gfx950():
+    """The library must carry device code for gfx950 and nothing else (a
+    mixed hipcc command line once silently fell back to another target)."""
+    from paper_2609_38169_amd.build import device_targets
+    assert device_targets(stepq.LIB_PATH) == ["gfx950"]
