@@ -23,7 +23,6 @@ CXX_SOURCES = ["stepq_setup.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-INCLUDES = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
 HIP_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     # packed fp32 VALU forms stay off: scalar fp32 only on the device
@@ -39,23 +38,26 @@ def device_targets(path: str) -> list[str]:
     return sorted(set(t.decode() for t in re.findall(rb"hipv4-amdgcn-amd-amdhsa--(gfx[0-9a-f]+)", data)))
 
 
-def build(extra_flags: list[str] | None = None, out: str = LIB, verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
+def build(extra_flags: list[str] | None = None, out: str = LIB, verbose: bool = False, csrc: str = CSRC,
+          build_dir: str = BUILD_DIR) -> str:
+    os.makedirs(build_dir, exist_ok=True)
     objs = []
 
     def run(cmd):
         if verbose:
             print(" ".join(cmd), flush=True)
-        subprocess.check_call(cmd, cwd=CSRC)
+        subprocess.check_call(cmd, cwd=csrc)
 
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", csrc]
     for s in HIP_SOURCES:
-        o = os.path.join(BUILD_DIR, s + ".o")
-        run([HIPCC] + HIP_FLAGS + (extra_flags or []) + INCLUDES + ["-c", os.path.join(CSRC, s), "-o", o])
+        o = os.path.join(build_dir, s + ".o")
+        run([HIPCC] + HIP_FLAGS + (extra_flags or []) + inc + ["-c", os.path.join(csrc, s), "-o", o])
         objs.append(o)
     for s in CXX_SOURCES:
-        o = os.path.join(BUILD_DIR, s + ".o")
-        run(["g++"] + CXX_FLAGS + INCLUDES + ["-c", os.path.join(CSRC, s), "-o", o])
+        o = os.path.join(build_dir, s + ".o")
+        run(["g++"] + CXX_FLAGS + inc + ["-c", os.path.join(csrc, s), "-o", o])
         objs.append(o)
+    out = os.path.abspath(out)
     tmp = out + ".tmp"
     run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-pthread", "-o", tmp] + objs)
     targets = device_targets(tmp)

@@ -22,6 +22,7 @@ struct stepq_pool {
     HeadInfo *d_heads = nullptr;
     uint8_t *d_perm = nullptr;
     int device = 0;
+    int layout = 0;                   // uniform layout of every head, or 0
 };
 
 namespace {
@@ -78,6 +79,14 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
         hi.g4 = static_cast<uint16_t>((n4 + 1) / 2);
         hi.g2 = static_cast<uint16_t>((n2 + 3) / 4);
         hi.groups = static_cast<uint32_t>(hi.g8 + hi.g4 + hi.g2);
+        hi.layout = 0;
+        // compile-time bodies: d = 128, whole word-steps of one width, no empty slots
+        if (dv == 128 && dk == 128 && n4 == 2 * hi.g4 && n2 == 4 * hi.g2 && hi.g8 % 8 == 0 && hi.g4 % 8 == 0 &&
+            hi.g2 % 8 == 0)
+            for (int L = 0; L < stepq::kNumUniformLayouts; ++L) {
+                const stepq::UniformLayout &u = stepq::kUniformLayouts[L];
+                if (u.m8 * 8 == hi.g8 && u.m4 * 8 == hi.g4 && u.m2 * 8 == hi.g2) hi.layout = L + 1;
+            }
         const size_t creg = round128(static_cast<size_t>(hi.groups) * dv);
         const size_t tb = round128(creg + 4u * static_cast<size_t>(dk) + 4u * static_cast<size_t>(dv));
         hi.r_off = static_cast<uint32_t>(creg);
@@ -87,6 +96,14 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
     }
     *slot_bytes = off;
     return STEPQ_OK;
+}
+
+stepq::FastDiv fast_div(uint32_t d)
+{
+    uint32_t sh = 0;
+    while ((1ull << sh) < d) ++sh;
+    const uint64_t m = ((1ull << 32) * ((1ull << sh) - d)) / d + 1;
+    return stepq::FastDiv{static_cast<uint32_t>(m), sh};
 }
 
 stepq::PoolView view(const stepq_pool *p)
@@ -101,6 +118,8 @@ stepq::PoolView view(const stepq_pool *p)
     v.Hqk = p->Hqk;
     v.dk = p->dk;
     v.dv = p->dv;
+    v.div_hv = fast_div(static_cast<uint32_t>(p->Hv));
+    v.div_g = fast_div(static_cast<uint32_t>(p->Hv / p->Hqk));
     return v;
 }
 
@@ -180,6 +199,9 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
     p->dk = desc->d_k;
     p->dv = desc->d_v;
     p->bits.assign(desc->row_bits, desc->row_bits + static_cast<size_t>(p->Hv) * p->dk);
+    p->layout = static_cast<int>(p->heads[0].layout);
+    for (const HeadInfo &hi : p->heads)
+        if (static_cast<int>(hi.layout) != p->layout) p->layout = 0;
     p->pool_bytes = p->slot_bytes * static_cast<size_t>(p->n_slots);
     hipError_t e = hipGetDevice(&p->device);
     if (e != hipSuccess) {
@@ -251,7 +273,7 @@ stepq_status stepq_decode_step(stepq_pool *p, const int32_t *slot_ids, int32_t b
     a.beta = beta;
     a.o = o;
     a.batch = batch;
-    hipError_t e = stepq::launch_decode(a, act_dtype == STEPQ_BF16, s);
+    hipError_t e = stepq::launch_decode(a, act_dtype == STEPQ_BF16, p->layout, s);
     return e == hipSuccess ? STEPQ_OK : hip_fail(e, "decode launch");
 }
 

@@ -16,7 +16,24 @@ struct HeadInfo {
     uint16_t n8, n4, n2;  // rows of each width
     uint16_t g8, g4, g2;  // row groups of each width
     uint32_t groups;      // g8 + g4 + g2
+    uint32_t layout;      // index into kUniformLayouts + 1, or 0 for the generic path
 };
+
+// Row-group mixes with a compile-time decode body at d_v = 128, in units of
+// 8 row groups (one word-step of a 256-thread workgroup): {8-bit, 4-bit,
+// 2-bit}.  Heads whose mix is listed keep their codes in registers between
+// the two passes; any other mix takes the generic body.
+struct UniformLayout {
+    int m8, m4, m2;
+};
+constexpr UniformLayout kUniformLayouts[] = {
+    {8, 4, 0},    // 64 rows @8 + 64 rows @4 (6 bits/element)
+    {4, 2, 2},    // 32 @8 + 32 @4 + 64 @2 (4 bits/element)
+    {16, 0, 0},   // all rows @8
+    {0, 8, 0},    // all rows @4
+    {0, 0, 4},    // all rows @2
+};
+constexpr int kNumUniformLayouts = sizeof(kUniformLayouts) / sizeof(kUniformLayouts[0]);
 
 // Row-constant table index space: 8-bit rows, then the two slots of every
 // 4-bit group, then the four slots of every 2-bit group (empty slots
@@ -25,12 +42,20 @@ struct HeadInfo {
 constexpr int kMaxDk = 128;
 constexpr int kSlotTable = kMaxDk + 4;
 
+// n / d for 0 <= n < 2^31 by multiply-high (Granlund-Montgomery), with the
+// constants prepared on the host so that uniform quotients stay scalar.
+struct FastDiv {
+    uint32_t mul, shift;
+};
+
 struct PoolView {
     uint8_t *base;
     uint64_t slot_bytes;
     const HeadInfo *heads;   // [Hv], device
     const uint8_t *perm;     // [Hv][d_k] physical row -> logical row, device
     int32_t n_slots, Hv, Hqk, dk, dv;
+    FastDiv div_hv;          // divide by Hv
+    FastDiv div_g;           // divide by Hv / Hqk
 };
 
 struct DecodeArgs {
@@ -56,7 +81,8 @@ struct TileArgs {
     float *deq_out;          // Dequant: [n][Hv][dk][dv]
 };
 
-hipError_t launch_decode(const DecodeArgs &a, bool bf16, hipStream_t stream);
+// pool_layout: the uniform layout shared by every head (1-based), or 0.
+hipError_t launch_decode(const DecodeArgs &a, bool bf16, int pool_layout, hipStream_t stream);
 hipError_t launch_tile_op(const TileArgs &a, TileOp op, hipStream_t stream);
 
 }  // namespace stepq

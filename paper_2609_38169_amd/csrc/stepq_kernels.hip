@@ -81,103 +81,103 @@ __device__ __forceinline__ float sbyte(uint32_t w, int e)
     return static_cast<float>(static_cast<int8_t>(static_cast<uint8_t>(w >> (8 * e))));
 }
 
+__device__ __forceinline__ int fdiv(int n, FastDiv d)
+{
+    const uint32_t u = static_cast<uint32_t>(n);
+    return static_cast<int>((__umulhi(u, d.mul) + u) >> d.shift);
+}
+
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_term(float x)
+{
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWS, 0xF, false));
+}
+
+// Sum over the 64 lanes of a wavefront with DPP row operations; the result
+// is returned uniform (read from the last lane).
 __device__ __forceinline__ float wave_sum(float x)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
-    return x;
+    x += dpp_term<0xB1, 0xF>(x);    // quad_perm [1,0,3,2]
+    x += dpp_term<0x4E, 0xF>(x);    // quad_perm [2,3,0,1]: quad sums
+    x += dpp_term<0x141, 0xF>(x);   // row_half_mirror: 8-lane sums
+    x += dpp_term<0x140, 0xF>(x);   // row_mirror: 16-lane row sums
+    x += dpp_term<0x142, 0xA>(x);   // row_bcast:15 into rows 1, 3
+    x += dpp_term<0x143, 0xC>(x);   // row_bcast:31 into rows 2, 3
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
 }
 
-template <int B>
-__device__ __forceinline__ void accumulate(uint32_t w, int x0, const float *s_kt, const float *s_qt,
-                                           float (&acK)[4], float (&acQ)[4])
+// ---------------------------------------------------------------------------
+// decode step
+
+template <int DV>
+struct DecodeShared {
+    float2 kq[kSlotTable];               // (k_i r_i f_i / q_b, q_i r_i f_i / q_b) per row-table slot
+    float av[kSlotTable];                // beta k_i q_b / r_i
+    float sk[kMaxDk], sq[kMaxDk];        // k, q of the tile in logical row order
+    float sr[kMaxDk];                    // r in physical row order
+    int sperm[kMaxDk];                   // logical row of each physical row
+    float4 red[2][256 / (DV / 4)][DV / 4];
+    float bcol[DV];                      // delta_j / c_j
+    float kap[4];
+};
+
+struct TileCtx {
+    int tile, b, h, hq;
+    HeadInfo hi;
+    uint32_t *codes;
+    const float *rr, *cc;
+    float alpha, beta;
+};
+
+// Per-tile operands of thread tid, loaded together at the start of a tile:
+// k_i, q_i for logical row i = tid; r_p and the logical index of physical
+// row p = tid; c_j, v_j for column j = tid.
+struct RowColOps {
+    float k, q, r, c, v;
+    int perm;
+};
+
+template <bool BF16, int DV>
+__device__ __forceinline__ RowColOps load_ops(const DecodeArgs &a, int tile, int b, int hq, int h, const float *rr,
+                                              const float *cc)
 {
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float kt = s_kt[x0 + s];
-        const float qt = s_qt[x0 + s];
-        const uint32_t W = slot_top<B>(w, s);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float U = sbyte(W, e);
-            acK[e] = fmaf(kt, U, acK[e]);
-            acQ[e] = fmaf(qt, U, acQ[e]);
-        }
-    }
-}
-
-template <int B>
-__device__ __forceinline__ uint32_t requant(uint32_t w, int x0, const float *s_al, const float *s_a,
-                                            const float (&bc)[4])
-{
-    constexpr float qb = static_cast<float>((1 << (B - 1)) - 1);
-    constexpr uint32_t fmask = (1u << B) - 1u;
-    uint32_t out = 0;
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float al = s_al[x0 + s];
-        const float av = s_a[x0 + s];
-        const uint32_t W = slot_top<B>(w, s);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float U = sbyte(W, e);
-            float y = fmaf(al, U, av * bc[e]);
-            y = __builtin_rintf(y);
-            y = fminf(fmaxf(y, -qb), qb);
-            const uint32_t f = static_cast<uint32_t>(static_cast<int>(y)) & fmask;
-            out |= f << (8 * e + s * B);
-        }
-    }
-    return out;
-}
-
-template <int DV, bool BF16>
-__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
-{
-    constexpr int CG = DV / 4;              // words per row group
-    constexpr int NSL = 256 / CG;           // threads sharing one column word
-    constexpr int MMAX = kMaxDk * CG / 256; // words per thread when every row is 8-bit
-
-    __shared__ float s_kt[kSlotTable], s_qt[kSlotTable], s_a[kSlotTable], s_al[kSlotTable];
-    __shared__ float4 s_red[2][NSL][CG];
-    __shared__ float s_b[DV];
-    __shared__ float s_kap[4];
-
     const PoolView &P = a.pool;
     const int tid = threadIdx.x;
-    const int ntiles = a.batch * P.Hv;
-    const int tile = xcd_tile(blockIdx.x, ntiles);
-    const int b = tile / P.Hv;
-    const int h = tile - b * P.Hv;
-    const int hq = h / (P.Hv / P.Hqk);
-    const HeadInfo hi = P.heads[h];
-    const int slot = a.slot_ids[b];
-    uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + hi.tile_off;
-    uint32_t *codes = reinterpret_cast<uint32_t *>(rec);
-    const float *rr = reinterpret_cast<const float *>(rec + hi.r_off);
-    const float *cc = rr + P.dk;
-
-    const int cg = tid % CG;
-    const int slice = tid / CG;
-    const int ngroups = static_cast<int>(hi.groups);
-
-    // 1. the thread's code words (streamed: read once, written once)
-    uint32_t w[MMAX];
-#pragma unroll
-    for (int m = 0; m < MMAX; ++m) {
-        const int g = slice + NSL * m;
-        w[m] = g < ngroups ? __builtin_nontemporal_load(codes + tid + 256 * m) : 0u;
+    RowColOps op{0.f, 0.f, 0.f, 0.f, 0.f, 0};
+    if (tid < P.dk) {
+        const size_t off = (static_cast<size_t>(b) * P.Hqk + hq) * P.dk + tid;
+        op.k = act_ld<BF16>(a.k, off);
+        op.q = act_ld<BF16>(a.q, off);
+        op.r = rr[tid];
+        op.perm = P.perm[h * P.dk + tid];
     }
+    if (tid < DV) {
+        op.c = cc[tid];
+        op.v = act_ld<BF16>(a.v, static_cast<size_t>(tile) * DV + tid);
+    }
+    return op;
+}
 
-    // 2. per-row constants, indexed by row-table slot
-    const float alpha = act_ld<BF16>(a.alpha, tile);
-    const float beta = act_ld<BF16>(a.beta, tile);
+// Row constants into LDS, indexed by row-table slot, and q.k.  Two barriers;
+// returns q.k.  Rows are read through the physical -> logical permutation
+// from the LDS copy of k and q.
+template <int DV>
+__device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float beta, const RowColOps &op,
+                                               DecodeShared<DV> &sh)
+{
+    const int tid = threadIdx.x;
+    if (tid < dk) {
+        sh.sk[tid] = op.k;
+        sh.sq[tid] = op.q;
+        sh.sr[tid] = op.r;
+        sh.sperm[tid] = op.perm;
+    }
+    __syncthreads();
     float kq = 0.f;
     if (tid < kSlotTable) {
         const int x = tid;
-        int bw = 0, p = -1;
+        int bw = 8, p = -1;
         if (x < hi.n8) {
-            bw = 8;
             p = x;
         } else if (x < hi.n8 + 2 * hi.g4) {
             bw = 4;
@@ -188,83 +188,385 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
             const int kk = x - hi.n8 - 2 * hi.g4;
             if (kk < hi.n2) p = hi.n8 + hi.n4 + kk;
         }
-        float kt = 0.f, qt = 0.f, av = 0.f, al = 0.f;
+        float kt = 0.f, qt = 0.f, av = 0.f;
         if (p >= 0) {
-            const int i = P.perm[h * P.dk + p];
-            const size_t qk_off = (static_cast<size_t>(b) * P.Hqk + hq) * P.dk + i;
-            const float ki = act_ld<BF16>(a.k, qk_off);
-            const float qi = act_ld<BF16>(a.q, qk_off);
-            const float rp = rr[p];
-            const float qb = static_cast<float>((1 << (bw - 1)) - 1);
-            const float fsc = 1.0f / static_cast<float>(1 << (8 - bw));
-            const float rs = rp * fsc / qb;
+            // slot x holds physical row p, whose r and permutation entry were
+            // loaded by thread p
+            const int i = sh.sperm[p];
+            const float ki = sh.sk[i];
+            const float qi = sh.sq[i];
+            const float rp = sh.sr[p];
+            const float qb = bw == 8 ? 127.0f : (bw == 4 ? 7.0f : 1.0f);
+            // 2^(b-8) / q_b: 1/127, 1/112, 1/64 (an unpacked field reads 2^(8-b) q)
+            const float fq = bw == 8 ? (1.0f / 127.0f) : (bw == 4 ? (1.0f / 112.0f) : (1.0f / 64.0f));
+            const float rs = rp * fq;
             kt = ki * rs;
             qt = qi * rs;
-            av = beta * ki * (qb / rp);
-            al = alpha * fsc;
+            av = beta * ki * qb * __builtin_amdgcn_rcpf(rp);
             kq = qi * ki;
         }
-        s_kt[x] = kt;
-        s_qt[x] = qt;
-        s_a[x] = av;
-        s_al[x] = al;
+        sh.kq[x] = make_float2(kt, qt);
+        sh.av[x] = av;
     }
     kq = wave_sum(kq);
-    if ((tid & 63) == 0) s_kap[tid >> 6] = kq;
+    if ((tid & 63) == 0) sh.kap[tid >> 6] = kq;
     __syncthreads();
-    const float kappa = (s_kap[0] + s_kap[1]) + (s_kap[2] + s_kap[3]);
+    return (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
+}
 
-    // 3. S^T k and S^T q partial sums over the thread's rows, 4 columns
+// Uniform layouts: table slot = physical row = tid, widths known at compile time.
+template <int M8, int M4, int DV>
+__device__ __forceinline__ float row_constants_uniform(float beta, const RowColOps &op, DecodeShared<DV> &sh)
+{
+    constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
+    const int tid = threadIdx.x;
+    if (tid < 128) {
+        sh.sk[tid] = op.k;
+        sh.sq[tid] = op.q;
+    }
+    __syncthreads();
+    float kq = 0.f;
+    if (tid < 128) {
+        const int p = tid;
+        const float qb = p < X4 ? 127.0f : (p < X2 ? 7.0f : 1.0f);
+        const float fq = p < X4 ? (1.0f / 127.0f) : (p < X2 ? (1.0f / 112.0f) : (1.0f / 64.0f));
+        const float ki = sh.sk[op.perm];
+        const float qi = sh.sq[op.perm];
+        const float rs = op.r * fq;
+        sh.kq[p] = make_float2(ki * rs, qi * rs);
+        sh.av[p] = beta * ki * qb * __builtin_amdgcn_rcpf(op.r);
+        kq = qi * ki;
+    }
+    kq = wave_sum(kq);
+    if ((tid & 63) == 0) sh.kap[tid >> 6] = kq;
+    __syncthreads();
+    return (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
+}
+
+// Column sums of the per-thread partials, residual, readout, column factor
+// of the code-space update.  cj, vj: column tid's scale and value (threads
+// < DV, loaded at the start of the tile).  Ends with a barrier.
+template <int DV>
+__device__ __forceinline__ void column_phase(const DecodeArgs &a, int tile, float alpha, float beta,
+                                             DecodeShared<DV> &sh, float kappa, const float (&acK)[4],
+                                             const float (&acQ)[4], float cj, float vj)
+{
+    constexpr int CG = DV / 4, NSL = 256 / CG;
+    const int tid = threadIdx.x;
+    sh.red[0][tid / CG][tid % CG] = make_float4(acK[0], acK[1], acK[2], acK[3]);
+    sh.red[1][tid / CG][tid % CG] = make_float4(acQ[0], acQ[1], acQ[2], acQ[3]);
+    __syncthreads();
+    if (tid < DV) {
+        const int j = tid;
+        const float *rk = reinterpret_cast<const float *>(&sh.red[0][0][0]);
+        const float *rq = reinterpret_cast<const float *>(&sh.red[1][0][0]);
+        float sk = rk[j], sq = rq[j];
+#pragma unroll
+        for (int s = 1; s < NSL; ++s) {
+            sk += rk[s * DV + j];
+            sq += rq[s * DV + j];
+        }
+        const float delta = vj - alpha * (cj * sk);     // v - alpha (S^T k)
+        a.o[static_cast<size_t>(tile) * DV + j] = alpha * (cj * sq) + beta * kappa * delta;
+        sh.bcol[j] = delta * __builtin_amdgcn_rcpf(cj);
+    }
+    __syncthreads();
+}
+
+// Unpack one word's slot-s fields (2^(8-B) q each) and add them, weighted
+// by the slot's row constants, to the 4 column partials.
+template <int B>
+__device__ __forceinline__ void unpack_acc(uint32_t w, const float2 *kq, int x0, float *U, float (&acK)[4],
+                                           float (&acQ)[4])
+{
+#pragma unroll
+    for (int s = 0; s < 8 / B; ++s) {
+        const float2 c = kq[x0 + s];
+        const uint32_t W = slot_top<B>(w, s);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float u = sbyte(W, e);
+            U[4 * s + e] = u;
+            acK[e] = fmaf(c.x, u, acK[e]);
+            acQ[e] = fmaf(c.y, u, acQ[e]);
+        }
+    }
+}
+
+template <int B>
+__device__ __forceinline__ void unpack_word(uint32_t w, float *U)
+{
+#pragma unroll
+    for (int s = 0; s < 8 / B; ++s) {
+        const uint32_t W = slot_top<B>(w, s);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) U[4 * s + e] = sbyte(W, e);
+    }
+}
+
+// ---- codes kept as packed f16 pairs between the passes (exact: |2^(8-B) q| <= 127)
+
+// Bytes LO and HI of w, read as signed, to an f16 pair: one SDWA convert per
+// field, the second one writing the upper half in place.
+template <int LO, int HI>
+__device__ __forceinline__ uint32_t sbytes_f16(uint32_t w)
+{
+    uint32_t r;
+    asm("v_cvt_f16_i16_sdwa %0, sext(%1) dst_sel:WORD_0 dst_unused:UNUSED_PAD src0_sel:BYTE_%c2"
+        : "=v"(r) : "v"(w), "i"(LO));
+    asm("v_cvt_f16_i16_sdwa %0, sext(%1) dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_%c2"
+        : "+v"(r) : "v"(w), "i"(HI));
+    return r;
+}
+
+// a * h + c with h the low (HI = 0) or high (HI = 1) f16 half of hp, in fp32
+// (v_fma_mix_f32: the half is widened exactly inside the FMA).
+template <int HI>
+__device__ __forceinline__ float fma_mix(float a, uint32_t hp, float c)
+{
+    float r;
+    if constexpr (HI)
+        asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel:[0,1,0] op_sel_hi:[0,1,0]" : "=v"(r) : "v"(a), "v"(hp), "v"(c));
+    else
+        asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel_hi:[0,1,0]" : "=v"(r) : "v"(a), "v"(hp), "v"(c));
+    return r;
+}
+
+template <int E>
+__device__ __forceinline__ float fma_mix_e(float a, const uint32_t *U2, int s, float c)
+{
+    return fma_mix<E & 1>(a, U2[2 * s + (E >> 1)], c);
+}
+
+template <int B>
+__device__ __forceinline__ void unpack_acc_h(uint32_t w, const float2 *kq, int x0, uint32_t *U2, float (&acK)[4],
+                                             float (&acQ)[4])
+{
+#pragma unroll
+    for (int s = 0; s < 8 / B; ++s) {
+        const float2 c = kq[x0 + s];
+        const uint32_t W = slot_top<B>(w, s);
+        U2[2 * s] = sbytes_f16<0, 1>(W);
+        U2[2 * s + 1] = sbytes_f16<2, 3>(W);
+        acK[0] = fma_mix_e<0>(c.x, U2, s, acK[0]);
+        acQ[0] = fma_mix_e<0>(c.y, U2, s, acQ[0]);
+        acK[1] = fma_mix_e<1>(c.x, U2, s, acK[1]);
+        acQ[1] = fma_mix_e<1>(c.y, U2, s, acQ[1]);
+        acK[2] = fma_mix_e<2>(c.x, U2, s, acK[2]);
+        acQ[2] = fma_mix_e<2>(c.y, U2, s, acQ[2]);
+        acK[3] = fma_mix_e<3>(c.x, U2, s, acK[3]);
+        acQ[3] = fma_mix_e<3>(c.y, U2, s, acQ[3]);
+    }
+}
+
+template <int B, int E>
+__device__ __forceinline__ uint32_t requant_field(const uint32_t *U2, int s, float al, float a_s, float bce, uint32_t P)
+{
+    constexpr float bias = static_cast<float>(1 << (B - 1));
+    constexpr float top = static_cast<float>((1 << B) - 1);
+    const float tt = fmaf(a_s, bce, bias);
+    float y = fma_mix_e<E>(al, U2, s, tt);
+    y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
+    return __builtin_amdgcn_cvt_pk_u8_f32(y, E, P);
+}
+
+template <int B>
+__device__ __forceinline__ uint32_t requant_word_h(const uint32_t *U2, const float *av, int x0, float al,
+                                                   const float (&bc)[4])
+{
+    constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
+    uint32_t out = 0;
+#pragma unroll
+    for (int s = 0; s < 8 / B; ++s) {
+        const float a_s = av[x0 + s];
+        uint32_t P = 0;
+        P = requant_field<B, 0>(U2, s, al, a_s, bc[0], P);
+        P = requant_field<B, 1>(U2, s, al, a_s, bc[1], P);
+        P = requant_field<B, 2>(U2, s, al, a_s, bc[2], P);
+        P = requant_field<B, 3>(U2, s, al, a_s, bc[3], P);
+        out |= P << (s * B);
+    }
+    return out ^ flip;
+}
+
+// New word from the unpacked old fields: per field
+//   y = al U + av_i bc_j + 2^(B-1)        (code + bias, Eq. 3 argument)
+// clamped to [1, 2^B - 1] (i.e. code in [-q_b, q_b]), rounded to nearest
+// even and packed to a byte by v_cvt_pk_u8_f32, then the bias is removed
+// from all fields at once by flipping each field's top bit.
+template <int B>
+__device__ __forceinline__ uint32_t requant_word(const float *U, const float *av, int x0, float al,
+                                                 const float (&bc)[4])
+{
+    constexpr float bias = static_cast<float>(1 << (B - 1));
+    constexpr float top = static_cast<float>((1 << B) - 1);
+    constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
+    uint32_t out = 0;
+#pragma unroll
+    for (int s = 0; s < 8 / B; ++s) {
+        const float a_s = av[x0 + s];
+        uint32_t P = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float tt = fmaf(a_s, bc[e], bias);
+            float y = fmaf(al, U[4 * s + e], tt);
+            y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
+            P = __builtin_amdgcn_cvt_pk_u8_f32(y, e, P);
+        }
+        out |= P << (s * B);
+    }
+    return out ^ flip;
+}
+
+// Rows of one width per word-step; codes stay in registers between passes.
+template <bool BF16, int M8, int M4, int M2>
+__device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCtx &t, DecodeShared<128> &sh)
+{
+    constexpr int M = M8 + M4 + M2;
+    constexpr int NE = 4 * (M8 + 2 * M4 + 4 * M2);
+    constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;    // row-table starts of the 4- and 2-bit slots
+    const int tid = threadIdx.x;
+    const int cg = tid & 31, slice = tid >> 5;
+    uint32_t w[M];
+#pragma unroll
+    for (int m = 0; m < M; ++m) w[m] = __builtin_nontemporal_load(t.codes + tid + 256 * m);
+
+    const RowColOps op = load_ops<BF16, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
+    const float kappa = row_constants_uniform<M8, M4, 128>(t.beta, op, sh);
+
+    uint32_t U[NE / 2];
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int m = 0; m < M8; ++m) unpack_acc_h<8>(w[m], sh.kq, slice + 8 * m, &U[2 * m], acK, acQ);
+#pragma unroll
+    for (int m = 0; m < M4; ++m)
+        unpack_acc_h<4>(w[M8 + m], sh.kq, X4 + 2 * (slice + 8 * m), &U[2 * M8 + 4 * m], acK, acQ);
+#pragma unroll
+    for (int m = 0; m < M2; ++m)
+        unpack_acc_h<2>(w[M8 + M4 + m], sh.kq, X2 + 4 * (slice + 8 * m), &U[2 * M8 + 4 * M4 + 8 * m], acK, acQ);
+
+    column_phase<128>(a, t.tile, t.alpha, t.beta, sh, kappa, acK, acQ, op.c, op.v);
+
+    const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
+    const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+    for (int m = 0; m < M8; ++m)
+        __builtin_nontemporal_store(requant_word_h<8>(&U[2 * m], sh.av, slice + 8 * m, t.alpha, bc),
+                                    t.codes + tid + 256 * m);
+#pragma unroll
+    for (int m = 0; m < M4; ++m)
+        __builtin_nontemporal_store(requant_word_h<4>(&U[2 * M8 + 4 * m], sh.av, X4 + 2 * (slice + 8 * m),
+                                                    t.alpha * (1.0f / 16.0f), bc),
+                                    t.codes + tid + 256 * (M8 + m));
+#pragma unroll
+    for (int m = 0; m < M2; ++m)
+        __builtin_nontemporal_store(requant_word_h<2>(&U[2 * M8 + 4 * M4 + 8 * m], sh.av, X2 + 4 * (slice + 8 * m),
+                                                    t.alpha * (1.0f / 64.0f), bc),
+                                    t.codes + tid + 256 * (M8 + M4 + m));
+}
+
+// Any row-width mix and d_v: the class of each word-step is looked up at run
+// time and the words are unpacked again for the second pass.
+template <bool BF16, int DV>
+__device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCtx &t, DecodeShared<DV> &sh)
+{
+    constexpr int CG = DV / 4;
+    constexpr int NSL = 256 / CG;
+    constexpr int MMAX = kMaxDk * CG / 256;
+    const int tid = threadIdx.x;
+    const int cg = tid % CG, slice = tid / CG;
+    const int ngroups = static_cast<int>(t.hi.groups);
+    uint32_t w[MMAX];
+#pragma unroll
+    for (int m = 0; m < MMAX; ++m) {
+        const int g = slice + NSL * m;
+        w[m] = g < ngroups ? __builtin_nontemporal_load(t.codes + tid + 256 * m) : 0u;
+    }
+    const RowColOps op = load_ops<BF16, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
+    const float kappa = row_constants<DV>(t.hi, a.pool.dk, t.beta, op, sh);
+
+    float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
+    float U[16];
 #pragma unroll
     for (int m = 0; m < MMAX; ++m) {
         const int g = slice + NSL * m;
         if (g < ngroups) {
-            const GroupRows gr = group_rows(hi, g);
-            if (gr.bits == 8) accumulate<8>(w[m], gr.x0, s_kt, s_qt, acK, acQ);
-            else if (gr.bits == 4) accumulate<4>(w[m], gr.x0, s_kt, s_qt, acK, acQ);
-            else accumulate<2>(w[m], gr.x0, s_kt, s_qt, acK, acQ);
+            const GroupRows gr = group_rows(t.hi, g);
+            if (gr.bits == 8) unpack_acc<8>(w[m], sh.kq, gr.x0, U, acK, acQ);
+            else if (gr.bits == 4) unpack_acc<4>(w[m], sh.kq, gr.x0, U, acK, acQ);
+            else unpack_acc<2>(w[m], sh.kq, gr.x0, U, acK, acQ);
         }
     }
-    s_red[0][slice][cg] = make_float4(acK[0], acK[1], acK[2], acK[3]);
-    s_red[1][slice][cg] = make_float4(acQ[0], acQ[1], acQ[2], acQ[3]);
-    __syncthreads();
+    column_phase<DV>(a, t.tile, t.alpha, t.beta, sh, kappa, acK, acQ, op.c, op.v);
 
-    // 4. column reductions, residual, readout, code-space column factor
-    if (tid < DV) {
-        const int j = tid;
-        const float *rk = reinterpret_cast<const float *>(&s_red[0][0][0]);
-        const float *rq = reinterpret_cast<const float *>(&s_red[1][0][0]);
-        float sk = 0.f, sq = 0.f;
-#pragma unroll
-        for (int s = 0; s < NSL; ++s) {
-            sk += rk[s * DV + j];
-            sq += rq[s * DV + j];
-        }
-        const float cj = cc[j];
-        const float u = cj * sk;
-        const float pq = cj * sq;
-        const float vj = act_ld<BF16>(a.v, static_cast<size_t>(tile) * DV + j);
-        const float delta = vj - alpha * u;
-        a.o[static_cast<size_t>(tile) * DV + j] = alpha * pq + beta * kappa * delta;
-        s_b[j] = delta / cj;
-    }
-    __syncthreads();
-
-    // 5. requantize in place
-    const float4 b4 = *reinterpret_cast<const float4 *>(&s_b[4 * cg]);
+    const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
     for (int m = 0; m < MMAX; ++m) {
         const int g = slice + NSL * m;
         if (g < ngroups) {
-            const GroupRows gr = group_rows(hi, g);
+            const GroupRows gr = group_rows(t.hi, g);
             uint32_t nw;
-            if (gr.bits == 8) nw = requant<8>(w[m], gr.x0, s_al, s_a, bc);
-            else if (gr.bits == 4) nw = requant<4>(w[m], gr.x0, s_al, s_a, bc);
-            else nw = requant<2>(w[m], gr.x0, s_al, s_a, bc);
-            __builtin_nontemporal_store(nw, codes + tid + 256 * m);
+            if (gr.bits == 8) {
+                unpack_word<8>(w[m], U);
+                nw = requant_word<8>(U, sh.av, gr.x0, t.alpha, bc);
+            } else if (gr.bits == 4) {
+                unpack_word<4>(w[m], U);
+                nw = requant_word<4>(U, sh.av, gr.x0, t.alpha * (1.0f / 16.0f), bc);
+            } else {
+                unpack_word<2>(w[m], U);
+                nw = requant_word<2>(U, sh.av, gr.x0, t.alpha * (1.0f / 64.0f), bc);
+            }
+            __builtin_nontemporal_store(nw, t.codes + tid + 256 * m);
         }
+    }
+}
+
+// LAYOUT > 0: every head of the pool has uniform layout LAYOUT (checked on
+// the host), so the kernel holds only that body and its register budget.
+// LAYOUT == 0: heads may differ; each workgroup branches on its head's
+// layout (uniformly, so without divergence); d_v = 64 and irregular
+// row-width mixes take the generic body.
+template <int DV, bool BF16, int LAYOUT>
+__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
+{
+    __shared__ DecodeShared<DV> sh;
+    const PoolView &P = a.pool;
+    TileCtx t;
+    t.tile = xcd_tile(blockIdx.x, a.batch * P.Hv);
+    t.b = fdiv(t.tile, P.div_hv);
+    t.h = t.tile - t.b * P.Hv;
+    t.hq = fdiv(t.h, P.div_g);
+    const int slot = a.slot_ids[t.b];
+    t.alpha = act_ld<BF16>(a.alpha, t.tile);
+    t.beta = act_ld<BF16>(a.beta, t.tile);
+    if constexpr (DV == 128 && LAYOUT > 0) {
+        // every tile record is (codes: 1024 bytes per word-step) + r + c
+        constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
+        constexpr uint32_t r_off = 1024u * (u.m8 + u.m4 + u.m2);
+        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes +
+                       static_cast<uint64_t>(t.h) * (r_off + 1024u);
+        t.codes = reinterpret_cast<uint32_t *>(rec);
+        t.rr = reinterpret_cast<const float *>(rec + r_off);
+        t.cc = t.rr + 128;
+        decode_uniform<BF16, u.m8, u.m4, u.m2>(a, t, sh);
+    } else {
+        t.hi = P.heads[t.h];
+        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.hi.tile_off;
+        t.codes = reinterpret_cast<uint32_t *>(rec);
+        t.rr = reinterpret_cast<const float *>(rec + t.hi.r_off);
+        t.cc = t.rr + P.dk;
+        if constexpr (DV == 128) {
+            switch (t.hi.layout) {
+            case 1: decode_uniform<BF16, 8, 4, 0>(a, t, sh); return;
+            case 2: decode_uniform<BF16, 4, 2, 2>(a, t, sh); return;
+            case 3: decode_uniform<BF16, 16, 0, 0>(a, t, sh); return;
+            case 4: decode_uniform<BF16, 0, 8, 0>(a, t, sh); return;
+            case 5: decode_uniform<BF16, 0, 0, 4>(a, t, sh); return;
+            default: break;
+            }
+        }
+        decode_generic<BF16, DV>(a, t, sh);
     }
 }
 
@@ -351,19 +653,31 @@ __global__ __launch_bounds__(256) void tile_kernel(TileArgs a)
     }
 }
 
+template <bool BF16>
+hipError_t launch_decode_128(const DecodeArgs &a, int layout, unsigned grid, hipStream_t s)
+{
+    switch (layout) {
+    case 1: hipLaunchKernelGGL((decode_kernel<128, BF16, 1>), dim3(grid), dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((decode_kernel<128, BF16, 2>), dim3(grid), dim3(256), 0, s, a); break;
+    case 3: hipLaunchKernelGGL((decode_kernel<128, BF16, 3>), dim3(grid), dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((decode_kernel<128, BF16, 4>), dim3(grid), dim3(256), 0, s, a); break;
+    case 5: hipLaunchKernelGGL((decode_kernel<128, BF16, 5>), dim3(grid), dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((decode_kernel<128, BF16, 0>), dim3(grid), dim3(256), 0, s, a); break;
+    }
+    return hipGetLastError();
+}
+
 }  // namespace
 
-hipError_t launch_decode(const DecodeArgs &a, bool bf16, hipStream_t stream)
+hipError_t launch_decode(const DecodeArgs &a, bool bf16, int pool_layout, hipStream_t stream)
 {
     const unsigned grid = static_cast<unsigned>(a.batch) * static_cast<unsigned>(a.pool.Hv);
     if (grid == 0) return hipSuccess;
-    if (a.pool.dv == 128) {
-        if (bf16) hipLaunchKernelGGL((decode_kernel<128, true>), dim3(grid), dim3(256), 0, stream, a);
-        else hipLaunchKernelGGL((decode_kernel<128, false>), dim3(grid), dim3(256), 0, stream, a);
-    } else {
-        if (bf16) hipLaunchKernelGGL((decode_kernel<64, true>), dim3(grid), dim3(256), 0, stream, a);
-        else hipLaunchKernelGGL((decode_kernel<64, false>), dim3(grid), dim3(256), 0, stream, a);
-    }
+    if (a.pool.dv == 128)
+        return bf16 ? launch_decode_128<true>(a, pool_layout, grid, stream)
+                    : launch_decode_128<false>(a, pool_layout, grid, stream);
+    if (bf16) hipLaunchKernelGGL((decode_kernel<64, true, 0>), dim3(grid), dim3(256), 0, stream, a);
+    else hipLaunchKernelGGL((decode_kernel<64, false, 0>), dim3(grid), dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -16,7 +16,8 @@ import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libstepq.so")
+# STEPQ_LIB may name another build of the same library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("STEPQ_LIB") or os.path.join(_HERE, "libstepq.so")
 
 STEPQ_F32, STEPQ_BF16 = 0, 1
 _STATUS = {0: "STEPQ_OK", 1: "STEPQ_E_INVALID", 2: "STEPQ_E_UNSUPPORTED", 3: "STEPQ_E_NOMEM", 4: "STEPQ_E_HIP"}
