@@ -12,7 +12,8 @@ Prints one JSON line (rank 0):
   value      state-updates/s (tiles advanced per second) over the timed steps
   roofline   the decode kernel's algorithmic state bytes per launch (codes
              read + codes written + scales read) / its mean launch duration
-             from HIP events around every launch, against the 8 TB/s HBM peak
+             (HIP events around the K back-to-back timed launches, gaps
+             included), against the 8 TB/s HBM peak
   cpu_baseline  the fp64 oracle on the host cores on a bounded sample
 """
 from __future__ import annotations
@@ -136,20 +137,30 @@ def main():
 
     K = args.steps
     stream = torch.cuda.current_stream()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * K)]
+    # timed region: K back-to-back launches between two events on the launch stream
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0.record(stream)
     for i in range(K):
-        ev[2 * i].record(stream)
         launch(args.warmup + i)
-        ev[2 * i + 1].record(stream)
     t1.record(stream)
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
-    per_launch_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(K)]
-    kern_ms = float(np.mean(per_launch_ms))
+    kern_ms = total_ms / K          # mean launch duration, gaps between launches included
+
+    # diagnostics outside the timed region: one event pair per launch
+    n_diag = min(K, 64)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * n_diag)]
+    for i in range(n_diag):
+        ev[2 * i].record(stream)
+        launch(args.warmup + K + i)
+        ev[2 * i + 1].record(stream)
+    torch.cuda.synchronize()
+    per_launch_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(n_diag)]
+    nsub = len(subsets)
+    per_subset = [float(np.mean([per_launch_ms[i] for i in range(n_diag) if (args.warmup + K + i) % nsub == j] or [0.0]))
+                  for j in range(nsub)]
 
     tiles = w.tiles_per_step
     per_tile = [state_bytes_per_tile(bits[h], w.d_k, w.d_v) for h in range(w.n_v_heads)]
@@ -187,7 +198,8 @@ def main():
             "traffic": traffic_entry(launch_bytes),
             "kernel": "decode_kernel<128, bf16>",
             "kernel_ms_mean": kern_ms,
-            "kernel_ms_min": float(np.min(per_launch_ms)),
+            "launch_ms_event_pairs": {"mean": float(np.mean(per_launch_ms)), "min": float(np.min(per_launch_ms)),
+                                      "max": float(np.max(per_launch_ms)), "per_slot_subset": per_subset},
             "bytes_per_launch": launch_bytes,
             "activation_bytes_per_launch": act_bytes,
             "kernel_sha": kernel_hash(),
