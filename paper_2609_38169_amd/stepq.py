@@ -155,6 +155,32 @@ class Pool:
     def step(self, slot_ids, q, k, v, alpha, beta, o, stream=None):
         stepq_decode_step(self, slot_ids, q, k, v, alpha, beta, o, stream)
 
+    def prepare_step(self, slot_ids, q, k, v, alpha, beta, o, stream=None):
+        """Validate the arguments of one decode step once and return a
+        callable that launches it with the cached pointers (for decode loops
+        where the per-call checks would dominate the launch cost)."""
+        n, ids = _ids(self, slot_ids)
+        dt = q.dtype
+        if dt not in (torch.float32, torch.bfloat16):
+            raise TypeError("activations must be float32 or bfloat16")
+        code = STEPQ_F32 if dt == torch.float32 else STEPQ_BF16
+        args = (self.handle, ids, n,
+                _dev(q, "q", dt, (n, self.Hqk, self.dk), self.device),
+                _dev(k, "k", dt, (n, self.Hqk, self.dk), self.device),
+                _dev(v, "v", dt, (n, self.Hv, self.dv), self.device),
+                _dev(alpha, "alpha", dt, (n, self.Hv), self.device),
+                _dev(beta, "beta", dt, (n, self.Hv), self.device), code,
+                _dev(o, "o", torch.float32, (n, self.Hv, self.dv), self.device), _stream(stream))
+        keep = (slot_ids, q, k, v, alpha, beta, o)      # the tensors must outlive the callable
+        fn = lib().stepq_decode_step
+
+        def launch():
+            _ = keep
+            st = fn(*args)
+            if st != 0:
+                _check(st)
+        return launch
+
     def dequant(self, slot_ids, out, stream=None):
         stepq_pool_dequant(self, slot_ids, out, stream)
 

@@ -281,3 +281,20 @@ def test_decode_stack48_graph():
         for L in layers_checked:
             locks[L].check_step(step_inp[L], bufs[L]["o"], t)
         _say(f"stack48: replay {t} ok")
+
+
+def test_prepared_step_matches_checked_call():
+    """Pool.prepare_step launches the same C call with cached arguments."""
+    w = W.workload(0)
+    bits = row_bits(w)
+    pa = build_pool(w, device=DEV, bits=bits)
+    pb = build_pool(w, device=DEV, bits=bits)
+    ids = W.active_slots(w).to(DEV)
+    inp = W.step_inputs(w, 0, 0, device=DEV)
+    oa = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=DEV)
+    ob = torch.empty_like(oa)
+    pa.step(ids, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], oa)
+    run = pb.prepare_step(ids, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], ob)
+    run()
+    torch.cuda.synchronize()
+    assert torch.equal(oa, ob) and torch.equal(pa.memory, pb.memory)
