@@ -109,6 +109,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-ref", action="store_true", help="also time a plain device copy of the same bytes")
+    ap.add_argument("--kda", action="store_true", help="channel-wise (KDA) gates [B][Hv][d_k] instead of alpha")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -131,6 +132,9 @@ def main():
     subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
     n_inp = min(w.steps, args.steps + args.warmup)
     inputs = [W.step_inputs(w, 0, t, device=dev) for t in range(n_inp)]
+    if args.kda:
+        for t, inp in enumerate(inputs):
+            inp["alpha"] = W.kda_gates(w, 0, t, device=dev)
     o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=dev)
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
@@ -183,7 +187,8 @@ def main():
     tiles = w.tiles_per_step
     per_tile = [state_bytes_per_tile(bits[h], w.d_k, w.d_v) for h in range(w.n_v_heads)]
     launch_bytes = w.batch * sum(per_tile)
-    act_bytes = w.batch * (2 * w.n_qk_heads * w.d_k * 2 + w.n_v_heads * w.d_v * 2 + 2 * w.n_v_heads * 2
+    gate_elems = w.n_v_heads * (w.d_k if args.kda else 1)
+    act_bytes = w.batch * (2 * w.n_qk_heads * w.d_k * 2 + w.n_v_heads * w.d_v * 2 + (gate_elems + w.n_v_heads) * 2
                            + w.n_v_heads * w.d_v * 4 + 4)
     achieved = launch_bytes / (kern_ms * 1e-3) / 1e9
     value = tiles * K / (total_ms * 1e-3)
@@ -204,7 +209,8 @@ def main():
         "config": {"workload": f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
                                f"d_k=d_v={w.d_k}, 6-bit mixed {{4,8}}, fp32 scales, bf16 activations",
                    "slot_rotation": 1 if args.resident else len(subsets),
-                   "cache_resident": bool(args.resident)},
+                   "cache_resident": bool(args.resident),
+                   "gate": "channel-wise d [B][Hv][d_k] (KDA)" if args.kda else "scalar alpha [B][Hv] (GDN)"},
         "GBps_state": launch_bytes * K / (total_ms * 1e-3) / 1e9,
         "pct_hbm_peak": 100.0 * launch_bytes * K / (total_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "roofline": {
@@ -213,8 +219,8 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic_entry(launch_bytes),
-            "kernel": "decode_kernel<128, bf16>",
+            "traffic": None if args.kda else traffic_entry(launch_bytes),
+            "kernel": "decode_kernel<128, bf16, kda>" if args.kda else "decode_kernel<128, bf16>",
             "kernel_ms_mean": kern_ms,
             "launch_ms_event_pairs": {"mean": float(np.mean(per_launch_ms)), "min": float(np.min(per_launch_ms)),
                                       "max": float(np.max(per_launch_ms)), "per_slot_subset": per_subset},

@@ -133,6 +133,17 @@ stepq_status stepq_decode_step(stepq_pool *pool, const int32_t *slot_ids, int32_
                                const void *k, const void *v, const void *alpha, const void *beta,
                                stepq_dtype act_dtype, float *o, void *stream);
 
+/* The same decode step with the channel-wise retention gate of KDA,
+ * D = diag(d) instead of alpha I (paper, Section 2.1 and Eq. 1):
+ *   X = D S^ + beta k (v - S^T D k)^T,   o = X^T q,
+ * requantized as above.  gate: [batch][Hv][d_k] in act_dtype, one retention
+ * factor per key row (logical order) of each (request, value head); the
+ * other arguments are those of stepq_decode_step.  With every d_i equal to
+ * alpha the two calls compute the same update. */
+stepq_status stepq_decode_step_kda(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
+                                   const void *k, const void *v, const void *gate, const void *beta,
+                                   stepq_dtype act_dtype, float *o, void *stream);
+
 /* Reconstruct S^_ij = r_i c_j q_ij / q_{b_i} (Section 4.3) for n slots into
  * out [n][Hv][d_k][d_v] fp32, logical row order.  Computed in fp32. */
 stepq_status stepq_pool_dequant(const stepq_pool *pool, const int32_t *slot_ids, int32_t n, float *out,

@@ -50,8 +50,8 @@ def lib():
         L.orc_fit_absmax.argtypes = [i, i, i, P, P, P, P]
         L.orc_quantize.argtypes = [i, i, i, P, P, P, P, P, P]
         L.orc_dequant.argtypes = [i, i, i, P, P, P, P, P]
-        L.orc_update_fp.argtypes = [i, i, i, P, P, P, P, P, P, P, P]
-        L.orc_decode_step.argtypes = [i, i, i, P, P, P, P, P, P, P, P, P, P, P, P]
+        L.orc_update_fp.argtypes = [i, i, i, P, P, P, P, P, i, P, P, P]
+        L.orc_decode_step.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P]
         L.orc_tile_bytes.argtypes = [i, i, P]
         L.orc_tile_bytes.restype = ctypes.c_size_t
         L.orc_slot_bytes.argtypes = [i, i, i, P]
@@ -110,30 +110,42 @@ def dequant(codes, r, c, bits):
     return S
 
 
+def _gates(alpha, n, dk):
+    """alpha [n] (scalar gate, GDN) or [n][dk] (channel-wise gate, KDA)."""
+    a = _c(alpha, np.float64)
+    if a.size == n:
+        return a.reshape(n), 0
+    return a.reshape(n, dk), 1
+
+
 def update_fp(S, q, k, v, alpha, beta):
-    """Eq. 1 (D = alpha I) on a real state, readout from X (Eq. 4)."""
+    """Eq. 1 with D = alpha I (alpha [n]) or D = diag(d) (alpha [n][dk]) on a
+    real state; readout from X (Eq. 4)."""
     S = _c(S, np.float64)
     n, dk, dv = S.shape
     q, k, v = _c(q, np.float64), _c(k, np.float64), _c(v, np.float64)
-    alpha, beta = _c(alpha, np.float64).reshape(n), _c(beta, np.float64).reshape(n)
+    a, per_row = _gates(alpha, n, dk)
+    beta = _c(beta, np.float64).reshape(n)
     X = np.empty_like(S)
     o = np.empty((n, dv), np.float64)
-    lib().orc_update_fp(n, dk, dv, _p(S), _p(q), _p(k), _p(v), _p(alpha), _p(beta), _p(X), _p(o))
+    lib().orc_update_fp(n, dk, dv, _p(S), _p(q), _p(k), _p(v), _p(a), per_row, _p(beta), _p(X), _p(o))
     return X, o
 
 
 def decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=False):
-    """One quantized decode step with frozen scales (Table C2 steps 1-3, 6)."""
+    """One quantized decode step with frozen scales (Table C2 steps 1-3, 6);
+    alpha [n] for the GDN gate or [n][dk] for the KDA channel-wise gate."""
     codes = _c(codes, np.int8)
     n, dk, dv = codes.shape
     r, c, bits = _c(r, np.float32), _c(c, np.float32), _c(np.broadcast_to(bits, (n, dk)), np.uint8)
     q, k, v = _c(q, np.float64), _c(k, np.float64), _c(v, np.float64)
-    alpha, beta = _c(alpha, np.float64).reshape(n), _c(beta, np.float64).reshape(n)
+    a, per_row = _gates(alpha, n, dk)
+    beta = _c(beta, np.float64).reshape(n)
     out = np.empty_like(codes)
     o = np.empty((n, dv), np.float64)
     y = np.empty((n, dk, dv), np.float64) if want_y else None
     lib().orc_decode_step(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(q), _p(k), _p(v),
-                          _p(alpha), _p(beta), _p(out), _p(o), _p(y))
+                          _p(a), per_row, _p(beta), _p(out), _p(o), _p(y))
     return (out, o, y) if want_y else (out, o)
 
 

@@ -115,19 +115,20 @@ void orc_dequant(int n_tiles, int dk, int dv, const int8_t *codes, const float *
 }
 
 /* ------------------------------------------------------------------------
- * Gated Delta update on a real-valued state, GDN gate D = alpha I
- * (Eq. 1, first form, and the readout of Eq. 4 taken from X before any
- * requantization):
- *   R = alpha S                       retained state
+ * Gated Delta update on a real-valued state (Eq. 1, first form) with a
+ * diagonal retention gate D = diag(d) -- the KDA form; GDN is d_i = alpha
+ * for every i -- and the readout of Eq. 4 taken from X before any
+ * requantization:
+ *   R = D S                           retained state
  *   e_j = v_j - sum_i k_i R_ij        residual of the retrieval k^T R
  *   X_ij = R_ij + beta k_i e_j
  *   o_j = sum_i X_ij q_i              (X^T q)
  */
 static void update_tile(int dk, int dv, const double *S, const double *q, const double *k,
-                        const double *v, double alpha, double beta, double *X, double *o)
+                        const double *v, const double *d, double beta, double *X, double *o)
 {
     for (int i = 0; i < dk; ++i)
-        for (int j = 0; j < dv; ++j) X[(size_t)i * dv + j] = alpha * S[(size_t)i * dv + j];
+        for (int j = 0; j < dv; ++j) X[(size_t)i * dv + j] = d[i] * S[(size_t)i * dv + j];
     for (int j = 0; j < dv; ++j) {
         double kr = 0.0;
         for (int i = 0; i < dk; ++i) kr += k[i] * X[(size_t)i * dv + j];
@@ -141,25 +142,39 @@ static void update_tile(int dk, int dv, const double *S, const double *q, const 
     }
 }
 
+/* gates: alpha [n] (scalar gate per tile) when per_row == 0, or d [n][dk] */
+static const double *gate_of(const double *alpha, int per_row, int t, int dk, double *buf)
+{
+    if (per_row) return alpha + (size_t)t * dk;
+    for (int i = 0; i < dk; ++i) buf[i] = alpha[t];
+    return buf;
+}
+
 void orc_update_fp(int n_tiles, int dk, int dv, const double *S, const double *q, const double *k,
-                   const double *v, const double *alpha, const double *beta, double *X, double *o)
+                   const double *v, const double *alpha, int per_row, const double *beta, double *X,
+                   double *o)
 {
     #pragma omp parallel for schedule(static)
-    for (int t = 0; t < n_tiles; ++t)
+    for (int t = 0; t < n_tiles; ++t) {
+        double *buf = (double *)malloc(sizeof(double) * dk);
         update_tile(dk, dv, S + (size_t)t * dk * dv, q + (size_t)t * dk, k + (size_t)t * dk,
-                    v + (size_t)t * dv, alpha[t], beta[t], X + (size_t)t * dk * dv, o + (size_t)t * dv);
+                    v + (size_t)t * dv, gate_of(alpha, per_row, t, dk, buf), beta[t],
+                    X + (size_t)t * dk * dv, o + (size_t)t * dv);
+        free(buf);
+    }
 }
 
 /* ------------------------------------------------------------------------
  * One decode step on a quantized tile (Appendix C, Table C2, with frozen
- * scales):  reconstruct S^ (step 1), X = alpha S^ + beta k (v - alpha k^T S^)
- * (step 2), emit o = X^T q before requantization (step 3), requantize X on
- * the same r, c and per-row widths (Eq. 3) as the new codes.
+ * scales):  reconstruct S^ (step 1), X = D S^ + beta k (v - k^T D S^)
+ * (step 2; D = alpha I or diag(d)), emit o = X^T q before requantization
+ * (step 3), requantize X on the same r, c and per-row widths (Eq. 3) as the
+ * new codes.
  * y (optional) receives X q_b/(r c) before rounding.
  */
 void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const float *r,
                      const float *c, const uint8_t *bits, const double *q, const double *k,
-                     const double *v, const double *alpha, const double *beta,
+                     const double *v, const double *alpha, int per_row, const double *beta,
                      int8_t *codes_out, double *o, double *y)
 {
     #pragma omp parallel for schedule(dynamic, 4)
@@ -167,6 +182,7 @@ void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const 
         size_t nel = (size_t)dk * dv;
         double *Sh = (double *)malloc(sizeof(double) * nel);
         double *X = (double *)malloc(sizeof(double) * nel);
+        double *gbuf = (double *)malloc(sizeof(double) * dk);
         const int8_t *ci = codes_in + (size_t)t * nel;
         const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
         const uint8_t *bt = bits + (size_t)t * dk;
@@ -176,7 +192,7 @@ void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const 
                 Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / qb;
         }
         update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
-                    alpha[t], beta[t], X, o + (size_t)t * dv);
+                    gate_of(alpha, per_row, t, dk, gbuf), beta[t], X, o + (size_t)t * dv);
         for (int i = 0; i < dk; ++i) {
             double qb = qb_of(bt[i]);
             for (int j = 0; j < dv; ++j) {
@@ -190,6 +206,7 @@ void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const 
         }
         free(Sh);
         free(X);
+        free(gbuf);
     }
 }
 

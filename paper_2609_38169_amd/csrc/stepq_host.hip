@@ -251,15 +251,15 @@ void stepq_pool_destroy(stepq_pool *p)
 
 void *stepq_pool_device_ptr(const stepq_pool *p) { return p ? p->mem : nullptr; }
 
-stepq_status stepq_decode_step(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q, const void *k,
-                               const void *v, const void *alpha, const void *beta, stepq_dtype act_dtype, float *o,
-                               void *stream)
+static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q,
+                                     const void *k, const void *v, const void *gate, const void *beta,
+                                     stepq_dtype act_dtype, float *o, void *stream, bool diag)
 {
     stepq_status st = common_checks(p, slot_ids, batch);
     if (st != STEPQ_OK) return st;
     if (act_dtype != STEPQ_F32 && act_dtype != STEPQ_BF16) return fail(STEPQ_E_INVALID, "unknown activation dtype");
     if (batch == 0) return STEPQ_OK;
-    if (!q || !k || !v || !alpha || !beta || !o) return fail(STEPQ_E_INVALID, "NULL activation or output pointer");
+    if (!q || !k || !v || !gate || !beta || !o) return fail(STEPQ_E_INVALID, "NULL activation or output pointer");
     auto s = static_cast<hipStream_t>(stream);
     st = check_slots(p, slot_ids, batch, s);
     if (st != STEPQ_OK) return st;
@@ -269,12 +269,26 @@ stepq_status stepq_decode_step(stepq_pool *p, const int32_t *slot_ids, int32_t b
     a.q = q;
     a.k = k;
     a.v = v;
-    a.alpha = alpha;
+    a.alpha = gate;
     a.beta = beta;
     a.o = o;
     a.batch = batch;
-    hipError_t e = stepq::launch_decode(a, act_dtype == STEPQ_BF16, p->layout, s);
+    hipError_t e = stepq::launch_decode(a, act_dtype == STEPQ_BF16, diag, p->layout, s);
     return e == hipSuccess ? STEPQ_OK : hip_fail(e, "decode launch");
+}
+
+stepq_status stepq_decode_step(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q, const void *k,
+                               const void *v, const void *alpha, const void *beta, stepq_dtype act_dtype, float *o,
+                               void *stream)
+{
+    return decode_step_impl(p, slot_ids, batch, q, k, v, alpha, beta, act_dtype, o, stream, false);
+}
+
+stepq_status stepq_decode_step_kda(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q,
+                                   const void *k, const void *v, const void *gate, const void *beta,
+                                   stepq_dtype act_dtype, float *o, void *stream)
+{
+    return decode_step_impl(p, slot_ids, batch, q, k, v, gate, beta, act_dtype, o, stream, true);
 }
 
 static stepq_status tile_op(const stepq_pool *p, const int32_t *ids, int32_t n, stepq::TileArgs &a,

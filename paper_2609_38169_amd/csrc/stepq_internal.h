@@ -82,7 +82,9 @@ struct TileArgs {
 };
 
 // pool_layout: the uniform layout shared by every head (1-based), or 0.
-hipError_t launch_decode(const DecodeArgs &a, bool bf16, int pool_layout, hipStream_t stream);
+// diag: a.alpha holds the channel-wise gate [batch][Hv][d_k] instead of the
+// scalar gate [batch][Hv].
+hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);
 hipError_t launch_tile_op(const TileArgs &a, TileOp op, hipStream_t stream);
 
 }  // namespace stepq

@@ -115,6 +115,8 @@ struct DecodeShared {
     float av[kSlotTable];                // beta k_i q_b / r_i
     float sk[kMaxDk], sq[kMaxDk];        // k, q of the tile in logical row order
     float sr[kMaxDk];                    // r in physical row order
+    float sd[kMaxDk];                    // channel-wise gate d in logical row order (diagonal gate only)
+    float al[kSlotTable];                // d_i 2^(b-8) per row-table slot (diagonal gate only)
     int sperm[kMaxDk];                   // logical row of each physical row
     float4 red[2][256 / (DV / 4)][DV / 4];
     float bcol[DV];                      // delta_j / c_j
@@ -134,17 +136,19 @@ struct TileCtx {
 // row p = tid; c_j, v_j for column j = tid.
 struct RowColOps {
     float k, q, r, c, v;
+    float d;                    // channel-wise gate of logical row tid (diagonal gate only)
     int perm;
 };
 
-template <bool BF16, int DV>
+template <bool BF16, bool DIAG, int DV>
 __device__ __forceinline__ RowColOps load_ops(const DecodeArgs &a, int tile, int b, int hq, int h, const float *rr,
                                               const float *cc)
 {
     const PoolView &P = a.pool;
     const int tid = threadIdx.x;
-    RowColOps op{0.f, 0.f, 0.f, 0.f, 0.f, 0};
+    RowColOps op{0.f, 0.f, 0.f, 0.f, 0.f, 1.f, 0};
     if (tid < P.dk) {
+        if constexpr (DIAG) op.d = act_ld<BF16>(a.alpha, static_cast<size_t>(tile) * P.dk + tid);
         const size_t off = (static_cast<size_t>(b) * P.Hqk + hq) * P.dk + tid;
         op.k = act_ld<BF16>(a.k, off);
         op.q = act_ld<BF16>(a.q, off);
@@ -161,7 +165,7 @@ __device__ __forceinline__ RowColOps load_ops(const DecodeArgs &a, int tile, int
 // Row constants into LDS, indexed by row-table slot, and q.k.  Two barriers;
 // returns q.k.  Rows are read through the physical -> logical permutation
 // from the LDS copy of k and q.
-template <int DV>
+template <bool DIAG, int DV>
 __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float beta, const RowColOps &op,
                                                DecodeShared<DV> &sh)
 {
@@ -171,6 +175,7 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
         sh.sq[tid] = op.q;
         sh.sr[tid] = op.r;
         sh.sperm[tid] = op.perm;
+        if constexpr (DIAG) sh.sd[tid] = op.d;
     }
     __syncthreads();
     float kq = 0.f;
@@ -188,7 +193,7 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
             const int kk = x - hi.n8 - 2 * hi.g4;
             if (kk < hi.n2) p = hi.n8 + hi.n4 + kk;
         }
-        float kt = 0.f, qt = 0.f, av = 0.f;
+        float kt = 0.f, qt = 0.f, av = 0.f, al = 0.f;
         if (p >= 0) {
             // slot x holds physical row p, whose r and permutation entry were
             // loaded by thread p
@@ -199,14 +204,17 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
             const float qb = bw == 8 ? 127.0f : (bw == 4 ? 7.0f : 1.0f);
             // 2^(b-8) / q_b: 1/127, 1/112, 1/64 (an unpacked field reads 2^(8-b) q)
             const float fq = bw == 8 ? (1.0f / 127.0f) : (bw == 4 ? (1.0f / 112.0f) : (1.0f / 64.0f));
-            const float rs = rp * fq;
+            const float di = DIAG ? sh.sd[i] : 1.0f;       // the gate folds into both row weights
+            const float rs = rp * fq * di;
             kt = ki * rs;
             qt = qi * rs;
             av = beta * ki * qb * __builtin_amdgcn_rcpf(rp);
+            al = di * (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
             kq = qi * ki;
         }
         sh.kq[x] = make_float2(kt, qt);
         sh.av[x] = av;
+        if constexpr (DIAG) sh.al[x] = al;
     }
     kq = wave_sum(kq);
     if ((tid & 63) == 0) sh.kap[tid >> 6] = kq;
@@ -215,7 +223,7 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
 }
 
 // Uniform layouts: table slot = physical row = tid, widths known at compile time.
-template <int M8, int M4, int DV>
+template <bool DIAG, int M8, int M4, int DV>
 __device__ __forceinline__ float row_constants_uniform(float beta, const RowColOps &op, DecodeShared<DV> &sh)
 {
     constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
@@ -223,6 +231,7 @@ __device__ __forceinline__ float row_constants_uniform(float beta, const RowColO
     if (tid < 128) {
         sh.sk[tid] = op.k;
         sh.sq[tid] = op.q;
+        if constexpr (DIAG) sh.sd[tid] = op.d;
     }
     __syncthreads();
     float kq = 0.f;
@@ -232,9 +241,11 @@ __device__ __forceinline__ float row_constants_uniform(float beta, const RowColO
         const float fq = p < X4 ? (1.0f / 127.0f) : (p < X2 ? (1.0f / 112.0f) : (1.0f / 64.0f));
         const float ki = sh.sk[op.perm];
         const float qi = sh.sq[op.perm];
-        const float rs = op.r * fq;
+        const float di = DIAG ? sh.sd[op.perm] : 1.0f;
+        const float rs = op.r * fq * di;
         sh.kq[p] = make_float2(ki * rs, qi * rs);
         sh.av[p] = beta * ki * qb * __builtin_amdgcn_rcpf(op.r);
+        if constexpr (DIAG) sh.al[p] = di * (p < X4 ? 1.0f : (p < X2 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
         kq = qi * ki;
     }
     kq = wave_sum(kq);
@@ -370,15 +381,17 @@ __device__ __forceinline__ uint32_t requant_field(const uint32_t *U2, int s, flo
     return __builtin_amdgcn_cvt_pk_u8_f32(y, E, P);
 }
 
-template <int B>
-__device__ __forceinline__ uint32_t requant_word_h(const uint32_t *U2, const float *av, int x0, float al,
-                                                   const float (&bc)[4])
+// al: the per-width gate factor (scalar gate) or, with a table alt, per row.
+template <int B, bool DIAG>
+__device__ __forceinline__ uint32_t requant_word_h(const uint32_t *U2, const float *av, const float *alt, int x0,
+                                                   float al_w, const float (&bc)[4])
 {
     constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
     uint32_t out = 0;
 #pragma unroll
     for (int s = 0; s < 8 / B; ++s) {
         const float a_s = av[x0 + s];
+        const float al = DIAG ? alt[x0 + s] : al_w;
         uint32_t P = 0;
         P = requant_field<B, 0>(U2, s, al, a_s, bc[0], P);
         P = requant_field<B, 1>(U2, s, al, a_s, bc[1], P);
@@ -394,9 +407,9 @@ __device__ __forceinline__ uint32_t requant_word_h(const uint32_t *U2, const flo
 // clamped to [1, 2^B - 1] (i.e. code in [-q_b, q_b]), rounded to nearest
 // even and packed to a byte by v_cvt_pk_u8_f32, then the bias is removed
 // from all fields at once by flipping each field's top bit.
-template <int B>
-__device__ __forceinline__ uint32_t requant_word(const float *U, const float *av, int x0, float al,
-                                                 const float (&bc)[4])
+template <int B, bool DIAG>
+__device__ __forceinline__ uint32_t requant_word(const float *U, const float *av, const float *alt, int x0,
+                                                 float al_w, const float (&bc)[4])
 {
     constexpr float bias = static_cast<float>(1 << (B - 1));
     constexpr float top = static_cast<float>((1 << B) - 1);
@@ -405,6 +418,7 @@ __device__ __forceinline__ uint32_t requant_word(const float *U, const float *av
 #pragma unroll
     for (int s = 0; s < 8 / B; ++s) {
         const float a_s = av[x0 + s];
+        const float al = DIAG ? alt[x0 + s] : al_w;
         uint32_t P = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -419,7 +433,7 @@ __device__ __forceinline__ uint32_t requant_word(const float *U, const float *av
 }
 
 // Rows of one width per word-step; codes stay in registers between passes.
-template <bool BF16, int M8, int M4, int M2>
+template <bool BF16, bool DIAG, int M8, int M4, int M2>
 __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCtx &t, DecodeShared<128> &sh)
 {
     constexpr int M = M8 + M4 + M2;
@@ -431,8 +445,8 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
 #pragma unroll
     for (int m = 0; m < M; ++m) w[m] = __builtin_nontemporal_load(t.codes + tid + 256 * m);
 
-    const RowColOps op = load_ops<BF16, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    const float kappa = row_constants_uniform<M8, M4, 128>(t.beta, op, sh);
+    const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
+    const float kappa = row_constants_uniform<DIAG, M8, M4, 128>(t.beta, op, sh);
 
     uint32_t U[NE / 2];
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
@@ -445,29 +459,29 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
     for (int m = 0; m < M2; ++m)
         unpack_acc_h<2>(w[M8 + M4 + m], sh.kq, X2 + 4 * (slice + 8 * m), &U[2 * M8 + 4 * M4 + 8 * m], acK, acQ);
 
-    column_phase<128>(a, t.tile, t.alpha, t.beta, sh, kappa, acK, acQ, op.c, op.v);
+    column_phase<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, acK, acQ, op.c, op.v);
 
     const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
     for (int m = 0; m < M8; ++m)
-        __builtin_nontemporal_store(requant_word_h<8>(&U[2 * m], sh.av, slice + 8 * m, t.alpha, bc),
+        __builtin_nontemporal_store(requant_word_h<8, DIAG>(&U[2 * m], sh.av, sh.al, slice + 8 * m, t.alpha, bc),
                                     t.codes + tid + 256 * m);
 #pragma unroll
     for (int m = 0; m < M4; ++m)
-        __builtin_nontemporal_store(requant_word_h<4>(&U[2 * M8 + 4 * m], sh.av, X4 + 2 * (slice + 8 * m),
+        __builtin_nontemporal_store(requant_word_h<4, DIAG>(&U[2 * M8 + 4 * m], sh.av, sh.al, X4 + 2 * (slice + 8 * m),
                                                     t.alpha * (1.0f / 16.0f), bc),
                                     t.codes + tid + 256 * (M8 + m));
 #pragma unroll
     for (int m = 0; m < M2; ++m)
-        __builtin_nontemporal_store(requant_word_h<2>(&U[2 * M8 + 4 * M4 + 8 * m], sh.av, X2 + 4 * (slice + 8 * m),
+        __builtin_nontemporal_store(requant_word_h<2, DIAG>(&U[2 * M8 + 4 * M4 + 8 * m], sh.av, sh.al, X2 + 4 * (slice + 8 * m),
                                                     t.alpha * (1.0f / 64.0f), bc),
                                     t.codes + tid + 256 * (M8 + M4 + m));
 }
 
 // Any row-width mix and d_v: the class of each word-step is looked up at run
 // time and the words are unpacked again for the second pass.
-template <bool BF16, int DV>
+template <bool BF16, bool DIAG, int DV>
 __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCtx &t, DecodeShared<DV> &sh)
 {
     constexpr int CG = DV / 4;
@@ -482,8 +496,8 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
         const int g = slice + NSL * m;
         w[m] = g < ngroups ? __builtin_nontemporal_load(t.codes + tid + 256 * m) : 0u;
     }
-    const RowColOps op = load_ops<BF16, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    const float kappa = row_constants<DV>(t.hi, a.pool.dk, t.beta, op, sh);
+    const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
+    const float kappa = row_constants<DIAG, DV>(t.hi, a.pool.dk, t.beta, op, sh);
 
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
     float U[16];
@@ -497,7 +511,7 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
             else unpack_acc<2>(w[m], sh.kq, gr.x0, U, acK, acQ);
         }
     }
-    column_phase<DV>(a, t.tile, t.alpha, t.beta, sh, kappa, acK, acQ, op.c, op.v);
+    column_phase<DV>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, acK, acQ, op.c, op.v);
 
     const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
@@ -509,13 +523,13 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
             uint32_t nw;
             if (gr.bits == 8) {
                 unpack_word<8>(w[m], U);
-                nw = requant_word<8>(U, sh.av, gr.x0, t.alpha, bc);
+                nw = requant_word<8, DIAG>(U, sh.av, sh.al, gr.x0, t.alpha, bc);
             } else if (gr.bits == 4) {
                 unpack_word<4>(w[m], U);
-                nw = requant_word<4>(U, sh.av, gr.x0, t.alpha * (1.0f / 16.0f), bc);
+                nw = requant_word<4, DIAG>(U, sh.av, sh.al, gr.x0, t.alpha * (1.0f / 16.0f), bc);
             } else {
                 unpack_word<2>(w[m], U);
-                nw = requant_word<2>(U, sh.av, gr.x0, t.alpha * (1.0f / 64.0f), bc);
+                nw = requant_word<2, DIAG>(U, sh.av, sh.al, gr.x0, t.alpha * (1.0f / 64.0f), bc);
             }
             __builtin_nontemporal_store(nw, t.codes + tid + 256 * m);
         }
@@ -527,7 +541,7 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
 // LAYOUT == 0: heads may differ; each workgroup branches on its head's
 // layout (uniformly, so without divergence); d_v = 64 and irregular
 // row-width mixes take the generic body.
-template <int DV, bool BF16, int LAYOUT>
+template <int DV, bool BF16, int LAYOUT, bool DIAG>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 {
     __shared__ DecodeShared<DV> sh;
@@ -538,7 +552,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
     t.h = t.tile - t.b * P.Hv;
     t.hq = fdiv(t.h, P.div_g);
     const int slot = a.slot_ids[t.b];
-    t.alpha = act_ld<BF16>(a.alpha, t.tile);
+    t.alpha = DIAG ? 1.0f : act_ld<BF16>(a.alpha, t.tile);
     t.beta = act_ld<BF16>(a.beta, t.tile);
     if constexpr (DV == 128 && LAYOUT > 0) {
         // every tile record is (codes: 1024 bytes per word-step) + r + c
@@ -549,7 +563,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
         t.codes = reinterpret_cast<uint32_t *>(rec);
         t.rr = reinterpret_cast<const float *>(rec + r_off);
         t.cc = t.rr + 128;
-        decode_uniform<BF16, u.m8, u.m4, u.m2>(a, t, sh);
+        decode_uniform<BF16, DIAG, u.m8, u.m4, u.m2>(a, t, sh);
     } else {
         t.hi = P.heads[t.h];
         uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.hi.tile_off;
@@ -558,15 +572,15 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
         t.cc = t.rr + P.dk;
         if constexpr (DV == 128) {
             switch (t.hi.layout) {
-            case 1: decode_uniform<BF16, 8, 4, 0>(a, t, sh); return;
-            case 2: decode_uniform<BF16, 4, 2, 2>(a, t, sh); return;
-            case 3: decode_uniform<BF16, 16, 0, 0>(a, t, sh); return;
-            case 4: decode_uniform<BF16, 0, 8, 0>(a, t, sh); return;
-            case 5: decode_uniform<BF16, 0, 0, 4>(a, t, sh); return;
+            case 1: decode_uniform<BF16, DIAG, 8, 4, 0>(a, t, sh); return;
+            case 2: decode_uniform<BF16, DIAG, 4, 2, 2>(a, t, sh); return;
+            case 3: decode_uniform<BF16, DIAG, 16, 0, 0>(a, t, sh); return;
+            case 4: decode_uniform<BF16, DIAG, 0, 8, 0>(a, t, sh); return;
+            case 5: decode_uniform<BF16, DIAG, 0, 0, 4>(a, t, sh); return;
             default: break;
             }
         }
-        decode_generic<BF16, DV>(a, t, sh);
+        decode_generic<BF16, DIAG, DV>(a, t, sh);
     }
 }
 
@@ -653,32 +667,38 @@ __global__ __launch_bounds__(256) void tile_kernel(TileArgs a)
     }
 }
 
-template <bool BF16>
+template <bool BF16, bool DIAG>
 hipError_t launch_decode_128(const DecodeArgs &a, int layout, unsigned grid, hipStream_t s)
 {
     switch (layout) {
-    case 1: hipLaunchKernelGGL((decode_kernel<128, BF16, 1>), dim3(grid), dim3(256), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((decode_kernel<128, BF16, 2>), dim3(grid), dim3(256), 0, s, a); break;
-    case 3: hipLaunchKernelGGL((decode_kernel<128, BF16, 3>), dim3(grid), dim3(256), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((decode_kernel<128, BF16, 4>), dim3(grid), dim3(256), 0, s, a); break;
-    case 5: hipLaunchKernelGGL((decode_kernel<128, BF16, 5>), dim3(grid), dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL((decode_kernel<128, BF16, 0>), dim3(grid), dim3(256), 0, s, a); break;
+    case 1: hipLaunchKernelGGL((decode_kernel<128, BF16, 1, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((decode_kernel<128, BF16, 2, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
+    case 3: hipLaunchKernelGGL((decode_kernel<128, BF16, 3, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((decode_kernel<128, BF16, 4, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
+    case 5: hipLaunchKernelGGL((decode_kernel<128, BF16, 5, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL((decode_kernel<128, BF16, 0, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
     }
+    return hipGetLastError();
+}
+
+template <bool BF16, bool DIAG>
+hipError_t launch_decode_any(const DecodeArgs &a, int layout, unsigned grid, hipStream_t s)
+{
+    if (a.pool.dv == 128) return launch_decode_128<BF16, DIAG>(a, layout, grid, s);
+    hipLaunchKernelGGL((decode_kernel<64, BF16, 0, DIAG>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_decode(const DecodeArgs &a, bool bf16, int pool_layout, hipStream_t stream)
+hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream)
 {
     const unsigned grid = static_cast<unsigned>(a.batch) * static_cast<unsigned>(a.pool.Hv);
     if (grid == 0) return hipSuccess;
-    if (a.pool.dv == 128)
-        return bf16 ? launch_decode_128<true>(a, pool_layout, grid, stream)
-                    : launch_decode_128<false>(a, pool_layout, grid, stream);
-    if (bf16) hipLaunchKernelGGL((decode_kernel<64, true, 0>), dim3(grid), dim3(256), 0, stream, a);
-    else hipLaunchKernelGGL((decode_kernel<64, false, 0>), dim3(grid), dim3(256), 0, stream, a);
-    return hipGetLastError();
+    if (bf16) return diag ? launch_decode_any<true, true>(a, pool_layout, grid, stream)
+                          : launch_decode_any<true, false>(a, pool_layout, grid, stream);
+    return diag ? launch_decode_any<false, true>(a, pool_layout, grid, stream)
+                : launch_decode_any<false, false>(a, pool_layout, grid, stream);
 }
 
 hipError_t launch_tile_op(const TileArgs &a, TileOp op, hipStream_t stream)

@@ -24,7 +24,7 @@ _STATUS = {0: "STEPQ_OK", 1: "STEPQ_E_INVALID", 2: "STEPQ_E_UNSUPPORTED", 3: "ST
 
 EXPORTED = (
     "stepq_pool_bytes", "stepq_pool_create", "stepq_pool_destroy", "stepq_pool_device_ptr",
-    "stepq_pool_load", "stepq_decode_step", "stepq_pool_dequant", "stepq_pool_export",
+    "stepq_pool_load", "stepq_decode_step", "stepq_decode_step_kda", "stepq_pool_dequant", "stepq_pool_export",
     "stepq_pool_import", "stepq_last_error", "stepq_setup_fit", "stepq_setup_lifetime_bits",
 )
 
@@ -59,6 +59,7 @@ def lib():
             "stepq_pool_device_ptr": ([P], P),
             "stepq_pool_load": ([P, P, i32, P, P, P, P], st),
             "stepq_decode_step": ([P, P, i32, P, P, P, P, P, st, P, P], st),
+            "stepq_decode_step_kda": ([P, P, i32, P, P, P, P, P, st, P, P], st),
             "stepq_pool_dequant": ([P, P, i32, P, P], st),
             "stepq_pool_export": ([P, P, i32, P, P, P, P], st),
             "stepq_pool_import": ([P, P, i32, P, P, P, P], st),
@@ -155,24 +156,30 @@ class Pool:
     def step(self, slot_ids, q, k, v, alpha, beta, o, stream=None):
         stepq_decode_step(self, slot_ids, q, k, v, alpha, beta, o, stream)
 
+    def step_kda(self, slot_ids, q, k, v, gate, beta, o, stream=None):
+        stepq_decode_step_kda(self, slot_ids, q, k, v, gate, beta, o, stream)
+
     def prepare_step(self, slot_ids, q, k, v, alpha, beta, o, stream=None):
         """Validate the arguments of one decode step once and return a
         callable that launches it with the cached pointers (for decode loops
-        where the per-call checks would dominate the launch cost)."""
+        where the per-call checks would dominate the launch cost).  alpha of
+        shape [B][Hv][d_k] selects the channel-wise (KDA) gate."""
         n, ids = _ids(self, slot_ids)
         dt = q.dtype
         if dt not in (torch.float32, torch.bfloat16):
             raise TypeError("activations must be float32 or bfloat16")
         code = STEPQ_F32 if dt == torch.float32 else STEPQ_BF16
+        kda = alpha.dim() == 3
+        gshape = (n, self.Hv, self.dk) if kda else (n, self.Hv)
         args = (self.handle, ids, n,
                 _dev(q, "q", dt, (n, self.Hqk, self.dk), self.device),
                 _dev(k, "k", dt, (n, self.Hqk, self.dk), self.device),
                 _dev(v, "v", dt, (n, self.Hv, self.dv), self.device),
-                _dev(alpha, "alpha", dt, (n, self.Hv), self.device),
+                _dev(alpha, "alpha", dt, gshape, self.device),
                 _dev(beta, "beta", dt, (n, self.Hv), self.device), code,
                 _dev(o, "o", torch.float32, (n, self.Hv, self.dv), self.device), _stream(stream))
         keep = (slot_ids, q, k, v, alpha, beta, o)      # the tensors must outlive the callable
-        fn = lib().stepq_decode_step
+        fn = lib().stepq_decode_step_kda if kda else lib().stepq_decode_step
 
         def launch():
             _ = keep
@@ -233,6 +240,23 @@ def stepq_decode_step(pool: Pool, slot_ids, q, k, v, alpha, beta, o, stream=None
         _dev(k, "k", dt, (n, P.Hqk, P.dk), P.device),
         _dev(v, "v", dt, (n, P.Hv, P.dv), P.device),
         _dev(alpha, "alpha", dt, (n, P.Hv), P.device),
+        _dev(beta, "beta", dt, (n, P.Hv), P.device), code,
+        _dev(o, "o", torch.float32, (n, P.Hv, P.dv), P.device), _stream(stream)))
+
+
+def stepq_decode_step_kda(pool: Pool, slot_ids, q, k, v, gate, beta, o, stream=None):
+    n, ids = _ids(pool, slot_ids)
+    P = pool
+    dt = q.dtype
+    if dt not in (torch.float32, torch.bfloat16):
+        raise TypeError("activations must be float32 or bfloat16")
+    code = STEPQ_F32 if dt == torch.float32 else STEPQ_BF16
+    _check(lib().stepq_decode_step_kda(
+        pool.handle, ids, n,
+        _dev(q, "q", dt, (n, P.Hqk, P.dk), P.device),
+        _dev(k, "k", dt, (n, P.Hqk, P.dk), P.device),
+        _dev(v, "v", dt, (n, P.Hv, P.dv), P.device),
+        _dev(gate, "gate", dt, (n, P.Hv, P.dk), P.device),
         _dev(beta, "beta", dt, (n, P.Hv), P.device), code,
         _dev(o, "o", torch.float32, (n, P.Hv, P.dv), P.device), _stream(stream)))
 

@@ -95,7 +95,7 @@ def _mix(*parts: int) -> int:
 
 
 _STREAM = {"init": 1, "q": 2, "k": 3, "v": 4, "alpha": 5, "beta": 6,
-           "bits": 7, "calib": 8, "slots": 9, "gain_r": 10, "gain_c": 11}
+           "bits": 7, "calib": 8, "slots": 9, "gain_r": 10, "gain_c": 11, "kda": 12}
 
 
 def _gen(device, w: Workload, layer: int, step: int, stream: str, chunk: int = 0) -> torch.Generator:
@@ -171,6 +171,14 @@ def step_inputs(w: Workload, layer: int, step: int, device="cpu") -> dict:
     beta = torch.sigmoid(torch.randn((B, Hv), generator=_gen(device, w, layer, step, "beta"),
                                      device=device, dtype=torch.float64)).to(dt)
     return {"q": q, "k": k, "v": v, "alpha": alpha, "beta": beta}
+
+
+def kda_gates(w: Workload, layer: int, step: int, device="cpu") -> torch.Tensor:
+    """Channel-wise retention gates d_{t,i} for the KDA form of the update,
+    [B][Hv][d_k] in the activation dtype: one draw per key row from the
+    workload's gate law, on a stream of its own."""
+    g = _gen(device, w, layer, step, "kda")
+    return _gates(w, g, (w.batch, w.n_v_heads, w.d_k), device).to(w.act_dtype)
 
 
 def calibration_gates(w: Workload, layer: int = 0) -> torch.Tensor:

@@ -48,7 +48,9 @@ def oracle_inputs(w: W.Workload, inp: dict, rows: np.ndarray):
     a = inp["alpha"].index_select(0, rows_t).double().cpu().numpy()
     b = inp["beta"].index_select(0, rows_t).double().cpu().numpy()
     n = len(rows) * w.n_v_heads
-    return (q.reshape(n, w.d_k), k.reshape(n, w.d_k), v.reshape(n, w.d_v), a.reshape(n), b.reshape(n))
+    # alpha [B][Hv] (GDN) or channel-wise gates [B][Hv][d_k] (KDA)
+    return (q.reshape(n, w.d_k), k.reshape(n, w.d_k), v.reshape(n, w.d_v), a.reshape((n,) + a.shape[2:]),
+            b.reshape(n))
 
 
 def compare_codes(gpu: np.ndarray, orc: np.ndarray, y: np.ndarray, what: str = "codes"):

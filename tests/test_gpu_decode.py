@@ -87,7 +87,7 @@ def test_pool_load_matches_oracle_quantizer(idx):
     PT.compare_codes(codes.cpu().numpy().reshape(oc.shape), oc, y, "pool_load codes")
 
 
-def _lockstep_run(w, steps, check_rows, layer=0, mutate=None):
+def _lockstep_run(w, steps, check_rows, layer=0, mutate=None, kda=False):
     bits = row_bits(w, layer)
     _say(f"lockstep {w.name}: building pool ({w.n_slots} slots)")
     pool = build_pool(w, layer, device=DEV, bits=bits)
@@ -98,13 +98,18 @@ def _lockstep_run(w, steps, check_rows, layer=0, mutate=None):
     o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=DEV)
     for t in range(steps):
         inp = W.step_inputs(w, layer, t, device=DEV)
+        if kda:
+            inp["alpha"] = W.kda_gates(w, layer, t, device=DEV)
         if mutate:
             inp = mutate(inp)
         ls.anchor()
-        pool.step(slots, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o)
+        if kda:
+            pool.step_kda(slots, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o)
+        else:
+            pool.step(slots, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o)
         torch.cuda.synchronize()
         ls.check_step(inp, o, t)
-    _say(f"lockstep {w.name}: {steps} steps ok, tie mismatches {ls.mismatches}, saturated {ls.saturated:.3f}")
+    _say(f"lockstep {w.name}{' kda' if kda else ''}: {steps} steps ok, tie mismatches {ls.mismatches}, saturated {ls.saturated:.3f}")
     return ls
 
 
@@ -296,5 +301,132 @@ def test_prepared_step_matches_checked_call():
     pa.step(ids, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], oa)
     run = pb.prepare_step(ids, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], ob)
     run()
+    torch.cuda.synchronize()
+    assert torch.equal(oa, ob) and torch.equal(pa.memory, pb.memory)
+
+
+# --- KDA: channel-wise retention gate D = diag(d) -----------------------------
+
+def test_kda_tiny_all_steps():
+    w = W.workload(0)
+    _lockstep_run(w, w.steps, np.arange(w.batch), kda=True)
+
+
+def test_kda_layer_b64_64_steps():
+    w = W.workload(1)
+    _lockstep_run(w, 64, np.arange(w.batch), kda=True)
+
+
+@pytest.mark.parametrize("idx", [2, 3])
+def test_kda_pool_sized_sampled(idx):
+    w = W.workload(idx)
+    rows = np.array([0, 3, 100, 255, 256, 384, 509, 511])
+    _lockstep_run(w, 12, rows, kda=True)
+
+
+def test_kda_identity_gate_keeps_codes():
+    """d = 1 on every row and beta = 0: X = S^, codes come back unchanged."""
+    w = W.workload(1)
+    bits = row_bits(w)
+    pool = build_pool(w, device=DEV, bits=bits)
+    ids = W.active_slots(w).to(DEV)
+    before = pool.memory.clone()
+    inp = W.step_inputs(w, 0, 0, device=DEV)
+    o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=DEV)
+    gate = torch.ones((w.batch, w.n_v_heads, w.d_k), dtype=inp["alpha"].dtype, device=DEV)
+    pool.step_kda(ids, inp["q"], inp["k"], inp["v"], gate, torch.zeros_like(inp["beta"]), o)
+    torch.cuda.synchronize()
+    assert torch.equal(before, pool.memory)
+
+
+def test_kda_uniform_gate_matches_gdn_call():
+    """d_i = alpha for every row: the KDA call and the GDN call compute the
+    same update (they fold the gate at different points, so codes may differ
+    only at rounding ties and o within the output tolerance)."""
+    w = W.workload(2)
+    bits = row_bits(w)
+    pa = build_pool(w, device=DEV, bits=bits)
+    pb = stepq.Pool(w.n_slots, w.n_v_heads, w.n_qk_heads, w.d_k, w.d_v, bits, device=DEV)
+    pb.memory.copy_(pa.memory)
+    ids = W.active_slots(w).to(DEV)
+    inp = W.step_inputs(w, 0, 0, device=DEV)
+    oa = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=DEV)
+    ob = torch.empty_like(oa)
+    pa.step(ids, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], oa)
+    gate = inp["alpha"][:, :, None].expand(-1, -1, w.d_k).contiguous()
+    pb.step_kda(ids, inp["q"], inp["k"], inp["v"], gate, inp["beta"], ob)
+    shape = (w.batch, w.n_v_heads, w.d_k, w.d_v)
+    ca, cb = torch.empty(shape, dtype=torch.int8, device=DEV), torch.empty(shape, dtype=torch.int8, device=DEV)
+    r = torch.empty((w.batch, w.n_v_heads, w.d_k), device=DEV)
+    c = torch.empty((w.batch, w.n_v_heads, w.d_v), device=DEV)
+    pa.export(ids, ca, r, c)
+    pb.export(ids, cb, r, c)
+    torch.cuda.synchronize()
+    d = (ca.to(torch.int16) - cb.to(torch.int16)).abs()
+    assert int(d.max()) <= 1 and int((d != 0).sum()) <= PT.CODE_MISMATCH_FRAC * d.numel()
+    PT.compare_out(ob.cpu().numpy(), oa.double().cpu().numpy(), "kda vs gdn o")
+
+
+@pytest.mark.parametrize("case", range(5))
+def test_kda_ragged_shapes(case):
+    """The generic (non-uniform layout) kernels with channel-wise gates."""
+    Hv, Hqk, dk, dv, n_slots, bits = _ragged_cases()[case]
+    _say(f"ragged kda case {case}: Hv={Hv} Hqk={Hqk} dk={dk} dv={dv}")
+    rng = np.random.default_rng(200 + case)
+    S = (rng.standard_normal((n_slots, Hv, dk, dv)) * 0.05).astype(np.float32)
+    r, c = oracle.fit_absmax(S.reshape(-1, dk, dv))
+    tb_all = np.broadcast_to(bits[None], (n_slots,) + bits.shape).reshape(-1, dk)
+    codes = oracle.quantize(S.reshape(-1, dk, dv).astype(np.float64), r, c, tb_all)
+    pool = stepq.Pool(n_slots, Hv, Hqk, dk, dv, bits, device=DEV)
+    all_ids = torch.arange(n_slots, dtype=torch.int32, device=DEV)
+    pool.import_(all_ids, torch.from_numpy(codes.reshape(n_slots, Hv, dk, dv)).to(DEV),
+                 torch.from_numpy(r.reshape(n_slots, Hv, dk)).to(DEV),
+                 torch.from_numpy(c.reshape(n_slots, Hv, dv)).to(DEV))
+    B = max(1, n_slots - 1)
+    sel = rng.permutation(n_slots)[:B].astype(np.int32)
+    ids = torch.from_numpy(sel).to(DEV)
+    q = rng.standard_normal((B, Hqk, dk)); q /= np.linalg.norm(q, axis=-1, keepdims=True)
+    k = rng.standard_normal((B, Hqk, dk)); k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    v = rng.standard_normal((B, Hv, dv))
+    dg = rng.uniform(0.5, 1.0, (B, Hv, dk)); be = rng.uniform(0, 1, (B, Hv))
+    t32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+    o = torch.empty((B, Hv, dv), dtype=torch.float32, device=DEV)
+    pool.step_kda(ids, t32(q), t32(k), t32(v), t32(dg), t32(be), o)
+    out = torch.empty((n_slots, Hv, dk, dv), dtype=torch.int8, device=DEV)
+    pool.export(all_ids, out, torch.empty((n_slots, Hv, dk), device=DEV), torch.empty((n_slots, Hv, dv), device=DEV))
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    hq = np.arange(Hv) // (Hv // Hqk)
+    f32 = lambda a: a.astype(np.float32).astype(np.float64)
+    qq, kk = f32(q)[:, hq].reshape(-1, dk), f32(k)[:, hq].reshape(-1, dk)
+    tiles = (sel[:, None] * Hv + np.arange(Hv)[None]).reshape(-1)
+    new, o_ref, y = oracle.decode_step(codes[tiles], r[tiles], c[tiles], tb_all[tiles], qq, kk,
+                                       f32(v).reshape(-1, dv), f32(dg).reshape(-1, dk), f32(be).reshape(-1),
+                                       want_y=True)
+    PT.compare_codes(got.reshape(-1, dk, dv)[tiles], new, y, f"ragged kda case {case}")
+    PT.compare_out(o.cpu().numpy().reshape(-1, dv), o_ref)
+    untouched = np.setdiff1d(np.arange(n_slots), sel)
+    for s in untouched:
+        assert np.array_equal(got[s], codes.reshape(n_slots, Hv, dk, dv)[s])
+
+
+def test_kda_argument_errors_and_prepared_call():
+    w = W.workload(0)
+    pool = stepq.Pool(2, w.n_v_heads, w.n_qk_heads, w.d_k, w.d_v, row_bits(w), device=DEV)
+    z = lambda *s, dt=torch.float32: torch.zeros(s, dtype=dt, device=DEV)
+    ids = torch.tensor([0, 1], dtype=torch.int32, device=DEV)
+    with pytest.raises(ValueError):          # a per-head gate is not a channel-wise gate
+        pool.step_kda(ids, z(2, 4, 64), z(2, 4, 64), z(2, 4, 64), z(2, 4), z(2, 4), z(2, 4, 64))
+    pool.step_kda(ids[:0], z(0, 4, 64), z(0, 4, 64), z(0, 4, 64), z(0, 4, 64), z(0, 4), z(0, 4, 64))
+    bits = row_bits(w)
+    pa = build_pool(w, device=DEV, bits=bits)
+    pb = build_pool(w, device=DEV, bits=bits)
+    ids = W.active_slots(w).to(DEV)
+    inp = W.step_inputs(w, 0, 0, device=DEV)
+    gate = W.kda_gates(w, 0, 0, device=DEV)
+    oa = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=DEV)
+    ob = torch.empty_like(oa)
+    pa.step_kda(ids, inp["q"], inp["k"], inp["v"], gate, inp["beta"], oa)
+    pb.prepare_step(ids, inp["q"], inp["k"], inp["v"], gate, inp["beta"], ob)()
     torch.cuda.synchronize()
     assert torch.equal(oa, ob) and torch.equal(pa.memory, pb.memory)

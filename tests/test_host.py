@@ -120,6 +120,12 @@ def test_workload_draws_are_seeded():
     assert sorted(torch.cat(W.rotation_slots(W.workload(2))).tolist()) == list(range(2048))
     bits = W.bit_map_draw(W.workload(3)).numpy()
     assert all(sorted(np.bincount(row, minlength=9)[[2, 4, 8]]) == [32, 32, 64] for row in bits)
+    for idx in range(5):                     # channel-wise gates: shape, dtype, range, seeded, own stream
+        wk = W.workload(idx)
+        d = W.kda_gates(wk, 0, 1)
+        assert d.shape == (wk.batch, wk.n_v_heads, wk.d_k) and d.dtype == wk.act_dtype
+        assert torch.equal(d, W.kda_gates(wk, 0, 1)) and not torch.equal(d, W.kda_gates(wk, 0, 2))
+        assert float(d.min()) > 0.0 and float(d.max()) <= 1.0
 
 
 def test_library_device_code_is_gfx950():

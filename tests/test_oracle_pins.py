@@ -401,3 +401,65 @@ def test_serving_capacity_model():
     Wb = g["qwen_weights_bf16_bytes"]["value"]
     first = next(B for B in range(1, 1000) if (5 * B + 1) * S32 > Wb)
     assert first == g["fp32_pool_exceeds_bf16_weights_at_b"]["value"]
+
+
+# ---------------------------------------------------------------- KDA channel-wise gate (Eq. 1, D = diag(d))
+def _kda_case(seed=20, n=3, dk=12, dv=9):
+    rng = np.random.default_rng(seed)
+    S = rng.standard_normal((n, dk, dv)) * 0.3
+    q, k = _unit(rng, n, dk), _unit(rng, n, dk)
+    v = rng.standard_normal((n, dv))
+    d = rng.uniform(0.3, 1.0, (n, dk))
+    beta = rng.uniform(0.0, 1.0, n)
+    return rng, S, q, k, v, d, beta
+
+
+def test_kda_update_matches_affine_form():
+    """Eq. 2 with D = diag(d): S_t = (I - beta k k^T) D S + beta k v^T."""
+    _, S, q, k, v, d, beta = _kda_case()
+    X, o = oracle.update_fp(S, q, k, v, d, beta)
+    for t in range(S.shape[0]):
+        A = (np.eye(S.shape[1]) - beta[t] * np.outer(k[t], k[t])) @ np.diag(d[t])
+        Xr = A @ S[t] + beta[t] * np.outer(k[t], v[t])
+        np.testing.assert_allclose(X[t], Xr, rtol=0, atol=1e-13)
+        np.testing.assert_allclose(o[t], Xr.T @ q[t], rtol=0, atol=1e-13)
+        assert np.linalg.norm(A, 2) <= np.max(d[t]) + 1e-12      # Proposition 1: ||A|| <= ||D|| <= 1
+
+
+def test_kda_uniform_gate_is_gdn():
+    """d_i = alpha for every row reproduces the scalar-gate path exactly."""
+    _, S, q, k, v, d, beta = _kda_case(21)
+    alpha = d[:, 0].copy()
+    X1, o1 = oracle.update_fp(S, q, k, v, alpha, beta)
+    X2, o2 = oracle.update_fp(S, q, k, v, np.repeat(alpha[:, None], S.shape[1], 1), beta)
+    assert np.array_equal(X1, X2) and np.array_equal(o1, o2)
+
+
+def test_kda_row_readout_sensitivity():
+    """Eq. kda_sensitivity: g_i = d_i (q_i - beta k_i (k^T q)); a unit-norm
+    error confined to key row i is read with squared norm g_i^2."""
+    rng = np.random.default_rng(22)
+    dk, dv = 10, 5
+    q, k = _unit(rng, 1, dk)[0], _unit(rng, 1, dk)[0]
+    d = rng.uniform(0.2, 1.0, dk)
+    beta = 0.7
+    g = d * (q - beta * k * (k @ q))
+    for i in range(dk):
+        E = np.zeros((1, dk, dv))
+        row = rng.standard_normal(dv)
+        E[0, i] = row / np.linalg.norm(row)
+        _, o = oracle.update_fp(E, q[None], k[None], np.zeros((1, dv)), d[None], [beta])
+        assert np.sum(o ** 2) == pytest.approx(g[i] ** 2, rel=1e-12, abs=1e-15)
+
+
+def test_kda_decode_step_composition():
+    rng, S, q, k, v, d, beta = _kda_case(23)
+    bits = rng.choice([2, 4, 8], size=S.shape[:2]).astype(np.uint8)
+    r, c = oracle.fit_absmax(S.astype(np.float32))
+    codes = oracle.quantize(S, r, c, bits)
+    new, o = oracle.decode_step(codes, r, c, bits, q, k, v, d, beta)
+    X, o_ref = oracle.update_fp(oracle.dequant(codes, r, c, bits), q, k, v, d, beta)
+    np.testing.assert_allclose(o, o_ref, rtol=0, atol=1e-14)
+    assert np.array_equal(new, oracle.quantize(X, r, c, bits))
+    same, _ = oracle.decode_step(codes, r, c, bits, q, k, v, np.ones_like(d), np.zeros_like(beta))
+    assert np.array_equal(same, codes)
