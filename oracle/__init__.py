@@ -52,6 +52,7 @@ def lib():
         L.orc_dequant.argtypes = [i, i, i, P, P, P, P, P]
         L.orc_update_fp.argtypes = [i, i, i, P, P, P, P, P, i, P, P, P]
         L.orc_decode_step.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P]
+        L.orc_decode_step_refit.argtypes = [i, i, i, P, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P]
         L.orc_tile_bytes.argtypes = [i, i, P]
         L.orc_tile_bytes.restype = ctypes.c_size_t
         L.orc_slot_bytes.argtypes = [i, i, i, P]
@@ -147,6 +148,29 @@ def decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=False):
     lib().orc_decode_step(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(q), _p(k), _p(v),
                           _p(a), per_row, _p(beta), _p(out), _p(o), _p(y))
     return (out, o, y) if want_y else (out, o)
+
+
+def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=()):
+    """One quantized decode step with the online dual-axis refit (Table C2
+    steps 1-6, Section 4.3, Appendix C.1).  Returns (codes, r, c, o) with the
+    new fp32 scales, plus a dict of the requested extras among "y", "y0", "X".
+    w: row-impact factors [n][dk] (None: 1)."""
+    codes = _c(codes, np.int8)
+    n, dk, dv = codes.shape
+    r, c, bits = _c(r, np.float32), _c(c, np.float32), _c(np.broadcast_to(bits, (n, dk)), np.uint8)
+    q, k, v = _c(q, np.float64), _c(k, np.float64), _c(v, np.float64)
+    a, per_row = _gates(alpha, n, dk)
+    beta = _c(beta, np.float64).reshape(n)
+    wt = None if w is None else _c(np.broadcast_to(w, (n, dk)), np.float64)
+    out = np.empty_like(codes)
+    r_out = np.empty((n, dk), np.float32)
+    c_out = np.empty((n, dv), np.float32)
+    o = np.empty((n, dv), np.float64)
+    extra = {key: np.empty((n, dk, dv), np.float64) for key in want}
+    lib().orc_decode_step_refit(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(wt), _p(q), _p(k), _p(v),
+                                _p(a), per_row, _p(beta), _p(out), _p(r_out), _p(c_out), _p(o),
+                                _p(extra.get("y")), _p(extra.get("y0")), _p(extra.get("X")))
+    return (out, r_out, c_out, o, extra) if want else (out, r_out, c_out, o)
 
 
 def tile_bytes(bits_row, d_v: int) -> int:

@@ -211,6 +211,117 @@ void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const 
 }
 
 /* ------------------------------------------------------------------------
+ * One decode step with the online Key-Row-Aware Dual-Axis refit (Appendix
+ * C, Table C2 steps 1-6; Section 4.3 "Row factors" and "Column factors";
+ * the fixed-code column update of Appendix C.1).  Steps 1-3 are those of
+ * orc_decode_step (X and o).  Then, per tile, with row-impact factors w
+ * (w == NULL: w_i = 1):
+ *   row factors   m_i = (1/d_v) sum_j |X_ij|,  r'_i = (m_i / w_i)^{1/2}
+ *   column start  c0_j = max_i |X_ij| / r'_i          (absmax: no fixed code clips)
+ *   fixed codes   z_ij = clip(round(X_ij q_b / (r'_i c0_j)), -q_b, q_b) / q_b
+ *   column fit    c'_j = sum_i w_i^2 v_ij X_ij / sum_i w_i^2 v_ij^2,  v_ij = r'_i z_ij
+ *                 (minimiser of sum_i w_i^2 (X_ij - r'_i c z_ij)^2 over c)
+ *                 a zero denominator keeps the previous scale c_j
+ *   requantize    q'_ij = clip(round(X_ij q_b / (r'_i c'_j)), -q_b, q_b)
+ * r', c0 and c' are floored at 2^-60.  r' and c' are the stored scales:
+ * each is rounded to fp32 when it is formed, and what follows it uses the
+ * rounded value.
+ * Optional outputs: y (X q_b / (r' c') before rounding), y0 (X q_b / (r' c0)
+ * before rounding), X.
+ */
+void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, const float *r,
+                           const float *c, const uint8_t *bits, const double *w, const double *q,
+                           const double *k, const double *v, const double *alpha, int per_row,
+                           const double *beta, int8_t *codes_out, float *r_out, float *c_out, double *o,
+                           double *y, double *y0, double *X_out)
+{
+    const double floor_ = ldexp(1.0, -60);
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int t = 0; t < n_tiles; ++t) {
+        size_t nel = (size_t)dk * dv;
+        double *Sh = (double *)malloc(sizeof(double) * nel);
+        double *X = (double *)malloc(sizeof(double) * nel);
+        double *gbuf = (double *)malloc(sizeof(double) * dk);
+        double *rn = (double *)malloc(sizeof(double) * dk);
+        double *zt = (double *)malloc(sizeof(double) * nel);
+        const int8_t *ci = codes_in + (size_t)t * nel;
+        const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
+        const uint8_t *bt = bits + (size_t)t * dk;
+        for (int i = 0; i < dk; ++i) {
+            double qb = qb_of(bt[i]);
+            for (int j = 0; j < dv; ++j)
+                Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / qb;
+        }
+        update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
+                    gate_of(alpha, per_row, t, dk, gbuf), beta[t], X, o + (size_t)t * dv);
+        if (X_out) memcpy(X_out + (size_t)t * nel, X, sizeof(double) * nel);
+
+        /* row factors */
+        for (int i = 0; i < dk; ++i) {
+            double m = 0.0;
+            for (int j = 0; j < dv; ++j) m += fabs(X[(size_t)i * dv + j]);
+            m /= (double)dv;
+            double wi = w ? w[(size_t)t * dk + i] : 1.0;
+            double ri = sqrt(m / wi);
+            if (ri < floor_) ri = floor_;
+            r_out[(size_t)t * dk + i] = (float)ri;
+            rn[i] = (double)r_out[(size_t)t * dk + i];
+        }
+        for (int j = 0; j < dv; ++j) {
+            /* absmax start of the column factor, then the fixed codes */
+            double c0 = 0.0;
+            for (int i = 0; i < dk; ++i) {
+                double a = fabs(X[(size_t)i * dv + j]) / rn[i];
+                if (a > c0) c0 = a;
+            }
+            if (c0 < floor_) c0 = floor_;
+            for (int i = 0; i < dk; ++i) {
+                double qb = qb_of(bt[i]);
+                double s = X[(size_t)i * dv + j] * qb / (rn[i] * c0);
+                if (y0) y0[(size_t)t * nel + (size_t)i * dv + j] = s;
+                double n = nearbyint(s);
+                if (n > qb) n = qb;
+                if (n < -qb) n = -qb;
+                zt[(size_t)i * dv + j] = n / qb;
+            }
+            /* weighted least squares in c with the codes held fixed */
+            double num = 0.0, den = 0.0;
+            for (int i = 0; i < dk; ++i) {
+                double wi = w ? w[(size_t)t * dk + i] : 1.0;
+                double vij = rn[i] * zt[(size_t)i * dv + j];
+                num += wi * wi * vij * X[(size_t)i * dv + j];
+                den += wi * wi * vij * vij;
+            }
+            double cj;
+            if (den > 0.0) {
+                cj = num / den;
+                if (cj < floor_) cj = floor_;
+            } else {
+                cj = (double)ct[j];
+            }
+            c_out[(size_t)t * dv + j] = (float)cj;
+        }
+        /* requantize against the stored scales */
+        for (int i = 0; i < dk; ++i) {
+            double qb = qb_of(bt[i]);
+            for (int j = 0; j < dv; ++j) {
+                double s = X[(size_t)i * dv + j] * qb / (rn[i] * (double)c_out[(size_t)t * dv + j]);
+                if (y) y[(size_t)t * nel + (size_t)i * dv + j] = s;
+                double n = nearbyint(s);
+                if (n > qb) n = qb;
+                if (n < -qb) n = -qb;
+                codes_out[(size_t)t * nel + (size_t)i * dv + j] = (int8_t)n;
+            }
+        }
+        free(Sh);
+        free(X);
+        free(gbuf);
+        free(rn);
+        free(zt);
+    }
+}
+
+/* ------------------------------------------------------------------------
  * Pool layout, re-derived from its definition in include/stepq.h:
  *  - physical key-row order: the 8-bit rows in increasing logical index,
  *    then the 4-bit rows, then the 2-bit rows;

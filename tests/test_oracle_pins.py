@@ -463,3 +463,104 @@ def test_kda_decode_step_composition():
     assert np.array_equal(new, oracle.quantize(X, r, c, bits))
     same, _ = oracle.decode_step(codes, r, c, bits, q, k, v, np.ones_like(d), np.zeros_like(beta))
     assert np.array_equal(same, codes)
+
+
+# ---------------------------------------------------------------- online dual-axis refit (Section 4.3, App. C)
+def _refit_case(seed=30, n=4, dk=24, dv=10, kda=False):
+    rng = np.random.default_rng(seed)
+    bits = rng.choice([2, 4, 8], size=(n, dk)).astype(np.uint8)
+    S = rng.standard_normal((n, dk, dv)) * np.exp(rng.standard_normal((n, dk, 1))) * 0.2
+    r, c = oracle.fit_absmax(S.astype(np.float32))
+    codes = oracle.quantize(S, r, c, bits)
+    q, k = _unit(rng, n, dk), _unit(rng, n, dk)
+    v = rng.standard_normal((n, dv))
+    gate = rng.uniform(0.5, 1.0, (n, dk)) if kda else rng.uniform(0.5, 1.0, n)
+    beta = rng.uniform(0.0, 1.0, n)
+    w = np.exp(0.5 * rng.standard_normal((n, dk)))        # non-uniform row-impact factors
+    return codes, r, c, bits, q, k, v, gate, beta, w
+
+
+@pytest.mark.parametrize("kda", [False, True])
+def test_refit_row_factors_closed_form(kda):
+    """r'_i = (m_i / w_i)^{1/2} with m_i the mean |X_ij| of the updated state
+    (Section 4.3), stored in fp32: r'^2 w = m up to that rounding."""
+    codes, r, c, bits, q, k, v, g, beta, w = _refit_case(kda=kda)
+    _, rn, _, _, ex = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w, want=("X",))
+    m = np.abs(ex["X"]).mean(axis=2)
+    np.testing.assert_allclose(rn.astype(np.float64) ** 2 * w, m, rtol=2.5e-7, atol=0)
+
+
+@pytest.mark.parametrize("kda", [False, True])
+def test_refit_column_fit_is_weighted_least_squares(kda):
+    """With the fixed codes z (the rounded y0 / q_b), c'_j solves
+    min_c sum_i w_i^2 (X_ij - r'_i c z_ij)^2: checked against a library
+    least-squares solve of the weighted system, and against nearby c."""
+    codes, r, c, bits, q, k, v, g, beta, w = _refit_case(seed=31, kda=kda)
+    _, rn, cn, _, ex = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w, want=("X", "y0"))
+    qb = (2.0 ** (bits.astype(np.int64) - 1) - 1)[:, :, None]
+    z = np.clip(np.rint(ex["y0"]), -qb, qb) / qb
+    X = ex["X"]
+    n, dk, dv = X.shape
+    for t in range(n):
+        for j in range(dv):
+            A = (w[t] * rn[t].astype(np.float64) * z[t, :, j])[:, None]
+            bvec = w[t] * X[t, :, j]
+            if not np.any(A):
+                assert cn[t, j] == c[t, j]            # zero denominator: the previous scale stays
+                continue
+            sol = np.linalg.lstsq(A, bvec, rcond=None)[0][0]
+            assert abs(float(cn[t, j]) - sol) <= 1e-7 * abs(sol)
+            obj = lambda cc: float(np.sum((bvec - A[:, 0] * cc) ** 2))
+            assert obj(sol) <= min(obj(sol * (1 + 1e-3)), obj(sol * (1 - 1e-3)))
+
+
+def test_refit_fixed_codes_start_from_column_absmax():
+    """The fixed codes come from the absmax column start: in every non-zero
+    column the largest |y0_ij| / q_b is exactly 1, so no fixed code clips."""
+    codes, r, c, bits, q, k, v, g, beta, w = _refit_case(seed=32)
+    *_, ex = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w, want=("y0",))
+    qb = (2.0 ** (bits.astype(np.int64) - 1) - 1)[:, :, None]
+    ratio = np.abs(ex["y0"]) / qb
+    np.testing.assert_allclose(ratio.max(axis=1), 1.0, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("kda", [False, True])
+def test_refit_scale_invariance(kda):
+    """Scaling the state and v by 4 scales X by 4: r' and c' double exactly
+    (power-of-two scaling commutes with every rounding), the codes are
+    unchanged and o scales by 4.  Scaling w by 4 halves r', doubles c' and
+    keeps the codes."""
+    codes, r, c, bits, q, k, v, g, beta, w = _refit_case(seed=33, kda=kda)
+    base = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w)
+    up = oracle.decode_step_refit(codes, 2 * r, 2 * c, bits, q, k, 4 * v, g, beta, w=w)
+    assert np.array_equal(up[0], base[0])
+    assert np.array_equal(up[1], 2 * base[1]) and np.array_equal(up[2], 2 * base[2])
+    assert np.array_equal(up[3], 4 * base[3])
+    ww = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=4 * w)
+    assert np.array_equal(ww[0], base[0])
+    assert np.array_equal(ww[1], base[1] / 2) and np.array_equal(ww[2], 2 * base[2])
+
+
+def test_refit_zero_row_and_zero_column():
+    """A row with k_i = 0 and zero codes stays zero: r' falls to the 2^-60
+    floor.  A column with zero codes and v_j = 0 stays zero: its denominator
+    is zero and the previous scale is kept (Appendix C.1)."""
+    codes, r, c, bits, q, k, v, g, beta, w = _refit_case(seed=34)
+    codes[:, 3, :] = 0
+    k[:, 3] = 0.0
+    codes[:, :, 5] = 0
+    v[:, 5] = 0.0
+    out, rn, cn, _ = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w)
+    assert np.all(rn[:, 3] == np.float32(2.0 ** -60)) and np.all(out[:, 3, :] == 0)
+    assert np.array_equal(cn[:, 5], c[:, 5]) and np.all(out[:, :, 5] == 0)
+
+
+def test_refit_requantizes_with_the_new_scales():
+    """Final codes are the quantizer (Eq. 3, pinned above) applied to X with
+    the refitted scales; the readout is taken before, so it equals the
+    frozen-scale step's readout (Table C2, step 3 precedes steps 4-6)."""
+    codes, r, c, bits, q, k, v, g, beta, w = _refit_case(seed=35)
+    out, rn, cn, o, ex = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w, want=("X",))
+    assert np.array_equal(out, oracle.quantize(ex["X"], rn, cn, bits))
+    _, o_frozen = oracle.decode_step(codes, r, c, bits, q, k, v, g, beta)
+    assert np.array_equal(o, o_frozen)
