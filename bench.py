@@ -31,7 +31,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 METRIC = "state-updates/s and achieved HBM GB/s (% of peak), B=512 heads=32 dk=dv=128"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode_pool_b512.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_38169_amd", "csrc", "stepq_kernels.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_38169_amd", "csrc", f)
+               for f in ("stepq_device.h", "stepq_internal.h", "stepq_kernels.hip")]
 
 
 def log(msg: str):
@@ -39,16 +40,20 @@ def log(msg: str):
 
 
 def kernel_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in KERNEL_SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
-def state_bytes_per_tile(bits_row, d_k, d_v) -> int:
+def state_bytes_per_tile(bits_row, d_k, d_v, refit: bool = False) -> int:
     """Algorithmic bytes one tile update moves: its codes read and written
-    once, its fp32 row and column scales read once."""
+    once, its fp32 row and column scales read once (and written once more
+    when the step refits them)."""
     import numpy as np
     n8 = int(np.sum(bits_row == 8)); n4 = int(np.sum(bits_row == 4)); n2 = int(np.sum(bits_row == 2))
     code_bytes = (8 * n8 + 4 * n4 + 2 * n2) * d_v // 8
-    return 2 * code_bytes + 4 * (d_k + d_v)
+    return 2 * code_bytes + (2 if refit else 1) * 4 * (d_k + d_v)
 
 
 def cpu_baseline(w, bits, seconds: float):
@@ -110,6 +115,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-ref", action="store_true", help="also time a plain device copy of the same bytes")
     ap.add_argument("--kda", action="store_true", help="channel-wise (KDA) gates [B][Hv][d_k] instead of alpha")
+    ap.add_argument("--refit", action="store_true", help="online dual-axis refit of the scales in every step")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -148,7 +154,8 @@ def main():
         if key not in prepared:
             inp = inputs[key[0]]
             prepared[key] = pool.prepare_step(subsets[key[1]], inp["q"], inp["k"], inp["v"], inp["alpha"],
-                                              inp["beta"], o, stream=torch.cuda.current_stream())
+                                              inp["beta"], o, stream=torch.cuda.current_stream(),
+                                              refit=args.refit)
         prepared[key]()
 
     log(f"pool and inputs ready in {time.perf_counter() - t_setup:.1f} s; timing")
@@ -185,7 +192,7 @@ def main():
                   for j in range(nsub)]
 
     tiles = w.tiles_per_step
-    per_tile = [state_bytes_per_tile(bits[h], w.d_k, w.d_v) for h in range(w.n_v_heads)]
+    per_tile = [state_bytes_per_tile(bits[h], w.d_k, w.d_v, args.refit) for h in range(w.n_v_heads)]
     launch_bytes = w.batch * sum(per_tile)
     gate_elems = w.n_v_heads * (w.d_k if args.kda else 1)
     act_bytes = w.batch * (2 * w.n_qk_heads * w.d_k * 2 + w.n_v_heads * w.d_v * 2 + (gate_elems + w.n_v_heads) * 2
@@ -210,7 +217,8 @@ def main():
                                f"d_k=d_v={w.d_k}, 6-bit mixed {{4,8}}, fp32 scales, bf16 activations",
                    "slot_rotation": 1 if args.resident else len(subsets),
                    "cache_resident": bool(args.resident),
-                   "gate": "channel-wise d [B][Hv][d_k] (KDA)" if args.kda else "scalar alpha [B][Hv] (GDN)"},
+                   "gate": "channel-wise d [B][Hv][d_k] (KDA)" if args.kda else "scalar alpha [B][Hv] (GDN)",
+                   "scales": "online dual-axis refit every step" if args.refit else "frozen"},
         "GBps_state": launch_bytes * K / (total_ms * 1e-3) / 1e9,
         "pct_hbm_peak": 100.0 * launch_bytes * K / (total_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "roofline": {
@@ -219,8 +227,9 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": None if args.kda else traffic_entry(launch_bytes),
-            "kernel": "decode_kernel<128, bf16, kda>" if args.kda else "decode_kernel<128, bf16>",
+            "traffic": None if (args.kda or args.refit) else traffic_entry(launch_bytes),
+            "kernel": ("refit_kernel" if args.refit else "decode_kernel") + ("<128, bf16, kda>" if args.kda
+                                                                              else "<128, bf16>"),
             "kernel_ms_mean": kern_ms,
             "launch_ms_event_pairs": {"mean": float(np.mean(per_launch_ms)), "min": float(np.min(per_launch_ms)),
                                       "max": float(np.max(per_launch_ms)), "per_slot_subset": per_subset},

@@ -144,6 +144,41 @@ stepq_status stepq_decode_step_kda(stepq_pool *pool, const int32_t *slot_ids, in
                                    const void *k, const void *v, const void *gate, const void *beta,
                                    stepq_dtype act_dtype, float *o, void *stream);
 
+/* Flags of stepq_decode_step_ex. */
+enum {
+    STEPQ_STEP_KDA_GATE = 1u,  /* gate is the channel-wise d [batch][Hv][d_k] (KDA), else alpha [batch][Hv] */
+    STEPQ_STEP_REFIT = 2u      /* refit both scale vectors to the updated state before requantizing */
+};
+
+/* The decode step with optional channel-wise gate and online scale refit.
+ * Without STEPQ_STEP_REFIT it is stepq_decode_step (or _kda with
+ * STEPQ_STEP_KDA_GATE).  With STEPQ_STEP_REFIT the stored scales of every
+ * updated tile are replaced by the Key-Row-Aware Dual-Axis fit of X (paper,
+ * Section 4.3, Appendix C.1 and Table C2 steps 4-6), w being the pool's
+ * row-impact factors (stepq_pool_set_row_weight, default 1), as the
+ * fixed-code column update of Appendix C.1 prescribes:
+ *   r'_i = (m_i / w_i)^{1/2},  m_i = (1/d_v) sum_j |X_ij|
+ *   c0_j = max_i |X_ij| / r'_i                     (start of the column fit)
+ *   z_ij = clip(round(X_ij q_b / (r'_i c0_j)), -q_b, q_b) / q_b   (fixed codes)
+ *   c'_j = c_j sum_i W_i z_ij y_ij / sum_i W_i z_ij^2,  W_i = (w_i r'_i / q_b)^2,
+ *          y_ij = X_ij q_b / (r'_i c_j)
+ *        = the minimiser over c of sum_i w_i^2 (X_ij - r'_i c z_ij)^2;
+ *          a zero denominator keeps c_j
+ *   q'_ij = clip(round(X_ij q_b / (r'_i c'_j)), -q_b, q_b)
+ * r', c0 and c' are floored at 2^-60; r' and c' are written as the new fp32
+ * scales.  The readout o is X^T q as without the flag.  Unknown flags:
+ * STEPQ_E_INVALID. */
+stepq_status stepq_decode_step_ex(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
+                                  const void *k, const void *v, const void *gate, const void *beta,
+                                  stepq_dtype act_dtype, uint32_t flags, float *o, void *stream);
+
+/* Row-impact factors w of every head (Section 4.3 and its footnote's
+ * normalisation; calibrated as in Appendices A.3 and C.1), used by
+ * STEPQ_STEP_REFIT.  row_weight: host [Hv][d_k] in logical row order, each
+ * finite and > 0; copied.  Synchronises the pool's device first, so no
+ * decode step is in flight while the table changes.  A new pool has w = 1. */
+stepq_status stepq_pool_set_row_weight(stepq_pool *pool, const float *row_weight);
+
 /* Reconstruct S^_ij = r_i c_j q_ij / q_{b_i} (Section 4.3) for n slots into
  * out [n][Hv][d_k][d_v] fp32, logical row order.  Computed in fp32. */
 stepq_status stepq_pool_dequant(const stepq_pool *pool, const int32_t *slot_ids, int32_t n, float *out,

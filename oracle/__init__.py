@@ -52,7 +52,8 @@ def lib():
         L.orc_dequant.argtypes = [i, i, i, P, P, P, P, P]
         L.orc_update_fp.argtypes = [i, i, i, P, P, P, P, P, i, P, P, P]
         L.orc_decode_step.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P]
-        L.orc_decode_step_refit.argtypes = [i, i, i, P, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P]
+        L.orc_decode_step_refit.argtypes = [i, i, i, P, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P,
+                                            ctypes.c_double, P, P]
         L.orc_tile_bytes.argtypes = [i, i, P]
         L.orc_tile_bytes.restype = ctypes.c_size_t
         L.orc_slot_bytes.argtypes = [i, i, i, P]
@@ -150,10 +151,12 @@ def decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=False):
     return (out, o, y) if want_y else (out, o)
 
 
-def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=()):
+def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=(), tie_window=2e-3):
     """One quantized decode step with the online dual-axis refit (Table C2
     steps 1-6, Section 4.3, Appendix C.1).  Returns (codes, r, c, o) with the
-    new fp32 scales, plus a dict of the requested extras among "y", "y0", "X".
+    new fp32 scales, plus a dict of the requested extras among "y", "y0", "X"
+    and "c_range" (the (lo, hi) column-factor bounds over the other roundings
+    of fixed codes within tie_window of a rounding boundary).
     w: row-impact factors [n][dk] (None: 1)."""
     codes = _c(codes, np.int8)
     n, dk, dv = codes.shape
@@ -166,10 +169,18 @@ def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=()):
     r_out = np.empty((n, dk), np.float32)
     c_out = np.empty((n, dv), np.float32)
     o = np.empty((n, dv), np.float64)
-    extra = {key: np.empty((n, dk, dv), np.float64) for key in want}
+    extra = {key: np.empty((n, dk, dv), np.float64) for key in want if key != "c_range"}
+    lo = hi = None
+    if "c_range" in want:
+        lo, hi = np.empty((n, dv), np.float64), np.empty((n, dv), np.float64)
+        if "y0" not in extra:
+            extra["y0"] = np.empty((n, dk, dv), np.float64)
     lib().orc_decode_step_refit(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(wt), _p(q), _p(k), _p(v),
                                 _p(a), per_row, _p(beta), _p(out), _p(r_out), _p(c_out), _p(o),
-                                _p(extra.get("y")), _p(extra.get("y0")), _p(extra.get("X")))
+                                _p(extra.get("y")), _p(extra.get("y0")), _p(extra.get("X")), float(tie_window),
+                                _p(lo), _p(hi))
+    if lo is not None:
+        extra["c_range"] = (lo, hi)
     return (out, r_out, c_out, o, extra) if want else (out, r_out, c_out, o)
 
 

@@ -228,12 +228,22 @@ void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const 
  * rounded value.
  * Optional outputs: y (X q_b / (r' c') before rounding), y0 (X q_b / (r' c0)
  * before rounding), X.
+ *
+ * c_lo, c_hi (optional, for comparing with lower-precision implementations):
+ * bounds on the column factor over every other rounding of the fixed codes
+ * whose y0 lies within tie_window of a rounding boundary (a rounding that
+ * arithmetic of lower precision may legitimately take).  Each such code
+ * moves the two sums by a known amount; the bounds combine the extremes,
+ * num_lo / den_hi and num_hi / den_lo, so they enclose every combination.
+ * When a combination can empty the denominator the previous scale is in the
+ * range and c_hi is +inf.
  */
 void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, const float *r,
                            const float *c, const uint8_t *bits, const double *w, const double *q,
                            const double *k, const double *v, const double *alpha, int per_row,
                            const double *beta, int8_t *codes_out, float *r_out, float *c_out, double *o,
-                           double *y, double *y0, double *X_out)
+                           double *y, double *y0, double *X_out, double tie_window, double *c_lo,
+                           double *c_hi)
 {
     const double floor_ = ldexp(1.0, -60);
     #pragma omp parallel for schedule(dynamic, 4)
@@ -300,6 +310,42 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
                 cj = (double)ct[j];
             }
             c_out[(size_t)t * dv + j] = (float)cj;
+            if (c_lo && c_hi) {
+                double nlo = num, nhi = num, dlo = den, dhi = den;
+                for (int i = 0; i < dk; ++i) {
+                    double qb = qb_of(bt[i]);
+                    double s = y0[(size_t)t * nel + (size_t)i * dv + j];
+                    double a = fabs(s);
+                    if (fabs(a - floor(a) - 0.5) > tie_window) continue;
+                    double z = zt[(size_t)i * dv + j] * qb;
+                    double alt = (z > s) ? z - 1.0 : z + 1.0;     /* the other neighbour of s */
+                    if (alt > qb || alt < -qb) continue;
+                    double wi = w ? w[(size_t)t * dk + i] : 1.0;
+                    double v0 = rn[i] * z / qb, v1 = rn[i] * alt / qb;
+                    double dn = wi * wi * (v1 - v0) * X[(size_t)i * dv + j];
+                    double dd = wi * wi * (v1 * v1 - v0 * v0);
+                    if (dn < 0) nlo += dn; else nhi += dn;
+                    if (dd < 0) dlo += dd; else dhi += dd;
+                }
+                double lo, hi;
+                if (dlo > 0.0) {
+                    lo = nlo / dhi;
+                    hi = nhi / dlo;
+                    if (lo < floor_) lo = floor_;
+                    if (hi < floor_) hi = floor_;
+                    if (den <= 0.0) {          /* this column kept its scale */
+                        if ((double)ct[j] < lo) lo = (double)ct[j];
+                        if ((double)ct[j] > hi) hi = (double)ct[j];
+                    }
+                } else {
+                    lo = (dhi > 0.0) ? nlo / dhi : (double)ct[j];
+                    if (lo < floor_) lo = floor_;
+                    if ((double)ct[j] < lo) lo = (double)ct[j];
+                    hi = INFINITY;
+                }
+                c_lo[(size_t)t * dv + j] = lo;
+                c_hi[(size_t)t * dv + j] = hi;
+            }
         }
         /* requantize against the stored scales */
         for (int i = 0; i < dk; ++i) {

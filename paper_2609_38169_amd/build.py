@@ -13,13 +13,14 @@ import os
 import re
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libstepq.so")
-HIP_SOURCES = ["stepq_host.hip", "stepq_kernels.hip"]
+HIP_SOURCES = ["stepq_host.hip", "stepq_kernels.hip", "stepq_refit.hip"]
 CXX_SOURCES = ["stepq_setup.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -56,14 +57,19 @@ def build(extra_flags: list[str] | None = None, out: str = LIB, verbose: bool = 
             raise subprocess.CalledProcessError(r.returncode, cmd)
 
     inc = ["-I", os.path.join(ROOT, "include"), "-I", csrc]
+    cmds = []
     for s in HIP_SOURCES:
         o = os.path.join(build_dir, s + ".o")
-        run([HIPCC] + HIP_FLAGS + (extra_flags or []) + inc + ["-c", os.path.join(csrc, s), "-o", o])
+        cmds.append([HIPCC] + HIP_FLAGS + (extra_flags or []) + inc + ["-c", os.path.join(csrc, s), "-o", o])
         objs.append(o)
     for s in CXX_SOURCES:
         o = os.path.join(build_dir, s + ".o")
-        run(["g++"] + CXX_FLAGS + inc + ["-c", os.path.join(csrc, s), "-o", o])
+        cmds.append(["g++"] + CXX_FLAGS + inc + ["-c", os.path.join(csrc, s), "-o", o])
         objs.append(o)
+    # the translation units are independent: compile them side by side
+    with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as ex:
+        for f in [ex.submit(run, c) for c in cmds]:
+            f.result()
     out = os.path.abspath(out)
     tmp = out + ".tmp"
     run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-pthread", "-o", tmp] + objs)

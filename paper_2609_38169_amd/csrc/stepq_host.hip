@@ -4,6 +4,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <cmath>
 #include <vector>
 
 #include "stepq.h"
@@ -21,6 +22,7 @@ struct stepq_pool {
     bool owns_mem = false;
     HeadInfo *d_heads = nullptr;
     uint8_t *d_perm = nullptr;
+    float *d_roww = nullptr;          // [Hv][dk] row-impact factors, physical order
     int device = 0;
     int layout = 0;                   // uniform layout of every head, or 0
 };
@@ -113,6 +115,7 @@ stepq::PoolView view(const stepq_pool *p)
     v.slot_bytes = p->slot_bytes;
     v.heads = p->d_heads;
     v.perm = p->d_perm;
+    v.roww = p->d_roww;
     v.n_slots = p->n_slots;
     v.Hv = p->Hv;
     v.Hqk = p->Hqk;
@@ -231,6 +234,11 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
     if (e == hipSuccess)
         e = hipMemcpy(p->d_heads, p->heads.data(), sizeof(HeadInfo) * p->heads.size(), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemcpy(p->d_perm, p->perm.data(), p->perm.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&p->d_roww), sizeof(float) * p->perm.size());
+    if (e == hipSuccess) {
+        const std::vector<float> ones(p->perm.size(), 1.0f);
+        e = hipMemcpy(p->d_roww, ones.data(), sizeof(float) * ones.size(), hipMemcpyHostToDevice);
+    }
     if (e != hipSuccess) {
         stepq_pool_destroy(p);
         return fail(STEPQ_E_NOMEM, std::string("layout tables: ") + hipGetErrorString(e));
@@ -246,18 +254,41 @@ void stepq_pool_destroy(stepq_pool *p)
     if (p->owns_mem && p->mem) (void)hipFree(p->mem);
     if (p->d_heads) (void)hipFree(p->d_heads);
     if (p->d_perm) (void)hipFree(p->d_perm);
+    if (p->d_roww) (void)hipFree(p->d_roww);
     delete p;
 }
 
 void *stepq_pool_device_ptr(const stepq_pool *p) { return p ? p->mem : nullptr; }
 
+stepq_status stepq_pool_set_row_weight(stepq_pool *p, const float *row_weight)
+{
+    if (!p || !row_weight) return fail(STEPQ_E_INVALID, "NULL pool or row_weight");
+    std::vector<float> phys(p->perm.size());
+    for (int h = 0; h < p->Hv; ++h)
+        for (int x = 0; x < p->dk; ++x) {
+            const size_t pi = static_cast<size_t>(h) * p->dk + x;
+            const float wv = row_weight[static_cast<size_t>(h) * p->dk + p->perm[pi]];
+            if (!(wv > 0.0f) || !std::isfinite(wv)) return fail(STEPQ_E_INVALID, "row weights must be finite and > 0");
+            phys[pi] = wv;
+        }
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e == hipSuccess && cur != p->device) e = hipSetDevice(p->device);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipMemcpy(p->d_roww, phys.data(), sizeof(float) * phys.size(), hipMemcpyHostToDevice);
+    if (cur != p->device) (void)hipSetDevice(cur);
+    return e == hipSuccess ? STEPQ_OK : hip_fail(e, "row weight upload");
+}
+
 static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q,
                                      const void *k, const void *v, const void *gate, const void *beta,
-                                     stepq_dtype act_dtype, float *o, void *stream, bool diag)
+                                     stepq_dtype act_dtype, float *o, void *stream, uint32_t flags)
 {
     stepq_status st = common_checks(p, slot_ids, batch);
     if (st != STEPQ_OK) return st;
     if (act_dtype != STEPQ_F32 && act_dtype != STEPQ_BF16) return fail(STEPQ_E_INVALID, "unknown activation dtype");
+    if (flags & ~static_cast<uint32_t>(STEPQ_STEP_KDA_GATE | STEPQ_STEP_REFIT))
+        return fail(STEPQ_E_INVALID, "unknown decode-step flags");
     if (batch == 0) return STEPQ_OK;
     if (!q || !k || !v || !gate || !beta || !o) return fail(STEPQ_E_INVALID, "NULL activation or output pointer");
     auto s = static_cast<hipStream_t>(stream);
@@ -273,22 +304,32 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     a.beta = beta;
     a.o = o;
     a.batch = batch;
-    hipError_t e = stepq::launch_decode(a, act_dtype == STEPQ_BF16, diag, p->layout, s);
+    const bool diag = (flags & STEPQ_STEP_KDA_GATE) != 0;
+    hipError_t e = (flags & STEPQ_STEP_REFIT)
+                       ? stepq::launch_decode_refit(a, act_dtype == STEPQ_BF16, diag, p->layout, s)
+                       : stepq::launch_decode(a, act_dtype == STEPQ_BF16, diag, p->layout, s);
     return e == hipSuccess ? STEPQ_OK : hip_fail(e, "decode launch");
+}
+
+stepq_status stepq_decode_step_ex(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q,
+                                  const void *k, const void *v, const void *gate, const void *beta,
+                                  stepq_dtype act_dtype, uint32_t flags, float *o, void *stream)
+{
+    return decode_step_impl(p, slot_ids, batch, q, k, v, gate, beta, act_dtype, o, stream, flags);
 }
 
 stepq_status stepq_decode_step(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q, const void *k,
                                const void *v, const void *alpha, const void *beta, stepq_dtype act_dtype, float *o,
                                void *stream)
 {
-    return decode_step_impl(p, slot_ids, batch, q, k, v, alpha, beta, act_dtype, o, stream, false);
+    return decode_step_impl(p, slot_ids, batch, q, k, v, alpha, beta, act_dtype, o, stream, 0u);
 }
 
 stepq_status stepq_decode_step_kda(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q,
                                    const void *k, const void *v, const void *gate, const void *beta,
                                    stepq_dtype act_dtype, float *o, void *stream)
 {
-    return decode_step_impl(p, slot_ids, batch, q, k, v, gate, beta, act_dtype, o, stream, true);
+    return decode_step_impl(p, slot_ids, batch, q, k, v, gate, beta, act_dtype, o, stream, STEPQ_STEP_KDA_GATE);
 }
 
 static stepq_status tile_op(const stepq_pool *p, const int32_t *ids, int32_t n, stepq::TileArgs &a,

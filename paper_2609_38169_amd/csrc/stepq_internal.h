@@ -53,6 +53,7 @@ struct PoolView {
     uint64_t slot_bytes;
     const HeadInfo *heads;   // [Hv], device
     const uint8_t *perm;     // [Hv][d_k] physical row -> logical row, device
+    const float *roww;       // [Hv][d_k] row-impact factors w in physical row order, device
     int32_t n_slots, Hv, Hqk, dk, dv;
     FastDiv div_hv;          // divide by Hv
     FastDiv div_g;           // divide by Hv / Hqk
@@ -85,6 +86,10 @@ struct TileArgs {
 // diag: a.alpha holds the channel-wise gate [batch][Hv][d_k] instead of the
 // scalar gate [batch][Hv].
 hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);
+// The decode step followed by the online dual-axis refit of both scale
+// vectors (the codes are requantized against the refitted scales, which
+// replace the stored ones).
+hipError_t launch_decode_refit(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);
 hipError_t launch_tile_op(const TileArgs &a, TileOp op, hipStream_t stream);
 
 }  // namespace stepq

@@ -23,414 +23,10 @@
 //
 // tile_kernel: pack (from fp32 states or raw codes), unpack and dequantize
 // whole tiles; not on the decode path.
-#include "stepq_internal.h"
+#include "stepq_device.h"
 
 namespace stepq {
 namespace {
-
-template <bool BF16>
-__device__ __forceinline__ float act_ld(const void *p, size_t i)
-{
-    if constexpr (BF16) {
-        const uint32_t u = static_cast<const uint16_t *>(p)[i];
-        return __uint_as_float(u << 16);
-    } else {
-        return static_cast<const float *>(p)[i];
-    }
-}
-
-// Workgroups are dispatched round-robin over the 8 XCDs.  Give each XCD a
-// contiguous run of tiles so that value heads sharing a q/k head, and
-// neighbouring slot records, are served from the same L2.
-__device__ __forceinline__ int xcd_tile(int wg, int n)
-{
-    if ((n & 7) != 0) return wg;
-    return (wg & 7) * (n >> 3) + (wg >> 3);
-}
-
-struct GroupRows {
-    int bits;   // width of the group's rows
-    int nslot;  // rows per group (8 / bits)
-    int p0;     // physical row of slot 0
-    int pend;   // one past the last physical row of this width
-    int x0;     // row-table index of slot 0
-};
-
-__device__ __forceinline__ GroupRows group_rows(const HeadInfo &hi, int g)
-{
-    if (g < hi.g8) return {8, 1, g, hi.n8, g};
-    if (g < hi.g8 + hi.g4) {
-        const int k = g - hi.g8;
-        return {4, 2, hi.n8 + 2 * k, hi.n8 + hi.n4, hi.n8 + 2 * k};
-    }
-    const int k = g - hi.g8 - hi.g4;
-    return {2, 4, hi.n8 + hi.n4 + 4 * k, hi.n8 + hi.n4 + hi.n2, hi.n8 + 2 * hi.g4 + 4 * k};
-}
-
-// The 4 fields of slot s of a word, each moved to the top of its byte
-// (bytes of other slots cleared): a signed byte read then gives 2^(8-B) q.
-template <int B>
-__device__ __forceinline__ uint32_t slot_top(uint32_t w, int s)
-{
-    constexpr uint32_t top = ((0xFFu << (8 - B)) & 0xFFu) * 0x01010101u;
-    return (w << (8 - B - s * B)) & top;
-}
-
-__device__ __forceinline__ float sbyte(uint32_t w, int e)
-{
-    return static_cast<float>(static_cast<int8_t>(static_cast<uint8_t>(w >> (8 * e))));
-}
-
-__device__ __forceinline__ int fdiv(int n, FastDiv d)
-{
-    const uint32_t u = static_cast<uint32_t>(n);
-    return static_cast<int>((__umulhi(u, d.mul) + u) >> d.shift);
-}
-
-template <int CTRL, int ROWS>
-__device__ __forceinline__ float dpp_term(float x)
-{
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWS, 0xF, false));
-}
-
-// Sum over the 64 lanes of a wavefront with DPP row operations; the result
-// is returned uniform (read from the last lane).
-__device__ __forceinline__ float wave_sum(float x)
-{
-    x += dpp_term<0xB1, 0xF>(x);    // quad_perm [1,0,3,2]
-    x += dpp_term<0x4E, 0xF>(x);    // quad_perm [2,3,0,1]: quad sums
-    x += dpp_term<0x141, 0xF>(x);   // row_half_mirror: 8-lane sums
-    x += dpp_term<0x140, 0xF>(x);   // row_mirror: 16-lane row sums
-    x += dpp_term<0x142, 0xA>(x);   // row_bcast:15 into rows 1, 3
-    x += dpp_term<0x143, 0xC>(x);   // row_bcast:31 into rows 2, 3
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
-}
-
-// ---------------------------------------------------------------------------
-// decode step
-
-template <int DV>
-struct DecodeShared {
-    float2 kq[kSlotTable];               // (k_i r_i f_i / q_b, q_i r_i f_i / q_b) per row-table slot
-    float av[kSlotTable];                // beta k_i q_b / r_i
-    float sk[kMaxDk], sq[kMaxDk];        // k, q of the tile in logical row order
-    float sr[kMaxDk];                    // r in physical row order
-    float sd[kMaxDk];                    // channel-wise gate d in logical row order (diagonal gate only)
-    float al[kSlotTable];                // d_i 2^(b-8) per row-table slot (diagonal gate only)
-    int sperm[kMaxDk];                   // logical row of each physical row
-    float4 red[2][256 / (DV / 4)][DV / 4];
-    float bcol[DV];                      // delta_j / c_j
-    float kap[4];
-};
-
-struct TileCtx {
-    int tile, b, h, hq;
-    HeadInfo hi;
-    uint32_t *codes;
-    const float *rr, *cc;
-    float alpha, beta;
-};
-
-// Per-tile operands of thread tid, loaded together at the start of a tile:
-// k_i, q_i for logical row i = tid; r_p and the logical index of physical
-// row p = tid; c_j, v_j for column j = tid.
-struct RowColOps {
-    float k, q, r, c, v;
-    float d;                    // channel-wise gate of logical row tid (diagonal gate only)
-    int perm;
-};
-
-template <bool BF16, bool DIAG, int DV>
-__device__ __forceinline__ RowColOps load_ops(const DecodeArgs &a, int tile, int b, int hq, int h, const float *rr,
-                                              const float *cc)
-{
-    const PoolView &P = a.pool;
-    const int tid = threadIdx.x;
-    RowColOps op{0.f, 0.f, 0.f, 0.f, 0.f, 1.f, 0};
-    if (tid < P.dk) {
-        if constexpr (DIAG) op.d = act_ld<BF16>(a.alpha, static_cast<size_t>(tile) * P.dk + tid);
-        const size_t off = (static_cast<size_t>(b) * P.Hqk + hq) * P.dk + tid;
-        op.k = act_ld<BF16>(a.k, off);
-        op.q = act_ld<BF16>(a.q, off);
-        op.r = rr[tid];
-        op.perm = P.perm[h * P.dk + tid];
-    }
-    if (tid < DV) {
-        op.c = cc[tid];
-        op.v = act_ld<BF16>(a.v, static_cast<size_t>(tile) * DV + tid);
-    }
-    return op;
-}
-
-// Row constants into LDS, indexed by row-table slot, and q.k.  Two barriers;
-// returns q.k.  Rows are read through the physical -> logical permutation
-// from the LDS copy of k and q.
-template <bool DIAG, int DV>
-__device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float beta, const RowColOps &op,
-                                               DecodeShared<DV> &sh)
-{
-    const int tid = threadIdx.x;
-    if (tid < dk) {
-        sh.sk[tid] = op.k;
-        sh.sq[tid] = op.q;
-        sh.sr[tid] = op.r;
-        sh.sperm[tid] = op.perm;
-        if constexpr (DIAG) sh.sd[tid] = op.d;
-    }
-    __syncthreads();
-    float kq = 0.f;
-    if (tid < kSlotTable) {
-        const int x = tid;
-        int bw = 8, p = -1;
-        if (x < hi.n8) {
-            p = x;
-        } else if (x < hi.n8 + 2 * hi.g4) {
-            bw = 4;
-            const int kk = x - hi.n8;
-            if (kk < hi.n4) p = hi.n8 + kk;
-        } else if (x < hi.n8 + 2 * hi.g4 + 4 * hi.g2) {
-            bw = 2;
-            const int kk = x - hi.n8 - 2 * hi.g4;
-            if (kk < hi.n2) p = hi.n8 + hi.n4 + kk;
-        }
-        float kt = 0.f, qt = 0.f, av = 0.f, al = 0.f;
-        if (p >= 0) {
-            // slot x holds physical row p, whose r and permutation entry were
-            // loaded by thread p
-            const int i = sh.sperm[p];
-            const float ki = sh.sk[i];
-            const float qi = sh.sq[i];
-            const float rp = sh.sr[p];
-            const float qb = bw == 8 ? 127.0f : (bw == 4 ? 7.0f : 1.0f);
-            // 2^(b-8) / q_b: 1/127, 1/112, 1/64 (an unpacked field reads 2^(8-b) q)
-            const float fq = bw == 8 ? (1.0f / 127.0f) : (bw == 4 ? (1.0f / 112.0f) : (1.0f / 64.0f));
-            const float di = DIAG ? sh.sd[i] : 1.0f;       // the gate folds into both row weights
-            const float rs = rp * fq * di;
-            kt = ki * rs;
-            qt = qi * rs;
-            av = beta * ki * qb * __builtin_amdgcn_rcpf(rp);
-            al = di * (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
-            kq = qi * ki;
-        }
-        sh.kq[x] = make_float2(kt, qt);
-        sh.av[x] = av;
-        if constexpr (DIAG) sh.al[x] = al;
-    }
-    kq = wave_sum(kq);
-    if ((tid & 63) == 0) sh.kap[tid >> 6] = kq;
-    __syncthreads();
-    return (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
-}
-
-// Uniform layouts: table slot = physical row = tid, widths known at compile time.
-template <bool DIAG, int M8, int M4, int DV>
-__device__ __forceinline__ float row_constants_uniform(float beta, const RowColOps &op, DecodeShared<DV> &sh)
-{
-    constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
-    const int tid = threadIdx.x;
-    if (tid < 128) {
-        sh.sk[tid] = op.k;
-        sh.sq[tid] = op.q;
-        if constexpr (DIAG) sh.sd[tid] = op.d;
-    }
-    __syncthreads();
-    float kq = 0.f;
-    if (tid < 128) {
-        const int p = tid;
-        const float qb = p < X4 ? 127.0f : (p < X2 ? 7.0f : 1.0f);
-        const float fq = p < X4 ? (1.0f / 127.0f) : (p < X2 ? (1.0f / 112.0f) : (1.0f / 64.0f));
-        const float ki = sh.sk[op.perm];
-        const float qi = sh.sq[op.perm];
-        const float di = DIAG ? sh.sd[op.perm] : 1.0f;
-        const float rs = op.r * fq * di;
-        sh.kq[p] = make_float2(ki * rs, qi * rs);
-        sh.av[p] = beta * ki * qb * __builtin_amdgcn_rcpf(op.r);
-        if constexpr (DIAG) sh.al[p] = di * (p < X4 ? 1.0f : (p < X2 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
-        kq = qi * ki;
-    }
-    kq = wave_sum(kq);
-    if ((tid & 63) == 0) sh.kap[tid >> 6] = kq;
-    __syncthreads();
-    return (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
-}
-
-// Column sums of the per-thread partials, residual, readout, column factor
-// of the code-space update.  cj, vj: column tid's scale and value (threads
-// < DV, loaded at the start of the tile).  Ends with a barrier.
-template <int DV>
-__device__ __forceinline__ void column_phase(const DecodeArgs &a, int tile, float alpha, float beta,
-                                             DecodeShared<DV> &sh, float kappa, const float (&acK)[4],
-                                             const float (&acQ)[4], float cj, float vj)
-{
-    constexpr int CG = DV / 4, NSL = 256 / CG;
-    const int tid = threadIdx.x;
-    sh.red[0][tid / CG][tid % CG] = make_float4(acK[0], acK[1], acK[2], acK[3]);
-    sh.red[1][tid / CG][tid % CG] = make_float4(acQ[0], acQ[1], acQ[2], acQ[3]);
-    __syncthreads();
-    if (tid < DV) {
-        const int j = tid;
-        const float *rk = reinterpret_cast<const float *>(&sh.red[0][0][0]);
-        const float *rq = reinterpret_cast<const float *>(&sh.red[1][0][0]);
-        float sk = rk[j], sq = rq[j];
-#pragma unroll
-        for (int s = 1; s < NSL; ++s) {
-            sk += rk[s * DV + j];
-            sq += rq[s * DV + j];
-        }
-        const float delta = vj - alpha * (cj * sk);     // v - alpha (S^T k)
-        a.o[static_cast<size_t>(tile) * DV + j] = alpha * (cj * sq) + beta * kappa * delta;
-        sh.bcol[j] = delta * __builtin_amdgcn_rcpf(cj);
-    }
-    __syncthreads();
-}
-
-// Unpack one word's slot-s fields (2^(8-B) q each) and add them, weighted
-// by the slot's row constants, to the 4 column partials.
-template <int B>
-__device__ __forceinline__ void unpack_acc(uint32_t w, const float2 *kq, int x0, float *U, float (&acK)[4],
-                                           float (&acQ)[4])
-{
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float2 c = kq[x0 + s];
-        const uint32_t W = slot_top<B>(w, s);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float u = sbyte(W, e);
-            U[4 * s + e] = u;
-            acK[e] = fmaf(c.x, u, acK[e]);
-            acQ[e] = fmaf(c.y, u, acQ[e]);
-        }
-    }
-}
-
-template <int B>
-__device__ __forceinline__ void unpack_word(uint32_t w, float *U)
-{
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const uint32_t W = slot_top<B>(w, s);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) U[4 * s + e] = sbyte(W, e);
-    }
-}
-
-// ---- codes kept as packed f16 pairs between the passes (exact: |2^(8-B) q| <= 127)
-
-// Bytes LO and HI of w, read as signed, to an f16 pair: one SDWA convert per
-// field, the second one writing the upper half in place.
-template <int LO, int HI>
-__device__ __forceinline__ uint32_t sbytes_f16(uint32_t w)
-{
-    uint32_t r;
-    asm("v_cvt_f16_i16_sdwa %0, sext(%1) dst_sel:WORD_0 dst_unused:UNUSED_PAD src0_sel:BYTE_%c2"
-        : "=v"(r) : "v"(w), "i"(LO));
-    asm("v_cvt_f16_i16_sdwa %0, sext(%1) dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_%c2"
-        : "+v"(r) : "v"(w), "i"(HI));
-    return r;
-}
-
-// a * h + c with h the low (HI = 0) or high (HI = 1) f16 half of hp, in fp32
-// (v_fma_mix_f32: the half is widened exactly inside the FMA).
-template <int HI>
-__device__ __forceinline__ float fma_mix(float a, uint32_t hp, float c)
-{
-    float r;
-    if constexpr (HI)
-        asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel:[0,1,0] op_sel_hi:[0,1,0]" : "=v"(r) : "v"(a), "v"(hp), "v"(c));
-    else
-        asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel_hi:[0,1,0]" : "=v"(r) : "v"(a), "v"(hp), "v"(c));
-    return r;
-}
-
-template <int E>
-__device__ __forceinline__ float fma_mix_e(float a, const uint32_t *U2, int s, float c)
-{
-    return fma_mix<E & 1>(a, U2[2 * s + (E >> 1)], c);
-}
-
-template <int B>
-__device__ __forceinline__ void unpack_acc_h(uint32_t w, const float2 *kq, int x0, uint32_t *U2, float (&acK)[4],
-                                             float (&acQ)[4])
-{
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float2 c = kq[x0 + s];
-        const uint32_t W = slot_top<B>(w, s);
-        U2[2 * s] = sbytes_f16<0, 1>(W);
-        U2[2 * s + 1] = sbytes_f16<2, 3>(W);
-        acK[0] = fma_mix_e<0>(c.x, U2, s, acK[0]);
-        acQ[0] = fma_mix_e<0>(c.y, U2, s, acQ[0]);
-        acK[1] = fma_mix_e<1>(c.x, U2, s, acK[1]);
-        acQ[1] = fma_mix_e<1>(c.y, U2, s, acQ[1]);
-        acK[2] = fma_mix_e<2>(c.x, U2, s, acK[2]);
-        acQ[2] = fma_mix_e<2>(c.y, U2, s, acQ[2]);
-        acK[3] = fma_mix_e<3>(c.x, U2, s, acK[3]);
-        acQ[3] = fma_mix_e<3>(c.y, U2, s, acQ[3]);
-    }
-}
-
-template <int B, int E>
-__device__ __forceinline__ uint32_t requant_field(const uint32_t *U2, int s, float al, float a_s, float bce, uint32_t P)
-{
-    constexpr float bias = static_cast<float>(1 << (B - 1));
-    constexpr float top = static_cast<float>((1 << B) - 1);
-    const float tt = fmaf(a_s, bce, bias);
-    float y = fma_mix_e<E>(al, U2, s, tt);
-    y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
-    return __builtin_amdgcn_cvt_pk_u8_f32(y, E, P);
-}
-
-// al: the per-width gate factor (scalar gate) or, with a table alt, per row.
-template <int B, bool DIAG>
-__device__ __forceinline__ uint32_t requant_word_h(const uint32_t *U2, const float *av, const float *alt, int x0,
-                                                   float al_w, const float (&bc)[4])
-{
-    constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
-    uint32_t out = 0;
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float a_s = av[x0 + s];
-        const float al = DIAG ? alt[x0 + s] : al_w;
-        uint32_t P = 0;
-        P = requant_field<B, 0>(U2, s, al, a_s, bc[0], P);
-        P = requant_field<B, 1>(U2, s, al, a_s, bc[1], P);
-        P = requant_field<B, 2>(U2, s, al, a_s, bc[2], P);
-        P = requant_field<B, 3>(U2, s, al, a_s, bc[3], P);
-        out |= P << (s * B);
-    }
-    return out ^ flip;
-}
-
-// New word from the unpacked old fields: per field
-//   y = al U + av_i bc_j + 2^(B-1)        (code + bias, Eq. 3 argument)
-// clamped to [1, 2^B - 1] (i.e. code in [-q_b, q_b]), rounded to nearest
-// even and packed to a byte by v_cvt_pk_u8_f32, then the bias is removed
-// from all fields at once by flipping each field's top bit.
-template <int B, bool DIAG>
-__device__ __forceinline__ uint32_t requant_word(const float *U, const float *av, const float *alt, int x0,
-                                                 float al_w, const float (&bc)[4])
-{
-    constexpr float bias = static_cast<float>(1 << (B - 1));
-    constexpr float top = static_cast<float>((1 << B) - 1);
-    constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
-    uint32_t out = 0;
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float a_s = av[x0 + s];
-        const float al = DIAG ? alt[x0 + s] : al_w;
-        uint32_t P = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float tt = fmaf(a_s, bc[e], bias);
-            float y = fmaf(al, U[4 * s + e], tt);
-            y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
-            P = __builtin_amdgcn_cvt_pk_u8_f32(y, e, P);
-        }
-        out |= P << (s * B);
-    }
-    return out ^ flip;
-}
 
 // Rows of one width per word-step; codes stay in registers between passes.
 template <bool BF16, bool DIAG, int M8, int M4, int M2>

@@ -20,12 +20,14 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("STEPQ_LIB") or os.path.join(_HERE, "libstepq.so")
 
 STEPQ_F32, STEPQ_BF16 = 0, 1
+STEPQ_STEP_KDA_GATE, STEPQ_STEP_REFIT = 1, 2
 _STATUS = {0: "STEPQ_OK", 1: "STEPQ_E_INVALID", 2: "STEPQ_E_UNSUPPORTED", 3: "STEPQ_E_NOMEM", 4: "STEPQ_E_HIP"}
 
 EXPORTED = (
     "stepq_pool_bytes", "stepq_pool_create", "stepq_pool_destroy", "stepq_pool_device_ptr",
-    "stepq_pool_load", "stepq_decode_step", "stepq_decode_step_kda", "stepq_pool_dequant", "stepq_pool_export",
-    "stepq_pool_import", "stepq_last_error", "stepq_setup_fit", "stepq_setup_lifetime_bits",
+    "stepq_pool_load", "stepq_decode_step", "stepq_decode_step_kda", "stepq_decode_step_ex",
+    "stepq_pool_set_row_weight", "stepq_pool_dequant", "stepq_pool_export", "stepq_pool_import",
+    "stepq_last_error", "stepq_setup_fit", "stepq_setup_lifetime_bits",
 )
 
 
@@ -60,6 +62,8 @@ def lib():
             "stepq_pool_load": ([P, P, i32, P, P, P, P], st),
             "stepq_decode_step": ([P, P, i32, P, P, P, P, P, st, P, P], st),
             "stepq_decode_step_kda": ([P, P, i32, P, P, P, P, P, st, P, P], st),
+            "stepq_decode_step_ex": ([P, P, i32, P, P, P, P, P, st, ctypes.c_uint32, P, P], st),
+            "stepq_pool_set_row_weight": ([P, P], st),
             "stepq_pool_dequant": ([P, P, i32, P, P], st),
             "stepq_pool_export": ([P, P, i32, P, P, P, P], st),
             "stepq_pool_import": ([P, P, i32, P, P, P, P], st),
@@ -153,33 +157,37 @@ class Pool:
     def load(self, slot_ids, state, r, c, stream=None):
         stepq_pool_load(self, slot_ids, state, r, c, stream)
 
-    def step(self, slot_ids, q, k, v, alpha, beta, o, stream=None):
-        stepq_decode_step(self, slot_ids, q, k, v, alpha, beta, o, stream)
+    def step(self, slot_ids, q, k, v, alpha, beta, o, stream=None, refit=False):
+        if refit:
+            stepq_decode_step_ex(self, slot_ids, q, k, v, alpha, beta, o, STEPQ_STEP_REFIT, stream)
+        else:
+            stepq_decode_step(self, slot_ids, q, k, v, alpha, beta, o, stream)
 
-    def step_kda(self, slot_ids, q, k, v, gate, beta, o, stream=None):
-        stepq_decode_step_kda(self, slot_ids, q, k, v, gate, beta, o, stream)
+    def step_kda(self, slot_ids, q, k, v, gate, beta, o, stream=None, refit=False):
+        if refit:
+            stepq_decode_step_ex(self, slot_ids, q, k, v, gate, beta, o, STEPQ_STEP_KDA_GATE | STEPQ_STEP_REFIT,
+                                 stream)
+        else:
+            stepq_decode_step_kda(self, slot_ids, q, k, v, gate, beta, o, stream)
 
-    def prepare_step(self, slot_ids, q, k, v, alpha, beta, o, stream=None):
+    def set_row_weight(self, w):
+        stepq_pool_set_row_weight(self, w)
+
+    def prepare_step(self, slot_ids, q, k, v, alpha, beta, o, stream=None, refit=False):
         """Validate the arguments of one decode step once and return a
         callable that launches it with the cached pointers (for decode loops
         where the per-call checks would dominate the launch cost).  alpha of
-        shape [B][Hv][d_k] selects the channel-wise (KDA) gate."""
-        n, ids = _ids(self, slot_ids)
-        dt = q.dtype
-        if dt not in (torch.float32, torch.bfloat16):
-            raise TypeError("activations must be float32 or bfloat16")
-        code = STEPQ_F32 if dt == torch.float32 else STEPQ_BF16
+        shape [B][Hv][d_k] selects the channel-wise (KDA) gate; refit the
+        online scale refit."""
         kda = alpha.dim() == 3
-        gshape = (n, self.Hv, self.dk) if kda else (n, self.Hv)
-        args = (self.handle, ids, n,
-                _dev(q, "q", dt, (n, self.Hqk, self.dk), self.device),
-                _dev(k, "k", dt, (n, self.Hqk, self.dk), self.device),
-                _dev(v, "v", dt, (n, self.Hv, self.dv), self.device),
-                _dev(alpha, "alpha", dt, gshape, self.device),
-                _dev(beta, "beta", dt, (n, self.Hv), self.device), code,
-                _dev(o, "o", torch.float32, (n, self.Hv, self.dv), self.device), _stream(stream))
+        args = _step_args(self, slot_ids, q, k, v, alpha, beta, o, stream, kda)
         keep = (slot_ids, q, k, v, alpha, beta, o)      # the tensors must outlive the callable
-        fn = lib().stepq_decode_step_kda if kda else lib().stepq_decode_step
+        if refit:
+            flags = ctypes.c_uint32(STEPQ_STEP_REFIT | (STEPQ_STEP_KDA_GATE if kda else 0))
+            fn = lib().stepq_decode_step_ex
+            args = args[:9] + (flags,) + args[9:]
+        else:
+            fn = lib().stepq_decode_step_kda if kda else lib().stepq_decode_step
 
         def launch():
             _ = keep
@@ -227,38 +235,45 @@ def stepq_pool_load(pool: Pool, slot_ids, state, r, c, stream=None):
         _dev(c, "c", torch.float32, (n, P.Hv, P.dv), P.device), _stream(stream)))
 
 
-def stepq_decode_step(pool: Pool, slot_ids, q, k, v, alpha, beta, o, stream=None):
+def _step_args(pool: Pool, slot_ids, q, k, v, gate, beta, o, stream, kda: bool):
+    """Checked pointer arguments of a decode-step call, in C order without
+    the flags: (pool, ids, batch, q, k, v, gate, beta, dtype, o, stream)."""
     n, ids = _ids(pool, slot_ids)
     P = pool
     dt = q.dtype
     if dt not in (torch.float32, torch.bfloat16):
         raise TypeError("activations must be float32 or bfloat16")
     code = STEPQ_F32 if dt == torch.float32 else STEPQ_BF16
-    _check(lib().stepq_decode_step(
-        pool.handle, ids, n,
-        _dev(q, "q", dt, (n, P.Hqk, P.dk), P.device),
-        _dev(k, "k", dt, (n, P.Hqk, P.dk), P.device),
-        _dev(v, "v", dt, (n, P.Hv, P.dv), P.device),
-        _dev(alpha, "alpha", dt, (n, P.Hv), P.device),
-        _dev(beta, "beta", dt, (n, P.Hv), P.device), code,
-        _dev(o, "o", torch.float32, (n, P.Hv, P.dv), P.device), _stream(stream)))
+    gshape = (n, P.Hv, P.dk) if kda else (n, P.Hv)
+    return (pool.handle, ids, n,
+            _dev(q, "q", dt, (n, P.Hqk, P.dk), P.device),
+            _dev(k, "k", dt, (n, P.Hqk, P.dk), P.device),
+            _dev(v, "v", dt, (n, P.Hv, P.dv), P.device),
+            _dev(gate, "gate" if kda else "alpha", dt, gshape, P.device),
+            _dev(beta, "beta", dt, (n, P.Hv), P.device), code,
+            _dev(o, "o", torch.float32, (n, P.Hv, P.dv), P.device), _stream(stream))
+
+
+def stepq_decode_step(pool: Pool, slot_ids, q, k, v, alpha, beta, o, stream=None):
+    _check(lib().stepq_decode_step(*_step_args(pool, slot_ids, q, k, v, alpha, beta, o, stream, False)))
 
 
 def stepq_decode_step_kda(pool: Pool, slot_ids, q, k, v, gate, beta, o, stream=None):
-    n, ids = _ids(pool, slot_ids)
-    P = pool
-    dt = q.dtype
-    if dt not in (torch.float32, torch.bfloat16):
-        raise TypeError("activations must be float32 or bfloat16")
-    code = STEPQ_F32 if dt == torch.float32 else STEPQ_BF16
-    _check(lib().stepq_decode_step_kda(
-        pool.handle, ids, n,
-        _dev(q, "q", dt, (n, P.Hqk, P.dk), P.device),
-        _dev(k, "k", dt, (n, P.Hqk, P.dk), P.device),
-        _dev(v, "v", dt, (n, P.Hv, P.dv), P.device),
-        _dev(gate, "gate", dt, (n, P.Hv, P.dk), P.device),
-        _dev(beta, "beta", dt, (n, P.Hv), P.device), code,
-        _dev(o, "o", torch.float32, (n, P.Hv, P.dv), P.device), _stream(stream)))
+    _check(lib().stepq_decode_step_kda(*_step_args(pool, slot_ids, q, k, v, gate, beta, o, stream, True)))
+
+
+def stepq_decode_step_ex(pool: Pool, slot_ids, q, k, v, gate, beta, o, flags: int, stream=None):
+    a = _step_args(pool, slot_ids, q, k, v, gate, beta, o, stream, bool(flags & STEPQ_STEP_KDA_GATE))
+    _check(lib().stepq_decode_step_ex(*a[:9], ctypes.c_uint32(flags), *a[9:]))
+
+
+def stepq_pool_set_row_weight(pool: Pool, w):
+    """w: [Hv][d_k] row-impact factors (host array or tensor), logical row order."""
+    wt = np.ascontiguousarray(w.cpu().numpy() if isinstance(w, torch.Tensor) else w, dtype=np.float32)
+    if wt.shape != (pool.Hv, pool.dk):
+        raise ValueError(f"row weights have shape {wt.shape}, expected {(pool.Hv, pool.dk)}")
+    with torch.cuda.device(pool.device):
+        _check(lib().stepq_pool_set_row_weight(pool.handle, wt.ctypes.data_as(ctypes.c_void_p)))
 
 
 def stepq_pool_dequant(pool: Pool, slot_ids, out, stream=None):

@@ -95,7 +95,8 @@ def _mix(*parts: int) -> int:
 
 
 _STREAM = {"init": 1, "q": 2, "k": 3, "v": 4, "alpha": 5, "beta": 6,
-           "bits": 7, "calib": 8, "slots": 9, "gain_r": 10, "gain_c": 11, "kda": 12}
+           "bits": 7, "calib": 8, "slots": 9, "gain_r": 10, "gain_c": 11, "kda": 12,
+           "roww": 13}
 
 
 def _gen(device, w: Workload, layer: int, step: int, stream: str, chunk: int = 0) -> torch.Generator:
@@ -179,6 +180,15 @@ def kda_gates(w: Workload, layer: int, step: int, device="cpu") -> torch.Tensor:
     workload's gate law, on a stream of its own."""
     g = _gen(device, w, layer, step, "kda")
     return _gates(w, g, (w.batch, w.n_v_heads, w.d_k), device).to(w.act_dtype)
+
+
+def row_weight_draw(w: Workload, layer: int = 0, sigma: float = 0.5) -> torch.Tensor:
+    """Synthetic row-impact factors, float32 [Hv][d_k]: lognormal with log
+    standard deviation sigma, each head's logs centred so that its geometric
+    mean is one (the normalisation the factors carry)."""
+    g = _gen("cpu", w, layer, 0, "roww")
+    x = torch.randn((w.n_v_heads, w.d_k), generator=g, dtype=torch.float64) * sigma
+    return torch.exp(x - x.mean(dim=1, keepdim=True)).to(torch.float32)
 
 
 def calibration_gates(w: Workload, layer: int = 0) -> torch.Tensor:

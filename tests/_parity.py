@@ -27,6 +27,12 @@ from paper_2609_38169_amd import workloads as W
 CODE_MISMATCH_FRAC = 1e-4
 TIE_WINDOW = 2e-3          # code units; fp32 error of the code-space update is ~1e-5
 O_ABS, O_REL = 1e-5, 1e-3
+# Refitted scales (fp32 sums on the GPU vs fp64): a scale is an fp32 value
+# formed from O(d) terms, so 1e-5 relative is ~100 ulp of headroom.  A
+# column factor may also come from another, equally valid, rounding of fixed
+# codes that sit within TIE_WINDOW of a rounding boundary: the oracle bounds
+# the factor over all such roundings (c_range) and the GPU's must lie inside.
+SCALE_REL = 1e-5
 
 
 def bits_for(w: W.Workload, layer: int = 0) -> np.ndarray:
@@ -69,6 +75,39 @@ def compare_codes(gpu: np.ndarray, orc: np.ndarray, y: np.ndarray, what: str = "
     return n_bad
 
 
+def compare_refit(g_codes, g_r, g_c, o_codes, o_r, o_c, y, c_range, what: str = "refit"):
+    """Tolerances of the refitting step, tile arrays [n][dk][dv], [n][dk],
+    [n][dv].  Returns (code mismatches, columns off the oracle's factor).
+
+    r' within SCALE_REL.  c' within SCALE_REL of the oracle's range over the
+    near-tie roundings of its fixed codes.  Codes: a mismatch is one level,
+    and its oracle value y lies within TIE_WINDOW of a rounding boundary after
+    allowing for the scale differences of its row and column; at most
+    CODE_MISMATCH_FRAC of the codes."""
+    g_r, g_c = g_r.astype(np.float64), g_c.astype(np.float64)
+    o_r, o_c = o_r.astype(np.float64), o_c.astype(np.float64)
+    dr = np.abs(g_r - o_r) / o_r
+    assert np.all(dr <= SCALE_REL), f"{what}: row scale off by {dr.max():.3g} relative"
+    lo, hi = c_range
+    inside = (g_c >= lo * (1 - SCALE_REL)) & (g_c <= hi * (1 + SCALE_REL))
+    assert np.all(inside), (f"{what}: {int((~inside).sum())} column scales outside the admissible range, e.g. "
+                            f"{g_c[~inside][:3]} vs [{lo[~inside][:3]}, {hi[~inside][:3]}]")
+    dc = np.abs(g_c - o_c) / o_c
+    diff = g_codes.astype(np.int16) - o_codes.astype(np.int16)
+    bad = np.nonzero(diff)
+    n_bad = bad[0].size
+    if n_bad:
+        assert np.all(np.abs(diff[bad]) == 1), f"{what}: a code differs by more than one level"
+        yb = np.abs(y[bad])
+        frac = yb - np.floor(yb)
+        allow = TIE_WINDOW + yb * (dr[bad[0], bad[1]] + dc[bad[0], bad[2]]) * 1.01
+        ok = np.abs(frac - 0.5) <= allow
+        assert np.all(ok), (f"{what}: {int((~ok).sum())} code mismatches not explained by a tie, e.g. "
+                            f"y={y[bad][~ok][:4]}")
+        assert n_bad <= CODE_MISMATCH_FRAC * g_codes.size, f"{what}: {n_bad} of {g_codes.size} codes differ"
+    return n_bad, int((dc > SCALE_REL).sum())
+
+
 def compare_out(gpu: np.ndarray, orc: np.ndarray, what: str = "o"):
     err = np.abs(gpu.astype(np.float64) - orc)
     lim = O_ABS + O_REL * np.abs(orc)
@@ -82,8 +121,10 @@ class Lockstep:
     ``check_rows`` (batch rows whose slots are compared each step)."""
 
     def __init__(self, w: W.Workload, pool, slots: torch.Tensor, bits: np.ndarray, check_rows: np.ndarray,
-                 S0_check: np.ndarray, layer: int = 0):
+                 S0_check: np.ndarray, layer: int = 0, refit: bool = False, row_weight=None):
         self.w, self.pool, self.slots, self.bits, self.layer = w, pool, slots, bits, layer
+        self.refit = refit
+        self.tie_cols = 0
         self.rows = np.asarray(check_rows)
         n = len(self.rows) * w.n_v_heads
         self.tile_bits = np.broadcast_to(bits[None], (len(self.rows),) + bits.shape).reshape(n, w.d_k)
@@ -93,6 +134,8 @@ class Lockstep:
         dev = pool.device
         self.ids = slots.index_select(0, torch.as_tensor(self.rows, dtype=torch.long, device=slots.device)).to(dev)
         self.n_tiles = n
+        self.row_w = None if row_weight is None else np.broadcast_to(
+            np.asarray(row_weight, np.float64)[None], (len(self.rows),) + bits.shape).reshape(n, w.d_k)
         self.mismatches = 0
         self.saturated = 0.0
 
@@ -121,14 +164,57 @@ class Lockstep:
         """Oracle step on its own state, compare with the GPU's result."""
         w = self.w
         q, k, v, a, b = oracle_inputs(w, inp, self.rows)
-        new, o, y = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True)
         g_codes, g_r, g_c = self.export()
-        assert np.array_equal(g_r.reshape(self.r.shape), self.r), "row scales changed"
-        assert np.array_equal(g_c.reshape(self.c.shape), self.c), "column scales changed"
-        self.mismatches += compare_codes(g_codes, new, y, f"layer {self.layer} step {step} codes")
+        if self.refit:
+            new, rn, cn, o, ex = oracle.decode_step_refit(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b,
+                                                          w=self.row_w, want=("y", "c_range"), tie_window=TIE_WINDOW)
+            nb, tc = compare_refit(g_codes, g_r.reshape(rn.shape), g_c.reshape(cn.shape), new, rn, cn,
+                                   ex["y"], ex["c_range"], f"layer {self.layer} step {step} refit")
+            self.mismatches += nb
+            self.tie_cols += tc
+            self.r, self.c = rn, cn
+        else:
+            new, o, y = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True)
+            assert np.array_equal(g_r.reshape(self.r.shape), self.r), "row scales changed"
+            assert np.array_equal(g_c.reshape(self.c.shape), self.c), "column scales changed"
+            self.mismatches += compare_codes(g_codes, new, y, f"layer {self.layer} step {step} codes")
         rows_t = torch.as_tensor(self.rows, dtype=torch.long, device=o_gpu.device)
         og = o_gpu.index_select(0, rows_t).cpu().numpy().reshape(self.n_tiles, w.d_v)
         compare_out(og, o, f"layer {self.layer} step {step} o")
         qb = (2 ** (self.tile_bits.astype(np.int32) - 1) - 1)[:, :, None]
         self.saturated = float(np.mean(np.abs(new) == qb))
         self.codes = new
+
+
+def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, mutate=None, kda: bool = False,
+                 refit: bool = False, row_weight=None, say=print):
+    """Full-size decode steps of one workload layer on the GPU, the rows
+    ``check_rows`` compared lockstep with the oracle at every step."""
+    from paper_2609_38169_amd.pools import build_pool, row_bits
+    bits = row_bits(w, layer)
+    say(f"lockstep {w.name}: building pool ({w.n_slots} slots)")
+    pool = build_pool(w, layer, device=device, bits=bits)
+    if row_weight is not None:
+        pool.set_row_weight(row_weight)
+    slots = W.active_slots(w).to(device)
+    check_slots = W.active_slots(w)[np.asarray(check_rows)]
+    S0 = W.initial_state(w, layer, [int(x) for x in check_slots], device=device).cpu().numpy()
+    ls = Lockstep(w, pool, slots, bits, check_rows, S0, layer, refit=refit, row_weight=row_weight)
+    o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=device)
+    for t in range(steps):
+        inp = W.step_inputs(w, layer, t, device=device)
+        if kda:
+            inp["alpha"] = W.kda_gates(w, layer, t, device=device)
+        if mutate:
+            inp = mutate(inp)
+        ls.anchor()
+        if kda:
+            pool.step_kda(slots, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o, refit=refit)
+        else:
+            pool.step(slots, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o, refit=refit)
+        torch.cuda.synchronize()
+        ls.check_step(inp, o, t)
+    say(f"lockstep {w.name}{' kda' if kda else ''}{' refit' if refit else ''}: {steps} steps ok, "
+        f"code mismatches {ls.mismatches}, columns on another tie rounding {ls.tie_cols}, "
+        f"saturated {ls.saturated:.3f}")
+    return ls

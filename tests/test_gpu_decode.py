@@ -88,29 +88,7 @@ def test_pool_load_matches_oracle_quantizer(idx):
 
 
 def _lockstep_run(w, steps, check_rows, layer=0, mutate=None, kda=False):
-    bits = row_bits(w, layer)
-    _say(f"lockstep {w.name}: building pool ({w.n_slots} slots)")
-    pool = build_pool(w, layer, device=DEV, bits=bits)
-    slots = W.active_slots(w).to(DEV)
-    check_slots = W.active_slots(w)[check_rows]
-    S0 = W.initial_state(w, layer, [int(s) for s in check_slots], device=DEV).cpu().numpy()
-    ls = PT.Lockstep(w, pool, slots, bits, check_rows, S0, layer)
-    o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=DEV)
-    for t in range(steps):
-        inp = W.step_inputs(w, layer, t, device=DEV)
-        if kda:
-            inp["alpha"] = W.kda_gates(w, layer, t, device=DEV)
-        if mutate:
-            inp = mutate(inp)
-        ls.anchor()
-        if kda:
-            pool.step_kda(slots, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o)
-        else:
-            pool.step(slots, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o)
-        torch.cuda.synchronize()
-        ls.check_step(inp, o, t)
-    _say(f"lockstep {w.name}{' kda' if kda else ''}: {steps} steps ok, tie mismatches {ls.mismatches}, saturated {ls.saturated:.3f}")
-    return ls
+    return PT.lockstep_run(w, steps, check_rows, DEV, layer=layer, mutate=mutate, kda=kda, say=_say)
 
 
 def test_decode_tiny_all_steps():
