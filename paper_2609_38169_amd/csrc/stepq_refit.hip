@@ -17,9 +17,10 @@
 //     q'_ij = clip(round(yh_ij c_j / c'_j), -q_b, q_b)
 // Four passes over the thread's values with three LDS reductions between
 // them: row sums (over the lanes that share a row), column maxima (kept per
-// width so that the division by q_b happens once per column), and the
-// column sums of the least-squares numerator and denominator.  The new r'
-// and c' overwrite the tile's scales; a zero denominator keeps c_j.
+// width in the thread, so that the scaling by 1/q_b happens once per column
+// and thread), and the column sums of the least-squares numerator and
+// denominator.  The new r' and c' overwrite
+// the tile's scales; a zero denominator keeps c_j.
 #include "stepq_device.h"
 
 #include <type_traits>
@@ -33,8 +34,8 @@ template <int DV>
 struct RefitShared {
     DecodeShared<DV> d;
     union {
-        float rowp[DV / 4][kSlotTable + 1];        // per column-lane partials of sum_j c_j |y_ij|, by row slot
-        float4 cmax[3][256 / (DV / 4)][DV / 4];    // per slice column maxima of |yh| for widths 8, 4, 2
+        float rowp[kSlotTable][DV / 4];            // partials of sum_j c_j |y_ij| by row slot, per column lane
+        float4 cmax[256 / (DV / 4)][DV / 4];       // per slice column maxima of |yh| / q_b
     } u;
     float hrow[kSlotTable];                        // r_i / r'_i by row slot (0 for empty slots)
     float wrow[kSlotTable];                        // W_i by row slot
@@ -44,45 +45,58 @@ struct RefitShared {
     float gcol[DV];                                // c_j / c'_j
 };
 
-__device__ __forceinline__ float qb_of_width(int bw) { return bw == 8 ? 127.0f : (bw == 4 ? 7.0f : 1.0f); }
+// One row partial of a thread (4 columns of one row slot).
+template <int DV>
+__device__ __forceinline__ void put_row_partial(RefitShared<DV> &sh, int x, int cg, float acc)
+{
+    sh.u.rowp[x][cg] = acc;
+}
 
 // Row slot x (physical row p, width bw, old scale r_p): r' from the lane
-// partials, written to the tile; h and W to LDS.
+// partials, written to the tile; h and W to LDS.  The row and column
+// factors are formed with the hardware reciprocal and square root (about one
+// ulp each): every later step uses the stored fp32 values, so the codes stay
+// consistent with them.
 template <int DV>
 __device__ __forceinline__ void refit_row(RefitShared<DV> &sh, int x, int p, int bw, float r_p, float *rr_out)
 {
     float sum = 0.f;
 #pragma unroll
-    for (int l = 0; l < DV / 4; ++l) sum += sh.u.rowp[l][x];
-    const float qb = qb_of_width(bw);
-    const float m = (r_p / qb) * sum * (1.0f / static_cast<float>(DV));
+    for (int l = 0; l < DV / 4; l += 4) {
+        const float4 v4 = *reinterpret_cast<const float4 *>(&sh.u.rowp[x][l]);
+        sum += (v4.x + v4.y) + (v4.z + v4.w);
+    }
+    const float iq = bw == 8 ? (1.0f / 127.0f) : (bw == 4 ? (1.0f / 7.0f) : 1.0f);
+    const float m = (r_p * iq) * (sum * (1.0f / static_cast<float>(DV)));
     const float w = sh.wphys[p];
-    const float rn = fmaxf(sqrtf(m / w), kScaleFloor);
-    sh.hrow[x] = r_p / rn;
-    const float t = w * rn / qb;
+    const float rn = fmaxf(__builtin_amdgcn_sqrtf(m * __builtin_amdgcn_rcpf(w)), kScaleFloor);
+    sh.hrow[x] = r_p * __builtin_amdgcn_rcpf(rn);
+    const float t = (w * rn) * iq;
     sh.wrow[x] = t * t;
     rr_out[p] = rn;
 }
 
-// Column j: absmax start c0_j from the per-width maxima; e_j = c_j / c0_j.
+// Per-thread column maxima of |yh| kept per width, divided by q_b once.
+__device__ __forceinline__ float4 width_max(const float (&m8)[4], const float (&m4)[4], const float (&m2)[4])
+{
+    float r[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) r[e] = fmaxf(fmaxf(m8[e] * (1.0f / 127.0f), m4[e] * (1.0f / 7.0f)), m2[e]);
+    return make_float4(r[0], r[1], r[2], r[3]);
+}
+
+// Column j: absmax start c0_j from the slice maxima; e_j = c_j / c0_j.
 template <int DV>
 __device__ __forceinline__ void refit_colmax(RefitShared<DV> &sh, int j)
 {
     constexpr int NSL = 256 / (DV / 4);
-    const float *m8 = reinterpret_cast<const float *>(&sh.u.cmax[0][0][0]);
-    const float *m4 = reinterpret_cast<const float *>(&sh.u.cmax[1][0][0]);
-    const float *m2 = reinterpret_cast<const float *>(&sh.u.cmax[2][0][0]);
-    float a8 = 0.f, a4 = 0.f, a2 = 0.f;
+    const float *mx = reinterpret_cast<const float *>(&sh.u.cmax[0][0]);
+    float M = 0.f;
 #pragma unroll
-    for (int s = 0; s < NSL; ++s) {
-        a8 = fmaxf(a8, m8[s * DV + j]);
-        a4 = fmaxf(a4, m4[s * DV + j]);
-        a2 = fmaxf(a2, m2[s * DV + j]);
-    }
-    const float M = fmaxf(fmaxf(a8 / 127.0f, a4 / 7.0f), a2);
+    for (int s = 0; s < NSL; ++s) M = fmaxf(M, mx[s * DV + j]);
     const float cj = sh.ccol[j];
     const float c0 = fmaxf(cj * M, kScaleFloor);
-    sh.ecol[j] = M > 0.f ? cj / c0 : 0.f;
+    sh.ecol[j] = M > 0.f ? cj * __builtin_amdgcn_rcpf(c0) : 0.f;
 }
 
 // Column j: the least-squares column factor from the slice sums in d.red.
@@ -99,22 +113,24 @@ __device__ __forceinline__ void refit_colfit(RefitShared<DV> &sh, int j, float *
         den += rd[s * DV + j];
     }
     const float cj = sh.ccol[j];
+    // num / den as a full division: den may be tiny for very small states
     const float cn = den > 0.f ? fmaxf(cj * (num / den), kScaleFloor) : cj;
-    sh.gcol[j] = cj / cn;
+    sh.gcol[j] = cj * __builtin_amdgcn_rcpf(cn);
     cc_out[j] = cn;
 }
 
 // ---- per-word passes on values held in registers (4 columns x 8/B rows)
 
-// y of a word from its f16-packed fields; rp[s] = sum_e c_e |y| of slot s.
+// y of a word from its f16-packed fields; the row partial sum_e c_e |y| of
+// each slot goes to LDS.
 template <int B, bool DIAG>
-__device__ __forceinline__ void word_y(const uint32_t *U2, const DecodeShared<128> &d, int x0, float al_w,
-                                       const float (&bc)[4], const float (&cc)[4], float *Y, float *rp)
+__device__ __forceinline__ void word_y(const uint32_t *U2, RefitShared<128> &sh, int x0, int cg, float al_w,
+                                       const float (&bc)[4], const float (&cc)[4], float *Y)
 {
 #pragma unroll
     for (int s = 0; s < 8 / B; ++s) {
-        const float a_s = d.av[x0 + s];
-        const float al = DIAG ? d.al[x0 + s] : al_w;
+        const float a_s = sh.d.av[x0 + s];
+        const float al = DIAG ? sh.d.al[x0 + s] : al_w;
         float *y = Y + 4 * s;
         y[0] = fma_mix_e<0>(al, U2, s, a_s * bc[0]);
         y[1] = fma_mix_e<1>(al, U2, s, a_s * bc[1]);
@@ -123,7 +139,7 @@ __device__ __forceinline__ void word_y(const uint32_t *U2, const DecodeShared<12
         float acc = fabsf(y[0]) * cc[0];
         acc = fmaf(fabsf(y[1]), cc[1], acc);
         acc = fmaf(fabsf(y[2]), cc[2], acc);
-        rp[s] = fmaf(fabsf(y[3]), cc[3], acc);
+        put_row_partial<128>(sh, x0 + s, cg, fmaf(fabsf(y[3]), cc[3], acc));
     }
 }
 
@@ -198,10 +214,8 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
 {
     constexpr int M = M8 + M4 + M2;
     constexpr int NE = 4 * (M8 + 2 * M4 + 4 * M2);
-    constexpr int NR = M8 + 2 * M4 + 4 * M2;
     constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
     constexpr int Y4 = 4 * M8, Y2 = 4 * M8 + 8 * M4;     // value offsets of the 4- and 2-bit words
-    constexpr int R4 = M8, R2 = M8 + 2 * M4;             // row-partial offsets
     const int tid = threadIdx.x;
     const int cg = tid & 31, slice = tid >> 5;
     float *rr_out = const_cast<float *>(t.rr);
@@ -234,27 +248,17 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     float bc[4], cc[4];
     ld4(&sh.d.bcol[4 * cg], bc);
     ld4(&sh.ccol[4 * cg], cc);
-    float Y[NE], rp[NR];
+    float Y[NE];
 #pragma unroll
-    for (int m = 0; m < M8; ++m) word_y<8, DIAG>(&U[2 * m], sh.d, slice + 8 * m, t.alpha, bc, cc, &Y[4 * m], &rp[m]);
-#pragma unroll
-    for (int m = 0; m < M4; ++m)
-        word_y<4, DIAG>(&U[2 * M8 + 4 * m], sh.d, X4 + 2 * (slice + 8 * m), t.alpha * (1.0f / 16.0f), bc, cc,
-                        &Y[Y4 + 8 * m], &rp[R4 + 2 * m]);
-#pragma unroll
-    for (int m = 0; m < M2; ++m)
-        word_y<2, DIAG>(&U[2 * M8 + 4 * M4 + 8 * m], sh.d, X2 + 4 * (slice + 8 * m), t.alpha * (1.0f / 64.0f), bc,
-                        cc, &Y[Y2 + 16 * m], &rp[R2 + 4 * m]);
-#pragma unroll
-    for (int m = 0; m < M8; ++m) sh.u.rowp[cg][slice + 8 * m] = rp[m];
+    for (int m = 0; m < M8; ++m) word_y<8, DIAG>(&U[2 * m], sh, slice + 8 * m, cg, t.alpha, bc, cc, &Y[4 * m]);
 #pragma unroll
     for (int m = 0; m < M4; ++m)
-#pragma unroll
-        for (int s = 0; s < 2; ++s) sh.u.rowp[cg][X4 + 2 * (slice + 8 * m) + s] = rp[R4 + 2 * m + s];
+        word_y<4, DIAG>(&U[2 * M8 + 4 * m], sh, X4 + 2 * (slice + 8 * m), cg, t.alpha * (1.0f / 16.0f), bc, cc,
+                        &Y[Y4 + 8 * m]);
 #pragma unroll
     for (int m = 0; m < M2; ++m)
-#pragma unroll
-        for (int s = 0; s < 4; ++s) sh.u.rowp[cg][X2 + 4 * (slice + 8 * m) + s] = rp[R2 + 4 * m + s];
+        word_y<2, DIAG>(&U[2 * M8 + 4 * M4 + 8 * m], sh, X2 + 4 * (slice + 8 * m), cg, t.alpha * (1.0f / 64.0f),
+                        bc, cc, &Y[Y2 + 16 * m]);
     __syncthreads();
     if (tid < 128) refit_row<128>(sh, tid, tid, tid < X4 ? 8 : (tid < X2 ? 4 : 2), op.r, rr_out);
     __syncthreads();
@@ -268,9 +272,7 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
         for (int m = 0; m < M4; ++m) word_scale_max<4>(&Y[Y4 + 8 * m], sh.hrow, X4 + 2 * (slice + 8 * m), mx4);
 #pragma unroll
         for (int m = 0; m < M2; ++m) word_scale_max<2>(&Y[Y2 + 16 * m], sh.hrow, X2 + 4 * (slice + 8 * m), mx2);
-        sh.u.cmax[0][slice][cg] = make_float4(mx8[0], mx8[1], mx8[2], mx8[3]);
-        sh.u.cmax[1][slice][cg] = make_float4(mx4[0], mx4[1], mx4[2], mx4[3]);
-        sh.u.cmax[2][slice][cg] = make_float4(mx2[0], mx2[1], mx2[2], mx2[3]);
+        sh.u.cmax[slice][cg] = width_max(mx8, mx4, mx2);
     }
     __syncthreads();
     if (tid < 128) refit_colmax<128>(sh, tid);
@@ -390,7 +392,7 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
             float acc = fabsf(Y[4 * s]) * cc[0];
             acc = fmaf(fabsf(Y[4 * s + 1]), cc[1], acc);
             acc = fmaf(fabsf(Y[4 * s + 2]), cc[2], acc);
-            sh.u.rowp[cg][gr.x0 + s] = fmaf(fabsf(Y[4 * s + 3]), cc[3], acc);
+            put_row_partial<DV>(sh, gr.x0 + s, cg, fmaf(fabsf(Y[4 * s + 3]), cc[3], acc));
         }
     });
     __syncthreads();
@@ -421,8 +423,7 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
                 for (int e = 0; e < 4; ++e) mx[K][e] = fmaxf(mx[K][e], fabsf(Y[4 * s + e] * h));
             }
         });
-#pragma unroll
-        for (int k = 0; k < 3; ++k) sh.u.cmax[k][slice][cg] = make_float4(mx[k][0], mx[k][1], mx[k][2], mx[k][3]);
+        sh.u.cmax[slice][cg] = width_max(mx[0], mx[1], mx[2]);
     }
     __syncthreads();
     if (tid < DV) refit_colmax<DV>(sh, tid);

@@ -264,6 +264,8 @@ def test_decode_stack48_graph():
         for L in layers_checked:
             locks[L].check_step(step_inp[L], bufs[L]["o"], t)
         _say(f"stack48: replay {t} ok")
+    for L in layers_checked:
+        assert locks[L].mismatches <= PT.CODE_MISMATCH_FRAC * locks[L].compared
 
 
 def test_prepared_step_matches_checked_call():

@@ -111,7 +111,7 @@ def test_refit_ragged_shapes(case, kda):
                                                       f32(v).reshape(-1, dv), gt, f32(be).reshape(-1), w=wt,
                                                       want=("y", "c_range"), tie_window=PT.TIE_WINDOW)
     PT.compare_refit(got.reshape(-1, dk, dv)[tiles], gr.reshape(-1, dk)[tiles], gc.reshape(-1, dv)[tiles],
-                     new, rn, cn, ex["y"], ex["c_range"], f"ragged refit case {case}")
+                     new, rn, cn, ex["y"], ex["c_range"], tb_all[tiles], f"ragged refit case {case}")
     PT.compare_out(o.cpu().numpy().reshape(-1, dv), o_ref)
     untouched = np.setdiff1d(np.arange(n_slots), sel)
     for s in untouched:
