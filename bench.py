@@ -29,19 +29,37 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+# fp32 VALU operations without packed math: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# fp32 operations per state element of one step, counted from the method in
+# its code-space form (each convert, add, multiply, FMA, max, round, clamp or
+# pack counts one): decode 1, S^T k and S^T q 2, new value 2, requantize 4;
+# the refit adds the row-magnitude sum 1, rescale 1, column max 1, fixed code
+# 2 and the two least-squares sums 3.
+OPS_PER_ELEMENT = {False: 9, True: 17}
 METRIC = "state-updates/s and achieved HBM GB/s (% of peak), B=512 heads=32 dk=dv=128"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode_pool_b512.json")
-KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_38169_amd", "csrc", f)
-               for f in ("stepq_device.h", "stepq_internal.h", "stepq_kernels.hip")]
+CSRC = os.path.join(ROOT, "paper_2609_38169_amd", "csrc")
+
+
+def traffic_file(refit: bool, kda: bool) -> str:
+    name = ("refit" if refit else "decode") + ("_kda" if kda else "")
+    return os.path.join(ROOT, "profiles", f"traffic_{name}_pool_b512.json")
+
+
+def kernel_sources(refit: bool):
+    return [os.path.join(CSRC, f) for f in
+            ("stepq_device.h", "stepq_internal.h", "stepq_refit.hip" if refit else "stepq_kernels.hip")]
 
 
 def log(msg: str):
     print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_hash() -> str:
+def kernel_hash(refit: bool = False) -> str:
+    """Hash of the sources of the timed kernel, to tell whether committed
+    counter summaries were taken on it."""
     h = hashlib.sha256()
-    for f in KERNEL_SRCS:
+    for f in kernel_sources(refit):
         h.update(open(f, "rb").read())
     return h.hexdigest()[:16]
 
@@ -93,16 +111,18 @@ def cpu_baseline(w, bits, seconds: float):
                       f"{elapsed:.1f} s of oracle time (4 distinct input steps cycled, draws excluded)"}
 
 
-def traffic_entry(launch_bytes):
-    """HBM traffic per launch from committed rocprofv3 counter summaries, if
-    they were taken on the current kernel source."""
+def traffic_entry(refit: bool, kda: bool):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
+    copy's counters) from the committed rocprofv3 summary of this kernel and
+    mode, if it was taken on the current kernel source; else None."""
     try:
-        t = json.load(open(TRAFFIC_FILE))
+        t = json.load(open(traffic_file(refit, kda)))
     except (OSError, ValueError):
         return None
-    if t.get("kernel_sha") != kernel_hash():
+    if t.get("kernel_sha") != kernel_hash(refit):
         return None
-    return t.get("bytes_per_launch")
+    b = t.get("bytes_per_launch")
+    return b.get("total") if isinstance(b, dict) else b
 
 
 def main():
@@ -198,6 +218,7 @@ def main():
     act_bytes = w.batch * (2 * w.n_qk_heads * w.d_k * 2 + w.n_v_heads * w.d_v * 2 + (gate_elems + w.n_v_heads) * 2
                            + w.n_v_heads * w.d_v * 4 + 4)
     achieved = launch_bytes / (kern_ms * 1e-3) / 1e9
+    valu_tops = w.batch * w.n_v_heads * w.d_k * w.d_v * OPS_PER_ELEMENT[args.refit] / (kern_ms * 1e-3) / 1e12
     value = tiles * K / (total_ms * 1e-3)
 
     line = {
@@ -227,7 +248,9 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": None if (args.kda or args.refit) else traffic_entry(launch_bytes),
+            "traffic": traffic_entry(args.refit, args.kda),
+            "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Top/s", "frac": valu_tops / VALU_PEAK_TOPS,
+                     "ops_per_element": OPS_PER_ELEMENT[args.refit]},
             "kernel": ("refit_kernel" if args.refit else "decode_kernel") + ("<128, bf16, kda>" if args.kda
                                                                               else "<128, bf16>"),
             "kernel_ms_mean": kern_ms,
@@ -235,11 +258,18 @@ def main():
                                       "max": float(np.max(per_launch_ms)), "per_slot_subset": per_subset},
             "bytes_per_launch": launch_bytes,
             "activation_bytes_per_launch": act_bytes,
-            "kernel_sha": kernel_hash(),
+            "kernel_sha": kernel_hash(args.refit),
         },
         "setup_s": setup_s,
 
     }
+    if args.refit:
+        # the refit step is bound by fp32 VALU work, not by HBM: that roofline is the primary one
+        rl = line["roofline"]
+        hbm = {k: rl[k] for k in ("achieved", "peak", "unit", "frac")}
+        valu = rl.pop("valu")
+        rl.update({"bound": "alu", "achieved": valu["achieved"], "peak": valu["peak"], "unit": valu["unit"],
+                   "frac": valu["frac"], "ops_per_element": valu["ops_per_element"], "hbm": hbm})
     if args.copy_ref:
         src = torch.empty(launch_bytes // 2, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
