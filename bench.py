@@ -36,7 +36,8 @@ VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 # pack counts one): decode 1, S^T k and S^T q 2, new value 2, requantize 4;
 # the refit adds the row-magnitude sum 1, rescale 1, column max 1, fixed code
 # 2 and the two least-squares sums 3.
-OPS_PER_ELEMENT = {False: 9, True: 17}
+# The row-absmax baseline adds the row maximum 1 and the rescale 1.
+OPS_PER_ELEMENT = {False: 9, True: 17, "row_absmax": 11}
 METRIC = "state-updates/s and achieved HBM GB/s (% of peak), B=512 heads=32 dk=dv=128"
 CSRC = os.path.join(ROOT, "paper_2609_38169_amd", "csrc")
 
@@ -47,8 +48,9 @@ def traffic_file(refit: bool, kda: bool) -> str:
 
 
 def kernel_sources(refit: bool):
-    return [os.path.join(CSRC, f) for f in
-            ("stepq_device.h", "stepq_internal.h", "stepq_refit.hip" if refit else "stepq_kernels.hip")]
+    files = ["stepq_device.h", "stepq_internal.h"]
+    files += ["stepq_refit_body.h", "stepq_refit.hip"] if refit else ["stepq_kernels.hip"]
+    return [os.path.join(CSRC, f) for f in files]
 
 
 def log(msg: str):
@@ -136,8 +138,15 @@ def main():
     ap.add_argument("--copy-ref", action="store_true", help="also time a plain device copy of the same bytes")
     ap.add_argument("--kda", action="store_true", help="channel-wise (KDA) gates [B][Hv][d_k] instead of alpha")
     ap.add_argument("--refit", action="store_true", help="online dual-axis refit of the scales in every step")
+    ap.add_argument("--row-absmax", action="store_true",
+                    help="requantize as the row-wise absmax INT-b baseline (row factors refit, column factors 1)")
     args = ap.parse_args()
 
+    if args.refit and args.row_absmax:
+        print("--refit and --row-absmax exclude each other", file=sys.stderr)
+        sys.exit(2)
+    mode = True if args.refit else ("row_absmax" if args.row_absmax else False)
+    rescale = bool(mode)          # the step writes the scales back
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (each (request, head) tile is "
               "independent; see the sharding note in DESIGN.md). Run with --gpus 1.", file=sys.stderr)
@@ -175,7 +184,7 @@ def main():
             inp = inputs[key[0]]
             prepared[key] = pool.prepare_step(subsets[key[1]], inp["q"], inp["k"], inp["v"], inp["alpha"],
                                               inp["beta"], o, stream=torch.cuda.current_stream(),
-                                              refit=args.refit)
+                                              refit=mode)
         prepared[key]()
 
     log(f"pool and inputs ready in {time.perf_counter() - t_setup:.1f} s; timing")
@@ -212,13 +221,13 @@ def main():
                   for j in range(nsub)]
 
     tiles = w.tiles_per_step
-    per_tile = [state_bytes_per_tile(bits[h], w.d_k, w.d_v, args.refit) for h in range(w.n_v_heads)]
+    per_tile = [state_bytes_per_tile(bits[h], w.d_k, w.d_v, rescale) for h in range(w.n_v_heads)]
     launch_bytes = w.batch * sum(per_tile)
     gate_elems = w.n_v_heads * (w.d_k if args.kda else 1)
     act_bytes = w.batch * (2 * w.n_qk_heads * w.d_k * 2 + w.n_v_heads * w.d_v * 2 + (gate_elems + w.n_v_heads) * 2
                            + w.n_v_heads * w.d_v * 4 + 4)
     achieved = launch_bytes / (kern_ms * 1e-3) / 1e9
-    valu_tops = w.batch * w.n_v_heads * w.d_k * w.d_v * OPS_PER_ELEMENT[args.refit] / (kern_ms * 1e-3) / 1e12
+    valu_tops = w.batch * w.n_v_heads * w.d_k * w.d_v * OPS_PER_ELEMENT[mode] / (kern_ms * 1e-3) / 1e12
     value = tiles * K / (total_ms * 1e-3)
 
     line = {
@@ -239,7 +248,8 @@ def main():
                    "slot_rotation": 1 if args.resident else len(subsets),
                    "cache_resident": bool(args.resident),
                    "gate": "channel-wise d [B][Hv][d_k] (KDA)" if args.kda else "scalar alpha [B][Hv] (GDN)",
-                   "scales": "online dual-axis refit every step" if args.refit else "frozen"},
+                   "scales": {True: "online dual-axis refit every step", "row_absmax": "row-wise absmax every step "
+                              "(INT-b baseline)", False: "frozen"}[mode]},
         "GBps_state": launch_bytes * K / (total_ms * 1e-3) / 1e9,
         "pct_hbm_peak": 100.0 * launch_bytes * K / (total_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
         "roofline": {
@@ -248,17 +258,17 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic_entry(args.refit, args.kda),
+            "traffic": traffic_entry(args.refit, args.kda) if not args.row_absmax else None,
             "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Top/s", "frac": valu_tops / VALU_PEAK_TOPS,
-                     "ops_per_element": OPS_PER_ELEMENT[args.refit]},
-            "kernel": ("refit_kernel" if args.refit else "decode_kernel") + ("<128, bf16, kda>" if args.kda
-                                                                              else "<128, bf16>"),
+                     "ops_per_element": OPS_PER_ELEMENT[mode]},
+            "kernel": ("refit_kernel" if rescale else "decode_kernel") + ("<128, bf16, kda" if args.kda else "<128, bf16")
+                      + {True: ", dual axis>", "row_absmax": ", row absmax>", False: ">"}[mode],
             "kernel_ms_mean": kern_ms,
             "launch_ms_event_pairs": {"mean": float(np.mean(per_launch_ms)), "min": float(np.min(per_launch_ms)),
                                       "max": float(np.max(per_launch_ms)), "per_slot_subset": per_subset},
             "bytes_per_launch": launch_bytes,
             "activation_bytes_per_launch": act_bytes,
-            "kernel_sha": kernel_hash(args.refit),
+            "kernel_sha": kernel_hash(rescale),
         },
         "setup_s": setup_s,
 

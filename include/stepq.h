@@ -147,7 +147,8 @@ stepq_status stepq_decode_step_kda(stepq_pool *pool, const int32_t *slot_ids, in
 /* Flags of stepq_decode_step_ex. */
 enum {
     STEPQ_STEP_KDA_GATE = 1u,  /* gate is the channel-wise d [batch][Hv][d_k] (KDA), else alpha [batch][Hv] */
-    STEPQ_STEP_REFIT = 2u      /* refit both scale vectors to the updated state before requantizing */
+    STEPQ_STEP_REFIT = 2u,     /* refit both scale vectors to the updated state before requantizing */
+    STEPQ_STEP_ROW_ABSMAX = 4u /* single-axis baseline: r'_i = max_j |X_ij|, c' = 1 (excludes REFIT) */
 };
 
 /* The decode step with optional channel-wise gate and online scale refit.
@@ -166,8 +167,12 @@ enum {
  *          a zero denominator keeps c_j
  *   q'_ij = clip(round(X_ij q_b / (r'_i c'_j)), -q_b, q_b)
  * r', c0 and c' are floored at 2^-60; r' and c' are written as the new fp32
- * scales.  The readout o is X^T q as without the flag.  Unknown flags:
- * STEPQ_E_INVALID. */
+ * scales.  The readout o is X^T q as without the flag.
+ * With STEPQ_STEP_ROW_ABSMAX the step requantizes as the symmetric row-wise
+ * absmax INT-b baseline the paper compares against (Section 5.1): per key
+ * row r'_i = max_j |X_ij| (floored at 2^-60), every c'_j = 1, and
+ *   q'_ij = clip(round(X_ij q_b / r'_i), -q_b, q_b).
+ * Unknown flags, or REFIT together with ROW_ABSMAX: STEPQ_E_INVALID. */
 stepq_status stepq_decode_step_ex(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
                                   const void *k, const void *v, const void *gate, const void *beta,
                                   stepq_dtype act_dtype, uint32_t flags, float *o, void *stream);

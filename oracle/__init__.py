@@ -54,6 +54,7 @@ def lib():
         L.orc_decode_step.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P]
         L.orc_decode_step_refit.argtypes = [i, i, i, P, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P,
                                             ctypes.c_double, P, P]
+        L.orc_decode_step_rowmax.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P]
         L.orc_tile_bytes.argtypes = [i, i, P]
         L.orc_tile_bytes.restype = ctypes.c_size_t
         L.orc_slot_bytes.argtypes = [i, i, i, P]
@@ -182,6 +183,26 @@ def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=(), 
     if lo is not None:
         extra["c_range"] = (lo, hi)
     return (out, r_out, c_out, o, extra) if want else (out, r_out, c_out, o)
+
+
+def decode_step_rowmax(codes, r, c, bits, q, k, v, alpha, beta, want_y=False):
+    """One decode step of the row-wise absmax INT-b baseline (Section 5.1) on
+    the same quantized tile: returns (codes, r, c, o[, y]) with r'_i =
+    max_j |X_ij| and c' = 1."""
+    codes = _c(codes, np.int8)
+    n, dk, dv = codes.shape
+    r, c, bits = _c(r, np.float32), _c(c, np.float32), _c(np.broadcast_to(bits, (n, dk)), np.uint8)
+    q, k, v = _c(q, np.float64), _c(k, np.float64), _c(v, np.float64)
+    a, per_row = _gates(alpha, n, dk)
+    beta = _c(beta, np.float64).reshape(n)
+    out = np.empty_like(codes)
+    r_out = np.empty((n, dk), np.float32)
+    c_out = np.empty((n, dv), np.float32)
+    o = np.empty((n, dv), np.float64)
+    y = np.empty((n, dk, dv), np.float64) if want_y else None
+    lib().orc_decode_step_rowmax(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(q), _p(k), _p(v), _p(a),
+                                 per_row, _p(beta), _p(out), _p(r_out), _p(c_out), _p(o), _p(y))
+    return (out, r_out, c_out, o, y) if want_y else (out, r_out, c_out, o)
 
 
 def tile_bytes(bits_row, d_v: int) -> int:

@@ -368,6 +368,62 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
 }
 
 /* ------------------------------------------------------------------------
+ * One decode step of the single-axis baseline the paper compares against
+ * (Section 5.1: symmetric row-wise absmax INT-b), on the same quantized
+ * tile: steps 1-3 of orc_decode_step, then per key row
+ *   r'_i = max_j |X_ij|  (floor 2^-60, stored fp32),   c'_j = 1,
+ *   q'_ij = clip(round(X_ij q_b / r'_i), -q_b, q_b)    with the stored r'.
+ * y (optional) receives X q_b / r' before rounding.
+ */
+void orc_decode_step_rowmax(int n_tiles, int dk, int dv, const int8_t *codes_in, const float *r,
+                            const float *c, const uint8_t *bits, const double *q, const double *k,
+                            const double *v, const double *alpha, int per_row, const double *beta,
+                            int8_t *codes_out, float *r_out, float *c_out, double *o, double *y)
+{
+    const double floor_ = ldexp(1.0, -60);
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int t = 0; t < n_tiles; ++t) {
+        size_t nel = (size_t)dk * dv;
+        double *Sh = (double *)malloc(sizeof(double) * nel);
+        double *X = (double *)malloc(sizeof(double) * nel);
+        double *gbuf = (double *)malloc(sizeof(double) * dk);
+        const int8_t *ci = codes_in + (size_t)t * nel;
+        const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
+        const uint8_t *bt = bits + (size_t)t * dk;
+        for (int i = 0; i < dk; ++i) {
+            double qb = qb_of(bt[i]);
+            for (int j = 0; j < dv; ++j)
+                Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / qb;
+        }
+        update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
+                    gate_of(alpha, per_row, t, dk, gbuf), beta[t], X, o + (size_t)t * dv);
+        for (int j = 0; j < dv; ++j) c_out[(size_t)t * dv + j] = 1.0f;
+        for (int i = 0; i < dk; ++i) {
+            double m = 0.0;
+            for (int j = 0; j < dv; ++j) {
+                double a = fabs(X[(size_t)i * dv + j]);
+                if (a > m) m = a;
+            }
+            if (m < floor_) m = floor_;
+            r_out[(size_t)t * dk + i] = (float)m;
+            double ri = (double)r_out[(size_t)t * dk + i];
+            double qb = qb_of(bt[i]);
+            for (int j = 0; j < dv; ++j) {
+                double s = X[(size_t)i * dv + j] * qb / ri;
+                if (y) y[(size_t)t * nel + (size_t)i * dv + j] = s;
+                double n = nearbyint(s);
+                if (n > qb) n = qb;
+                if (n < -qb) n = -qb;
+                codes_out[(size_t)t * nel + (size_t)i * dv + j] = (int8_t)n;
+            }
+        }
+        free(Sh);
+        free(X);
+        free(gbuf);
+    }
+}
+
+/* ------------------------------------------------------------------------
  * Pool layout, re-derived from its definition in include/stepq.h:
  *  - physical key-row order: the 8-bit rows in increasing logical index,
  *    then the 4-bit rows, then the 2-bit rows;

@@ -20,7 +20,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libstepq.so")
-HIP_SOURCES = ["stepq_host.hip", "stepq_kernels.hip", "stepq_refit.hip"]
+HIP_SOURCES = ["stepq_host.hip", "stepq_kernels.hip", "stepq_refit.hip", "stepq_rowmax.hip"]
 CXX_SOURCES = ["stepq_setup.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -287,8 +287,10 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     stepq_status st = common_checks(p, slot_ids, batch);
     if (st != STEPQ_OK) return st;
     if (act_dtype != STEPQ_F32 && act_dtype != STEPQ_BF16) return fail(STEPQ_E_INVALID, "unknown activation dtype");
-    if (flags & ~static_cast<uint32_t>(STEPQ_STEP_KDA_GATE | STEPQ_STEP_REFIT))
+    if (flags & ~static_cast<uint32_t>(STEPQ_STEP_KDA_GATE | STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX))
         return fail(STEPQ_E_INVALID, "unknown decode-step flags");
+    if ((flags & STEPQ_STEP_REFIT) && (flags & STEPQ_STEP_ROW_ABSMAX))
+        return fail(STEPQ_E_INVALID, "STEPQ_STEP_REFIT and STEPQ_STEP_ROW_ABSMAX exclude each other");
     if (batch == 0) return STEPQ_OK;
     if (!q || !k || !v || !gate || !beta || !o) return fail(STEPQ_E_INVALID, "NULL activation or output pointer");
     auto s = static_cast<hipStream_t>(stream);
@@ -305,9 +307,10 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     a.o = o;
     a.batch = batch;
     const bool diag = (flags & STEPQ_STEP_KDA_GATE) != 0;
-    hipError_t e = (flags & STEPQ_STEP_REFIT)
-                       ? stepq::launch_decode_refit(a, act_dtype == STEPQ_BF16, diag, p->layout, s)
-                       : stepq::launch_decode(a, act_dtype == STEPQ_BF16, diag, p->layout, s);
+    const bool bf16 = act_dtype == STEPQ_BF16;
+    hipError_t e = (flags & STEPQ_STEP_REFIT)        ? stepq::launch_decode_refit(a, bf16, diag, p->layout, s)
+                   : (flags & STEPQ_STEP_ROW_ABSMAX) ? stepq::launch_decode_rowmax(a, bf16, diag, p->layout, s)
+                                                     : stepq::launch_decode(a, bf16, diag, p->layout, s);
     return e == hipSuccess ? STEPQ_OK : hip_fail(e, "decode launch");
 }
 

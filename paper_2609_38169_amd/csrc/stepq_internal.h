@@ -90,6 +90,9 @@ hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_lay
 // vectors (the codes are requantized against the refitted scales, which
 // replace the stored ones).
 hipError_t launch_decode_refit(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);
+// The decode step with the single-axis baseline's requantization: row
+// factors r'_i = max_j |X_ij|, column factors 1.
+hipError_t launch_decode_rowmax(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);
 hipError_t launch_tile_op(const TileArgs &a, TileOp op, hipStream_t stream);
 
 }  // namespace stepq

@@ -1,545 +1,12 @@
-// Decode step with the online Key-Row-Aware Dual-Axis refit fused in
-// (paper: Section 4.3 row and column factors, the fixed-code column update
-// of Appendix C.1, Table C2 steps 4-6).  One 256-thread workgroup per
-// (request, value head) tile, as in the frozen-scale kernel, and the same
-// first half: unpack, S^T k and S^T q, residual, readout.
-//
-// Working unit.  Per element the frozen-scale body forms the unrounded new
-// code on the old scales,
-//     y_ij = X_ij q_b / (r_i c_j).
-// Every quantity of the refit is a row or column rescaling of y, so the tile
-// is still never formed in real units:
-//     m_i   = (r_i / (q_b d_v)) sum_j c_j |y_ij|       r'_i = (m_i / w_i)^(1/2)
-//     yh_ij = y_ij r_i / r'_i                         (= X_ij q_b / (r'_i c_j))
-//     c0_j  = c_j max_i |yh_ij| / q_b                 (absmax start)
-//     z_ij  = round(yh_ij c_j / c0_j)                 (fixed codes; |.| <= q_b)
-//     c'_j  = c_j sum_i W_i z_ij yh_ij / sum_i W_i z_ij^2,   W_i = (w_i r'_i / q_b)^2
-//     q'_ij = clip(round(yh_ij c_j / c'_j), -q_b, q_b)
-// Four passes over the thread's values with three LDS reductions between
-// them: row sums (over the lanes that share a row), column maxima (kept per
-// width in the thread, so that the scaling by 1/q_b happens once per column
-// and thread), and the column sums of the least-squares numerator and
-// denominator.  The new r' and c' overwrite
-// the tile's scales; a zero denominator keeps c_j.
-#include "stepq_device.h"
-
-#include <type_traits>
+// Launcher of the decode step with the online Key-Row-Aware Dual-Axis refit
+// (the kernel body is in stepq_refit_body.h).
+#include "stepq_refit_body.h"
 
 namespace stepq {
-namespace {
-
-constexpr float kScaleFloor = 0x1p-60f;
-
-template <int DV>
-struct RefitShared {
-    DecodeShared<DV> d;
-    union {
-        float rowp[kSlotTable][DV / 4];            // partials of sum_j c_j |y_ij| by row slot, per column lane
-        float4 cmax[256 / (DV / 4)][DV / 4];       // per slice column maxima of |yh| / q_b
-    } u;
-    float hrow[kSlotTable];                        // r_i / r'_i by row slot (0 for empty slots)
-    float wrow[kSlotTable];                        // W_i by row slot
-    float wphys[kMaxDk];                           // w by physical row
-    float ccol[DV];                                // previous c_j
-    float ecol[DV];                                // c_j / c0_j
-    float gcol[DV];                                // c_j / c'_j
-};
-
-// One row partial of a thread (4 columns of one row slot).
-template <int DV>
-__device__ __forceinline__ void put_row_partial(RefitShared<DV> &sh, int x, int cg, float acc)
-{
-    sh.u.rowp[x][cg] = acc;
-}
-
-// Row slot x (physical row p, width bw, old scale r_p): r' from the lane
-// partials, written to the tile; h and W to LDS.  The row and column
-// factors are formed with the hardware reciprocal and square root (about one
-// ulp each): every later step uses the stored fp32 values, so the codes stay
-// consistent with them.
-template <int DV>
-__device__ __forceinline__ void refit_row(RefitShared<DV> &sh, int x, int p, int bw, float r_p, float *rr_out)
-{
-    float sum = 0.f;
-#pragma unroll
-    for (int l = 0; l < DV / 4; l += 4) {
-        const float4 v4 = *reinterpret_cast<const float4 *>(&sh.u.rowp[x][l]);
-        sum += (v4.x + v4.y) + (v4.z + v4.w);
-    }
-    const float iq = bw == 8 ? (1.0f / 127.0f) : (bw == 4 ? (1.0f / 7.0f) : 1.0f);
-    const float m = (r_p * iq) * (sum * (1.0f / static_cast<float>(DV)));
-    const float w = sh.wphys[p];
-    const float rn = fmaxf(__builtin_amdgcn_sqrtf(m * __builtin_amdgcn_rcpf(w)), kScaleFloor);
-    sh.hrow[x] = r_p * __builtin_amdgcn_rcpf(rn);
-    const float t = (w * rn) * iq;
-    sh.wrow[x] = t * t;
-    rr_out[p] = rn;
-}
-
-// Per-thread column maxima of |yh| kept per width, divided by q_b once.
-__device__ __forceinline__ float4 width_max(const float (&m8)[4], const float (&m4)[4], const float (&m2)[4])
-{
-    float r[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) r[e] = fmaxf(fmaxf(m8[e] * (1.0f / 127.0f), m4[e] * (1.0f / 7.0f)), m2[e]);
-    return make_float4(r[0], r[1], r[2], r[3]);
-}
-
-// Column j: absmax start c0_j from the slice maxima; e_j = c_j / c0_j.
-template <int DV>
-__device__ __forceinline__ void refit_colmax(RefitShared<DV> &sh, int j)
-{
-    constexpr int NSL = 256 / (DV / 4);
-    const float *mx = reinterpret_cast<const float *>(&sh.u.cmax[0][0]);
-    float M = 0.f;
-#pragma unroll
-    for (int s = 0; s < NSL; ++s) M = fmaxf(M, mx[s * DV + j]);
-    const float cj = sh.ccol[j];
-    const float c0 = fmaxf(cj * M, kScaleFloor);
-    sh.ecol[j] = M > 0.f ? cj * __builtin_amdgcn_rcpf(c0) : 0.f;
-}
-
-// Column j: the least-squares column factor from the slice sums in d.red.
-template <int DV>
-__device__ __forceinline__ void refit_colfit(RefitShared<DV> &sh, int j, float *cc_out)
-{
-    constexpr int NSL = 256 / (DV / 4);
-    const float *rn = reinterpret_cast<const float *>(&sh.d.red[0][0][0]);
-    const float *rd = reinterpret_cast<const float *>(&sh.d.red[1][0][0]);
-    float num = rn[j], den = rd[j];
-#pragma unroll
-    for (int s = 1; s < NSL; ++s) {
-        num += rn[s * DV + j];
-        den += rd[s * DV + j];
-    }
-    const float cj = sh.ccol[j];
-    // num / den as a full division: den may be tiny for very small states
-    const float cn = den > 0.f ? fmaxf(cj * (num / den), kScaleFloor) : cj;
-    sh.gcol[j] = cj * __builtin_amdgcn_rcpf(cn);
-    cc_out[j] = cn;
-}
-
-// ---- per-word passes on values held in registers (4 columns x 8/B rows)
-
-// y of a word from its f16-packed fields; the row partial sum_e c_e |y| of
-// each slot goes to LDS.
-template <int B, bool DIAG>
-__device__ __forceinline__ void word_y(const uint32_t *U2, RefitShared<128> &sh, int x0, int cg, float al_w,
-                                       const float (&bc)[4], const float (&cc)[4], float *Y)
-{
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float a_s = sh.d.av[x0 + s];
-        const float al = DIAG ? sh.d.al[x0 + s] : al_w;
-        float *y = Y + 4 * s;
-        y[0] = fma_mix_e<0>(al, U2, s, a_s * bc[0]);
-        y[1] = fma_mix_e<1>(al, U2, s, a_s * bc[1]);
-        y[2] = fma_mix_e<2>(al, U2, s, a_s * bc[2]);
-        y[3] = fma_mix_e<3>(al, U2, s, a_s * bc[3]);
-        float acc = fabsf(y[0]) * cc[0];
-        acc = fmaf(fabsf(y[1]), cc[1], acc);
-        acc = fmaf(fabsf(y[2]), cc[2], acc);
-        put_row_partial<128>(sh, x0 + s, cg, fmaf(fabsf(y[3]), cc[3], acc));
-    }
-}
-
-template <int B>
-__device__ __forceinline__ void word_scale_max(float *Y, const float *hrow, int x0, float (&mx)[4])
-{
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float h = hrow[x0 + s];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            Y[4 * s + e] *= h;
-            mx[e] = fmaxf(mx[e], fabsf(Y[4 * s + e]));
-        }
-    }
-}
-
-template <int B>
-__device__ __forceinline__ void word_fit(const float *Y, const float *wrow, int x0, const float (&ec)[4],
-                                         float (&num)[4], float (&den)[4])
-{
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float W = wrow[x0 + s];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float yh = Y[4 * s + e];
-            const float z = __builtin_rintf(yh * ec[e]);
-            const float u = W * z;
-            num[e] = fmaf(u, yh, num[e]);
-            den[e] = fmaf(u, z, den[e]);
-        }
-    }
-}
-
-// New word: per field round(yh g_j) clamped to +-q_b, packed with a bias of
-// 2^(B-1) that the final XOR removes (as in the frozen-scale requantizer).
-template <int B>
-__device__ __forceinline__ uint32_t word_requant(const float *Y, const float (&g)[4])
-{
-    constexpr float bias = static_cast<float>(1 << (B - 1));
-    constexpr float top = static_cast<float>((1 << B) - 1);
-    constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
-    uint32_t out = 0;
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        uint32_t P = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            float y = fmaf(Y[4 * s + e], g[e], bias);
-            y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
-            P = __builtin_amdgcn_cvt_pk_u8_f32(y, e, P);
-        }
-        out |= P << (s * B);
-    }
-    return out ^ flip;
-}
-
-__device__ __forceinline__ void ld4(const float *p, float (&v)[4])
-{
-    const float4 t = *reinterpret_cast<const float4 *>(p);
-    v[0] = t.x;
-    v[1] = t.y;
-    v[2] = t.z;
-    v[3] = t.w;
-}
-
-// Uniform layouts at d_v = 128: widths known at compile time, all 64 values
-// of the thread kept in registers across the four passes.
-template <bool BF16, bool DIAG, int M8, int M4, int M2>
-__device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx &t, RefitShared<128> &sh)
-{
-    constexpr int M = M8 + M4 + M2;
-    constexpr int NE = 4 * (M8 + 2 * M4 + 4 * M2);
-    constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
-    constexpr int Y4 = 4 * M8, Y2 = 4 * M8 + 8 * M4;     // value offsets of the 4- and 2-bit words
-    const int tid = threadIdx.x;
-    const int cg = tid & 31, slice = tid >> 5;
-    float *rr_out = const_cast<float *>(t.rr);
-    float *cc_out = const_cast<float *>(t.cc);
-    uint32_t w[M];
-#pragma unroll
-    for (int m = 0; m < M; ++m) w[m] = __builtin_nontemporal_load(t.codes + tid + 256 * m);
-
-    const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    if (tid < 128) {
-        sh.ccol[tid] = op.c;
-        sh.wphys[tid] = a.pool.roww[t.h * 128 + tid];
-    }
-    const float kappa = row_constants_uniform<DIAG, M8, M4, 128>(t.beta, op, sh.d);
-
-    uint32_t U[NE / 2];
-    float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int m = 0; m < M8; ++m) unpack_acc_h<8>(w[m], sh.d.kq, slice + 8 * m, &U[2 * m], acK, acQ);
-#pragma unroll
-    for (int m = 0; m < M4; ++m)
-        unpack_acc_h<4>(w[M8 + m], sh.d.kq, X4 + 2 * (slice + 8 * m), &U[2 * M8 + 4 * m], acK, acQ);
-#pragma unroll
-    for (int m = 0; m < M2; ++m)
-        unpack_acc_h<2>(w[M8 + M4 + m], sh.d.kq, X2 + 4 * (slice + 8 * m), &U[2 * M8 + 4 * M4 + 8 * m], acK, acQ);
-
-    column_phase<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh.d, kappa, acK, acQ, op.c, op.v);
-
-    // pass 1: y on the old scales and the row partials
-    float bc[4], cc[4];
-    ld4(&sh.d.bcol[4 * cg], bc);
-    ld4(&sh.ccol[4 * cg], cc);
-    float Y[NE];
-#pragma unroll
-    for (int m = 0; m < M8; ++m) word_y<8, DIAG>(&U[2 * m], sh, slice + 8 * m, cg, t.alpha, bc, cc, &Y[4 * m]);
-#pragma unroll
-    for (int m = 0; m < M4; ++m)
-        word_y<4, DIAG>(&U[2 * M8 + 4 * m], sh, X4 + 2 * (slice + 8 * m), cg, t.alpha * (1.0f / 16.0f), bc, cc,
-                        &Y[Y4 + 8 * m]);
-#pragma unroll
-    for (int m = 0; m < M2; ++m)
-        word_y<2, DIAG>(&U[2 * M8 + 4 * M4 + 8 * m], sh, X2 + 4 * (slice + 8 * m), cg, t.alpha * (1.0f / 64.0f),
-                        bc, cc, &Y[Y2 + 16 * m]);
-    __syncthreads();
-    if (tid < 128) refit_row<128>(sh, tid, tid, tid < X4 ? 8 : (tid < X2 ? 4 : 2), op.r, rr_out);
-    __syncthreads();
-
-    // pass 2: yh = y r / r' and the column maxima per width
-    {
-        float mx8[4] = {0.f, 0.f, 0.f, 0.f}, mx4[4] = {0.f, 0.f, 0.f, 0.f}, mx2[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int m = 0; m < M8; ++m) word_scale_max<8>(&Y[4 * m], sh.hrow, slice + 8 * m, mx8);
-#pragma unroll
-        for (int m = 0; m < M4; ++m) word_scale_max<4>(&Y[Y4 + 8 * m], sh.hrow, X4 + 2 * (slice + 8 * m), mx4);
-#pragma unroll
-        for (int m = 0; m < M2; ++m) word_scale_max<2>(&Y[Y2 + 16 * m], sh.hrow, X2 + 4 * (slice + 8 * m), mx2);
-        sh.u.cmax[slice][cg] = width_max(mx8, mx4, mx2);
-    }
-    __syncthreads();
-    if (tid < 128) refit_colmax<128>(sh, tid);
-    __syncthreads();
-
-    // pass 3: fixed codes and the least-squares sums
-    {
-        float ec[4];
-        ld4(&sh.ecol[4 * cg], ec);
-        float num[4] = {0.f, 0.f, 0.f, 0.f}, den[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int m = 0; m < M8; ++m) word_fit<8>(&Y[4 * m], sh.wrow, slice + 8 * m, ec, num, den);
-#pragma unroll
-        for (int m = 0; m < M4; ++m) word_fit<4>(&Y[Y4 + 8 * m], sh.wrow, X4 + 2 * (slice + 8 * m), ec, num, den);
-#pragma unroll
-        for (int m = 0; m < M2; ++m) word_fit<2>(&Y[Y2 + 16 * m], sh.wrow, X2 + 4 * (slice + 8 * m), ec, num, den);
-        sh.d.red[0][slice][cg] = make_float4(num[0], num[1], num[2], num[3]);
-        sh.d.red[1][slice][cg] = make_float4(den[0], den[1], den[2], den[3]);
-    }
-    __syncthreads();
-    if (tid < 128) refit_colfit<128>(sh, tid, cc_out);
-    __syncthreads();
-
-    // pass 4: requantize on the new scales, store in place
-    float g[4];
-    ld4(&sh.gcol[4 * cg], g);
-#pragma unroll
-    for (int m = 0; m < M8; ++m) __builtin_nontemporal_store(word_requant<8>(&Y[4 * m], g), t.codes + tid + 256 * m);
-#pragma unroll
-    for (int m = 0; m < M4; ++m)
-        __builtin_nontemporal_store(word_requant<4>(&Y[Y4 + 8 * m], g), t.codes + tid + 256 * (M8 + m));
-#pragma unroll
-    for (int m = 0; m < M2; ++m)
-        __builtin_nontemporal_store(word_requant<2>(&Y[Y2 + 16 * m], g), t.codes + tid + 256 * (M8 + M4 + m));
-}
-
-// ---- any row-width mix and d_v: the words stay packed in registers and
-// each pass unpacks them again.
-
-template <int B, bool DIAG, int DV>
-__device__ __forceinline__ void gen_word_y(uint32_t w, const DecodeShared<DV> &d, int x0, float alpha,
-                                           const float (&bc)[4], float (&Y)[16])
-{
-    float U[16];
-    unpack_word<B>(w, U);
-    const float al_w = alpha * (B == 8 ? 1.0f : (B == 4 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float a_s = d.av[x0 + s];
-        const float al = DIAG ? d.al[x0 + s] : al_w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) Y[4 * s + e] = fmaf(al, U[4 * s + e], a_s * bc[e]);
-    }
-}
-
-// Calls f(width constant, group geometry, word index) for every word of the
-// thread that holds codes.
-template <int DV, class F>
-__device__ __forceinline__ void each_word(const TileCtx &t, int slice, F &&f)
-{
-    constexpr int NSL = 256 / (DV / 4);
-    constexpr int MMAX = kMaxDk * (DV / 4) / 256;
-    const int ngroups = static_cast<int>(t.hi.groups);
-#pragma unroll
-    for (int m = 0; m < MMAX; ++m) {
-        const int g = slice + NSL * m;
-        if (g < ngroups) {
-            const GroupRows gr = group_rows(t.hi, g);
-            if (gr.bits == 8) f(std::integral_constant<int, 8>(), gr, m);
-            else if (gr.bits == 4) f(std::integral_constant<int, 4>(), gr, m);
-            else f(std::integral_constant<int, 2>(), gr, m);
-        }
-    }
-}
-
-template <bool BF16, bool DIAG, int DV>
-__device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx &t, RefitShared<DV> &sh)
-{
-    constexpr int CG = DV / 4;
-    constexpr int NSL = 256 / CG;
-    constexpr int MMAX = kMaxDk * CG / 256;
-    const int tid = threadIdx.x;
-    const int cg = tid % CG, slice = tid / CG;
-    const int ngroups = static_cast<int>(t.hi.groups);
-    const int dk = a.pool.dk;
-    float *rr_out = const_cast<float *>(t.rr);
-    float *cc_out = const_cast<float *>(t.cc);
-    uint32_t w[MMAX];
-#pragma unroll
-    for (int m = 0; m < MMAX; ++m) {
-        const int g = slice + NSL * m;
-        w[m] = g < ngroups ? __builtin_nontemporal_load(t.codes + tid + 256 * m) : 0u;
-    }
-    const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    if (tid < DV) sh.ccol[tid] = op.c;
-    if (tid < dk) sh.wphys[tid] = a.pool.roww[t.h * dk + tid];
-    const float kappa = row_constants<DIAG, DV>(t.hi, dk, t.beta, op, sh.d);
-
-    float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
-    each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {
-        float U[16];
-        unpack_acc<decltype(bw)::value>(w[m], sh.d.kq, gr.x0, U, acK, acQ);
-    });
-    column_phase<DV>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh.d, kappa, acK, acQ, op.c, op.v);
-
-    float bc[4], cc[4];
-    ld4(&sh.d.bcol[4 * cg], bc);
-    ld4(&sh.ccol[4 * cg], cc);
-
-    // pass 1: row partials straight to LDS (each (lane, slot) has one writer)
-    each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {
-        constexpr int B = decltype(bw)::value;
-        float Y[16];
-        gen_word_y<B, DIAG, DV>(w[m], sh.d, gr.x0, t.alpha, bc, Y);
-#pragma unroll
-        for (int s = 0; s < 8 / B; ++s) {
-            float acc = fabsf(Y[4 * s]) * cc[0];
-            acc = fmaf(fabsf(Y[4 * s + 1]), cc[1], acc);
-            acc = fmaf(fabsf(Y[4 * s + 2]), cc[2], acc);
-            put_row_partial<DV>(sh, gr.x0 + s, cg, fmaf(fabsf(Y[4 * s + 3]), cc[3], acc));
-        }
-    });
-    __syncthreads();
-    if (tid < kSlotTable) {
-        int bw;
-        const int p = slot_row(t.hi, tid, bw);
-        if (p >= 0) {
-            refit_row<DV>(sh, tid, p, bw, sh.d.sr[p], rr_out);
-        } else {
-            sh.hrow[tid] = 0.f;
-            sh.wrow[tid] = 0.f;
-        }
-    }
-    __syncthreads();
-
-    // pass 2: column maxima of |yh| per width
-    {
-        float mx[3][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-        each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {
-            constexpr int B = decltype(bw)::value;
-            constexpr int K = B == 8 ? 0 : (B == 4 ? 1 : 2);
-            float Y[16];
-            gen_word_y<B, DIAG, DV>(w[m], sh.d, gr.x0, t.alpha, bc, Y);
-#pragma unroll
-            for (int s = 0; s < 8 / B; ++s) {
-                const float h = sh.hrow[gr.x0 + s];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) mx[K][e] = fmaxf(mx[K][e], fabsf(Y[4 * s + e] * h));
-            }
-        });
-        sh.u.cmax[slice][cg] = width_max(mx[0], mx[1], mx[2]);
-    }
-    __syncthreads();
-    if (tid < DV) refit_colmax<DV>(sh, tid);
-    __syncthreads();
-
-    // pass 3: fixed codes, least-squares sums
-    {
-        float ec[4];
-        ld4(&sh.ecol[4 * cg], ec);
-        float num[4] = {0.f, 0.f, 0.f, 0.f}, den[4] = {0.f, 0.f, 0.f, 0.f};
-        each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {
-            constexpr int B = decltype(bw)::value;
-            float Y[16];
-            gen_word_y<B, DIAG, DV>(w[m], sh.d, gr.x0, t.alpha, bc, Y);
-#pragma unroll
-            for (int s = 0; s < 8 / B; ++s) {
-                const float h = sh.hrow[gr.x0 + s];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) Y[4 * s + e] *= h;
-            }
-            word_fit<B>(Y, sh.wrow, gr.x0, ec, num, den);
-        });
-        sh.d.red[0][slice][cg] = make_float4(num[0], num[1], num[2], num[3]);
-        sh.d.red[1][slice][cg] = make_float4(den[0], den[1], den[2], den[3]);
-    }
-    __syncthreads();
-    if (tid < DV) refit_colfit<DV>(sh, tid, cc_out);
-    __syncthreads();
-
-    // pass 4: requantize and store
-    float g[4];
-    ld4(&sh.gcol[4 * cg], g);
-    each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {
-        constexpr int B = decltype(bw)::value;
-        float Y[16];
-        gen_word_y<B, DIAG, DV>(w[m], sh.d, gr.x0, t.alpha, bc, Y);
-#pragma unroll
-        for (int s = 0; s < 8 / B; ++s) {
-            const float h = sh.hrow[gr.x0 + s];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) Y[4 * s + e] *= h;
-        }
-        __builtin_nontemporal_store(word_requant<B>(Y, g), t.codes + tid + 256 * m);
-    });
-}
-
-template <int DV, bool BF16, int LAYOUT, bool DIAG>
-__global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
-{
-    __shared__ RefitShared<DV> sh;
-    const PoolView &P = a.pool;
-    TileCtx t;
-    t.tile = xcd_tile(blockIdx.x, a.batch * P.Hv);
-    t.b = fdiv(t.tile, P.div_hv);
-    t.h = t.tile - t.b * P.Hv;
-    t.hq = fdiv(t.h, P.div_g);
-    const int slot = a.slot_ids[t.b];
-    t.alpha = DIAG ? 1.0f : act_ld<BF16>(a.alpha, t.tile);
-    t.beta = act_ld<BF16>(a.beta, t.tile);
-    if constexpr (DV == 128 && LAYOUT > 0) {
-        constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
-        constexpr uint32_t r_off = 1024u * (u.m8 + u.m4 + u.m2);
-        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes +
-                       static_cast<uint64_t>(t.h) * (r_off + 1024u);
-        t.codes = reinterpret_cast<uint32_t *>(rec);
-        t.rr = reinterpret_cast<const float *>(rec + r_off);
-        t.cc = t.rr + 128;
-        refit_uniform<BF16, DIAG, u.m8, u.m4, u.m2>(a, t, sh);
-    } else {
-        t.hi = P.heads[t.h];
-        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.hi.tile_off;
-        t.codes = reinterpret_cast<uint32_t *>(rec);
-        t.rr = reinterpret_cast<const float *>(rec + t.hi.r_off);
-        t.cc = t.rr + P.dk;
-        if constexpr (DV == 128) {
-            switch (t.hi.layout) {
-            case 1: refit_uniform<BF16, DIAG, 8, 4, 0>(a, t, sh); return;
-            case 2: refit_uniform<BF16, DIAG, 4, 2, 2>(a, t, sh); return;
-            case 3: refit_uniform<BF16, DIAG, 16, 0, 0>(a, t, sh); return;
-            case 4: refit_uniform<BF16, DIAG, 0, 8, 0>(a, t, sh); return;
-            case 5: refit_uniform<BF16, DIAG, 0, 0, 4>(a, t, sh); return;
-            default: break;
-            }
-        }
-        refit_generic<BF16, DIAG, DV>(a, t, sh);
-    }
-}
-
-template <bool BF16, bool DIAG>
-hipError_t launch_refit_any(const DecodeArgs &a, int layout, unsigned grid, hipStream_t s)
-{
-    if (a.pool.dv == 128) {
-        switch (layout) {
-        case 1: hipLaunchKernelGGL((refit_kernel<128, BF16, 1, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
-        case 2: hipLaunchKernelGGL((refit_kernel<128, BF16, 2, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
-        case 3: hipLaunchKernelGGL((refit_kernel<128, BF16, 3, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
-        case 4: hipLaunchKernelGGL((refit_kernel<128, BF16, 4, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
-        case 5: hipLaunchKernelGGL((refit_kernel<128, BF16, 5, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
-        default: hipLaunchKernelGGL((refit_kernel<128, BF16, 0, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
-        }
-    } else {
-        hipLaunchKernelGGL((refit_kernel<64, BF16, 0, DIAG>), dim3(grid), dim3(256), 0, s, a);
-    }
-    return hipGetLastError();
-}
-
-}  // namespace
 
 hipError_t launch_decode_refit(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream)
 {
-    const unsigned grid = static_cast<unsigned>(a.batch) * static_cast<unsigned>(a.pool.Hv);
-    if (grid == 0) return hipSuccess;
-    if (bf16) return diag ? launch_refit_any<true, true>(a, pool_layout, grid, stream)
-                          : launch_refit_any<true, false>(a, pool_layout, grid, stream);
-    return diag ? launch_refit_any<false, true>(a, pool_layout, grid, stream)
-                : launch_refit_any<false, false>(a, pool_layout, grid, stream);
+    return launch_refit_mode<Refit::DualAxis>(a, bf16, diag, pool_layout, stream);
 }
 
 }  // namespace stepq

@@ -20,7 +20,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("STEPQ_LIB") or os.path.join(_HERE, "libstepq.so")
 
 STEPQ_F32, STEPQ_BF16 = 0, 1
-STEPQ_STEP_KDA_GATE, STEPQ_STEP_REFIT = 1, 2
+STEPQ_STEP_KDA_GATE, STEPQ_STEP_REFIT, STEPQ_STEP_ROW_ABSMAX = 1, 2, 4
 _STATUS = {0: "STEPQ_OK", 1: "STEPQ_E_INVALID", 2: "STEPQ_E_UNSUPPORTED", 3: "STEPQ_E_NOMEM", 4: "STEPQ_E_HIP"}
 
 EXPORTED = (
@@ -157,15 +157,17 @@ class Pool:
     def load(self, slot_ids, state, r, c, stream=None):
         stepq_pool_load(self, slot_ids, state, r, c, stream)
 
+    # refit: False (frozen scales), True (dual-axis refit) or "row_absmax"
+    # (the single-axis INT-b baseline)
     def step(self, slot_ids, q, k, v, alpha, beta, o, stream=None, refit=False):
         if refit:
-            stepq_decode_step_ex(self, slot_ids, q, k, v, alpha, beta, o, STEPQ_STEP_REFIT, stream)
+            stepq_decode_step_ex(self, slot_ids, q, k, v, alpha, beta, o, _refit_flags(refit), stream)
         else:
             stepq_decode_step(self, slot_ids, q, k, v, alpha, beta, o, stream)
 
     def step_kda(self, slot_ids, q, k, v, gate, beta, o, stream=None, refit=False):
         if refit:
-            stepq_decode_step_ex(self, slot_ids, q, k, v, gate, beta, o, STEPQ_STEP_KDA_GATE | STEPQ_STEP_REFIT,
+            stepq_decode_step_ex(self, slot_ids, q, k, v, gate, beta, o, STEPQ_STEP_KDA_GATE | _refit_flags(refit),
                                  stream)
         else:
             stepq_decode_step_kda(self, slot_ids, q, k, v, gate, beta, o, stream)
@@ -183,7 +185,7 @@ class Pool:
         args = _step_args(self, slot_ids, q, k, v, alpha, beta, o, stream, kda)
         keep = (slot_ids, q, k, v, alpha, beta, o)      # the tensors must outlive the callable
         if refit:
-            flags = ctypes.c_uint32(STEPQ_STEP_REFIT | (STEPQ_STEP_KDA_GATE if kda else 0))
+            flags = ctypes.c_uint32(_refit_flags(refit) | (STEPQ_STEP_KDA_GATE if kda else 0))
             fn = lib().stepq_decode_step_ex
             args = args[:9] + (flags,) + args[9:]
         else:
@@ -233,6 +235,14 @@ def stepq_pool_load(pool: Pool, slot_ids, state, r, c, stream=None):
         _dev(state, "state", torch.float32, (n, P.Hv, P.dk, P.dv), P.device),
         _dev(r, "r", torch.float32, (n, P.Hv, P.dk), P.device),
         _dev(c, "c", torch.float32, (n, P.Hv, P.dv), P.device), _stream(stream)))
+
+
+def _refit_flags(refit) -> int:
+    if refit is True:
+        return STEPQ_STEP_REFIT
+    if refit == "row_absmax":
+        return STEPQ_STEP_ROW_ABSMAX
+    raise ValueError(f"refit must be False, True or 'row_absmax', not {refit!r}")
 
 
 def _step_args(pool: Pool, slot_ids, q, k, v, gate, beta, o, stream, kda: bool):

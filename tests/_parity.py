@@ -179,7 +179,19 @@ class Lockstep:
         w = self.w
         q, k, v, a, b = oracle_inputs(w, inp, self.rows)
         g_codes, g_r, g_c = self.export()
-        if self.refit:
+        if self.refit == "row_absmax":
+            new, rn, cn, o, y = oracle.decode_step_rowmax(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b,
+                                                          want_y=True)
+            g_c = g_c.reshape(cn.shape)
+            assert np.all(g_c == 1.0), "row-absmax step: column factors must all be 1"
+            ones = np.ones(cn.shape, np.float64)
+            nb, _ = compare_refit(g_codes, g_r.reshape(rn.shape), g_c, new, rn, cn, y, (ones, ones),
+                                  self.tile_bits, f"layer {self.layer} step {step} row absmax",
+                                  frac=STEP_MISMATCH_FRAC)
+            self.mismatches += nb
+            self.r, self.c = rn, cn
+            self.compared += g_codes.size
+        elif self.refit:
             new, rn, cn, o, ex = oracle.decode_step_refit(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b,
                                                           w=self.row_w, want=("y", "c_range"), tie_window=TIE_WINDOW)
             nb, tc = compare_refit(g_codes, g_r.reshape(rn.shape), g_c.reshape(cn.shape), new, rn, cn,
@@ -234,7 +246,8 @@ def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, 
         ls.check_step(inp, o, t)
     assert ls.mismatches <= CODE_MISMATCH_FRAC * ls.compared, \
         f"{ls.mismatches} of {ls.compared} codes differ over the run"
-    say(f"lockstep {w.name}{' kda' if kda else ''}{' refit' if refit else ''}: {steps} steps ok, "
+    mode = {False: "", True: " refit", "row_absmax": " row-absmax"}[refit]
+    say(f"lockstep {w.name}{' kda' if kda else ''}{mode}: {steps} steps ok, "
         f"code mismatches {ls.mismatches}, columns on another tie rounding {ls.tie_cols}, "
         f"saturated {ls.saturated:.3f}")
     return ls

@@ -605,3 +605,37 @@ def test_refit_column_range_encloses_every_tie_rounding():
     *_, ex0 = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w, want=("c_range",), tie_window=0.0)
     lo0, hi0 = ex0["c_range"]
     assert np.array_equal(lo0, hi0) and np.array_equal(lo0.astype(np.float32), cn)
+
+
+# ---------------------------------------------------------------- row-wise absmax INT-b baseline (Section 5.1)
+@pytest.mark.parametrize("kda", [False, True])
+def test_rowmax_baseline_closed_form(kda):
+    """r'_i is the row's largest |X_ij| (computed here from X of the pinned
+    update), c' = 1, the largest entry of every row lands on +-q_b, and no
+    entry is off by more than half a level r'/(2 q_b)."""
+    codes, r, c, bits, q, k, v, g, beta, _ = _refit_case(seed=40, kda=kda)
+    out, rn, cn, o = oracle.decode_step_rowmax(codes, r, c, bits, q, k, v, g, beta)
+    S = oracle.dequant(codes, r, c, bits)
+    X, o_ref = oracle.update_fp(S, q, k, v, g, beta)
+    np.testing.assert_allclose(rn, np.abs(X).max(axis=2), rtol=6e-8, atol=0)
+    assert np.all(cn == 1.0)
+    qb = (2.0 ** (bits.astype(np.int64) - 1) - 1)[:, :, None]
+    am = np.abs(X).argmax(axis=2)
+    top = np.take_along_axis(out, am[:, :, None], axis=2)[:, :, 0]
+    assert np.array_equal(np.abs(top), qb[:, :, 0].astype(np.int8))
+    Xh = rn.astype(np.float64)[:, :, None] * out / qb
+    assert np.all(np.abs(Xh - X) <= rn.astype(np.float64)[:, :, None] / (2 * qb) * (1 + 1e-6))
+    assert np.array_equal(o, o_ref)
+
+
+def test_rowmax_baseline_is_refit_free_of_columns():
+    """With all column factors 1 the row-absmax requantization is the
+    quantizer (pinned above) with r = row max and c = 1; scaling a row of
+    the state scales its r' and leaves its codes (power of two: exactly)."""
+    codes, r, c, bits, q, k, v, g, beta, _ = _refit_case(seed=41)
+    out, rn, cn, _, y = oracle.decode_step_rowmax(codes, r, c, bits, q, k, v, g, beta, want_y=True)
+    S = oracle.dequant(codes, r, c, bits)
+    X, _ = oracle.update_fp(S, q, k, v, g, beta)
+    assert np.array_equal(out, oracle.quantize(X, rn, cn, bits))
+    up = oracle.decode_step_rowmax(codes, 4 * r, c, bits, q, k, 4 * v, g, beta)
+    assert np.array_equal(up[0], out) and np.array_equal(up[1], 4 * rn)
