@@ -47,20 +47,22 @@ def lib():
         L = ctypes.CDLL(_LIB_PATH)
         P = ctypes.c_void_p
         i = ctypes.c_int
-        L.orc_fit_absmax.argtypes = [i, i, i, P, P, P, P]
-        L.orc_quantize.argtypes = [i, i, i, P, P, P, P, P, P]
-        L.orc_dequant.argtypes = [i, i, i, P, P, P, P, P]
+        L.orc_fit_absmax.argtypes = [i, i, i, P, P, P, P, P]
+        L.orc_quantize.argtypes = [i, i, i, P, P, P, P, P, P, P]
+        L.orc_dequant.argtypes = [i, i, i, P, P, P, P, P, P]
         L.orc_update_fp.argtypes = [i, i, i, P, P, P, P, P, i, P, P, P]
-        L.orc_decode_step.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P]
+        L.orc_decode_step.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P]
         L.orc_decode_step_refit.argtypes = [i, i, i, P, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P,
-                                            ctypes.c_double, P, P]
-        L.orc_decode_step_rowmax.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P]
+                                            ctypes.c_double, P, P, P, P]
+        L.orc_decode_step_rowmax.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P]
+        L.orc_half_to_double.argtypes = [ctypes.c_size_t, P, P]
+        L.orc_double_to_half.argtypes = [ctypes.c_size_t, P, P]
         L.orc_tile_bytes.argtypes = [i, i, P]
         L.orc_tile_bytes.restype = ctypes.c_size_t
         L.orc_slot_bytes.argtypes = [i, i, i, P]
         L.orc_slot_bytes.restype = ctypes.c_size_t
-        L.orc_pack_pool.argtypes = [i, i, i, i, P, P, P, P, P]
-        L.orc_unpack_pool.argtypes = [i, i, i, i, P, P, P, P, P]
+        L.orc_pack_pool.argtypes = [i, i, i, i, P, P, P, P, P, P]
+        L.orc_unpack_pool.argtypes = [i, i, i, i, P, P, P, P, P, P]
         L.orc_max_threads.restype = ctypes.c_int
         _lib = L
     return _lib
@@ -78,17 +80,49 @@ def max_threads() -> int:
     return int(lib().orc_max_threads())
 
 
+# FP16 pivot rows (width 16): their values travel as binary16 bit patterns,
+# pv [n][dk][dv] uint16 (only pivot rows read or written).  Every function
+# below that takes a bit map with pivot rows needs pv and returns the new pv
+# as its last result.
+def _has_pivots(bits) -> bool:
+    return bool(np.any(np.asarray(bits) == 16))
+
+
+def _pv_in(pv, bits, shape):
+    if not _has_pivots(bits):
+        return None
+    if pv is None:
+        raise ValueError("the bit map has pivot rows: pass their binary16 values as pv")
+    return _c(np.broadcast_to(pv, shape), np.uint16)
+
+
+def half_to_double(h):
+    h = _c(h, np.uint16)
+    out = np.empty(h.shape, np.float64)
+    lib().orc_half_to_double(h.size, _p(h), _p(out))
+    return out
+
+
+def double_to_half(x):
+    x = _c(x, np.float64)
+    out = np.empty(x.shape, np.uint16)
+    lib().orc_double_to_half(x.size, _p(x), _p(out))
+    return out
+
+
 # ---------------------------------------------------------------------------
 # numeric entry points (shapes: tiles flattened to a leading n)
-def fit_absmax(S, w=None):
+def fit_absmax(S, w=None, bits=None):
     """Setup fit (Section 4.3 row factors, absmax column factor).
-    S: [n][dk][dv] float32 -> (r [n][dk], c [n][dv]) float32."""
+    S: [n][dk][dv] float32 -> (r [n][dk], c [n][dv]) float32.  bits
+    (optional): pivot rows (16) are left out of the column factor."""
     S = _c(S, np.float32)
     n, dk, dv = S.shape
     r = np.empty((n, dk), np.float32)
     c = np.empty((n, dv), np.float32)
     wv = None if w is None else _c(np.broadcast_to(w, (n, dk)), np.float64)
-    lib().orc_fit_absmax(n, dk, dv, _p(S), _p(wv), _p(r), _p(c))
+    bt = None if bits is None else _c(np.broadcast_to(bits, (n, dk)), np.uint8)
+    lib().orc_fit_absmax(n, dk, dv, _p(S), _p(wv), _p(bt), _p(r), _p(c))
     return r, c
 
 
@@ -100,16 +134,20 @@ def quantize(X, r, c, bits, want_y=False):
     r, c, bits = _c(r, np.float32), _c(c, np.float32), _c(np.broadcast_to(bits, (n, dk)), np.uint8)
     codes = np.empty((n, dk, dv), np.int8)
     y = np.empty((n, dk, dv), np.float64) if want_y else None
-    lib().orc_quantize(n, dk, dv, _p(X), _p(r), _p(c), _p(bits), _p(codes), _p(y))
-    return (codes, y) if want_y else codes
+    pv = np.zeros((n, dk, dv), np.uint16) if _has_pivots(bits) else None
+    lib().orc_quantize(n, dk, dv, _p(X), _p(r), _p(c), _p(bits), _p(codes), _p(y), _p(pv))
+    out = (codes, y) if want_y else (codes,)
+    out = out + ((pv,) if pv is not None else ())
+    return out if len(out) > 1 else out[0]
 
 
-def dequant(codes, r, c, bits):
+def dequant(codes, r, c, bits, pv=None):
     codes = _c(codes, np.int8)
     n, dk, dv = codes.shape
     r, c, bits = _c(r, np.float32), _c(c, np.float32), _c(np.broadcast_to(bits, (n, dk)), np.uint8)
+    pvi = _pv_in(pv, bits, (n, dk, dv))
     S = np.empty((n, dk, dv), np.float64)
-    lib().orc_dequant(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(S))
+    lib().orc_dequant(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(pvi), _p(S))
     return S
 
 
@@ -135,7 +173,7 @@ def update_fp(S, q, k, v, alpha, beta):
     return X, o
 
 
-def decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=False):
+def decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=False, pv=None):
     """One quantized decode step with frozen scales (Table C2 steps 1-3, 6);
     alpha [n] for the GDN gate or [n][dk] for the KDA channel-wise gate."""
     codes = _c(codes, np.int8)
@@ -147,12 +185,15 @@ def decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=False):
     out = np.empty_like(codes)
     o = np.empty((n, dv), np.float64)
     y = np.empty((n, dk, dv), np.float64) if want_y else None
+    pvi = _pv_in(pv, bits, (n, dk, dv))
+    pvo = np.zeros((n, dk, dv), np.uint16) if pvi is not None else None
     lib().orc_decode_step(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(q), _p(k), _p(v),
-                          _p(a), per_row, _p(beta), _p(out), _p(o), _p(y))
-    return (out, o, y) if want_y else (out, o)
+                          _p(a), per_row, _p(beta), _p(out), _p(o), _p(y), _p(pvi), _p(pvo))
+    res = (out, o, y) if want_y else (out, o)
+    return res + (pvo,) if pvo is not None else res
 
 
-def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=(), tie_window=2e-3):
+def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=(), tie_window=2e-3, pv=None):
     """One quantized decode step with the online dual-axis refit (Table C2
     steps 1-6, Section 4.3, Appendix C.1).  Returns (codes, r, c, o) with the
     new fp32 scales, plus a dict of the requested extras among "y", "y0", "X"
@@ -176,16 +217,19 @@ def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=(), 
         lo, hi = np.empty((n, dv), np.float64), np.empty((n, dv), np.float64)
         if "y0" not in extra:
             extra["y0"] = np.empty((n, dk, dv), np.float64)
+    pvi = _pv_in(pv, bits, (n, dk, dv))
+    pvo = np.zeros((n, dk, dv), np.uint16) if pvi is not None else None
     lib().orc_decode_step_refit(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(wt), _p(q), _p(k), _p(v),
                                 _p(a), per_row, _p(beta), _p(out), _p(r_out), _p(c_out), _p(o),
                                 _p(extra.get("y")), _p(extra.get("y0")), _p(extra.get("X")), float(tie_window),
-                                _p(lo), _p(hi))
+                                _p(lo), _p(hi), _p(pvi), _p(pvo))
     if lo is not None:
         extra["c_range"] = (lo, hi)
-    return (out, r_out, c_out, o, extra) if want else (out, r_out, c_out, o)
+    res = (out, r_out, c_out, o, extra) if want else (out, r_out, c_out, o)
+    return res + (pvo,) if pvo is not None else res
 
 
-def decode_step_rowmax(codes, r, c, bits, q, k, v, alpha, beta, want_y=False):
+def decode_step_rowmax(codes, r, c, bits, q, k, v, alpha, beta, want_y=False, pv=None):
     """One decode step of the row-wise absmax INT-b baseline (Section 5.1) on
     the same quantized tile: returns (codes, r, c, o[, y]) with r'_i =
     max_j |X_ij| and c' = 1."""
@@ -200,9 +244,12 @@ def decode_step_rowmax(codes, r, c, bits, q, k, v, alpha, beta, want_y=False):
     c_out = np.empty((n, dv), np.float32)
     o = np.empty((n, dv), np.float64)
     y = np.empty((n, dk, dv), np.float64) if want_y else None
+    pvi = _pv_in(pv, bits, (n, dk, dv))
+    pvo = np.zeros((n, dk, dv), np.uint16) if pvi is not None else None
     lib().orc_decode_step_rowmax(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(q), _p(k), _p(v), _p(a),
-                                 per_row, _p(beta), _p(out), _p(r_out), _p(c_out), _p(o), _p(y))
-    return (out, r_out, c_out, o, y) if want_y else (out, r_out, c_out, o)
+                                 per_row, _p(beta), _p(out), _p(r_out), _p(c_out), _p(o), _p(y), _p(pvi), _p(pvo))
+    res = (out, r_out, c_out, o, y) if want_y else (out, r_out, c_out, o)
+    return res + (pvo,) if pvo is not None else res
 
 
 def tile_bytes(bits_row, d_v: int) -> int:
@@ -216,25 +263,29 @@ def slot_bytes(bits, d_v: int) -> int:
     return int(lib().orc_slot_bytes(Hv, dk, d_v, _p(bits)))
 
 
-def pack_pool(codes, r, c, bits):
-    """Pool image (bytes) per the layout definition. codes [S][Hv][dk][dv]."""
+def pack_pool(codes, r, c, bits, pv=None):
+    """Pool image (bytes) per the layout definition. codes [S][Hv][dk][dv];
+    pv [S][Hv][dk][dv] binary16 values of pivot rows (if the map has any)."""
     codes = _c(codes, np.int8)
     S, Hv, dk, dv = codes.shape
     r, c, bits = _c(r, np.float32), _c(c, np.float32), _c(bits, np.uint8)
+    pvi = _pv_in(pv, bits, codes.shape)
     out = np.zeros(S * slot_bytes(bits, dv), np.uint8)
-    lib().orc_pack_pool(S, Hv, dk, dv, _p(bits), _p(codes), _p(r), _p(c), _p(out))
+    lib().orc_pack_pool(S, Hv, dk, dv, _p(bits), _p(codes), _p(pvi), _p(r), _p(c), _p(out))
     return out
 
 
 def unpack_pool(pool, n_slots, bits, d_v):
+    """(codes, r, c[, pv]) of a pool image; pv only if the map has pivots."""
     bits = _c(bits, np.uint8)
     Hv, dk = bits.shape
     pool = _c(pool, np.uint8)
     codes = np.empty((n_slots, Hv, dk, d_v), np.int8)
     r = np.empty((n_slots, Hv, dk), np.float32)
     c = np.empty((n_slots, Hv, d_v), np.float32)
-    lib().orc_unpack_pool(n_slots, Hv, dk, d_v, _p(bits), _p(pool), _p(codes), _p(r), _p(c))
-    return codes, r, c
+    pv = np.zeros((n_slots, Hv, dk, d_v), np.uint16) if _has_pivots(bits) else None
+    lib().orc_unpack_pool(n_slots, Hv, dk, d_v, _p(bits), _p(pool), _p(codes), _p(pv), _p(r), _p(c))
+    return (codes, r, c, pv) if pv is not None else (codes, r, c)
 
 
 # ---------------------------------------------------------------------------

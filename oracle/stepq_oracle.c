@@ -17,6 +17,13 @@
  * i.e. the level set is normalised so that |S^_ij| <= r_i c_j at every
  * width (this is the reading that makes "r_i c_j >= |S_ij|" the no-clip
  * condition of a symmetric absmax fit).
+ *
+ * FP16 pivot rows (Section 3.2, Table C1): a row of width 16 holds its
+ * values as IEEE binary16 (pv, bit patterns, [dk][dv] per tile, only pivot
+ * rows used) instead of codes and scales.  The update treats them like any
+ * other row; their new values are X rounded to binary16 (nearest, ties to
+ * even), and they take no part in the scale fits (Appendix C.1 fits the
+ * non-pivot integer rows).
  */
 #include <math.h>
 #include <stddef.h>
@@ -25,6 +32,84 @@
 #include <stdlib.h>
 
 static double qb_of(int b) { return (double)((1 << (b - 1)) - 1); }
+
+/* IEEE 754 binary16, from its definition: 1 sign bit, 5 exponent bits (bias
+ * 15), 10 fraction bits; exponent 0 holds subnormals k 2^-24. */
+static double h2d(uint16_t h)
+{
+    int sgn = (h >> 15) & 1, e = (h >> 10) & 31, f = h & 1023;
+    double v;
+    if (e == 0) v = ldexp((double)f, -24);
+    else if (e == 31) v = f ? NAN : INFINITY;
+    else v = ldexp((double)(1024 + f), e - 25);
+    return sgn ? -v : v;
+}
+
+/* Round to the nearest binary16, ties to even; beyond the largest finite
+ * value (65504) by half an ulp or more, to infinity. */
+static uint16_t d2h(double x)
+{
+    uint16_t sgn = signbit(x) ? 0x8000u : 0u;
+    double a = fabs(x);
+    if (isnan(a)) return (uint16_t)(sgn | 0x7e00u);
+    if (a >= 65520.0) return (uint16_t)(sgn | 0x7c00u);
+    if (a < ldexp(1.0, -14)) {                    /* subnormal range: k 2^-24, k <= 1024 */
+        double k = nearbyint(ldexp(a, 24));
+        return (uint16_t)(sgn | (uint16_t)k);      /* k = 1024 is the smallest normal */
+    }
+    int e;
+    frexp(a, &e);                                 /* a = m 2^e, m in [0.5, 1) */
+    double m = nearbyint(ldexp(a, 11 - e));       /* 11 significant bits, in [1024, 2048] */
+    if (m == 2048.0) {
+        m = 1024.0;
+        ++e;
+    }
+    int ef = e - 1 + 15;
+    if (ef >= 31) return (uint16_t)(sgn | 0x7c00u);
+    return (uint16_t)(sgn | (uint16_t)(ef << 10) | (uint16_t)((int)m - 1024));
+}
+
+void orc_half_to_double(size_t n, const uint16_t *h, double *out)
+{
+    for (size_t i = 0; i < n; ++i) out[i] = h2d(h[i]);
+}
+
+void orc_double_to_half(size_t n, const double *x, uint16_t *out)
+{
+    for (size_t i = 0; i < n; ++i) out[i] = d2h(x[i]);
+}
+
+/* Reconstruction of one tile (Section 4.3, and the stored binary16 values of
+ * pivot rows). */
+static void reconstruct_tile(int dk, int dv, const int8_t *ci, const uint16_t *pv, const float *rt,
+                             const float *ct, const uint8_t *bt, double *Sh)
+{
+    for (int i = 0; i < dk; ++i) {
+        if (bt[i] == 16) {
+            for (int j = 0; j < dv; ++j) Sh[(size_t)i * dv + j] = h2d(pv[(size_t)i * dv + j]);
+            continue;
+        }
+        double qb = qb_of(bt[i]);
+        for (int j = 0; j < dv; ++j)
+            Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / qb;
+    }
+}
+
+/* Pivot rows of an updated tile: X rounded to binary16, codes 0; y (if
+ * given) receives X itself for those rows. */
+static void store_pivots(int dk, int dv, const uint8_t *bt, const double *X, uint16_t *pv_out,
+                         int8_t *codes_out, double *y)
+{
+    for (int i = 0; i < dk; ++i) {
+        if (bt[i] != 16) continue;
+        for (int j = 0; j < dv; ++j) {
+            size_t e = (size_t)i * dv + j;
+            if (pv_out) pv_out[e] = d2h(X[e]);
+            codes_out[e] = 0;
+            if (y) y[e] = X[e];
+        }
+    }
+}
 
 /* ------------------------------------------------------------------------
  * Scale fit used by the setup step (Section 4.3, "Row factors"; the column
@@ -35,9 +120,10 @@ static double qb_of(int b) { return (double)((1 << (b - 1)) - 1); }
  * A positive floor of 2^-60 keeps both factors strictly positive
  * (Appendix C.1 asks for a positive numerical floor).  The results are
  * rounded once to fp32, the storage precision of the scales.
- * w == NULL means w_i = 1.
+ * w == NULL means w_i = 1.  bits (optional, [n_tiles][dk]): rows of width 16
+ * (pivots) are left out of the column factor.
  */
-void orc_fit_absmax(int n_tiles, int dk, int dv, const float *S, const double *w,
+void orc_fit_absmax(int n_tiles, int dk, int dv, const float *S, const double *w, const uint8_t *bits,
                     float *r_out, float *c_out)
 {
     const double floor_ = ldexp(1.0, -60);
@@ -58,6 +144,7 @@ void orc_fit_absmax(int n_tiles, int dk, int dv, const float *S, const double *w
         for (int j = 0; j < dv; ++j) {
             double cj = 0.0;
             for (int i = 0; i < dk; ++i) {
+                if (bits && bits[(size_t)t * dk + i] == 16) continue;     /* pivots keep their own values */
                 double a = fabs((double)St[(size_t)i * dv + j]) / r[i];
                 if (a > cj) cj = a;
             }
@@ -77,13 +164,18 @@ void orc_fit_absmax(int n_tiles, int dk, int dv, const float *S, const double *w
  *   q_ij = clip(round(X_ij * q_b / (r_i c_j)), -q_b, q_b)
  * round = nearest, ties to even (nearbyint under the default rounding mode).
  * bits: [n_tiles][dk].  y (optional) receives the unrounded X q_b/(r c).
+ * Pivot rows (width 16): pv receives X in binary16, codes 0.
  */
 void orc_quantize(int n_tiles, int dk, int dv, const double *X, const float *r, const float *c,
-                  const uint8_t *bits, int8_t *codes, double *y)
+                  const uint8_t *bits, int8_t *codes, double *y, uint16_t *pv)
 {
     #pragma omp parallel for schedule(static)
     for (int t = 0; t < n_tiles; ++t) {
+        size_t nel = (size_t)dk * dv;
+        store_pivots(dk, dv, bits + (size_t)t * dk, X + t * nel, pv ? pv + t * nel : NULL, codes + t * nel,
+                     y ? y + t * nel : NULL);
         for (int i = 0; i < dk; ++i) {
+            if (bits[(size_t)t * dk + i] == 16) continue;
             double qb = qb_of(bits[(size_t)t * dk + i]);
             double ri = (double)r[(size_t)t * dk + i];
             for (int j = 0; j < dv; ++j) {
@@ -99,19 +191,17 @@ void orc_quantize(int n_tiles, int dk, int dv, const double *X, const float *r, 
     }
 }
 
-/* Reconstruction (Section 4.3): S^_ij = r_i c_j q_ij / q_{b_i}. */
+/* Reconstruction (Section 4.3): S^_ij = r_i c_j q_ij / q_{b_i}; pivot rows
+ * from their binary16 values. */
 void orc_dequant(int n_tiles, int dk, int dv, const int8_t *codes, const float *r, const float *c,
-                 const uint8_t *bits, double *S)
+                 const uint8_t *bits, const uint16_t *pv, double *S)
 {
     #pragma omp parallel for schedule(static)
-    for (int t = 0; t < n_tiles; ++t)
-        for (int i = 0; i < dk; ++i) {
-            double qb = qb_of(bits[(size_t)t * dk + i]);
-            for (int j = 0; j < dv; ++j) {
-                size_t e = ((size_t)t * dk + i) * dv + j;
-                S[e] = (double)r[(size_t)t * dk + i] * (double)c[(size_t)t * dv + j] * (double)codes[e] / qb;
-            }
-        }
+    for (int t = 0; t < n_tiles; ++t) {
+        size_t nel = (size_t)dk * dv;
+        reconstruct_tile(dk, dv, codes + t * nel, pv ? pv + t * nel : NULL, r + (size_t)t * dk,
+                         c + (size_t)t * dv, bits + (size_t)t * dk, S + t * nel);
+    }
 }
 
 /* ------------------------------------------------------------------------
@@ -170,12 +260,13 @@ void orc_update_fp(int n_tiles, int dk, int dv, const double *S, const double *q
  * (step 2; D = alpha I or diag(d)), emit o = X^T q before requantization
  * (step 3), requantize X on the same r, c and per-row widths (Eq. 3) as the
  * new codes.
- * y (optional) receives X q_b/(r c) before rounding.
+ * y (optional) receives X q_b/(r c) before rounding (X itself on pivot
+ * rows).  pv_in / pv_out: binary16 values of pivot rows (NULL without pivots).
  */
 void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const float *r,
                      const float *c, const uint8_t *bits, const double *q, const double *k,
                      const double *v, const double *alpha, int per_row, const double *beta,
-                     int8_t *codes_out, double *o, double *y)
+                     int8_t *codes_out, double *o, double *y, const uint16_t *pv_in, uint16_t *pv_out)
 {
     #pragma omp parallel for schedule(dynamic, 4)
     for (int t = 0; t < n_tiles; ++t) {
@@ -186,14 +277,13 @@ void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const 
         const int8_t *ci = codes_in + (size_t)t * nel;
         const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
         const uint8_t *bt = bits + (size_t)t * dk;
-        for (int i = 0; i < dk; ++i) {
-            double qb = qb_of(bt[i]);
-            for (int j = 0; j < dv; ++j)
-                Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / qb;
-        }
+        reconstruct_tile(dk, dv, ci, pv_in ? pv_in + (size_t)t * nel : NULL, rt, ct, bt, Sh);
         update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
                     gate_of(alpha, per_row, t, dk, gbuf), beta[t], X, o + (size_t)t * dv);
+        store_pivots(dk, dv, bt, X, pv_out ? pv_out + (size_t)t * nel : NULL, codes_out + (size_t)t * nel,
+                     y ? y + (size_t)t * nel : NULL);
         for (int i = 0; i < dk; ++i) {
+            if (bt[i] == 16) continue;
             double qb = qb_of(bt[i]);
             for (int j = 0; j < dv; ++j) {
                 double s = X[(size_t)i * dv + j] * qb / ((double)rt[i] * (double)ct[j]);
@@ -227,7 +317,8 @@ void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const 
  * each is rounded to fp32 when it is formed, and what follows it uses the
  * rounded value.
  * Optional outputs: y (X q_b / (r' c') before rounding), y0 (X q_b / (r' c0)
- * before rounding), X.
+ * before rounding), X.  Pivot rows (width 16) are updated in binary16
+ * (pv_in / pv_out), keep their stored r, and are left out of both fits.
  *
  * c_lo, c_hi (optional, for comparing with lower-precision implementations):
  * bounds on the column factor over every other rounding of the fixed codes
@@ -243,7 +334,7 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
                            const double *k, const double *v, const double *alpha, int per_row,
                            const double *beta, int8_t *codes_out, float *r_out, float *c_out, double *o,
                            double *y, double *y0, double *X_out, double tie_window, double *c_lo,
-                           double *c_hi)
+                           double *c_hi, const uint16_t *pv_in, uint16_t *pv_out)
 {
     const double floor_ = ldexp(1.0, -60);
     #pragma omp parallel for schedule(dynamic, 4)
@@ -257,17 +348,20 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
         const int8_t *ci = codes_in + (size_t)t * nel;
         const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
         const uint8_t *bt = bits + (size_t)t * dk;
-        for (int i = 0; i < dk; ++i) {
-            double qb = qb_of(bt[i]);
-            for (int j = 0; j < dv; ++j)
-                Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / qb;
-        }
+        reconstruct_tile(dk, dv, ci, pv_in ? pv_in + (size_t)t * nel : NULL, rt, ct, bt, Sh);
         update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
                     gate_of(alpha, per_row, t, dk, gbuf), beta[t], X, o + (size_t)t * dv);
         if (X_out) memcpy(X_out + (size_t)t * nel, X, sizeof(double) * nel);
+        store_pivots(dk, dv, bt, X, pv_out ? pv_out + (size_t)t * nel : NULL, codes_out + (size_t)t * nel,
+                     y ? y + (size_t)t * nel : NULL);
 
-        /* row factors */
+        /* row factors (a pivot row keeps its stored, unused, factor) */
         for (int i = 0; i < dk; ++i) {
+            if (bt[i] == 16) {
+                r_out[(size_t)t * dk + i] = rt[i];
+                rn[i] = (double)rt[i];
+                continue;
+            }
             double m = 0.0;
             for (int j = 0; j < dv; ++j) m += fabs(X[(size_t)i * dv + j]);
             m /= (double)dv;
@@ -281,11 +375,17 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
             /* absmax start of the column factor, then the fixed codes */
             double c0 = 0.0;
             for (int i = 0; i < dk; ++i) {
+                if (bt[i] == 16) continue;
                 double a = fabs(X[(size_t)i * dv + j]) / rn[i];
                 if (a > c0) c0 = a;
             }
             if (c0 < floor_) c0 = floor_;
             for (int i = 0; i < dk; ++i) {
+                if (bt[i] == 16) {
+                    zt[(size_t)i * dv + j] = 0.0;            /* no part in the column fit */
+                    if (y0) y0[(size_t)t * nel + (size_t)i * dv + j] = 0.0;
+                    continue;
+                }
                 double qb = qb_of(bt[i]);
                 double s = X[(size_t)i * dv + j] * qb / (rn[i] * c0);
                 if (y0) y0[(size_t)t * nel + (size_t)i * dv + j] = s;
@@ -313,6 +413,7 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
             if (c_lo && c_hi) {
                 double nlo = num, nhi = num, dlo = den, dhi = den;
                 for (int i = 0; i < dk; ++i) {
+                    if (bt[i] == 16) continue;
                     double qb = qb_of(bt[i]);
                     double s = y0[(size_t)t * nel + (size_t)i * dv + j];
                     double a = fabs(s);
@@ -349,6 +450,7 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
         }
         /* requantize against the stored scales */
         for (int i = 0; i < dk; ++i) {
+            if (bt[i] == 16) continue;
             double qb = qb_of(bt[i]);
             for (int j = 0; j < dv; ++j) {
                 double s = X[(size_t)i * dv + j] * qb / (rn[i] * (double)c_out[(size_t)t * dv + j]);
@@ -373,12 +475,14 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
  * tile: steps 1-3 of orc_decode_step, then per key row
  *   r'_i = max_j |X_ij|  (floor 2^-60, stored fp32),   c'_j = 1,
  *   q'_ij = clip(round(X_ij q_b / r'_i), -q_b, q_b)    with the stored r'.
- * y (optional) receives X q_b / r' before rounding.
+ * y (optional) receives X q_b / r' before rounding.  Pivot rows as in
+ * orc_decode_step_refit.
  */
 void orc_decode_step_rowmax(int n_tiles, int dk, int dv, const int8_t *codes_in, const float *r,
                             const float *c, const uint8_t *bits, const double *q, const double *k,
                             const double *v, const double *alpha, int per_row, const double *beta,
-                            int8_t *codes_out, float *r_out, float *c_out, double *o, double *y)
+                            int8_t *codes_out, float *r_out, float *c_out, double *o, double *y,
+                            const uint16_t *pv_in, uint16_t *pv_out)
 {
     const double floor_ = ldexp(1.0, -60);
     #pragma omp parallel for schedule(dynamic, 4)
@@ -390,15 +494,17 @@ void orc_decode_step_rowmax(int n_tiles, int dk, int dv, const int8_t *codes_in,
         const int8_t *ci = codes_in + (size_t)t * nel;
         const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
         const uint8_t *bt = bits + (size_t)t * dk;
-        for (int i = 0; i < dk; ++i) {
-            double qb = qb_of(bt[i]);
-            for (int j = 0; j < dv; ++j)
-                Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / qb;
-        }
+        reconstruct_tile(dk, dv, ci, pv_in ? pv_in + (size_t)t * nel : NULL, rt, ct, bt, Sh);
         update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
                     gate_of(alpha, per_row, t, dk, gbuf), beta[t], X, o + (size_t)t * dv);
         for (int j = 0; j < dv; ++j) c_out[(size_t)t * dv + j] = 1.0f;
+        store_pivots(dk, dv, bt, X, pv_out ? pv_out + (size_t)t * nel : NULL, codes_out + (size_t)t * nel,
+                     y ? y + (size_t)t * nel : NULL);
         for (int i = 0; i < dk; ++i) {
+            if (bt[i] == 16) {
+                r_out[(size_t)t * dk + i] = rt[i];
+                continue;
+            }
             double m = 0.0;
             for (int j = 0; j < dv; ++j) {
                 double a = fabs(X[(size_t)i * dv + j]);
@@ -425,23 +531,25 @@ void orc_decode_step_rowmax(int n_tiles, int dk, int dv, const int8_t *codes_in,
 
 /* ------------------------------------------------------------------------
  * Pool layout, re-derived from its definition in include/stepq.h:
- *  - physical key-row order: the 8-bit rows in increasing logical index,
- *    then the 4-bit rows, then the 2-bit rows;
- *  - row groups of 8/b physical rows of one width (1, 2 or 4 rows); a last
- *    partial group of a width is completed with empty slots;
+ *  - physical key-row order: the pivot (16) rows, then the 8-bit rows, the
+ *    4-bit rows and the 2-bit rows, each class in increasing logical index;
+ *  - row groups of 8/b physical integer rows of one width (1, 2 or 4 rows);
+ *    a last partial group of a width is completed with empty slots;
  *  - each group is d_v bytes; byte j holds column j, slot s of the group at
  *    bits [s*b, s*b+b) as b-bit two's complement, empty slots zero;
- *  - codes region padded with zeros to a multiple of 128 bytes, followed by
- *    r (d_k fp32, physical row order) and c (d_v fp32), the whole tile
- *    record padded with zeros to a multiple of 128 bytes.
+ *  - codes region padded with zeros to a multiple of 128 bytes; then the
+ *    pivot rows, d_v binary16 values each (little-endian), in physical
+ *    order; then r (d_k fp32, physical row order) and c (d_v fp32), the
+ *    whole tile record padded with zeros to a multiple of 128 bytes.
  */
 static size_t round128(size_t x) { return (x + 127) & ~(size_t)127; }
 
-static void class_counts(int dk, const uint8_t *bits, int *n8, int *n4, int *n2)
+static void class_counts(int dk, const uint8_t *bits, int *n16, int *n8, int *n4, int *n2)
 {
-    *n8 = *n4 = *n2 = 0;
+    *n16 = *n8 = *n4 = *n2 = 0;
     for (int i = 0; i < dk; ++i) {
-        if (bits[i] == 8) ++*n8;
+        if (bits[i] == 16) ++*n16;
+        else if (bits[i] == 8) ++*n8;
         else if (bits[i] == 4) ++*n4;
         else if (bits[i] == 2) ++*n2;
     }
@@ -449,42 +557,54 @@ static void class_counts(int dk, const uint8_t *bits, int *n8, int *n4, int *n2)
 
 static size_t codes_region(int dk, int dv, const uint8_t *bits)
 {
-    int n8, n4, n2;
-    class_counts(dk, bits, &n8, &n4, &n2);
+    int n16, n8, n4, n2;
+    class_counts(dk, bits, &n16, &n8, &n4, &n2);
     size_t groups = (size_t)n8 + (size_t)(n4 + 1) / 2 + (size_t)(n2 + 3) / 4;
     return round128(groups * (size_t)dv);
 }
 
+static size_t pivot_region(int dk, int dv, const uint8_t *bits)
+{
+    int n16, n8, n4, n2;
+    class_counts(dk, bits, &n16, &n8, &n4, &n2);
+    return round128((size_t)n16 * 2u * (size_t)dv);
+}
+
 size_t orc_tile_bytes(int dk, int dv, const uint8_t *bits)
 {
-    return round128(codes_region(dk, dv, bits) + 4u * (size_t)dk + 4u * (size_t)dv);
+    return round128(codes_region(dk, dv, bits) + pivot_region(dk, dv, bits) + 4u * (size_t)dk + 4u * (size_t)dv);
 }
 
 /* logical row of each physical row, and the (group, slot) position of each
- * logical row inside the codes region */
+ * logical integer row inside the codes region (pivot rows: their index
+ * among the pivot rows in group, slot -1) */
 static void row_positions(int dk, const uint8_t *bits, int *phys_to_log, int *group, int *slot)
 {
-    int n8, n4, n2;
-    class_counts(dk, bits, &n8, &n4, &n2);
+    int n16, n8, n4, n2;
+    class_counts(dk, bits, &n16, &n8, &n4, &n2);
     int p = 0;
-    static const int order[3] = {8, 4, 2};
-    for (int cl = 0; cl < 3; ++cl)
+    static const int order[4] = {16, 8, 4, 2};
+    for (int cl = 0; cl < 4; ++cl)
         for (int i = 0; i < dk; ++i)
             if (bits[i] == order[cl]) phys_to_log[p++] = i;
     int g4 = n8, g2 = n8 + (n4 + 1) / 2;
     for (int pp = 0; pp < dk; ++pp) {
         int i = phys_to_log[pp];
-        if (pp < n8) { group[i] = pp; slot[i] = 0; }
-        else if (pp < n8 + n4) { int k = pp - n8; group[i] = g4 + k / 2; slot[i] = k % 2; }
-        else { int k = pp - n8 - n4; group[i] = g2 + k / 4; slot[i] = k % 4; }
+        int q = pp - n16;                          /* index among the integer rows */
+        if (pp < n16) { group[i] = pp; slot[i] = -1; }
+        else if (q < n8) { group[i] = q; slot[i] = 0; }
+        else if (q < n8 + n4) { int k = q - n8; group[i] = g4 + k / 2; slot[i] = k % 2; }
+        else { int k = q - n8 - n4; group[i] = g2 + k / 4; slot[i] = k % 4; }
     }
 }
 
-/* codes: [dk][dv] logical order; r: [dk] logical order; c: [dv] */
-void orc_pack_tile(int dk, int dv, const uint8_t *bits, const int8_t *codes, const float *r,
-                   const float *c, uint8_t *rec)
+/* codes: [dk][dv] logical order; pv: [dk][dv] binary16 (pivot rows only;
+ * NULL if there are none); r: [dk] logical order; c: [dv] */
+void orc_pack_tile(int dk, int dv, const uint8_t *bits, const int8_t *codes, const uint16_t *pv,
+                   const float *r, const float *c, uint8_t *rec)
 {
     size_t creg = codes_region(dk, dv, bits);
+    size_t preg = pivot_region(dk, dv, bits);
     size_t tb = orc_tile_bytes(dk, dv, bits);
     memset(rec, 0, tb);
     int *p2l = (int *)malloc(sizeof(int) * dk * 3);
@@ -492,28 +612,46 @@ void orc_pack_tile(int dk, int dv, const uint8_t *bits, const int8_t *codes, con
     row_positions(dk, bits, p2l, grp, slt);
     for (int i = 0; i < dk; ++i) {
         int b = bits[i];
+        if (b == 16) {
+            uint8_t *row = rec + creg + (size_t)grp[i] * 2u * dv;
+            for (int j = 0; j < dv; ++j) {
+                uint16_t h = pv[(size_t)i * dv + j];
+                row[2 * j] = (uint8_t)(h & 0xff);
+                row[2 * j + 1] = (uint8_t)(h >> 8);
+            }
+            continue;
+        }
         unsigned mask = (1u << b) - 1u;
         for (int j = 0; j < dv; ++j) {
             unsigned field = ((unsigned)(int)codes[(size_t)i * dv + j]) & mask;
             rec[(size_t)grp[i] * dv + j] |= (uint8_t)(field << (slt[i] * b));
         }
     }
-    float *rr = (float *)(rec + creg);
+    float *rr = (float *)(rec + creg + preg);
     float *cc = rr + dk;
     for (int p = 0; p < dk; ++p) rr[p] = r[p2l[p]];
     for (int j = 0; j < dv; ++j) cc[j] = c[j];
     free(p2l);
 }
 
-void orc_unpack_tile(int dk, int dv, const uint8_t *bits, const uint8_t *rec, int8_t *codes,
+void orc_unpack_tile(int dk, int dv, const uint8_t *bits, const uint8_t *rec, int8_t *codes, uint16_t *pv,
                      float *r, float *c)
 {
     size_t creg = codes_region(dk, dv, bits);
+    size_t preg = pivot_region(dk, dv, bits);
     int *p2l = (int *)malloc(sizeof(int) * dk * 3);
     int *grp = p2l + dk, *slt = p2l + 2 * dk;
     row_positions(dk, bits, p2l, grp, slt);
     for (int i = 0; i < dk; ++i) {
         int b = bits[i];
+        if (b == 16) {
+            const uint8_t *row = rec + creg + (size_t)grp[i] * 2u * dv;
+            for (int j = 0; j < dv; ++j) {
+                codes[(size_t)i * dv + j] = 0;
+                if (pv) pv[(size_t)i * dv + j] = (uint16_t)(row[2 * j] | (row[2 * j + 1] << 8));
+            }
+            continue;
+        }
         for (int j = 0; j < dv; ++j) {
             unsigned byte = rec[(size_t)grp[i] * dv + j];
             int field = (int)((byte >> (slt[i] * b)) & ((1u << b) - 1u));
@@ -521,7 +659,7 @@ void orc_unpack_tile(int dk, int dv, const uint8_t *bits, const uint8_t *rec, in
             codes[(size_t)i * dv + j] = (int8_t)field;
         }
     }
-    const float *rr = (const float *)(rec + creg);
+    const float *rr = (const float *)(rec + creg + preg);
     const float *cc = rr + dk;
     for (int p = 0; p < dk; ++p) r[p2l[p]] = rr[p];
     for (int j = 0; j < dv; ++j) c[j] = cc[j];
@@ -539,7 +677,7 @@ size_t orc_slot_bytes(int Hv, int dk, int dv, const uint8_t *bits)
 }
 
 void orc_pack_pool(int n_slots, int Hv, int dk, int dv, const uint8_t *bits, const int8_t *codes,
-                   const float *r, const float *c, uint8_t *pool)
+                   const uint16_t *pv, const float *r, const float *c, uint8_t *pool)
 {
     size_t sb = orc_slot_bytes(Hv, dk, dv, bits);
     #pragma omp parallel for schedule(static)
@@ -547,15 +685,15 @@ void orc_pack_pool(int n_slots, int Hv, int dk, int dv, const uint8_t *bits, con
         size_t off = (size_t)s * sb;
         for (int h = 0; h < Hv; ++h) {
             size_t t = (size_t)s * Hv + h;
-            orc_pack_tile(dk, dv, bits + (size_t)h * dk, codes + t * dk * dv, r + t * dk, c + t * dv,
-                          pool + off);
+            orc_pack_tile(dk, dv, bits + (size_t)h * dk, codes + t * dk * dv, pv ? pv + t * dk * dv : NULL,
+                          r + t * dk, c + t * dv, pool + off);
             off += orc_tile_bytes(dk, dv, bits + (size_t)h * dk);
         }
     }
 }
 
 void orc_unpack_pool(int n_slots, int Hv, int dk, int dv, const uint8_t *bits, const uint8_t *pool,
-                     int8_t *codes, float *r, float *c)
+                     int8_t *codes, uint16_t *pv, float *r, float *c)
 {
     size_t sb = orc_slot_bytes(Hv, dk, dv, bits);
     #pragma omp parallel for schedule(static)
@@ -563,8 +701,8 @@ void orc_unpack_pool(int n_slots, int Hv, int dk, int dv, const uint8_t *bits, c
         size_t off = (size_t)s * sb;
         for (int h = 0; h < Hv; ++h) {
             size_t t = (size_t)s * Hv + h;
-            orc_unpack_tile(dk, dv, bits + (size_t)h * dk, pool + off, codes + t * dk * dv, r + t * dk,
-                            c + t * dv);
+            orc_unpack_tile(dk, dv, bits + (size_t)h * dk, pool + off, codes + t * dk * dv,
+                            pv ? pv + t * dk * dv : NULL, r + t * dk, c + t * dv);
             off += orc_tile_bytes(dk, dv, bits + (size_t)h * dk);
         }
     }

@@ -639,3 +639,127 @@ def test_rowmax_baseline_is_refit_free_of_columns():
     assert np.array_equal(out, oracle.quantize(X, rn, cn, bits))
     up = oracle.decode_step_rowmax(codes, 4 * r, c, bits, q, k, 4 * v, g, beta)
     assert np.array_equal(up[0], out) and np.array_equal(up[1], 4 * rn)
+
+
+# ---------------------------------------------------------------- FP16 pivot rows (Section 3.2, Table C1)
+def test_binary16_conversions_match_ieee():
+    """The oracle's binary16 decoding of every bit pattern, and its rounding
+    of doubles (ties to even, subnormals, overflow), agree with numpy's
+    IEEE half type."""
+    h = np.arange(65536, dtype=np.uint16)
+    ref = h.view(np.float16).astype(np.float64)
+    got = oracle.half_to_double(h)
+    fin = ~np.isnan(ref)
+    assert np.array_equal(got[fin], ref[fin]) and np.all(np.isnan(got[~fin]))
+    rng = np.random.default_rng(50)
+    vals = np.unique(ref[np.isfinite(ref)])
+    x = np.concatenate([
+        rng.standard_normal(20000) * np.exp(rng.uniform(-20, 12, 20000)),
+        vals[:-1] + 0.5 * np.diff(vals),                  # exact midpoints between neighbours
+        np.array([65504.0, 65519.99, 65520.0, 1e6, -65520.0, 2.0 ** -25, 2.0 ** -24, 3 * 2.0 ** -26, 0.0, -0.0]),
+    ])
+    x = x[np.isfinite(x)]
+    with np.errstate(over="ignore"):
+        want = x.astype(np.float16).view(np.uint16)
+    assert np.array_equal(oracle.double_to_half(x), want)
+
+
+def _pivot_map(rng, n, dk, n_piv):
+    bits = rng.choice([2, 4, 8], size=(n, dk)).astype(np.uint8)
+    for t in range(n):
+        bits[t, rng.choice(dk, size=n_piv, replace=False)] = 16
+    return bits
+
+
+def test_pivot_layout_placement_and_roundtrip():
+    """A pivot row's binary16 values sit after the codes region, in physical
+    order, little-endian; the integer rows and scales are unaffected; pack
+    and unpack are inverse."""
+    dk, dv = 10, 64
+    bits = np.array([[8, 16, 4, 2, 16, 8, 4, 4, 2, 2]], np.uint8)
+    codes = np.zeros((1, 1, dk, dv), np.int8)
+    pv = np.zeros((1, 1, dk, dv), np.uint16)
+    pv[0, 0, 4, 3] = 0xBEEF                           # second pivot row, column 3
+    r = np.arange(1, dk + 1, dtype=np.float32)[None, None]
+    c = np.full((1, 1, dv), 0.5, np.float32)
+    img = oracle.pack_pool(codes, r, c, bits, pv=pv)
+    groups = 2 + 2 + 1                                # two 8-bit rows, three 4-bit rows, three 2-bit rows
+    creg = ((groups * dv + 127) // 128) * 128
+    piv = img[creg:creg + 2 * 2 * dv]
+    nz = np.nonzero(piv)[0]
+    assert list(nz) == [2 * dv + 6, 2 * dv + 7] and piv[2 * dv + 6] == 0xEF and piv[2 * dv + 7] == 0xBE
+    rr = img[creg + 4 * dv: creg + 4 * dv + 4 * dk].view(np.float32)
+    assert list(rr) == [2, 5, 1, 6, 3, 7, 8, 4, 9, 10]   # physical order: pivots, 8, 4, 2
+    assert len(img) == oracle.slot_bytes(bits, dv) == ((creg + 4 * dv + 4 * (dk + dv) + 127) // 128) * 128
+    rng = np.random.default_rng(51)
+    bits2 = _pivot_map(rng, 3, 20, 3)
+    qb = 2 ** (bits2.astype(np.int64) - 1) - 1
+    codes2 = np.where(bits2[None, :, :, None] == 16, 0,
+                      rng.integers(-qb[None, :, :, None], qb[None, :, :, None] + 1, size=(2, 3, 20, 64))).astype(np.int8)
+    pv2 = rng.integers(0, 65536, size=(2, 3, 20, 64)).astype(np.uint16) * (bits2[None, :, :, None] == 16)
+    r2 = rng.uniform(0.1, 1, (2, 3, 20)).astype(np.float32)
+    c2 = rng.uniform(0.1, 1, (2, 3, 64)).astype(np.float32)
+    back = oracle.unpack_pool(oracle.pack_pool(codes2, r2, c2, bits2, pv=pv2), 2, bits2, 64)
+    assert np.array_equal(back[0], codes2) and np.array_equal(back[3], pv2)
+    assert np.array_equal(back[1], r2) and np.array_equal(back[2], c2)
+
+
+@pytest.mark.parametrize("kda", [False, True])
+def test_pivot_decode_is_update_then_binary16(kda):
+    """Pivot rows enter the update with their binary16 values and leave as X
+    rounded to binary16 (pinned conversion); integer rows follow the pinned
+    quantizer; o is read from X as without pivots."""
+    rng = np.random.default_rng(52)
+    n, dk, dv = 3, 16, 12
+    bits = _pivot_map(rng, n, dk, 2)
+    S = rng.standard_normal((n, dk, dv)) * 0.3
+    r, c = oracle.fit_absmax(S.astype(np.float32), bits=bits)
+    codes, pv = oracle.quantize(S, r, c, bits)
+    np.testing.assert_array_equal(oracle.half_to_double(pv)[bits == 16], oracle.half_to_double(
+        oracle.double_to_half(S))[bits == 16])
+    q, k = _unit(rng, n, dk), _unit(rng, n, dk)
+    v = rng.standard_normal((n, dv))
+    g = rng.uniform(0.5, 1, (n, dk)) if kda else rng.uniform(0.5, 1, n)
+    beta = rng.uniform(0, 1, n)
+    out, o, pv2 = oracle.decode_step(codes, r, c, bits, q, k, v, g, beta, pv=pv)
+    Sh = oracle.dequant(codes, r, c, bits, pv=pv)
+    X, o_ref = oracle.update_fp(Sh, q, k, v, g, beta)
+    assert np.array_equal(o, o_ref)
+    assert np.array_equal(pv2[bits == 16], oracle.double_to_half(X)[bits == 16])
+    want, _ = oracle.quantize(X, r, c, bits)
+    assert np.array_equal(out, want) and np.all(out[bits == 16] == 0)
+
+
+@pytest.mark.parametrize("mode", ["refit", "rowmax"])
+def test_pivots_take_no_part_in_the_scale_fits(mode):
+    """With k = 0 on the pivot rows they do not feed the other rows' update,
+    so the refit of the integer rows must equal the refit of the tile with
+    the pivot rows removed, bit for bit, however large the pivot values
+    (Appendix C.1 fits the non-pivot integer rows)."""
+    rng = np.random.default_rng(53 if mode == "refit" else 54)
+    n, dk, dv = 2, 14, 10
+    bits = np.tile(np.array([[8, 16, 4, 8, 2, 16, 4, 8, 8, 4, 2, 16, 8, 4]], np.uint8), (n, 1))
+    keep = bits[0] != 16
+    S = rng.standard_normal((n, dk, dv)) * 0.2
+    S[:, ~keep, :] *= 1e3                                      # outlier pivot rows
+    r, c = oracle.fit_absmax(S.astype(np.float32), bits=bits)
+    r_int, c_int = oracle.fit_absmax(S[:, keep].astype(np.float32))
+    assert np.array_equal(c, c_int) and np.array_equal(r[:, keep], r_int)
+    codes, pv = oracle.quantize(S, r, c, bits)
+    q, k = _unit(rng, n, dk), _unit(rng, n, dk)
+    k[:, ~keep] = 0.0
+    v = rng.standard_normal((n, dv))
+    g = rng.uniform(0.5, 1, n)
+    beta = rng.uniform(0, 1, n)
+    w = np.exp(0.3 * rng.standard_normal((n, dk)))
+    if mode == "refit":
+        full = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w, pv=pv)
+        part = oracle.decode_step_refit(codes[:, keep], r[:, keep], c, bits[:, keep], q[:, keep], k[:, keep], v, g,
+                                        beta, w=w[:, keep])
+    else:
+        full = oracle.decode_step_rowmax(codes, r, c, bits, q, k, v, g, beta, pv=pv)
+        part = oracle.decode_step_rowmax(codes[:, keep], r[:, keep], c, bits[:, keep], q[:, keep], k[:, keep], v,
+                                         g, beta)
+    assert np.array_equal(full[0][:, keep], part[0])
+    assert np.array_equal(full[1][:, keep], part[1]) and np.array_equal(full[2], part[2])
+    assert np.array_equal(full[1][:, ~keep], r[:, ~keep])       # pivots keep their (unused) row factor
