@@ -37,12 +37,14 @@
  * The pool is n_slots slot records of slot_bytes each, back to back.  A slot
  * record is the tile records of value heads 0 .. n_v_heads-1 in order.  The
  * tile record of head h, whose key rows have widths row_bits[h][0 .. d_k-1]
- * (each 8, 4 or 2; the same for every slot, the paper's fixed precision map):
+ * (each 8, 4 or 2, or 16 for an FP16 pivot row; the same for every slot, the
+ * paper's fixed precision map and pivot set, Section 3.2):
  *
- *  - Physical row order: the 8-bit rows in increasing logical row index,
- *    then the 4-bit rows, then the 2-bit rows.  n8, n4, n2 = row counts.
- *  - Row groups: each group holds 8/b physical rows of one width b -- one
- *    8-bit row, two 4-bit rows or four 2-bit rows -- filled in physical
+ *  - Physical row order: the pivot rows in increasing logical row index, then
+ *    the 8-bit rows, the 4-bit rows and the 2-bit rows, each the same way.
+ *    n16, n8, n4, n2 = row counts; n16 <= 32.
+ *  - Row groups: each group holds 8/b physical integer rows of one width b --
+ *    one 8-bit row, two 4-bit rows or four 2-bit rows -- filled in physical
  *    order.  A width's last group may have empty slots.  Groups are ordered
  *    8-bit, 4-bit, 2-bit: G = n8 + ceil(n4/2) + ceil(n2/4).
  *  - Codes region: G groups of d_v bytes each.  Byte j of a group holds
@@ -50,8 +52,15 @@
  *    order) occupies bits [s*b, s*b + b) as a b-bit two's-complement integer
  *    in [-q_b, q_b]; empty slots are 0.  The region is zero-padded to a
  *    multiple of 128 bytes.
- *  - Then r: d_k fp32 row scales in physical row order; then c: d_v fp32
- *    column scales.  The record is zero-padded to a multiple of 128 bytes.
+ *  - Pivot region: the n16 pivot rows in physical order, d_v IEEE binary16
+ *    values each (little-endian): 2 d_v bytes per row.
+ *  - Then r: d_k fp32 row scales in physical row order (a pivot row's entry
+ *    is carried but unused); then c: d_v fp32 column scales.  The record is
+ *    zero-padded to a multiple of 128 bytes.
+ *
+ * Pivot rows hold their values directly: every step updates them like any
+ * other row and stores X rounded to binary16 (nearest, ties to even); they
+ * take no part in the scale fits.
  *
  * So a 6-bit tile (64 rows @8 + 64 rows @4, d = 128) is 12,288 code bytes +
  * 1,024 scale bytes = 13,312 bytes, read once and its codes written once per
@@ -89,7 +98,7 @@ typedef struct {
     int32_t n_qk_heads;       /* Hqk >= 1, Hv % Hqk == 0; value head h reads q/k head h / (Hv/Hqk) */
     int32_t d_k;              /* key rows per tile, 1 .. 128 */
     int32_t d_v;              /* value columns per tile, 64 or 128 */
-    const uint8_t *row_bits;  /* host [Hv][d_k], each 2, 4 or 8; copied by stepq_pool_create */
+    const uint8_t *row_bits;  /* host [Hv][d_k], each 2, 4, 8 or 16 (pivot); copied by stepq_pool_create */
 } stepq_pool_desc;
 
 /* Size of the pool described by desc (layout above).  Either output may be
@@ -184,21 +193,34 @@ stepq_status stepq_decode_step_ex(stepq_pool *pool, const int32_t *slot_ids, int
  * decode step is in flight while the table changes.  A new pool has w = 1. */
 stepq_status stepq_pool_set_row_weight(stepq_pool *pool, const float *row_weight);
 
-/* Reconstruct S^_ij = r_i c_j q_ij / q_{b_i} (Section 4.3) for n slots into
- * out [n][Hv][d_k][d_v] fp32, logical row order.  Computed in fp32. */
+/* Reconstruct S^_ij = r_i c_j q_ij / q_{b_i} (Section 4.3; pivot rows: their
+ * binary16 values) for n slots into out [n][Hv][d_k][d_v] fp32, logical row
+ * order.  Computed in fp32. */
 stepq_status stepq_pool_dequant(const stepq_pool *pool, const int32_t *slot_ids, int32_t n, float *out,
                                 void *stream);
 
-/* Unpack n slots to raw codes [n][Hv][d_k][d_v] int8 (logical row order) and
- * scales r [n][Hv][d_k] (logical order), c [n][Hv][d_v].  Bit-exact. */
+/* Unpack n slots to raw codes [n][Hv][d_k][d_v] int8 (logical row order; 0
+ * on pivot rows) and scales r [n][Hv][d_k] (logical order), c [n][Hv][d_v].
+ * Bit-exact. */
 stepq_status stepq_pool_export(const stepq_pool *pool, const int32_t *slot_ids, int32_t n, int8_t *codes,
                                float *r, float *c, void *stream);
 
 /* Pack raw codes and scales (shapes as in stepq_pool_export) into n slots.
  * Codes must lie in [-q_b, q_b] of their row; out-of-range fields are
- * written modulo 2^b.  Bit-exact inverse of stepq_pool_export. */
+ * written modulo 2^b.  Bit-exact inverse of stepq_pool_export.  Pivot rows'
+ * codes are ignored and their values left as they are (see
+ * stepq_pool_import_pivots). */
 stepq_status stepq_pool_import(stepq_pool *pool, const int32_t *slot_ids, int32_t n, const int8_t *codes,
                                const float *r, const float *c, void *stream);
+
+/* Pivot-row values of n slots as binary16 bit patterns, pivots
+ * [n][Hv][d_k][d_v] uint16 in logical row order: export writes the pivot
+ * rows and zeros elsewhere; import reads the pivot rows only.  Bit-exact;
+ * with stepq_pool_export / _import they save and restore a whole slot. */
+stepq_status stepq_pool_export_pivots(const stepq_pool *pool, const int32_t *slot_ids, int32_t n,
+                                      uint16_t *pivots, void *stream);
+stepq_status stepq_pool_import_pivots(stepq_pool *pool, const int32_t *slot_ids, int32_t n,
+                                      const uint16_t *pivots, void *stream);
 
 /* Last failure message of the calling thread ("" if none). */
 const char *stepq_last_error(void);
@@ -217,6 +239,14 @@ const char *stepq_last_error(void);
  *   r [n_tiles][d_k], c [n_tiles][d_v] (outputs). */
 stepq_status stepq_setup_fit(int64_t n_tiles, int32_t d_k, int32_t d_v, const float *state,
                              const float *row_weight, float *r, float *c, int32_t n_threads);
+
+/* stepq_setup_fit with the tiles' widths row_bits [n_tiles][d_k] (NULL: as
+ * stepq_setup_fit): pivot rows (16) are left out of the column factors, as
+ * the paper fits only the integer rows (Appendix C.1).  Their r entries are
+ * fitted but unused. */
+stepq_status stepq_setup_fit_ex(int64_t n_tiles, int32_t d_k, int32_t d_v, const float *state,
+                                const float *row_weight, const uint8_t *row_bits, float *r, float *c,
+                                int32_t n_threads);
 
 /* Lifetime-aware bit allocation over key rows (Section 3.2, Eq. 6) with two
  * candidate widths lo < hi and an average budget lo <= budget <= hi.

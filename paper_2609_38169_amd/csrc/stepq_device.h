@@ -39,33 +39,37 @@ struct GroupRows {
     int x0;     // row-table index of slot 0
 };
 
+// Physical rows: the n16 pivot rows first, then the integer rows 8, 4, 2;
+// the row table and the groups cover the integer rows only.
 __device__ __forceinline__ GroupRows group_rows(const HeadInfo &hi, int g)
 {
-    if (g < hi.g8) return {8, 1, g, hi.n8, g};
+    const int P = hi.n16;
+    if (g < hi.g8) return {8, 1, P + g, P + hi.n8, g};
     if (g < hi.g8 + hi.g4) {
         const int k = g - hi.g8;
-        return {4, 2, hi.n8 + 2 * k, hi.n8 + hi.n4, hi.n8 + 2 * k};
+        return {4, 2, P + hi.n8 + 2 * k, P + hi.n8 + hi.n4, hi.n8 + 2 * k};
     }
     const int k = g - hi.g8 - hi.g4;
-    return {2, 4, hi.n8 + hi.n4 + 4 * k, hi.n8 + hi.n4 + hi.n2, hi.n8 + 2 * hi.g4 + 4 * k};
+    return {2, 4, P + hi.n8 + hi.n4 + 4 * k, P + hi.n8 + hi.n4 + hi.n2, hi.n8 + 2 * hi.g4 + 4 * k};
 }
 
 // Row-table slot x -> physical row (or -1 for an empty slot) and its width.
 __device__ __forceinline__ int slot_row(const HeadInfo &hi, int x, int &bw)
 {
+    const int P = hi.n16;
     if (x < hi.n8) {
         bw = 8;
-        return x;
+        return P + x;
     }
     if (x < hi.n8 + 2 * hi.g4) {
         bw = 4;
         const int kk = x - hi.n8;
-        return kk < hi.n4 ? hi.n8 + kk : -1;
+        return kk < hi.n4 ? P + hi.n8 + kk : -1;
     }
     bw = 2;
     if (x < hi.n8 + 2 * hi.g4 + 4 * hi.g2) {
         const int kk = x - hi.n8 - 2 * hi.g4;
-        return kk < hi.n2 ? hi.n8 + hi.n4 + kk : -1;
+        return kk < hi.n2 ? P + hi.n8 + hi.n4 + kk : -1;
     }
     return -1;
 }
@@ -124,6 +128,10 @@ struct DecodeShared {
     float4 red[2][256 / (DV / 4)][DV / 4];
     float bcol[DV];                      // delta_j / c_j
     float kap[4];
+    // FP16 pivot rows (generic bodies only), by physical row p < n16:
+    // (k_i d_i, q_i d_i, d_i, beta k_i) with d_i the row's gate (alpha for GDN)
+    float4 pvc[kMaxPivots];
+    float cpiv[DV];                      // c_j, for the pivot rows' share of S^T k and S^T q
 };
 
 struct TileCtx {
@@ -169,8 +177,8 @@ __device__ __forceinline__ RowColOps load_ops(const DecodeArgs &a, int tile, int
 // returns q.k.  Rows are read through the physical -> logical permutation
 // from the LDS copy of k and q.
 template <bool DIAG, int DV>
-__device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float beta, const RowColOps &op,
-                                               DecodeShared<DV> &sh)
+__device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float alpha, float beta,
+                                               const RowColOps &op, DecodeShared<DV> &sh)
 {
     const int tid = threadIdx.x;
     if (tid < dk) {
@@ -180,8 +188,18 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
         sh.sperm[tid] = op.perm;
         if constexpr (DIAG) sh.sd[tid] = op.d;
     }
+    if (tid < DV) sh.cpiv[tid] = op.c;
     __syncthreads();
     float kq = 0.f;
+    if (tid < hi.n16) {
+        // pivot row p = tid (physical rows 0 .. n16-1); it also takes its share of q.k
+        const int i = sh.sperm[tid];
+        const float d = DIAG ? sh.sd[i] : alpha;
+        const float kd = DIAG ? sh.sk[i] * d : sh.sk[i];     // the scalar gate is applied with the columns
+        const float qd = DIAG ? sh.sq[i] * d : sh.sq[i];
+        sh.pvc[tid] = make_float4(kd, qd, d, beta * sh.sk[i]);
+        kq = sh.sq[i] * sh.sk[i];
+    }
     if (tid < kSlotTable) {
         const int x = tid;
         int bw;
@@ -203,7 +221,7 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
             qt = qi * rs;
             av = beta * ki * qb * __builtin_amdgcn_rcpf(rp);
             al = di * (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
-            kq = qi * ki;
+            kq += qi * ki;
         }
         sh.kq[x] = make_float2(kt, qt);
         sh.av[x] = av;
@@ -213,6 +231,95 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
     if ((tid & 63) == 0) sh.kap[tid >> 6] = kq;
     __syncthreads();
     return (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
+}
+
+// ---- FP16 pivot rows (generic bodies): thread (slice, cg) holds columns
+// 4 cg .. 4 cg + 3 of pivot rows p = slice + NSL m, as 4 binary16 values.
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <int DV>
+struct PivotRegs {
+    static constexpr int NSL = 256 / (DV / 4);
+    static constexpr int M = (kMaxPivots + NSL - 1) / NSL;
+    u32x2 v[M];
+};
+
+template <int DV>
+__device__ __forceinline__ u32x2 *pivot_ptr(const TileCtx &t, int p, int cg)
+{
+    return reinterpret_cast<u32x2 *>(reinterpret_cast<uint8_t *>(t.codes) + t.hi.piv_off +
+                                     static_cast<uint32_t>(p) * (2u * DV) + 8u * static_cast<uint32_t>(cg));
+}
+
+template <int DV>
+__device__ __forceinline__ void pivot_load(const TileCtx &t, int slice, int cg, PivotRegs<DV> &pr)
+{
+#pragma unroll
+    for (int m = 0; m < PivotRegs<DV>::M; ++m) {
+        const int p = slice + PivotRegs<DV>::NSL * m;
+        pr.v[m] = p < t.hi.n16 ? __builtin_nontemporal_load(pivot_ptr<DV>(t, p, cg)) : u32x2{0u, 0u};
+    }
+}
+
+__device__ __forceinline__ float half_lo(uint32_t u) { return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(u))); }
+__device__ __forceinline__ float half_hi(uint32_t u) { return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(u >> 16))); }
+
+__device__ __forceinline__ uint32_t pack_halves(float a, float b)
+{
+    const uint16_t lo = __builtin_bit_cast(uint16_t, static_cast<_Float16>(a));   // round to nearest even
+    const uint16_t hi = __builtin_bit_cast(uint16_t, static_cast<_Float16>(b));
+    return static_cast<uint32_t>(lo) | (static_cast<uint32_t>(hi) << 16);
+}
+
+// The pivot rows' share of the column partials, pre-divided by c_j (the
+// column phase multiplies the partials by c_j).
+template <int DV>
+__device__ __forceinline__ void pivot_acc(const TileCtx &t, int slice, int cg, const PivotRegs<DV> &pr,
+                                          const DecodeShared<DV> &sh, float (&acK)[4], float (&acQ)[4])
+{
+    if (t.hi.n16 == 0) return;
+    const float4 c4 = *reinterpret_cast<const float4 *>(&sh.cpiv[4 * cg]);
+    const float rc[4] = {__builtin_amdgcn_rcpf(c4.x), __builtin_amdgcn_rcpf(c4.y), __builtin_amdgcn_rcpf(c4.z),
+                         __builtin_amdgcn_rcpf(c4.w)};
+#pragma unroll
+    for (int m = 0; m < PivotRegs<DV>::M; ++m) {
+        const int p = slice + PivotRegs<DV>::NSL * m;
+        if (p < t.hi.n16) {
+            const float4 k = sh.pvc[p];
+            const float sv[4] = {half_lo(pr.v[m].x), half_hi(pr.v[m].x), half_lo(pr.v[m].y), half_hi(pr.v[m].y)};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float s = sv[e] * rc[e];
+                acK[e] = fmaf(k.x, s, acK[e]);
+                acQ[e] = fmaf(k.y, s, acQ[e]);
+            }
+        }
+    }
+}
+
+// New pivot values X_pj = d_i S_pj + beta k_i delta_j in binary16, stored in
+// place (delta_j = bc_j c_j).
+template <int DV>
+__device__ __forceinline__ void pivot_update(const TileCtx &t, int slice, int cg, const PivotRegs<DV> &pr,
+                                             const DecodeShared<DV> &sh, const float (&bc)[4])
+{
+    if (t.hi.n16 == 0) return;
+    const float4 c4 = *reinterpret_cast<const float4 *>(&sh.cpiv[4 * cg]);
+    const float dl[4] = {bc[0] * c4.x, bc[1] * c4.y, bc[2] * c4.z, bc[3] * c4.w};
+#pragma unroll
+    for (int m = 0; m < PivotRegs<DV>::M; ++m) {
+        const int p = slice + PivotRegs<DV>::NSL * m;
+        if (p < t.hi.n16) {
+            const float4 k = sh.pvc[p];
+            const float sv[4] = {half_lo(pr.v[m].x), half_hi(pr.v[m].x), half_lo(pr.v[m].y), half_hi(pr.v[m].y)};
+            float x[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[e] = fmaf(k.w, dl[e], k.z * sv[e]);
+            __builtin_nontemporal_store(u32x2{pack_halves(x[0], x[1]), pack_halves(x[2], x[3])},
+                                        pivot_ptr<DV>(t, p, cg));
+        }
+    }
 }
 
 // Uniform layouts: table slot = physical row = tid, widths known at compile time.

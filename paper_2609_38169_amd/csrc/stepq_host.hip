@@ -62,18 +62,21 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
     size_t off = 0;
     for (int h = 0; h < Hv; ++h) {
         const uint8_t *b = d->row_bits + static_cast<size_t>(h) * dk;
-        int n8 = 0, n4 = 0, n2 = 0;
+        int n16 = 0, n8 = 0, n4 = 0, n2 = 0;
         for (int i = 0; i < dk; ++i) {
-            if (b[i] == 8) ++n8;
+            if (b[i] == 16) ++n16;
+            else if (b[i] == 8) ++n8;
             else if (b[i] == 4) ++n4;
             else if (b[i] == 2) ++n2;
-            else return fail(STEPQ_E_INVALID, "row_bits entries must be 2, 4 or 8");
+            else return fail(STEPQ_E_INVALID, "row_bits entries must be 2, 4, 8 or 16");
         }
+        if (n16 > stepq::kMaxPivots) return fail(STEPQ_E_UNSUPPORTED, "at most 32 pivot (16) rows per head");
         int p = 0;
-        for (int width : {8, 4, 2})
+        for (int width : {16, 8, 4, 2})
             for (int i = 0; i < dk; ++i)
                 if (b[i] == width) (*perm)[static_cast<size_t>(h) * dk + p++] = static_cast<uint8_t>(i);
         HeadInfo &hi = (*heads)[h];
+        hi.n16 = static_cast<uint16_t>(n16);
         hi.n8 = static_cast<uint16_t>(n8);
         hi.n4 = static_cast<uint16_t>(n4);
         hi.n2 = static_cast<uint16_t>(n2);
@@ -83,15 +86,17 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
         hi.groups = static_cast<uint32_t>(hi.g8 + hi.g4 + hi.g2);
         hi.layout = 0;
         // compile-time bodies: d = 128, whole word-steps of one width, no empty slots
-        if (dv == 128 && dk == 128 && n4 == 2 * hi.g4 && n2 == 4 * hi.g2 && hi.g8 % 8 == 0 && hi.g4 % 8 == 0 &&
+        if (dv == 128 && dk == 128 && n16 == 0 && n4 == 2 * hi.g4 && n2 == 4 * hi.g2 && hi.g8 % 8 == 0 && hi.g4 % 8 == 0 &&
             hi.g2 % 8 == 0)
             for (int L = 0; L < stepq::kNumUniformLayouts; ++L) {
                 const stepq::UniformLayout &u = stepq::kUniformLayouts[L];
                 if (u.m8 * 8 == hi.g8 && u.m4 * 8 == hi.g4 && u.m2 * 8 == hi.g2) hi.layout = L + 1;
             }
         const size_t creg = round128(static_cast<size_t>(hi.groups) * dv);
-        const size_t tb = round128(creg + 4u * static_cast<size_t>(dk) + 4u * static_cast<size_t>(dv));
-        hi.r_off = static_cast<uint32_t>(creg);
+        const size_t preg = round128(static_cast<size_t>(n16) * 2u * dv);
+        const size_t tb = round128(creg + preg + 4u * static_cast<size_t>(dk) + 4u * static_cast<size_t>(dv));
+        hi.piv_off = static_cast<uint32_t>(creg);
+        hi.r_off = static_cast<uint32_t>(creg + preg);
         hi.tile_bytes = static_cast<uint32_t>(tb);
         hi.tile_off = static_cast<uint32_t>(off);
         off += tb;
@@ -388,6 +393,30 @@ stepq_status stepq_pool_export(const stepq_pool *p, const int32_t *slot_ids, int
     a.r_out = r;
     a.c_out = c;
     return tile_op(p, slot_ids, n, a, stepq::TileOp::Export, stream);
+}
+
+stepq_status stepq_pool_export_pivots(const stepq_pool *p, const int32_t *slot_ids, int32_t n, uint16_t *pivots,
+                                      void *stream)
+{
+    stepq_status st = common_checks(p, slot_ids, n);
+    if (st != STEPQ_OK) return st;
+    if (n == 0) return STEPQ_OK;
+    if (!pivots) return fail(STEPQ_E_INVALID, "NULL output pointer");
+    stepq::TileArgs a{};
+    a.piv_out = pivots;
+    return tile_op(p, slot_ids, n, a, stepq::TileOp::ExportPivots, stream);
+}
+
+stepq_status stepq_pool_import_pivots(stepq_pool *p, const int32_t *slot_ids, int32_t n, const uint16_t *pivots,
+                                      void *stream)
+{
+    stepq_status st = common_checks(p, slot_ids, n);
+    if (st != STEPQ_OK) return st;
+    if (n == 0) return STEPQ_OK;
+    if (!pivots) return fail(STEPQ_E_INVALID, "NULL pivot pointer");
+    stepq::TileArgs a{};
+    a.piv_in = pivots;
+    return tile_op(p, slot_ids, n, a, stepq::TileOp::ImportPivots, stream);
 }
 
 stepq_status stepq_pool_dequant(const stepq_pool *p, const int32_t *slot_ids, int32_t n, float *out, void *stream)

@@ -12,8 +12,10 @@ namespace stepq {
 struct HeadInfo {
     uint32_t tile_off;    // byte offset of the tile inside a slot record
     uint32_t tile_bytes;  // record size (multiple of 128)
-    uint32_t r_off;       // byte offset of r inside the tile (= padded codes region)
-    uint16_t n8, n4, n2;  // rows of each width
+    uint32_t piv_off;     // byte offset of the pivot rows (= padded codes region)
+    uint32_t r_off;       // byte offset of r inside the tile (after the pivot rows)
+    uint16_t n16;         // pivot rows (binary16 values, physical rows 0 .. n16-1)
+    uint16_t n8, n4, n2;  // integer rows of each width
     uint16_t g8, g4, g2;  // row groups of each width
     uint32_t groups;      // g8 + g4 + g2
     uint32_t layout;      // index into kUniformLayouts + 1, or 0 for the generic path
@@ -41,6 +43,7 @@ constexpr int kNumUniformLayouts = sizeof(kUniformLayouts) / sizeof(kUniformLayo
 // Its size is at most d_k + 4.
 constexpr int kMaxDk = 128;
 constexpr int kSlotTable = kMaxDk + 4;
+constexpr int kMaxPivots = 32;    // FP16 pivot rows per head
 
 // n / d for 0 <= n < 2^31 by multiply-high (Granlund-Montgomery), with the
 // constants prepared on the host so that uniform quotients stay scalar.
@@ -67,7 +70,7 @@ struct DecodeArgs {
     int32_t batch;
 };
 
-enum class TileOp : int { Load = 0, Import = 1, Export = 2, Dequant = 3 };
+enum class TileOp : int { Load = 0, Import = 1, Export = 2, Dequant = 3, ExportPivots = 4, ImportPivots = 5 };
 
 struct TileArgs {
     PoolView pool;
@@ -80,6 +83,8 @@ struct TileArgs {
     int8_t *codes_out;       // Export
     float *r_out, *c_out;    // Export
     float *deq_out;          // Dequant: [n][Hv][dk][dv]
+    const uint16_t *piv_in;  // ImportPivots: [n][Hv][dk][dv] binary16, pivot rows read
+    uint16_t *piv_out;       // ExportPivots: [n][Hv][dk][dv] binary16, pivot rows written, others 0
 };
 
 // pool_layout: the uniform layout shared by every head (1-based), or 0.

@@ -92,8 +92,10 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
         const int g = slice + NSL * m;
         w[m] = g < ngroups ? __builtin_nontemporal_load(t.codes + tid + 256 * m) : 0u;
     }
+    PivotRegs<DV> pr;
+    pivot_load<DV>(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    const float kappa = row_constants<DIAG, DV>(t.hi, a.pool.dk, t.beta, op, sh);
+    const float kappa = row_constants<DIAG, DV>(t.hi, a.pool.dk, t.alpha, t.beta, op, sh);
 
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
     float U[16];
@@ -107,10 +109,12 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
             else unpack_acc<2>(w[m], sh.kq, gr.x0, U, acK, acQ);
         }
     }
+    pivot_acc<DV>(t, slice, cg, pr, sh, acK, acQ);
     column_phase<DV>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, acK, acQ, op.c, op.v);
 
     const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
+    pivot_update<DV>(t, slice, cg, pr, sh, bc);
 #pragma unroll
     for (int m = 0; m < MMAX; ++m) {
         const int g = slice + NSL * m;
@@ -204,12 +208,36 @@ __global__ __launch_bounds__(256) void tile_kernel(TileArgs a)
         for (int j = tid; j < dv; j += 256) cc[j] = a.c_in[tdv + j];
         // zero padding: end of the codes region and end of the record
         uint32_t *rec32 = reinterpret_cast<uint32_t *>(rec);
-        for (uint32_t d = hi.groups * CG + tid; d < hi.r_off / 4; d += 256) rec32[d] = 0u;
+        for (uint32_t d = hi.groups * CG + tid; d < hi.piv_off / 4; d += 256) rec32[d] = 0u;
         for (uint32_t d = (hi.r_off + 4u * (dk + dv)) / 4 + tid; d < hi.tile_bytes / 4; d += 256) rec32[d] = 0u;
     }
     if constexpr (OP == TileOp::Export) {
         for (int p = tid; p < dk; p += 256) a.r_out[tdk + perm[p]] = rr[p];
         for (int j = tid; j < dv; j += 256) a.c_out[tdv + j] = cc[j];
+    }
+
+    // FP16 pivot rows: physical rows 0 .. n16-1, d_v binary16 values each
+    uint16_t *piv = reinterpret_cast<uint16_t *>(rec + hi.piv_off);
+    const int npv = static_cast<int>(hi.n16) * dv;
+    if constexpr (OP == TileOp::ExportPivots || OP == TileOp::ImportPivots) {
+        for (int e = tid; e < dk * dv; e += 256) {
+            const int p = e / dv, j = e - p * dv;
+            const size_t o = (tdk + perm[p]) * dv + j;
+            if constexpr (OP == TileOp::ExportPivots) a.piv_out[o] = p < hi.n16 ? piv[e] : static_cast<uint16_t>(0);
+            else if (p < hi.n16) piv[e] = a.piv_in[o];
+        }
+        return;
+    } else {
+        for (int e = tid; e < npv; e += 256) {
+            const int p = e / dv, j = e - p * dv;
+            const size_t o = (tdk + perm[p]) * dv + j;
+            if constexpr (OP == TileOp::Load)
+                piv[e] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(a.state[o]));    // nearest even
+            else if constexpr (OP == TileOp::Export)
+                a.codes_out[o] = 0;
+            else if constexpr (OP == TileOp::Dequant)
+                a.deq_out[o] = static_cast<float>(__builtin_bit_cast(_Float16, piv[e]));
+        }
     }
 
     const int nw = static_cast<int>(hi.groups) * CG;
@@ -306,6 +334,12 @@ hipError_t launch_tile_op(const TileArgs &a, TileOp op, hipStream_t stream)
     case TileOp::Import: hipLaunchKernelGGL(tile_kernel<TileOp::Import>, dim3(grid), dim3(256), 0, stream, a); break;
     case TileOp::Export: hipLaunchKernelGGL(tile_kernel<TileOp::Export>, dim3(grid), dim3(256), 0, stream, a); break;
     case TileOp::Dequant: hipLaunchKernelGGL(tile_kernel<TileOp::Dequant>, dim3(grid), dim3(256), 0, stream, a); break;
+    case TileOp::ExportPivots:
+        hipLaunchKernelGGL(tile_kernel<TileOp::ExportPivots>, dim3(grid), dim3(256), 0, stream, a);
+        break;
+    case TileOp::ImportPivots:
+        hipLaunchKernelGGL(tile_kernel<TileOp::ImportPivots>, dim3(grid), dim3(256), 0, stream, a);
+        break;
     }
     return hipGetLastError();
 }

@@ -438,21 +438,25 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
         const int g = slice + NSL * m;
         w[m] = g < ngroups ? __builtin_nontemporal_load(t.codes + tid + 256 * m) : 0u;
     }
+    PivotRegs<DV> pr;
+    pivot_load<DV>(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
     if (tid < DV) sh.ccol[tid] = op.c;
     if (tid < dk) sh.wphys[tid] = a.pool.roww[t.h * dk + tid];
-    const float kappa = row_constants<DIAG, DV>(t.hi, dk, t.beta, op, sh.d);
+    const float kappa = row_constants<DIAG, DV>(t.hi, dk, t.alpha, t.beta, op, sh.d);
 
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
     each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {
         float U[16];
         unpack_acc<decltype(bw)::value>(w[m], sh.d.kq, gr.x0, U, acK, acQ);
     });
+    pivot_acc<DV>(t, slice, cg, pr, sh.d, acK, acQ);
     column_phase<DV>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh.d, kappa, acK, acQ, op.c, op.v);
 
     float bc[4], cc[4];
     ld4(&sh.d.bcol[4 * cg], bc);
     ld4(&sh.ccol[4 * cg], cc);
+    pivot_update<DV>(t, slice, cg, pr, sh.d, bc);      // pivot rows take no part in the fits
 
     // pass 1: row partials straight to LDS (each (lane, slot) has one writer)
     each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {

@@ -11,7 +11,8 @@
 
 namespace {
 
-void fit_tiles(int64_t t0, int64_t t1, int32_t dk, int32_t dv, const float *S, const float *w, float *r, float *c)
+void fit_tiles(int64_t t0, int64_t t1, int32_t dk, int32_t dv, const float *S, const float *w, const uint8_t *bits,
+               float *r, float *c)
 {
     const double fl = std::ldexp(1.0, -60);
     std::vector<double> rd(dk);
@@ -32,6 +33,7 @@ void fit_tiles(int64_t t0, int64_t t1, int32_t dk, int32_t dv, const float *S, c
         }
         std::fill(cmax.begin(), cmax.end(), 0.0);
         for (int i = 0; i < dk; ++i) {
+            if (bits && bits[t * dk + i] == 16) continue;    // pivot rows keep their own values
             const float *row = St + static_cast<int64_t>(i) * dv;
             const double inv = rd[i];
             for (int j = 0; j < dv; ++j) {
@@ -55,13 +57,20 @@ extern "C" {
 stepq_status stepq_setup_fit(int64_t n_tiles, int32_t d_k, int32_t d_v, const float *state, const float *row_weight,
                              float *r, float *c, int32_t n_threads)
 {
+    return stepq_setup_fit_ex(n_tiles, d_k, d_v, state, row_weight, nullptr, r, c, n_threads);
+}
+
+stepq_status stepq_setup_fit_ex(int64_t n_tiles, int32_t d_k, int32_t d_v, const float *state,
+                                const float *row_weight, const uint8_t *row_bits, float *r, float *c,
+                                int32_t n_threads)
+{
     if (n_tiles < 0 || d_k < 1 || d_v < 1) return STEPQ_E_INVALID;
     if (n_tiles == 0) return STEPQ_OK;
     if (!state || !r || !c) return STEPQ_E_INVALID;
     int nt = n_threads > 0 ? n_threads : static_cast<int>(std::max(1u, std::thread::hardware_concurrency()));
     nt = static_cast<int>(std::min<int64_t>(nt, n_tiles));
     if (nt <= 1) {
-        fit_tiles(0, n_tiles, d_k, d_v, state, row_weight, r, c);
+        fit_tiles(0, n_tiles, d_k, d_v, state, row_weight, row_bits, r, c);
         return STEPQ_OK;
     }
     std::vector<std::thread> pool;
@@ -69,7 +78,7 @@ stepq_status stepq_setup_fit(int64_t n_tiles, int32_t d_k, int32_t d_v, const fl
     for (int k = 0; k < nt; ++k) {
         const int64_t t0 = k * per, t1 = std::min<int64_t>(n_tiles, t0 + per);
         if (t0 >= t1) break;
-        pool.emplace_back(fit_tiles, t0, t1, d_k, d_v, state, row_weight, r, c);
+        pool.emplace_back(fit_tiles, t0, t1, d_k, d_v, state, row_weight, row_bits, r, c);
     }
     for (auto &th : pool) th.join();
     return STEPQ_OK;

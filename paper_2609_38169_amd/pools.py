@@ -29,7 +29,8 @@ def build_pool(w: W.Workload, layer: int = 0, device="cuda", chunk: int = 128, n
     for s0 in range(0, w.n_slots, chunk):
         slots = range(s0, min(w.n_slots, s0 + chunk))
         S = W.initial_state(w, layer, slots, device=dev)
-        r, c = stepq.stepq_setup_fit(S.cpu(), n_threads=n_threads)
+        r, c = stepq.stepq_setup_fit(S.cpu(), n_threads=n_threads,
+                                     row_bits=np.broadcast_to(b, (len(slots),) + b.shape) if np.any(b == 16) else None)
         ids = torch.arange(slots.start, slots.stop, dtype=torch.int32, device=dev)
         pool.load(ids, S, torch.from_numpy(r).to(dev), torch.from_numpy(c).to(dev))
         del S

@@ -27,7 +27,8 @@ EXPORTED = (
     "stepq_pool_bytes", "stepq_pool_create", "stepq_pool_destroy", "stepq_pool_device_ptr",
     "stepq_pool_load", "stepq_decode_step", "stepq_decode_step_kda", "stepq_decode_step_ex",
     "stepq_pool_set_row_weight", "stepq_pool_dequant", "stepq_pool_export", "stepq_pool_import",
-    "stepq_last_error", "stepq_setup_fit", "stepq_setup_lifetime_bits",
+    "stepq_pool_export_pivots", "stepq_pool_import_pivots", "stepq_last_error", "stepq_setup_fit",
+    "stepq_setup_fit_ex", "stepq_setup_lifetime_bits",
 )
 
 
@@ -67,6 +68,9 @@ def lib():
             "stepq_pool_dequant": ([P, P, i32, P, P], st),
             "stepq_pool_export": ([P, P, i32, P, P, P, P], st),
             "stepq_pool_import": ([P, P, i32, P, P, P, P], st),
+            "stepq_pool_export_pivots": ([P, P, i32, P, P], st),
+            "stepq_pool_import_pivots": ([P, P, i32, P, P], st),
+            "stepq_setup_fit_ex": ([i64, i32, i32, P, P, P, P, P, i32], st),
             "stepq_last_error": ([], ctypes.c_char_p),
             "stepq_setup_fit": ([i64, i32, i32, P, P, P, P, i32], st),
             "stepq_setup_lifetime_bits": ([P, i32, i32, i32, i32, ctypes.c_double, i32, i32, P], st),
@@ -207,6 +211,12 @@ class Pool:
     def import_(self, slot_ids, codes, r, c, stream=None):
         stepq_pool_import(self, slot_ids, codes, r, c, stream)
 
+    def export_pivots(self, slot_ids, pivots, stream=None):
+        stepq_pool_export_pivots(self, slot_ids, pivots, stream)
+
+    def import_pivots(self, slot_ids, pivots, stream=None):
+        stepq_pool_import_pivots(self, slot_ids, pivots, stream)
+
 
 def stepq_pool_create(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits, device=None) -> Pool:
     return Pool(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits, device)
@@ -314,14 +324,38 @@ def stepq_pool_import(pool: Pool, slot_ids, codes, r, c, stream=None):
         _dev(c, "c", torch.float32, (n, P.Hv, P.dv), P.device), _stream(stream)))
 
 
+def stepq_pool_export_pivots(pool: Pool, slot_ids, pivots, stream=None):
+    """pivots: [n][Hv][d_k][d_v] torch.int16 or uint16 on the pool's device
+    (binary16 bit patterns of the pivot rows, zeros elsewhere)."""
+    n, ids = _ids(pool, slot_ids)
+    P = pool
+    _check(lib().stepq_pool_export_pivots(pool.handle, ids, n,
+                                          _dev16(pivots, "pivots", (n, P.Hv, P.dk, P.dv), P.device), _stream(stream)))
+
+
+def stepq_pool_import_pivots(pool: Pool, slot_ids, pivots, stream=None):
+    n, ids = _ids(pool, slot_ids)
+    P = pool
+    _check(lib().stepq_pool_import_pivots(pool.handle, ids, n,
+                                          _dev16(pivots, "pivots", (n, P.Hv, P.dk, P.dv), P.device), _stream(stream)))
+
+
+def _dev16(t, name, shape, device):
+    # binary16 bit patterns travel in a 16-bit integer tensor
+    if not isinstance(t, torch.Tensor) or t.dtype not in (torch.int16, torch.uint16):
+        raise TypeError(f"{name} must be a torch.int16 or torch.uint16 tensor of binary16 bit patterns")
+    return _dev(t, name, t.dtype, shape, device)
+
+
 def stepq_last_error() -> str:
     return lib().stepq_last_error().decode()
 
 
 # ---------------------------------------------------------------------------
 # CPU setup step (host arrays)
-def stepq_setup_fit(state, row_weight=None, n_threads: int = 0):
-    """state: [..., d_k, d_v] float32 (host) -> (r [..., d_k], c [..., d_v]) float32 numpy."""
+def stepq_setup_fit(state, row_weight=None, n_threads: int = 0, row_bits=None):
+    """state: [..., d_k, d_v] float32 (host) -> (r [..., d_k], c [..., d_v]) float32 numpy.
+    row_bits [..., d_k] (optional): pivot rows (16) are left out of c."""
     S = np.ascontiguousarray(state.numpy() if isinstance(state, torch.Tensor) else state, dtype=np.float32)
     dk, dv = S.shape[-2:]
     lead = S.shape[:-2]
@@ -331,9 +365,12 @@ def stepq_setup_fit(state, row_weight=None, n_threads: int = 0):
     w = None
     if row_weight is not None:
         w = np.ascontiguousarray(np.broadcast_to(row_weight, lead + (dk,)), dtype=np.float32)
-    _check(lib().stepq_setup_fit(n, dk, dv, S.ctypes.data_as(ctypes.c_void_p),
-                                 None if w is None else w.ctypes.data_as(ctypes.c_void_p),
-                                 r.ctypes.data_as(ctypes.c_void_p), c.ctypes.data_as(ctypes.c_void_p), n_threads))
+    vp = lambda a: None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+    if row_bits is None:
+        _check(lib().stepq_setup_fit(n, dk, dv, vp(S), vp(w), vp(r), vp(c), n_threads))
+    else:
+        b = np.ascontiguousarray(np.broadcast_to(row_bits, lead + (dk,)), dtype=np.uint8)
+        _check(lib().stepq_setup_fit_ex(n, dk, dv, vp(S), vp(w), vp(b), vp(r), vp(c), n_threads))
     return r, c
 
 

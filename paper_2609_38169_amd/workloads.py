@@ -96,7 +96,7 @@ def _mix(*parts: int) -> int:
 
 _STREAM = {"init": 1, "q": 2, "k": 3, "v": 4, "alpha": 5, "beta": 6,
            "bits": 7, "calib": 8, "slots": 9, "gain_r": 10, "gain_c": 11, "kda": 12,
-           "roww": 13}
+           "roww": 13, "pivots": 14}
 
 
 def _gen(device, w: Workload, layer: int, step: int, stream: str, chunk: int = 0) -> torch.Generator:
@@ -189,6 +189,20 @@ def row_weight_draw(w: Workload, layer: int = 0, sigma: float = 0.5) -> torch.Te
     g = _gen("cpu", w, layer, 0, "roww")
     x = torch.randn((w.n_v_heads, w.d_k), generator=g, dtype=torch.float64) * sigma
     return torch.exp(x - x.mean(dim=1, keepdim=True)).to(torch.float32)
+
+
+def pivot_mask_draw(w: Workload, layer: int = 0, head_frac: float = 0.25, max_rows: int = 3) -> torch.Tensor:
+    """Synthetic FP16 pivot rows, bool [Hv][d_k]: a seeded share of the heads
+    get 1 .. max_rows pivot rows at seeded positions (the paper keeps a few
+    hundred rows of a model in FP16, spread over its heads)."""
+    g = _gen("cpu", w, layer, 0, "pivots")
+    mask = torch.zeros((w.n_v_heads, w.d_k), dtype=torch.bool)
+    pick = torch.rand(w.n_v_heads, generator=g) < head_frac
+    count = torch.randint(1, max_rows + 1, (w.n_v_heads,), generator=g)
+    for h in range(w.n_v_heads):
+        if pick[h]:
+            mask[h, torch.randperm(w.d_k, generator=g)[: int(count[h])]] = True
+    return mask
 
 
 def calibration_gates(w: Workload, layer: int = 0) -> torch.Tensor:

@@ -35,6 +35,14 @@ O_ABS, O_REL = 1e-5, 1e-3
 # codes that sit within TIE_WINDOW of a rounding boundary: the oracle bounds
 # the factor over all such roundings (c_range) and the GPU's must lie inside.
 SCALE_REL = 1e-5
+# Pivot rows hold X rounded to binary16.  X carries the fp32 error of the
+# update (~1e-7 of its terms), and binary16 spacing is only 2^-11 relative,
+# so fp32 and fp64 land on different sides of a binary16 rounding boundary
+# about 2e-4 of the time (codes, with spacing 1 on values up to 127, see
+# ties ~20x less often).  Each pivot value is checked to be a correct
+# rounding of X within the fp32 error; at most PIVOT_MISMATCH_FRAC may
+# differ from the oracle's.
+PIVOT_MISMATCH_FRAC = 2e-3
 
 
 def bits_for(w: W.Workload, layer: int = 0) -> np.ndarray:
@@ -106,6 +114,7 @@ def compare_refit(g_codes, g_r, g_c, o_codes, o_r, o_c, y, c_range, bits, what: 
     qb = (2.0 ** (bits.astype(np.int64) - 1) - 1)[:, :, None]
     ys = y * (o_r / g_r)[:, :, None] * (o_c / g_c)[:, None, :]
     expect = np.clip(np.rint(ys), -qb, qb).astype(np.int16)
+    expect[np.broadcast_to((bits == 16)[:, :, None], expect.shape)] = 0     # pivot rows carry no codes
     diff = g_codes.astype(np.int16) - expect
     bad = np.nonzero(diff)
     n_bad = bad[0].size
@@ -121,6 +130,33 @@ def compare_refit(g_codes, g_r, g_c, o_codes, o_r, o_c, y, c_range, bits, what: 
     return int(np.count_nonzero(g_codes != o_codes)), int((dc > SCALE_REL).sum())
 
 
+def _half_ulp(x):
+    """Spacing of binary16 values around |x| (subnormal spacing 2^-24)."""
+    a = np.abs(x)
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.exp2(np.maximum(e - 10, -24))
+
+
+def compare_pivots(g_pv, o_pv, X, mask, what: str = "pivots", frac: float = PIVOT_MISMATCH_FRAC):
+    """Pivot rows (mask [n][dk]): the GPU's binary16 value must be a correct
+    rounding of the oracle's X up to the error of X in fp32 arithmetic (1% of
+    half a binary16 spacing, or 1e-6 of the row's largest |X| for values near
+    zero, where X is a difference of much larger terms), so it can differ from
+    the oracle's own rounding only at a rounding tie; at most one value plus
+    ``frac`` of them may differ (a single comparison holds only a few
+    thousand pivot values).  Returns the number that differ."""
+    sel = np.broadcast_to(mask[:, :, None], g_pv.shape)
+    g = g_pv[sel].view(np.float16).astype(np.float64)
+    x = X[sel]
+    row_mag = np.broadcast_to(np.abs(X).max(axis=2, keepdims=True), X.shape)[sel]
+    allow = 0.5 * _half_ulp(x) * 1.01 + 1e-6 * row_mag
+    assert np.all(np.abs(g - x) <= allow), \
+        f"{what}: a pivot value is not a binary16 rounding of X (max err {np.max(np.abs(g - x) / _half_ulp(x)):.3f} ulp)"
+    n_bad = int(np.count_nonzero(g_pv[sel] != o_pv[sel]))
+    assert n_bad <= 1 + frac * g.size, f"{what}: {n_bad} of {g.size} pivot values differ"
+    return n_bad
+
+
 def compare_out(gpu: np.ndarray, orc: np.ndarray, what: str = "o"):
     err = np.abs(gpu.astype(np.float64) - orc)
     lim = O_ABS + O_REL * np.abs(orc)
@@ -134,7 +170,7 @@ class Lockstep:
     ``check_rows`` (batch rows whose slots are compared each step)."""
 
     def __init__(self, w: W.Workload, pool, slots: torch.Tensor, bits: np.ndarray, check_rows: np.ndarray,
-                 S0_check: np.ndarray, layer: int = 0, refit: bool = False, row_weight=None):
+                 S0_check: np.ndarray, layer: int = 0, refit=False, row_weight=None):
         self.w, self.pool, self.slots, self.bits, self.layer = w, pool, slots, bits, layer
         self.refit = refit
         self.tie_cols = 0
@@ -142,8 +178,11 @@ class Lockstep:
         n = len(self.rows) * w.n_v_heads
         self.tile_bits = np.broadcast_to(bits[None], (len(self.rows),) + bits.shape).reshape(n, w.d_k)
         S = S0_check.reshape(n, w.d_k, w.d_v)
-        self.r, self.c = oracle.fit_absmax(S)
-        self.codes = oracle.quantize(S.astype(np.float64), self.r, self.c, self.tile_bits)
+        self.pivots = bool(np.any(bits == 16))
+        self.r, self.c = oracle.fit_absmax(S, bits=self.tile_bits)
+        q = oracle.quantize(S.astype(np.float64), self.r, self.c, self.tile_bits)
+        self.codes, self.pv = (q[0], q[1]) if self.pivots else (q, None)
+        self.piv_mismatches = 0
         dev = pool.device
         self.ids = slots.index_select(0, torch.as_tensor(self.rows, dtype=torch.long, device=slots.device)).to(dev)
         self.n_tiles = n
@@ -163,6 +202,9 @@ class Lockstep:
                           torch.from_numpy(np.ascontiguousarray(self.shaped(self.codes, (w.d_k, w.d_v)))).to(dev),
                           torch.from_numpy(np.ascontiguousarray(self.shaped(self.r, (w.d_k,)))).to(dev),
                           torch.from_numpy(np.ascontiguousarray(self.shaped(self.c, (w.d_v,)))).to(dev))
+        if self.pivots:
+            pv = np.ascontiguousarray(self.shaped(self.pv, (w.d_k, w.d_v))).view(np.int16)
+            self.pool.import_pivots(self.ids, torch.from_numpy(pv).to(dev))
 
     def export(self):
         w, dev = self.w, self.pool.device
@@ -171,6 +213,11 @@ class Lockstep:
         r = torch.empty((n, w.n_v_heads, w.d_k), dtype=torch.float32, device=dev)
         c = torch.empty((n, w.n_v_heads, w.d_v), dtype=torch.float32, device=dev)
         self.pool.export(self.ids, codes, r, c)
+        self.g_pv = None
+        if self.pivots:
+            pv = torch.empty((n, w.n_v_heads, w.d_k, w.d_v), dtype=torch.int16, device=dev)
+            self.pool.export_pivots(self.ids, pv)
+            self.g_pv = pv.cpu().numpy().view(np.uint16).reshape(self.n_tiles, w.d_k, w.d_v)
         torch.cuda.synchronize()
         return codes.cpu().numpy().reshape(self.n_tiles, w.d_k, w.d_v), r.cpu().numpy(), c.cpu().numpy()
 
@@ -179,9 +226,15 @@ class Lockstep:
         w = self.w
         q, k, v, a, b = oracle_inputs(w, inp, self.rows)
         g_codes, g_r, g_c = self.export()
+        pvk = dict(pv=self.pv) if self.pivots else {}
+        pmask = self.tile_bits == 16
         if self.refit == "row_absmax":
-            new, rn, cn, o, y = oracle.decode_step_rowmax(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b,
-                                                          want_y=True)
+            res = oracle.decode_step_rowmax(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True,
+                                            **pvk)
+            new, rn, cn, o, y = res[:5]
+            if self.pivots:
+                self.piv_mismatches += compare_pivots(self.g_pv, res[5], y, pmask, f"step {step} pivots")
+                self.pv = res[5]
             g_c = g_c.reshape(cn.shape)
             assert np.all(g_c == 1.0), "row-absmax step: column factors must all be 1"
             ones = np.ones(cn.shape, np.float64)
@@ -192,8 +245,12 @@ class Lockstep:
             self.r, self.c = rn, cn
             self.compared += g_codes.size
         elif self.refit:
-            new, rn, cn, o, ex = oracle.decode_step_refit(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b,
-                                                          w=self.row_w, want=("y", "c_range"), tie_window=TIE_WINDOW)
+            res = oracle.decode_step_refit(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b,
+                                           w=self.row_w, want=("y", "c_range"), tie_window=TIE_WINDOW, **pvk)
+            new, rn, cn, o, ex = res[:5]
+            if self.pivots:
+                self.piv_mismatches += compare_pivots(self.g_pv, res[5], ex["y"], pmask, f"step {step} pivots")
+                self.pv = res[5]
             nb, tc = compare_refit(g_codes, g_r.reshape(rn.shape), g_c.reshape(cn.shape), new, rn, cn,
                                    ex["y"], ex["c_range"], self.tile_bits, f"layer {self.layer} step {step} refit",
                                    frac=STEP_MISMATCH_FRAC)
@@ -202,7 +259,11 @@ class Lockstep:
             self.r, self.c = rn, cn
             self.compared += g_codes.size
         else:
-            new, o, y = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True)
+            res = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True, **pvk)
+            new, o, y = res[:3]
+            if self.pivots:
+                self.piv_mismatches += compare_pivots(self.g_pv, res[3], y, pmask, f"step {step} pivots")
+                self.pv = res[3]
             assert np.array_equal(g_r.reshape(self.r.shape), self.r), "row scales changed"
             assert np.array_equal(g_c.reshape(self.c.shape), self.c), "column scales changed"
             self.mismatches += compare_codes(g_codes, new, y, f"layer {self.layer} step {step} codes",
@@ -217,11 +278,11 @@ class Lockstep:
 
 
 def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, mutate=None, kda: bool = False,
-                 refit: bool = False, row_weight=None, say=print):
+                 refit=False, row_weight=None, say=print, bits=None):
     """Full-size decode steps of one workload layer on the GPU, the rows
     ``check_rows`` compared lockstep with the oracle at every step."""
     from paper_2609_38169_amd.pools import build_pool, row_bits
-    bits = row_bits(w, layer)
+    bits = row_bits(w, layer) if bits is None else bits
     say(f"lockstep {w.name}: building pool ({w.n_slots} slots)")
     pool = build_pool(w, layer, device=device, bits=bits)
     if row_weight is not None:
@@ -246,8 +307,13 @@ def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, 
         ls.check_step(inp, o, t)
     assert ls.mismatches <= CODE_MISMATCH_FRAC * ls.compared, \
         f"{ls.mismatches} of {ls.compared} codes differ over the run"
+    if ls.pivots:
+        n_piv = int(np.count_nonzero(ls.tile_bits == 16)) * w.d_v * steps
+        assert ls.piv_mismatches <= PIVOT_MISMATCH_FRAC * n_piv + 1, \
+            f"{ls.piv_mismatches} of {n_piv} pivot values differ over the run"
     mode = {False: "", True: " refit", "row_absmax": " row-absmax"}[refit]
     say(f"lockstep {w.name}{' kda' if kda else ''}{mode}: {steps} steps ok, "
-        f"code mismatches {ls.mismatches}, columns on another tie rounding {ls.tie_cols}, "
+        f"code mismatches {ls.mismatches}, pivot mismatches {ls.piv_mismatches}, "
+        f"columns on another tie rounding {ls.tie_cols}, "
         f"saturated {ls.saturated:.3f}")
     return ls

@@ -1,0 +1,173 @@
+"""GPU parity with FP16 pivot rows (width 16 in the precision map): layout
+round trips, boundary pack, reconstruction, and the decode step in all three
+scale modes (frozen, dual-axis refit, row-absmax baseline), GDN and KDA,
+against the fp64 oracle through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_38169_amd import stepq, workloads as W
+from paper_2609_38169_amd.pools import row_bits
+import _parity as PT
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda", 0)
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def _cases():
+    rng = np.random.default_rng(11)
+    cases = []
+    for (Hv, Hqk, dk, dv, n_slots, npiv) in [(3, 1, 37, 64, 5, 3), (2, 2, 96, 128, 4, 5), (4, 2, 128, 128, 3, 2),
+                                             (2, 1, 128, 128, 2, 32), (1, 1, 1, 64, 2, 1)]:
+        bits = rng.choice([2, 4, 8], size=(Hv, dk)).astype(np.uint8)
+        for h in range(Hv):
+            if h % 2 == 0 or Hv == 1:
+                bits[h, rng.choice(dk, size=min(npiv, dk), replace=False)] = 16
+        cases.append((Hv, Hqk, dk, dv, n_slots, bits))
+    return cases
+
+
+def _state(case, seed):
+    Hv, Hqk, dk, dv, n_slots, bits = _cases()[case]
+    rng = np.random.default_rng(seed)
+    S = (rng.standard_normal((n_slots, Hv, dk, dv)) * 0.05).astype(np.float32)
+    tb = np.broadcast_to(bits[None], (n_slots,) + bits.shape).reshape(-1, dk)
+    r, c = oracle.fit_absmax(S.reshape(-1, dk, dv), bits=tb)
+    codes, pv = oracle.quantize(S.reshape(-1, dk, dv).astype(np.float64), r, c, tb)
+    return rng, S, tb, r, c, codes, pv
+
+
+def _pool_with(case, codes, pv, r, c):
+    Hv, Hqk, dk, dv, n_slots, bits = _cases()[case]
+    pool = stepq.Pool(n_slots, Hv, Hqk, dk, dv, bits, device=DEV)
+    ids = torch.arange(n_slots, dtype=torch.int32, device=DEV)
+    pool.import_(ids, torch.from_numpy(codes.reshape(n_slots, Hv, dk, dv)).to(DEV),
+                 torch.from_numpy(r.reshape(n_slots, Hv, dk)).to(DEV),
+                 torch.from_numpy(c.reshape(n_slots, Hv, dv)).to(DEV))
+    pool.import_pivots(ids, torch.from_numpy(pv.reshape(n_slots, Hv, dk, dv).view(np.int16)).to(DEV))
+    return pool, ids
+
+
+@pytest.mark.parametrize("case", range(5))
+def test_pivot_import_export_and_image(case):
+    Hv, Hqk, dk, dv, n_slots, bits = _cases()[case]
+    _say(f"pivot layout case {case}: Hv={Hv} dk={dk} dv={dv} pivots/head={list((bits == 16).sum(1))}")
+    _, S, tb, r, c, codes, pv = _state(case, 500 + case)
+    pool, ids = _pool_with(case, codes, pv, r, c)
+    img = pool.memory.cpu().numpy()
+    shp = (n_slots, Hv, dk, dv)
+    assert np.array_equal(img, oracle.pack_pool(codes.reshape(shp), r.reshape(n_slots, Hv, dk),
+                                                c.reshape(n_slots, Hv, dv), bits, pv=pv.reshape(shp)))
+    oc = torch.empty(shp, dtype=torch.int8, device=DEV)
+    opv = torch.empty(shp, dtype=torch.int16, device=DEV)
+    pool.export(ids, oc, torch.empty((n_slots, Hv, dk), device=DEV), torch.empty((n_slots, Hv, dv), device=DEV))
+    pool.export_pivots(ids, opv)
+    deq = torch.empty(shp, dtype=torch.float32, device=DEV)
+    pool.dequant(ids, deq)
+    torch.cuda.synchronize()
+    assert np.array_equal(oc.cpu().numpy().reshape(codes.shape), codes)
+    assert np.array_equal(opv.cpu().numpy().view(np.uint16).reshape(pv.shape), pv)
+    piv = tb == 16
+    d = deq.cpu().numpy().reshape(codes.shape)
+    assert np.array_equal(d[piv], oracle.half_to_double(pv)[piv].astype(np.float32))
+
+
+@pytest.mark.parametrize("case", [0, 2])
+def test_pivot_boundary_pack(case):
+    """stepq_pool_load: pivot rows are the fp32 state rounded to binary16,
+    bit for bit; integer rows as the quantizer."""
+    Hv, Hqk, dk, dv, n_slots, bits = _cases()[case]
+    _, S, tb, r, c, codes, pv = _state(case, 600 + case)
+    pool = stepq.Pool(n_slots, Hv, Hqk, dk, dv, bits, device=DEV)
+    ids = torch.arange(n_slots, dtype=torch.int32, device=DEV)
+    pool.load(ids, torch.from_numpy(S).to(DEV), torch.from_numpy(r.reshape(n_slots, Hv, dk)).to(DEV),
+              torch.from_numpy(c.reshape(n_slots, Hv, dv)).to(DEV))
+    shp = (n_slots, Hv, dk, dv)
+    oc = torch.empty(shp, dtype=torch.int8, device=DEV)
+    opv = torch.empty(shp, dtype=torch.int16, device=DEV)
+    pool.export(ids, oc, torch.empty((n_slots, Hv, dk), device=DEV), torch.empty((n_slots, Hv, dv), device=DEV))
+    pool.export_pivots(ids, opv)
+    torch.cuda.synchronize()
+    assert np.array_equal(opv.cpu().numpy().view(np.uint16).reshape(pv.shape), pv)
+    _, y, _ = oracle.quantize(S.reshape(-1, dk, dv).astype(np.float64), r, c, tb, want_y=True)
+    PT.compare_codes(oc.cpu().numpy().reshape(codes.shape), codes, y, "pivot pool_load codes")
+
+
+@pytest.mark.parametrize("mode", [False, True, "row_absmax"])
+@pytest.mark.parametrize("kda", [False, True])
+@pytest.mark.parametrize("case", range(5))
+def test_pivot_decode_step(case, kda, mode):
+    Hv, Hqk, dk, dv, n_slots, bits = _cases()[case]
+    _say(f"pivot decode case {case} kda={kda} mode={mode}")
+    rng, S, tb, r, c, codes, pv = _state(case, 700 + case)
+    pool, all_ids = _pool_with(case, codes, pv, r, c)
+    wrow = np.exp(0.3 * rng.standard_normal((Hv, dk))).astype(np.float32)
+    pool.set_row_weight(wrow)
+    B = max(1, n_slots - 1)
+    sel = rng.permutation(n_slots)[:B].astype(np.int32)
+    ids = torch.from_numpy(sel).to(DEV)
+    q = rng.standard_normal((B, Hqk, dk)); q /= np.linalg.norm(q, axis=-1, keepdims=True)
+    k = rng.standard_normal((B, Hqk, dk)); k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    v = rng.standard_normal((B, Hv, dv))
+    gate = rng.uniform(0.5, 1.0, (B, Hv, dk)) if kda else rng.uniform(0.9, 1.0, (B, Hv))
+    be = rng.uniform(0, 1, (B, Hv))
+    t32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+    o = torch.empty((B, Hv, dv), dtype=torch.float32, device=DEV)
+    step = pool.step_kda if kda else pool.step
+    step(ids, t32(q), t32(k), t32(v), t32(gate), t32(be), o, refit=mode)
+    shp = (n_slots, Hv, dk, dv)
+    g_codes = torch.empty(shp, dtype=torch.int8, device=DEV)
+    g_pv = torch.empty(shp, dtype=torch.int16, device=DEV)
+    g_r = torch.empty((n_slots, Hv, dk), device=DEV)
+    g_c = torch.empty((n_slots, Hv, dv), device=DEV)
+    pool.export(all_ids, g_codes, g_r, g_c)
+    pool.export_pivots(all_ids, g_pv)
+    torch.cuda.synchronize()
+    got = g_codes.cpu().numpy().reshape(-1, dk, dv)
+    gpv = g_pv.cpu().numpy().view(np.uint16).reshape(-1, dk, dv)
+    gr, gc = g_r.cpu().numpy().reshape(-1, dk), g_c.cpu().numpy().reshape(-1, dv)
+    hq = np.arange(Hv) // (Hv // Hqk)
+    f32 = lambda a: a.astype(np.float32).astype(np.float64)
+    tiles = (sel[:, None] * Hv + np.arange(Hv)[None]).reshape(-1)
+    args = (codes[tiles], r[tiles], c[tiles], tb[tiles], f32(q)[:, hq].reshape(-1, dk),
+            f32(k)[:, hq].reshape(-1, dk), f32(v).reshape(-1, dv), f32(gate).reshape((-1, dk) if kda else (-1,)),
+            f32(be).reshape(-1))
+    pmask = tb[tiles] == 16
+    if mode is True:
+        wt = np.broadcast_to(wrow[None].astype(np.float64), (B, Hv, dk)).reshape(-1, dk)
+        new, rn, cn, o_ref, ex, npv = oracle.decode_step_refit(*args, w=wt, want=("y", "c_range"),
+                                                               tie_window=PT.TIE_WINDOW, pv=pv[tiles])
+        PT.compare_refit(got[tiles], gr[tiles], gc[tiles], new, rn, cn, ex["y"], ex["c_range"], tb[tiles],
+                         f"pivot refit case {case}")
+        y = ex["y"]
+        assert np.array_equal(gr[tiles][pmask], r[tiles][pmask])          # pivots keep their row factor
+    elif mode == "row_absmax":
+        new, rn, cn, o_ref, y, npv = oracle.decode_step_rowmax(*args, want_y=True, pv=pv[tiles])
+        ones = np.ones(cn.shape)
+        PT.compare_refit(got[tiles], gr[tiles], gc[tiles], new, rn, cn, y, (ones, ones), tb[tiles],
+                         f"pivot row-absmax case {case}")
+        assert np.all(gc[tiles] == 1.0)
+    else:
+        new, o_ref, y, npv = oracle.decode_step(*args, want_y=True, pv=pv[tiles])
+        PT.compare_codes(got[tiles], new, y, f"pivot decode case {case}")
+        assert np.array_equal(gr[tiles], r[tiles]) and np.array_equal(gc[tiles], c[tiles])
+    PT.compare_pivots(gpv[tiles], npv, y, pmask, f"pivot values case {case}")
+    PT.compare_out(o.cpu().numpy().reshape(-1, dv), o_ref)
+    untouched = np.setdiff1d(np.arange(n_slots * Hv), tiles)
+    assert np.array_equal(got[untouched], codes[untouched]) and np.array_equal(gpv[untouched], pv[untouched])
+
+
+@pytest.mark.parametrize("mode", [False, True, "row_absmax"])
+def test_pivot_pool_b512_lockstep(mode):
+    """The B=512 pool with pivot rows in a quarter of the heads (those heads
+    take the generic body, the rest the compiled 6-bit one), all slots
+    stepped, sampled slots compared lockstep."""
+    w = W.workload(2)
+    bits = row_bits(w)
+    bits[W.pivot_mask_draw(w).numpy()] = 16
+    PT.lockstep_run(w, 6, np.array([0, 200, 511]), DEV, refit=mode, say=_say, bits=bits)

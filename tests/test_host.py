@@ -47,11 +47,15 @@ def test_ragged_layout_sizes():
         bits = rng.choice([2, 4, 8], size=(5, dk)).astype(np.uint8)
         pb, sb = stepq.stepq_pool_bytes(3, 5, 5, dk, dv, bits)
         assert sb == oracle.slot_bytes(bits, dv) and pb == 3 * sb
+        bits[rng.random(bits.shape) < 0.1] = 16          # FP16 pivot rows
+        pb, sb = stepq.stepq_pool_bytes(3, 5, 5, dk, dv, bits)
+        assert sb == oracle.slot_bytes(bits, dv) and pb == 3 * sb
 
 
 @pytest.mark.parametrize("bad,status", [
     (dict(n_slots=0), 1), (dict(n_v_heads=6, n_qk_heads=4), 1), (dict(d_k=129), 2), (dict(d_v=96), 2),
-    (dict(bitval=3), 1), (dict(bitval=16), 1),
+    (dict(bitval=3), 1), (dict(bitval=12), 1),
+    (dict(bitval=16), 2),                       # 64 pivot rows per head: more than the 32 supported
 ])
 def test_bad_descriptor_rejected(bad, status):
     a = dict(n_slots=2, n_v_heads=4, n_qk_heads=2, d_k=64, d_v=64)
@@ -86,6 +90,12 @@ def test_setup_fit_matches_oracle(idx):
     wts = np.random.default_rng(1).uniform(0.5, 2, S.shape[:-1]).astype(np.float32)
     r1, c1 = stepq.stepq_setup_fit(S, wts)
     r2, c2 = oracle.fit_absmax(S.reshape(-1, w.d_k, w.d_v), wts.reshape(-1, w.d_k).astype(np.float64))
+    assert np.array_equal(r1.reshape(r2.shape), r2) and np.array_equal(c1.reshape(c2.shape), c2)
+    # pivot rows (16) left out of the column factors
+    bits = np.random.default_rng(2).choice([4, 8, 16], size=S.shape[:-1], p=[0.45, 0.45, 0.1]).astype(np.uint8)
+    r1, c1 = stepq.stepq_setup_fit(S, wts, row_bits=bits)
+    r2, c2 = oracle.fit_absmax(S.reshape(-1, w.d_k, w.d_v), wts.reshape(-1, w.d_k).astype(np.float64),
+                               bits=bits.reshape(-1, w.d_k))
     assert np.array_equal(r1.reshape(r2.shape), r2) and np.array_equal(c1.reshape(c2.shape), c2)
 
 

@@ -81,3 +81,23 @@ def test_compare_out_rules():
     PT.compare_out(o + 1e-3 * np.abs(o) * 0.9, o)
     with pytest.raises(AssertionError):
         PT.compare_out(o + 2e-3 * np.abs(o) + 1e-4, o)
+
+
+def test_compare_pivots_rules():
+    rng = np.random.default_rng(3)
+    X = rng.standard_normal((2, 5, 8)) * 0.3
+    mask = np.zeros((2, 5), bool)
+    mask[0, 1] = mask[1, 3] = True
+    o_pv = X.astype(np.float16).view(np.uint16)
+    assert PT.compare_pivots(o_pv.copy(), o_pv, X, mask, frac=1.0) == 0
+    g = o_pv.copy()
+    g[0, 1, 2] += 1                                  # one binary16 step away from the rounding of X
+    X2 = X.copy()
+    X2[0, 1, 2] = (g[0, 1, 2:3].view(np.float16).astype(np.float64)[0]
+                   + o_pv[0, 1, 2:3].view(np.float16).astype(np.float64)[0]) / 2    # exactly between: a tie
+    assert PT.compare_pivots(g, o_pv, X2, mask, frac=1.0) == 1
+    with pytest.raises(AssertionError):            # not a tie: the value is wrong
+        PT.compare_pivots(g, o_pv, X, mask, frac=1.0)
+    g2 = o_pv.copy()
+    g2[0, 2, 0] += 7                                 # outside the pivot rows: not compared
+    assert PT.compare_pivots(g2, o_pv, X, mask, frac=0.0) == 0
