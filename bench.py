@@ -273,8 +273,8 @@ def main():
         "setup_s": setup_s,
 
     }
-    if args.refit:
-        # the refit step is bound by fp32 VALU work, not by HBM: that roofline is the primary one
+    if rescale:
+        # the refitting steps are bound by fp32 VALU work, not by HBM: that roofline is the primary one
         rl = line["roofline"]
         hbm = {k: rl[k] for k in ("achieved", "peak", "unit", "frac")}
         valu = rl.pop("valu")
