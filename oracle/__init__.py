@@ -55,6 +55,7 @@ def lib():
         L.orc_decode_step_refit.argtypes = [i, i, i, P, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P,
                                             ctypes.c_double, P, P, P, P]
         L.orc_decode_step_rowmax.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P]
+        L.orc_fit_dual_axis.argtypes = [i, i, i, P, P, P, P, P, P, P]
         L.orc_half_to_double.argtypes = [ctypes.c_size_t, P, P]
         L.orc_double_to_half.argtypes = [ctypes.c_size_t, P, P]
         L.orc_tile_bytes.argtypes = [i, i, P]
@@ -285,6 +286,21 @@ def unpack_pool(pool, n_slots, bits, d_v):
     c = np.empty((n_slots, Hv, d_v), np.float32)
     pv = np.zeros((n_slots, Hv, dk, d_v), np.uint16) if _has_pivots(bits) else None
     lib().orc_unpack_pool(n_slots, Hv, dk, d_v, _p(bits), _p(pool), _p(codes), _p(pv), _p(r), _p(c))
+    return (codes, r, c, pv) if pv is not None else (codes, r, c)
+
+
+def fit_dual_axis(X, bits, w=None):
+    """Key-Row-Aware Dual-Axis fit of states X [n][dk][dv] (fp64): returns
+    (codes, r, c[, pv]) -- the spatial codec of Section 4.3 / Appendix C.1."""
+    X = _c(X, np.float64)
+    n, dk, dv = X.shape
+    bits = _c(np.broadcast_to(bits, (n, dk)), np.uint8)
+    wt = None if w is None else _c(np.broadcast_to(w, (n, dk)), np.float64)
+    r = np.empty((n, dk), np.float32)
+    c = np.empty((n, dv), np.float32)
+    codes = np.empty((n, dk, dv), np.int8)
+    pv = np.zeros((n, dk, dv), np.uint16) if _has_pivots(bits) else None
+    lib().orc_fit_dual_axis(n, dk, dv, _p(X), _p(bits), _p(wt), _p(r), _p(c), _p(codes), _p(pv))
     return (codes, r, c, pv) if pv is not None else (codes, r, c)
 
 

@@ -470,6 +470,85 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
 }
 
 /* ------------------------------------------------------------------------
+ * The Key-Row-Aware Dual-Axis fit of a given state X (Section 4.3,
+ * Appendix C.1) -- the spatial codec used for calibration distortions
+ * (Appendix A.3): per tile
+ *   r_i = (m_i / w_i)^{1/2}, m_i = mean_j |X_ij|          (floor, stored fp32)
+ *   c0_j = max_i |X_ij| / r_i                              (floor)
+ *   z_ij = clip(round(X_ij q_b / (r_i c0_j))) / q_b
+ *   c_j = sum_i w_i^2 v_ij X_ij / sum_i w_i^2 v_ij^2, v = r z   (floor, stored
+ *         fp32; a zero denominator keeps c0_j, there being no earlier scale)
+ *   codes = clip(round(X q_b / (r c)))                     (stored scales)
+ * Pivot rows (16) take no part and get X rounded to binary16 (pv_out).
+ */
+void orc_fit_dual_axis(int n_tiles, int dk, int dv, const double *Xall, const uint8_t *bits, const double *w,
+                       float *r_out, float *c_out, int8_t *codes_out, uint16_t *pv_out)
+{
+    const double floor_ = ldexp(1.0, -60);
+    #pragma omp parallel for schedule(dynamic, 4)
+    for (int t = 0; t < n_tiles; ++t) {
+        size_t nel = (size_t)dk * dv;
+        const double *X = Xall + (size_t)t * nel;
+        const uint8_t *bt = bits + (size_t)t * dk;
+        double *rn = (double *)malloc(sizeof(double) * dk);
+        double *zt = (double *)malloc(sizeof(double) * nel);
+        store_pivots(dk, dv, bt, X, pv_out ? pv_out + (size_t)t * nel : NULL, codes_out + (size_t)t * nel, NULL);
+        for (int i = 0; i < dk; ++i) {
+            rn[i] = 1.0;
+            if (bt[i] == 16) {
+                r_out[(size_t)t * dk + i] = 1.0f;
+                continue;
+            }
+            double m = 0.0;
+            for (int j = 0; j < dv; ++j) m += fabs(X[(size_t)i * dv + j]);
+            m /= (double)dv;
+            double wi = w ? w[(size_t)t * dk + i] : 1.0;
+            double ri = sqrt(m / wi);
+            if (ri < floor_) ri = floor_;
+            r_out[(size_t)t * dk + i] = (float)ri;
+            rn[i] = (double)r_out[(size_t)t * dk + i];
+        }
+        for (int j = 0; j < dv; ++j) {
+            double c0 = 0.0;
+            for (int i = 0; i < dk; ++i) {
+                if (bt[i] == 16) continue;
+                double a = fabs(X[(size_t)i * dv + j]) / rn[i];
+                if (a > c0) c0 = a;
+            }
+            if (c0 < floor_) c0 = floor_;
+            double num = 0.0, den = 0.0;
+            for (int i = 0; i < dk; ++i) {
+                if (bt[i] == 16) continue;
+                double qb = qb_of(bt[i]);
+                double n = nearbyint(X[(size_t)i * dv + j] * qb / (rn[i] * c0));
+                if (n > qb) n = qb;
+                if (n < -qb) n = -qb;
+                double wi = w ? w[(size_t)t * dk + i] : 1.0;
+                double vij = rn[i] * n / qb;
+                num += wi * wi * vij * X[(size_t)i * dv + j];
+                den += wi * wi * vij * vij;
+            }
+            double cj = den > 0.0 ? num / den : c0;
+            if (cj < floor_) cj = floor_;
+            c_out[(size_t)t * dv + j] = (float)cj;
+        }
+        for (int i = 0; i < dk; ++i) {
+            if (bt[i] == 16) continue;
+            double qb = qb_of(bt[i]);
+            for (int j = 0; j < dv; ++j) {
+                double s = X[(size_t)i * dv + j] * qb / (rn[i] * (double)c_out[(size_t)t * dv + j]);
+                double n = nearbyint(s);
+                if (n > qb) n = qb;
+                if (n < -qb) n = -qb;
+                codes_out[(size_t)t * nel + (size_t)i * dv + j] = (int8_t)n;
+            }
+        }
+        free(rn);
+        free(zt);
+    }
+}
+
+/* ------------------------------------------------------------------------
  * One decode step of the single-axis baseline the paper compares against
  * (Section 5.1: symmetric row-wise absmax INT-b), on the same quantized
  * tile: steps 1-3 of orc_decode_step, then per key row
