@@ -258,6 +258,59 @@ stepq_status stepq_setup_fit_ex(int64_t n_tiles, int32_t d_k, int32_t d_v, const
 stepq_status stepq_setup_lifetime_bits(const double *gates, int32_t T, int32_t B, int32_t H, int32_t d_k,
                                        double budget, int32_t lo, int32_t hi, uint8_t *row_bits);
 
+/* ---------------------------------------------------------------------------
+ * Calibration side of the setup step (offline, host memory, double precision
+ * sums).  Units are key rows (KDA) or whole heads (Qwen), Section 3.2.
+ */
+
+/* Row-impact factors (Section 4.3 and its footnote; Appendix A.2 with one
+ * future read, Appendix C.1): per head and key row
+ *   omega_i = mean_t g_{t,i}^2,  g_t = A_t^T q_t = D_t (q_t - beta_t k_t (k_t^T q_t)),
+ *   w_i = omega_i^{gamma/2} / GM_j(omega_j^{gamma/2})   (the paper uses gamma = 0.25).
+ * q, k [T][H][d_k], beta [T][H], gate [T][H] (gate_per_row 0: D = alpha I) or
+ * [T][H][d_k] (gate_per_row 1: D = diag(d)); T calibration samples (tokens x
+ * requests).  omega is floored at 2^-120.  Outputs row_weight [H][d_k] fp32
+ * and, if not NULL, omega [H][d_k]. */
+stepq_status stepq_setup_row_impact(int64_t T, int32_t H, int32_t d_k, const float *q, const float *k,
+                                    const float *beta, const float *gate, int32_t gate_per_row, double gamma,
+                                    float *row_weight, double *omega);
+
+/* Candidate-format distortion d_u(b) (Appendix A.3): each sampled state
+ * states [C][H][d_k][d_v] is coded at every candidate width b in cand_bits
+ * (2, 4, 8: all non-pivot rows at b by the Key-Row-Aware Dual-Axis fit with
+ * row_weight [H][d_k] (NULL: 1) -- absmax column start, one fixed-code
+ * least-squares column update, a zero denominator keeping the start; 16:
+ * binary16 rounding) and reconstructed.  pivots [H][d_k] (NULL: none) marks
+ * rows held in binary16, left out of the column fit.
+ *   unit 0 (key rows, KDA):  d_out [H*d_k][n_cand], unweighted MSE of the row;
+ *   unit 1 (heads, Qwen):    d_out [H][n_cand], w_i^2-weighted MSE of the head. */
+stepq_status stepq_setup_distortion(int64_t C, int32_t H, int32_t d_k, int32_t d_v, const float *states,
+                                    const float *row_weight, const uint8_t *pivots, int32_t n_cand,
+                                    const int32_t *cand_bits, int32_t unit, double *d_out, int32_t n_threads);
+
+/* Lifetime weights L_u = sum_{j=0}^{horizon-1} exp(2 j ell_u) (Section 3.2)
+ * from the mean log retention ell_u (Appendix A.3). */
+stepq_status stepq_setup_lifetime_weights(int32_t U, const double *ell, int32_t horizon, double *L);
+
+/* Bit allocation (Eq. 6): choose choice[u] in [0, n_cand) minimising
+ * sum_u cost[u][choice[u]] (cost = L_u d_u(b), [U][n_cand]) subject to
+ * sum_u n_u b_u <= budget * sum_u n_u.
+ *   method 0: multiple-choice dynamic program over spent bits (the Qwen
+ *             optimizer, Appendix C.2); exact.  STEPQ_E_UNSUPPORTED when
+ *             units x budget steps exceed 4e8 (use method 1).
+ *   method 1: Lagrangian (the KDA optimizer): per unit argmin of
+ *             cost + lam n_u b for the smallest multiplier lam that fits
+ *             (bisection), then repair: repeatedly the single upgrade with
+ *             the largest cost decrease per extra bit that still fits.
+ * STEPQ_E_INVALID when nothing fits the budget. */
+stepq_status stepq_setup_allocate(int32_t U, int32_t n_cand, const int32_t *cand_bits, const double *cost,
+                                  const int32_t *n_u, double budget, int32_t method, int32_t *choice);
+
+/* FP16 pivots (Section 3.2, Table C1): is_pivot[u] = 1 for the count units of
+ * largest risk (ties: lower index), e.g. the lifetime-weighted distortion
+ * reduction L_u (d_u(b) - d_u(16)) of Appendix C.2. */
+stepq_status stepq_setup_select_pivots(int32_t U, const double *risk, int32_t count, uint8_t *is_pivot);
+
 #ifdef __cplusplus
 }
 #endif

@@ -28,7 +28,8 @@ EXPORTED = (
     "stepq_pool_load", "stepq_decode_step", "stepq_decode_step_kda", "stepq_decode_step_ex",
     "stepq_pool_set_row_weight", "stepq_pool_dequant", "stepq_pool_export", "stepq_pool_import",
     "stepq_pool_export_pivots", "stepq_pool_import_pivots", "stepq_last_error", "stepq_setup_fit",
-    "stepq_setup_fit_ex", "stepq_setup_lifetime_bits",
+    "stepq_setup_fit_ex", "stepq_setup_lifetime_bits", "stepq_setup_row_impact", "stepq_setup_distortion",
+    "stepq_setup_lifetime_weights", "stepq_setup_allocate", "stepq_setup_select_pivots",
 )
 
 
@@ -71,6 +72,11 @@ def lib():
             "stepq_pool_export_pivots": ([P, P, i32, P, P], st),
             "stepq_pool_import_pivots": ([P, P, i32, P, P], st),
             "stepq_setup_fit_ex": ([i64, i32, i32, P, P, P, P, P, i32], st),
+            "stepq_setup_row_impact": ([i64, i32, i32, P, P, P, P, i32, ctypes.c_double, P, P], st),
+            "stepq_setup_distortion": ([i64, i32, i32, i32, P, P, P, i32, P, i32, P, i32], st),
+            "stepq_setup_lifetime_weights": ([i32, P, i32, P], st),
+            "stepq_setup_allocate": ([i32, i32, P, P, P, ctypes.c_double, i32, P], st),
+            "stepq_setup_select_pivots": ([i32, P, i32, P], st),
             "stepq_last_error": ([], ctypes.c_char_p),
             "stepq_setup_fit": ([i64, i32, i32, P, P, P, P, i32], st),
             "stepq_setup_lifetime_bits": ([P, i32, i32, i32, i32, ctypes.c_double, i32, i32, P], st),
@@ -384,3 +390,70 @@ def stepq_setup_lifetime_bits(gates, d_k: int, budget: float = 6.0, lo: int = 4,
     if st != 0:
         raise StepqError(st, "invalid lifetime allocation arguments")
     return out
+
+
+# ---------------------------------------------------------------------------
+# calibration side of the setup step (host arrays)
+def _vp(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _host(a, dtype):
+    return np.ascontiguousarray(a.cpu().numpy() if isinstance(a, torch.Tensor) else a, dtype=dtype)
+
+
+def _setup_check(st, what):
+    if st != 0:
+        raise StepqError(st, what)
+
+
+def stepq_setup_row_impact(q, k, beta, gate, gamma: float = 0.25):
+    """q, k [T][H][d_k], beta [T][H], gate [T][H] or [T][H][d_k] -> (w, omega) [H][d_k]."""
+    q, k = _host(q, np.float32), _host(k, np.float32)
+    beta, gate = _host(beta, np.float32), _host(gate, np.float32)
+    T, H, dk = q.shape
+    w = np.empty((H, dk), np.float32)
+    om = np.empty((H, dk), np.float64)
+    _setup_check(lib().stepq_setup_row_impact(T, H, dk, _vp(q), _vp(k), _vp(beta), _vp(gate), int(gate.ndim == 3),
+                                              float(gamma), _vp(w), _vp(om)), "row impact")
+    return w, om
+
+
+def stepq_setup_distortion(states, cand_bits, unit: str, row_weight=None, pivots=None, n_threads: int = 0):
+    """states [C][H][d_k][d_v] -> d [U][len(cand_bits)] (unit "row" or "head")."""
+    S = _host(states, np.float32)
+    C, H, dk, dv = S.shape
+    cb = np.ascontiguousarray(cand_bits, dtype=np.int32)
+    w = None if row_weight is None else _host(row_weight, np.float32)
+    pv = None if pivots is None else _host(pivots, np.uint8)
+    u = {"row": 0, "head": 1}[unit]
+    out = np.empty((H * dk if u == 0 else H, len(cb)), np.float64)
+    _setup_check(lib().stepq_setup_distortion(C, H, dk, dv, _vp(S), _vp(w), _vp(pv), len(cb), _vp(cb), u, _vp(out),
+                                              n_threads), "distortion")
+    return out
+
+
+def stepq_setup_lifetime_weights(ell, horizon: int):
+    e = _host(ell, np.float64)
+    out = np.empty(e.shape, np.float64)
+    _setup_check(lib().stepq_setup_lifetime_weights(e.size, _vp(e), horizon, _vp(out)), "lifetime weights")
+    return out
+
+
+def stepq_setup_allocate(cost, n_u, cand_bits, budget: float, method: str = "dp"):
+    """cost [U][n_cand], n_u [U] -> candidate index per unit (method "dp" or "lagrangian")."""
+    c = _host(cost, np.float64)
+    U, nc = c.shape
+    n = np.ascontiguousarray(np.broadcast_to(n_u, (U,)), dtype=np.int32)
+    cb = np.ascontiguousarray(cand_bits, dtype=np.int32)
+    out = np.empty(U, np.int32)
+    _setup_check(lib().stepq_setup_allocate(U, nc, _vp(cb), _vp(c), _vp(n), float(budget),
+                                            {"dp": 0, "lagrangian": 1}[method], _vp(out)), "allocation")
+    return out
+
+
+def stepq_setup_select_pivots(risk, count: int):
+    r = _host(risk, np.float64)
+    out = np.empty(r.shape, np.uint8)
+    _setup_check(lib().stepq_setup_select_pivots(r.size, _vp(r), count, _vp(out)), "pivot selection")
+    return out.astype(bool)

@@ -171,3 +171,25 @@ def test_pivot_pool_b512_lockstep(mode):
     bits = row_bits(w)
     bits[W.pivot_mask_draw(w).numpy()] = 16
     PT.lockstep_run(w, 6, np.array([0, 200, 511]), DEV, refit=mode, say=_say, bits=bits)
+
+
+def test_calibrated_map_runs_lockstep():
+    """The calibration pipeline (row impact, distortions, lifetime weights,
+    pivots, Lagrangian allocation) on the layer_b64 workload's own draws
+    yields a map with FP16 pivot rows and 4/8-bit rows; a pool built on it,
+    refit with the calibrated row factors, matches the oracle lockstep."""
+    from paper_2609_38169_amd.calibrate import calibrate
+    w = W.workload(1)
+    T = 8
+    steps = [W.step_inputs(w, 0, 1000 + t) for t in range(T)]        # calibration draws, not the test steps
+    g = w.n_v_heads // w.n_qk_heads
+    cat = lambda key: np.concatenate([s[key].numpy() for s in steps])
+    q = np.repeat(cat("q"), g, axis=1)
+    k = np.repeat(cat("k"), g, axis=1)
+    S = W.initial_state(w, 0, range(4)).numpy()
+    cal = calibrate(q, k, cat("beta"), cat("alpha"), S, budget=6.0, cand_bits=(4, 8), unit="row",
+                    n_pivots=24, horizon=1024)
+    bits = cal.row_bits
+    assert (bits == 16).sum() == 24 and bits[bits != 16].mean() <= 6.0
+    _say(f"calibrated map: {(bits == 8).sum()} rows @8, {(bits == 4).sum()} @4, {(bits == 16).sum()} pivots")
+    PT.lockstep_run(w, 8, np.arange(0, 64, 9), DEV, refit=True, row_weight=cal.row_weight, say=_say, bits=bits)

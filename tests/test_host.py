@@ -143,3 +143,91 @@ def test_library_device_code_is_gfx950():
     mixed hipcc command line once silently fell back to another target)."""
     from paper_2609_38169_amd.build import device_targets
     assert device_targets(stepq.LIB_PATH) == ["gfx950"]
+
+
+# ---------------------------------------------------------------- calibration side (host code vs oracle)
+def _calib_stream(seed, T=30, H=3, dk=8, kda=True):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((T, H, dk)).astype(np.float32)
+    k = rng.standard_normal((T, H, dk)).astype(np.float32)
+    q /= np.linalg.norm(q, axis=-1, keepdims=True)
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    beta = rng.uniform(0, 1, (T, H)).astype(np.float32)
+    gate = (rng.uniform(0.7, 1.0, (T, H, dk)) if kda else rng.uniform(0.7, 1.0, (T, H))).astype(np.float32)
+    return q, k, beta, gate
+
+
+@pytest.mark.parametrize("kda", [False, True])
+def test_row_impact_matches_oracle(kda):
+    import oracle.calibration as CAL
+    q, k, beta, gate = _calib_stream(10, kda=kda)
+    w, om = stepq.stepq_setup_row_impact(q, k, beta, gate)
+    w_o, om_o = CAL.row_impact(q, k, beta, gate)
+    np.testing.assert_allclose(om, om_o, rtol=1e-12)
+    np.testing.assert_allclose(w, w_o, rtol=2e-7)
+
+
+@pytest.mark.parametrize("unit", ["row", "head"])
+def test_distortion_matches_oracle(unit):
+    import oracle.calibration as CAL
+    rng = np.random.default_rng(11)
+    C, H, dk, dv = 3, 2, 12, 16
+    S = (rng.standard_normal((C, H, dk, dv)) * np.exp(rng.standard_normal((C, H, dk, 1)))).astype(np.float32)
+    w = np.exp(0.3 * rng.standard_normal((H, dk))).astype(np.float32)
+    piv = np.zeros((H, dk), bool)
+    piv[1, 4] = True
+    for pv in (None, piv):
+        d = stepq.stepq_setup_distortion(S, [2, 4, 8, 16], unit, row_weight=w, pivots=pv, n_threads=3)
+        d_o = CAL.calib_distortion(S.astype(np.float64), [2, 4, 8, 16], unit, w=w.astype(np.float64), pivots=pv)
+        np.testing.assert_allclose(d, d_o, rtol=1e-12)
+
+
+def test_lifetime_weights_and_pivots_match_oracle():
+    import oracle.calibration as CAL
+    ell = np.array([-0.5, -0.02, -1e-6, 0.0, -3e-13])
+    np.testing.assert_allclose(stepq.stepq_setup_lifetime_weights(ell, 512), CAL.lifetime_weights(ell, 512),
+                               rtol=1e-9)
+    risk = np.random.default_rng(12).uniform(0, 1, 40)
+    assert np.array_equal(stepq.stepq_setup_select_pivots(risk, 5), CAL.select_pivots(risk, 5))
+
+
+def test_allocators_match_oracle():
+    import oracle.calibration as CAL
+    rng = np.random.default_rng(13)
+    cands = [2, 4, 8]
+    for trial in range(25):
+        U = int(rng.integers(2, 12))
+        n_u = rng.choice([64, 128], size=U).astype(np.int32)
+        cost = np.sort(rng.uniform(0, 1, (U, 3)), axis=1)[:, ::-1] * rng.uniform(0.1, 10, (U, 1))
+        budget = float(rng.choice([2.5, 3.0, 4.0, 5.0, 6.0, 7.9]))
+        dp = stepq.stepq_setup_allocate(cost, n_u, cands, budget, "dp")
+        dp_o = CAL.allocate_dp(cost, n_u, cands, budget)
+        tot = lambda ch: sum(cost[u, ch[u]] for u in range(U))
+        assert abs(tot(dp) - tot(dp_o)) <= 1e-12 * max(1.0, tot(dp_o))
+        lg = stepq.stepq_setup_allocate(cost, n_u, cands, budget, "lagrangian")
+        lg_o = CAL.allocate_lagrangian(cost, n_u, cands, budget)
+        assert np.array_equal(lg, lg_o)
+    with pytest.raises(stepq.StepqError):        # nothing fits
+        stepq.stepq_setup_allocate(np.ones((3, 3)), 64, cands, 1.0, "dp")
+
+
+@pytest.mark.parametrize("unit,kda", [("row", True), ("head", False)])
+def test_calibration_pipeline_meets_the_budget(unit, kda):
+    """calibrate(): pivots are the requested count, the integer units meet the
+    average budget, and wider codes go to units whose lifetime-weighted
+    distortion gains most."""
+    from paper_2609_38169_amd.calibrate import calibrate
+    q, k, beta, gate = _calib_stream(14, T=40, H=4, dk=16, kda=kda)
+    rng = np.random.default_rng(15)
+    S = (rng.standard_normal((6, 4, 16, 64)) * 0.1).astype(np.float32)
+    cal = calibrate(q, k, beta, gate, S, budget=5.0, cand_bits=(2, 4, 8), unit=unit,
+                    n_pivots=3 if unit == "row" else 1, horizon=256)
+    bits = cal.row_bits
+    piv = bits == 16
+    units_piv = piv.sum() if unit == "row" else piv.all(axis=1).sum()
+    assert units_piv == (3 if unit == "row" else 1)
+    integer = bits[~piv].astype(np.float64)
+    assert integer.mean() <= 5.0 + 1e-9 and set(np.unique(integer)) <= {2, 4, 8}
+    np.testing.assert_allclose(np.exp(np.log(cal.row_weight.astype(np.float64)).mean(axis=1)), 1.0, rtol=1e-6)
+    pb, sb = stepq.stepq_pool_bytes(2, 4, 4, 16, 64, bits)        # a valid pool layout
+    assert pb == 2 * sb
