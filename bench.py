@@ -130,8 +130,10 @@ def traffic_entry(refit: bool, kda: bool):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=128)
+    ap.add_argument("--steps", type=int, default=256)
     ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--settle-ms", type=float, default=150.0,
+                    help="untimed launches before the warmup until this much GPU time has elapsed (clock ramp)")
     ap.add_argument("--resident", action="store_true", help="no slot rotation (cache-resident number)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -187,7 +189,23 @@ def main():
                                               refit=mode)
         prepared[key]()
 
-    log(f"pool and inputs ready in {time.perf_counter() - t_setup:.1f} s; timing")
+    log(f"pool and inputs ready in {time.perf_counter() - t_setup:.1f} s; settling clocks")
+    # Settle: the GPU's clocks ramp up over the first ~50 ms of sustained
+    # load (a step measured on a cold GPU is ~20% slower), so launches run
+    # untimed until args.settle_ms of GPU time has elapsed; then the W
+    # warmup steps; then the K timed steps.
+    settle_n, settle_ms = 0, 0.0
+    s0 = torch.cuda.Event(enable_timing=True)
+    s1 = torch.cuda.Event(enable_timing=True)
+    while settle_ms < args.settle_ms:
+        s0.record(stream)
+        for i in range(64):
+            launch(settle_n + i)
+        s1.record(stream)
+        torch.cuda.synchronize()
+        settle_n += 64
+        settle_ms += s0.elapsed_time(s1)
+    log(f"settled after {settle_n} untimed launches ({settle_ms:.0f} ms); warmup and timing")
     for i in range(args.warmup):
         launch(i)
     torch.cuda.synchronize()
@@ -271,6 +289,8 @@ def main():
             "kernel_sha": kernel_hash(rescale),
         },
         "setup_s": setup_s,
+        "settle": {"launches": settle_n, "gpu_ms": settle_ms,
+                   "why": "untimed launches before warmup until the GPU clocks reach steady state under load"},
 
     }
     if rescale:

@@ -22,6 +22,30 @@ __device__ __forceinline__ float act_ld(const void *p, size_t i)
     }
 }
 
+// The code words of one tile, addressed through a buffer resource: the tile
+// base is uniform (scalar registers) and each thread adds a 32-bit offset, so
+// no 64-bit per-lane addresses are formed or kept live.  Word accesses stream
+// past the caches: loads non-temporal, stores non-temporal at device scope
+// (sc1 nt), the fastest policy measured for the in-place update on gfx950.
+// Accesses beyond `bytes` read 0 and write nothing.
+struct CodeWords {
+    static constexpr int kLoad = 2;         // nt
+    static constexpr int kStore = 16 | 2;   // sc1 nt
+    __amdgpu_buffer_rsrc_t r;
+    __device__ __forceinline__ CodeWords(const void *base, uint32_t bytes)
+        : r(__builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, static_cast<int>(bytes), 0x00020000))
+    {
+    }
+    __device__ __forceinline__ uint32_t load(int word) const
+    {
+        return __builtin_amdgcn_raw_buffer_load_b32(r, 4 * word, 0, kLoad);
+    }
+    __device__ __forceinline__ void store(int word, uint32_t v) const
+    {
+        __builtin_amdgcn_raw_buffer_store_b32(v, r, 4 * word, 0, kStore);
+    }
+};
+
 // Workgroups are dispatched round-robin over the 8 XCDs.  Give each XCD a
 // contiguous run of tiles so that value heads sharing a q/k head, and
 // neighbouring slot records, are served from the same L2.

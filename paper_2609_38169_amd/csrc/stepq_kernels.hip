@@ -37,9 +37,10 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
     constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;    // row-table starts of the 4- and 2-bit slots
     const int tid = threadIdx.x;
     const int cg = tid & 31, slice = tid >> 5;
+    const CodeWords cw(t.codes, 1024u * M);
     uint32_t w[M];
 #pragma unroll
-    for (int m = 0; m < M; ++m) w[m] = __builtin_nontemporal_load(t.codes + tid + 256 * m);
+    for (int m = 0; m < M; ++m) w[m] = cw.load(tid + 256 * m);
 
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
     const float kappa = row_constants_uniform<DIAG, M8, M4, 128>(t.beta, op, sh);
@@ -61,18 +62,15 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
     for (int m = 0; m < M8; ++m)
-        __builtin_nontemporal_store(requant_word_h<8, DIAG>(&U[2 * m], sh.av, sh.al, slice + 8 * m, t.alpha, bc),
-                                    t.codes + tid + 256 * m);
+        cw.store(tid + 256 * m, requant_word_h<8, DIAG>(&U[2 * m], sh.av, sh.al, slice + 8 * m, t.alpha, bc));
 #pragma unroll
     for (int m = 0; m < M4; ++m)
-        __builtin_nontemporal_store(requant_word_h<4, DIAG>(&U[2 * M8 + 4 * m], sh.av, sh.al, X4 + 2 * (slice + 8 * m),
-                                                    t.alpha * (1.0f / 16.0f), bc),
-                                    t.codes + tid + 256 * (M8 + m));
+        cw.store(tid + 256 * (M8 + m), requant_word_h<4, DIAG>(&U[2 * M8 + 4 * m], sh.av, sh.al, X4 + 2 * (slice + 8 * m),
+                                                               t.alpha * (1.0f / 16.0f), bc));
 #pragma unroll
     for (int m = 0; m < M2; ++m)
-        __builtin_nontemporal_store(requant_word_h<2, DIAG>(&U[2 * M8 + 4 * M4 + 8 * m], sh.av, sh.al, X2 + 4 * (slice + 8 * m),
-                                                    t.alpha * (1.0f / 64.0f), bc),
-                                    t.codes + tid + 256 * (M8 + M4 + m));
+        cw.store(tid + 256 * (M8 + M4 + m), requant_word_h<2, DIAG>(&U[2 * M8 + 4 * M4 + 8 * m], sh.av, sh.al,
+                                                                    X2 + 4 * (slice + 8 * m), t.alpha * (1.0f / 64.0f), bc));
 }
 
 // Any row-width mix and d_v: the class of each word-step is looked up at run
@@ -86,11 +84,12 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
     const int tid = threadIdx.x;
     const int cg = tid % CG, slice = tid / CG;
     const int ngroups = static_cast<int>(t.hi.groups);
+    const CodeWords cw(t.codes, t.hi.piv_off);
     uint32_t w[MMAX];
 #pragma unroll
     for (int m = 0; m < MMAX; ++m) {
         const int g = slice + NSL * m;
-        w[m] = g < ngroups ? __builtin_nontemporal_load(t.codes + tid + 256 * m) : 0u;
+        w[m] = g < ngroups ? cw.load(tid + 256 * m) : 0u;
     }
     PivotRegs<DV> pr;
     pivot_load<DV>(t, slice, cg, pr);
@@ -131,7 +130,7 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
                 unpack_word<2>(w[m], U);
                 nw = requant_word<2, DIAG>(U, sh.av, sh.al, gr.x0, t.alpha * (1.0f / 64.0f), bc);
             }
-            __builtin_nontemporal_store(nw, t.codes + tid + 256 * m);
+            cw.store(tid + 256 * m, nw);
         }
     }
 }

@@ -268,9 +268,10 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     const int cg = tid & 31, slice = tid >> 5;
     float *rr_out = const_cast<float *>(t.rr);
     float *cc_out = const_cast<float *>(t.cc);
+    const CodeWords cw(t.codes, 1024u * M);
     uint32_t w[M];
 #pragma unroll
-    for (int m = 0; m < M; ++m) w[m] = __builtin_nontemporal_load(t.codes + tid + 256 * m);
+    for (int m = 0; m < M; ++m) w[m] = cw.load(tid + 256 * m);
 
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
     if (tid < 128) {
@@ -325,13 +326,13 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
         for (int m = 0; m < M2; ++m) word_scale<2>(&Y[Y2 + 16 * m], sh.hrow, X2 + 4 * (slice + 8 * m));
 #pragma unroll
         for (int m = 0; m < M8; ++m)
-            __builtin_nontemporal_store(word_requant<8>(&Y[4 * m], cc), t.codes + tid + 256 * m);
+            cw.store(tid + 256 * m, word_requant<8>(&Y[4 * m], cc));
 #pragma unroll
         for (int m = 0; m < M4; ++m)
-            __builtin_nontemporal_store(word_requant<4>(&Y[Y4 + 8 * m], cc), t.codes + tid + 256 * (M8 + m));
+            cw.store(tid + 256 * (M8 + m), word_requant<4>(&Y[Y4 + 8 * m], cc));
 #pragma unroll
         for (int m = 0; m < M2; ++m)
-            __builtin_nontemporal_store(word_requant<2>(&Y[Y2 + 16 * m], cc), t.codes + tid + 256 * (M8 + M4 + m));
+            cw.store(tid + 256 * (M8 + M4 + m), word_requant<2>(&Y[Y2 + 16 * m], cc));
         return;
     }
 
@@ -372,13 +373,13 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     float g[4];
     ld4(&sh.gcol[4 * cg], g);
 #pragma unroll
-    for (int m = 0; m < M8; ++m) __builtin_nontemporal_store(word_requant<8>(&Y[4 * m], g), t.codes + tid + 256 * m);
+    for (int m = 0; m < M8; ++m) cw.store(tid + 256 * m, word_requant<8>(&Y[4 * m], g));
 #pragma unroll
     for (int m = 0; m < M4; ++m)
-        __builtin_nontemporal_store(word_requant<4>(&Y[Y4 + 8 * m], g), t.codes + tid + 256 * (M8 + m));
+        cw.store(tid + 256 * (M8 + m), word_requant<4>(&Y[Y4 + 8 * m], g));
 #pragma unroll
     for (int m = 0; m < M2; ++m)
-        __builtin_nontemporal_store(word_requant<2>(&Y[Y2 + 16 * m], g), t.codes + tid + 256 * (M8 + M4 + m));
+        cw.store(tid + 256 * (M8 + M4 + m), word_requant<2>(&Y[Y2 + 16 * m], g));
 }
 
 // ---- any row-width mix and d_v: the words stay packed in registers and
@@ -432,11 +433,12 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
     const int dk = a.pool.dk;
     float *rr_out = const_cast<float *>(t.rr);
     float *cc_out = const_cast<float *>(t.cc);
+    const CodeWords cw(t.codes, t.hi.piv_off);
     uint32_t w[MMAX];
 #pragma unroll
     for (int m = 0; m < MMAX; ++m) {
         const int g = slice + NSL * m;
-        w[m] = g < ngroups ? __builtin_nontemporal_load(t.codes + tid + 256 * m) : 0u;
+        w[m] = g < ngroups ? cw.load(tid + 256 * m) : 0u;
     }
     PivotRegs<DV> pr;
     pivot_load<DV>(t, slice, cg, pr);
@@ -488,7 +490,7 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
             float Y[16];
             gen_word_y<B, DIAG, DV>(w[m], sh.d, gr.x0, t.alpha, bc, Y);
             word_scale<B>(Y, sh.hrow, gr.x0);
-            __builtin_nontemporal_store(word_requant<B>(Y, cc), t.codes + tid + 256 * m);
+            cw.store(tid + 256 * m, word_requant<B>(Y, cc));
         });
         return;
     }
@@ -551,7 +553,7 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
 #pragma unroll
             for (int e = 0; e < 4; ++e) Y[4 * s + e] *= h;
         }
-        __builtin_nontemporal_store(word_requant<B>(Y, g), t.codes + tid + 256 * m);
+        cw.store(tid + 256 * m, word_requant<B>(Y, g));
     });
 }
 
