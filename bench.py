@@ -1,12 +1,18 @@
 """Decode-step throughput of the quantized gated-Delta state pool on one MI355X.
 
-Default workload: a 2048-slot pool, 512 active requests x 32 heads,
-d_k = d_v = 128, 6-bit mixed {4,8} codes with fp32 row/column scales, bf16
-activations.  One "step" is one fused decode launch over all 16,384 active
-(request, head) tiles.  By default successive steps rotate over four
+Default workload (pool_b512): a 2048-slot pool, 512 active requests x 32
+heads, d_k = d_v = 128, 6-bit mixed {4,8} codes with fp32 row/column scales,
+bf16 activations.  One "step" is one fused decode launch over all 16,384
+active (request, head) tiles.  By default successive steps rotate over four
 disjoint 512-slot subsets of the pool (832 MiB cycle), so a step's 208 MiB
 of state is not still resident in the 256 MB last-level cache from the
 previous one; --resident keeps one subset (reported as cache-resident).
+
+--workload pool_4bit: 512 active of a 2048-slot pool (rotated the same way),
+32 heads, {2,4,8} codes at 4.0 bits per element, heavy-tailed states.
+--workload stack48: 48 layers x 256 requests x 32 value heads (16 q/k heads),
+6-bit {4,8}; one step is one replay of a HIP graph holding the 48 per-layer
+launches (the 5.2 GB of packed state is far beyond the last-level cache).
 
 Prints one JSON line (rank 0):
   value      state-updates/s (tiles advanced per second) over the timed steps
@@ -42,9 +48,9 @@ METRIC = "state-updates/s and achieved HBM GB/s (% of peak), B=512 heads=32 dk=d
 CSRC = os.path.join(ROOT, "paper_2609_38169_amd", "csrc")
 
 
-def traffic_file(refit: bool, kda: bool) -> str:
+def traffic_file(refit: bool, kda: bool, workload: str = "pool_b512") -> str:
     name = ("refit" if refit else "decode") + ("_kda" if kda else "")
-    return os.path.join(ROOT, "profiles", f"traffic_{name}_pool_b512.json")
+    return os.path.join(ROOT, "profiles", f"traffic_{name}_{workload}.json")
 
 
 def kernel_sources(refit: bool):
@@ -78,7 +84,7 @@ def state_bytes_per_tile(bits_row, d_k, d_v, refit: bool = False) -> int:
 
 def cpu_baseline(w, bits, seconds: float):
     """The fp64 oracle on the host: decode steps on a sample of tiles of the
-    same workload until ~seconds have elapsed."""
+    same workload (layer 0) until ~seconds have elapsed."""
     import numpy as np
     import oracle
     from paper_2609_38169_amd import workloads as W
@@ -113,12 +119,13 @@ def cpu_baseline(w, bits, seconds: float):
                       f"{elapsed:.1f} s of oracle time (4 distinct input steps cycled, draws excluded)"}
 
 
-def traffic_entry(refit: bool, kda: bool):
+def traffic_entry(refit: bool, kda: bool, workload: str = "pool_b512"):
     """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
-    copy's counters) from the committed rocprofv3 summary of this kernel and
-    mode, if it was taken on the current kernel source; else None."""
+    copy's counters) from the committed rocprofv3 summary of this kernel,
+    mode and workload, if it was taken on the current kernel source; else
+    None."""
     try:
-        t = json.load(open(traffic_file(refit, kda)))
+        t = json.load(open(traffic_file(refit, kda, workload)))
     except (OSError, ValueError):
         return None
     if t.get("kernel_sha") != kernel_hash(refit):
@@ -127,13 +134,108 @@ def traffic_entry(refit: bool, kda: bool):
     return b.get("total") if isinstance(b, dict) else b
 
 
+class Case:
+    """One benchmark workload on the device: step(i) enqueues decode step i
+    (launches_per_step kernel launches) on the current stream."""
+
+    def __init__(self, **kw):
+        self.__dict__.update(kw)
+
+
+def pool_case(args, w, mode, dev):
+    """A single-layer pool whose steps rotate over disjoint slot subsets."""
+    import numpy as np
+    import torch
+    from paper_2609_38169_amd import workloads as W
+    from paper_2609_38169_amd.pools import build_pool, row_bits
+
+    bits = row_bits(w)
+    log(f"building the {w.n_slots}-slot pool")
+    pool = build_pool(w, device=dev, bits=bits)
+    subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
+    n_inp = min(w.steps, args.steps + args.warmup)
+    inputs = [W.step_inputs(w, 0, t, device=dev) for t in range(n_inp)]
+    if args.kda:
+        for t, inp in enumerate(inputs):
+            inp["alpha"] = W.kda_gates(w, 0, t, device=dev)
+    o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=dev)
+    prepared = {}      # one prepared call per (input step, slot subset) pair: arguments checked once
+
+    def step(i):
+        key = (i % n_inp, i % len(subsets))
+        if key not in prepared:
+            inp = inputs[key[0]]
+            prepared[key] = pool.prepare_step(subsets[key[1]], inp["q"], inp["k"], inp["v"], inp["alpha"],
+                                              inp["beta"], o, stream=torch.cuda.current_stream(), refit=mode)
+        prepared[key]()
+
+    mix = {"pool_b512": "6-bit mixed {4,8}", "pool_4bit": "4-bit mixed {2,4,8}, heavy-tailed states"}[w.name]
+    return Case(w=w, bits=bits, step=step, launches_per_step=1, n_subsets=len(subsets), keep=(pool, inputs, o),
+                tiles_per_step=w.batch * w.n_v_heads, layers=1,
+                workload=f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
+                         f"d_k=d_v={w.d_k}, {mix}, fp32 scales, bf16 activations",
+                extra={"slot_rotation": len(subsets), "cache_resident": bool(args.resident)},
+                pool_bytes=pool.pool_bytes)
+
+
+def stack_case(args, w, mode, dev):
+    """48 layer pools; one step is one graph replay of the 48 launches."""
+    import numpy as np
+    import torch
+    from paper_2609_38169_amd import workloads as W
+    from paper_2609_38169_amd.pools import build_pool, row_bits
+
+    slots = W.active_slots(w).to(dev)
+    pools, bufs, bits0 = [], [], None
+    for L in range(w.layers):
+        b = row_bits(w, L)
+        bits0 = b if bits0 is None else bits0
+        pools.append(build_pool(w, L, device=dev, bits=b))
+        inp = W.step_inputs(w, L, 0, device=dev)
+        if args.kda:
+            inp["alpha"] = W.kda_gates(w, L, 0, device=dev)
+        inp["o"] = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=dev)
+        bufs.append(inp)
+        if L % 8 == 7:
+            log(f"{L + 1} of {w.layers} layer pools built")
+    main_stream = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    side.wait_stream(main_stream)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        calls = [pools[L].prepare_step(slots, bufs[L]["q"], bufs[L]["k"], bufs[L]["v"], bufs[L]["alpha"],
+                                       bufs[L]["beta"], bufs[L]["o"], stream=side, refit=mode)
+                 for L in range(w.layers)]
+        with torch.cuda.graph(graph, stream=side):
+            for c in calls:
+                c()
+    main_stream.wait_stream(side)
+    torch.cuda.synchronize()
+
+    def step(i):
+        graph.replay()
+
+    pool_bytes = sum(p.pool_bytes for p in pools)
+    fp32_bytes = w.layers * w.n_slots * w.n_v_heads * w.d_k * w.d_v * 4
+    return Case(w=w, bits=bits0, step=step, launches_per_step=w.layers, n_subsets=1,
+                keep=(pools, bufs, graph, calls, side), tiles_per_step=w.layers * w.batch * w.n_v_heads,
+                layers=w.layers,
+                workload=f"{w.name}: {w.layers} layers x B={w.batch} requests x {w.n_v_heads} value heads "
+                         f"({w.n_qk_heads} q/k heads), d_k=d_v={w.d_k}, 6-bit mixed {{4,8}}, fp32 scales, "
+                         f"bf16 activations, one HIP graph of {w.layers} launches per step",
+                extra={"graph_launches_per_step": w.layers, "pool_bytes": pool_bytes, "fp32_pool_bytes": fp32_bytes,
+                       "pool_compression": fp32_bytes / pool_bytes},
+                pool_bytes=pool_bytes)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=256)
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--settle-ms", type=float, default=150.0,
-                    help="untimed launches before the warmup until this much GPU time has elapsed (clock ramp)")
+                    help="untimed steps before the warmup until this much GPU time has elapsed (clock ramp)")
+    ap.add_argument("--workload", choices=["pool_b512", "pool_4bit", "stack48"], default="pool_b512")
     ap.add_argument("--resident", action="store_true", help="no slot rotation (cache-resident number)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -154,99 +256,90 @@ def main():
               "independent; see the sharding note in DESIGN.md). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
+    import dataclasses
     import numpy as np
     import torch
-    from paper_2609_38169_amd import stepq, workloads as W
-    from paper_2609_38169_amd.pools import build_pool, row_bits
+    from paper_2609_38169_amd import workloads as W
 
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    w = W.workload(2)
-    bits = row_bits(w)
     t_setup = time.perf_counter()
-    log("building the 2048-slot pool")
-    pool = build_pool(w, device=dev, bits=bits)
-    subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
-    n_inp = min(w.steps, args.steps + args.warmup)
-    inputs = [W.step_inputs(w, 0, t, device=dev) for t in range(n_inp)]
-    if args.kda:
-        for t, inp in enumerate(inputs):
-            inp["alpha"] = W.kda_gates(w, 0, t, device=dev)
-    o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=dev)
+    if args.workload == "pool_b512":
+        case = pool_case(args, W.workload(2), mode, dev)
+    elif args.workload == "pool_4bit":
+        # the 512-request workload on a 2048-slot pool, so that rotating slot
+        # subsets keeps each step's state out of the last-level cache
+        case = pool_case(args, dataclasses.replace(W.workload(3), n_slots=2048), mode, dev)
+    else:
+        case = stack_case(args, W.workload(4), mode, dev)
+    w = case.w
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
-
     stream = torch.cuda.current_stream()
-    # one prepared call per (input step, slot subset) pair: arguments checked once
-    prepared = {}
+    LPS = case.launches_per_step
 
-    def launch(i):
-        key = (i % n_inp, i % len(subsets))
-        if key not in prepared:
-            inp = inputs[key[0]]
-            prepared[key] = pool.prepare_step(subsets[key[1]], inp["q"], inp["k"], inp["v"], inp["alpha"],
-                                              inp["beta"], o, stream=torch.cuda.current_stream(),
-                                              refit=mode)
-        prepared[key]()
-
-    log(f"pool and inputs ready in {time.perf_counter() - t_setup:.1f} s; settling clocks")
+    log(f"setup done in {setup_s:.1f} s; settling clocks")
     # Settle: the GPU's clocks ramp up over the first ~50 ms of sustained
-    # load (a step measured on a cold GPU is ~20% slower), so launches run
+    # load (a step measured on a cold GPU is ~20% slower), so steps run
     # untimed until args.settle_ms of GPU time has elapsed; then the W
     # warmup steps; then the K timed steps.
     settle_n, settle_ms = 0, 0.0
     s0 = torch.cuda.Event(enable_timing=True)
     s1 = torch.cuda.Event(enable_timing=True)
+    chunk = max(1, 64 // LPS)
     while settle_ms < args.settle_ms:
         s0.record(stream)
-        for i in range(64):
-            launch(settle_n + i)
+        for i in range(chunk):
+            case.step(settle_n + i)
         s1.record(stream)
         torch.cuda.synchronize()
-        settle_n += 64
+        settle_n += chunk
         settle_ms += s0.elapsed_time(s1)
-    log(f"settled after {settle_n} untimed launches ({settle_ms:.0f} ms); warmup and timing")
+    log(f"settled after {settle_n} untimed steps ({settle_ms:.0f} ms); warmup and timing")
     for i in range(args.warmup):
-        launch(i)
+        case.step(i)
     torch.cuda.synchronize()
 
     K = args.steps
-    # timed region: K back-to-back launches between two events on the launch stream
     for i in range(args.warmup, args.warmup + K):
-        launch(i)                       # prepare every call outside the timed region
+        case.step(i)                    # prepare every call outside the timed region
     torch.cuda.synchronize()
+    # timed region: K back-to-back steps between two events on the launch stream
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record(stream)
     for i in range(K):
-        launch(args.warmup + i)
+        case.step(args.warmup + i)
     t1.record(stream)
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
-    kern_ms = total_ms / K          # mean launch duration, gaps between launches included
+    kern_ms = total_ms / (K * LPS)  # mean launch duration, gaps between launches included
 
-    # diagnostics outside the timed region: one event pair per launch
+    # diagnostics outside the timed region: one event pair per step
     n_diag = min(K, 64)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * n_diag)]
     for i in range(n_diag):
         ev[2 * i].record(stream)
-        launch(args.warmup + K + i)
+        case.step(args.warmup + K + i)
         ev[2 * i + 1].record(stream)
     torch.cuda.synchronize()
-    per_launch_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(n_diag)]
-    nsub = len(subsets)
+    per_launch_ms = [ev[2 * i].elapsed_time(ev[2 * i + 1]) / LPS for i in range(n_diag)]
+    nsub = case.n_subsets
     per_subset = [float(np.mean([per_launch_ms[i] for i in range(n_diag) if (args.warmup + K + i) % nsub == j] or [0.0]))
                   for j in range(nsub)]
 
-    tiles = w.tiles_per_step
+    bits = case.bits
     per_tile = [state_bytes_per_tile(bits[h], w.d_k, w.d_v, rescale) for h in range(w.n_v_heads)]
-    launch_bytes = w.batch * sum(per_tile)
+    launch_bytes = w.batch * sum(per_tile)           # one launch = one layer of the step
     gate_elems = w.n_v_heads * (w.d_k if args.kda else 1)
     act_bytes = w.batch * (2 * w.n_qk_heads * w.d_k * 2 + w.n_v_heads * w.d_v * 2 + (gate_elems + w.n_v_heads) * 2
                            + w.n_v_heads * w.d_v * 4 + 4)
     achieved = launch_bytes / (kern_ms * 1e-3) / 1e9
     valu_tops = w.batch * w.n_v_heads * w.d_k * w.d_v * OPS_PER_ELEMENT[mode] / (kern_ms * 1e-3) / 1e12
-    value = tiles * K / (total_ms * 1e-3)
+    value = case.tiles_per_step * K / (total_ms * 1e-3)
+    state_gbps = launch_bytes * LPS * K / (total_ms * 1e-3) / 1e9
+    kern_name = ("refit_kernel" if rescale else "decode_kernel") + ("<128, bf16, kda" if args.kda else "<128, bf16")
+    kern_name += {True: ", dual axis>", "row_absmax": ", row absmax>", False: ">"}[mode]
 
     line = {
         "metric": METRIC,
@@ -261,27 +354,24 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
-                               f"d_k=d_v={w.d_k}, 6-bit mixed {{4,8}}, fp32 scales, bf16 activations",
-                   "slot_rotation": 1 if args.resident else len(subsets),
-                   "cache_resident": bool(args.resident),
-                   "gate": "channel-wise d [B][Hv][d_k] (KDA)" if args.kda else "scalar alpha [B][Hv] (GDN)",
-                   "scales": {True: "online dual-axis refit every step", "row_absmax": "row-wise absmax every step "
-                              "(INT-b baseline)", False: "frozen"}[mode]},
-        "GBps_state": launch_bytes * K / (total_ms * 1e-3) / 1e9,
-        "pct_hbm_peak": 100.0 * launch_bytes * K / (total_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "config": dict({"workload": case.workload,
+                        "gate": "channel-wise d [B][Hv][d_k] (KDA)" if args.kda else "scalar alpha [B][Hv] (GDN)",
+                        "scales": {True: "online dual-axis refit every step", "row_absmax": "row-wise absmax every "
+                                   "step (INT-b baseline)", False: "frozen"}[mode]}, **case.extra),
+        "GBps_state": state_gbps,
+        "pct_hbm_peak": 100.0 * state_gbps / HBM_PEAK_GBPS,
         "roofline": {
             "bound": "hbm",
             "achieved": achieved,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic_entry(args.refit, args.kda) if not args.row_absmax else None,
+            "traffic": traffic_entry(args.refit, args.kda, w.name) if not args.row_absmax else None,
             "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Top/s", "frac": valu_tops / VALU_PEAK_TOPS,
                      "ops_per_element": OPS_PER_ELEMENT[mode]},
-            "kernel": ("refit_kernel" if rescale else "decode_kernel") + ("<128, bf16, kda" if args.kda else "<128, bf16")
-                      + {True: ", dual axis>", "row_absmax": ", row absmax>", False: ">"}[mode],
+            "kernel": kern_name,
             "kernel_ms_mean": kern_ms,
+            "launches_per_step": LPS,
             "launch_ms_event_pairs": {"mean": float(np.mean(per_launch_ms)), "min": float(np.min(per_launch_ms)),
                                       "max": float(np.max(per_launch_ms)), "per_slot_subset": per_subset},
             "bytes_per_launch": launch_bytes,
@@ -289,9 +379,8 @@ def main():
             "kernel_sha": kernel_hash(rescale),
         },
         "setup_s": setup_s,
-        "settle": {"launches": settle_n, "gpu_ms": settle_ms,
-                   "why": "untimed launches before warmup until the GPU clocks reach steady state under load"},
-
+        "settle": {"steps": settle_n, "gpu_ms": settle_ms,
+                   "why": "untimed steps before warmup until the GPU clocks reach steady state under load"},
     }
     if rescale:
         # the refitting steps are bound by fp32 VALU work, not by HBM: that roofline is the primary one
