@@ -382,8 +382,11 @@ def main():
         "settle": {"steps": settle_n, "gpu_ms": settle_ms,
                    "why": "untimed steps before warmup until the GPU clocks reach steady state under load"},
     }
-    if rescale:
-        # the refitting steps are bound by fp32 VALU work, not by HBM: that roofline is the primary one
+    if rescale or w.name == "pool_4bit":
+        # Bound by fp32 VALU work, not by HBM, so that roofline is the primary one: the refitting
+        # steps, and the {2,4,8} pool, whose 2-bit rows carry four codes per byte (a copy of the
+        # frozen kernel with its arithmetic removed moves the pool_4bit bytes in ~52 us against
+        # ~72 us for the full kernel; on pool_b512 and stack48 the two are within a few percent).
         rl = line["roofline"]
         hbm = {k: rl[k] for k in ("achieved", "peak", "unit", "frac")}
         valu = rl.pop("valu")
