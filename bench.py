@@ -48,14 +48,19 @@ METRIC = "state-updates/s and achieved HBM GB/s (% of peak), B=512 heads=32 dk=d
 CSRC = os.path.join(ROOT, "paper_2609_38169_amd", "csrc")
 
 
-def traffic_file(refit: bool, kda: bool, workload: str = "pool_b512") -> str:
-    name = ("refit" if refit else "decode") + ("_kda" if kda else "")
+def mode_name(mode) -> str:
+    return {False: "decode", True: "refit", "row_absmax": "rowmax"}[mode]
+
+
+def traffic_file(mode, kda: bool, workload: str = "pool_b512", pivots: bool = False) -> str:
+    name = mode_name(mode) + ("_kda" if kda else "") + ("_pivots" if pivots else "")
     return os.path.join(ROOT, "profiles", f"traffic_{name}_{workload}.json")
 
 
-def kernel_sources(refit: bool):
+def kernel_sources(mode):
     files = ["stepq_device.h", "stepq_internal.h"]
-    files += ["stepq_refit_body.h", "stepq_refit.hip"] if refit else ["stepq_kernels.hip"]
+    files += {False: ["stepq_kernels.hip"], True: ["stepq_refit_body.h", "stepq_refit.hip"],
+              "row_absmax": ["stepq_refit_body.h", "stepq_rowmax.hip"]}[mode]
     return [os.path.join(CSRC, f) for f in files]
 
 
@@ -63,22 +68,23 @@ def log(msg: str):
     print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_hash(refit: bool = False) -> str:
+def kernel_hash(mode=False) -> str:
     """Hash of the sources of the timed kernel, to tell whether committed
     counter summaries were taken on it."""
     h = hashlib.sha256()
-    for f in kernel_sources(refit):
+    for f in kernel_sources(mode):
         h.update(open(f, "rb").read())
     return h.hexdigest()[:16]
 
 
 def state_bytes_per_tile(bits_row, d_k, d_v, refit: bool = False) -> int:
-    """Algorithmic bytes one tile update moves: its codes read and written
-    once, its fp32 row and column scales read once (and written once more
-    when the step refits them)."""
+    """Algorithmic bytes one tile update moves: its codes (and binary16
+    pivot rows) read and written once, its fp32 row and column scales read
+    once (and written once more when the step refits them)."""
     import numpy as np
+    n16 = int(np.sum(bits_row == 16))
     n8 = int(np.sum(bits_row == 8)); n4 = int(np.sum(bits_row == 4)); n2 = int(np.sum(bits_row == 2))
-    code_bytes = (8 * n8 + 4 * n4 + 2 * n2) * d_v // 8
+    code_bytes = (16 * n16 + 8 * n8 + 4 * n4 + 2 * n2) * d_v // 8
     return 2 * code_bytes + (2 if refit else 1) * 4 * (d_k + d_v)
 
 
@@ -119,16 +125,16 @@ def cpu_baseline(w, bits, seconds: float):
                       f"{elapsed:.1f} s of oracle time (4 distinct input steps cycled, draws excluded)"}
 
 
-def traffic_entry(refit: bool, kda: bool, workload: str = "pool_b512"):
+def traffic_entry(mode, kda: bool, workload: str = "pool_b512", pivots: bool = False):
     """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
     copy's counters) from the committed rocprofv3 summary of this kernel,
     mode and workload, if it was taken on the current kernel source; else
     None."""
     try:
-        t = json.load(open(traffic_file(refit, kda, workload)))
+        t = json.load(open(traffic_file(mode, kda, workload, pivots)))
     except (OSError, ValueError):
         return None
-    if t.get("kernel_sha") != kernel_hash(refit):
+    if t.get("kernel_sha") != kernel_hash(mode):
         return None
     b = t.get("bytes_per_launch")
     return b.get("total") if isinstance(b, dict) else b
@@ -150,6 +156,10 @@ def pool_case(args, w, mode, dev):
     from paper_2609_38169_amd.pools import build_pool, row_bits
 
     bits = row_bits(w)
+    if args.pivots:
+        # FP16 pivot rows: a seeded quarter of the heads keep 1-3 key rows in binary16
+        bits = bits.copy()
+        bits[W.pivot_mask_draw(w).numpy()] = 16
     log(f"building the {w.n_slots}-slot pool")
     pool = build_pool(w, device=dev, bits=bits)
     subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
@@ -170,6 +180,8 @@ def pool_case(args, w, mode, dev):
         prepared[key]()
 
     mix = {"pool_b512": "6-bit mixed {4,8}", "pool_4bit": "4-bit mixed {2,4,8}, heavy-tailed states"}[w.name]
+    if args.pivots:
+        mix += f", {int((bits == 16).sum())} FP16 pivot rows in {int((bits == 16).any(1).sum())} of {w.n_v_heads} heads"
     return Case(w=w, bits=bits, step=step, launches_per_step=1, n_subsets=len(subsets), keep=(pool, inputs, o),
                 tiles_per_step=w.batch * w.n_v_heads, layers=1,
                 workload=f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
@@ -244,10 +256,15 @@ def main():
     ap.add_argument("--refit", action="store_true", help="online dual-axis refit of the scales in every step")
     ap.add_argument("--row-absmax", action="store_true",
                     help="requantize as the row-wise absmax INT-b baseline (row factors refit, column factors 1)")
+    ap.add_argument("--pivots", action="store_true",
+                    help="a seeded quarter of the heads keep 1-3 FP16 pivot rows (pool workloads)")
     args = ap.parse_args()
 
     if args.refit and args.row_absmax:
         print("--refit and --row-absmax exclude each other", file=sys.stderr)
+        sys.exit(2)
+    if args.pivots and args.workload == "stack48":
+        print("--pivots applies to the single-layer pool workloads", file=sys.stderr)
         sys.exit(2)
     mode = True if args.refit else ("row_absmax" if args.row_absmax else False)
     rescale = bool(mode)          # the step writes the scales back
@@ -339,7 +356,8 @@ def main():
     value = case.tiles_per_step * K / (total_ms * 1e-3)
     state_gbps = launch_bytes * LPS * K / (total_ms * 1e-3) / 1e9
     kern_name = ("refit_kernel" if rescale else "decode_kernel") + ("<128, bf16, kda" if args.kda else "<128, bf16")
-    kern_name += {True: ", dual axis>", "row_absmax": ", row absmax>", False: ">"}[mode]
+    kern_name += {True: ", dual axis", "row_absmax": ", row absmax", False: ""}[mode]
+    kern_name += (", heads with pivots on the generic body>" if args.pivots else ">")
 
     line = {
         "metric": METRIC,
@@ -366,7 +384,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic_entry(args.refit, args.kda, w.name) if not args.row_absmax else None,
+            "traffic": traffic_entry(mode, args.kda, w.name, args.pivots),
             "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Top/s", "frac": valu_tops / VALU_PEAK_TOPS,
                      "ops_per_element": OPS_PER_ELEMENT[mode]},
             "kernel": kern_name,
@@ -376,7 +394,7 @@ def main():
                                       "max": float(np.max(per_launch_ms)), "per_slot_subset": per_subset},
             "bytes_per_launch": launch_bytes,
             "activation_bytes_per_launch": act_bytes,
-            "kernel_sha": kernel_hash(rescale),
+            "kernel_sha": kernel_hash(mode),
         },
         "setup_s": setup_s,
         "settle": {"steps": settle_n, "gpu_ms": settle_ms,

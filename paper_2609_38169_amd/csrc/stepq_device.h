@@ -160,11 +160,33 @@ struct DecodeShared {
 
 struct TileCtx {
     int tile, b, h, hq;
+    uint32_t off;            // byte offset of the tile in its slot record (uniform bodies)
     HeadInfo hi;
     uint32_t *codes;
     const float *rr, *cc;
     float alpha, beta;
 };
+
+// The (request, value head) tile of this workgroup among the batch x
+// n_heads tiles of the launch; t.tile = b Hv + h indexes the activations.
+// tile_bytes: the tile size shared by every head when the launch covers the
+// whole pool in head order (a.head_list NULL).
+__device__ __forceinline__ void tile_of(const DecodeArgs &a, uint32_t tile_bytes, TileCtx &t)
+{
+    const int l = xcd_tile(blockIdx.x, a.batch * a.n_heads);
+    t.b = fdiv(l, a.div_heads);
+    const int j = l - t.b * a.n_heads;
+    if (a.head_list) {
+        const LaunchHead lh = a.head_list[j];
+        t.h = lh.h;
+        t.off = lh.tile_off;
+    } else {
+        t.h = j;
+        t.off = static_cast<uint32_t>(j) * tile_bytes;
+    }
+    t.tile = t.b * a.pool.Hv + t.h;
+    t.hq = fdiv(t.h, a.pool.div_g);
+}
 
 // Per-tile operands of thread tid, loaded together at the start of a tile:
 // k_i, q_i for logical row i = tid; r_p and the logical index of physical

@@ -25,6 +25,11 @@ struct stepq_pool {
     float *d_roww = nullptr;          // [Hv][dk] row-impact factors, physical order
     int device = 0;
     int layout = 0;                   // uniform layout of every head, or 0
+    // Layout classes of a mixed pool at d_v = 128: heads grouped by their
+    // uniform layout (1-5) or 0 (generic body); one decode launch per class.
+    // Empty when one launch covers every head.
+    std::vector<int> cls_layout, cls_off, cls_cnt;
+    stepq::LaunchHead *d_head_order = nullptr;  // [Hv] heads ordered by class, device
 };
 
 namespace {
@@ -99,6 +104,13 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
         hi.r_off = static_cast<uint32_t>(creg + preg);
         hi.tile_bytes = static_cast<uint32_t>(tb);
         hi.tile_off = static_cast<uint32_t>(off);
+        if (hi.layout > 0) {
+            // the compiled bodies address codes, r and c from these sizes
+            const stepq::UniformLayout &u = stepq::kUniformLayouts[hi.layout - 1];
+            const uint32_t m = static_cast<uint32_t>(u.m8 + u.m4 + u.m2);
+            if (hi.r_off != 1024u * m || hi.tile_bytes != 1024u * (m + 1))
+                return fail(STEPQ_E_INVALID, "internal: uniform head layout does not match its tile size");
+        }
         off += tb;
     }
     *slot_bytes = off;
@@ -244,6 +256,28 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
         const std::vector<float> ones(p->perm.size(), 1.0f);
         e = hipMemcpy(p->d_roww, ones.data(), sizeof(float) * ones.size(), hipMemcpyHostToDevice);
     }
+    if (e == hipSuccess && p->layout == 0 && p->dv == 128) {
+        // one class per layout present; larger classes are launched first
+        std::vector<stepq::LaunchHead> order;
+        std::vector<std::pair<int, int>> cls;   // (-count, layout)
+        for (int L = 0; L <= stepq::kNumUniformLayouts; ++L) {
+            int n = 0;
+            for (const HeadInfo &hi : p->heads) n += static_cast<int>(hi.layout) == L;
+            if (n > 0) cls.emplace_back(-n, L);
+        }
+        std::sort(cls.begin(), cls.end());
+        for (const auto &c : cls) {
+            p->cls_layout.push_back(c.second);
+            p->cls_off.push_back(static_cast<int>(order.size()));
+            p->cls_cnt.push_back(-c.first);
+            for (int h = 0; h < p->Hv; ++h)
+                if (static_cast<int>(p->heads[h].layout) == c.second) order.push_back({h, p->heads[h].tile_off});
+        }
+        e = hipMalloc(reinterpret_cast<void **>(&p->d_head_order), sizeof(stepq::LaunchHead) * order.size());
+        if (e == hipSuccess)
+            e = hipMemcpy(p->d_head_order, order.data(), sizeof(stepq::LaunchHead) * order.size(),
+                          hipMemcpyHostToDevice);
+    }
     if (e != hipSuccess) {
         stepq_pool_destroy(p);
         return fail(STEPQ_E_NOMEM, std::string("layout tables: ") + hipGetErrorString(e));
@@ -260,6 +294,7 @@ void stepq_pool_destroy(stepq_pool *p)
     if (p->d_heads) (void)hipFree(p->d_heads);
     if (p->d_perm) (void)hipFree(p->d_perm);
     if (p->d_roww) (void)hipFree(p->d_roww);
+    if (p->d_head_order) (void)hipFree(p->d_head_order);
     delete p;
 }
 
@@ -313,9 +348,26 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     a.batch = batch;
     const bool diag = (flags & STEPQ_STEP_KDA_GATE) != 0;
     const bool bf16 = act_dtype == STEPQ_BF16;
-    hipError_t e = (flags & STEPQ_STEP_REFIT)        ? stepq::launch_decode_refit(a, bf16, diag, p->layout, s)
-                   : (flags & STEPQ_STEP_ROW_ABSMAX) ? stepq::launch_decode_rowmax(a, bf16, diag, p->layout, s)
-                                                     : stepq::launch_decode(a, bf16, diag, p->layout, s);
+    auto launch = [&](int layout) {
+        return (flags & STEPQ_STEP_REFIT)        ? stepq::launch_decode_refit(a, bf16, diag, layout, s)
+               : (flags & STEPQ_STEP_ROW_ABSMAX) ? stepq::launch_decode_rowmax(a, bf16, diag, layout, s)
+                                                 : stepq::launch_decode(a, bf16, diag, layout, s);
+    };
+    hipError_t e = hipSuccess;
+    if (p->cls_layout.empty()) {
+        a.head_list = nullptr;
+        a.n_heads = p->Hv;
+        a.div_heads = fast_div(static_cast<uint32_t>(p->Hv));
+        e = launch(p->layout);
+    } else {
+        // a mixed pool: one launch per layout class, each with its own register budget
+        for (size_t c = 0; c < p->cls_layout.size() && e == hipSuccess; ++c) {
+            a.head_list = p->d_head_order + p->cls_off[c];
+            a.n_heads = p->cls_cnt[c];
+            a.div_heads = fast_div(static_cast<uint32_t>(p->cls_cnt[c]));
+            e = launch(p->cls_layout[c]);
+        }
+    }
     return e == hipSuccess ? STEPQ_OK : hip_fail(e, "decode launch");
 }
 

@@ -62,12 +62,25 @@ struct PoolView {
     FastDiv div_g;           // divide by Hv / Hqk
 };
 
+// One value head of a decode launch over part of a pool's heads: its index
+// and the byte offset of its tile within a slot record.
+struct LaunchHead {
+    int32_t h;
+    uint32_t tile_off;
+};
+
 struct DecodeArgs {
     PoolView pool;
     const int32_t *slot_ids;
     const void *q, *k, *v, *alpha, *beta;
     float *o;
     int32_t batch;
+    // The value heads one launch covers: head_list[0 .. n_heads) (device),
+    // or every head 0 .. Hv-1 in order when head_list is NULL (then every
+    // head has the same tile size).  The grid is batch x n_heads workgroups.
+    const LaunchHead *head_list;
+    int32_t n_heads;
+    FastDiv div_heads;       // divide by n_heads
 };
 
 enum class TileOp : int { Load = 0, Import = 1, Export = 2, Dequant = 3, ExportPivots = 4, ImportPivots = 5 };
@@ -87,7 +100,9 @@ struct TileArgs {
     uint16_t *piv_out;       // ExportPivots: [n][Hv][dk][dv] binary16, pivot rows written, others 0
 };
 
-// pool_layout: the uniform layout shared by every head (1-based), or 0.
+// pool_layout: the uniform layout (1-based) shared by every head of the
+// launch (a.head_list), or 0 for the generic body (irregular row-width
+// mixes, FP16 pivot rows, d_v = 64).
 // diag: a.alpha holds the channel-wise gate [batch][Hv][d_k] instead of the
 // scalar gate [batch][Hv].
 hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);

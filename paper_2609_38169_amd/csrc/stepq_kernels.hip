@@ -135,21 +135,22 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
     }
 }
 
-// LAYOUT > 0: every head of the pool has uniform layout LAYOUT (checked on
-// the host), so the kernel holds only that body and its register budget.
-// LAYOUT == 0: heads may differ; each workgroup branches on its head's
-// layout (uniformly, so without divergence); d_v = 64 and irregular
-// row-width mixes take the generic body.
+// LAYOUT > 0: every head of the launch has uniform layout LAYOUT (the host
+// launches each layout class of a pool separately), so the kernel holds
+// only that body and its register budget.  LAYOUT == 0: the generic body
+// (irregular row-width mixes, FP16 pivot rows, d_v = 64).
 template <int DV, bool BF16, int LAYOUT, bool DIAG>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 {
     __shared__ DecodeShared<DV> sh;
     const PoolView &P = a.pool;
     TileCtx t;
-    t.tile = xcd_tile(blockIdx.x, a.batch * P.Hv);
-    t.b = fdiv(t.tile, P.div_hv);
-    t.h = t.tile - t.b * P.Hv;
-    t.hq = fdiv(t.h, P.div_g);
+    uint32_t tile_bytes = 0;
+    if constexpr (DV == 128 && LAYOUT > 0) {
+        constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
+        tile_bytes = 1024u * (u.m8 + u.m4 + u.m2 + 1);
+    }
+    tile_of(a, tile_bytes, t);
     const int slot = a.slot_ids[t.b];
     t.alpha = DIAG ? 1.0f : act_ld<BF16>(a.alpha, t.tile);
     t.beta = act_ld<BF16>(a.beta, t.tile);
@@ -157,8 +158,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
         // every tile record is (codes: 1024 bytes per word-step) + r + c
         constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
         constexpr uint32_t r_off = 1024u * (u.m8 + u.m4 + u.m2);
-        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes +
-                       static_cast<uint64_t>(t.h) * (r_off + 1024u);
+        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.off;
         t.codes = reinterpret_cast<uint32_t *>(rec);
         t.rr = reinterpret_cast<const float *>(rec + r_off);
         t.cc = t.rr + 128;
@@ -169,16 +169,6 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
         t.codes = reinterpret_cast<uint32_t *>(rec);
         t.rr = reinterpret_cast<const float *>(rec + t.hi.r_off);
         t.cc = t.rr + P.dk;
-        if constexpr (DV == 128) {
-            switch (t.hi.layout) {
-            case 1: decode_uniform<BF16, DIAG, 8, 4, 0>(a, t, sh); return;
-            case 2: decode_uniform<BF16, DIAG, 4, 2, 2>(a, t, sh); return;
-            case 3: decode_uniform<BF16, DIAG, 16, 0, 0>(a, t, sh); return;
-            case 4: decode_uniform<BF16, DIAG, 0, 8, 0>(a, t, sh); return;
-            case 5: decode_uniform<BF16, DIAG, 0, 0, 4>(a, t, sh); return;
-            default: break;
-            }
-        }
         decode_generic<BF16, DIAG, DV>(a, t, sh);
     }
 }
@@ -316,7 +306,7 @@ hipError_t launch_decode_any(const DecodeArgs &a, int layout, unsigned grid, hip
 
 hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream)
 {
-    const unsigned grid = static_cast<unsigned>(a.batch) * static_cast<unsigned>(a.pool.Hv);
+    const unsigned grid = static_cast<unsigned>(a.batch) * static_cast<unsigned>(a.n_heads);
     if (grid == 0) return hipSuccess;
     if (bf16) return diag ? launch_decode_any<true, true>(a, pool_layout, grid, stream)
                           : launch_decode_any<true, false>(a, pool_layout, grid, stream);

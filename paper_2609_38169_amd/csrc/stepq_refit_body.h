@@ -563,18 +563,19 @@ __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
     __shared__ RefitShared<DV> sh;
     const PoolView &P = a.pool;
     TileCtx t;
-    t.tile = xcd_tile(blockIdx.x, a.batch * P.Hv);
-    t.b = fdiv(t.tile, P.div_hv);
-    t.h = t.tile - t.b * P.Hv;
-    t.hq = fdiv(t.h, P.div_g);
+    uint32_t tile_bytes = 0;
+    if constexpr (DV == 128 && LAYOUT > 0) {
+        constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
+        tile_bytes = 1024u * (u.m8 + u.m4 + u.m2 + 1);
+    }
+    tile_of(a, tile_bytes, t);
     const int slot = a.slot_ids[t.b];
     t.alpha = DIAG ? 1.0f : act_ld<BF16>(a.alpha, t.tile);
     t.beta = act_ld<BF16>(a.beta, t.tile);
     if constexpr (DV == 128 && LAYOUT > 0) {
         constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
         constexpr uint32_t r_off = 1024u * (u.m8 + u.m4 + u.m2);
-        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes +
-                       static_cast<uint64_t>(t.h) * (r_off + 1024u);
+        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.off;
         t.codes = reinterpret_cast<uint32_t *>(rec);
         t.rr = reinterpret_cast<const float *>(rec + r_off);
         t.cc = t.rr + 128;
@@ -585,16 +586,6 @@ __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
         t.codes = reinterpret_cast<uint32_t *>(rec);
         t.rr = reinterpret_cast<const float *>(rec + t.hi.r_off);
         t.cc = t.rr + P.dk;
-        if constexpr (DV == 128) {
-            switch (t.hi.layout) {
-            case 1: refit_uniform<BF16, DIAG, 8, 4, 0, MODE>(a, t, sh); return;
-            case 2: refit_uniform<BF16, DIAG, 4, 2, 2, MODE>(a, t, sh); return;
-            case 3: refit_uniform<BF16, DIAG, 16, 0, 0, MODE>(a, t, sh); return;
-            case 4: refit_uniform<BF16, DIAG, 0, 8, 0, MODE>(a, t, sh); return;
-            case 5: refit_uniform<BF16, DIAG, 0, 0, 4, MODE>(a, t, sh); return;
-            default: break;
-            }
-        }
         refit_generic<BF16, DIAG, DV, MODE>(a, t, sh);
     }
 }
@@ -620,7 +611,7 @@ hipError_t launch_refit_any(const DecodeArgs &a, int layout, unsigned grid, hipS
 template <Refit MODE>
 hipError_t launch_refit_mode(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream)
 {
-    const unsigned grid = static_cast<unsigned>(a.batch) * static_cast<unsigned>(a.pool.Hv);
+    const unsigned grid = static_cast<unsigned>(a.batch) * static_cast<unsigned>(a.n_heads);
     if (grid == 0) return hipSuccess;
     if (bf16) return diag ? launch_refit_any<true, true, MODE>(a, pool_layout, grid, stream)
                           : launch_refit_any<true, false, MODE>(a, pool_layout, grid, stream);
