@@ -161,6 +161,7 @@ struct DecodeShared {
 struct TileCtx {
     int tile, b, h, hq;
     uint32_t off;            // byte offset of the tile in its slot record (uniform bodies)
+    int layout;              // the head's uniform layout (1-based) or 0, when the launch has a head list
     HeadInfo hi;
     uint32_t *codes;
     const float *rr, *cc;
@@ -180,9 +181,11 @@ __device__ __forceinline__ void tile_of(const DecodeArgs &a, uint32_t tile_bytes
         const LaunchHead lh = a.head_list[j];
         t.h = lh.h;
         t.off = lh.tile_off;
+        t.layout = lh.layout;
     } else {
         t.h = j;
         t.off = static_cast<uint32_t>(j) * tile_bytes;
+        t.layout = 0;
     }
     t.tile = t.b * a.pool.Hv + t.h;
     t.hq = fdiv(t.h, a.pool.div_g);
@@ -284,10 +287,11 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-template <int DV>
+// PMAX: the most pivot rows a head of the launch may hold.
+template <int DV, int PMAX = kMaxPivots>
 struct PivotRegs {
     static constexpr int NSL = 256 / (DV / 4);
-    static constexpr int M = (kMaxPivots + NSL - 1) / NSL;
+    static constexpr int M = (PMAX + NSL - 1) / NSL;
     u32x2 v[M];
 };
 
@@ -298,12 +302,12 @@ __device__ __forceinline__ u32x2 *pivot_ptr(const TileCtx &t, int p, int cg)
                                      static_cast<uint32_t>(p) * (2u * DV) + 8u * static_cast<uint32_t>(cg));
 }
 
-template <int DV>
-__device__ __forceinline__ void pivot_load(const TileCtx &t, int slice, int cg, PivotRegs<DV> &pr)
+template <int DV, int PMAX>
+__device__ __forceinline__ void pivot_load(const TileCtx &t, int slice, int cg, PivotRegs<DV, PMAX> &pr)
 {
 #pragma unroll
-    for (int m = 0; m < PivotRegs<DV>::M; ++m) {
-        const int p = slice + PivotRegs<DV>::NSL * m;
+    for (int m = 0; m < PivotRegs<DV, PMAX>::M; ++m) {
+        const int p = slice + PivotRegs<DV, PMAX>::NSL * m;
         pr.v[m] = p < t.hi.n16 ? __builtin_nontemporal_load(pivot_ptr<DV>(t, p, cg)) : u32x2{0u, 0u};
     }
 }
@@ -320,8 +324,8 @@ __device__ __forceinline__ uint32_t pack_halves(float a, float b)
 
 // The pivot rows' share of the column partials, pre-divided by c_j (the
 // column phase multiplies the partials by c_j).
-template <int DV>
-__device__ __forceinline__ void pivot_acc(const TileCtx &t, int slice, int cg, const PivotRegs<DV> &pr,
+template <int DV, int PMAX>
+__device__ __forceinline__ void pivot_acc(const TileCtx &t, int slice, int cg, const PivotRegs<DV, PMAX> &pr,
                                           const DecodeShared<DV> &sh, float (&acK)[4], float (&acQ)[4])
 {
     if (t.hi.n16 == 0) return;
@@ -329,8 +333,8 @@ __device__ __forceinline__ void pivot_acc(const TileCtx &t, int slice, int cg, c
     const float rc[4] = {__builtin_amdgcn_rcpf(c4.x), __builtin_amdgcn_rcpf(c4.y), __builtin_amdgcn_rcpf(c4.z),
                          __builtin_amdgcn_rcpf(c4.w)};
 #pragma unroll
-    for (int m = 0; m < PivotRegs<DV>::M; ++m) {
-        const int p = slice + PivotRegs<DV>::NSL * m;
+    for (int m = 0; m < PivotRegs<DV, PMAX>::M; ++m) {
+        const int p = slice + PivotRegs<DV, PMAX>::NSL * m;
         if (p < t.hi.n16) {
             const float4 k = sh.pvc[p];
             const float sv[4] = {half_lo(pr.v[m].x), half_hi(pr.v[m].x), half_lo(pr.v[m].y), half_hi(pr.v[m].y)};
@@ -346,16 +350,16 @@ __device__ __forceinline__ void pivot_acc(const TileCtx &t, int slice, int cg, c
 
 // New pivot values X_pj = d_i S_pj + beta k_i delta_j in binary16, stored in
 // place (delta_j = bc_j c_j).
-template <int DV>
-__device__ __forceinline__ void pivot_update(const TileCtx &t, int slice, int cg, const PivotRegs<DV> &pr,
+template <int DV, int PMAX>
+__device__ __forceinline__ void pivot_update(const TileCtx &t, int slice, int cg, const PivotRegs<DV, PMAX> &pr,
                                              const DecodeShared<DV> &sh, const float (&bc)[4])
 {
     if (t.hi.n16 == 0) return;
     const float4 c4 = *reinterpret_cast<const float4 *>(&sh.cpiv[4 * cg]);
     const float dl[4] = {bc[0] * c4.x, bc[1] * c4.y, bc[2] * c4.z, bc[3] * c4.w};
 #pragma unroll
-    for (int m = 0; m < PivotRegs<DV>::M; ++m) {
-        const int p = slice + PivotRegs<DV>::NSL * m;
+    for (int m = 0; m < PivotRegs<DV, PMAX>::M; ++m) {
+        const int p = slice + PivotRegs<DV, PMAX>::NSL * m;
         if (p < t.hi.n16) {
             const float4 k = sh.pvc[p];
             const float sv[4] = {half_lo(pr.v[m].x), half_hi(pr.v[m].x), half_lo(pr.v[m].y), half_hi(pr.v[m].y)};

@@ -26,9 +26,14 @@ struct stepq_pool {
     int device = 0;
     int layout = 0;                   // uniform layout of every head, or 0
     // Layout classes of a mixed pool at d_v = 128: heads grouped by their
-    // uniform layout (1-5) or 0 (generic body); one decode launch per class.
-    // Empty when one launch covers every head.
+    // uniform layout (1-5), or the generic heads (0, or kCompactGeneric when
+    // all of them fit the compact body); one decode launch per class.  Empty
+    // when one launch covers every head.
     std::vector<int> cls_layout, cls_off, cls_cnt;
+    // kMixedBase + L when the classes are uniform layout L (1 or 2) plus
+    // compact generic heads: then a decode step (without refit) is one
+    // launch over the whole head list.  0 otherwise.
+    int mixed_code = 0;
     stepq::LaunchHead *d_head_order = nullptr;  // [Hv] heads ordered by class, device
 };
 
@@ -267,11 +272,27 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
         }
         std::sort(cls.begin(), cls.end());
         for (const auto &c : cls) {
-            p->cls_layout.push_back(c.second);
+            int code = c.second;
+            if (code == 0) {
+                // the generic heads take the compact body when all of them fit it
+                bool fits = true;
+                for (const HeadInfo &hi : p->heads)
+                    if (hi.layout == 0 && (hi.groups > static_cast<uint32_t>(stepq::kCompactGroups) ||
+                                           hi.n16 > stepq::kCompactPivots))
+                        fits = false;
+                if (fits) code = stepq::kCompactGeneric;
+            }
+            p->cls_layout.push_back(code);
             p->cls_off.push_back(static_cast<int>(order.size()));
             p->cls_cnt.push_back(-c.first);
             for (int h = 0; h < p->Hv; ++h)
-                if (static_cast<int>(p->heads[h].layout) == c.second) order.push_back({h, p->heads[h].tile_off});
+                if (static_cast<int>(p->heads[h].layout) == c.second)
+                    order.push_back({h, p->heads[h].tile_off, static_cast<int32_t>(p->heads[h].layout), 0});
+        }
+        if (p->cls_layout.size() == 2) {
+            const int a0 = p->cls_layout[0], a1 = p->cls_layout[1];
+            const int L = a0 == stepq::kCompactGeneric ? a1 : (a1 == stepq::kCompactGeneric ? a0 : 0);
+            if (L == 1 || L == 2) p->mixed_code = stepq::kMixedBase + L;
         }
         e = hipMalloc(reinterpret_cast<void **>(&p->d_head_order), sizeof(stepq::LaunchHead) * order.size());
         if (e == hipSuccess)
@@ -354,7 +375,13 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
                                                  : stepq::launch_decode(a, bf16, diag, layout, s);
     };
     hipError_t e = hipSuccess;
-    if (p->cls_layout.empty()) {
+    if (p->mixed_code != 0 && !(flags & (STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX))) {
+        // uniform heads and compact generic heads share one launch
+        a.head_list = p->d_head_order;
+        a.n_heads = p->Hv;
+        a.div_heads = fast_div(static_cast<uint32_t>(p->Hv));
+        e = launch(p->mixed_code);
+    } else if (p->cls_layout.empty()) {
         a.head_list = nullptr;
         a.n_heads = p->Hv;
         a.div_heads = fast_div(static_cast<uint32_t>(p->Hv));

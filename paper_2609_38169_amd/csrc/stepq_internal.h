@@ -44,6 +44,14 @@ constexpr int kNumUniformLayouts = sizeof(kUniformLayouts) / sizeof(kUniformLayo
 constexpr int kMaxDk = 128;
 constexpr int kSlotTable = kMaxDk + 4;
 constexpr int kMaxPivots = 32;    // FP16 pivot rows per head
+// The compact generic decode body (layout code -1, d_v = 128) holds at most
+// this many row groups and pivot rows per head, and fits 8 waves per SIMD.
+constexpr int kCompactGeneric = -1;
+// Layout code kMixedBase + L (L = 1, 2): heads of uniform layout L and
+// compact generic heads in one decode launch.
+constexpr int kMixedBase = 8;
+constexpr int kCompactGroups = 96;
+constexpr int kCompactPivots = 8;
 
 // n / d for 0 <= n < 2^31 by multiply-high (Granlund-Montgomery), with the
 // constants prepared on the host so that uniform quotients stay scalar.
@@ -67,6 +75,8 @@ struct PoolView {
 struct LaunchHead {
     int32_t h;
     uint32_t tile_off;
+    int32_t layout;          // the head's uniform layout (1-based), or 0
+    int32_t pad;
 };
 
 struct DecodeArgs {
@@ -101,8 +111,11 @@ struct TileArgs {
 };
 
 // pool_layout: the uniform layout (1-based) shared by every head of the
-// launch (a.head_list), or 0 for the generic body (irregular row-width
-// mixes, FP16 pivot rows, d_v = 64).
+// launch (a.head_list), 0 for the generic body (irregular row-width mixes,
+// FP16 pivot rows, d_v = 64), kCompactGeneric when every head of the launch
+// fits the compact generic body's bounds, or kMixedBase + L (decode step
+// only) for uniform layout-L heads mixed with compact generic heads.  The
+// refitting steps take their generic body for kCompactGeneric.
 // diag: a.alpha holds the channel-wise gate [batch][Hv][d_k] instead of the
 // scalar gate [batch][Hv].
 hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);

@@ -74,13 +74,13 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
 }
 
 // Any row-width mix and d_v: the class of each word-step is looked up at run
-// time and the words are unpacked again for the second pass.
-template <bool BF16, bool DIAG, int DV>
+// time and the words are unpacked again for the second pass.  MMAX word-steps
+// (row groups / NSL) and PMAX pivot rows per head at most.
+template <bool BF16, bool DIAG, int DV, int MMAX, int PMAX>
 __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCtx &t, DecodeShared<DV> &sh)
 {
     constexpr int CG = DV / 4;
     constexpr int NSL = 256 / CG;
-    constexpr int MMAX = kMaxDk * CG / 256;
     const int tid = threadIdx.x;
     const int cg = tid % CG, slice = tid / CG;
     const int ngroups = static_cast<int>(t.hi.groups);
@@ -91,8 +91,8 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
         const int g = slice + NSL * m;
         w[m] = g < ngroups ? cw.load(tid + 256 * m) : 0u;
     }
-    PivotRegs<DV> pr;
-    pivot_load<DV>(t, slice, cg, pr);
+    PivotRegs<DV, PMAX> pr;
+    pivot_load(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
     const float kappa = row_constants<DIAG, DV>(t.hi, a.pool.dk, t.alpha, t.beta, op, sh);
 
@@ -108,12 +108,12 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
             else unpack_acc<2>(w[m], sh.kq, gr.x0, U, acK, acQ);
         }
     }
-    pivot_acc<DV>(t, slice, cg, pr, sh, acK, acQ);
+    pivot_acc(t, slice, cg, pr, sh, acK, acQ);
     column_phase<DV>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, acK, acQ, op.c, op.v);
 
     const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
-    pivot_update<DV>(t, slice, cg, pr, sh, bc);
+    pivot_update(t, slice, cg, pr, sh, bc);
 #pragma unroll
     for (int m = 0; m < MMAX; ++m) {
         const int g = slice + NSL * m;
@@ -135,18 +135,49 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
     }
 }
 
-// LAYOUT > 0: every head of the launch has uniform layout LAYOUT (the host
-// launches each layout class of a pool separately), so the kernel holds
-// only that body and its register budget.  LAYOUT == 0: the generic body
-// (irregular row-width mixes, FP16 pivot rows, d_v = 64).
+template <bool BF16, bool DIAG, int L>
+__device__ __forceinline__ void run_uniform(const DecodeArgs &a, TileCtx &t, int slot, DecodeShared<128> &sh)
+{
+    // every tile record of layout L is (codes: 1024 bytes per word-step) + r + c
+    constexpr UniformLayout u = kUniformLayouts[L - 1];
+    constexpr uint32_t r_off = 1024u * (u.m8 + u.m4 + u.m2);
+    uint8_t *rec = a.pool.base + static_cast<uint64_t>(slot) * a.pool.slot_bytes + t.off;
+    t.codes = reinterpret_cast<uint32_t *>(rec);
+    t.rr = reinterpret_cast<const float *>(rec + r_off);
+    t.cc = t.rr + 128;
+    decode_uniform<BF16, DIAG, u.m8, u.m4, u.m2>(a, t, sh);
+}
+
+template <bool BF16, bool DIAG, int DV, bool COMPACT>
+__device__ __forceinline__ void run_generic(const DecodeArgs &a, TileCtx &t, int slot, DecodeShared<DV> &sh)
+{
+    const PoolView &P = a.pool;
+    t.hi = P.heads[t.h];
+    uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.hi.tile_off;
+    t.codes = reinterpret_cast<uint32_t *>(rec);
+    t.rr = reinterpret_cast<const float *>(rec + t.hi.r_off);
+    t.cc = t.rr + P.dk;
+    constexpr int full_m = kMaxDk * (DV / 4) / 256;
+    decode_generic<BF16, DIAG, DV, COMPACT ? kCompactGroups / 8 : full_m, COMPACT ? kCompactPivots : kMaxPivots>(
+        a, t, sh);
+}
+
+// LAYOUT in 1 .. kNumUniformLayouts: every head of the launch has that
+// uniform layout (the host launches each layout class of a pool
+// separately), so the kernel holds only that body and its register budget.
+// LAYOUT == 0: the generic body (irregular row-width mixes, FP16 pivot
+// rows, d_v = 64).  LAYOUT == kCompactGeneric: the generic body for heads of
+// at most kCompactGroups row groups and kCompactPivots pivot rows (d_v =
+// 128), in fewer registers.  LAYOUT == kMixedBase + L: heads of uniform
+// layout L and compact generic heads in one launch, told apart by the head
+// list (both bodies fit the same register budget).
 template <int DV, bool BF16, int LAYOUT, bool DIAG>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 {
     __shared__ DecodeShared<DV> sh;
-    const PoolView &P = a.pool;
     TileCtx t;
     uint32_t tile_bytes = 0;
-    if constexpr (DV == 128 && LAYOUT > 0) {
+    if constexpr (DV == 128 && LAYOUT > 0 && LAYOUT <= kNumUniformLayouts) {
         constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
         tile_bytes = 1024u * (u.m8 + u.m4 + u.m2 + 1);
     }
@@ -154,22 +185,13 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
     const int slot = a.slot_ids[t.b];
     t.alpha = DIAG ? 1.0f : act_ld<BF16>(a.alpha, t.tile);
     t.beta = act_ld<BF16>(a.beta, t.tile);
-    if constexpr (DV == 128 && LAYOUT > 0) {
-        // every tile record is (codes: 1024 bytes per word-step) + r + c
-        constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
-        constexpr uint32_t r_off = 1024u * (u.m8 + u.m4 + u.m2);
-        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.off;
-        t.codes = reinterpret_cast<uint32_t *>(rec);
-        t.rr = reinterpret_cast<const float *>(rec + r_off);
-        t.cc = t.rr + 128;
-        decode_uniform<BF16, DIAG, u.m8, u.m4, u.m2>(a, t, sh);
+    if constexpr (DV == 128 && LAYOUT > 0 && LAYOUT <= kNumUniformLayouts) {
+        run_uniform<BF16, DIAG, LAYOUT>(a, t, slot, sh);
+    } else if constexpr (DV == 128 && LAYOUT > kMixedBase) {
+        if (t.layout == LAYOUT - kMixedBase) run_uniform<BF16, DIAG, LAYOUT - kMixedBase>(a, t, slot, sh);
+        else run_generic<BF16, DIAG, 128, true>(a, t, slot, sh);
     } else {
-        t.hi = P.heads[t.h];
-        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.hi.tile_off;
-        t.codes = reinterpret_cast<uint32_t *>(rec);
-        t.rr = reinterpret_cast<const float *>(rec + t.hi.r_off);
-        t.cc = t.rr + P.dk;
-        decode_generic<BF16, DIAG, DV>(a, t, sh);
+        run_generic<BF16, DIAG, DV, DV == 128 && LAYOUT == kCompactGeneric>(a, t, slot, sh);
     }
 }
 
@@ -289,6 +311,15 @@ hipError_t launch_decode_128(const DecodeArgs &a, int layout, unsigned grid, hip
     case 3: hipLaunchKernelGGL((decode_kernel<128, BF16, 3, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
     case 4: hipLaunchKernelGGL((decode_kernel<128, BF16, 4, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
     case 5: hipLaunchKernelGGL((decode_kernel<128, BF16, 5, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
+    case kCompactGeneric:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kCompactGeneric, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kMixedBase + 1:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kMixedBase + 1, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kMixedBase + 2:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kMixedBase + 2, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
     default: hipLaunchKernelGGL((decode_kernel<128, BF16, 0, DIAG>), dim3(grid), dim3(256), 0, s, a); break;
     }
     return hipGetLastError();

@@ -441,7 +441,7 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
         w[m] = g < ngroups ? cw.load(tid + 256 * m) : 0u;
     }
     PivotRegs<DV> pr;
-    pivot_load<DV>(t, slice, cg, pr);
+    pivot_load(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
     if (tid < DV) sh.ccol[tid] = op.c;
     if (tid < dk) sh.wphys[tid] = a.pool.roww[t.h * dk + tid];
@@ -452,13 +452,13 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
         float U[16];
         unpack_acc<decltype(bw)::value>(w[m], sh.d.kq, gr.x0, U, acK, acQ);
     });
-    pivot_acc<DV>(t, slice, cg, pr, sh.d, acK, acQ);
+    pivot_acc(t, slice, cg, pr, sh.d, acK, acQ);
     column_phase<DV>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh.d, kappa, acK, acQ, op.c, op.v);
 
     float bc[4], cc[4];
     ld4(&sh.d.bcol[4 * cg], bc);
     ld4(&sh.ccol[4 * cg], cc);
-    pivot_update<DV>(t, slice, cg, pr, sh.d, bc);      // pivot rows take no part in the fits
+    pivot_update(t, slice, cg, pr, sh.d, bc);      // pivot rows take no part in the fits
 
     // pass 1: row partials straight to LDS (each (lane, slot) has one writer)
     each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {

@@ -1,9 +1,11 @@
-"""GPU parity on pools whose heads span every compiled row-width layout and
-the generic body at once.  Such a pool is advanced with one decode launch
-per layout class (each head's tile found through the launch's head list),
-so every class must address its own heads' tiles inside slot records whose
-tiles differ in size.  Frozen, refit and row-absmax steps, GDN and KDA
-gates, against the fp64 oracle through the C ABI."""
+"""GPU parity on pools whose heads differ in row-width layout.  A pool
+spanning every compiled layout and the generic body is advanced with one
+launch per layout class (each head's tile found through the launch's head
+list), so every class must address its own heads' tiles inside slot records
+whose tiles differ in size.  A pool of one uniform layout plus generic heads
+takes a single decode launch that holds both bodies.  Frozen, refit and
+row-absmax steps, GDN and KDA gates, against the fp64 oracle through the
+C ABI."""
 import numpy as np
 import pytest
 import torch
@@ -15,19 +17,25 @@ import _parity as PT
 pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda", 0)
 
-# per head: the five uniform layouts (rows per width), a generic mix, and
-# layouts 2 and 1 again, so that classes hold non-adjacent heads
-MIXES = [{8: 64, 4: 64}, {8: 32, 4: 32, 2: 64}, {8: 128}, {4: 128}, {2: 128}, None,
-         {8: 32, 4: 32, 2: 64}, {8: 64, 4: 64}]
+L1, L2 = {8: 64, 4: 64}, {8: 32, 4: 32, 2: 64}
+# rows per width of each head (None: a random {2,4,8} map, the generic body)
+MIXES = {
+    # the five uniform layouts, a generic mix, then layouts 2 and 1 again, so
+    # that classes hold non-adjacent heads: one launch per class
+    "all": [L1, L2, {8: 128}, {4: 128}, {2: 128}, None, L2, L1],
+    # one uniform layout plus generic heads: one decode launch for both
+    "l1_generic": [L1, None, L1, L1, None, L1, L1, L1],
+    "l2_generic": [None, L2, L2, L2, L2, L2, L2, None],
+}
 
 
 def _say(*a):
     print(*a, flush=True)
 
 
-def _bits(rng):
+def _bits(rng, mixes):
     rows = []
-    for m in MIXES:
+    for m in mixes:
         if m is None:
             rows.append(rng.choice([2, 4, 8], size=128).astype(np.uint8))
         else:
@@ -37,11 +45,13 @@ def _bits(rng):
 
 @pytest.mark.parametrize("mode", ["frozen", "refit", "row_absmax"])
 @pytest.mark.parametrize("kda", [False, True])
-def test_layout_classes_one_step(mode, kda):
-    Hv, Hqk, dk, dv, n_slots = len(MIXES), 4, 128, 128, 6
-    rng = np.random.default_rng(900 + 10 * ["frozen", "refit", "row_absmax"].index(mode) + int(kda))
-    bits = _bits(rng)
-    _say(f"layout classes: mode={mode} kda={kda} Hv={Hv} n_slots={n_slots}")
+@pytest.mark.parametrize("mix", list(MIXES))
+def test_layout_classes_one_step(mix, mode, kda):
+    Hv, Hqk, dk, dv, n_slots = len(MIXES[mix]), 4, 128, 128, 6
+    rng = np.random.default_rng(900 + 100 * list(MIXES).index(mix) + 10 * ["frozen", "refit", "row_absmax"].index(mode)
+                                + int(kda))
+    bits = _bits(rng, MIXES[mix])
+    _say(f"layout classes {mix}: mode={mode} kda={kda} Hv={Hv} n_slots={n_slots}")
     S = (rng.standard_normal((n_slots, Hv, dk, dv)) * 0.05).astype(np.float32)
     r, c = oracle.fit_absmax(S.reshape(-1, dk, dv))
     tb_all = np.broadcast_to(bits[None], (n_slots,) + bits.shape).reshape(-1, dk)
@@ -79,7 +89,7 @@ def test_layout_classes_one_step(mode, kda):
     vv, bb = f32(v).reshape(-1, dv), f32(be).reshape(-1)
     gt = f32(gate).reshape((-1, dk) if kda else (-1,))
     tiles = (sel[:, None] * Hv + np.arange(Hv)[None]).reshape(-1)
-    what = f"layout classes {mode} kda={kda}"
+    what = f"layout classes {mix} {mode} kda={kda}"
     gcodes = got.reshape(-1, dk, dv)[tiles]
     if mode == "frozen":
         new, o_ref, y = oracle.decode_step(codes[tiles], r[tiles], c[tiles], tb_all[tiles], qq, kk, vv, gt, bb,
