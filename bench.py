@@ -269,8 +269,9 @@ def main():
     mode = True if args.refit else ("row_absmax" if args.row_absmax else False)
     rescale = bool(mode)          # the step writes the scales back
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (each (request, head) tile is "
-              "independent; see the sharding note in DESIGN.md). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (each (request, head) tile is "
+              "independent, so heads or requests shard across GPUs with no exchange). Run with --gpus 1.",
+              file=sys.stderr)
         sys.exit(2)
 
     import dataclasses
