@@ -80,11 +80,14 @@ def kernel_hash(mode=False) -> str:
 def state_bytes_per_tile(bits_row, d_k, d_v, refit: bool = False) -> int:
     """Algorithmic bytes one tile update moves: its codes (and binary16
     pivot rows) read and written once, its fp32 row and column scales read
-    once (and written once more when the step refits them)."""
+    once (and written once more when the step refits them).  A head held
+    entirely in FP16 has no scales to read or fit."""
     import numpy as np
     n16 = int(np.sum(bits_row == 16))
     n8 = int(np.sum(bits_row == 8)); n4 = int(np.sum(bits_row == 4)); n2 = int(np.sum(bits_row == 2))
     code_bytes = (16 * n16 + 8 * n8 + 4 * n4 + 2 * n2) * d_v // 8
+    if n16 == d_k:
+        return 2 * code_bytes
     return 2 * code_bytes + (2 if refit else 1) * 4 * (d_k + d_v)
 
 
@@ -160,6 +163,10 @@ def pool_case(args, w, mode, dev):
         # FP16 pivot rows: a seeded quarter of the heads keep 1-3 key rows in binary16
         bits = bits.copy()
         bits[W.pivot_mask_draw(w).numpy()] = 16
+    if args.fp16_heads:
+        # whole FP16 heads: a seeded choice of value heads keeps every row in binary16
+        bits = bits.copy()
+        bits[W.pivot_head_draw(w, 0, args.fp16_heads).numpy()] = 16
     log(f"building the {w.n_slots}-slot pool")
     pool = build_pool(w, device=dev, bits=bits)
     subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
@@ -180,8 +187,11 @@ def pool_case(args, w, mode, dev):
         prepared[key]()
 
     mix = {"pool_b512": "6-bit mixed {4,8}", "pool_4bit": "4-bit mixed {2,4,8}, heavy-tailed states"}[w.name]
-    if args.pivots:
-        mix += f", {int((bits == 16).sum())} FP16 pivot rows in {int((bits == 16).any(1).sum())} of {w.n_v_heads} heads"
+    if args.pivots or args.fp16_heads:
+        full = int((bits == 16).all(1).sum())
+        rows = int((bits == 16).sum()) - full * w.d_k
+        mix += f", {rows} FP16 pivot rows in {int(((bits == 16).any(1) & ~(bits == 16).all(1)).sum())} heads" if rows else ""
+        mix += f", {full} of {w.n_v_heads} heads entirely FP16" if full else ""
     return Case(w=w, bits=bits, step=step, launches_per_step=1, n_subsets=len(subsets), keep=(pool, inputs, o),
                 tiles_per_step=w.batch * w.n_v_heads, layers=1,
                 workload=f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
@@ -258,13 +268,15 @@ def main():
                     help="requantize as the row-wise absmax INT-b baseline (row factors refit, column factors 1)")
     ap.add_argument("--pivots", action="store_true",
                     help="a seeded quarter of the heads keep 1-3 FP16 pivot rows (pool workloads)")
+    ap.add_argument("--fp16-heads", type=int, default=0,
+                    help="this many seeded value heads are kept entirely in FP16 (pool workloads)")
     args = ap.parse_args()
 
     if args.refit and args.row_absmax:
         print("--refit and --row-absmax exclude each other", file=sys.stderr)
         sys.exit(2)
-    if args.pivots and args.workload == "stack48":
-        print("--pivots applies to the single-layer pool workloads", file=sys.stderr)
+    if (args.pivots or args.fp16_heads) and args.workload == "stack48":
+        print("--pivots and --fp16-heads apply to the single-layer pool workloads", file=sys.stderr)
         sys.exit(2)
     mode = True if args.refit else ("row_absmax" if args.row_absmax else False)
     rescale = bool(mode)          # the step writes the scales back
@@ -358,7 +370,8 @@ def main():
     state_gbps = launch_bytes * LPS * K / (total_ms * 1e-3) / 1e9
     kern_name = ("refit_kernel" if rescale else "decode_kernel") + ("<128, bf16, kda" if args.kda else "<128, bf16")
     kern_name += {True: ", dual axis", "row_absmax": ", row absmax", False: ""}[mode]
-    kern_name += (", heads with pivots on the generic body>" if args.pivots else ">")
+    kern_name += (", heads with pivots on the generic body" if args.pivots else "")
+    kern_name += (", FP16 heads" if args.fp16_heads else "") + ">"
 
     line = {
         "metric": METRIC,
@@ -385,7 +398,7 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic_entry(mode, args.kda, w.name, args.pivots),
+            "traffic": traffic_entry(mode, args.kda, w.name, args.pivots) if not args.fp16_heads else None,
             "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Top/s", "frac": valu_tops / VALU_PEAK_TOPS,
                      "ops_per_element": OPS_PER_ELEMENT[mode]},
             "kernel": kern_name,

@@ -42,7 +42,10 @@
  *
  *  - Physical row order: the pivot rows in increasing logical row index, then
  *    the 8-bit rows, the 4-bit rows and the 2-bit rows, each the same way.
- *    n16, n8, n4, n2 = row counts; n16 <= 32.
+ *    n16, n8, n4, n2 = row counts; n16 <= 32, or n16 = d_k = d_v = 128: a
+ *    head held entirely in FP16 (Table C1 keeps whole heads of the GDN model
+ *    as pivots).  Such a tile is its 32 KiB pivot region plus the r and c
+ *    slots, which stay unused (the paper's serving layout omits them).
  *  - Row groups: each group holds 8/b physical integer rows of one width b --
  *    one 8-bit row, two 4-bit rows or four 2-bit rows -- filled in physical
  *    order.  A width's last group may have empty slots.  Groups are ordered

@@ -31,8 +31,8 @@ struct stepq_pool {
     // when one launch covers every head.
     std::vector<int> cls_layout, cls_off, cls_cnt;
     // kMixedBase + L when the classes are uniform layout L (1 or 2) plus
-    // compact generic heads: then a decode step (without refit) is one
-    // launch over the whole head list.  0 otherwise.
+    // compact generic and/or whole FP16 heads: then a decode step (without
+    // refit) is one launch over the whole head list.  0 otherwise.
     int mixed_code = 0;
     stepq::LaunchHead *d_head_order = nullptr;  // [Hv] heads ordered by class, device
 };
@@ -80,7 +80,9 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
             else if (b[i] == 2) ++n2;
             else return fail(STEPQ_E_INVALID, "row_bits entries must be 2, 4, 8 or 16");
         }
-        if (n16 > stepq::kMaxPivots) return fail(STEPQ_E_UNSUPPORTED, "at most 32 pivot (16) rows per head");
+        const bool f16_head = n16 == dk && dk == 128 && dv == 128;   // a whole FP16 head
+        if (n16 > stepq::kMaxPivots && !f16_head)
+            return fail(STEPQ_E_UNSUPPORTED, "at most 32 pivot (16) rows per head, or all rows of a 128x128 head");
         int p = 0;
         for (int width : {16, 8, 4, 2})
             for (int i = 0; i < dk; ++i)
@@ -102,6 +104,7 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
                 const stepq::UniformLayout &u = stepq::kUniformLayouts[L];
                 if (u.m8 * 8 == hi.g8 && u.m4 * 8 == hi.g4 && u.m2 * 8 == hi.g2) hi.layout = L + 1;
             }
+        if (f16_head) hi.layout = stepq::kF16HeadLayout;
         const size_t creg = round128(static_cast<size_t>(hi.groups) * dv);
         const size_t preg = round128(static_cast<size_t>(n16) * 2u * dv);
         const size_t tb = round128(creg + preg + 4u * static_cast<size_t>(dk) + 4u * static_cast<size_t>(dv));
@@ -109,13 +112,16 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
         hi.r_off = static_cast<uint32_t>(creg + preg);
         hi.tile_bytes = static_cast<uint32_t>(tb);
         hi.tile_off = static_cast<uint32_t>(off);
-        if (hi.layout > 0) {
-            // the compiled bodies address codes, r and c from these sizes
+        // the compiled bodies address codes (or FP16 values), r and c from these sizes
+        if (hi.layout > 0 && static_cast<int>(hi.layout) <= stepq::kNumUniformLayouts) {
             const stepq::UniformLayout &u = stepq::kUniformLayouts[hi.layout - 1];
             const uint32_t m = static_cast<uint32_t>(u.m8 + u.m4 + u.m2);
             if (hi.r_off != 1024u * m || hi.tile_bytes != 1024u * (m + 1))
                 return fail(STEPQ_E_INVALID, "internal: uniform head layout does not match its tile size");
         }
+        if (static_cast<int>(hi.layout) == stepq::kF16HeadLayout &&
+            (hi.piv_off != 0 || hi.r_off != 128u * 256u || hi.tile_bytes != 128u * 256u + 1024u))
+            return fail(STEPQ_E_INVALID, "internal: FP16 head layout does not match its tile size");
         off += tb;
     }
     *slot_bytes = off;
@@ -265,7 +271,7 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
         // one class per layout present; larger classes are launched first
         std::vector<stepq::LaunchHead> order;
         std::vector<std::pair<int, int>> cls;   // (-count, layout)
-        for (int L = 0; L <= stepq::kNumUniformLayouts; ++L) {
+        for (int L = 0; L <= stepq::kF16HeadLayout; ++L) {
             int n = 0;
             for (const HeadInfo &hi : p->heads) n += static_cast<int>(hi.layout) == L;
             if (n > 0) cls.emplace_back(-n, L);
@@ -289,11 +295,22 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
                 if (static_cast<int>(p->heads[h].layout) == c.second)
                     order.push_back({h, p->heads[h].tile_off, static_cast<int32_t>(p->heads[h].layout), 0});
         }
-        if (p->cls_layout.size() == 2) {
-            const int a0 = p->cls_layout[0], a1 = p->cls_layout[1];
-            const int L = a0 == stepq::kCompactGeneric ? a1 : (a1 == stepq::kCompactGeneric ? a0 : 0);
-            if (L == 1 || L == 2) p->mixed_code = stepq::kMixedBase + L;
+        // one uniform class of layout 1 or 2 whose other classes are compact
+        // generic or whole FP16 heads: a decode step is one combined launch
+        int L = 0, others = 0;
+        bool fits = true, f16 = false;
+        for (int code : p->cls_layout) {
+            if (code == 1 || code == 2) {
+                if (L != 0) fits = false;
+                L = code;
+            } else if (code == stepq::kCompactGeneric || code == stepq::kF16HeadLayout) {
+                ++others;
+                f16 = f16 || code == stepq::kF16HeadLayout;
+            } else {
+                fits = false;
+            }
         }
+        if (fits && L != 0 && others > 0) p->mixed_code = (f16 ? stepq::kMixedF16Base : stepq::kMixedBase) + L;
         e = hipMalloc(reinterpret_cast<void **>(&p->d_head_order), sizeof(stepq::LaunchHead) * order.size());
         if (e == hipSuccess)
             e = hipMemcpy(p->d_head_order, order.data(), sizeof(stepq::LaunchHead) * order.size(),
@@ -369,7 +386,15 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     a.batch = batch;
     const bool diag = (flags & STEPQ_STEP_KDA_GATE) != 0;
     const bool bf16 = act_dtype == STEPQ_BF16;
+    a.f16_c_one = 0;
     auto launch = [&](int layout) {
+        if (layout == stepq::kF16HeadLayout) {
+            // whole FP16 heads: no integer rows to fit, so every mode is the same update
+            a.f16_c_one = (flags & STEPQ_STEP_ROW_ABSMAX) ? 1 : 0;
+            const hipError_t r = stepq::launch_decode(a, bf16, diag, layout, s);
+            a.f16_c_one = 0;
+            return r;
+        }
         return (flags & STEPQ_STEP_REFIT)        ? stepq::launch_decode_refit(a, bf16, diag, layout, s)
                : (flags & STEPQ_STEP_ROW_ABSMAX) ? stepq::launch_decode_rowmax(a, bf16, diag, layout, s)
                                                  : stepq::launch_decode(a, bf16, diag, layout, s);

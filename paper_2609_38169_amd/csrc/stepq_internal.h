@@ -36,6 +36,10 @@ constexpr UniformLayout kUniformLayouts[] = {
     {0, 0, 4},    // all rows @2
 };
 constexpr int kNumUniformLayouts = sizeof(kUniformLayouts) / sizeof(kUniformLayouts[0]);
+// Layout code of a head whose every row is an FP16 pivot (d_k = d_v = 128):
+// its tile is the pivot region (32 KiB of binary16 values) and the unused r
+// and c slots.
+constexpr int kF16HeadLayout = kNumUniformLayouts + 1;
 
 // Row-constant table index space: 8-bit rows, then the two slots of every
 // 4-bit group, then the four slots of every 2-bit group (empty slots
@@ -48,8 +52,10 @@ constexpr int kMaxPivots = 32;    // FP16 pivot rows per head
 // this many row groups and pivot rows per head, and fits 8 waves per SIMD.
 constexpr int kCompactGeneric = -1;
 // Layout code kMixedBase + L (L = 1, 2): heads of uniform layout L and
-// compact generic heads in one decode launch.
+// compact generic heads in one decode launch; kMixedF16Base + L: the same
+// with whole FP16 heads too (one more body, a few more registers).
 constexpr int kMixedBase = 8;
+constexpr int kMixedF16Base = 16;
 constexpr int kCompactGroups = 96;
 constexpr int kCompactPivots = 8;
 
@@ -91,6 +97,9 @@ struct DecodeArgs {
     const LaunchHead *head_list;
     int32_t n_heads;
     FastDiv div_heads;       // divide by n_heads
+    // Whole FP16 heads in a row-absmax step: their column factors become 1
+    // (the baseline's c' = 1); their values update as in every other mode.
+    int32_t f16_c_one;
 };
 
 enum class TileOp : int { Load = 0, Import = 1, Export = 2, Dequant = 3, ExportPivots = 4, ImportPivots = 5 };
@@ -113,8 +122,9 @@ struct TileArgs {
 // pool_layout: the uniform layout (1-based) shared by every head of the
 // launch (a.head_list), 0 for the generic body (irregular row-width mixes,
 // FP16 pivot rows, d_v = 64), kCompactGeneric when every head of the launch
-// fits the compact generic body's bounds, or kMixedBase + L (decode step
-// only) for uniform layout-L heads mixed with compact generic heads.  The
+// fits the compact generic body's bounds, kF16HeadLayout for whole FP16
+// heads, or kMixedBase + L / kMixedF16Base + L (decode step only) for
+// uniform layout-L heads mixed with compact generic (and whole FP16) heads.  The
 // refitting steps take their generic body for kCompactGeneric.
 // diag: a.alpha holds the channel-wise gate [batch][Hv][d_k] instead of the
 // scalar gate [batch][Hv].

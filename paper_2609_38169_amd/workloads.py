@@ -96,7 +96,7 @@ def _mix(*parts: int) -> int:
 
 _STREAM = {"init": 1, "q": 2, "k": 3, "v": 4, "alpha": 5, "beta": 6,
            "bits": 7, "calib": 8, "slots": 9, "gain_r": 10, "gain_c": 11, "kda": 12,
-           "roww": 13, "pivots": 14}
+           "roww": 13, "pivots": 14, "pivot_heads": 15}
 
 
 def _gen(device, w: Workload, layer: int, step: int, stream: str, chunk: int = 0) -> torch.Generator:
@@ -202,6 +202,16 @@ def pivot_mask_draw(w: Workload, layer: int = 0, head_frac: float = 0.25, max_ro
     for h in range(w.n_v_heads):
         if pick[h]:
             mask[h, torch.randperm(w.d_k, generator=g)[: int(count[h])]] = True
+    return mask
+
+
+def pivot_head_draw(w: Workload, layer: int = 0, count: int = 1) -> torch.Tensor:
+    """Synthetic FP16 pivot heads, bool [Hv]: a seeded choice of ``count``
+    value heads kept entirely in FP16 (the paper keeps whole heads of its
+    GDN model in FP16)."""
+    g = _gen("cpu", w, layer, 0, "pivot_heads")
+    mask = torch.zeros(w.n_v_heads, dtype=torch.bool)
+    mask[torch.randperm(w.n_v_heads, generator=g)[:count]] = True
     return mask
 
 

@@ -29,7 +29,18 @@ def _cases():
             if h % 2 == 0 or Hv == 1:
                 bits[h, rng.choice(dk, size=min(npiv, dk), replace=False)] = 16
         cases.append((Hv, Hqk, dk, dv, n_slots, bits))
+    # whole FP16 heads (the paper's Qwen pivots are entire heads): every other
+    # head of random widths, then one FP16 head beside 64@8 + 64@4 heads
+    bits = rng.choice([2, 4, 8], size=(4, 128)).astype(np.uint8)
+    bits[0::2] = 16
+    cases.append((4, 2, 128, 128, 3, bits))
+    bits = np.stack([rng.permutation(np.repeat(np.array([8, 4], np.uint8), 64)) for _ in range(4)])
+    bits[1] = 16
+    cases.append((4, 4, 128, 128, 3, bits))
     return cases
+
+
+N_CASES = 7
 
 
 def _state(case, seed):
@@ -53,7 +64,7 @@ def _pool_with(case, codes, pv, r, c):
     return pool, ids
 
 
-@pytest.mark.parametrize("case", range(5))
+@pytest.mark.parametrize("case", range(N_CASES))
 def test_pivot_import_export_and_image(case):
     Hv, Hqk, dk, dv, n_slots, bits = _cases()[case]
     _say(f"pivot layout case {case}: Hv={Hv} dk={dk} dv={dv} pivots/head={list((bits == 16).sum(1))}")
@@ -100,7 +111,7 @@ def test_pivot_boundary_pack(case):
 
 @pytest.mark.parametrize("mode", [False, True, "row_absmax"])
 @pytest.mark.parametrize("kda", [False, True])
-@pytest.mark.parametrize("case", range(5))
+@pytest.mark.parametrize("case", range(N_CASES))
 def test_pivot_decode_step(case, kda, mode):
     Hv, Hqk, dk, dv, n_slots, bits = _cases()[case]
     _say(f"pivot decode case {case} kda={kda} mode={mode}")
@@ -171,6 +182,18 @@ def test_pivot_pool_b512_lockstep(mode):
     bits = row_bits(w)
     bits[W.pivot_mask_draw(w).numpy()] = 16
     PT.lockstep_run(w, 6, np.array([0, 200, 511]), DEV, refit=mode, say=_say, bits=bits)
+
+
+@pytest.mark.parametrize("mode", [False, True, "row_absmax"])
+def test_fp16_heads_pool_b512_lockstep(mode):
+    """The B=512 pool with two value heads kept entirely in FP16 (the
+    frozen step takes one launch holding the 6-bit, FP16-head and generic
+    bodies; the refitting steps one launch per class), sampled slots
+    compared lockstep."""
+    w = W.workload(2)
+    bits = row_bits(w)
+    bits[W.pivot_head_draw(w, 0, 2).numpy()] = 16
+    PT.lockstep_run(w, 4, np.array([0, 311, 511]), DEV, refit=mode, say=_say, bits=bits)
 
 
 def test_calibrated_map_runs_lockstep():

@@ -52,10 +52,36 @@ def test_ragged_layout_sizes():
         assert sb == oracle.slot_bytes(bits, dv) and pb == 3 * sb
 
 
+def test_whole_fp16_head_layout():
+    """A 128x128 head whose every row is an FP16 pivot is accepted (the
+    paper's Qwen pivots are whole heads): its tile is 32 KiB of binary16
+    values plus the unused r and c slots, as the oracle's packer lays it out.
+    Between 33 and 127 pivot rows a head is refused."""
+    rng = np.random.default_rng(3)
+    bits = rng.permutation(np.repeat(np.array([8, 4], np.uint8), 64))[None].repeat(4, 0)
+    bits[1] = 16
+    bits[3] = 16
+    pb, sb = stepq.stepq_pool_bytes(2, 4, 4, 128, 128, bits)
+    assert sb == oracle.slot_bytes(bits, 128) == 2 * 13312 + 2 * (128 * 256 + 1024)
+    for n16, status in [(32, None), (33, 2), (127, 2)]:
+        b = bits.copy()
+        b[1] = 8
+        b[1, :n16] = 16
+        if status is None:
+            assert stepq.stepq_pool_bytes(2, 4, 4, 128, 128, b)[1] == oracle.slot_bytes(b, 128)
+        else:
+            with pytest.raises(stepq.StepqError) as e:
+                stepq.stepq_pool_bytes(2, 4, 4, 128, 128, b)
+            assert e.value.status == status
+    with pytest.raises(stepq.StepqError) as e:           # whole FP16 heads need d_k = d_v = 128
+        stepq.stepq_pool_bytes(2, 4, 4, 128, 64, bits)
+    assert e.value.status == 2
+
+
 @pytest.mark.parametrize("bad,status", [
     (dict(n_slots=0), 1), (dict(n_v_heads=6, n_qk_heads=4), 1), (dict(d_k=129), 2), (dict(d_v=96), 2),
     (dict(bitval=3), 1), (dict(bitval=12), 1),
-    (dict(bitval=16), 2),                       # 64 pivot rows per head: more than the 32 supported
+    (dict(bitval=16), 2),                       # 64 pivot rows per 64x64 head: more than the 32 supported
 ])
 def test_bad_descriptor_rejected(bad, status):
     a = dict(n_slots=2, n_v_heads=4, n_qk_heads=2, d_k=64, d_v=64)
@@ -231,3 +257,17 @@ def test_calibration_pipeline_meets_the_budget(unit, kda):
     np.testing.assert_allclose(np.exp(np.log(cal.row_weight.astype(np.float64)).mean(axis=1)), 1.0, rtol=1e-6)
     pb, sb = stepq.stepq_pool_bytes(2, 4, 4, 16, 64, bits)        # a valid pool layout
     assert pb == 2 * sb
+
+
+def test_synthetic_pivot_draws():
+    """The seeded pivot draws are reproducible and have the stated shape:
+    1-3 pivot rows in a share of the heads, or whole FP16 heads."""
+    w = W.workload(2)
+    m = W.pivot_mask_draw(w)
+    assert m.shape == (w.n_v_heads, w.d_k) and torch.equal(m, W.pivot_mask_draw(w))
+    per_head = m.sum(1)
+    assert per_head.max() <= 3 and 0 < (per_head > 0).sum() < w.n_v_heads
+    for count in (1, 2, 5):
+        h = W.pivot_head_draw(w, 0, count)
+        assert h.shape == (w.n_v_heads,) and int(h.sum()) == count and torch.equal(h, W.pivot_head_draw(w, 0, count))
+    assert not torch.equal(W.pivot_head_draw(w, 0, 2), W.pivot_head_draw(w, 1, 2))
