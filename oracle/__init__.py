@@ -47,14 +47,14 @@ def lib():
         L = ctypes.CDLL(_LIB_PATH)
         P = ctypes.c_void_p
         i = ctypes.c_int
-        L.orc_fit_absmax.argtypes = [i, i, i, P, P, P, P, P]
-        L.orc_quantize.argtypes = [i, i, i, P, P, P, P, P, P, P]
-        L.orc_dequant.argtypes = [i, i, i, P, P, P, P, P, P]
+        L.orc_fit_absmax.argtypes = [i, i, i, P, P, P, P, P, i]
+        L.orc_quantize.argtypes = [i, i, i, P, P, P, P, P, P, P, i]
+        L.orc_dequant.argtypes = [i, i, i, P, P, P, P, P, P, i]
         L.orc_update_fp.argtypes = [i, i, i, P, P, P, P, P, i, P, P, P]
-        L.orc_decode_step.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P]
+        L.orc_decode_step.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, i]
         L.orc_decode_step_refit.argtypes = [i, i, i, P, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P,
-                                            ctypes.c_double, P, P, P, P]
-        L.orc_decode_step_rowmax.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P]
+                                            ctypes.c_double, P, P, P, P, i]
+        L.orc_decode_step_rowmax.argtypes = [i, i, i, P, P, P, P, P, P, P, P, i, P, P, P, P, P, P, P, P, i]
         L.orc_fit_dual_axis.argtypes = [i, i, i, P, P, P, P, P, P, P]
         L.orc_half_to_double.argtypes = [ctypes.c_size_t, P, P]
         L.orc_double_to_half.argtypes = [ctypes.c_size_t, P, P]
@@ -79,6 +79,18 @@ def _c(a, dtype):
 
 def max_threads() -> int:
     return int(lib().orc_max_threads())
+
+
+# Level normalisation of the stored integers (Section 4.3, Appendix C.1):
+# levels 0 (N1) z = q / q_b; levels 1 (N2) z = 2^(8-b) q, the paper's KDA
+# codebook.  Every numeric entry point below takes it (default N1).
+LEVELS_ABSMAX, LEVELS_POW2 = 0, 1
+
+
+def _lv(levels) -> int:
+    if levels not in (LEVELS_ABSMAX, LEVELS_POW2):
+        raise ValueError("levels must be 0 (N1: q / q_b) or 1 (N2: 2^(8-b) q)")
+    return int(levels)
 
 
 # FP16 pivot rows (width 16): their values travel as binary16 bit patterns,
@@ -113,21 +125,24 @@ def double_to_half(x):
 
 # ---------------------------------------------------------------------------
 # numeric entry points (shapes: tiles flattened to a leading n)
-def fit_absmax(S, w=None, bits=None):
+def fit_absmax(S, w=None, bits=None, levels=LEVELS_ABSMAX):
     """Setup fit (Section 4.3 row factors, absmax column factor).
     S: [n][dk][dv] float32 -> (r [n][dk], c [n][dv]) float32.  bits
-    (optional): pivot rows (16) are left out of the column factor."""
+    (optional under N1, needed under N2, whose largest level depends on
+    the width): pivot rows (16) are left out of the column factor."""
+    if _lv(levels) and bits is None:
+        raise ValueError("the N2 fit needs the row widths")
     S = _c(S, np.float32)
     n, dk, dv = S.shape
     r = np.empty((n, dk), np.float32)
     c = np.empty((n, dv), np.float32)
     wv = None if w is None else _c(np.broadcast_to(w, (n, dk)), np.float64)
     bt = None if bits is None else _c(np.broadcast_to(bits, (n, dk)), np.uint8)
-    lib().orc_fit_absmax(n, dk, dv, _p(S), _p(wv), _p(bt), _p(r), _p(c))
+    lib().orc_fit_absmax(n, dk, dv, _p(S), _p(wv), _p(bt), _p(r), _p(c), _lv(levels))
     return r, c
 
 
-def quantize(X, r, c, bits, want_y=False):
+def quantize(X, r, c, bits, want_y=False, levels=LEVELS_ABSMAX):
     """Eq. 3 on the dual-axis representation. X [n][dk][dv] (fp64),
     bits [n][dk] -> int8 codes (and the unrounded values if want_y)."""
     X = _c(X, np.float64)
@@ -136,19 +151,19 @@ def quantize(X, r, c, bits, want_y=False):
     codes = np.empty((n, dk, dv), np.int8)
     y = np.empty((n, dk, dv), np.float64) if want_y else None
     pv = np.zeros((n, dk, dv), np.uint16) if _has_pivots(bits) else None
-    lib().orc_quantize(n, dk, dv, _p(X), _p(r), _p(c), _p(bits), _p(codes), _p(y), _p(pv))
+    lib().orc_quantize(n, dk, dv, _p(X), _p(r), _p(c), _p(bits), _p(codes), _p(y), _p(pv), _lv(levels))
     out = (codes, y) if want_y else (codes,)
     out = out + ((pv,) if pv is not None else ())
     return out if len(out) > 1 else out[0]
 
 
-def dequant(codes, r, c, bits, pv=None):
+def dequant(codes, r, c, bits, pv=None, levels=LEVELS_ABSMAX):
     codes = _c(codes, np.int8)
     n, dk, dv = codes.shape
     r, c, bits = _c(r, np.float32), _c(c, np.float32), _c(np.broadcast_to(bits, (n, dk)), np.uint8)
     pvi = _pv_in(pv, bits, (n, dk, dv))
     S = np.empty((n, dk, dv), np.float64)
-    lib().orc_dequant(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(pvi), _p(S))
+    lib().orc_dequant(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(pvi), _p(S), _lv(levels))
     return S
 
 
@@ -174,7 +189,7 @@ def update_fp(S, q, k, v, alpha, beta):
     return X, o
 
 
-def decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=False, pv=None):
+def decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=False, pv=None, levels=LEVELS_ABSMAX):
     """One quantized decode step with frozen scales (Table C2 steps 1-3, 6);
     alpha [n] for the GDN gate or [n][dk] for the KDA channel-wise gate."""
     codes = _c(codes, np.int8)
@@ -189,12 +204,13 @@ def decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=False, pv=None):
     pvi = _pv_in(pv, bits, (n, dk, dv))
     pvo = np.zeros((n, dk, dv), np.uint16) if pvi is not None else None
     lib().orc_decode_step(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(q), _p(k), _p(v),
-                          _p(a), per_row, _p(beta), _p(out), _p(o), _p(y), _p(pvi), _p(pvo))
+                          _p(a), per_row, _p(beta), _p(out), _p(o), _p(y), _p(pvi), _p(pvo), _lv(levels))
     res = (out, o, y) if want_y else (out, o)
     return res + (pvo,) if pvo is not None else res
 
 
-def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=(), tie_window=2e-3, pv=None):
+def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=(), tie_window=2e-3, pv=None,
+                      levels=LEVELS_ABSMAX):
     """One quantized decode step with the online dual-axis refit (Table C2
     steps 1-6, Section 4.3, Appendix C.1).  Returns (codes, r, c, o) with the
     new fp32 scales, plus a dict of the requested extras among "y", "y0", "X"
@@ -223,14 +239,14 @@ def decode_step_refit(codes, r, c, bits, q, k, v, alpha, beta, w=None, want=(), 
     lib().orc_decode_step_refit(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(wt), _p(q), _p(k), _p(v),
                                 _p(a), per_row, _p(beta), _p(out), _p(r_out), _p(c_out), _p(o),
                                 _p(extra.get("y")), _p(extra.get("y0")), _p(extra.get("X")), float(tie_window),
-                                _p(lo), _p(hi), _p(pvi), _p(pvo))
+                                _p(lo), _p(hi), _p(pvi), _p(pvo), _lv(levels))
     if lo is not None:
         extra["c_range"] = (lo, hi)
     res = (out, r_out, c_out, o, extra) if want else (out, r_out, c_out, o)
     return res + (pvo,) if pvo is not None else res
 
 
-def decode_step_rowmax(codes, r, c, bits, q, k, v, alpha, beta, want_y=False, pv=None):
+def decode_step_rowmax(codes, r, c, bits, q, k, v, alpha, beta, want_y=False, pv=None, levels=LEVELS_ABSMAX):
     """One decode step of the row-wise absmax INT-b baseline (Section 5.1) on
     the same quantized tile: returns (codes, r, c, o[, y]) with r'_i =
     max_j |X_ij| and c' = 1."""
@@ -248,7 +264,8 @@ def decode_step_rowmax(codes, r, c, bits, q, k, v, alpha, beta, want_y=False, pv
     pvi = _pv_in(pv, bits, (n, dk, dv))
     pvo = np.zeros((n, dk, dv), np.uint16) if pvi is not None else None
     lib().orc_decode_step_rowmax(n, dk, dv, _p(codes), _p(r), _p(c), _p(bits), _p(q), _p(k), _p(v), _p(a),
-                                 per_row, _p(beta), _p(out), _p(r_out), _p(c_out), _p(o), _p(y), _p(pvi), _p(pvo))
+                                 per_row, _p(beta), _p(out), _p(r_out), _p(c_out), _p(o), _p(y), _p(pvi), _p(pvo),
+                                 _lv(levels))
     res = (out, r_out, c_out, o, y) if want_y else (out, r_out, c_out, o)
     return res + (pvo,) if pvo is not None else res
 

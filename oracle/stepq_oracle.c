@@ -13,10 +13,14 @@
  * S in R^{d_k x d_v}; key rows i, value columns j.  Row i holds a b_i-bit
  * signed integer code per entry with q_b = 2^(b-1) - 1 (Eq. 3).  The
  * dual-axis representation (Section 4.3) reconstructs
- *     S^_ij = r_i * c_j * z_ij ,   z_ij = q_ij / q_{b_i}
- * i.e. the level set is normalised so that |S^_ij| <= r_i c_j at every
- * width (this is the reading that makes "r_i c_j >= |S_ij|" the no-clip
- * condition of a symmetric absmax fit).
+ *     S^_ij = r_i * c_j * z_ij
+ * from the level z_ij of the stored integer q_ij, in one of two level
+ * normalisations (argument levels):
+ *   0 (N1): z = q / q_b, so |S^_ij| <= r_i c_j at every width (the reading
+ *           that makes "r_i c_j >= |S_ij|" the no-clip condition of a
+ *           symmetric absmax fit);
+ *   1 (N2): z = 2^(8-b) q, the fixed normalisation of the paper's KDA
+ *           codebook (Appendix C.1), whose largest level is 2^(8-b) q_b.
  *
  * FP16 pivot rows (Section 3.2, Table C1): a row of width 16 holds its
  * values as IEEE binary16 (pv, bit patterns, [dk][dv] per tile, only pivot
@@ -32,6 +36,11 @@
 #include <stdlib.h>
 
 static double qb_of(int b) { return (double)((1 << (b - 1)) - 1); }
+
+/* q = z * inv_nu(b): N1 q_b, N2 2^(b-8) (exact).  top_of(b): the largest
+ * level q_b / inv_nu(b), 1 under N1. */
+static double inv_nu(int b, int levels) { return levels ? ldexp(1.0, b - 8) : qb_of(b); }
+static double top_of(int b, int levels) { return levels ? qb_of(b) * ldexp(1.0, 8 - b) : 1.0; }
 
 /* IEEE 754 binary16, from its definition: 1 sign bit, 5 exponent bits (bias
  * 15), 10 fraction bits; exponent 0 holds subnormals k 2^-24. */
@@ -82,16 +91,16 @@ void orc_double_to_half(size_t n, const double *x, uint16_t *out)
 /* Reconstruction of one tile (Section 4.3, and the stored binary16 values of
  * pivot rows). */
 static void reconstruct_tile(int dk, int dv, const int8_t *ci, const uint16_t *pv, const float *rt,
-                             const float *ct, const uint8_t *bt, double *Sh)
+                             const float *ct, const uint8_t *bt, double *Sh, int levels)
 {
     for (int i = 0; i < dk; ++i) {
         if (bt[i] == 16) {
             for (int j = 0; j < dv; ++j) Sh[(size_t)i * dv + j] = h2d(pv[(size_t)i * dv + j]);
             continue;
         }
-        double qb = qb_of(bt[i]);
+        double iv = inv_nu(bt[i], levels);
         for (int j = 0; j < dv; ++j)
-            Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / qb;
+            Sh[(size_t)i * dv + j] = (double)rt[i] * (double)ct[j] * (double)ci[(size_t)i * dv + j] / iv;
     }
 }
 
@@ -116,15 +125,15 @@ static void store_pivots(int dk, int dv, const uint8_t *bt, const double *X, uin
  * factor in its absmax form).
  *   m_i = (1/d_v) sum_j |S_ij|
  *   r_i = m_i^{1/2} w_i^{-1/2}
- *   c_j = max_i |S_ij| / r_i            (so that r_i c_j >= |S_ij|)
+ *   c_j = max_i |S_ij| / (r_i top_i)    (so that r_i c_j top_i >= |S_ij|; top = 1 under N1)
  * A positive floor of 2^-60 keeps both factors strictly positive
  * (Appendix C.1 asks for a positive numerical floor).  The results are
  * rounded once to fp32, the storage precision of the scales.
- * w == NULL means w_i = 1.  bits (optional, [n_tiles][dk]): rows of width 16
- * (pivots) are left out of the column factor.
+ * w == NULL means w_i = 1.  bits (optional under N1, [n_tiles][dk]): rows of
+ * width 16 (pivots) are left out of the column factor.
  */
 void orc_fit_absmax(int n_tiles, int dk, int dv, const float *S, const double *w, const uint8_t *bits,
-                    float *r_out, float *c_out)
+                    float *r_out, float *c_out, int levels)
 {
     const double floor_ = ldexp(1.0, -60);
     #pragma omp parallel for schedule(static)
@@ -146,6 +155,7 @@ void orc_fit_absmax(int n_tiles, int dk, int dv, const float *S, const double *w
             for (int i = 0; i < dk; ++i) {
                 if (bits && bits[(size_t)t * dk + i] == 16) continue;     /* pivots keep their own values */
                 double a = fabs((double)St[(size_t)i * dv + j]) / r[i];
+                if (levels) a /= top_of(bits[(size_t)t * dk + i], levels);
                 if (a > cj) cj = a;
             }
             if (cj < floor_) cj = floor_;
@@ -161,13 +171,13 @@ void orc_fit_absmax(int n_tiles, int dk, int dv, const float *S, const double *w
 
 /* ------------------------------------------------------------------------
  * Quantizer (Eq. 3, applied to the dual-axis representation of Section 4.3):
- *   q_ij = clip(round(X_ij * q_b / (r_i c_j)), -q_b, q_b)
+ *   q_ij = clip(round(X_ij * inv_nu / (r_i c_j)), -q_b, q_b)     (inv_nu = q_b under N1)
  * round = nearest, ties to even (nearbyint under the default rounding mode).
- * bits: [n_tiles][dk].  y (optional) receives the unrounded X q_b/(r c).
+ * bits: [n_tiles][dk].  y (optional) receives the unrounded X inv_nu/(r c).
  * Pivot rows (width 16): pv receives X in binary16, codes 0.
  */
 void orc_quantize(int n_tiles, int dk, int dv, const double *X, const float *r, const float *c,
-                  const uint8_t *bits, int8_t *codes, double *y, uint16_t *pv)
+                  const uint8_t *bits, int8_t *codes, double *y, uint16_t *pv, int levels)
 {
     #pragma omp parallel for schedule(static)
     for (int t = 0; t < n_tiles; ++t) {
@@ -177,10 +187,11 @@ void orc_quantize(int n_tiles, int dk, int dv, const double *X, const float *r, 
         for (int i = 0; i < dk; ++i) {
             if (bits[(size_t)t * dk + i] == 16) continue;
             double qb = qb_of(bits[(size_t)t * dk + i]);
+            double iv = inv_nu(bits[(size_t)t * dk + i], levels);
             double ri = (double)r[(size_t)t * dk + i];
             for (int j = 0; j < dv; ++j) {
                 size_t e = ((size_t)t * dk + i) * dv + j;
-                double s = X[e] * qb / (ri * (double)c[(size_t)t * dv + j]);
+                double s = X[e] * iv / (ri * (double)c[(size_t)t * dv + j]);
                 if (y) y[e] = s;
                 double n = nearbyint(s);
                 if (n > qb) n = qb;
@@ -191,16 +202,16 @@ void orc_quantize(int n_tiles, int dk, int dv, const double *X, const float *r, 
     }
 }
 
-/* Reconstruction (Section 4.3): S^_ij = r_i c_j q_ij / q_{b_i}; pivot rows
- * from their binary16 values. */
+/* Reconstruction (Section 4.3): S^_ij = r_i c_j q_ij / inv_nu(b_i); pivot
+ * rows from their binary16 values. */
 void orc_dequant(int n_tiles, int dk, int dv, const int8_t *codes, const float *r, const float *c,
-                 const uint8_t *bits, const uint16_t *pv, double *S)
+                 const uint8_t *bits, const uint16_t *pv, double *S, int levels)
 {
     #pragma omp parallel for schedule(static)
     for (int t = 0; t < n_tiles; ++t) {
         size_t nel = (size_t)dk * dv;
         reconstruct_tile(dk, dv, codes + t * nel, pv ? pv + t * nel : NULL, r + (size_t)t * dk,
-                         c + (size_t)t * dv, bits + (size_t)t * dk, S + t * nel);
+                         c + (size_t)t * dv, bits + (size_t)t * dk, S + t * nel, levels);
     }
 }
 
@@ -260,13 +271,14 @@ void orc_update_fp(int n_tiles, int dk, int dv, const double *S, const double *q
  * (step 2; D = alpha I or diag(d)), emit o = X^T q before requantization
  * (step 3), requantize X on the same r, c and per-row widths (Eq. 3) as the
  * new codes.
- * y (optional) receives X q_b/(r c) before rounding (X itself on pivot
+ * y (optional) receives X inv_nu/(r c) before rounding (X itself on pivot
  * rows).  pv_in / pv_out: binary16 values of pivot rows (NULL without pivots).
  */
 void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const float *r,
                      const float *c, const uint8_t *bits, const double *q, const double *k,
                      const double *v, const double *alpha, int per_row, const double *beta,
-                     int8_t *codes_out, double *o, double *y, const uint16_t *pv_in, uint16_t *pv_out)
+                     int8_t *codes_out, double *o, double *y, const uint16_t *pv_in, uint16_t *pv_out,
+                     int levels)
 {
     #pragma omp parallel for schedule(dynamic, 4)
     for (int t = 0; t < n_tiles; ++t) {
@@ -277,16 +289,16 @@ void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const 
         const int8_t *ci = codes_in + (size_t)t * nel;
         const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
         const uint8_t *bt = bits + (size_t)t * dk;
-        reconstruct_tile(dk, dv, ci, pv_in ? pv_in + (size_t)t * nel : NULL, rt, ct, bt, Sh);
+        reconstruct_tile(dk, dv, ci, pv_in ? pv_in + (size_t)t * nel : NULL, rt, ct, bt, Sh, levels);
         update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
                     gate_of(alpha, per_row, t, dk, gbuf), beta[t], X, o + (size_t)t * dv);
         store_pivots(dk, dv, bt, X, pv_out ? pv_out + (size_t)t * nel : NULL, codes_out + (size_t)t * nel,
                      y ? y + (size_t)t * nel : NULL);
         for (int i = 0; i < dk; ++i) {
             if (bt[i] == 16) continue;
-            double qb = qb_of(bt[i]);
+            double qb = qb_of(bt[i]), iv = inv_nu(bt[i], levels);
             for (int j = 0; j < dv; ++j) {
-                double s = X[(size_t)i * dv + j] * qb / ((double)rt[i] * (double)ct[j]);
+                double s = X[(size_t)i * dv + j] * iv / ((double)rt[i] * (double)ct[j]);
                 if (y) y[(size_t)t * nel + (size_t)i * dv + j] = s;
                 double n = nearbyint(s);
                 if (n > qb) n = qb;
@@ -307,17 +319,18 @@ void orc_decode_step(int n_tiles, int dk, int dv, const int8_t *codes_in, const 
  * orc_decode_step (X and o).  Then, per tile, with row-impact factors w
  * (w == NULL: w_i = 1):
  *   row factors   m_i = (1/d_v) sum_j |X_ij|,  r'_i = (m_i / w_i)^{1/2}
- *   column start  c0_j = max_i |X_ij| / r'_i          (absmax: no fixed code clips)
- *   fixed codes   z_ij = clip(round(X_ij q_b / (r'_i c0_j)), -q_b, q_b) / q_b
+ *   column start  c0_j = max_i |X_ij| / (r'_i top_i)   (absmax: no fixed code clips)
+ *   fixed codes   z_ij = clip(round(X_ij inv_nu / (r'_i c0_j)), -q_b, q_b) / inv_nu   (the levels)
  *   column fit    c'_j = sum_i w_i^2 v_ij X_ij / sum_i w_i^2 v_ij^2,  v_ij = r'_i z_ij
  *                 (minimiser of sum_i w_i^2 (X_ij - r'_i c z_ij)^2 over c)
  *                 a zero denominator keeps the previous scale c_j
- *   requantize    q'_ij = clip(round(X_ij q_b / (r'_i c'_j)), -q_b, q_b)
+ *   requantize    q'_ij = clip(round(X_ij inv_nu / (r'_i c'_j)), -q_b, q_b)
+ * (inv_nu = q_b and top = 1 under N1.)
  * r', c0 and c' are floored at 2^-60.  r' and c' are the stored scales:
  * each is rounded to fp32 when it is formed, and what follows it uses the
  * rounded value.
- * Optional outputs: y (X q_b / (r' c') before rounding), y0 (X q_b / (r' c0)
- * before rounding), X.  Pivot rows (width 16) are updated in binary16
+ * Optional outputs: y (X inv_nu / (r' c') before rounding), y0 (X inv_nu /
+ * (r' c0) before rounding), X.  Pivot rows (width 16) are updated in binary16
  * (pv_in / pv_out), keep their stored r, and are left out of both fits.
  *
  * c_lo, c_hi (optional, for comparing with lower-precision implementations):
@@ -334,7 +347,7 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
                            const double *k, const double *v, const double *alpha, int per_row,
                            const double *beta, int8_t *codes_out, float *r_out, float *c_out, double *o,
                            double *y, double *y0, double *X_out, double tie_window, double *c_lo,
-                           double *c_hi, const uint16_t *pv_in, uint16_t *pv_out)
+                           double *c_hi, const uint16_t *pv_in, uint16_t *pv_out, int levels)
 {
     const double floor_ = ldexp(1.0, -60);
     #pragma omp parallel for schedule(dynamic, 4)
@@ -348,7 +361,7 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
         const int8_t *ci = codes_in + (size_t)t * nel;
         const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
         const uint8_t *bt = bits + (size_t)t * dk;
-        reconstruct_tile(dk, dv, ci, pv_in ? pv_in + (size_t)t * nel : NULL, rt, ct, bt, Sh);
+        reconstruct_tile(dk, dv, ci, pv_in ? pv_in + (size_t)t * nel : NULL, rt, ct, bt, Sh, levels);
         update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
                     gate_of(alpha, per_row, t, dk, gbuf), beta[t], X, o + (size_t)t * dv);
         if (X_out) memcpy(X_out + (size_t)t * nel, X, sizeof(double) * nel);
@@ -377,6 +390,7 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
             for (int i = 0; i < dk; ++i) {
                 if (bt[i] == 16) continue;
                 double a = fabs(X[(size_t)i * dv + j]) / rn[i];
+                if (levels) a /= top_of(bt[i], levels);
                 if (a > c0) c0 = a;
             }
             if (c0 < floor_) c0 = floor_;
@@ -386,13 +400,13 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
                     if (y0) y0[(size_t)t * nel + (size_t)i * dv + j] = 0.0;
                     continue;
                 }
-                double qb = qb_of(bt[i]);
-                double s = X[(size_t)i * dv + j] * qb / (rn[i] * c0);
+                double qb = qb_of(bt[i]), iv = inv_nu(bt[i], levels);
+                double s = X[(size_t)i * dv + j] * iv / (rn[i] * c0);
                 if (y0) y0[(size_t)t * nel + (size_t)i * dv + j] = s;
                 double n = nearbyint(s);
                 if (n > qb) n = qb;
                 if (n < -qb) n = -qb;
-                zt[(size_t)i * dv + j] = n / qb;
+                zt[(size_t)i * dv + j] = n / iv;
             }
             /* weighted least squares in c with the codes held fixed */
             double num = 0.0, den = 0.0;
@@ -414,15 +428,15 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
                 double nlo = num, nhi = num, dlo = den, dhi = den;
                 for (int i = 0; i < dk; ++i) {
                     if (bt[i] == 16) continue;
-                    double qb = qb_of(bt[i]);
+                    double qb = qb_of(bt[i]), iv = inv_nu(bt[i], levels);
                     double s = y0[(size_t)t * nel + (size_t)i * dv + j];
                     double a = fabs(s);
                     if (fabs(a - floor(a) - 0.5) > tie_window) continue;
-                    double z = zt[(size_t)i * dv + j] * qb;
+                    double z = zt[(size_t)i * dv + j] * iv;
                     double alt = (z > s) ? z - 1.0 : z + 1.0;     /* the other neighbour of s */
                     if (alt > qb || alt < -qb) continue;
                     double wi = w ? w[(size_t)t * dk + i] : 1.0;
-                    double v0 = rn[i] * z / qb, v1 = rn[i] * alt / qb;
+                    double v0 = rn[i] * z / iv, v1 = rn[i] * alt / iv;
                     double dn = wi * wi * (v1 - v0) * X[(size_t)i * dv + j];
                     double dd = wi * wi * (v1 * v1 - v0 * v0);
                     if (dn < 0) nlo += dn; else nhi += dn;
@@ -451,9 +465,9 @@ void orc_decode_step_refit(int n_tiles, int dk, int dv, const int8_t *codes_in, 
         /* requantize against the stored scales */
         for (int i = 0; i < dk; ++i) {
             if (bt[i] == 16) continue;
-            double qb = qb_of(bt[i]);
+            double qb = qb_of(bt[i]), iv = inv_nu(bt[i], levels);
             for (int j = 0; j < dv; ++j) {
-                double s = X[(size_t)i * dv + j] * qb / (rn[i] * (double)c_out[(size_t)t * dv + j]);
+                double s = X[(size_t)i * dv + j] * iv / (rn[i] * (double)c_out[(size_t)t * dv + j]);
                 if (y) y[(size_t)t * nel + (size_t)i * dv + j] = s;
                 double n = nearbyint(s);
                 if (n > qb) n = qb;
@@ -552,16 +566,17 @@ void orc_fit_dual_axis(int n_tiles, int dk, int dv, const double *Xall, const ui
  * One decode step of the single-axis baseline the paper compares against
  * (Section 5.1: symmetric row-wise absmax INT-b), on the same quantized
  * tile: steps 1-3 of orc_decode_step, then per key row
- *   r'_i = max_j |X_ij|  (floor 2^-60, stored fp32),   c'_j = 1,
- *   q'_ij = clip(round(X_ij q_b / r'_i), -q_b, q_b)    with the stored r'.
- * y (optional) receives X q_b / r' before rounding.  Pivot rows as in
+ *   r'_i = max_j |X_ij| / top_i  (floor 2^-60, stored fp32),   c'_j = 1,
+ *   q'_ij = clip(round(X_ij inv_nu / r'_i), -q_b, q_b)    with the stored r',
+ * so each row's largest entry lands on the top level (inv_nu = q_b and
+ * top = 1 under N1).  y (optional) receives X inv_nu / r' before rounding.  Pivot rows as in
  * orc_decode_step_refit.
  */
 void orc_decode_step_rowmax(int n_tiles, int dk, int dv, const int8_t *codes_in, const float *r,
                             const float *c, const uint8_t *bits, const double *q, const double *k,
                             const double *v, const double *alpha, int per_row, const double *beta,
                             int8_t *codes_out, float *r_out, float *c_out, double *o, double *y,
-                            const uint16_t *pv_in, uint16_t *pv_out)
+                            const uint16_t *pv_in, uint16_t *pv_out, int levels)
 {
     const double floor_ = ldexp(1.0, -60);
     #pragma omp parallel for schedule(dynamic, 4)
@@ -573,7 +588,7 @@ void orc_decode_step_rowmax(int n_tiles, int dk, int dv, const int8_t *codes_in,
         const int8_t *ci = codes_in + (size_t)t * nel;
         const float *rt = r + (size_t)t * dk, *ct = c + (size_t)t * dv;
         const uint8_t *bt = bits + (size_t)t * dk;
-        reconstruct_tile(dk, dv, ci, pv_in ? pv_in + (size_t)t * nel : NULL, rt, ct, bt, Sh);
+        reconstruct_tile(dk, dv, ci, pv_in ? pv_in + (size_t)t * nel : NULL, rt, ct, bt, Sh, levels);
         update_tile(dk, dv, Sh, q + (size_t)t * dk, k + (size_t)t * dk, v + (size_t)t * dv,
                     gate_of(alpha, per_row, t, dk, gbuf), beta[t], X, o + (size_t)t * dv);
         for (int j = 0; j < dv; ++j) c_out[(size_t)t * dv + j] = 1.0f;
@@ -589,12 +604,13 @@ void orc_decode_step_rowmax(int n_tiles, int dk, int dv, const int8_t *codes_in,
                 double a = fabs(X[(size_t)i * dv + j]);
                 if (a > m) m = a;
             }
+            if (levels) m /= top_of(bt[i], levels);
             if (m < floor_) m = floor_;
             r_out[(size_t)t * dk + i] = (float)m;
             double ri = (double)r_out[(size_t)t * dk + i];
-            double qb = qb_of(bt[i]);
+            double qb = qb_of(bt[i]), iv = inv_nu(bt[i], levels);
             for (int j = 0; j < dv; ++j) {
-                double s = X[(size_t)i * dv + j] * qb / ri;
+                double s = X[(size_t)i * dv + j] * iv / ri;
                 if (y) y[(size_t)t * nel + (size_t)i * dv + j] = s;
                 double n = nearbyint(s);
                 if (n > qb) n = qb;
