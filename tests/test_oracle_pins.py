@@ -566,17 +566,20 @@ def test_refit_requantizes_with_the_new_scales():
     assert np.array_equal(o, o_frozen)
 
 
-def test_refit_column_range_encloses_every_tie_rounding():
+@pytest.mark.parametrize("levels", [oracle.LEVELS_ABSMAX, oracle.LEVELS_POW2])
+def test_refit_column_range_encloses_every_tie_rounding(levels):
     """The (lo, hi) column-factor range encloses the least-squares factor of
     every combination of other roundings of the near-tie fixed codes,
     enumerated here and solved with a library least-squares routine; with a
-    zero window the range is the factor itself."""
+    zero window the range is the factor itself.  Both level normalisations
+    (a code q of a b-bit row is the level q / q_b, or 2^(8-b) q)."""
     codes, r, c, bits, q, k, v, g, beta, w = _refit_case(seed=36, n=2, dk=10, dv=6)
     win = 0.15                                   # wide, so that several codes per column qualify
     _, rn, cn, _, ex = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w,
-                                                want=("X", "y0", "c_range"), tie_window=win)
+                                                want=("X", "y0", "c_range"), tie_window=win, levels=levels)
     lo, hi = ex["c_range"]
     qb = (2.0 ** (bits.astype(np.int64) - 1) - 1)[:, :, None]
+    lev = 1.0 / qb if levels == oracle.LEVELS_ABSMAX else (2.0 ** (8 - bits.astype(np.int64)))[:, :, None]
     y0, X = ex["y0"], ex["X"]
     z = np.clip(np.rint(y0), -qb, qb)
     n_multi = 0
@@ -595,14 +598,15 @@ def test_refit_column_range_encloses_every_tie_rounding():
                 for (i, alt), m in zip(alts, mask):
                     if m:
                         zz[i] = alt
-                A = (w[t] * rn[t].astype(np.float64) * zz / qb[t, :, 0])[:, None]
+                A = (w[t] * rn[t].astype(np.float64) * zz * lev[t, :, 0])[:, None]
                 if not np.any(A):
                     continue
                 cs = np.linalg.lstsq(A, w[t] * X[t, :, j], rcond=None)[0][0]
                 assert lo[t, j] * (1 - 1e-12) <= cs <= hi[t, j] * (1 + 1e-12)
             assert lo[t, j] <= cn[t, j] * (1 + 1e-7) and cn[t, j] <= hi[t, j] * (1 + 1e-7)
     assert n_multi > 0
-    *_, ex0 = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w, want=("c_range",), tie_window=0.0)
+    *_, ex0 = oracle.decode_step_refit(codes, r, c, bits, q, k, v, g, beta, w=w, want=("c_range",), tie_window=0.0,
+                                       levels=levels)
     lo0, hi0 = ex0["c_range"]
     assert np.array_equal(lo0, hi0) and np.array_equal(lo0.astype(np.float32), cn)
 
