@@ -93,6 +93,15 @@ typedef enum {
     STEPQ_BF16 = 1            /* activations as bfloat16 (upper half of a float) */
 } stepq_dtype;
 
+/* Level normalisation of the stored integers (Section 4.3, Appendix C.1): a
+ * b-bit code q (|q| <= q_b = 2^(b-1) - 1) stands for the level z, and
+ * S^_ij = r_i c_j z_ij.  Every scale fit, quantization and reconstruction of
+ * a pool uses its normalisation. */
+typedef enum {
+    STEPQ_LEVELS_ABSMAX = 0,  /* N1: z = q / q_b, so |S^_ij| <= r_i c_j at every width (default) */
+    STEPQ_LEVELS_POW2 = 1     /* N2: z = 2^(8-b) q, the paper's KDA codebook; top level 2^(8-b) q_b */
+} stepq_levels;
+
 typedef struct stepq_pool stepq_pool;   /* opaque */
 
 typedef struct {
@@ -102,6 +111,7 @@ typedef struct {
     int32_t d_k;              /* key rows per tile, 1 .. 128 */
     int32_t d_v;              /* value columns per tile, 64 or 128 */
     const uint8_t *row_bits;  /* host [Hv][d_k], each 2, 4, 8 or 16 (pivot); copied by stepq_pool_create */
+    int32_t levels;           /* stepq_levels; 0 (a zero-initialised descriptor) is N1 */
 } stepq_pool_desc;
 
 /* Size of the pool described by desc (layout above).  Either output may be
@@ -126,8 +136,9 @@ void *stepq_pool_device_ptr(const stepq_pool *pool);
 
 /* Quantize and pack full-precision states into slots (the boundary pack after
  * prefill).  For i < n: slot slot_ids[i] receives
- *   q_hj = clip(round(state[i][h][j][:] q_b / (r c)), -q_b, q_b)
- * with scales r (logical row order) and c stored alongside.
+ *   q_hj = clip(round(state[i][h][j][:] / (r c nu)), -q_b, q_b)
+ * with scales r (logical row order) and c stored alongside, nu the level
+ * step of the row's width (1/q_b under N1, 2^(8-b) under N2).
  *   slot_ids [n] int32, state [n][Hv][d_k][d_v] fp32 (logical row order),
  *   r [n][Hv][d_k] fp32 > 0, c [n][Hv][d_v] fp32 > 0.
  * The rounding is taken in fp32. */
@@ -196,8 +207,8 @@ stepq_status stepq_decode_step_ex(stepq_pool *pool, const int32_t *slot_ids, int
  * decode step is in flight while the table changes.  A new pool has w = 1. */
 stepq_status stepq_pool_set_row_weight(stepq_pool *pool, const float *row_weight);
 
-/* Reconstruct S^_ij = r_i c_j q_ij / q_{b_i} (Section 4.3; pivot rows: their
- * binary16 values) for n slots into out [n][Hv][d_k][d_v] fp32, logical row
+/* Reconstruct S^_ij = r_i c_j z_ij (Section 4.3; z the level of the code in
+ * the pool's normalisation, q / q_b under N1; pivot rows: their binary16 values) for n slots into out [n][Hv][d_k][d_v] fp32, logical row
  * order.  Computed in fp32. */
 stepq_status stepq_pool_dequant(const stepq_pool *pool, const int32_t *slot_ids, int32_t n, float *out,
                                 void *stream);
@@ -250,6 +261,15 @@ stepq_status stepq_setup_fit(int64_t n_tiles, int32_t d_k, int32_t d_v, const fl
 stepq_status stepq_setup_fit_ex(int64_t n_tiles, int32_t d_k, int32_t d_v, const float *state,
                                 const float *row_weight, const uint8_t *row_bits, float *r, float *c,
                                 int32_t n_threads);
+
+/* stepq_setup_fit_ex for a pool of either level normalisation: the column
+ * factors are c_j = max_i |S_ij| / (r_i top_i), top_i = 1 under N1 and
+ * 2^(8-b_i) q_{b_i} under N2, so that every code of the fitted state lies in
+ * [-q_b, q_b] and each column reaches the top level.  row_bits is required
+ * under N2 (STEPQ_E_INVALID when NULL); levels is a stepq_levels value. */
+stepq_status stepq_setup_fit_levels(int64_t n_tiles, int32_t d_k, int32_t d_v, const float *state,
+                                    const float *row_weight, const uint8_t *row_bits, int32_t levels, float *r,
+                                    float *c, int32_t n_threads);
 
 /* Lifetime-aware bit allocation over key rows (Section 3.2, Eq. 6) with two
  * candidate widths lo < hi and an average budget lo <= budget <= hi.

@@ -227,7 +227,7 @@ __device__ __forceinline__ RowColOps load_ops(const DecodeArgs &a, int tile, int
 // from the LDS copy of k and q.
 template <bool DIAG, int DV>
 __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float alpha, float beta,
-                                               const RowColOps &op, DecodeShared<DV> &sh)
+                                               const RowColOps &op, DecodeShared<DV> &sh, const LevelTable &lv)
 {
     const int tid = threadIdx.x;
     if (tid < dk) {
@@ -261,9 +261,10 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
             const float ki = sh.sk[i];
             const float qi = sh.sq[i];
             const float rp = sh.sr[p];
-            const float qb = bw == 8 ? 127.0f : (bw == 4 ? 7.0f : 1.0f);
-            // 2^(b-8) / q_b: 1/127, 1/112, 1/64 (an unpacked field reads 2^(8-b) q)
-            const float fq = bw == 8 ? (1.0f / 127.0f) : (bw == 4 ? (1.0f / 112.0f) : (1.0f / 64.0f));
+            // level of an unpacked field 2^(8-b) q: times fq (N1: 1/127, 1/112, 1/64)
+            const int wi = bw == 8 ? 0 : (bw == 4 ? 1 : 2);
+            const float qb = lv.iq[wi];
+            const float fq = lv.fq[wi];
             const float di = DIAG ? sh.sd[i] : 1.0f;       // the gate folds into both row weights
             const float rs = rp * fq * di;
             kt = ki * rs;
@@ -374,7 +375,8 @@ __device__ __forceinline__ void pivot_update(const TileCtx &t, int slice, int cg
 
 // Uniform layouts: table slot = physical row = tid, widths known at compile time.
 template <bool DIAG, int M8, int M4, int DV>
-__device__ __forceinline__ float row_constants_uniform(float beta, const RowColOps &op, DecodeShared<DV> &sh)
+__device__ __forceinline__ float row_constants_uniform(float beta, const RowColOps &op, DecodeShared<DV> &sh,
+                                                       const LevelTable &lv)
 {
     constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
     const int tid = threadIdx.x;
@@ -387,8 +389,9 @@ __device__ __forceinline__ float row_constants_uniform(float beta, const RowColO
     float kq = 0.f;
     if (tid < 128) {
         const int p = tid;
-        const float qb = p < X4 ? 127.0f : (p < X2 ? 7.0f : 1.0f);
-        const float fq = p < X4 ? (1.0f / 127.0f) : (p < X2 ? (1.0f / 112.0f) : (1.0f / 64.0f));
+        const int wi = p < X4 ? 0 : (p < X2 ? 1 : 2);
+        const float qb = lv.iq[wi];
+        const float fq = lv.fq[wi];
         const float ki = sh.sk[op.perm];
         const float qi = sh.sq[op.perm];
         const float di = DIAG ? sh.sd[op.perm] : 1.0f;

@@ -24,6 +24,7 @@ struct stepq_pool {
     uint8_t *d_perm = nullptr;
     float *d_roww = nullptr;          // [Hv][dk] row-impact factors, physical order
     int device = 0;
+    int levels = STEPQ_LEVELS_ABSMAX; // level normalisation of the codes
     int layout = 0;                   // uniform layout of every head, or 0
     // Layout classes of a mixed pool at d_v = 128: heads grouped by their
     // uniform layout (1-5), or the generic heads (0, or kCompactGeneric when
@@ -66,6 +67,8 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
     if (d->d_k < 1 || d->d_k > stepq::kMaxDk) return fail(STEPQ_E_UNSUPPORTED, "d_k must be in 1..128");
     if (d->d_v != 64 && d->d_v != 128) return fail(STEPQ_E_UNSUPPORTED, "d_v must be 64 or 128");
     if (!d->row_bits) return fail(STEPQ_E_INVALID, "row_bits is NULL");
+    if (d->levels != STEPQ_LEVELS_ABSMAX && d->levels != STEPQ_LEVELS_POW2)
+        return fail(STEPQ_E_INVALID, "levels must be STEPQ_LEVELS_ABSMAX or STEPQ_LEVELS_POW2");
     const int Hv = d->n_v_heads, dk = d->d_k, dv = d->d_v;
     heads->assign(Hv, HeadInfo{});
     perm->assign(static_cast<size_t>(Hv) * dk, 0);
@@ -151,6 +154,22 @@ stepq::PoolView view(const stepq_pool *p)
     v.dv = p->dv;
     v.div_hv = fast_div(static_cast<uint32_t>(p->Hv));
     v.div_g = fast_div(static_cast<uint32_t>(p->Hv / p->Hqk));
+    // per width 8 / 4 / 2: q = level * iq; nu = 1 / iq; fq = 2^(b-8) / iq
+    const int widths[3] = {8, 4, 2};
+    for (int w = 0; w < 3; ++w) {
+        const int b = widths[w];
+        const float qb = static_cast<float>((1 << (b - 1)) - 1);
+        const float p2 = std::ldexp(1.0f, b - 8);       // 2^(b-8)
+        if (p->levels == STEPQ_LEVELS_POW2) {
+            v.lv.iq[w] = p2;
+            v.lv.nu[w] = 1.0f / p2;
+            v.lv.fq[w] = 1.0f;
+        } else {
+            v.lv.iq[w] = qb;
+            v.lv.nu[w] = 1.0f / qb;
+            v.lv.fq[w] = p2 / qb;
+        }
+    }
     return v;
 }
 
@@ -225,6 +244,7 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
         return st;
     }
     p->n_slots = desc->n_slots;
+    p->levels = desc->levels;
     p->Hv = desc->n_v_heads;
     p->Hqk = desc->n_qk_heads;
     p->dk = desc->d_k;

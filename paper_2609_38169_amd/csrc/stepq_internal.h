@@ -65,6 +65,15 @@ struct FastDiv {
     uint32_t mul, shift;
 };
 
+// Per-width constants of the pool's level normalisation, index 0 / 1 / 2 for
+// 8- / 4- / 2-bit rows.  The stored integer q of a row stands for the level
+// z = q / iq (iq = q_b under N1, 2^(b-8) under N2, the paper's KDA
+// codebook); nu = 1 / iq; fq = 2^(b-8) / iq turns an unpacked field
+// 2^(8-b) q into z.
+struct LevelTable {
+    float iq[3], nu[3], fq[3];
+};
+
 struct PoolView {
     uint8_t *base;
     uint64_t slot_bytes;
@@ -74,6 +83,7 @@ struct PoolView {
     int32_t n_slots, Hv, Hqk, dk, dv;
     FastDiv div_hv;          // divide by Hv
     FastDiv div_g;           // divide by Hv / Hqk
+    LevelTable lv;
 };
 
 // One value head of a decode launch over part of a pool's heads: its index

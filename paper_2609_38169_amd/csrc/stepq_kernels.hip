@@ -43,7 +43,7 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
     for (int m = 0; m < M; ++m) w[m] = cw.load(tid + 256 * m);
 
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    const float kappa = row_constants_uniform<DIAG, M8, M4, 128>(t.beta, op, sh);
+    const float kappa = row_constants_uniform<DIAG, M8, M4, 128>(t.beta, op, sh, a.pool.lv);
 
     uint32_t U[NE / 2];
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
@@ -94,7 +94,7 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
     PivotRegs<DV, PMAX> pr;
     pivot_load(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    const float kappa = row_constants<DIAG, DV>(t.hi, a.pool.dk, t.alpha, t.beta, op, sh);
+    const float kappa = row_constants<DIAG, DV>(t.hi, a.pool.dk, t.alpha, t.beta, op, sh, a.pool.lv);
 
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
     float U[16];
@@ -364,6 +364,7 @@ __global__ __launch_bounds__(256) void tile_kernel(TileArgs a)
         const GroupRows gr = group_rows(hi, g);
         const int B = gr.bits;
         const int qbi = (1 << (B - 1)) - 1;
+        const float iq = P.lv.iq[B == 8 ? 0 : (B == 4 ? 1 : 2)];     // q = level * iq
         const uint32_t fmask = (1u << B) - 1u;
         if constexpr (OP == TileOp::Load || OP == TileOp::Import) {
             uint32_t word = 0;
@@ -377,7 +378,7 @@ __global__ __launch_bounds__(256) void tile_kernel(TileArgs a)
                     if constexpr (OP == TileOp::Load) {
                         const float x = a.state[(tdk + i) * dv + j];
                         const float rc = a.r_in[tdk + i] * a.c_in[tdv + j];
-                        float y = __builtin_rintf((x * static_cast<float>(qbi)) / rc);
+                        float y = __builtin_rintf((x * iq) / rc);
                         y = fminf(fmaxf(y, -static_cast<float>(qbi)), static_cast<float>(qbi));
                         code = static_cast<int>(y);
                     } else {
@@ -400,7 +401,7 @@ __global__ __launch_bounds__(256) void tile_kernel(TileArgs a)
                     if constexpr (OP == TileOp::Export) {
                         a.codes_out[(tdk + i) * dv + j] = static_cast<int8_t>(f);
                     } else {
-                        a.deq_out[(tdk + i) * dv + j] = (rr[p] * cc[j]) * (static_cast<float>(f) / static_cast<float>(qbi));
+                        a.deq_out[(tdk + i) * dv + j] = (rr[p] * cc[j]) * (static_cast<float>(f) / iq);
                     }
                 }
             }

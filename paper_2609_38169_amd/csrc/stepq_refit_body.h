@@ -81,14 +81,20 @@ __device__ __forceinline__ float row_partial(const float *y, const float (&cc)[4
 }
 
 // Row slot x (physical row p, width bw, old scale r_p): r' from the lane
-// partials, written to the tile; h and W to LDS.  The row and column
+// partials, written to the tile; h and W to LDS.  The partials are sums (or
+// maxima) of c_j |y_ij| with y = X / (r c nu), nu the width's level step:
+// the mean |X_ij| is r nu sum / d_v, W = (w r' nu)^2, and the row-absmax
+// factor r' = r max / q_b puts the row's largest entry on the top level in
+// either normalisation.  The row and column
 // factors are formed with the hardware reciprocal and square root (about one
 // ulp each): every later step uses the stored fp32 values, so the codes stay
 // consistent with them.
 template <int DV, Refit MODE>
-__device__ __forceinline__ void refit_row(RefitShared<DV> &sh, int x, int p, int bw, float r_p, float *rr_out)
+__device__ __forceinline__ void refit_row(RefitShared<DV> &sh, int x, int p, int bw, float r_p, float *rr_out,
+                                          const LevelTable &lv)
 {
-    const float iq = bw == 8 ? (1.0f / 127.0f) : (bw == 4 ? (1.0f / 7.0f) : 1.0f);
+    const float iq = bw == 8 ? (1.0f / 127.0f) : (bw == 4 ? (1.0f / 7.0f) : 1.0f);     // 1 / q_b
+    const float nu = lv.nu[bw == 8 ? 0 : (bw == 4 ? 1 : 2)];
     if constexpr (MODE == Refit::RowAbsmax) {
         float mx = 0.f;
 #pragma unroll
@@ -107,11 +113,11 @@ __device__ __forceinline__ void refit_row(RefitShared<DV> &sh, int x, int p, int
         const float4 v4 = *reinterpret_cast<const float4 *>(&sh.u.rowp[x][l]);
         sum += (v4.x + v4.y) + (v4.z + v4.w);
     }
-    const float m = (r_p * iq) * (sum * (1.0f / static_cast<float>(DV)));
+    const float m = (r_p * nu) * (sum * (1.0f / static_cast<float>(DV)));
     const float w = sh.wphys[p];
     const float rn = fmaxf(__builtin_amdgcn_sqrtf(m * __builtin_amdgcn_rcpf(w)), kScaleFloor);
     sh.hrow[x] = r_p * __builtin_amdgcn_rcpf(rn);
-    const float t = (w * rn) * iq;
+    const float t = (w * rn) * nu;
     sh.wrow[x] = t * t;
     rr_out[p] = rn;
 }
@@ -278,7 +284,7 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
         sh.ccol[tid] = op.c;
         sh.wphys[tid] = a.pool.roww[t.h * 128 + tid];
     }
-    const float kappa = row_constants_uniform<DIAG, M8, M4, 128>(t.beta, op, sh.d);
+    const float kappa = row_constants_uniform<DIAG, M8, M4, 128>(t.beta, op, sh.d, a.pool.lv);
 
     uint32_t U[NE / 2];
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
@@ -310,7 +316,7 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
         word_y<2, DIAG, MODE>(&U[2 * M8 + 4 * M4 + 8 * m], sh, X2 + 4 * (slice + 8 * m), cg,
                               t.alpha * (1.0f / 64.0f), bc, cc, &Y[Y2 + 16 * m]);
     __syncthreads();
-    if (tid < 128) refit_row<128, MODE>(sh, tid, tid, tid < X4 ? 8 : (tid < X2 ? 4 : 2), op.r, rr_out);
+    if (tid < 128) refit_row<128, MODE>(sh, tid, tid, tid < X4 ? 8 : (tid < X2 ? 4 : 2), op.r, rr_out, a.pool.lv);
     if constexpr (MODE == Refit::RowAbsmax) {
         if (tid < 128) cc_out[tid] = 1.0f;
     }
@@ -445,7 +451,7 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
     const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
     if (tid < DV) sh.ccol[tid] = op.c;
     if (tid < dk) sh.wphys[tid] = a.pool.roww[t.h * dk + tid];
-    const float kappa = row_constants<DIAG, DV>(t.hi, dk, t.alpha, t.beta, op, sh.d);
+    const float kappa = row_constants<DIAG, DV>(t.hi, dk, t.alpha, t.beta, op, sh.d, a.pool.lv);
 
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
     each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {
@@ -473,7 +479,7 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
         int bw;
         const int p = slot_row(t.hi, tid, bw);
         if (p >= 0) {
-            refit_row<DV, MODE>(sh, tid, p, bw, sh.d.sr[p], rr_out);
+            refit_row<DV, MODE>(sh, tid, p, bw, sh.d.sr[p], rr_out, a.pool.lv);
         } else {
             sh.hrow[tid] = 0.f;
             sh.wrow[tid] = 0.f;

@@ -17,7 +17,7 @@
 namespace {
 
 void fit_tiles(int64_t t0, int64_t t1, int32_t dk, int32_t dv, const float *S, const float *w, const uint8_t *bits,
-               float *r, float *c)
+               int levels, float *r, float *c)
 {
     const double fl = std::ldexp(1.0, -60);
     std::vector<double> rd(dk);
@@ -41,8 +41,14 @@ void fit_tiles(int64_t t0, int64_t t1, int32_t dk, int32_t dv, const float *S, c
             if (bits && bits[t * dk + i] == 16) continue;    // pivot rows keep their own values
             const float *row = St + static_cast<int64_t>(i) * dv;
             const double inv = rd[i];
+            double top = 1.0;                        // the width's top level: 1 (N1), 2^(8-b) q_b (N2)
+            if (levels == STEPQ_LEVELS_POW2) {
+                const int b = bits[t * dk + i];
+                top = static_cast<double>((1 << (b - 1)) - 1) * std::ldexp(1.0, 8 - b);
+            }
             for (int j = 0; j < dv; ++j) {
-                const double a = std::fabs(static_cast<double>(row[j])) / inv;
+                double a = std::fabs(static_cast<double>(row[j])) / inv;
+                if (levels == STEPQ_LEVELS_POW2) a /= top;
                 if (a > cmax[j]) cmax[j] = a;
             }
         }
@@ -160,13 +166,26 @@ stepq_status stepq_setup_fit_ex(int64_t n_tiles, int32_t d_k, int32_t d_v, const
                                 const float *row_weight, const uint8_t *row_bits, float *r, float *c,
                                 int32_t n_threads)
 {
+    return stepq_setup_fit_levels(n_tiles, d_k, d_v, state, row_weight, row_bits, STEPQ_LEVELS_ABSMAX, r, c,
+                                  n_threads);
+}
+
+stepq_status stepq_setup_fit_levels(int64_t n_tiles, int32_t d_k, int32_t d_v, const float *state,
+                                    const float *row_weight, const uint8_t *row_bits, int32_t levels, float *r,
+                                    float *c, int32_t n_threads)
+{
     if (n_tiles < 0 || d_k < 1 || d_v < 1) return STEPQ_E_INVALID;
+    if (levels != STEPQ_LEVELS_ABSMAX && levels != STEPQ_LEVELS_POW2) return STEPQ_E_INVALID;
+    if (levels == STEPQ_LEVELS_POW2 && n_tiles > 0 && !row_bits) return STEPQ_E_INVALID;
+    if (row_bits)
+        for (int64_t e = 0; e < n_tiles * d_k; ++e)
+            if (row_bits[e] != 2 && row_bits[e] != 4 && row_bits[e] != 8 && row_bits[e] != 16) return STEPQ_E_INVALID;
     if (n_tiles == 0) return STEPQ_OK;
     if (!state || !r || !c) return STEPQ_E_INVALID;
     int nt = n_threads > 0 ? n_threads : static_cast<int>(std::max(1u, std::thread::hardware_concurrency()));
     nt = static_cast<int>(std::min<int64_t>(nt, n_tiles));
     if (nt <= 1) {
-        fit_tiles(0, n_tiles, d_k, d_v, state, row_weight, row_bits, r, c);
+        fit_tiles(0, n_tiles, d_k, d_v, state, row_weight, row_bits, levels, r, c);
         return STEPQ_OK;
     }
     std::vector<std::thread> pool;
@@ -174,7 +193,7 @@ stepq_status stepq_setup_fit_ex(int64_t n_tiles, int32_t d_k, int32_t d_v, const
     for (int k = 0; k < nt; ++k) {
         const int64_t t0 = k * per, t1 = std::min<int64_t>(n_tiles, t0 + per);
         if (t0 >= t1) break;
-        pool.emplace_back(fit_tiles, t0, t1, d_k, d_v, state, row_weight, row_bits, r, c);
+        pool.emplace_back(fit_tiles, t0, t1, d_k, d_v, state, row_weight, row_bits, levels, r, c);
     }
     for (auto &th : pool) th.join();
     return STEPQ_OK;

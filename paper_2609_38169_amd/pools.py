@@ -19,18 +19,21 @@ def row_bits(w: W.Workload, layer: int = 0) -> np.ndarray:
 
 
 def build_pool(w: W.Workload, layer: int = 0, device="cuda", chunk: int = 128, n_threads: int = 0,
-               bits: np.ndarray | None = None) -> stepq.Pool:
+               bits: np.ndarray | None = None, levels: int = stepq.STEPQ_LEVELS_ABSMAX) -> stepq.Pool:
     """Allocate a pool for one layer of ``w`` and fill every slot from its
     seeded initial state.  States are drawn on ``device`` ``chunk`` slots at a
-    time, fitted on the host and packed on the device."""
+    time, fitted on the host (in the pool's level normalisation) and packed
+    on the device."""
     dev = torch.device(device)
     b = row_bits(w, layer) if bits is None else bits
-    pool = stepq.Pool(w.n_slots, w.n_v_heads, w.n_qk_heads, w.d_k, w.d_v, b, device=dev)
+    pool = stepq.Pool(w.n_slots, w.n_v_heads, w.n_qk_heads, w.d_k, w.d_v, b, device=dev, levels=levels)
     for s0 in range(0, w.n_slots, chunk):
         slots = range(s0, min(w.n_slots, s0 + chunk))
         S = W.initial_state(w, layer, slots, device=dev)
+        need_bits = np.any(b == 16) or levels != stepq.STEPQ_LEVELS_ABSMAX
         r, c = stepq.stepq_setup_fit(S.cpu(), n_threads=n_threads,
-                                     row_bits=np.broadcast_to(b, (len(slots),) + b.shape) if np.any(b == 16) else None)
+                                     row_bits=np.broadcast_to(b, (len(slots),) + b.shape) if need_bits else None,
+                                     levels=levels)
         ids = torch.arange(slots.start, slots.stop, dtype=torch.int32, device=dev)
         pool.load(ids, S, torch.from_numpy(r).to(dev), torch.from_numpy(c).to(dev))
         del S

@@ -20,6 +20,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("STEPQ_LIB") or os.path.join(_HERE, "libstepq.so")
 
 STEPQ_F32, STEPQ_BF16 = 0, 1
+STEPQ_LEVELS_ABSMAX, STEPQ_LEVELS_POW2 = 0, 1     # N1: z = q / q_b;  N2: z = 2^(8-b) q
 STEPQ_STEP_KDA_GATE, STEPQ_STEP_REFIT, STEPQ_STEP_ROW_ABSMAX = 1, 2, 4
 _STATUS = {0: "STEPQ_OK", 1: "STEPQ_E_INVALID", 2: "STEPQ_E_UNSUPPORTED", 3: "STEPQ_E_NOMEM", 4: "STEPQ_E_HIP"}
 
@@ -28,7 +29,7 @@ EXPORTED = (
     "stepq_pool_load", "stepq_decode_step", "stepq_decode_step_kda", "stepq_decode_step_ex",
     "stepq_pool_set_row_weight", "stepq_pool_dequant", "stepq_pool_export", "stepq_pool_import",
     "stepq_pool_export_pivots", "stepq_pool_import_pivots", "stepq_last_error", "stepq_setup_fit",
-    "stepq_setup_fit_ex", "stepq_setup_lifetime_bits", "stepq_setup_row_impact", "stepq_setup_distortion",
+    "stepq_setup_fit_ex", "stepq_setup_fit_levels", "stepq_setup_lifetime_bits", "stepq_setup_row_impact", "stepq_setup_distortion",
     "stepq_setup_lifetime_weights", "stepq_setup_allocate", "stepq_setup_select_pivots",
 )
 
@@ -41,7 +42,8 @@ class StepqError(RuntimeError):
 
 class stepq_pool_desc(ctypes.Structure):
     _fields_ = [("n_slots", ctypes.c_int32), ("n_v_heads", ctypes.c_int32), ("n_qk_heads", ctypes.c_int32),
-                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("row_bits", ctypes.c_void_p)]
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("row_bits", ctypes.c_void_p),
+                ("levels", ctypes.c_int32)]
 
 
 _lib = None
@@ -72,6 +74,7 @@ def lib():
             "stepq_pool_export_pivots": ([P, P, i32, P, P], st),
             "stepq_pool_import_pivots": ([P, P, i32, P, P], st),
             "stepq_setup_fit_ex": ([i64, i32, i32, P, P, P, P, P, i32], st),
+            "stepq_setup_fit_levels": ([i64, i32, i32, P, P, P, i32, P, P, i32], st),
             "stepq_setup_row_impact": ([i64, i32, i32, P, P, P, P, i32, ctypes.c_double, P, P], st),
             "stepq_setup_distortion": ([i64, i32, i32, i32, P, P, P, i32, P, i32, P, i32], st),
             "stepq_setup_lifetime_weights": ([i32, P, i32, P], st),
@@ -116,18 +119,18 @@ def _dev(t: torch.Tensor, name: str, dtype, shape, device):
     return ctypes.c_void_p(t.data_ptr())
 
 
-def _desc(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits: np.ndarray):
+def _desc(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits: np.ndarray, levels: int = STEPQ_LEVELS_ABSMAX):
     bits = np.ascontiguousarray(row_bits, dtype=np.uint8)
     if bits.shape != (n_v_heads, d_k):
         raise ValueError(f"row_bits has shape {bits.shape}, expected {(n_v_heads, d_k)}")
-    d = stepq_pool_desc(n_slots, n_v_heads, n_qk_heads, d_k, d_v, bits.ctypes.data_as(ctypes.c_void_p))
+    d = stepq_pool_desc(n_slots, n_v_heads, n_qk_heads, d_k, d_v, bits.ctypes.data_as(ctypes.c_void_p), int(levels))
     return d, bits
 
 
 # ---------------------------------------------------------------------------
 # C-ABI functions under their own names
-def stepq_pool_bytes(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits):
-    d, _keep = _desc(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits)
+def stepq_pool_bytes(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits, levels=STEPQ_LEVELS_ABSMAX):
+    d, _keep = _desc(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits, levels)
     pb, sb = ctypes.c_size_t(), ctypes.c_size_t()
     _check(lib().stepq_pool_bytes(ctypes.byref(d), ctypes.byref(pb), ctypes.byref(sb)))
     return pb.value, sb.value
@@ -136,16 +139,19 @@ def stepq_pool_bytes(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits):
 class Pool:
     """A state pool whose memory is a torch uint8 tensor on the current device."""
 
-    def __init__(self, n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits, device=None):
+    def __init__(self, n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits, device=None,
+                 levels=STEPQ_LEVELS_ABSMAX):
         self.device = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
         self.n_slots, self.Hv, self.Hqk, self.dk, self.dv = n_slots, n_v_heads, n_qk_heads, d_k, d_v
+        self.levels = int(levels)
         self.row_bits = np.ascontiguousarray(row_bits, dtype=np.uint8).copy()
-        self.pool_bytes, self.slot_bytes = stepq_pool_bytes(n_slots, n_v_heads, n_qk_heads, d_k, d_v, self.row_bits)
+        self.pool_bytes, self.slot_bytes = stepq_pool_bytes(n_slots, n_v_heads, n_qk_heads, d_k, d_v, self.row_bits,
+                                                            self.levels)
         with torch.cuda.device(self.device):
             self.memory = torch.empty(self.pool_bytes, dtype=torch.uint8, device=self.device)
             if self.memory.data_ptr() % 256:
                 raise RuntimeError("torch returned pool memory that is not 256-byte aligned")
-            d, _keep = _desc(n_slots, n_v_heads, n_qk_heads, d_k, d_v, self.row_bits)
+            d, _keep = _desc(n_slots, n_v_heads, n_qk_heads, d_k, d_v, self.row_bits, self.levels)
             h = ctypes.c_void_p()
             _check(lib().stepq_pool_create(ctypes.byref(d), ctypes.c_void_p(self.memory.data_ptr()),
                                            self.pool_bytes, ctypes.byref(h)))
@@ -359,9 +365,10 @@ def stepq_last_error() -> str:
 
 # ---------------------------------------------------------------------------
 # CPU setup step (host arrays)
-def stepq_setup_fit(state, row_weight=None, n_threads: int = 0, row_bits=None):
+def stepq_setup_fit(state, row_weight=None, n_threads: int = 0, row_bits=None, levels=STEPQ_LEVELS_ABSMAX):
     """state: [..., d_k, d_v] float32 (host) -> (r [..., d_k], c [..., d_v]) float32 numpy.
-    row_bits [..., d_k] (optional): pivot rows (16) are left out of c."""
+    row_bits [..., d_k] (optional under N1, needed under N2): pivot rows (16)
+    are left out of c; levels: the pool's level normalisation."""
     S = np.ascontiguousarray(state.numpy() if isinstance(state, torch.Tensor) else state, dtype=np.float32)
     dk, dv = S.shape[-2:]
     lead = S.shape[:-2]
@@ -372,7 +379,12 @@ def stepq_setup_fit(state, row_weight=None, n_threads: int = 0, row_bits=None):
     if row_weight is not None:
         w = np.ascontiguousarray(np.broadcast_to(row_weight, lead + (dk,)), dtype=np.float32)
     vp = lambda a: None if a is None else a.ctypes.data_as(ctypes.c_void_p)
-    if row_bits is None:
+    if levels != STEPQ_LEVELS_ABSMAX:
+        if row_bits is None:
+            raise ValueError("the N2 fit needs the row widths")
+        b = np.ascontiguousarray(np.broadcast_to(row_bits, lead + (dk,)), dtype=np.uint8)
+        _check(lib().stepq_setup_fit_levels(n, dk, dv, vp(S), vp(w), vp(b), int(levels), vp(r), vp(c), n_threads))
+    elif row_bits is None:
         _check(lib().stepq_setup_fit(n, dk, dv, vp(S), vp(w), vp(r), vp(c), n_threads))
     else:
         b = np.ascontiguousarray(np.broadcast_to(row_bits, lead + (dk,)), dtype=np.uint8)

@@ -170,17 +170,18 @@ class Lockstep:
     ``check_rows`` (batch rows whose slots are compared each step)."""
 
     def __init__(self, w: W.Workload, pool, slots: torch.Tensor, bits: np.ndarray, check_rows: np.ndarray,
-                 S0_check: np.ndarray, layer: int = 0, refit=False, row_weight=None):
+                 S0_check: np.ndarray, layer: int = 0, refit=False, row_weight=None, levels: int = 0):
         self.w, self.pool, self.slots, self.bits, self.layer = w, pool, slots, bits, layer
         self.refit = refit
+        self.lv = dict(levels=levels)
         self.tie_cols = 0
         self.rows = np.asarray(check_rows)
         n = len(self.rows) * w.n_v_heads
         self.tile_bits = np.broadcast_to(bits[None], (len(self.rows),) + bits.shape).reshape(n, w.d_k)
         S = S0_check.reshape(n, w.d_k, w.d_v)
         self.pivots = bool(np.any(bits == 16))
-        self.r, self.c = oracle.fit_absmax(S, bits=self.tile_bits)
-        q = oracle.quantize(S.astype(np.float64), self.r, self.c, self.tile_bits)
+        self.r, self.c = oracle.fit_absmax(S, bits=self.tile_bits, **self.lv)
+        q = oracle.quantize(S.astype(np.float64), self.r, self.c, self.tile_bits, **self.lv)
         self.codes, self.pv = (q[0], q[1]) if self.pivots else (q, None)
         self.piv_mismatches = 0
         dev = pool.device
@@ -230,7 +231,7 @@ class Lockstep:
         pmask = self.tile_bits == 16
         if self.refit == "row_absmax":
             res = oracle.decode_step_rowmax(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True,
-                                            **pvk)
+                                            **pvk, **self.lv)
             new, rn, cn, o, y = res[:5]
             if self.pivots:
                 self.piv_mismatches += compare_pivots(self.g_pv, res[5], y, pmask, f"step {step} pivots")
@@ -246,7 +247,8 @@ class Lockstep:
             self.compared += g_codes.size
         elif self.refit:
             res = oracle.decode_step_refit(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b,
-                                           w=self.row_w, want=("y", "c_range"), tie_window=TIE_WINDOW, **pvk)
+                                           w=self.row_w, want=("y", "c_range"), tie_window=TIE_WINDOW, **pvk,
+                                           **self.lv)
             new, rn, cn, o, ex = res[:5]
             if self.pivots:
                 self.piv_mismatches += compare_pivots(self.g_pv, res[5], ex["y"], pmask, f"step {step} pivots")
@@ -259,7 +261,8 @@ class Lockstep:
             self.r, self.c = rn, cn
             self.compared += g_codes.size
         else:
-            res = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True, **pvk)
+            res = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True, **pvk,
+                                     **self.lv)
             new, o, y = res[:3]
             if self.pivots:
                 self.piv_mismatches += compare_pivots(self.g_pv, res[3], y, pmask, f"step {step} pivots")
@@ -278,19 +281,19 @@ class Lockstep:
 
 
 def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, mutate=None, kda: bool = False,
-                 refit=False, row_weight=None, say=print, bits=None):
+                 refit=False, row_weight=None, say=print, bits=None, levels: int = 0):
     """Full-size decode steps of one workload layer on the GPU, the rows
     ``check_rows`` compared lockstep with the oracle at every step."""
     from paper_2609_38169_amd.pools import build_pool, row_bits
     bits = row_bits(w, layer) if bits is None else bits
     say(f"lockstep {w.name}: building pool ({w.n_slots} slots)")
-    pool = build_pool(w, layer, device=device, bits=bits)
+    pool = build_pool(w, layer, device=device, bits=bits, levels=levels)
     if row_weight is not None:
         pool.set_row_weight(row_weight)
     slots = W.active_slots(w).to(device)
     check_slots = W.active_slots(w)[np.asarray(check_rows)]
     S0 = W.initial_state(w, layer, [int(x) for x in check_slots], device=device).cpu().numpy()
-    ls = Lockstep(w, pool, slots, bits, check_rows, S0, layer, refit=refit, row_weight=row_weight)
+    ls = Lockstep(w, pool, slots, bits, check_rows, S0, layer, refit=refit, row_weight=row_weight, levels=levels)
     o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=device)
     for t in range(steps):
         inp = W.step_inputs(w, layer, t, device=device)
@@ -311,7 +314,7 @@ def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, 
         n_piv = int(np.count_nonzero(ls.tile_bits == 16)) * w.d_v * steps
         assert ls.piv_mismatches <= PIVOT_MISMATCH_FRAC * n_piv + 1, \
             f"{ls.piv_mismatches} of {n_piv} pivot values differ over the run"
-    mode = {False: "", True: " refit", "row_absmax": " row-absmax"}[refit]
+    mode = {False: "", True: " refit", "row_absmax": " row-absmax"}[refit] + (" N2 levels" if levels else "")
     say(f"lockstep {w.name}{' kda' if kda else ''}{mode}: {steps} steps ok, "
         f"code mismatches {ls.mismatches}, pivot mismatches {ls.piv_mismatches}, "
         f"columns on another tie rounding {ls.tie_cols}, "

@@ -43,20 +43,22 @@ def _bits(rng, mixes):
     return np.stack(rows)
 
 
+@pytest.mark.parametrize("levels", [stepq.STEPQ_LEVELS_ABSMAX, stepq.STEPQ_LEVELS_POW2])
 @pytest.mark.parametrize("mode", ["frozen", "refit", "row_absmax"])
 @pytest.mark.parametrize("kda", [False, True])
 @pytest.mark.parametrize("mix", list(MIXES))
-def test_layout_classes_one_step(mix, mode, kda):
+def test_layout_classes_one_step(mix, mode, kda, levels):
     Hv, Hqk, dk, dv, n_slots = len(MIXES[mix]), 4, 128, 128, 6
     rng = np.random.default_rng(900 + 100 * list(MIXES).index(mix) + 10 * ["frozen", "refit", "row_absmax"].index(mode)
-                                + int(kda))
+                                + int(kda) + 1000 * levels)
     bits = _bits(rng, MIXES[mix])
-    _say(f"layout classes {mix}: mode={mode} kda={kda} Hv={Hv} n_slots={n_slots}")
+    lv = dict(levels=levels)
+    _say(f"layout classes {mix}: mode={mode} kda={kda} levels={levels} Hv={Hv} n_slots={n_slots}")
     S = (rng.standard_normal((n_slots, Hv, dk, dv)) * 0.05).astype(np.float32)
-    r, c = oracle.fit_absmax(S.reshape(-1, dk, dv))
     tb_all = np.broadcast_to(bits[None], (n_slots,) + bits.shape).reshape(-1, dk)
-    codes = oracle.quantize(S.reshape(-1, dk, dv).astype(np.float64), r, c, tb_all)
-    pool = stepq.Pool(n_slots, Hv, Hqk, dk, dv, bits, device=DEV)
+    r, c = oracle.fit_absmax(S.reshape(-1, dk, dv), bits=tb_all, **lv)
+    codes = oracle.quantize(S.reshape(-1, dk, dv).astype(np.float64), r, c, tb_all, **lv)
+    pool = stepq.Pool(n_slots, Hv, Hqk, dk, dv, bits, device=DEV, levels=levels)
     all_ids = torch.arange(n_slots, dtype=torch.int32, device=DEV)
     pool.import_(all_ids, torch.from_numpy(codes.reshape(n_slots, Hv, dk, dv)).to(DEV),
                  torch.from_numpy(r.reshape(n_slots, Hv, dk)).to(DEV),
@@ -89,23 +91,23 @@ def test_layout_classes_one_step(mix, mode, kda):
     vv, bb = f32(v).reshape(-1, dv), f32(be).reshape(-1)
     gt = f32(gate).reshape((-1, dk) if kda else (-1,))
     tiles = (sel[:, None] * Hv + np.arange(Hv)[None]).reshape(-1)
-    what = f"layout classes {mix} {mode} kda={kda}"
+    what = f"layout classes {mix} {mode} kda={kda} levels={levels}"
     gcodes = got.reshape(-1, dk, dv)[tiles]
     if mode == "frozen":
         new, o_ref, y = oracle.decode_step(codes[tiles], r[tiles], c[tiles], tb_all[tiles], qq, kk, vv, gt, bb,
-                                           want_y=True)
+                                           want_y=True, **lv)
         PT.compare_codes(gcodes, new, y, what)
         assert np.array_equal(gr.reshape(-1, dk)[tiles], r[tiles])
         assert np.array_equal(gc.reshape(-1, dv)[tiles], c[tiles])
     elif mode == "refit":
         new, rn, cn, o_ref, ex = oracle.decode_step_refit(codes[tiles], r[tiles], c[tiles], tb_all[tiles], qq, kk,
                                                           vv, gt, bb, want=("y", "c_range"),
-                                                          tie_window=PT.TIE_WINDOW)
+                                                          tie_window=PT.TIE_WINDOW, **lv)
         PT.compare_refit(gcodes, gr.reshape(-1, dk)[tiles], gc.reshape(-1, dv)[tiles], new, rn, cn, ex["y"],
                          ex["c_range"], tb_all[tiles], what)
     else:
         new, rn, cn, o_ref, y = oracle.decode_step_rowmax(codes[tiles], r[tiles], c[tiles], tb_all[tiles], qq, kk,
-                                                          vv, gt, bb, want_y=True)
+                                                          vv, gt, bb, want_y=True, **lv)
         ones = np.ones(cn.shape)
         PT.compare_refit(gcodes, gr.reshape(-1, dk)[tiles], gc.reshape(-1, dv)[tiles], new, rn, cn, y,
                          (ones, ones), tb_all[tiles], what)

@@ -123,6 +123,16 @@ def test_setup_fit_matches_oracle(idx):
     r2, c2 = oracle.fit_absmax(S.reshape(-1, w.d_k, w.d_v), wts.reshape(-1, w.d_k).astype(np.float64),
                                bits=bits.reshape(-1, w.d_k))
     assert np.array_equal(r1.reshape(r2.shape), r2) and np.array_equal(c1.reshape(c2.shape), c2)
+    # the N2 level normalisation (top level 2^(8-b) q_b per width)
+    bits = np.random.default_rng(3).choice([2, 4, 8, 16], size=S.shape[:-1]).astype(np.uint8)
+    r1, c1 = stepq.stepq_setup_fit(S, wts, row_bits=bits, levels=stepq.STEPQ_LEVELS_POW2, n_threads=2)
+    r2, c2 = oracle.fit_absmax(S.reshape(-1, w.d_k, w.d_v), wts.reshape(-1, w.d_k).astype(np.float64),
+                               bits=bits.reshape(-1, w.d_k), levels=oracle.LEVELS_POW2)
+    assert np.array_equal(r1.reshape(r2.shape), r2) and np.array_equal(c1.reshape(c2.shape), c2)
+    with pytest.raises(ValueError):
+        stepq.stepq_setup_fit(S, levels=stepq.STEPQ_LEVELS_POW2)
+    with pytest.raises(stepq.StepqError):
+        stepq.stepq_pool_bytes(2, 4, 4, 16, 64, np.full((4, 16), 8, np.uint8), levels=7)
 
 
 def test_lifetime_bits_match_oracle():
