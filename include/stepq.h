@@ -12,7 +12,10 @@
  *   X     = alpha S^ + beta k (v - alpha S^T k)^T   gated Delta update
  *   o     = X^T q                                  readout, taken before requantization
  *   q'_ij = clip(round(X_ij q_{b_i} / (r_i c_j)), -q_{b_i}, q_{b_i})   round = ties-to-even
- * and q' replaces q in place; r and c are left unchanged.
+ * and q' replaces q in place; r and c are left unchanged.  These are the
+ * formulas of the default level normalisation N1 (stepq_levels below); under
+ * N2 every q / q_b becomes 2^(8-b) q and every X q_b / (...) becomes
+ * X 2^(b-8) / (...).
  *
  * Conventions for every call:
  *  - Pointers named *_dev, and every array argument of the device calls, are
@@ -195,6 +198,9 @@ enum {
  * absmax INT-b baseline the paper compares against (Section 5.1): per key
  * row r'_i = max_j |X_ij| (floored at 2^-60), every c'_j = 1, and
  *   q'_ij = clip(round(X_ij q_b / r'_i), -q_b, q_b).
+ * (N1 formulas.  Under N2 the levels are 2^(8-b) q: the column start and the
+ * row-absmax factor divide by the top level 2^(8-b) q_b, and q_b / r' becomes
+ * 2^(b-8) / r' throughout, so the largest entry still lands on +-q_b.)
  * Unknown flags, or REFIT together with ROW_ABSMAX: STEPQ_E_INVALID. */
 stepq_status stepq_decode_step_ex(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
                                   const void *k, const void *v, const void *gate, const void *beta,
@@ -208,7 +214,8 @@ stepq_status stepq_decode_step_ex(stepq_pool *pool, const int32_t *slot_ids, int
 stepq_status stepq_pool_set_row_weight(stepq_pool *pool, const float *row_weight);
 
 /* Reconstruct S^_ij = r_i c_j z_ij (Section 4.3; z the level of the code in
- * the pool's normalisation, q / q_b under N1; pivot rows: their binary16 values) for n slots into out [n][Hv][d_k][d_v] fp32, logical row
+ * the pool's normalisation, q / q_b under N1; pivot rows: their binary16
+ * values) for n slots into out [n][Hv][d_k][d_v] fp32, logical row
  * order.  Computed in fp32. */
 stepq_status stepq_pool_dequant(const stepq_pool *pool, const int32_t *slot_ids, int32_t n, float *out,
                                 void *stream);
