@@ -168,7 +168,7 @@ def pool_case(args, w, mode, dev):
         bits = bits.copy()
         bits[W.pivot_head_draw(w, 0, args.fp16_heads).numpy()] = 16
     log(f"building the {w.n_slots}-slot pool")
-    pool = build_pool(w, device=dev, bits=bits)
+    pool = build_pool(w, device=dev, bits=bits, levels=args.levels)
     subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
     n_inp = min(w.steps, args.steps + args.warmup)
     inputs = [W.step_inputs(w, 0, t, device=dev) for t in range(n_inp)]
@@ -212,7 +212,7 @@ def stack_case(args, w, mode, dev):
     for L in range(w.layers):
         b = row_bits(w, L)
         bits0 = b if bits0 is None else bits0
-        pools.append(build_pool(w, L, device=dev, bits=b))
+        pools.append(build_pool(w, L, device=dev, bits=b, levels=args.levels))
         inp = W.step_inputs(w, L, 0, device=dev)
         if args.kda:
             inp["alpha"] = W.kda_gates(w, L, 0, device=dev)
@@ -268,6 +268,8 @@ def main():
                     help="requantize as the row-wise absmax INT-b baseline (row factors refit, column factors 1)")
     ap.add_argument("--pivots", action="store_true",
                     help="a seeded quarter of the heads keep 1-3 FP16 pivot rows (pool workloads)")
+    ap.add_argument("--levels", type=int, choices=[0, 1], default=0,
+                    help="level normalisation of the codes: 0 = N1 (q / q_b), 1 = N2 (2^(8-b) q, the KDA codebook)")
     ap.add_argument("--fp16-heads", type=int, default=0,
                     help="this many seeded value heads are kept entirely in FP16 (pool workloads)")
     args = ap.parse_args()
@@ -389,7 +391,8 @@ def main():
         "config": dict({"workload": case.workload,
                         "gate": "channel-wise d [B][Hv][d_k] (KDA)" if args.kda else "scalar alpha [B][Hv] (GDN)",
                         "scales": {True: "online dual-axis refit every step", "row_absmax": "row-wise absmax every "
-                                   "step (INT-b baseline)", False: "frozen"}[mode]}, **case.extra),
+                                   "step (INT-b baseline)", False: "frozen"}[mode],
+                        "levels": "N2: z = 2^(8-b) q" if args.levels else "N1: z = q / q_b"}, **case.extra),
         "GBps_state": state_gbps,
         "pct_hbm_peak": 100.0 * state_gbps / HBM_PEAK_GBPS,
         "roofline": {
