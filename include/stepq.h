@@ -29,6 +29,8 @@
  *    tile is rewritten in place by exactly one workgroup.  With the
  *    environment variable STEPQ_DEBUG=1 this is checked on the host (a
  *    synchronising copy of the ids) and violations return STEPQ_E_INVALID.
+ *  - One call handles at most 2^24 (slot, head) tiles (n x n_v_heads); larger
+ *    calls return STEPQ_E_UNSUPPORTED and are split by the caller.
  *  - Nothing is thrown across the ABI.  Invalid arguments return
  *    STEPQ_E_INVALID before anything is enqueued; a failing HIP call returns
  *    STEPQ_E_HIP.  stepq_last_error() describes the last failure of the

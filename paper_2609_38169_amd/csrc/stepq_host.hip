@@ -205,11 +205,17 @@ stepq_status check_slots(const stepq_pool *p, const int32_t *ids, int32_t n, hip
     return STEPQ_OK;
 }
 
+// One launch covers n x Hv tiles of 256 work-items, and a dispatch counts its
+// work-items in 32 bits.
+constexpr int64_t kMaxTilesPerCall = int64_t(1) << 24;
+
 stepq_status common_checks(const stepq_pool *p, const int32_t *ids, int32_t n)
 {
     if (!p) return fail(STEPQ_E_INVALID, "pool is NULL");
     if (n < 0) return fail(STEPQ_E_INVALID, "negative count");
     if (n > p->n_slots) return fail(STEPQ_E_INVALID, "more slots requested than the pool holds");
+    if (static_cast<int64_t>(n) * p->Hv > kMaxTilesPerCall)
+        return fail(STEPQ_E_UNSUPPORTED, "more than 2^24 (slot, head) tiles in one call: split the batch");
     if (n > 0 && !ids) return fail(STEPQ_E_INVALID, "slot_ids is NULL");
     return check_device(p);
 }
@@ -421,7 +427,7 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     };
     hipError_t e = hipSuccess;
     if (p->mixed_code != 0 && !(flags & (STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX))) {
-        // uniform heads and compact generic heads share one launch
+        // uniform heads share one launch with compact generic and whole FP16 heads
         a.head_list = p->d_head_order;
         a.n_heads = p->Hv;
         a.div_heads = fast_div(static_cast<uint32_t>(p->Hv));
