@@ -216,3 +216,31 @@ def test_calibrated_map_runs_lockstep():
     assert (bits == 16).sum() == 24 and bits[bits != 16].mean() <= 6.0
     _say(f"calibrated map: {(bits == 8).sum()} rows @8, {(bits == 4).sum()} @4, {(bits == 16).sum()} pivots")
     PT.lockstep_run(w, 8, np.arange(0, 64, 9), DEV, refit=True, row_weight=cal.row_weight, say=_say, bits=bits)
+
+
+def test_calibrated_head_map_runs_lockstep():
+    """The calibration pipeline with head units (the paper's recipe for its
+    GDN model: per-head widths by the multiple-choice DP, whole heads kept
+    in FP16 as pivots) on the stack48 workload's own draws: the map has
+    whole FP16 heads and 4/8-bit heads, and a pool built on it, refit with
+    the calibrated row factors, matches the oracle lockstep."""
+    from paper_2609_38169_amd.calibrate import calibrate
+    w = W.workload(4)
+    T = 6
+    steps = [W.step_inputs(w, 0, 1000 + t) for t in range(T)]        # calibration draws, not the test steps
+    g = w.n_v_heads // w.n_qk_heads
+    cat = lambda key: np.concatenate([s[key].float().numpy() for s in steps])
+    q = np.repeat(cat("q"), g, axis=1)
+    k = np.repeat(cat("k"), g, axis=1)
+    S = W.initial_state(w, 0, range(2)).float().numpy()
+    cal = calibrate(q, k, cat("beta"), cat("alpha"), S, budget=6.0, cand_bits=(4, 8), unit="head",
+                    n_pivots=2, horizon=1024)
+    bits = cal.row_bits
+    full16 = (bits == 16).all(axis=1)
+    assert full16.sum() == 2 and ((bits == 16).any(axis=1) == full16).all()
+    per_head = [set(np.unique(b)) for b in bits]
+    assert all(len(h) == 1 for h in per_head)                          # one width per head
+    assert bits[~full16].mean() <= 6.0
+    _say(f"calibrated head map: {int((bits[:, 0] == 8).sum())} heads @8, {int((bits[:, 0] == 4).sum())} @4, "
+         f"{int(full16.sum())} FP16 heads")
+    PT.lockstep_run(w, 4, np.array([0, 100, 255]), DEV, refit=True, row_weight=cal.row_weight, say=_say, bits=bits)
