@@ -120,7 +120,8 @@ typedef struct {
 } stepq_pool_desc;
 
 /* Size of the pool described by desc (layout above).  Either output may be
- * NULL.  Host only, no device work. */
+ * NULL.  Host only, no device work.  STEPQ_E_UNSUPPORTED when one slot
+ * record would exceed 4 GiB (tile offsets inside a record are 32-bit). */
 stepq_status stepq_pool_bytes(const stepq_pool_desc *desc, size_t *pool_bytes, size_t *slot_bytes);
 
 /* Create a pool.  device_mem: caller-owned device memory of at least
@@ -128,7 +129,8 @@ stepq_status stepq_pool_bytes(const stepq_pool_desc *desc, size_t *pool_bytes, s
  * pool; or NULL, in which case the library allocates (and later frees) it.
  * The pool contents are undefined until written by stepq_pool_load or
  * stepq_pool_import.  Allocates the small per-head layout tables on the
- * current device.  Blocks until they are copied. */
+ * current device.  Blocks until they are copied.  STEPQ_E_NOMEM when an
+ * allocation fails, STEPQ_E_HIP when a copy does. */
 stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, size_t device_mem_bytes,
                                stepq_pool **out);
 

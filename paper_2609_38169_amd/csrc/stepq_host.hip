@@ -2,6 +2,7 @@
 // Argument checking, the per-head layout tables, launches.
 #include <algorithm>
 #include <cstdlib>
+#include <cstdint>
 #include <cstring>
 #include <string>
 #include <cmath>
@@ -126,6 +127,8 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
             (hi.piv_off != 0 || hi.r_off != 128u * 256u || hi.tile_bytes != 128u * 256u + 1024u))
             return fail(STEPQ_E_INVALID, "internal: FP16 head layout does not match its tile size");
         off += tb;
+        // tile offsets inside a slot record are 32-bit
+        if (off > UINT32_MAX) return fail(STEPQ_E_UNSUPPORTED, "slot record over 4 GiB: too many heads");
     }
     *slot_bytes = off;
     return STEPQ_OK;
@@ -344,7 +347,8 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
     }
     if (e != hipSuccess) {
         stepq_pool_destroy(p);
-        return fail(STEPQ_E_NOMEM, std::string("layout tables: ") + hipGetErrorString(e));
+        return fail(e == hipErrorOutOfMemory ? STEPQ_E_NOMEM : STEPQ_E_HIP,
+                    std::string("layout tables: ") + hipGetErrorString(e));
     }
     *out = p;
     return STEPQ_OK;

@@ -82,6 +82,8 @@ def test_whole_fp16_head_layout():
     (dict(n_slots=0), 1), (dict(n_v_heads=6, n_qk_heads=4), 1), (dict(d_k=129), 2), (dict(d_v=96), 2),
     (dict(bitval=3), 1), (dict(bitval=12), 1),
     (dict(bitval=16), 2),                       # 64 pivot rows per 64x64 head: more than the 32 supported
+    # 130,000 whole FP16 128x128 heads: a 4.4 GB slot record, past the 32-bit tile offsets
+    (dict(n_v_heads=130000, n_qk_heads=1, d_k=128, d_v=128, bitval=16), 2),
 ])
 def test_bad_descriptor_rejected(bad, status):
     a = dict(n_slots=2, n_v_heads=4, n_qk_heads=2, d_k=64, d_v=64)
