@@ -43,7 +43,10 @@ VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 # the refit adds the row-magnitude sum 1, rescale 1, column max 1, fixed code
 # 2 and the two least-squares sums 3.
 # The row-absmax baseline adds the row maximum 1 and the rescale 1.
+# The frozen step's compiled bodies run S^T k and S^T q on the matrix cores
+# (4x4x4 binary16 blocks), so 7 of its 9 operations are VALU work there.
 OPS_PER_ELEMENT = {False: 9, True: 17, "row_absmax": 11}
+MATRIX_CORE_OPS = {False: 2, True: 0, "row_absmax": 0}
 METRIC = "state-updates/s and achieved HBM GB/s (% of peak), B=512 heads=32 dk=dv=128"
 CSRC = os.path.join(ROOT, "paper_2609_38169_amd", "csrc")
 
@@ -367,7 +370,8 @@ def main():
     act_bytes = w.batch * (2 * w.n_qk_heads * w.d_k * 2 + w.n_v_heads * w.d_v * 2 + (gate_elems + w.n_v_heads) * 2
                            + w.n_v_heads * w.d_v * 4 + 4)
     achieved = launch_bytes / (kern_ms * 1e-3) / 1e9
-    valu_tops = w.batch * w.n_v_heads * w.d_k * w.d_v * OPS_PER_ELEMENT[mode] / (kern_ms * 1e-3) / 1e12
+    valu_ops = OPS_PER_ELEMENT[mode] - MATRIX_CORE_OPS[mode]
+    valu_tops = w.batch * w.n_v_heads * w.d_k * w.d_v * valu_ops / (kern_ms * 1e-3) / 1e12
     value = case.tiles_per_step * K / (total_ms * 1e-3)
     state_gbps = launch_bytes * LPS * K / (total_ms * 1e-3) / 1e9
     kern_name = ("refit_kernel" if rescale else "decode_kernel") + ("<128, bf16, kda" if args.kda else "<128, bf16")
@@ -403,7 +407,7 @@ def main():
             "frac": achieved / HBM_PEAK_GBPS,
             "traffic": traffic_entry(mode, args.kda, w.name, args.pivots) if not args.fp16_heads else None,
             "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Top/s", "frac": valu_tops / VALU_PEAK_TOPS,
-                     "ops_per_element": OPS_PER_ELEMENT[mode]},
+                     "ops_per_element": valu_ops, "matrix_core_ops_per_element": MATRIX_CORE_OPS[mode]},
             "kernel": kern_name,
             "kernel_ms_mean": kern_ms,
             "launches_per_step": LPS,
@@ -426,7 +430,8 @@ def main():
         hbm = {k: rl[k] for k in ("achieved", "peak", "unit", "frac")}
         valu = rl.pop("valu")
         rl.update({"bound": "alu", "achieved": valu["achieved"], "peak": valu["peak"], "unit": valu["unit"],
-                   "frac": valu["frac"], "ops_per_element": valu["ops_per_element"], "hbm": hbm})
+                   "frac": valu["frac"], "ops_per_element": valu["ops_per_element"],
+                   "matrix_core_ops_per_element": valu["matrix_core_ops_per_element"], "hbm": hbm})
     if args.copy_ref:
         src = torch.empty(launch_bytes // 2, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)

@@ -44,6 +44,18 @@ struct CodeWords {
     {
         __builtin_amdgcn_raw_buffer_store_b32(v, r, 4 * word, 0, kStore);
     }
+    // Word tid + 256 m with the per-m part of the byte offset in the
+    // instruction's immediate (m mod 4) and scalar (m / 4) offsets, so one
+    // address register serves every m.  All such words lie inside the
+    // record (the uniform bodies' tiles hold 256 words per m).
+    __device__ __forceinline__ uint32_t load_m(int tid, int m) const
+    {
+        return __builtin_amdgcn_raw_buffer_load_b32(r, 4 * tid + 1024 * (m & 3), 4096 * (m >> 2), kLoad);
+    }
+    __device__ __forceinline__ void store_m(int tid, int m, uint32_t v) const
+    {
+        __builtin_amdgcn_raw_buffer_store_b32(v, r, 4 * tid + 1024 * (m & 3), 4096 * (m >> 2), kStore);
+    }
 };
 
 // Workgroups are dispatched round-robin over the 8 XCDs.  Give each XCD a
@@ -124,6 +136,27 @@ __device__ __forceinline__ float dpp_term(float x)
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROWS, 0xF, false));
 }
 
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_bits(uint32_t x)
+{
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), CTRL, ROWS, 0xF, false));
+}
+
+// Largest value over the 64 lanes of a wavefront, for x >= 0 (lanes a DPP
+// step leaves out contribute 0); uniform result.  Non-negative floats order
+// as their bit patterns do, so the steps are integer maxima.
+__device__ __forceinline__ float wave_max(float x)
+{
+    uint32_t u = __float_as_uint(x);
+    u = max(u, dpp_bits<0xB1, 0xF>(u));
+    u = max(u, dpp_bits<0x4E, 0xF>(u));
+    u = max(u, dpp_bits<0x141, 0xF>(u));
+    u = max(u, dpp_bits<0x140, 0xF>(u));
+    u = max(u, dpp_bits<0x142, 0xA>(u));
+    u = max(u, dpp_bits<0x143, 0xC>(u));
+    return __uint_as_float(static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(u), 63)));
+}
+
 // Sum over the 64 lanes of a wavefront with DPP row operations; the result
 // is returned uniform (read from the last lane).
 __device__ __forceinline__ float wave_sum(float x)
@@ -156,6 +189,11 @@ struct DecodeShared {
     // (k_i d_i, q_i d_i, d_i, beta k_i) with d_i the row's gate (alpha for GDN)
     float4 pvc[kMaxPivots];
     float cpiv[DV];                      // c_j, for the pivot rows' share of S^T k and S^T q
+    // Uniform bodies: the row weights as binary16 A operands of the 4x4x4
+    // matrix-core blocks, [slice][row group][type][row in group], types
+    // 0/1 = k weight hi/lo, 2/3 = q weight hi/lo (prescaled by powers of two)
+    alignas(16) _Float16 aop[8][4][4][4];
+    float2 wmx[4];                       // per wavefront: largest |k weight|, |q weight|
 };
 
 struct TileCtx {
@@ -407,18 +445,116 @@ __device__ __forceinline__ float row_constants_uniform(float beta, const RowColO
     return (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
 }
 
+// Power-of-two exponent that brings the largest weight m into [2^14, 2^15),
+// where binary16 keeps its full precision and the hi/lo split below is
+// exact to 22 significant bits.
+__device__ __forceinline__ int weight_scale_exp(float m)
+{
+    const int e = __builtin_amdgcn_frexp_expf(m);   // m = f 2^e, f in [0.5, 1); 0 for m = 0
+    return min(max(15 - e, -126), 126);
+}
+
+// Uniform layouts with the two matrix-vector products on the matrix cores.
+// Row table slot = physical row = tid, as in row_constants_uniform; the k
+// and q weights of each row are split into binary16 hi + lo parts (after
+// the tile's prescales 2^ek, 2^eq) and written as the A operands of the
+// 4x4x4 blocks of the thread's slice: aop[slice][group][type][row in
+// group], the thread's 16 rows being its 8-bit rows, then the two slots of
+// each 4-bit word, then the four slots of each 2-bit word (4 to a group).
+// Two barriers; the operand table is complete only after one more.
+template <bool DIAG, int M8, int M4, int M2, int DV>
+__device__ __forceinline__ float row_constants_mfma(float beta, const RowColOps &op, DecodeShared<DV> &sh,
+                                                    const LevelTable &lv, int &ek, int &eq)
+{
+    constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
+    const int tid = threadIdx.x;
+    if (tid < 128) {
+        sh.sk[tid] = op.k;
+        sh.sq[tid] = op.q;
+        if constexpr (DIAG) sh.sd[tid] = op.d;
+    }
+    __syncthreads();
+    float kq = 0.f, kt = 0.f, qt = 0.f;
+    if (tid < 128) {
+        const int p = tid;
+        const int wi = p < X4 ? 0 : (p < X2 ? 1 : 2);
+        const float qb = lv.iq[wi];
+        const float fq = lv.fq[wi];
+        const float ki = sh.sk[op.perm];
+        const float qi = sh.sq[op.perm];
+        const float di = DIAG ? sh.sd[op.perm] : 1.0f;
+        const float rs = op.r * fq * di;
+        kt = ki * rs;
+        qt = qi * rs;
+        sh.av[p] = beta * ki * qb * __builtin_amdgcn_rcpf(op.r);
+        if constexpr (DIAG) sh.al[p] = di * (p < X4 ? 1.0f : (p < X2 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
+        kq = qi * ki;
+    }
+    kq = wave_sum(kq);
+    const float mk = wave_max(fabsf(kt)), mq = wave_max(fabsf(qt));
+    if ((tid & 63) == 0) {
+        sh.kap[tid >> 6] = kq;
+        sh.wmx[tid >> 6] = make_float2(mk, mq);
+    }
+    __syncthreads();
+    const float2 w0 = sh.wmx[0], w1 = sh.wmx[1];     // the rows live in wavefronts 0 and 1
+    ek = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(w0.x, w1.x)));
+    eq = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(w0.y, w1.y)));
+    const float kappa = (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
+    if (tid < 128) {
+        const int p = tid;
+        int slice, ridx;
+        if (p < X4) {
+            slice = p & 7;
+            ridx = p >> 3;
+        } else if (p < X2) {
+            const int c = (p - X4) >> 1;
+            slice = c & 7;
+            ridx = M8 + 2 * (c >> 3) + ((p - X4) & 1);
+        } else {
+            const int c = (p - X2) >> 2;
+            slice = c & 7;
+            ridx = M8 + 2 * M4 + 4 * (c >> 3) + ((p - X2) & 3);
+        }
+        const float ks = __builtin_amdgcn_ldexpf(kt, ek), qs = __builtin_amdgcn_ldexpf(qt, eq);
+        const _Float16 kh = static_cast<_Float16>(ks), qh = static_cast<_Float16>(qs);
+        const _Float16 kl = static_cast<_Float16>(ks - static_cast<float>(kh));
+        const _Float16 ql = static_cast<_Float16>(qs - static_cast<float>(qh));
+        _Float16(&dst)[4][4] = sh.aop[slice][ridx >> 2];
+        dst[0][ridx & 3] = kh;
+        dst[1][ridx & 3] = kl;
+        dst[2][ridx & 3] = qh;
+        dst[3][ridx & 3] = ql;
+    }
+    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(kappa)));
+}
+
 // Column sums of the per-thread partials, residual, readout, column factor
 // of the code-space update.  cj, vj: column tid's scale and value (threads
 // < DV, loaded at the start of the tile).  Ends with a barrier.
+template <int DV>
+__device__ __forceinline__ void column_sums(const DecodeArgs &a, int tile, float alpha, float beta,
+                                            DecodeShared<DV> &sh, float kappa, float cj, float vj);
+
 template <int DV>
 __device__ __forceinline__ void column_phase(const DecodeArgs &a, int tile, float alpha, float beta,
                                              DecodeShared<DV> &sh, float kappa, const float (&acK)[4],
                                              const float (&acQ)[4], float cj, float vj)
 {
-    constexpr int CG = DV / 4, NSL = 256 / CG;
+    constexpr int CG = DV / 4;
     const int tid = threadIdx.x;
     sh.red[0][tid / CG][tid % CG] = make_float4(acK[0], acK[1], acK[2], acK[3]);
     sh.red[1][tid / CG][tid % CG] = make_float4(acQ[0], acQ[1], acQ[2], acQ[3]);
+    column_sums<DV>(a, tile, alpha, beta, sh, kappa, cj, vj);
+}
+
+// The column phase once every thread has written its partials to sh.red.
+template <int DV>
+__device__ __forceinline__ void column_sums(const DecodeArgs &a, int tile, float alpha, float beta,
+                                            DecodeShared<DV> &sh, float kappa, float cj, float vj)
+{
+    constexpr int NSL = 256 / (DV / 4);
+    const int tid = threadIdx.x;
     __syncthreads();
     if (tid < DV) {
         const int j = tid;
@@ -521,6 +657,83 @@ __device__ __forceinline__ void unpack_acc_h(uint32_t w, const float2 *kq, int x
         acK[3] = fma_mix_e<3>(c.x, U2, s, acK[3]);
         acQ[3] = fma_mix_e<3>(c.y, U2, s, acQ[3]);
     }
+}
+
+// ---- row-pair layout of the uniform bodies' matrix-core path: register
+// Ub[e][g][h] holds column e of rows 4g + 2h (low half) and 4g + 2h + 1
+// (high half) of the thread's 16 rows, i.e. half of the B operand of the
+// 4x4x4 block for column e and row group g.
+
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// Byte E of lo_w and of hi_w, read as signed, to an f16 pair (exact).
+template <int E>
+__device__ __forceinline__ uint32_t sbyte_pair_f16(uint32_t lo_w, uint32_t hi_w)
+{
+    uint32_t r;
+    asm("v_cvt_f16_i16_sdwa %0, sext(%1) dst_sel:WORD_0 dst_unused:UNUSED_PAD src0_sel:BYTE_%c2"
+        : "=v"(r) : "v"(lo_w), "i"(E));
+    asm("v_cvt_f16_i16_sdwa %0, sext(%1) dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_%c2"
+        : "+v"(r) : "v"(hi_w), "i"(E));
+    return r;
+}
+
+// v_mfma_f32_4x4x4_16b_f16: 16 independent 4x4x4 products, block b on
+// lanes 4b .. 4b+3.  Lane 4b+i supplies row i of A (4 values along k),
+// lane 4b+j column j of B (4 values along k) and receives column j of
+// D = A B + C (4 values along i).
+__device__ __forceinline__ f32x4 mfma4x4x4(u32x2 a, uint32_t b0, uint32_t b1, f32x4 c)
+{
+    const u32x2 b{b0, b1};
+    return __builtin_amdgcn_mfma_f32_4x4x4f16(__builtin_bit_cast(f16x4, a), __builtin_bit_cast(f16x4, b), c, 0, 0,
+                                              0);
+}
+
+// New field in byte E of P from the old field in half HALF of hp; the same
+// arithmetic as requant_field.
+template <int B, int E, int HALF>
+__device__ __forceinline__ uint32_t requant_field_p(uint32_t hp, float al, float a_s, float bce, uint32_t P)
+{
+    constexpr float bias = static_cast<float>(1 << (B - 1));
+    constexpr float top = static_cast<float>((1 << B) - 1);
+    const float tt = fmaf(a_s, bce, bias);
+    float y = fma_mix<HALF>(al, hp, tt);
+    y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
+    return __builtin_amdgcn_cvt_pk_u8_f32(y, E, P);
+}
+
+template <int B, int HALF>
+__device__ __forceinline__ uint32_t requant_slot_p(const uint32_t (&Ub)[4][4][2], int g, int h, float al, float a_s,
+                                                   const float (&bc)[4])
+{
+    uint32_t P = 0;
+    P = requant_field_p<B, 0, HALF>(Ub[0][g][h], al, a_s, bc[0], P);
+    P = requant_field_p<B, 1, HALF>(Ub[1][g][h], al, a_s, bc[1], P);
+    P = requant_field_p<B, 2, HALF>(Ub[2][g][h], al, a_s, bc[2], P);
+    P = requant_field_p<B, 3, HALF>(Ub[3][g][h], al, a_s, bc[3], P);
+    return P;
+}
+
+// New word of 8/B slots (row-table slots x0 + s, thread rows r0 + s) from
+// the row-pair registers; as requant_word_h otherwise.  r0 is a constant
+// once the caller's loops are unrolled, so every register index folds.
+template <int B, bool DIAG>
+__device__ __forceinline__ uint32_t requant_word_p(const uint32_t (&Ub)[4][4][2], int r0, const float *av,
+                                                   const float *alt, int x0, float al_w, const float (&bc)[4])
+{
+    constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
+    uint32_t out = 0;
+#pragma unroll
+    for (int s = 0; s < 8 / B; ++s) {
+        const int r = r0 + s;
+        const float a_s = av[x0 + s];
+        const float al = DIAG ? alt[x0 + s] : al_w;
+        const uint32_t P = (r & 1) ? requant_slot_p<B, 1>(Ub, r >> 2, (r >> 1) & 1, al, a_s, bc)
+                                   : requant_slot_p<B, 0>(Ub, r >> 2, (r >> 1) & 1, al, a_s, bc);
+        out |= P << (s * B);
+    }
+    return out ^ flip;
 }
 
 template <int B, int E>
