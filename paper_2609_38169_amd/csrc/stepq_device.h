@@ -411,40 +411,6 @@ __device__ __forceinline__ void pivot_update(const TileCtx &t, int slice, int cg
     }
 }
 
-// Uniform layouts: table slot = physical row = tid, widths known at compile time.
-template <bool DIAG, int M8, int M4, int DV>
-__device__ __forceinline__ float row_constants_uniform(float beta, const RowColOps &op, DecodeShared<DV> &sh,
-                                                       const LevelTable &lv)
-{
-    constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
-    const int tid = threadIdx.x;
-    if (tid < 128) {
-        sh.sk[tid] = op.k;
-        sh.sq[tid] = op.q;
-        if constexpr (DIAG) sh.sd[tid] = op.d;
-    }
-    __syncthreads();
-    float kq = 0.f;
-    if (tid < 128) {
-        const int p = tid;
-        const int wi = p < X4 ? 0 : (p < X2 ? 1 : 2);
-        const float qb = lv.iq[wi];
-        const float fq = lv.fq[wi];
-        const float ki = sh.sk[op.perm];
-        const float qi = sh.sq[op.perm];
-        const float di = DIAG ? sh.sd[op.perm] : 1.0f;
-        const float rs = op.r * fq * di;
-        sh.kq[p] = make_float2(ki * rs, qi * rs);
-        sh.av[p] = beta * ki * qb * __builtin_amdgcn_rcpf(op.r);
-        if constexpr (DIAG) sh.al[p] = di * (p < X4 ? 1.0f : (p < X2 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
-        kq = qi * ki;
-    }
-    kq = wave_sum(kq);
-    if ((tid & 63) == 0) sh.kap[tid >> 6] = kq;
-    __syncthreads();
-    return (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
-}
-
 // Power-of-two exponent that brings the largest weight m into [2^14, 2^15),
 // where binary16 keeps its full precision and the hi/lo split below is
 // exact to 22 significant bits.
@@ -604,20 +570,7 @@ __device__ __forceinline__ void unpack_word(uint32_t w, float *U)
     }
 }
 
-// ---- codes kept as packed f16 pairs between the passes (exact: |2^(8-B) q| <= 127)
-
-// Bytes LO and HI of w, read as signed, to an f16 pair: one SDWA convert per
-// field, the second one writing the upper half in place.
-template <int LO, int HI>
-__device__ __forceinline__ uint32_t sbytes_f16(uint32_t w)
-{
-    uint32_t r;
-    asm("v_cvt_f16_i16_sdwa %0, sext(%1) dst_sel:WORD_0 dst_unused:UNUSED_PAD src0_sel:BYTE_%c2"
-        : "=v"(r) : "v"(w), "i"(LO));
-    asm("v_cvt_f16_i16_sdwa %0, sext(%1) dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:BYTE_%c2"
-        : "+v"(r) : "v"(w), "i"(HI));
-    return r;
-}
+// ---- codes kept as binary16 between the passes (exact: |2^(8-B) q| <= 127)
 
 // a * h + c with h the low (HI = 0) or high (HI = 1) f16 half of hp, in fp32
 // (v_fma_mix_f32: the half is widened exactly inside the FMA).
@@ -630,33 +583,6 @@ __device__ __forceinline__ float fma_mix(float a, uint32_t hp, float c)
     else
         asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel_hi:[0,1,0]" : "=v"(r) : "v"(a), "v"(hp), "v"(c));
     return r;
-}
-
-template <int E>
-__device__ __forceinline__ float fma_mix_e(float a, const uint32_t *U2, int s, float c)
-{
-    return fma_mix<E & 1>(a, U2[2 * s + (E >> 1)], c);
-}
-
-template <int B>
-__device__ __forceinline__ void unpack_acc_h(uint32_t w, const float2 *kq, int x0, uint32_t *U2, float (&acK)[4],
-                                             float (&acQ)[4])
-{
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float2 c = kq[x0 + s];
-        const uint32_t W = slot_top<B>(w, s);
-        U2[2 * s] = sbytes_f16<0, 1>(W);
-        U2[2 * s + 1] = sbytes_f16<2, 3>(W);
-        acK[0] = fma_mix_e<0>(c.x, U2, s, acK[0]);
-        acQ[0] = fma_mix_e<0>(c.y, U2, s, acQ[0]);
-        acK[1] = fma_mix_e<1>(c.x, U2, s, acK[1]);
-        acQ[1] = fma_mix_e<1>(c.y, U2, s, acQ[1]);
-        acK[2] = fma_mix_e<2>(c.x, U2, s, acK[2]);
-        acQ[2] = fma_mix_e<2>(c.y, U2, s, acQ[2]);
-        acK[3] = fma_mix_e<3>(c.x, U2, s, acK[3]);
-        acQ[3] = fma_mix_e<3>(c.y, U2, s, acQ[3]);
-    }
 }
 
 // ---- row-pair layout of the uniform bodies' matrix-core path: register
@@ -690,8 +616,73 @@ __device__ __forceinline__ f32x4 mfma4x4x4(u32x2 a, uint32_t b0, uint32_t b1, f3
                                               0);
 }
 
-// New field in byte E of P from the old field in half HALF of hp; the same
-// arithmetic as requant_field.
+// The thread's 16 rows (8-bit words, then the slots of the 4-bit and 2-bit
+// words) as row-pair f16 registers.
+template <int M8, int M4, int M2>
+__device__ __forceinline__ void unpack_row_pairs(const uint32_t (&w)[M8 + M4 + M2], uint32_t (&Ub)[4][4][2])
+{
+    static_assert(M8 + 2 * M4 + 4 * M2 == 16, "16 rows per thread");
+    static_assert(M8 % 4 == 0 && M4 % 2 == 0, "row groups of 4 hold rows of one width");
+    constexpr int G4 = M8 / 4, G2 = (M8 + 2 * M4) / 4;    // first row group of the 4- and 2-bit rows
+#pragma unroll
+    for (int g = 0; g < G4; ++g)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const uint32_t lo = w[4 * g + 2 * h], hi = w[4 * g + 2 * h + 1];
+            Ub[0][g][h] = sbyte_pair_f16<0>(lo, hi);
+            Ub[1][g][h] = sbyte_pair_f16<1>(lo, hi);
+            Ub[2][g][h] = sbyte_pair_f16<2>(lo, hi);
+            Ub[3][g][h] = sbyte_pair_f16<3>(lo, hi);
+        }
+#pragma unroll
+    for (int m = 0; m < M4; ++m) {
+        const uint32_t s0 = slot_top<4>(w[M8 + m], 0), s1 = slot_top<4>(w[M8 + m], 1);
+        const int g = G4 + m / 2, h = m & 1;
+        Ub[0][g][h] = sbyte_pair_f16<0>(s0, s1);
+        Ub[1][g][h] = sbyte_pair_f16<1>(s0, s1);
+        Ub[2][g][h] = sbyte_pair_f16<2>(s0, s1);
+        Ub[3][g][h] = sbyte_pair_f16<3>(s0, s1);
+    }
+#pragma unroll
+    for (int m = 0; m < M2; ++m) {
+        const uint32_t wm = w[M8 + M4 + m];
+        const int g = G2 + m;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const uint32_t s0 = slot_top<2>(wm, 2 * h), s1 = slot_top<2>(wm, 2 * h + 1);
+            Ub[0][g][h] = sbyte_pair_f16<0>(s0, s1);
+            Ub[1][g][h] = sbyte_pair_f16<1>(s0, s1);
+            Ub[2][g][h] = sbyte_pair_f16<2>(s0, s1);
+            Ub[3][g][h] = sbyte_pair_f16<3>(s0, s1);
+        }
+    }
+}
+
+// The thread's column partials of S^T k and S^T q (before the c_j factor)
+// from 16 4x4x4 products, written to sh.red for the column phase.  The
+// operand table of row_constants_mfma must be complete (a barrier after
+// it).  The 4 threads of a block share their rows and own 4 different
+// column words; thread type cg & 3 supplies weight type cg & 3.
+__device__ __forceinline__ void matvec_partials(DecodeShared<128> &sh, int slice, int cg,
+                                                const uint32_t (&Ub)[4][4][2], int ek, int eq)
+{
+    u32x2 A[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) A[g] = *reinterpret_cast<const u32x2 *>(&sh.aop[slice][g][cg & 3][0]);
+    float *redK = &sh.red[0][slice][cg].x, *redQ = &sh.red[1][slice][cg].x;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        f32x4 d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int g = 0; g < 4; ++g) d = mfma4x4x4(A[g], Ub[e][g][0], Ub[e][g][1], d);
+        redK[e] = __builtin_amdgcn_ldexpf(d[0] + d[1], -ek);    // the column partials go straight to LDS
+        redQ[e] = __builtin_amdgcn_ldexpf(d[2] + d[3], -eq);
+        __builtin_amdgcn_sched_barrier(0);    // one column's chain at a time: 4 accumulators live
+    }
+}
+
+// New field in byte E of P from the old field in half HALF of hp; the
+// arithmetic of requant_word below.
 template <int B, int E, int HALF>
 __device__ __forceinline__ uint32_t requant_field_p(uint32_t hp, float al, float a_s, float bce, uint32_t P)
 {
@@ -716,7 +707,7 @@ __device__ __forceinline__ uint32_t requant_slot_p(const uint32_t (&Ub)[4][4][2]
 }
 
 // New word of 8/B slots (row-table slots x0 + s, thread rows r0 + s) from
-// the row-pair registers; as requant_word_h otherwise.  r0 is a constant
+// the row-pair registers; as requant_word otherwise.  r0 is a constant
 // once the caller's loops are unrolled, so every register index folds.
 template <int B, bool DIAG>
 __device__ __forceinline__ uint32_t requant_word_p(const uint32_t (&Ub)[4][4][2], int r0, const float *av,
@@ -731,38 +722,6 @@ __device__ __forceinline__ uint32_t requant_word_p(const uint32_t (&Ub)[4][4][2]
         const float al = DIAG ? alt[x0 + s] : al_w;
         const uint32_t P = (r & 1) ? requant_slot_p<B, 1>(Ub, r >> 2, (r >> 1) & 1, al, a_s, bc)
                                    : requant_slot_p<B, 0>(Ub, r >> 2, (r >> 1) & 1, al, a_s, bc);
-        out |= P << (s * B);
-    }
-    return out ^ flip;
-}
-
-template <int B, int E>
-__device__ __forceinline__ uint32_t requant_field(const uint32_t *U2, int s, float al, float a_s, float bce, uint32_t P)
-{
-    constexpr float bias = static_cast<float>(1 << (B - 1));
-    constexpr float top = static_cast<float>((1 << B) - 1);
-    const float tt = fmaf(a_s, bce, bias);
-    float y = fma_mix_e<E>(al, U2, s, tt);
-    y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
-    return __builtin_amdgcn_cvt_pk_u8_f32(y, E, P);
-}
-
-// al: the per-width gate factor (scalar gate) or, with a table alt, per row.
-template <int B, bool DIAG>
-__device__ __forceinline__ uint32_t requant_word_h(const uint32_t *U2, const float *av, const float *alt, int x0,
-                                                   float al_w, const float (&bc)[4])
-{
-    constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
-    uint32_t out = 0;
-#pragma unroll
-    for (int s = 0; s < 8 / B; ++s) {
-        const float a_s = av[x0 + s];
-        const float al = DIAG ? alt[x0 + s] : al_w;
-        uint32_t P = 0;
-        P = requant_field<B, 0>(U2, s, al, a_s, bc[0], P);
-        P = requant_field<B, 1>(U2, s, al, a_s, bc[1], P);
-        P = requant_field<B, 2>(U2, s, al, a_s, bc[2], P);
-        P = requant_field<B, 3>(U2, s, al, a_s, bc[3], P);
         out |= P << (s * B);
     }
     return out ^ flip;

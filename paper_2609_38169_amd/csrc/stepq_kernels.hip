@@ -41,7 +41,6 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
     static_assert(M8 + 2 * M4 + 4 * M2 == 16, "a uniform body holds 16 rows per thread");
     static_assert(M8 % 4 == 0 && M4 % 2 == 0, "row groups of 4 hold rows of one width");
     constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;    // row-table starts of the 4- and 2-bit slots
-    constexpr int G4 = M8 / 4, G2 = (M8 + 2 * M4) / 4;    // first row group of the 4- and 2-bit rows
     const int tid = threadIdx.x;
     const int cg = tid & 31, slice = tid >> 5;
     const CodeWords cw(t.codes, 1024u * M);
@@ -54,53 +53,9 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
     const float kappa = row_constants_mfma<DIAG, M8, M4, M2, 128>(t.beta, op, sh, a.pool.lv, ek, eq);
 
     uint32_t Ub[4][4][2];
-#pragma unroll
-    for (int g = 0; g < G4; ++g)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const uint32_t lo = w[4 * g + 2 * h], hi = w[4 * g + 2 * h + 1];
-            Ub[0][g][h] = sbyte_pair_f16<0>(lo, hi);
-            Ub[1][g][h] = sbyte_pair_f16<1>(lo, hi);
-            Ub[2][g][h] = sbyte_pair_f16<2>(lo, hi);
-            Ub[3][g][h] = sbyte_pair_f16<3>(lo, hi);
-        }
-#pragma unroll
-    for (int m = 0; m < M4; ++m) {
-        const uint32_t s0 = slot_top<4>(w[M8 + m], 0), s1 = slot_top<4>(w[M8 + m], 1);
-        const int g = G4 + m / 2, h = m & 1;
-        Ub[0][g][h] = sbyte_pair_f16<0>(s0, s1);
-        Ub[1][g][h] = sbyte_pair_f16<1>(s0, s1);
-        Ub[2][g][h] = sbyte_pair_f16<2>(s0, s1);
-        Ub[3][g][h] = sbyte_pair_f16<3>(s0, s1);
-    }
-#pragma unroll
-    for (int m = 0; m < M2; ++m) {
-        const uint32_t wm = w[M8 + M4 + m];
-        const int g = G2 + m;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const uint32_t s0 = slot_top<2>(wm, 2 * h), s1 = slot_top<2>(wm, 2 * h + 1);
-            Ub[0][g][h] = sbyte_pair_f16<0>(s0, s1);
-            Ub[1][g][h] = sbyte_pair_f16<1>(s0, s1);
-            Ub[2][g][h] = sbyte_pair_f16<2>(s0, s1);
-            Ub[3][g][h] = sbyte_pair_f16<3>(s0, s1);
-        }
-    }
+    unpack_row_pairs<M8, M4, M2>(w, Ub);
     __syncthreads();    // operand table written
-
-    u32x2 A[4];
-#pragma unroll
-    for (int g = 0; g < 4; ++g) A[g] = *reinterpret_cast<const u32x2 *>(&sh.aop[slice][g][cg & 3][0]);
-    float *redK = &sh.red[0][slice][cg].x, *redQ = &sh.red[1][slice][cg].x;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        f32x4 d = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int g = 0; g < 4; ++g) d = mfma4x4x4(A[g], Ub[e][g][0], Ub[e][g][1], d);
-        redK[e] = __builtin_amdgcn_ldexpf(d[0] + d[1], -ek);    // the column partials go straight to LDS
-        redQ[e] = __builtin_amdgcn_ldexpf(d[2] + d[3], -eq);
-        __builtin_amdgcn_sched_barrier(0);    // one column's chain at a time: 4 accumulators live
-    }
+    matvec_partials(sh, slice, cg, Ub, ek, eq);
 
     column_sums<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, op.c, op.v);
 
@@ -112,12 +67,12 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
 #pragma unroll
     for (int m = 0; m < M4; ++m)
         cw.store_m(tid, M8 + m, requant_word_p<4, DIAG>(Ub, M8 + 2 * m, sh.av, sh.al, X4 + 2 * (slice + 8 * m),
-                                                               t.alpha * (1.0f / 16.0f), bc));
+                                                        t.alpha * (1.0f / 16.0f), bc));
 #pragma unroll
     for (int m = 0; m < M2; ++m)
         cw.store_m(tid, M8 + M4 + m,
-                 requant_word_p<2, DIAG>(Ub, M8 + 2 * M4 + 4 * m, sh.av, sh.al, X2 + 4 * (slice + 8 * m),
-                                         t.alpha * (1.0f / 64.0f), bc));
+                   requant_word_p<2, DIAG>(Ub, M8 + 2 * M4 + 4 * m, sh.av, sh.al, X2 + 4 * (slice + 8 * m),
+                                           t.alpha * (1.0f / 64.0f), bc));
 }
 
 // Any row-width mix and d_v: the class of each word-step is looked up at run

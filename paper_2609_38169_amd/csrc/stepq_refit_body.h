@@ -167,21 +167,30 @@ __device__ __forceinline__ void refit_colfit(RefitShared<DV> &sh, int j, float *
 
 // ---- per-word passes on values held in registers (4 columns x 8/B rows)
 
-// y of a word from its f16-packed fields; the row partial sum_e c_e |y| of
-// each slot goes to LDS.
+// y of a word from the row-pair registers of the matrix-core path; the row
+// partial sum_e c_e |y| (or max) of each slot goes to LDS.  Slot s of the
+// word is thread row r0 + s (a constant once the caller's loops unroll).
 template <int B, bool DIAG, Refit MODE>
-__device__ __forceinline__ void word_y(const uint32_t *U2, RefitShared<128> &sh, int x0, int cg, float al_w,
-                                       const float (&bc)[4], const float (&cc)[4], float *Y)
+__device__ __forceinline__ void word_y_p(const uint32_t (&Ub)[4][4][2], int r0, RefitShared<128> &sh, int x0, int cg,
+                                         float al_w, const float (&bc)[4], const float (&cc)[4], float *Y)
 {
 #pragma unroll
     for (int s = 0; s < 8 / B; ++s) {
+        const int r = r0 + s, g = r >> 2, h = (r >> 1) & 1;
         const float a_s = sh.d.av[x0 + s];
         const float al = DIAG ? sh.d.al[x0 + s] : al_w;
         float *y = Y + 4 * s;
-        y[0] = fma_mix_e<0>(al, U2, s, a_s * bc[0]);
-        y[1] = fma_mix_e<1>(al, U2, s, a_s * bc[1]);
-        y[2] = fma_mix_e<2>(al, U2, s, a_s * bc[2]);
-        y[3] = fma_mix_e<3>(al, U2, s, a_s * bc[3]);
+        if (r & 1) {
+            y[0] = fma_mix<1>(al, Ub[0][g][h], a_s * bc[0]);
+            y[1] = fma_mix<1>(al, Ub[1][g][h], a_s * bc[1]);
+            y[2] = fma_mix<1>(al, Ub[2][g][h], a_s * bc[2]);
+            y[3] = fma_mix<1>(al, Ub[3][g][h], a_s * bc[3]);
+        } else {
+            y[0] = fma_mix<0>(al, Ub[0][g][h], a_s * bc[0]);
+            y[1] = fma_mix<0>(al, Ub[1][g][h], a_s * bc[1]);
+            y[2] = fma_mix<0>(al, Ub[2][g][h], a_s * bc[2]);
+            y[3] = fma_mix<0>(al, Ub[3][g][h], a_s * bc[3]);
+        }
         put_row_partial<128>(sh, x0 + s, cg, row_partial<MODE>(y, cc));
     }
 }
@@ -277,27 +286,22 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     const CodeWords cw(t.codes, 1024u * M);
     uint32_t w[M];
 #pragma unroll
-    for (int m = 0; m < M; ++m) w[m] = cw.load(tid + 256 * m);
+    for (int m = 0; m < M; ++m) w[m] = cw.load_m(tid, m);
 
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
     if (tid < 128) {
         sh.ccol[tid] = op.c;
         sh.wphys[tid] = a.pool.roww[t.h * 128 + tid];
     }
-    const float kappa = row_constants_uniform<DIAG, M8, M4, 128>(t.beta, op, sh.d, a.pool.lv);
+    // S^T k and S^T q on the matrix cores, as in the frozen-scale body
+    int ek, eq;
+    const float kappa = row_constants_mfma<DIAG, M8, M4, M2, 128>(t.beta, op, sh.d, a.pool.lv, ek, eq);
+    uint32_t Ub[4][4][2];
+    unpack_row_pairs<M8, M4, M2>(w, Ub);
+    __syncthreads();    // operand table written
+    matvec_partials(sh.d, slice, cg, Ub, ek, eq);
 
-    uint32_t U[NE / 2];
-    float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int m = 0; m < M8; ++m) unpack_acc_h<8>(w[m], sh.d.kq, slice + 8 * m, &U[2 * m], acK, acQ);
-#pragma unroll
-    for (int m = 0; m < M4; ++m)
-        unpack_acc_h<4>(w[M8 + m], sh.d.kq, X4 + 2 * (slice + 8 * m), &U[2 * M8 + 4 * m], acK, acQ);
-#pragma unroll
-    for (int m = 0; m < M2; ++m)
-        unpack_acc_h<2>(w[M8 + M4 + m], sh.d.kq, X2 + 4 * (slice + 8 * m), &U[2 * M8 + 4 * M4 + 8 * m], acK, acQ);
-
-    column_phase<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh.d, kappa, acK, acQ, op.c, op.v);
+    column_sums<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh.d, kappa, op.c, op.v);
 
     // pass 1: y on the old scales and the row partials
     float bc[4], cc[4];
@@ -305,16 +309,15 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     ld4(&sh.ccol[4 * cg], cc);
     float Y[NE];
 #pragma unroll
-    for (int m = 0; m < M8; ++m)
-        word_y<8, DIAG, MODE>(&U[2 * m], sh, slice + 8 * m, cg, t.alpha, bc, cc, &Y[4 * m]);
+    for (int m = 0; m < M8; ++m) word_y_p<8, DIAG, MODE>(Ub, m, sh, slice + 8 * m, cg, t.alpha, bc, cc, &Y[4 * m]);
 #pragma unroll
     for (int m = 0; m < M4; ++m)
-        word_y<4, DIAG, MODE>(&U[2 * M8 + 4 * m], sh, X4 + 2 * (slice + 8 * m), cg, t.alpha * (1.0f / 16.0f), bc, cc,
-                              &Y[Y4 + 8 * m]);
+        word_y_p<4, DIAG, MODE>(Ub, M8 + 2 * m, sh, X4 + 2 * (slice + 8 * m), cg, t.alpha * (1.0f / 16.0f), bc, cc,
+                                &Y[Y4 + 8 * m]);
 #pragma unroll
     for (int m = 0; m < M2; ++m)
-        word_y<2, DIAG, MODE>(&U[2 * M8 + 4 * M4 + 8 * m], sh, X2 + 4 * (slice + 8 * m), cg,
-                              t.alpha * (1.0f / 64.0f), bc, cc, &Y[Y2 + 16 * m]);
+        word_y_p<2, DIAG, MODE>(Ub, M8 + 2 * M4 + 4 * m, sh, X2 + 4 * (slice + 8 * m), cg, t.alpha * (1.0f / 64.0f),
+                                bc, cc, &Y[Y2 + 16 * m]);
     __syncthreads();
     if (tid < 128) refit_row<128, MODE>(sh, tid, tid, tid < X4 ? 8 : (tid < X2 ? 4 : 2), op.r, rr_out, a.pool.lv);
     if constexpr (MODE == Refit::RowAbsmax) {
@@ -332,13 +335,13 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
         for (int m = 0; m < M2; ++m) word_scale<2>(&Y[Y2 + 16 * m], sh.hrow, X2 + 4 * (slice + 8 * m));
 #pragma unroll
         for (int m = 0; m < M8; ++m)
-            cw.store(tid + 256 * m, word_requant<8>(&Y[4 * m], cc));
+            cw.store_m(tid, m, word_requant<8>(&Y[4 * m], cc));
 #pragma unroll
         for (int m = 0; m < M4; ++m)
-            cw.store(tid + 256 * (M8 + m), word_requant<4>(&Y[Y4 + 8 * m], cc));
+            cw.store_m(tid, M8 + m, word_requant<4>(&Y[Y4 + 8 * m], cc));
 #pragma unroll
         for (int m = 0; m < M2; ++m)
-            cw.store(tid + 256 * (M8 + M4 + m), word_requant<2>(&Y[Y2 + 16 * m], cc));
+            cw.store_m(tid, M8 + M4 + m, word_requant<2>(&Y[Y2 + 16 * m], cc));
         return;
     }
 
@@ -379,13 +382,13 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     float g[4];
     ld4(&sh.gcol[4 * cg], g);
 #pragma unroll
-    for (int m = 0; m < M8; ++m) cw.store(tid + 256 * m, word_requant<8>(&Y[4 * m], g));
+    for (int m = 0; m < M8; ++m) cw.store_m(tid, m, word_requant<8>(&Y[4 * m], g));
 #pragma unroll
     for (int m = 0; m < M4; ++m)
-        cw.store(tid + 256 * (M8 + m), word_requant<4>(&Y[Y4 + 8 * m], g));
+        cw.store_m(tid, M8 + m, word_requant<4>(&Y[Y4 + 8 * m], g));
 #pragma unroll
     for (int m = 0; m < M2; ++m)
-        cw.store(tid + 256 * (M8 + M4 + m), word_requant<2>(&Y[Y2 + 16 * m], g));
+        cw.store_m(tid, M8 + M4 + m, word_requant<2>(&Y[Y2 + 16 * m], g));
 }
 
 // ---- any row-width mix and d_v: the words stay packed in registers and
