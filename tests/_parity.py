@@ -69,10 +69,50 @@ def oracle_inputs(w: W.Workload, inp: dict, rows: np.ndarray):
             b.reshape(n))
 
 
+FP32_EPS = 2.0 ** -24
+
+
+def fp32_step_bounds(codes, r, c, bits, q, k, v, alpha, beta, levels: int = 0):
+    """Forward error bounds of an fp32 evaluation of the frozen-scale step
+    (any summation order, dot products of length d_k), from the oracle's
+    own inputs: per code, in code units, and per output.  Used where the
+    inputs' dynamic range makes the fixed tie window too narrow: with
+    u_j = sum_i g_i k_i S_ij (g = alpha, or the channel gate d),
+    delta_j = v_j - u_j and X_ij = g_i S_ij + beta k_i delta_j,
+        |d delta_j| <= gam sum_i |g_i k_i S_ij| + 4 eps |v_j|
+        |d y_ij|    <= (4 eps (|g_i S_ij| + |beta k_i delta_j|) + |beta k_i| |d delta_j|) / (r_i c_j nu_i)
+        |d o_j|     <= gam sum_i |g_i q_i S_ij| + |beta| (|kappa| |d delta_j| + gam sum_i |q_i k_i| |delta_j|)
+                       + 4 eps |o_j|
+    with gam = (d_k + 8) eps and nu_i the level step of row i."""
+    n, dk, dv = codes.shape
+    S = oracle.dequant(codes, r, c, bits, levels=levels)
+    a = np.asarray(alpha, np.float64)
+    g = np.broadcast_to(a.reshape(n, -1), (n, dk)) if a.ndim > 1 else np.broadcast_to(a.reshape(n, 1), (n, dk))
+    bw = np.broadcast_to(bits, (n, dk)).astype(np.float64)
+    nu = np.exp2(8.0 - bw) if levels else 1.0 / (np.exp2(bw - 1) - 1)
+    beta = np.asarray(beta, np.float64).reshape(n, 1)
+    eps, gam = FP32_EPS, (dk + 8) * FP32_EPS
+    gks = (g * k)[:, :, None] * S
+    u = gks.sum(axis=1)
+    delta = v - u
+    d_delta = gam * np.abs(gks).sum(axis=1) + 4 * eps * np.abs(v)
+    X = g[:, :, None] * S + (beta * k)[:, :, None] * delta[:, None, :]
+    scale = 1.0 / (np.asarray(r, np.float64)[:, :, None] * np.asarray(c, np.float64)[:, None, :] * nu[:, :, None])
+    dy = (4 * eps * (np.abs(g[:, :, None] * S) + np.abs((beta * k)[:, :, None] * delta[:, None, :]))
+          + np.abs(beta * k)[:, :, None] * d_delta[:, None, :]) * scale
+    kappa = (q * k).sum(axis=1, keepdims=True)
+    o = (X * q[:, :, None]).sum(axis=1)
+    do = (gam * np.abs((g * q)[:, :, None] * S).sum(axis=1)
+          + np.abs(beta) * (np.abs(kappa) * d_delta + gam * np.abs(q * k).sum(axis=1, keepdims=True) * np.abs(delta))
+          + 4 * eps * np.abs(o))
+    return dy, do
+
+
 def compare_codes(gpu: np.ndarray, orc: np.ndarray, y: np.ndarray, what: str = "codes",
-                  frac: float = CODE_MISMATCH_FRAC):
+                  frac: float = CODE_MISMATCH_FRAC, window=TIE_WINDOW):
     """Apply the code tolerance to one comparison (at most ``frac`` of the
-    entries mismatched); returns the number of tie mismatches."""
+    entries mismatched, each within ``window`` of a rounding tie: a scalar
+    or a per-code array); returns the number of tie mismatches."""
     diff = gpu.astype(np.int16) - orc.astype(np.int16)
     bad = np.nonzero(diff)
     n_bad = bad[0].size
@@ -80,7 +120,8 @@ def compare_codes(gpu: np.ndarray, orc: np.ndarray, y: np.ndarray, what: str = "
         return 0
     assert np.all(np.abs(diff[bad]) == 1), f"{what}: a code differs by more than one level"
     fpart = np.abs(y[bad]) - np.floor(np.abs(y[bad]))
-    near_tie = np.abs(fpart - 0.5) <= TIE_WINDOW
+    win = np.broadcast_to(window, y.shape)[bad]
+    near_tie = np.abs(fpart - 0.5) <= win
     assert np.all(near_tie), (f"{what}: {int((~near_tie).sum())} mismatches away from a rounding tie, e.g. "
                               f"y={y[bad][~near_tie][:4]}")
     assert n_bad <= frac * gpu.size, f"{what}: {n_bad} of {gpu.size} codes differ"
@@ -157,9 +198,13 @@ def compare_pivots(g_pv, o_pv, X, mask, what: str = "pivots", frac: float = PIVO
     return n_bad
 
 
-def compare_out(gpu: np.ndarray, orc: np.ndarray, what: str = "o"):
+def compare_out(gpu: np.ndarray, orc: np.ndarray, what: str = "o", bound=None):
+    """|o_gpu - o_oracle| within O_ABS + O_REL |o_oracle|, or within
+    ``bound`` (per output) where that is larger."""
     err = np.abs(gpu.astype(np.float64) - orc)
     lim = O_ABS + O_REL * np.abs(orc)
+    if bound is not None:
+        lim = np.maximum(lim, bound)
     worst = np.argmax(err - lim)
     assert np.all(err <= lim), (f"{what}: |diff| {err.flat[worst]:.3g} > {lim.flat[worst]:.3g} "
                                 f"(oracle {orc.flat[worst]:.6g}); {int((err > lim).sum())} entries out")
@@ -170,8 +215,10 @@ class Lockstep:
     ``check_rows`` (batch rows whose slots are compared each step)."""
 
     def __init__(self, w: W.Workload, pool, slots: torch.Tensor, bits: np.ndarray, check_rows: np.ndarray,
-                 S0_check: np.ndarray, layer: int = 0, refit=False, row_weight=None, levels: int = 0):
+                 S0_check: np.ndarray, layer: int = 0, refit=False, row_weight=None, levels: int = 0,
+                 fp32_bounds: bool = False):
         self.w, self.pool, self.slots, self.bits, self.layer = w, pool, slots, bits, layer
+        self.fp32_bounds = fp32_bounds      # o limit (and the frozen steps' tie window) from fp32_step_bounds
         self.refit = refit
         self.lv = dict(levels=levels)
         self.tie_cols = 0
@@ -229,6 +276,11 @@ class Lockstep:
         g_codes, g_r, g_c = self.export()
         pvk = dict(pv=self.pv) if self.pivots else {}
         pmask = self.tile_bits == 16
+        o_bound = dy = None
+        if self.fp32_bounds:
+            assert not self.pivots, "fp32 step bounds cover integer rows only"
+            dy, o_bound = fp32_step_bounds(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b,
+                                           self.lv["levels"])
         if self.refit == "row_absmax":
             res = oracle.decode_step_rowmax(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True,
                                             **pvk, **self.lv)
@@ -269,21 +321,28 @@ class Lockstep:
                 self.pv = res[3]
             assert np.array_equal(g_r.reshape(self.r.shape), self.r), "row scales changed"
             assert np.array_equal(g_c.reshape(self.c.shape), self.c), "column scales changed"
+            win = TIE_WINDOW if dy is None else TIE_WINDOW + dy
             self.mismatches += compare_codes(g_codes, new, y, f"layer {self.layer} step {step} codes",
-                                             frac=STEP_MISMATCH_FRAC)
+                                             frac=STEP_MISMATCH_FRAC, window=win)
         self.compared += g_codes.size
         rows_t = torch.as_tensor(self.rows, dtype=torch.long, device=o_gpu.device)
         og = o_gpu.index_select(0, rows_t).cpu().numpy().reshape(self.n_tiles, w.d_v)
-        compare_out(og, o, f"layer {self.layer} step {step} o")
+        compare_out(og, o, f"layer {self.layer} step {step} o", bound=o_bound)
         qb = (2 ** (self.tile_bits.astype(np.int32) - 1) - 1)[:, :, None]
         self.saturated = float(np.mean(np.abs(new) == qb))
         self.codes = new
 
 
 def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, mutate=None, kda: bool = False,
-                 refit=False, row_weight=None, say=print, bits=None, levels: int = 0):
+                 refit=False, row_weight=None, say=print, bits=None, levels: int = 0, state_map=None,
+                 fp32_bounds: bool = False):
     """Full-size decode steps of one workload layer on the GPU, the rows
-    ``check_rows`` compared lockstep with the oracle at every step."""
+    ``check_rows`` compared lockstep with the oracle at every step.
+    ``state_map`` (optional) transforms the checked slots' initial states
+    [rows][Hv][d_k][d_v] before the oracle fits and quantizes them.
+    ``fp32_bounds``: judge o (every mode) and, on frozen steps, the codes'
+    distance from a rounding tie against the fp32 forward error bounds of
+    the step as well as the fixed limits."""
     from paper_2609_38169_amd.pools import build_pool, row_bits
     bits = row_bits(w, layer) if bits is None else bits
     say(f"lockstep {w.name}: building pool ({w.n_slots} slots)")
@@ -293,7 +352,10 @@ def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, 
     slots = W.active_slots(w).to(device)
     check_slots = W.active_slots(w)[np.asarray(check_rows)]
     S0 = W.initial_state(w, layer, [int(x) for x in check_slots], device=device).cpu().numpy()
-    ls = Lockstep(w, pool, slots, bits, check_rows, S0, layer, refit=refit, row_weight=row_weight, levels=levels)
+    if state_map is not None:
+        S0 = np.ascontiguousarray(state_map(S0), dtype=np.float32)
+    ls = Lockstep(w, pool, slots, bits, check_rows, S0, layer, refit=refit, row_weight=row_weight, levels=levels,
+                  fp32_bounds=fp32_bounds)
     o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=device)
     for t in range(steps):
         inp = W.step_inputs(w, layer, t, device=device)

@@ -1,9 +1,13 @@
 """GPU parity at the extremes of the decode step, lockstep against the fp64
 oracle through the C ABI: every slot of the 2048-slot pool stepped in one
-launch (65,536 workgroups), and the degenerate gates of the update:
+launch (65,536 workgroups), the degenerate gates of the update:
 alpha = 0 (the state is replaced by the rank-one write beta k v^T),
 beta = 0 (pure decay, X = alpha S), and channel-wise gates of exactly 0 or 1
-(rows forgotten or kept whole)."""
+(rows forgotten or kept whole); and the dynamic range of the matrix-core
+products, whose row weights are split into binary16 hi + lo parts under a
+power-of-two prescale per tile: weights spanning ~40 binades inside a tile,
+whole tiles at 2^60 and 2^-60 (outside binary16's range without the
+prescale), and heads whose keys or queries are all zero."""
 import dataclasses
 
 import numpy as np
@@ -59,3 +63,89 @@ def test_kda_gates_zero_or_one():
         return (d > d.median()).to(d.dtype)
 
     PT.lockstep_run(w, 3, np.array([0, 255, 511]), DEV, mutate=_set("alpha", binary), kda=True, say=_say)
+
+
+def _row_scaled(seed, lo, hi):
+    def f(S):
+        rng = np.random.default_rng(seed)
+        e = rng.integers(lo, hi + 1, size=S.shape[:3]).astype(np.float64)
+        return S.astype(np.float64) * np.exp2(e)[..., None]
+    return f
+
+
+def _tile_exponents(n_rows, n_heads):
+    """Tiles of the checked rows alternately at 2^60, 1 and 2^-60."""
+    return np.array([60.0, 0.0, -60.0])[np.arange(n_rows * n_heads) % 3].reshape(n_rows, n_heads)
+
+
+def _spread_keys(seed, lo, hi):
+    """Key entries scaled by 2^e, e uniform in lo..hi (exact in bf16)."""
+    def mutate(inp):
+        inp = dict(inp)
+        rng = np.random.default_rng(seed)
+        e = torch.from_numpy(np.exp2(rng.integers(lo, hi + 1, size=tuple(inp["k"].shape))).astype(np.float32))
+        inp["k"] = (inp["k"].float() * e.to(inp["k"].device)).to(inp["k"].dtype)
+        return inp
+    return mutate
+
+
+@pytest.mark.parametrize("kda", [False, True])
+def test_weights_span_40_binades(kda):
+    """Rows scaled by 2^[-4, 4] and key entries by 2^[-16, 16]: the k weights
+    of one tile span ~40 binades, beyond the 17 over which the binary16
+    hi + lo split keeps full precision.  fp32 itself then loses the fixed
+    tie window's accuracy on a few codes, so mismatches and o are judged
+    against the step's fp32 forward error bounds."""
+    w = W.workload(2)
+    PT.lockstep_run(w, 3, np.array([0, 200, 511]), DEV, kda=kda, say=_say, state_map=_row_scaled(7, -4, 4),
+                    mutate=_spread_keys(8, -16, 16), fp32_bounds=True)
+
+
+@pytest.mark.parametrize("refit,kda", [(False, False), (True, False), ("row_absmax", False), (False, True)])
+def test_tiles_at_extreme_magnitudes(refit, kda):
+    """Tiles at 2^60, 1 and 2^-60, their values v scaled with them, so the
+    step is exactly equivariant under the scaling (X, o and the refitted
+    factors scale by the same power of two): the weights lie far outside
+    binary16's range until the per-tile prescale brings them in.  The fixed
+    absolute part of the o limit does not scale with the tile, so o is also
+    allowed the step's fp32 forward error bound (which does)."""
+    w = W.workload(2)
+    rows = np.array([1, 300, 510])
+    e = _tile_exponents(len(rows), w.n_v_heads)
+
+    def scale_state(S):
+        return S.astype(np.float64) * np.exp2(e)[:, :, None, None]
+
+    def scale_v(inp):
+        inp = dict(inp)
+        v = inp["v"].clone()
+        f = torch.from_numpy(np.exp2(e).astype(np.float32)).to(v.device)
+        idx = torch.as_tensor(rows, dtype=torch.long, device=v.device)
+        v[idx] = (v[idx].float() * f[:, :, None]).to(v.dtype)
+        inp["v"] = v
+        return inp
+
+    PT.lockstep_run(w, 3, rows, DEV, refit=refit, kda=kda, say=_say, state_map=scale_state, mutate=scale_v,
+                    fp32_bounds=True)
+
+
+def test_zero_keys_and_queries():
+    """All-zero k on some q/k heads and all-zero q on others: a tile whose
+    largest k (or q) weight is 0.  With k = 0 the step is a pure decay,
+    y = alpha q exactly; the gates are put on odd multiples of 2^-8 so that
+    alpha q is never exactly half-way between codes (an exact tie, which the
+    kernel rounds to even and the fp64 oracle's own rounding of
+    X q_b / (r c) decides either way)."""
+    w = W.workload(2)
+
+    def zero_heads(inp):
+        inp = dict(inp)
+        k, q = inp["k"].clone(), inp["q"].clone()
+        k[:, 0::3] = 0
+        q[:, 1::3] = 0
+        m = torch.round(inp["alpha"].float() * 256.0)
+        m = m - (1 - torch.remainder(m, 2))          # the odd multiple of 2^-8 at or below
+        inp["k"], inp["q"], inp["alpha"] = k, q, (m / 256.0).to(inp["alpha"].dtype)
+        return inp
+
+    PT.lockstep_run(w, 3, np.array([2, 256, 509]), DEV, mutate=zero_heads, say=_say)

@@ -5,6 +5,7 @@ import numpy as np
 import pytest
 
 import _parity as PT
+import oracle
 
 
 def _codes(seed=0, n=2, dk=8, dv=6):
@@ -101,3 +102,82 @@ def test_compare_pivots_rules():
     g2 = o_pv.copy()
     g2[0, 2, 0] += 7                                 # outside the pivot rows: not compared
     assert PT.compare_pivots(g2, o_pv, X, mask, frac=0.0) == 0
+
+
+def _fp32_step(codes, r, c, bits, q, k, v, alpha, beta, split: bool):
+    """The frozen step's code-space form evaluated in fp32 (the decode
+    kernel's arithmetic): weights k r 2^(b-8)/q_b, optionally rounded to the
+    binary16 hi + lo pair under a power-of-two prescale per tile; y in code
+    units and o."""
+    f32 = np.float32
+    n, dk, dv = codes.shape
+    bw = bits.astype(np.int64)
+    qb = np.exp2(bw - 1) - 1
+    U = (codes.astype(np.float64) * np.exp2(8 - bw)[:, :, None]).astype(f32)
+    fq = (np.exp2(bw - 8) / qb).astype(f32)
+    kt = (k.astype(f32) * (r * fq)).astype(f32)
+    qt = (q.astype(f32) * (r * fq)).astype(f32)
+
+    def matvec(wt):
+        if split:
+            e = np.clip(15 - np.frexp(np.abs(wt).max(axis=1))[1], -126, 126)
+            ws = (wt * np.exp2(e)[:, None]).astype(f32)
+            hi = ws.astype(np.float16)
+            lo = (ws - hi.astype(f32)).astype(np.float16)
+            s = np.zeros((n, dv), f32)
+            for i in range(dk):
+                s = (s + (hi[:, i].astype(f32)[:, None] * U[:, i, :]).astype(f32)
+                     + (lo[:, i].astype(f32)[:, None] * U[:, i, :]).astype(f32)).astype(f32)
+            return (s * np.exp2(-e)[:, None]).astype(f32)
+        s = np.zeros((n, dv), f32)
+        for i in range(dk):
+            s = (s + wt[:, i, None] * U[:, i, :]).astype(f32)
+        return s
+
+    al = alpha.astype(f32)[:, None]
+    b32 = beta.astype(f32)[:, None]
+    cu = (c * matvec(kt)).astype(f32)
+    cp = (c * matvec(qt)).astype(f32)
+    delta = (v.astype(f32) - al * cu).astype(f32)
+    kappa = (q.astype(f32) * k.astype(f32)).sum(axis=1, dtype=f32)[:, None]
+    o = (al * cp + b32 * kappa * delta).astype(f32)
+    ai = (b32 * k.astype(f32) * qb.astype(f32) * (f32(1) / r)).astype(f32)
+    bcol = (delta * (f32(1) / c)).astype(f32)
+    y = (al[:, :, None] * np.exp2(bw - 8).astype(f32)[:, :, None] * U + ai[:, :, None] * bcol[:, None, :]).astype(f32)
+    return y, o
+
+
+@pytest.mark.parametrize("spread", [(0, 0, 0, 0), (-4, 4, -16, 16)])
+def test_fp32_step_bounds_cover_fp32_evaluations(spread):
+    """The per-code and per-output bounds used for wide-range GPU cases hold
+    for fp32 evaluations of the step (the code-space form with fp32 weights,
+    and with the binary16 hi + lo weight split), on ordinary tiles and on
+    tiles whose weights span ~40 binades."""
+    s_lo, s_hi, k_lo, k_hi = spread
+    rng = np.random.default_rng(11)
+    n, dk, dv = 8, 128, 128
+    bits = rng.choice(np.array([4, 8], np.uint8), size=(n, dk))
+    S = rng.normal(0.0, 0.05, (n, dk, dv)) * np.exp2(rng.integers(s_lo, s_hi + 1, (n, dk, 1)))
+    r, c = oracle.fit_absmax(S.astype(np.float32), bits=bits)
+    codes = oracle.quantize(S, r, c, bits)
+    unit = lambda x: x / np.linalg.norm(x, axis=1, keepdims=True)
+    q = unit(rng.normal(size=(n, dk))).astype(np.float32).astype(np.float64)
+    k = (unit(rng.normal(size=(n, dk))) * np.exp2(rng.integers(k_lo, k_hi + 1, (n, dk)))).astype(np.float32)
+    k = k.astype(np.float64)
+    v = rng.normal(size=(n, dv)).astype(np.float32).astype(np.float64)
+    alpha = (1.0 - rng.uniform(0, 0.05, n)).astype(np.float32).astype(np.float64)
+    beta = rng.uniform(0.1, 0.9, n).astype(np.float32).astype(np.float64)
+    _, o64, y64 = oracle.decode_step(codes, r, c, bits, q, k, v, alpha, beta, want_y=True)
+    dy, do = PT.fp32_step_bounds(codes, r, c, bits, q, k, v, alpha, beta)
+    qb = (np.exp2(bits.astype(np.int64) - 1) - 1)[:, :, None]
+    live = np.abs(y64) < qb + 0.5          # clamped codes do not depend on the error
+    if spread == (0, 0, 0, 0):
+        # on ordinary tiles the bound is tighter than the fixed tie window
+        assert np.quantile(dy[live], 0.999) < PT.TIE_WINDOW
+    else:
+        # and where fp32 cannot resolve a code it widens the window for few codes only
+        assert np.mean(dy[live] > 0.05) < 0.01
+    for split in (False, True):
+        y, o = _fp32_step(codes, r, c, bits, q, k, v, alpha, beta, split)
+        assert np.all(np.abs(y.astype(np.float64) - y64)[live] <= dy[live]), split
+        assert np.all(np.abs(o.astype(np.float64) - o64) <= do), split
