@@ -173,6 +173,9 @@ def pool_case(args, w, mode, dev):
     log(f"building the {w.n_slots}-slot pool")
     pool = build_pool(w, device=dev, bits=bits, levels=args.levels)
     subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
+    if args.sorted_batch:
+        # the same requests, listed in slot order (a caller-side choice: any batch order is valid)
+        subsets = [torch.sort(s).values for s in subsets]
     n_inp = min(w.steps, args.steps + args.warmup)
     inputs = [W.step_inputs(w, 0, t, device=dev) for t in range(n_inp)]
     if args.kda:
@@ -199,7 +202,8 @@ def pool_case(args, w, mode, dev):
                 tiles_per_step=w.batch * w.n_v_heads, layers=1,
                 workload=f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
                          f"d_k=d_v={w.d_k}, {mix}, fp32 scales, bf16 activations",
-                extra={"slot_rotation": len(subsets), "cache_resident": bool(args.resident)},
+                extra={"slot_rotation": len(subsets), "cache_resident": bool(args.resident),
+                       "batch_order": "slot order" if args.sorted_batch else "as drawn"},
                 pool_bytes=pool.pool_bytes)
 
 
@@ -262,6 +266,8 @@ def main():
                     help="untimed steps before the warmup until this much GPU time has elapsed (clock ramp)")
     ap.add_argument("--workload", choices=["pool_b512", "pool_4bit", "stack48"], default="pool_b512")
     ap.add_argument("--resident", action="store_true", help="no slot rotation (cache-resident number)")
+    ap.add_argument("--sorted-batch", action="store_true",
+                    help="list each step's active requests in slot order (pool workloads; default: as drawn)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-ref", action="store_true", help="also time a plain device copy of the same bytes")
