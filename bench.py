@@ -118,17 +118,30 @@ def cpu_baseline(w, bits, seconds: float):
                          inp["v"][rows].double().numpy().reshape(n, w.d_v),
                          inp["alpha"][rows].double().numpy().reshape(n),
                          inp["beta"][rows].double().numpy().reshape(n)))
-    done, step, elapsed = 0, 0, 0.0
-    while elapsed < seconds:
-        q, k, v, a, b = steps_in[step % len(steps_in)]
-        ts = time.perf_counter()
-        codes, _ = oracle.decode_step(codes, r, c, tb, q, k, v, a, b)
-        elapsed += time.perf_counter() - ts
-        done += n
-        step += 1
-    return {"value": done / elapsed, "unit": "state-updates/s", "cores": oracle.max_threads(), "kind": "oracle",
+    def timed(budget):
+        nonlocal codes
+        done, step, elapsed = 0, 0, 0.0
+        while elapsed < budget:
+            q, k, v, a, b = steps_in[step % len(steps_in)]
+            ts = time.perf_counter()
+            codes, _ = oracle.decode_step(codes, r, c, tb, q, k, v, a, b)
+            elapsed += time.perf_counter() - ts
+            done += n
+            step += 1
+        return done / elapsed, step, elapsed
+
+    cores = oracle.max_threads()
+    value, step, elapsed = timed(seconds)
+    oracle.set_threads(1)
+    try:
+        one, step1, elapsed1 = timed(seconds / 3)
+    finally:
+        oracle.set_threads(cores)
+    return {"value": value, "unit": "state-updates/s", "cores": cores, "kind": "oracle",
             "sample": f"{step} decode steps x {n} tiles (16 requests x {w.n_v_heads} heads) of {w.name}, "
-                      f"{elapsed:.1f} s of oracle time (4 distinct input steps cycled, draws excluded)"}
+                      f"{elapsed:.1f} s of oracle time (4 distinct input steps cycled, draws excluded)",
+            "single_core": {"value": one, "unit": "state-updates/s", "cores": 1,
+                            "sample": f"{step1} decode steps of the same tiles, {elapsed1:.1f} s"}}
 
 
 def traffic_entry(mode, kda: bool, workload: str = "pool_b512", pivots: bool = False):

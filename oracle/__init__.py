@@ -65,6 +65,8 @@ def lib():
         L.orc_pack_pool.argtypes = [i, i, i, i, P, P, P, P, P, P]
         L.orc_unpack_pool.argtypes = [i, i, i, i, P, P, P, P, P, P]
         L.orc_max_threads.restype = ctypes.c_int
+        L.orc_set_threads.argtypes = [ctypes.c_int]
+        L.orc_set_threads.restype = None
         _lib = L
     return _lib
 
@@ -79,6 +81,11 @@ def _c(a, dtype):
 
 def max_threads() -> int:
     return int(lib().orc_max_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's tile loops from now on (timing only)."""
+    lib().orc_set_threads(int(n))
 
 
 # Level normalisation of the stored integers (Section 4.3, Appendix C.1):

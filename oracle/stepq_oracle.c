@@ -812,3 +812,14 @@ int orc_max_threads(void)
     return 1;
 #endif
 }
+
+/* Threads of the tile loops from now on (n >= 1); for timing only. */
+void orc_set_threads(int n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    if (n >= 1) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
