@@ -53,8 +53,17 @@
  *    slots, which stay unused (the paper's serving layout omits them).
  *  - Row groups: each group holds 8/b physical integer rows of one width b --
  *    one 8-bit row, two 4-bit rows or four 2-bit rows -- filled in physical
- *    order.  A width's last group may have empty slots.  Groups are ordered
- *    8-bit, 4-bit, 2-bit: G = n8 + ceil(n4/2) + ceil(n2/4).
+ *    order.  Groups are ordered 8-bit, 4-bit, 2-bit, with G8, G4, G2 groups
+ *    of each width, G = G8 + G4 + G2.  Normally G8 = n8, G4 = ceil(n4/2),
+ *    G2 = ceil(n2/4), and a width's last group may have empty slots.  At
+ *    d_k = d_v = 128 (whole-FP16 heads aside) the integer rows may fit one
+ *    of the uniform mixes, in units of 8 groups {8-bit, 4-bit, 2-bit}:
+ *    {8,4,0}, {4,2,2}, {16,0,0}, {0,8,0}, {0,0,4}.  The first mix in this
+ *    order with 8 m8 >= n8, 16 m4 >= n4 and 32 m2 >= n2 then sets
+ *    G8 = 8 m8, G4 = 8 m4, G2 = 8 m2: each width's rows fill its groups from
+ *    the first, and the groups after them stay empty.  Without pivot rows
+ *    this is exactly the tight layout; a head with pivot rows is padded to
+ *    the mix, so that the compiled decode body for that mix can run it.
  *  - Codes region: G groups of d_v bytes each.  Byte j of a group holds
  *    column j of all its rows: the row in slot s (0-based, in physical
  *    order) occupies bits [s*b, s*b + b) as a b-bit two's-complement integer

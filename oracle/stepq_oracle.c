@@ -650,12 +650,37 @@ static void class_counts(int dk, const uint8_t *bits, int *n16, int *n8, int *n4
     }
 }
 
-static size_t codes_region(int dk, int dv, const uint8_t *bits)
+/* Row groups of each width class.  Tight (one per 8-bit row, per two 4-bit
+ * rows, per four 2-bit rows), except at d_k = d_v = 128 (whole-FP16 heads
+ * aside): integer rows that fit one of the uniform mixes, in word-steps of
+ * 8 groups {8-bit, 4-bit, 2-bit} and taken in this order, get exactly that
+ * mix's group counts, the classes padded with empty groups. */
+static const int uniform_mix[5][3] = {{8, 4, 0}, {4, 2, 2}, {16, 0, 0}, {0, 8, 0}, {0, 0, 4}};
+
+static void class_groups(int dk, int dv, const uint8_t *bits, int *g8, int *g4, int *g2)
 {
     int n16, n8, n4, n2;
     class_counts(dk, bits, &n16, &n8, &n4, &n2);
-    size_t groups = (size_t)n8 + (size_t)(n4 + 1) / 2 + (size_t)(n2 + 3) / 4;
-    return round128(groups * (size_t)dv);
+    *g8 = n8;
+    *g4 = (n4 + 1) / 2;
+    *g2 = (n2 + 3) / 4;
+    if (dk != 128 || dv != 128 || n16 == dk) return;
+    for (int L = 0; L < 5; ++L) {
+        const int *m = uniform_mix[L];
+        if (8 * m[0] >= n8 && 16 * m[1] >= n4 && 32 * m[2] >= n2) {
+            *g8 = 8 * m[0];
+            *g4 = 8 * m[1];
+            *g2 = 8 * m[2];
+            return;
+        }
+    }
+}
+
+static size_t codes_region(int dk, int dv, const uint8_t *bits)
+{
+    int g8, g4, g2;
+    class_groups(dk, dv, bits, &g8, &g4, &g2);
+    return round128((size_t)(g8 + g4 + g2) * (size_t)dv);
 }
 
 static size_t pivot_region(int dk, int dv, const uint8_t *bits)
@@ -673,16 +698,18 @@ size_t orc_tile_bytes(int dk, int dv, const uint8_t *bits)
 /* logical row of each physical row, and the (group, slot) position of each
  * logical integer row inside the codes region (pivot rows: their index
  * among the pivot rows in group, slot -1) */
-static void row_positions(int dk, const uint8_t *bits, int *phys_to_log, int *group, int *slot)
+static void row_positions(int dk, int dv, const uint8_t *bits, int *phys_to_log, int *group, int *slot)
 {
-    int n16, n8, n4, n2;
+    int n16, n8, n4, n2, c8, c4, c2;
     class_counts(dk, bits, &n16, &n8, &n4, &n2);
+    class_groups(dk, dv, bits, &c8, &c4, &c2);
     int p = 0;
     static const int order[4] = {16, 8, 4, 2};
     for (int cl = 0; cl < 4; ++cl)
         for (int i = 0; i < dk; ++i)
             if (bits[i] == order[cl]) phys_to_log[p++] = i;
-    int g4 = n8, g2 = n8 + (n4 + 1) / 2;
+    int g4 = c8, g2 = c8 + c4;                     /* first 4-bit and 2-bit groups */
+    (void)c2;
     for (int pp = 0; pp < dk; ++pp) {
         int i = phys_to_log[pp];
         int q = pp - n16;                          /* index among the integer rows */
@@ -704,7 +731,7 @@ void orc_pack_tile(int dk, int dv, const uint8_t *bits, const int8_t *codes, con
     memset(rec, 0, tb);
     int *p2l = (int *)malloc(sizeof(int) * dk * 3);
     int *grp = p2l + dk, *slt = p2l + 2 * dk;
-    row_positions(dk, bits, p2l, grp, slt);
+    row_positions(dk, dv, bits, p2l, grp, slt);
     for (int i = 0; i < dk; ++i) {
         int b = bits[i];
         if (b == 16) {
@@ -736,7 +763,7 @@ void orc_unpack_tile(int dk, int dv, const uint8_t *bits, const uint8_t *rec, in
     size_t preg = pivot_region(dk, dv, bits);
     int *p2l = (int *)malloc(sizeof(int) * dk * 3);
     int *grp = p2l + dk, *slt = p2l + 2 * dk;
-    row_positions(dk, bits, p2l, grp, slt);
+    row_positions(dk, dv, bits, p2l, grp, slt);
     for (int i = 0; i < dk; ++i) {
         int b = bits[i];
         if (b == 16) {

@@ -76,35 +76,38 @@ struct GroupRows {
 };
 
 // Physical rows: the n16 pivot rows first, then the integer rows 8, 4, 2;
-// the row table and the groups cover the integer rows only.
+// the row table and the groups cover the integer rows only.  A width class
+// may hold more groups than its rows fill (g8 > n8, or a padded 4- or 2-bit
+// class): its slots past the class's last row are empty (p0 + s >= pend)
+// and their codes stay 0.
 __device__ __forceinline__ GroupRows group_rows(const HeadInfo &hi, int g)
 {
     const int P = hi.n16;
     if (g < hi.g8) return {8, 1, P + g, P + hi.n8, g};
     if (g < hi.g8 + hi.g4) {
         const int k = g - hi.g8;
-        return {4, 2, P + hi.n8 + 2 * k, P + hi.n8 + hi.n4, hi.n8 + 2 * k};
+        return {4, 2, P + hi.n8 + 2 * k, P + hi.n8 + hi.n4, hi.g8 + 2 * k};
     }
     const int k = g - hi.g8 - hi.g4;
-    return {2, 4, P + hi.n8 + hi.n4 + 4 * k, P + hi.n8 + hi.n4 + hi.n2, hi.n8 + 2 * hi.g4 + 4 * k};
+    return {2, 4, P + hi.n8 + hi.n4 + 4 * k, P + hi.n8 + hi.n4 + hi.n2, hi.g8 + 2 * hi.g4 + 4 * k};
 }
 
 // Row-table slot x -> physical row (or -1 for an empty slot) and its width.
 __device__ __forceinline__ int slot_row(const HeadInfo &hi, int x, int &bw)
 {
     const int P = hi.n16;
-    if (x < hi.n8) {
+    if (x < hi.g8) {
         bw = 8;
-        return P + x;
+        return x < hi.n8 ? P + x : -1;
     }
-    if (x < hi.n8 + 2 * hi.g4) {
+    if (x < hi.g8 + 2 * hi.g4) {
         bw = 4;
-        const int kk = x - hi.n8;
+        const int kk = x - hi.g8;
         return kk < hi.n4 ? P + hi.n8 + kk : -1;
     }
     bw = 2;
-    if (x < hi.n8 + 2 * hi.g4 + 4 * hi.g2) {
-        const int kk = x - hi.n8 - 2 * hi.g4;
+    if (x < hi.g8 + 2 * hi.g4 + 4 * hi.g2) {
+        const int kk = x - hi.g8 - 2 * hi.g4;
         return kk < hi.n2 ? P + hi.n8 + hi.n4 + kk : -1;
     }
     return -1;
@@ -200,6 +203,7 @@ struct TileCtx {
     int tile, b, h, hq;
     uint32_t off;            // byte offset of the tile in its slot record (uniform bodies)
     int layout;              // the head's uniform layout (1-based) or 0, when the launch has a head list
+    int counts;              // n16 | n8 << 8 | n4 << 16 of the head (from the head list)
     HeadInfo hi;
     uint32_t *codes;
     const float *rr, *cc;
@@ -220,10 +224,12 @@ __device__ __forceinline__ void tile_of(const DecodeArgs &a, uint32_t tile_bytes
         t.h = lh.h;
         t.off = lh.tile_off;
         t.layout = lh.layout;
+        t.counts = lh.counts;
     } else {
         t.h = j;
         t.off = static_cast<uint32_t>(j) * tile_bytes;
         t.layout = 0;
+        t.counts = 0;
     }
     t.tile = t.b * a.pool.Hv + t.h;
     t.hq = fdiv(t.h, a.pool.div_g);
@@ -481,6 +487,98 @@ __device__ __forceinline__ float row_constants_mfma(float beta, const RowColOps 
             const int c = (p - X2) >> 2;
             slice = c & 7;
             ridx = M8 + 2 * M4 + 4 * (c >> 3) + ((p - X2) & 3);
+        }
+        const float ks = __builtin_amdgcn_ldexpf(kt, ek), qs = __builtin_amdgcn_ldexpf(qt, eq);
+        const _Float16 kh = static_cast<_Float16>(ks), qh = static_cast<_Float16>(qs);
+        const _Float16 kl = static_cast<_Float16>(ks - static_cast<float>(kh));
+        const _Float16 ql = static_cast<_Float16>(qs - static_cast<float>(qh));
+        _Float16(&dst)[4][4] = sh.aop[slice][ridx >> 2];
+        dst[0][ridx & 3] = kh;
+        dst[1][ridx & 3] = kl;
+        dst[2][ridx & 3] = qh;
+        dst[3][ridx & 3] = ql;
+    }
+    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(kappa)));
+}
+
+// row_constants_mfma for a padded pivot head (layout code
+// kPivotUniformBase + L): physical rows are the hi.n16 pivot rows, then the
+// integer rows; table slot x = tid maps to its physical row through
+// slot_row (empty slots get zero weights and update factors, so their zero
+// codes stay zero).  Also the pivot rows' constants (pvc) and c (cpiv), as
+// in row_constants.  Two barriers; the operand table needs one more.
+template <bool DIAG, int M8, int M4, int M2, int DV>
+__device__ __forceinline__ float row_constants_mfma_piv(const HeadInfo &hi, float alpha, float beta,
+                                                        const RowColOps &op, DecodeShared<DV> &sh,
+                                                        const LevelTable &lv, int &ek, int &eq)
+{
+    const int tid = threadIdx.x;
+    if (tid < 128) {
+        sh.sk[tid] = op.k;
+        sh.sq[tid] = op.q;
+        sh.sr[tid] = op.r;
+        sh.sperm[tid] = op.perm;
+        sh.cpiv[tid] = op.c;
+        if constexpr (DIAG) sh.sd[tid] = op.d;
+    }
+    __syncthreads();
+    float kq = 0.f, kt = 0.f, qt = 0.f;
+    if (tid < hi.n16) {
+        // pivot row p = tid: its constants and its share of q.k
+        const int i = sh.sperm[tid];
+        const float d = DIAG ? sh.sd[i] : alpha;
+        const float kd = DIAG ? sh.sk[i] * d : sh.sk[i];     // the scalar gate is applied with the columns
+        const float qd = DIAG ? sh.sq[i] * d : sh.sq[i];
+        sh.pvc[tid] = make_float4(kd, qd, d, beta * sh.sk[i]);
+        kq = sh.sq[i] * sh.sk[i];
+    }
+    if (tid < 128) {
+        const int x = tid;
+        int bw;
+        const int p = slot_row(hi, x, bw);
+        float av = 0.f, al = 0.f;
+        if (p >= 0) {
+            const int wi = bw == 8 ? 0 : (bw == 4 ? 1 : 2);
+            const int i = sh.sperm[p];
+            const float r = sh.sr[p];
+            const float ki = sh.sk[i], qi = sh.sq[i];
+            const float di = DIAG ? sh.sd[i] : 1.0f;
+            const float rs = r * lv.fq[wi] * di;
+            kt = ki * rs;
+            qt = qi * rs;
+            av = beta * ki * lv.iq[wi] * __builtin_amdgcn_rcpf(r);
+            al = di * (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
+            kq += qi * ki;
+        }
+        sh.av[x] = av;
+        if constexpr (DIAG) sh.al[x] = al;
+    }
+    kq = wave_sum(kq);
+    const float mk = wave_max(fabsf(kt)), mq = wave_max(fabsf(qt));
+    if ((tid & 63) == 0) {
+        sh.kap[tid >> 6] = kq;
+        sh.wmx[tid >> 6] = make_float2(mk, mq);
+    }
+    __syncthreads();
+    const float2 w0 = sh.wmx[0], w1 = sh.wmx[1];     // the table slots live in wavefronts 0 and 1
+    ek = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(w0.x, w1.x)));
+    eq = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(w0.y, w1.y)));
+    const float kappa = (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
+    if (tid < 128) {
+        constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
+        const int x = tid;
+        int slice, ridx;
+        if (x < X4) {
+            slice = x & 7;
+            ridx = x >> 3;
+        } else if (x < X2) {
+            const int c = (x - X4) >> 1;
+            slice = c & 7;
+            ridx = M8 + 2 * (c >> 3) + ((x - X4) & 1);
+        } else {
+            const int c = (x - X2) >> 2;
+            slice = c & 7;
+            ridx = M8 + 2 * M4 + 4 * (c >> 3) + ((x - X2) & 3);
         }
         const float ks = __builtin_amdgcn_ldexpf(kt, ek), qs = __builtin_amdgcn_ldexpf(qt, eq);
         const _Float16 kh = static_cast<_Float16>(ks), qh = static_cast<_Float16>(qs);

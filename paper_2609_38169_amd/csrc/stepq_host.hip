@@ -99,15 +99,22 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
         hi.g8 = static_cast<uint16_t>(n8);
         hi.g4 = static_cast<uint16_t>((n4 + 1) / 2);
         hi.g2 = static_cast<uint16_t>((n2 + 3) / 4);
-        hi.groups = static_cast<uint32_t>(hi.g8 + hi.g4 + hi.g2);
         hi.layout = 0;
-        // compile-time bodies: d = 128, whole word-steps of one width, no empty slots
-        if (dv == 128 && dk == 128 && n16 == 0 && n4 == 2 * hi.g4 && n2 == 4 * hi.g2 && hi.g8 % 8 == 0 && hi.g4 % 8 == 0 &&
-            hi.g2 % 8 == 0)
+        // At d = 128, integer rows that fit a uniform mix (first in table
+        // order) are stored in it: exactly, or, when pivot rows take some of
+        // the 128, with each width class padded by empty groups.
+        if (dv == 128 && dk == 128 && !f16_head)
             for (int L = 0; L < stepq::kNumUniformLayouts; ++L) {
                 const stepq::UniformLayout &u = stepq::kUniformLayouts[L];
-                if (u.m8 * 8 == hi.g8 && u.m4 * 8 == hi.g4 && u.m2 * 8 == hi.g2) hi.layout = L + 1;
+                if (8 * u.m8 < n8 || 16 * u.m4 < n4 || 32 * u.m2 < n2) continue;
+                hi.g8 = static_cast<uint16_t>(8 * u.m8);
+                hi.g4 = static_cast<uint16_t>(8 * u.m4);
+                hi.g2 = static_cast<uint16_t>(8 * u.m2);
+                if (n16 == 0) hi.layout = L + 1;
+                else if (n16 <= stepq::kCompactPivots) hi.layout = stepq::kPivotUniformBase + L + 1;
+                break;
             }
+        hi.groups = static_cast<uint32_t>(hi.g8 + hi.g4 + hi.g2);
         if (f16_head) hi.layout = stepq::kF16HeadLayout;
         const size_t creg = round128(static_cast<size_t>(hi.groups) * dv);
         const size_t preg = round128(static_cast<size_t>(n16) * 2u * dv);
@@ -122,6 +129,12 @@ stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads
             const uint32_t m = static_cast<uint32_t>(u.m8 + u.m4 + u.m2);
             if (hi.r_off != 1024u * m || hi.tile_bytes != 1024u * (m + 1))
                 return fail(STEPQ_E_INVALID, "internal: uniform head layout does not match its tile size");
+        }
+        if (static_cast<int>(hi.layout) > stepq::kPivotUniformBase) {
+            const stepq::UniformLayout &u = stepq::kUniformLayouts[hi.layout - stepq::kPivotUniformBase - 1];
+            const uint32_t m = static_cast<uint32_t>(u.m8 + u.m4 + u.m2);
+            if (hi.piv_off != 1024u * m || hi.r_off != 1024u * m + 256u * n16 || hi.tile_bytes != hi.r_off + 1024u)
+                return fail(STEPQ_E_INVALID, "internal: padded pivot head layout does not match its tile size");
         }
         if (static_cast<int>(hi.layout) == stepq::kF16HeadLayout &&
             (hi.piv_off != 0 || hi.r_off != 128u * 256u || hi.tile_bytes != 128u * 256u + 1024u))
@@ -262,6 +275,8 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
     p->layout = static_cast<int>(p->heads[0].layout);
     for (const HeadInfo &hi : p->heads)
         if (static_cast<int>(hi.layout) != p->layout) p->layout = 0;
+    // padded pivot heads differ in their row counts, which travel in the head list
+    if (p->layout > stepq::kPivotUniformBase) p->layout = 0;
     p->pool_bytes = p->slot_bytes * static_cast<size_t>(p->n_slots);
     hipError_t e = hipGetDevice(&p->device);
     if (e != hipSuccess) {
@@ -300,7 +315,10 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
         // one class per layout present; larger classes are launched first
         std::vector<stepq::LaunchHead> order;
         std::vector<std::pair<int, int>> cls;   // (-count, layout)
-        for (int L = 0; L <= stepq::kF16HeadLayout; ++L) {
+        std::vector<int> codes;
+        for (int L = 0; L <= stepq::kF16HeadLayout; ++L) codes.push_back(L);
+        for (int L = 1; L <= stepq::kNumUniformLayouts; ++L) codes.push_back(stepq::kPivotUniformBase + L);
+        for (int L : codes) {
             int n = 0;
             for (const HeadInfo &hi : p->heads) n += static_cast<int>(hi.layout) == L;
             if (n > 0) cls.emplace_back(-n, L);
@@ -320,26 +338,37 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
             p->cls_layout.push_back(code);
             p->cls_off.push_back(static_cast<int>(order.size()));
             p->cls_cnt.push_back(-c.first);
-            for (int h = 0; h < p->Hv; ++h)
-                if (static_cast<int>(p->heads[h].layout) == c.second)
-                    order.push_back({h, p->heads[h].tile_off, static_cast<int32_t>(p->heads[h].layout), 0});
+            for (int h = 0; h < p->Hv; ++h) {
+                const HeadInfo &hi = p->heads[h];
+                if (static_cast<int>(hi.layout) != c.second) continue;
+                const int32_t counts = static_cast<int32_t>(hi.n16 | (hi.n8 << 8) | (hi.n4 << 16));
+                order.push_back({h, hi.tile_off, static_cast<int32_t>(hi.layout), counts});
+            }
         }
-        // one uniform class of layout 1 or 2 whose other classes are compact
-        // generic or whole FP16 heads: a decode step is one combined launch
-        int L = 0, others = 0;
+        // one uniform class of layout 1 or 2 whose other classes are its
+        // padded pivot heads, compact generic or whole FP16 heads: a decode
+        // step is one combined launch
+        int L = 0, others = 0, pivots = 0;
         bool fits = true, f16 = false;
-        for (int code : p->cls_layout) {
+        for (int code : p->cls_layout)
             if (code == 1 || code == 2) {
                 if (L != 0) fits = false;
                 L = code;
-            } else if (code == stepq::kCompactGeneric || code == stepq::kF16HeadLayout) {
+            }
+        for (int code : p->cls_layout) {
+            if (code == 1 || code == 2) continue;
+            if (code == stepq::kCompactGeneric || code == stepq::kF16HeadLayout ||
+                (L != 0 && code == stepq::kPivotUniformBase + L)) {
                 ++others;
                 f16 = f16 || code == stepq::kF16HeadLayout;
+                pivots += code == stepq::kPivotUniformBase + L;
             } else {
                 fits = false;
             }
         }
-        if (fits && L != 0 && others > 0) p->mixed_code = (f16 ? stepq::kMixedF16Base : stepq::kMixedBase) + L;
+        if (fits && L != 0 && others > 0)
+            p->mixed_code = others == pivots ? stepq::kMixedPivotBase + L
+                                             : (f16 ? stepq::kMixedF16Base : stepq::kMixedBase) + L;
         e = hipMalloc(reinterpret_cast<void **>(&p->d_head_order), sizeof(stepq::LaunchHead) * order.size());
         if (e == hipSuccess)
             e = hipMemcpy(p->d_head_order, order.data(), sizeof(stepq::LaunchHead) * order.size(),

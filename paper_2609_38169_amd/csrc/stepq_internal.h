@@ -41,10 +41,10 @@ constexpr int kNumUniformLayouts = sizeof(kUniformLayouts) / sizeof(kUniformLayo
 // and c slots.
 constexpr int kF16HeadLayout = kNumUniformLayouts + 1;
 
-// Row-constant table index space: 8-bit rows, then the two slots of every
-// 4-bit group, then the four slots of every 2-bit group (empty slots
-// included), so group g / slot s maps to one index without a lookup.
-// Its size is at most d_k + 4.
+// Row-constant table index space: the slots of the 8-bit groups, then the
+// two slots of every 4-bit group, then the four slots of every 2-bit group
+// (empty slots included), so group g / slot s maps to one index without a
+// lookup.  Its size is at most d_k + 4.
 constexpr int kMaxDk = 128;
 constexpr int kSlotTable = kMaxDk + 4;
 constexpr int kMaxPivots = 32;    // FP16 pivot rows per head
@@ -58,6 +58,16 @@ constexpr int kMixedBase = 8;
 constexpr int kMixedF16Base = 16;
 constexpr int kCompactGroups = 96;
 constexpr int kCompactPivots = 8;
+// Layout code kPivotUniformBase + L: a head with 1 .. kCompactPivots FP16
+// pivot rows whose integer rows are stored in uniform layout L, each width
+// class padded with empty groups (zero codes) to L's group counts; the
+// uniform decode body runs it with the pivot rows added, taking the row
+// counts from its LaunchHead.
+constexpr int kPivotUniformBase = 32;
+// Layout code kMixedPivotBase + L (L = 1, 2): uniform layout-L heads and
+// layout-L padded pivot heads only, in one decode launch of one body (a
+// layout-L head is a padded pivot head without pivot rows).
+constexpr int kMixedPivotBase = 24;
 
 // n / d for 0 <= n < 2^31 by multiply-high (Granlund-Montgomery), with the
 // constants prepared on the host so that uniform quotients stay scalar.
@@ -92,7 +102,7 @@ struct LaunchHead {
     int32_t h;
     uint32_t tile_off;
     int32_t layout;          // the head's uniform layout (1-based), or 0
-    int32_t pad;
+    int32_t counts;          // n16 | n8 << 8 | n4 << 16 (read for padded pivot and uniform heads)
 };
 
 struct DecodeArgs {
@@ -133,9 +143,11 @@ struct TileArgs {
 // launch (a.head_list), 0 for the generic body (irregular row-width mixes,
 // FP16 pivot rows, d_v = 64), kCompactGeneric when every head of the launch
 // fits the compact generic body's bounds, kF16HeadLayout for whole FP16
-// heads, or kMixedBase + L / kMixedF16Base + L (decode step only) for
-// uniform layout-L heads mixed with compact generic (and whole FP16) heads.  The
-// refitting steps take their generic body for kCompactGeneric.
+// heads, kPivotUniformBase + L for uniform-layout heads with pivot rows, or
+// kMixedBase + L / kMixedF16Base + L (decode step only) for uniform layout-L
+// heads mixed with such pivot heads, compact generic (and whole FP16) heads.
+// The refitting steps take their generic body for kCompactGeneric and
+// kPivotUniformBase + L.
 // diag: a.alpha holds the channel-wise gate [batch][Hv][d_k] instead of the
 // scalar gate [batch][Hv].
 hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);

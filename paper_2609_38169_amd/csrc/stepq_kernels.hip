@@ -34,7 +34,9 @@ namespace {
 // threads that share their rows: A = the rows' k and q weights split into
 // binary16 hi + lo parts (4 types), B = the old codes of the 4 threads'
 // columns, so each thread receives the 4 weighted sums of its column.
-template <bool BF16, bool DIAG, int M8, int M4, int M2>
+// PIV: a padded pivot head (up to kCompactPivots FP16 pivot rows beside
+// the padded uniform mix; t.hi holds its row counts and pivot offset).
+template <bool BF16, bool DIAG, int M8, int M4, int M2, bool PIV = false>
 __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCtx &t, DecodeShared<128> &sh)
 {
     constexpr int M = M8 + M4 + M2;
@@ -47,20 +49,46 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
     uint32_t w[M];
 #pragma unroll
     for (int m = 0; m < M; ++m) w[m] = cw.load_m(tid, m);
+    PivotRegs<128, kCompactPivots> pr;
+    if constexpr (PIV) pivot_load<128, kCompactPivots>(t, slice, cg, pr);
 
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
     int ek, eq;
-    const float kappa = row_constants_mfma<DIAG, M8, M4, M2, 128>(t.beta, op, sh, a.pool.lv, ek, eq);
+    float kappa;
+    if constexpr (PIV)
+        kappa = row_constants_mfma_piv<DIAG, M8, M4, M2, 128>(t.hi, t.alpha, t.beta, op, sh, a.pool.lv, ek, eq);
+    else
+        kappa = row_constants_mfma<DIAG, M8, M4, M2, 128>(t.beta, op, sh, a.pool.lv, ek, eq);
 
     uint32_t Ub[4][4][2];
     unpack_row_pairs<M8, M4, M2>(w, Ub);
     __syncthreads();    // operand table written
     matvec_partials(sh, slice, cg, Ub, ek, eq);
+    if constexpr (PIV) {
+        // pivot row p = slice (at most one per thread: kCompactPivots = 8
+        // slices): its share k_i S_pj / c_j and q_i S_pj / c_j (the column
+        // phase multiplies by c_j), added to this thread's own partials
+        static_assert(PivotRegs<128, kCompactPivots>::M == 1, "one pivot row per thread");
+        if (slice < t.hi.n16) {
+            const float4 c4 = *reinterpret_cast<const float4 *>(&sh.cpiv[4 * cg]);
+            const uint32_t lo = pr.v[0].x, hi = pr.v[0].y;
+            const float sv[4] = {half_lo(lo) * __builtin_amdgcn_rcpf(c4.x), half_hi(lo) * __builtin_amdgcn_rcpf(c4.y),
+                                 half_lo(hi) * __builtin_amdgcn_rcpf(c4.z), half_hi(hi) * __builtin_amdgcn_rcpf(c4.w)};
+            const float4 kp = sh.pvc[slice];
+            float4 &rk = sh.red[0][slice][cg];
+            rk = make_float4(fmaf(kp.x, sv[0], rk.x), fmaf(kp.x, sv[1], rk.y), fmaf(kp.x, sv[2], rk.z),
+                             fmaf(kp.x, sv[3], rk.w));
+            float4 &rq = sh.red[1][slice][cg];
+            rq = make_float4(fmaf(kp.y, sv[0], rq.x), fmaf(kp.y, sv[1], rq.y), fmaf(kp.y, sv[2], rq.z),
+                             fmaf(kp.y, sv[3], rq.w));
+        }
+    }
 
     column_sums<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, op.c, op.v);
 
     const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
+    if constexpr (PIV) pivot_update<128, kCompactPivots>(t, slice, cg, pr, sh, bc);
 #pragma unroll
     for (int m = 0; m < M8; ++m)
         cw.store_m(tid, m, requant_word_p<8, DIAG>(Ub, m, sh.av, sh.al, slice + 8 * m, t.alpha, bc));
@@ -241,6 +269,30 @@ __device__ __forceinline__ void run_uniform(const DecodeArgs &a, TileCtx &t, int
     decode_uniform<BF16, DIAG, u.m8, u.m4, u.m2>(a, t, sh);
 }
 
+// A padded pivot head of uniform layout L: codes (1024 bytes per
+// word-step), the n16 pivot rows (256 bytes each), r, c; its row counts
+// come from the head list.
+template <bool BF16, bool DIAG, int L>
+__device__ __forceinline__ void run_uniform_piv(const DecodeArgs &a, TileCtx &t, int slot, DecodeShared<128> &sh)
+{
+    constexpr UniformLayout u = kUniformLayouts[L - 1];
+    constexpr uint32_t piv_off = 1024u * (u.m8 + u.m4 + u.m2);
+    const int n16 = t.counts & 0xff, n8 = (t.counts >> 8) & 0xff, n4 = (t.counts >> 16) & 0xff;
+    t.hi.n16 = static_cast<uint16_t>(n16);
+    t.hi.n8 = static_cast<uint16_t>(n8);
+    t.hi.n4 = static_cast<uint16_t>(n4);
+    t.hi.n2 = static_cast<uint16_t>(128 - n16 - n8 - n4);
+    t.hi.g8 = static_cast<uint16_t>(8 * u.m8);
+    t.hi.g4 = static_cast<uint16_t>(8 * u.m4);
+    t.hi.g2 = static_cast<uint16_t>(8 * u.m2);
+    t.hi.piv_off = piv_off;
+    uint8_t *rec = a.pool.base + static_cast<uint64_t>(slot) * a.pool.slot_bytes + t.off;
+    t.codes = reinterpret_cast<uint32_t *>(rec);
+    t.rr = reinterpret_cast<const float *>(rec + piv_off + 256u * static_cast<uint32_t>(n16));
+    t.cc = t.rr + 128;
+    decode_uniform<BF16, DIAG, u.m8, u.m4, u.m2, true>(a, t, sh);
+}
+
 template <bool BF16, bool DIAG, int DV, bool COMPACT>
 __device__ __forceinline__ void run_generic(const DecodeArgs &a, TileCtx &t, int slot, DecodeShared<DV> &sh)
 {
@@ -263,10 +315,12 @@ __device__ __forceinline__ void run_generic(const DecodeArgs &a, TileCtx &t, int
 // at most kCompactGroups row groups and kCompactPivots pivot rows (d_v =
 // 128), in fewer registers.  LAYOUT == kMixedBase + L: heads of uniform
 // layout L and compact generic heads in one launch, told apart by the head
-// list (both bodies fit the same register budget); kMixedF16Base + L: the
-// same with whole FP16 heads too.  LAYOUT ==
-// kF16HeadLayout: heads held entirely in FP16 (every mode; the host sets
-// a.f16_c_one for the row-absmax step).
+// list (both bodies fit the same register budget), together with layout-L
+// padded pivot heads; kMixedF16Base + L: the same with whole FP16 heads too.
+// LAYOUT == kMixedPivotBase + L: uniform layout-L heads and layout-L padded
+// pivot heads only.  LAYOUT == kPivotUniformBase + L: padded pivot heads of
+// uniform layout L only.  LAYOUT == kF16HeadLayout: heads held entirely in FP16 (every mode;
+// the host sets a.f16_c_one for the row-absmax step).
 template <int DV, bool BF16, int LAYOUT, bool DIAG>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 {
@@ -287,16 +341,26 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
         run_uniform<BF16, DIAG, LAYOUT>(a, t, slot, sh);
     } else if constexpr (DV == 128 && LAYOUT == kF16HeadLayout) {
         run_f16head<BF16, DIAG>(a, t, slot, sh);
+    } else if constexpr (DV == 128 && LAYOUT > kPivotUniformBase) {
+        run_uniform_piv<BF16, DIAG, LAYOUT - kPivotUniformBase>(a, t, slot, sh);
+    } else if constexpr (DV == 128 && LAYOUT > kMixedPivotBase) {
+        // one body for both: a layout-L head is a padded pivot head with no pivot rows
+        run_uniform_piv<BF16, DIAG, LAYOUT - kMixedPivotBase>(a, t, slot, sh);
     } else if constexpr (DV == 128 && LAYOUT > kMixedF16Base) {
-        if (t.layout == LAYOUT - kMixedF16Base) {
-            run_uniform<BF16, DIAG, LAYOUT - kMixedF16Base>(a, t, slot, sh);
+        constexpr int L = LAYOUT - kMixedF16Base;
+        if (t.layout == L) {
+            run_uniform<BF16, DIAG, L>(a, t, slot, sh);
+        } else if (t.layout == kPivotUniformBase + L) {
+            run_uniform_piv<BF16, DIAG, L>(a, t, slot, sh);
         } else if (t.layout == kF16HeadLayout) {
             run_f16head<BF16, DIAG>(a, t, slot, sh);
         } else {
             run_generic<BF16, DIAG, 128, true>(a, t, slot, sh);
         }
     } else if constexpr (DV == 128 && LAYOUT > kMixedBase) {
-        if (t.layout == LAYOUT - kMixedBase) run_uniform<BF16, DIAG, LAYOUT - kMixedBase>(a, t, slot, sh);
+        constexpr int L = LAYOUT - kMixedBase;
+        if (t.layout == L) run_uniform<BF16, DIAG, L>(a, t, slot, sh);
+        else if (t.layout == kPivotUniformBase + L) run_uniform_piv<BF16, DIAG, L>(a, t, slot, sh);
         else run_generic<BF16, DIAG, 128, true>(a, t, slot, sh);
     } else {
         run_generic<BF16, DIAG, DV, DV == 128 && LAYOUT == kCompactGeneric>(a, t, slot, sh);
@@ -425,6 +489,27 @@ hipError_t launch_decode_128(const DecodeArgs &a, int layout, unsigned grid, hip
         break;
     case kF16HeadLayout:
         hipLaunchKernelGGL((decode_kernel<128, BF16, kF16HeadLayout, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kPivotUniformBase + 1:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kPivotUniformBase + 1, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kPivotUniformBase + 2:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kPivotUniformBase + 2, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kPivotUniformBase + 3:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kPivotUniformBase + 3, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kPivotUniformBase + 4:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kPivotUniformBase + 4, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kPivotUniformBase + 5:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kPivotUniformBase + 5, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kMixedPivotBase + 1:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kMixedPivotBase + 1, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kMixedPivotBase + 2:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kMixedPivotBase + 2, DIAG>), dim3(grid), dim3(256), 0, s, a);
         break;
     case kMixedBase + 1:
         hipLaunchKernelGGL((decode_kernel<128, BF16, kMixedBase + 1, DIAG>), dim3(grid), dim3(256), 0, s, a);

@@ -41,6 +41,39 @@ def test_pool_bytes_match_oracle_layout(idx):
         assert w.layers * w.n_slots * w.n_v_heads * w.d_k * w.d_v * 4 == 24 * 2 ** 30
 
 
+def test_pivot_heads_padded_to_a_uniform_mix():
+    """Integer rows that fit a uniform mix are stored in it, width classes
+    padded with empty groups: a 6-bit head with 2 pivot rows keeps the
+    12,288-byte codes region of 64 @ 8 + 64 @ 4 (tight it would be 94
+    groups); rows that fit no mix stay tight.  Library and oracle agree."""
+    def head(n16, n8, n4, n2):
+        b = np.array([16] * n16 + [8] * n8 + [4] * n4 + [2] * n2, np.uint8)
+        return np.random.default_rng(n16 + 3 * n8).permutation(b)
+
+    cases = [
+        (head(2, 62, 64, 0), 12288 + 2 * 256 + 1024),             # {8,4,0}: 2 empty 8-bit groups
+        (head(3, 64, 61, 0), 12288 + 3 * 256 + 1024),             # one 4-bit group half empty, one empty
+        (head(8, 30, 30, 60), 8192 + 8 * 256 + 1024),             # {4,2,2}
+        (head(5, 123, 0, 0), 16384 + 5 * 256 + 1024),             # {16,0,0}
+        (head(32, 0, 0, 96), 4096 + 32 * 256 + 1024),             # {0,0,4} with the most pivot rows
+        (head(8, 100, 20, 0), (100 + 10) * 128 + 8 * 256 + 1024),  # fits no mix: tight
+        (head(0, 64, 64, 0), 13312),                              # no pivots: the uniform layout itself
+    ]
+    for bits, tile in cases:
+        bits = bits[None]
+        pb, sb = stepq.stepq_pool_bytes(2, 1, 1, 128, 128, bits)
+        assert sb == tile, (sb, tile)
+        assert oracle.slot_bytes(bits, 128) == tile
+    # the padded groups hold only zero bytes in the oracle's own packing
+    bits = head(2, 62, 64, 0)[None]
+    rng = np.random.default_rng(5)
+    codes = rng.integers(-7, 8, size=(1, 1, 128, 128)).astype(np.int8)
+    img = oracle.pack_pool(codes, np.ones((1, 1, 128), np.float32), np.ones((1, 1, 128), np.float32), bits,
+                           pv=np.zeros((1, 1, 128, 128), np.uint16))
+    assert not img[62 * 128:64 * 128].any()                       # 8-bit groups 62, 63 are empty
+    assert img[64 * 128:96 * 128].any()                           # the 4-bit groups follow at group 64
+
+
 def test_ragged_layout_sizes():
     rng = np.random.default_rng(0)
     for dk, dv in [(37, 64), (96, 128), (1, 64), (128, 128)]:
