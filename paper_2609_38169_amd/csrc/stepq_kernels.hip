@@ -17,9 +17,12 @@
 // Work split: the tile's codes region is a run of 32-bit words; thread t owns
 // words t + 256 m.  At d_v = 128 a row group is 32 words, so a thread always
 // owns the same 4 columns (word t % 32) in groups t/32 + 8 m, and a
-// wavefront's load covers two whole 128-byte groups.  Per-column partial sums
-// of the 8 threads that share a column meet in LDS; one pass over the words
-// kept in registers then rewrites the codes in place.
+// wavefront's load covers two whole 128-byte groups.  In the compiled
+// (uniform-layout) bodies the two sums over i run on the matrix cores, as
+// 4x4x4 binary16 products over the 16 rows a thread holds (decode_uniform);
+// the generic bodies accumulate them with v_fma_mix.  Per-column partial
+// sums of the 8 threads that share a column meet in LDS; one pass over the
+// words kept in registers then rewrites the codes in place.
 //
 // tile_kernel: pack (from fp32 states or raw codes), unpack and dequantize
 // whole tiles; not on the decode path.
