@@ -159,6 +159,13 @@ def traffic_entry(mode, kda: bool, workload: str = "pool_b512", pivots: bool = F
     return b.get("total") if isinstance(b, dict) else b
 
 
+def adjacent_ids(ids) -> bool:
+    """Whether a batch lists adjacent slots in increasing order (then the
+    decode step gets the STEPQ_STEP_ADJACENT_SLOTS scheduling hint)."""
+    d = ids[1:] - ids[:-1]
+    return bool((d == 1).all().item()) if d.numel() else True
+
+
 class Case:
     """One benchmark workload on the device: step(i) enqueues decode step i
     (launches_per_step kernel launches) on the current stream."""
@@ -189,6 +196,7 @@ def pool_case(args, w, mode, dev):
     if args.sorted_batch:
         # the same requests, listed in slot order (a caller-side choice: any batch order is valid)
         subsets = [torch.sort(s).values for s in subsets]
+    adjacent = [adjacent_ids(s) for s in subsets]
     n_inp = min(w.steps, args.steps + args.warmup)
     inputs = [W.step_inputs(w, 0, t, device=dev) for t in range(n_inp)]
     if args.kda:
@@ -202,7 +210,8 @@ def pool_case(args, w, mode, dev):
         if key not in prepared:
             inp = inputs[key[0]]
             prepared[key] = pool.prepare_step(subsets[key[1]], inp["q"], inp["k"], inp["v"], inp["alpha"],
-                                              inp["beta"], o, stream=torch.cuda.current_stream(), refit=mode)
+                                              inp["beta"], o, stream=torch.cuda.current_stream(), refit=mode,
+                                              adjacent=adjacent[key[1]])
         prepared[key]()
 
     mix = {"pool_b512": "6-bit mixed {4,8}", "pool_4bit": "4-bit mixed {2,4,8}, heavy-tailed states"}[w.name]
@@ -216,7 +225,8 @@ def pool_case(args, w, mode, dev):
                 workload=f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
                          f"d_k=d_v={w.d_k}, {mix}, fp32 scales, bf16 activations",
                 extra={"slot_rotation": len(subsets), "cache_resident": bool(args.resident),
-                       "batch_order": "slot order" if args.sorted_batch else "as drawn"},
+                       "batch_order": "slot order" if args.sorted_batch else "as drawn",
+                       "adjacent_slots_hint": bool(all(adjacent))},
                 pool_bytes=pool.pool_bytes)
 
 
@@ -244,9 +254,10 @@ def stack_case(args, w, mode, dev):
     side = torch.cuda.Stream()
     side.wait_stream(main_stream)
     graph = torch.cuda.CUDAGraph()
+    adjacent = adjacent_ids(slots)
     with torch.cuda.stream(side):
         calls = [pools[L].prepare_step(slots, bufs[L]["q"], bufs[L]["k"], bufs[L]["v"], bufs[L]["alpha"],
-                                       bufs[L]["beta"], bufs[L]["o"], stream=side, refit=mode)
+                                       bufs[L]["beta"], bufs[L]["o"], stream=side, refit=mode, adjacent=adjacent)
                  for L in range(w.layers)]
         with torch.cuda.graph(graph, stream=side):
             for c in calls:
@@ -266,7 +277,7 @@ def stack_case(args, w, mode, dev):
                          f"({w.n_qk_heads} q/k heads), d_k=d_v={w.d_k}, 6-bit mixed {{4,8}}, fp32 scales, "
                          f"bf16 activations, one HIP graph of {w.layers} launches per step",
                 extra={"graph_launches_per_step": w.layers, "pool_bytes": pool_bytes, "fp32_pool_bytes": fp32_bytes,
-                       "pool_compression": fp32_bytes / pool_bytes},
+                       "pool_compression": fp32_bytes / pool_bytes, "adjacent_slots_hint": adjacent},
                 pool_bytes=pool_bytes)
 
 

@@ -187,7 +187,8 @@ stepq_status stepq_decode_step_kda(stepq_pool *pool, const int32_t *slot_ids, in
 enum {
     STEPQ_STEP_KDA_GATE = 1u,  /* gate is the channel-wise d [batch][Hv][d_k] (KDA), else alpha [batch][Hv] */
     STEPQ_STEP_REFIT = 2u,     /* refit both scale vectors to the updated state before requantizing */
-    STEPQ_STEP_ROW_ABSMAX = 4u /* single-axis baseline: r'_i = max_j |X_ij|, c' = 1 (excludes REFIT) */
+    STEPQ_STEP_ROW_ABSMAX = 4u, /* single-axis baseline: r'_i = max_j |X_ij|, c' = 1 (excludes REFIT) */
+    STEPQ_STEP_ADJACENT_SLOTS = 8u /* hint: slot_ids[b] = slot_ids[0] + b (see below) */
 };
 
 /* The decode step with optional channel-wise gate and online scale refit.
@@ -214,6 +215,11 @@ enum {
  * (N1 formulas.  Under N2 the levels are 2^(8-b) q: the column start and the
  * row-absmax factor divide by the top level 2^(8-b) q_b, and q_b / r' becomes
  * 2^(b-8) / r' throughout, so the largest entry still lands on +-q_b.)
+ * STEPQ_STEP_ADJACENT_SLOTS is a scheduling hint, never a change of the
+ * result: the tiles are then taken in launch order, which streams adjacent
+ * slot records best; without it each XCD takes a contiguous run of the
+ * batch, which suits scattered slots.  Set it when the batch lists adjacent
+ * slots in increasing order; the results are bit-identical either way.
  * Unknown flags, or REFIT together with ROW_ABSMAX: STEPQ_E_INVALID. */
 stepq_status stepq_decode_step_ex(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
                                   const void *k, const void *v, const void *gate, const void *beta,

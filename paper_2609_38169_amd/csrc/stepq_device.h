@@ -211,12 +211,13 @@ struct TileCtx {
 };
 
 // The (request, value head) tile of this workgroup among the batch x
-// n_heads tiles of the launch; t.tile = b Hv + h indexes the activations.
+// n_heads tiles of the launch, in launch order or in XCD runs
+// (a.launch_order); t.tile = b Hv + h indexes the activations.
 // tile_bytes: the tile size shared by every head when the launch covers the
 // whole pool in head order (a.head_list NULL).
 __device__ __forceinline__ void tile_of(const DecodeArgs &a, uint32_t tile_bytes, TileCtx &t)
 {
-    const int l = xcd_tile(blockIdx.x, a.batch * a.n_heads);
+    const int l = a.launch_order ? static_cast<int>(blockIdx.x) : xcd_tile(blockIdx.x, a.batch * a.n_heads);
     t.b = fdiv(l, a.div_heads);
     const int j = l - t.b * a.n_heads;
     if (a.head_list) {

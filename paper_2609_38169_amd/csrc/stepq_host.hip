@@ -424,7 +424,8 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     stepq_status st = common_checks(p, slot_ids, batch);
     if (st != STEPQ_OK) return st;
     if (act_dtype != STEPQ_F32 && act_dtype != STEPQ_BF16) return fail(STEPQ_E_INVALID, "unknown activation dtype");
-    if (flags & ~static_cast<uint32_t>(STEPQ_STEP_KDA_GATE | STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX))
+    if (flags & ~static_cast<uint32_t>(STEPQ_STEP_KDA_GATE | STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX |
+                                       STEPQ_STEP_ADJACENT_SLOTS))
         return fail(STEPQ_E_INVALID, "unknown decode-step flags");
     if ((flags & STEPQ_STEP_REFIT) && (flags & STEPQ_STEP_ROW_ABSMAX))
         return fail(STEPQ_E_INVALID, "STEPQ_STEP_REFIT and STEPQ_STEP_ROW_ABSMAX exclude each other");
@@ -446,6 +447,7 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     const bool diag = (flags & STEPQ_STEP_KDA_GATE) != 0;
     const bool bf16 = act_dtype == STEPQ_BF16;
     a.f16_c_one = 0;
+    a.launch_order = (flags & STEPQ_STEP_ADJACENT_SLOTS) ? 1 : 0;
     auto launch = [&](int layout) {
         if (layout == stepq::kF16HeadLayout) {
             // whole FP16 heads: no integer rows to fit, so every mode is the same update

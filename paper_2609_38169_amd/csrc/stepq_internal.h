@@ -120,6 +120,7 @@ struct DecodeArgs {
     // Whole FP16 heads in a row-absmax step: their column factors become 1
     // (the baseline's c' = 1); their values update as in every other mode.
     int32_t f16_c_one;
+    int32_t launch_order;    // 1: tile l of the launch is workgroup l (adjacent slots); 0: XCD runs
 };
 
 enum class TileOp : int { Load = 0, Import = 1, Export = 2, Dequant = 3, ExportPivots = 4, ImportPivots = 5 };

@@ -21,7 +21,7 @@ LIB_PATH = os.environ.get("STEPQ_LIB") or os.path.join(_HERE, "libstepq.so")
 
 STEPQ_F32, STEPQ_BF16 = 0, 1
 STEPQ_LEVELS_ABSMAX, STEPQ_LEVELS_POW2 = 0, 1     # N1: z = q / q_b;  N2: z = 2^(8-b) q
-STEPQ_STEP_KDA_GATE, STEPQ_STEP_REFIT, STEPQ_STEP_ROW_ABSMAX = 1, 2, 4
+STEPQ_STEP_KDA_GATE, STEPQ_STEP_REFIT, STEPQ_STEP_ROW_ABSMAX, STEPQ_STEP_ADJACENT_SLOTS = 1, 2, 4, 8
 _STATUS = {0: "STEPQ_OK", 1: "STEPQ_E_INVALID", 2: "STEPQ_E_UNSUPPORTED", 3: "STEPQ_E_NOMEM", 4: "STEPQ_E_HIP"}
 
 EXPORTED = (
@@ -174,34 +174,37 @@ class Pool:
         stepq_pool_load(self, slot_ids, state, r, c, stream)
 
     # refit: False (frozen scales), True (dual-axis refit) or "row_absmax"
-    # (the single-axis INT-b baseline)
-    def step(self, slot_ids, q, k, v, alpha, beta, o, stream=None, refit=False):
-        if refit:
-            stepq_decode_step_ex(self, slot_ids, q, k, v, alpha, beta, o, _refit_flags(refit), stream)
+    # (the single-axis INT-b baseline); adjacent: the STEPQ_STEP_ADJACENT_SLOTS
+    # hint (slot_ids[b] = slot_ids[0] + b)
+    def step(self, slot_ids, q, k, v, alpha, beta, o, stream=None, refit=False, adjacent=False):
+        flags = _refit_flags(refit) | (STEPQ_STEP_ADJACENT_SLOTS if adjacent else 0)
+        if flags:
+            stepq_decode_step_ex(self, slot_ids, q, k, v, alpha, beta, o, flags, stream)
         else:
             stepq_decode_step(self, slot_ids, q, k, v, alpha, beta, o, stream)
 
-    def step_kda(self, slot_ids, q, k, v, gate, beta, o, stream=None, refit=False):
-        if refit:
-            stepq_decode_step_ex(self, slot_ids, q, k, v, gate, beta, o, STEPQ_STEP_KDA_GATE | _refit_flags(refit),
-                                 stream)
+    def step_kda(self, slot_ids, q, k, v, gate, beta, o, stream=None, refit=False, adjacent=False):
+        flags = _refit_flags(refit) | (STEPQ_STEP_ADJACENT_SLOTS if adjacent else 0)
+        if flags:
+            stepq_decode_step_ex(self, slot_ids, q, k, v, gate, beta, o, STEPQ_STEP_KDA_GATE | flags, stream)
         else:
             stepq_decode_step_kda(self, slot_ids, q, k, v, gate, beta, o, stream)
 
     def set_row_weight(self, w):
         stepq_pool_set_row_weight(self, w)
 
-    def prepare_step(self, slot_ids, q, k, v, alpha, beta, o, stream=None, refit=False):
+    def prepare_step(self, slot_ids, q, k, v, alpha, beta, o, stream=None, refit=False, adjacent=False):
         """Validate the arguments of one decode step once and return a
         callable that launches it with the cached pointers (for decode loops
         where the per-call checks would dominate the launch cost).  alpha of
         shape [B][Hv][d_k] selects the channel-wise (KDA) gate; refit the
-        online scale refit."""
+        online scale refit; adjacent the STEPQ_STEP_ADJACENT_SLOTS hint."""
         kda = alpha.dim() == 3
         args = _step_args(self, slot_ids, q, k, v, alpha, beta, o, stream, kda)
         keep = (slot_ids, q, k, v, alpha, beta, o)      # the tensors must outlive the callable
-        if refit:
-            flags = ctypes.c_uint32(_refit_flags(refit) | (STEPQ_STEP_KDA_GATE if kda else 0))
+        if refit or adjacent:
+            flags = ctypes.c_uint32(_refit_flags(refit) | (STEPQ_STEP_KDA_GATE if kda else 0) |
+                                    (STEPQ_STEP_ADJACENT_SLOTS if adjacent else 0))
             fn = lib().stepq_decode_step_ex
             args = args[:9] + (flags,) + args[9:]
         else:
@@ -260,6 +263,8 @@ def stepq_pool_load(pool: Pool, slot_ids, state, r, c, stream=None):
 
 
 def _refit_flags(refit) -> int:
+    if refit is False:
+        return 0
     if refit is True:
         return STEPQ_STEP_REFIT
     if refit == "row_absmax":

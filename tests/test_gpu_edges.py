@@ -149,3 +149,35 @@ def test_zero_keys_and_queries():
         return inp
 
     PT.lockstep_run(w, 3, np.array([2, 256, 509]), DEV, mutate=zero_heads, say=_say)
+
+
+@pytest.mark.parametrize("idx,refit", [(1, False), (1, True), (2, False), (2, "row_absmax")])
+def test_adjacent_slots_hint_changes_nothing(idx, refit):
+    """STEPQ_STEP_ADJACENT_SLOTS only reorders the tiles of a launch: codes,
+    scales and o are bit-identical with and without it, on a batch of
+    adjacent slots (layer_b64) and on a scattered one (pool_b512), where the
+    hint is wrong."""
+    from paper_2609_38169_amd.pools import build_pool
+    from paper_2609_38169_amd import stepq
+    w = W.workload(idx)
+    slots = W.active_slots(w).to(DEV)
+    _say(f"adjacent hint {w.name} refit={refit}: building two pools")
+    pools = [build_pool(w, 0, device=DEV) for _ in range(2)]
+    outs = []
+    for adjacent, pool in zip((False, True), pools):
+        o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=DEV)
+        for t in range(2):
+            inp = W.step_inputs(w, 0, t, device=DEV)
+            pool.step(slots, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o, refit=refit,
+                      adjacent=adjacent)
+        n = w.batch
+        codes = torch.empty((n, w.n_v_heads, w.d_k, w.d_v), dtype=torch.int8, device=DEV)
+        r = torch.empty((n, w.n_v_heads, w.d_k), dtype=torch.float32, device=DEV)
+        c = torch.empty((n, w.n_v_heads, w.d_v), dtype=torch.float32, device=DEV)
+        pool.export(slots, codes, r, c)
+        torch.cuda.synchronize()
+        outs.append((codes.cpu(), r.cpu(), c.cpu(), o.cpu()))
+    for a, b in zip(*outs):
+        assert torch.equal(a.view(torch.uint8) if a.dtype == torch.int8 else a.view(torch.int32),
+                           b.view(torch.uint8) if b.dtype == torch.int8 else b.view(torch.int32))
+    _say(f"adjacent hint {w.name}: bit-identical")
