@@ -37,10 +37,39 @@ def _cases():
     bits = np.stack([rng.permutation(np.repeat(np.array([8, 4], np.uint8), 64)) for _ in range(4)])
     bits[1] = 16
     cases.append((4, 4, 128, 128, 3, bits))
+
+    # heads of a uniform mix with some rows turned into FP16 pivots: stored
+    # padded to the mix and run by its compiled body (with the pivot rows)
+    def mix(counts, n_heads):
+        row = np.concatenate([np.full(n, b, np.uint8) for b, n in counts])
+        return np.stack([rng.permutation(row) for _ in range(n_heads)])
+
+    def pivots(bits, heads, n):
+        for h, k in zip(heads, n):
+            bits[h, rng.choice(128, size=k, replace=False)] = 16
+        return bits
+
+    six, four = [(8, 64), (4, 64)], [(8, 32), (4, 32), (2, 64)]
+    # 7: every head a padded pivot head of 64@8 + 64@4 (1 to 8 pivots)
+    cases.append((4, 2, 128, 128, 3, pivots(mix(six, 4), range(4), [1, 3, 5, 8])))
+    # 8: 32@8 + 32@4 + 64@2 heads, two of them with pivots (uniform and pivot heads in one launch)
+    cases.append((4, 4, 128, 128, 3, pivots(mix(four, 4), [1, 2], [2, 7])))
+    # 9: all-8, all-4 and all-2 heads with pivots (one launch per class)
+    b9 = np.concatenate([mix([(8, 128)], 2), mix([(4, 128)], 2), mix([(2, 128)], 2)])
+    cases.append((6, 3, 128, 128, 3, pivots(b9, range(6), [2, 1, 4, 8, 3, 6])))
+    # 10: 64@8 + 64@4 heads, a pivot one, a compact generic one (random widths,
+    # 2 pivots), and one with 10 pivots (padded, on the generic body)
+    b10 = mix(six, 4)
+    b10[2] = rng.choice([2, 4, 8], size=128).astype(np.uint8)
+    cases.append((4, 2, 128, 128, 3, pivots(b10, [1, 2, 3], [4, 2, 10])))
+    # 11: 64@8 + 64@4 heads, a pivot one and a whole FP16 head
+    b11 = pivots(mix(six, 4), [2], [6])
+    b11[3] = 16
+    cases.append((4, 4, 128, 128, 3, b11))
     return cases
 
 
-N_CASES = 7
+N_CASES = 12
 
 
 def _state(case, seed):
