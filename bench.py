@@ -182,6 +182,20 @@ def pool_case(args, w, mode, dev):
     from paper_2609_38169_amd.pools import build_pool, row_bits
 
     bits = row_bits(w)
+    row_weight = None
+    if args.calibrated:
+        # the calibration side of the setup step on this workload's own draws:
+        # row units with 24 FP16 pivot rows (0.6% of the rows, as in the
+        # paper's KDA setting) or head units with one whole FP16 head
+        from paper_2609_38169_amd.calibrate import calibrate
+        T = 8
+        draws = [W.step_inputs(w, 0, 1000 + t) for t in range(T)]
+        g = w.n_v_heads // w.n_qk_heads
+        cat = lambda key: np.concatenate([d[key].float().numpy() for d in draws])
+        cal = calibrate(np.repeat(cat("q"), g, axis=1), np.repeat(cat("k"), g, axis=1), cat("beta"), cat("alpha"),
+                        W.initial_state(w, 0, range(4)).numpy(), budget=6.0, cand_bits=(4, 8), unit=args.calibrated,
+                        n_pivots=24 if args.calibrated == "row" else 1, horizon=1024)
+        bits, row_weight = cal.row_bits, cal.row_weight
     if args.pivots:
         # FP16 pivot rows: a seeded quarter of the heads keep 1-3 key rows in binary16
         bits = bits.copy()
@@ -192,6 +206,8 @@ def pool_case(args, w, mode, dev):
         bits[W.pivot_head_draw(w, 0, args.fp16_heads).numpy()] = 16
     log(f"building the {w.n_slots}-slot pool")
     pool = build_pool(w, device=dev, bits=bits, levels=args.levels)
+    if row_weight is not None:
+        pool.set_row_weight(row_weight)
     subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
     if args.sorted_batch:
         # the same requests, listed in slot order (a caller-side choice: any batch order is valid)
@@ -215,6 +231,10 @@ def pool_case(args, w, mode, dev):
         prepared[key]()
 
     mix = {"pool_b512": "6-bit mixed {4,8}", "pool_4bit": "4-bit mixed {2,4,8}, heavy-tailed states"}[w.name]
+    if args.calibrated:
+        ints = bits[bits != 16]
+        mix = (f"calibrated {args.calibrated} map ({ints.mean():.2f} bits/element on {(bits == 8).sum()} rows @8 and "
+               f"{(bits == 4).sum()} @4, {(bits == 16).sum()} FP16 rows)")
     if args.pivots or args.fp16_heads:
         full = int((bits == 16).all(1).sum())
         rows = int((bits == 16).sum()) - full * w.d_k
@@ -290,6 +310,9 @@ def main():
                     help="untimed steps before the warmup until this much GPU time has elapsed (clock ramp)")
     ap.add_argument("--workload", choices=["pool_b512", "pool_4bit", "stack48"], default="pool_b512")
     ap.add_argument("--resident", action="store_true", help="no slot rotation (cache-resident number)")
+    ap.add_argument("--calibrated", choices=["row", "head"], default=None,
+                    help="pool workloads: the precision map from the calibration side of the setup step "
+                         "(row units with 24 FP16 pivot rows, or head units with one FP16 head)")
     ap.add_argument("--sorted-batch", action="store_true",
                     help="list each step's active requests in slot order (pool workloads; default: as drawn)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
@@ -310,8 +333,8 @@ def main():
     if args.refit and args.row_absmax:
         print("--refit and --row-absmax exclude each other", file=sys.stderr)
         sys.exit(2)
-    if (args.pivots or args.fp16_heads) and args.workload == "stack48":
-        print("--pivots and --fp16-heads apply to the single-layer pool workloads", file=sys.stderr)
+    if (args.pivots or args.fp16_heads or args.calibrated) and args.workload == "stack48":
+        print("--pivots, --fp16-heads and --calibrated apply to the single-layer pool workloads", file=sys.stderr)
         sys.exit(2)
     mode = True if args.refit else ("row_absmax" if args.row_absmax else False)
     rescale = bool(mode)          # the step writes the scales back
@@ -435,7 +458,8 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic_entry(mode, args.kda, w.name, args.pivots) if not args.fp16_heads else None,
+            "traffic": traffic_entry(mode, args.kda, w.name, args.pivots)
+                       if not (args.fp16_heads or args.calibrated) else None,
             "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Top/s", "frac": valu_tops / VALU_PEAK_TOPS,
                      "ops_per_element": valu_ops, "matrix_core_ops_per_element": MATRIX_CORE_OPS[mode]},
             "kernel": kern_name,

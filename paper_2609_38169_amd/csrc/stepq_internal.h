@@ -68,6 +68,12 @@ constexpr int kPivotUniformBase = 32;
 // layout-L padded pivot heads only, in one decode launch of one body (a
 // layout-L head is a padded pivot head without pivot rows).
 constexpr int kMixedPivotBase = 24;
+// Layout code kMultiUniform: heads of several compiled layouts (uniform
+// mixes and whole FP16 heads) in one decode launch, each tile taking its
+// own body; kMultiPivot: the same with padded pivot heads too (their body
+// needs a few more registers).
+constexpr int kMultiUniform = 40;
+constexpr int kMultiPivot = 41;
 
 // n / d for 0 <= n < 2^31 by multiply-high (Granlund-Montgomery), with the
 // constants prepared on the host so that uniform quotients stay scalar.

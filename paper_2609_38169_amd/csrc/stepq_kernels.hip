@@ -320,6 +320,9 @@ __device__ __forceinline__ void run_generic(const DecodeArgs &a, TileCtx &t, int
 // layout L and compact generic heads in one launch, told apart by the head
 // list (both bodies fit the same register budget), together with layout-L
 // padded pivot heads; kMixedF16Base + L: the same with whole FP16 heads too.
+// LAYOUT == kMultiUniform: heads of several compiled layouts (uniform,
+// whole FP16), each tile dispatched to its own body; kMultiPivot: with
+// padded pivot heads too.
 // LAYOUT == kMixedPivotBase + L: uniform layout-L heads and layout-L padded
 // pivot heads only.  LAYOUT == kPivotUniformBase + L: padded pivot heads of
 // uniform layout L only.  LAYOUT == kF16HeadLayout: heads held entirely in FP16 (every mode;
@@ -340,7 +343,27 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
     const int slot = a.slot_ids[t.b];
     t.alpha = DIAG ? 1.0f : act_ld<BF16>(a.alpha, t.tile);
     t.beta = act_ld<BF16>(a.beta, t.tile);
-    if constexpr (DV == 128 && LAYOUT > 0 && LAYOUT <= kNumUniformLayouts) {
+    if constexpr (DV == 128 && (LAYOUT == kMultiUniform || LAYOUT == kMultiPivot)) {
+        switch (t.layout) {
+        case 1: run_uniform<BF16, DIAG, 1>(a, t, slot, sh); break;
+        case 2: run_uniform<BF16, DIAG, 2>(a, t, slot, sh); break;
+        case 3: run_uniform<BF16, DIAG, 3>(a, t, slot, sh); break;
+        case 4: run_uniform<BF16, DIAG, 4>(a, t, slot, sh); break;
+        case 5: run_uniform<BF16, DIAG, 5>(a, t, slot, sh); break;
+        case kF16HeadLayout: run_f16head<BF16, DIAG>(a, t, slot, sh); break;
+        default:
+            if constexpr (LAYOUT == kMultiPivot) {
+                switch (t.layout - kPivotUniformBase) {
+                case 1: run_uniform_piv<BF16, DIAG, 1>(a, t, slot, sh); break;
+                case 2: run_uniform_piv<BF16, DIAG, 2>(a, t, slot, sh); break;
+                case 3: run_uniform_piv<BF16, DIAG, 3>(a, t, slot, sh); break;
+                case 4: run_uniform_piv<BF16, DIAG, 4>(a, t, slot, sh); break;
+                default: run_uniform_piv<BF16, DIAG, 5>(a, t, slot, sh); break;
+                }
+            }
+            break;
+        }
+    } else if constexpr (DV == 128 && LAYOUT > 0 && LAYOUT <= kNumUniformLayouts) {
         run_uniform<BF16, DIAG, LAYOUT>(a, t, slot, sh);
     } else if constexpr (DV == 128 && LAYOUT == kF16HeadLayout) {
         run_f16head<BF16, DIAG>(a, t, slot, sh);
@@ -507,6 +530,12 @@ hipError_t launch_decode_128(const DecodeArgs &a, int layout, unsigned grid, hip
         break;
     case kPivotUniformBase + 5:
         hipLaunchKernelGGL((decode_kernel<128, BF16, kPivotUniformBase + 5, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kMultiUniform:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kMultiUniform, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kMultiPivot:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kMultiPivot, DIAG>), dim3(grid), dim3(256), 0, s, a);
         break;
     case kMixedPivotBase + 1:
         hipLaunchKernelGGL((decode_kernel<128, BF16, kMixedPivotBase + 1, DIAG>), dim3(grid), dim3(256), 0, s, a);

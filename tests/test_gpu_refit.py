@@ -170,4 +170,4 @@ def test_refit_prepared_call_and_argument_errors():
     with pytest.raises(ValueError):
         pa.set_row_weight(np.ones((w.n_v_heads, w.d_k + 1), np.float32))
     with pytest.raises(stepq.StepqError):      # unknown flag bits
-        stepq.stepq_decode_step_ex(pa, ids, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], oa, 8)
+        stepq.stepq_decode_step_ex(pa, ids, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], oa, 16)
