@@ -219,8 +219,11 @@ __device__ __forceinline__ void tile_of(const DecodeArgs &a, uint32_t tile_bytes
 {
     const int l = a.launch_order ? static_cast<int>(blockIdx.x) : xcd_tile(blockIdx.x, a.batch * a.n_heads);
     t.b = fdiv(l, a.div_heads);
-    const int j = l - t.b * a.n_heads;
+    int j = l - t.b * a.n_heads;
     if (a.head_list) {
+        // rotate each request's heads by its index: tiles of one head then do
+        // not recur at the same launch position modulo the CUs of an XCD
+        j += t.b - a.n_heads * fdiv(j + t.b, a.div_heads);
         const LaunchHead lh = a.head_list[j];
         t.h = lh.h;
         t.off = lh.tile_off;

@@ -366,21 +366,24 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
                 fits = false;
             }
         }
-        if (fits && L != 0 && others > 0)
-            p->mixed_code = others == pivots ? stepq::kMixedPivotBase + L
-                                             : (f16 ? stepq::kMixedF16Base : stepq::kMixedBase) + L;
-        // otherwise several classes that all have compiled bodies (uniform
-        // mixes, their padded pivot heads, whole FP16 heads): one launch too
-        if (p->mixed_code == 0 && p->cls_layout.size() > 1) {
-            bool compiled = true, piv = false;
-            for (int code : p->cls_layout) {
-                const bool pc = code > stepq::kPivotUniformBase &&
-                                code <= stepq::kPivotUniformBase + stepq::kNumUniformLayouts;
-                compiled = compiled && ((code >= 1 && code <= stepq::kF16HeadLayout) || pc);
-                piv = piv || pc;
-            }
-            if (compiled) p->mixed_code = piv ? stepq::kMultiPivot : stepq::kMultiUniform;
+        // several classes that all have compiled bodies (uniform mixes,
+        // their padded pivot heads, whole FP16 heads): one launch of those
+        // bodies only, which fits fewer registers than the ones below.  The
+        // head list keeps the classes together: tiles of one kind in runs
+        // stream better than interleaved kinds.
+        bool compiled = p->cls_layout.size() > 1, piv = false;
+        for (int code : p->cls_layout) {
+            const bool pc = code > stepq::kPivotUniformBase &&
+                            code <= stepq::kPivotUniformBase + stepq::kNumUniformLayouts;
+            compiled = compiled && ((code >= 1 && code <= stepq::kF16HeadLayout) || pc);
+            piv = piv || pc;
         }
+        if (fits && L != 0 && others > 0 && others == pivots)
+            p->mixed_code = stepq::kMixedPivotBase + L;       // one uniform mix and its pivot heads: one body
+        else if (compiled)
+            p->mixed_code = piv ? stepq::kMultiPivot : stepq::kMultiUniform;
+        else if (fits && L != 0 && others > 0)
+            p->mixed_code = (f16 ? stepq::kMixedF16Base : stepq::kMixedBase) + L;
         e = hipMalloc(reinterpret_cast<void **>(&p->d_head_order), sizeof(stepq::LaunchHead) * order.size());
         if (e == hipSuccess)
             e = hipMemcpy(p->d_head_order, order.data(), sizeof(stepq::LaunchHead) * order.size(),

@@ -180,13 +180,12 @@ __device__ __forceinline__ void decode_f16head(const DecodeArgs &a, const TileCt
     const int tid = threadIdx.x;
     const int cg = tid & 31, slice = tid >> 5;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(t.codes, 0, 128 * 256, 0x00020000);
+    // one 8-byte access per row and thread: a half-wavefront covers a whole
+    // 256-byte row
     u32x2 S[16];
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-        const int off = (slice + 8 * m) * 256 + 8 * cg;
-        S[m] = u32x2{__builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, CodeWords::kLoad),
-                     __builtin_amdgcn_raw_buffer_load_b32(rs, off + 4, 0, CodeWords::kLoad)};
-    }
+    for (int m = 0; m < 16; ++m)
+        S[m] = __builtin_amdgcn_raw_buffer_load_b64(rs, (slice + 8 * m) * 256 + 8 * cg, 0, CodeWords::kLoad);
     // k, q, the gate and the permutation by row, v by column (the r and c
     // slots of the record are not read)
     const PoolView &P = a.pool;
@@ -242,9 +241,8 @@ __device__ __forceinline__ void decode_f16head(const DecodeArgs &a, const TileCt
         const float dg = DIAG ? sh.al[p] : t.alpha;
         const float x0 = fmaf(bk, dl[0], dg * half_lo(S[m].x)), x1 = fmaf(bk, dl[1], dg * half_hi(S[m].x));
         const float x2 = fmaf(bk, dl[2], dg * half_lo(S[m].y)), x3 = fmaf(bk, dl[3], dg * half_hi(S[m].y));
-        const int off = p * 256 + 8 * cg;
-        __builtin_amdgcn_raw_buffer_store_b32(pack_halves(x0, x1), rs, off, 0, CodeWords::kStore);
-        __builtin_amdgcn_raw_buffer_store_b32(pack_halves(x2, x3), rs, off + 4, 0, CodeWords::kStore);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack_halves(x0, x1), pack_halves(x2, x3)}, rs, p * 256 + 8 * cg, 0,
+                                              CodeWords::kStore);
     }
 }
 
