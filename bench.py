@@ -105,8 +105,10 @@ def cpu_baseline(w, bits, seconds: float):
     S = W.initial_state(w, 0, slots).numpy().reshape(-1, w.d_k, w.d_v)
     n = S.shape[0]
     tb = np.broadcast_to(bits[None], (len(rows),) + bits.shape).reshape(n, w.d_k)
-    r, c = oracle.fit_absmax(S)
-    codes = oracle.quantize(S.astype(np.float64), r, c, tb)
+    r, c = oracle.fit_absmax(S, bits=tb)
+    # maps with FP16 pivot rows also carry the pivot values
+    out = oracle.quantize(S.astype(np.float64), r, c, tb)
+    codes, pv = out if isinstance(out, tuple) else (out, None)
     g = w.n_v_heads // w.n_qk_heads
     hq = np.arange(w.n_v_heads) // g
     # a few distinct steps of the sampled requests, drawn once and cycled
@@ -119,13 +121,16 @@ def cpu_baseline(w, bits, seconds: float):
                          inp["alpha"][rows].double().numpy().reshape(n),
                          inp["beta"][rows].double().numpy().reshape(n)))
     def timed(budget):
-        nonlocal codes
+        nonlocal codes, pv
         done, step, elapsed = 0, 0, 0.0
         while elapsed < budget:
             q, k, v, a, b = steps_in[step % len(steps_in)]
             ts = time.perf_counter()
-            codes, _ = oracle.decode_step(codes, r, c, tb, q, k, v, a, b)
+            res = oracle.decode_step(codes, r, c, tb, q, k, v, a, b, pv=pv)
             elapsed += time.perf_counter() - ts
+            codes = res[0]
+            if pv is not None:
+                pv = res[-1]
             done += n
             step += 1
         return done / elapsed, step, elapsed

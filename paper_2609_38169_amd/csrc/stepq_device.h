@@ -194,8 +194,12 @@ struct DecodeShared {
     float cpiv[DV];                      // c_j, for the pivot rows' share of S^T k and S^T q
     // Uniform bodies: the row weights as binary16 A operands of the 4x4x4
     // matrix-core blocks, [slice][row group][type][row in group], types
-    // 0/1 = k weight hi/lo, 2/3 = q weight hi/lo (prescaled by powers of two)
-    alignas(16) _Float16 aop[8][4][4][4];
+    // 0/1 = k weight hi/lo, 2/3 = q weight hi/lo (prescaled by powers of two).
+    // Row-mix body: [slice][word group][slot][type][word in group].
+    union {
+        alignas(16) _Float16 aop[8][4][4][4];
+        alignas(16) _Float16 aopv[8][4][2][4][4];
+    };
     float2 wmx[4];                       // per wavefront: largest |k weight|, |q weight|
 };
 
@@ -781,6 +785,68 @@ __device__ __forceinline__ void matvec_partials(DecodeShared<128> &sh, int slice
         redQ[e] = __builtin_amdgcn_ldexpf(d[2] + d[3], -eq);
         __builtin_amdgcn_sched_barrier(0);    // one column's chain at a time: 4 accumulators live
     }
+}
+
+// ---- row-mix heads (compact layout, 8- and 4-bit rows in any split, d_v =
+// 128).  Word m of thread (slice, cg) is row group g = slice + 8 m.  A block's
+// K dimension is 4 consecutive words of one slice (word group j = m / 4)
+// read through slot view s: s = 0 the 8-bit row or slot 0 of a 4-bit
+// group, s = 1 slot 1 of a 4-bit group.
+
+// The A operands of the row-mix blocks from the row-table weights that
+// row_constants left in sh.kq, prescaled by 2^ek and 2^eq as in
+// row_constants_mfma: aopv[slice][j][s][type][m mod 4].  Views that hold no
+// row (slot 1 of an 8-bit group, an empty 4-bit slot, a group past the
+// head's last) get zero weights.  Two barriers; the table is complete
+// after the second.
+__device__ __forceinline__ void row_operands_rowmix(const HeadInfo &hi, DecodeShared<128> &sh, int &ek, int &eq)
+{
+    const int tid = threadIdx.x;
+    float mk = 0.f, mq = 0.f;
+    if (tid < kSlotTable) {
+        const float2 c = sh.kq[tid];
+        mk = fabsf(c.x);
+        mq = fabsf(c.y);
+    }
+    mk = wave_max(mk);
+    mq = wave_max(mq);
+    if ((tid & 63) == 0) sh.wmx[tid >> 6] = make_float2(mk, mq);
+    __syncthreads();
+    const float2 w0 = sh.wmx[0], w1 = sh.wmx[1], w2 = sh.wmx[2];    // the table slots live in wavefronts 0 .. 2
+    ek = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(fmaxf(w0.x, w1.x), w2.x)));
+    eq = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(fmaxf(w0.y, w1.y), w2.y)));
+    // one (slice, word, view) entry per thread
+    const int slice = tid & 7, m = (tid >> 3) & 15, v = tid >> 7;
+    const int g = slice + 8 * m;
+    const int g8 = hi.g8;
+    int x = -1;
+    if (g < g8) x = v == 0 ? g : -1;
+    else if (g < static_cast<int>(hi.groups)) x = g8 + 2 * (g - g8) + v;
+    const float2 c = x >= 0 ? sh.kq[x] : make_float2(0.f, 0.f);
+    const float ks = __builtin_amdgcn_ldexpf(c.x, ek), qs = __builtin_amdgcn_ldexpf(c.y, eq);
+    const _Float16 kh = static_cast<_Float16>(ks), qh = static_cast<_Float16>(qs);
+    const _Float16 kl = static_cast<_Float16>(ks - static_cast<float>(kh));
+    const _Float16 ql = static_cast<_Float16>(qs - static_cast<float>(qh));
+    _Float16(&dst)[4][4] = sh.aopv[slice][m >> 2][v];
+    dst[0][m & 3] = kh;
+    dst[1][m & 3] = kl;
+    dst[2][m & 3] = qh;
+    dst[3][m & 3] = ql;
+    __syncthreads();
+}
+
+// One view of a word group: the 4x4x4 block of column E of the thread,
+// added to that column's accumulator.  The B operands come from inline
+// assembly, whose register writes the compiler's hazard checks do not see,
+// and are read by the matrix core right after: the s_nop, tied to them,
+// keeps the wait states a VALU write needs before such a read.
+template <int E>
+__device__ __forceinline__ f32x4 mfma_view(const _Float16 (&A)[4][4], const uint32_t (&v)[4], int cg, f32x4 d)
+{
+    const u32x2 a = *reinterpret_cast<const u32x2 *>(&A[cg & 3][0]);
+    uint32_t b0 = sbyte_pair_f16<E>(v[0], v[1]), b1 = sbyte_pair_f16<E>(v[2], v[3]);
+    asm volatile("s_nop 4" : "+v"(b0), "+v"(b1));
+    return mfma4x4x4(a, b0, b1, d);
 }
 
 // New field in byte E of P from the old field in half HALF of hp; the

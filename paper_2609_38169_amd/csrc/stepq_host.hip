@@ -327,13 +327,20 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
         for (const auto &c : cls) {
             int code = c.second;
             if (code == 0) {
-                // the generic heads take the compact body when all of them fit it
-                bool fits = true;
-                for (const HeadInfo &hi : p->heads)
-                    if (hi.layout == 0 && (hi.groups > static_cast<uint32_t>(stepq::kCompactGroups) ||
-                                           hi.n16 > stepq::kCompactPivots))
+                // the generic heads take the row-mix body when every one of
+                // them is a compact 8/4-bit head with few pivot rows, else the
+                // compact generic body when all of them fit it
+                bool fits = true, rowmix = p->dk == 128;
+                for (const HeadInfo &hi : p->heads) {
+                    if (hi.layout != 0) continue;
+                    if (hi.groups > static_cast<uint32_t>(stepq::kCompactGroups) || hi.n16 > stepq::kCompactPivots)
                         fits = false;
-                if (fits) code = stepq::kCompactGeneric;
+                    if (hi.n2 != 0 || hi.n16 > stepq::kCompactPivots || hi.g8 != hi.n8 ||
+                        hi.g4 != (hi.n4 + 1) / 2 || hi.g2 != 0)
+                        rowmix = false;
+                }
+                if (rowmix) code = stepq::kRowMix;
+                else if (fits) code = stepq::kCompactGeneric;
             }
             p->cls_layout.push_back(code);
             p->cls_off.push_back(static_cast<int>(order.size()));

@@ -74,6 +74,12 @@ constexpr int kMixedPivotBase = 24;
 // needs a few more registers).
 constexpr int kMultiUniform = 40;
 constexpr int kMultiPivot = 41;
+// Layout code kRowMix: generic heads at d_k = d_v = 128 whose integer rows
+// are 8- and 4-bit only, in any split, with at most kCompactPivots pivot
+// rows, in the compact layout (row groups g8 = n8, g4 = ceil(n4 / 2)); one
+// decode body runs them with the matrix cores whatever the split.  The
+// heads keep layout 0 in their HeadInfo.
+constexpr int kRowMix = 42;
 
 // n / d for 0 <= n < 2^31 by multiply-high (Granlund-Montgomery), with the
 // constants prepared on the host so that uniform quotients stay scalar.

@@ -168,6 +168,109 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
     }
 }
 
+// Column E of the row-mix thread's two sums: one chain over the word groups
+// and their slot views (one accumulator live), written to LDS unscaled.
+// The views are recomputed per column rather than kept.
+template <int E>
+__device__ __forceinline__ void rowmix_column(const DecodeShared<128> &sh, const uint32_t (&w)[16], int slice, int cg,
+                                              int g8, int ng, int ek, int eq, float *redK, float *redQ)
+{
+    f32x4 d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (32 * j >= ng) break;
+        uint32_t v[4];
+        if (32 * j + 32 <= g8) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = w[4 * j + k];
+        } else if (32 * j >= g8) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 0);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                v[k] = slice + 8 * (4 * j + k) < g8 ? w[4 * j + k] : slot_top<4>(w[4 * j + k], 0);
+        }
+        d = mfma_view<E>(sh.aopv[slice][j][0], v, cg, d);
+        if (32 * j + 32 > g8) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 1);
+            d = mfma_view<E>(sh.aopv[slice][j][1], v, cg, d);
+        }
+    }
+    redK[E] = __builtin_amdgcn_ldexpf(d[0] + d[1], -ek);
+    redQ[E] = __builtin_amdgcn_ldexpf(d[2] + d[3], -eq);
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// A head at d = 128 whose integer rows are 8- and 4-bit in any split, in the
+// compact layout, with up to kCompactPivots FP16 pivot rows (the per-row
+// maps of a row-unit calibration).  Groups below hi.g8 are 8-bit, the rest
+// up to hi.groups 4-bit, so a word-step's width changes between slices at
+// most once.  Both sums over rows run on the matrix cores: per word group
+// of 4 word-steps, a 4x4x4 block per column for the words' slot-0 view and,
+// where the group holds 4-bit words, one for their slot-1 view.  The
+// requantization reads the fields again from the words kept in registers.
+template <bool BF16, bool DIAG>
+__device__ __forceinline__ void decode_rowmix(const DecodeArgs &a, const TileCtx &t, DecodeShared<128> &sh)
+{
+    const int tid = threadIdx.x;
+    const int cg = tid & 31, slice = tid >> 5;
+    const int g8 = __builtin_amdgcn_readfirstlane(static_cast<int>(t.hi.g8));
+    const int ng = __builtin_amdgcn_readfirstlane(static_cast<int>(t.hi.groups));
+    const CodeWords cw(t.codes, t.hi.piv_off);
+    uint32_t w[16];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) w[m] = slice + 8 * m < ng ? cw.load(tid + 256 * m) : 0u;
+    PivotRegs<128, kCompactPivots> pr;
+    pivot_load<128, kCompactPivots>(t, slice, cg, pr);
+    const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
+    const float kappa = row_constants<DIAG, 128>(t.hi, 128, t.alpha, t.beta, op, sh, a.pool.lv);
+    int ek, eq;
+    row_operands_rowmix(t.hi, sh, ek, eq);
+
+    float *redK = &sh.red[0][slice][cg].x, *redQ = &sh.red[1][slice][cg].x;
+    rowmix_column<0>(sh, w, slice, cg, g8, ng, ek, eq, redK, redQ);
+    rowmix_column<1>(sh, w, slice, cg, g8, ng, ek, eq, redK, redQ);
+    rowmix_column<2>(sh, w, slice, cg, g8, ng, ek, eq, redK, redQ);
+    rowmix_column<3>(sh, w, slice, cg, g8, ng, ek, eq, redK, redQ);
+    // pivot row p = slice (kCompactPivots = 8 slices): its share of the
+    // partials, added to this thread's own (the column phase multiplies by c_j)
+    static_assert(PivotRegs<128, kCompactPivots>::M == 1, "one pivot row per thread");
+    if (slice < t.hi.n16) {
+        const float4 c4 = *reinterpret_cast<const float4 *>(&sh.cpiv[4 * cg]);
+        const uint32_t lo = pr.v[0].x, hi = pr.v[0].y;
+        const float sv[4] = {half_lo(lo) * __builtin_amdgcn_rcpf(c4.x), half_hi(lo) * __builtin_amdgcn_rcpf(c4.y),
+                             half_lo(hi) * __builtin_amdgcn_rcpf(c4.z), half_hi(hi) * __builtin_amdgcn_rcpf(c4.w)};
+        const float4 kp = sh.pvc[slice];
+        float4 &rk = sh.red[0][slice][cg];
+        rk = make_float4(fmaf(kp.x, sv[0], rk.x), fmaf(kp.x, sv[1], rk.y), fmaf(kp.x, sv[2], rk.z),
+                         fmaf(kp.x, sv[3], rk.w));
+        float4 &rq = sh.red[1][slice][cg];
+        rq = make_float4(fmaf(kp.y, sv[0], rq.x), fmaf(kp.y, sv[1], rq.y), fmaf(kp.y, sv[2], rq.z),
+                         fmaf(kp.y, sv[3], rq.w));
+    }
+
+    column_sums<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, op.c, op.v);
+
+    const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
+    const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
+    pivot_update<128, kCompactPivots>(t, slice, cg, pr, sh, bc);
+    float U[8];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+        const int g = slice + 8 * m;
+        if (g < g8) {
+            unpack_word<8>(w[m], U);
+            cw.store(tid + 256 * m, requant_word<8, DIAG>(U, sh.av, sh.al, g, t.alpha, bc));
+        } else if (g < ng) {
+            unpack_word<4>(w[m], U);
+            cw.store(tid + 256 * m, requant_word<4, DIAG>(U, sh.av, sh.al, g8 + 2 * (g - g8),
+                                                          t.alpha * (1.0f / 16.0f), bc));
+        }
+    }
+}
+
 // A head whose every row is an FP16 pivot (d = 128).  Thread (slice, cg)
 // holds columns 4 cg .. 4 cg + 3 of rows p = slice + 8 m as two binary16
 // pairs; the FMAs read the halves directly (v_fma_mix), so nothing is
@@ -294,6 +397,18 @@ __device__ __forceinline__ void run_uniform_piv(const DecodeArgs &a, TileCtx &t,
     decode_uniform<BF16, DIAG, u.m8, u.m4, u.m2, true>(a, t, sh);
 }
 
+template <bool BF16, bool DIAG>
+__device__ __forceinline__ void run_rowmix(const DecodeArgs &a, TileCtx &t, int slot, DecodeShared<128> &sh)
+{
+    const PoolView &P = a.pool;
+    t.hi = P.heads[t.h];
+    uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.hi.tile_off;
+    t.codes = reinterpret_cast<uint32_t *>(rec);
+    t.rr = reinterpret_cast<const float *>(rec + t.hi.r_off);
+    t.cc = t.rr + 128;
+    decode_rowmix<BF16, DIAG>(a, t, sh);
+}
+
 template <bool BF16, bool DIAG, int DV, bool COMPACT>
 __device__ __forceinline__ void run_generic(const DecodeArgs &a, TileCtx &t, int slot, DecodeShared<DV> &sh)
 {
@@ -321,6 +436,9 @@ __device__ __forceinline__ void run_generic(const DecodeArgs &a, TileCtx &t, int
 // LAYOUT == kMultiUniform: heads of several compiled layouts (uniform,
 // whole FP16), each tile dispatched to its own body; kMultiPivot: with
 // padded pivot heads too.
+// LAYOUT == kRowMix: compact heads of 8- and 4-bit rows in any split with at
+// most kCompactPivots pivot rows (decode_rowmix), launched as a class of its
+// own (in the combined launches it would raise their register count).
 // LAYOUT == kMixedPivotBase + L: uniform layout-L heads and layout-L padded
 // pivot heads only.  LAYOUT == kPivotUniformBase + L: padded pivot heads of
 // uniform layout L only.  LAYOUT == kF16HeadLayout: heads held entirely in FP16 (every mode;
@@ -361,6 +479,8 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
             }
             break;
         }
+    } else if constexpr (DV == 128 && LAYOUT == kRowMix) {
+        run_rowmix<BF16, DIAG>(a, t, slot, sh);
     } else if constexpr (DV == 128 && LAYOUT > 0 && LAYOUT <= kNumUniformLayouts) {
         run_uniform<BF16, DIAG, LAYOUT>(a, t, slot, sh);
     } else if constexpr (DV == 128 && LAYOUT == kF16HeadLayout) {
@@ -534,6 +654,9 @@ hipError_t launch_decode_128(const DecodeArgs &a, int layout, unsigned grid, hip
         break;
     case kMultiPivot:
         hipLaunchKernelGGL((decode_kernel<128, BF16, kMultiPivot, DIAG>), dim3(grid), dim3(256), 0, s, a);
+        break;
+    case kRowMix:
+        hipLaunchKernelGGL((decode_kernel<128, BF16, kRowMix, DIAG>), dim3(grid), dim3(256), 0, s, a);
         break;
     case kMixedPivotBase + 1:
         hipLaunchKernelGGL((decode_kernel<128, BF16, kMixedPivotBase + 1, DIAG>), dim3(grid), dim3(256), 0, s, a);
