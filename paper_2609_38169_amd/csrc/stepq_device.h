@@ -127,6 +127,12 @@ __device__ __forceinline__ float sbyte(uint32_t w, int e)
     return static_cast<float>(static_cast<int8_t>(static_cast<uint8_t>(w >> (8 * e))));
 }
 
+// A value every lane of the wavefront holds, moved to a scalar register.
+__device__ __forceinline__ float uniform_f(float x)
+{
+    return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+
 __device__ __forceinline__ int fdiv(int n, FastDiv d)
 {
     const uint32_t u = static_cast<uint32_t>(n);

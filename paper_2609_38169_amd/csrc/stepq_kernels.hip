@@ -172,27 +172,27 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
 // and their slot views (one accumulator live), written to LDS unscaled.
 // The views are recomputed per column rather than kept.
 template <int E>
-__device__ __forceinline__ void rowmix_column(const DecodeShared<128> &sh, const uint32_t (&w)[16], int slice, int cg,
-                                              int g8, int ng, int ek, int eq, float *redK, float *redQ)
+__device__ __forceinline__ void rowmix_column(const DecodeShared<128> &sh, const uint32_t (&w)[16],
+                                              const uint32_t (&vb)[4], int slice, int cg, int g8, int ng, int ek,
+                                              int eq, float *redK, float *redQ)
 {
     f32x4 d = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         if (32 * j >= ng) break;
-        uint32_t v[4];
         if (32 * j + 32 <= g8) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) v[k] = w[4 * j + k];
-        } else if (32 * j >= g8) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 0);
+            // 8-bit words only: their bytes are the codes
+            const uint32_t v[4] = {w[4 * j], w[4 * j + 1], w[4 * j + 2], w[4 * j + 3]};
+            d = mfma_view<E>(sh.aopv[slice][j][0], v, cg, d);
         } else {
+            uint32_t v[4];
+            if (32 * j >= g8) {
 #pragma unroll
-            for (int k = 0; k < 4; ++k)
-                v[k] = slice + 8 * (4 * j + k) < g8 ? w[4 * j + k] : slot_top<4>(w[4 * j + k], 0);
-        }
-        d = mfma_view<E>(sh.aopv[slice][j][0], v, cg, d);
-        if (32 * j + 32 > g8) {
+                for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 0);
+                d = mfma_view<E>(sh.aopv[slice][j][0], v, cg, d);
+            } else {
+                d = mfma_view<E>(sh.aopv[slice][j][0], vb, cg, d);    // the group of the width boundary
+            }
 #pragma unroll
             for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 1);
             d = mfma_view<E>(sh.aopv[slice][j][1], v, cg, d);
@@ -221,19 +221,35 @@ __device__ __forceinline__ void decode_rowmix(const DecodeArgs &a, const TileCtx
     const CodeWords cw(t.codes, t.hi.piv_off);
     uint32_t w[16];
 #pragma unroll
-    for (int m = 0; m < 16; ++m) w[m] = slice + 8 * m < ng ? cw.load(tid + 256 * m) : 0u;
+    for (int m = 0; m < 16; ++m) {
+        if (8 * m + 8 <= ng) w[m] = cw.load(tid + 256 * m);
+        else w[m] = slice + 8 * m < ng ? cw.load(tid + 256 * m) : 0u;
+    }
     PivotRegs<128, kCompactPivots> pr;
     pivot_load<128, kCompactPivots>(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    const float kappa = row_constants<DIAG, 128>(t.hi, 128, t.alpha, t.beta, op, sh, a.pool.lv);
+    // v_j waits in LDS for the column phase (c_j is kept there for the pivot
+    // rows), so neither is held in registers through the row sums
+    if (tid < 128) sh.bcol[tid] = op.v;
+    const float kappa = uniform_f(row_constants<DIAG, 128>(t.hi, 128, t.alpha, t.beta, op, sh, a.pool.lv));
     int ek, eq;
     row_operands_rowmix(t.hi, sh, ek, eq);
 
     float *redK = &sh.red[0][slice][cg].x, *redQ = &sh.red[1][slice][cg].x;
-    rowmix_column<0>(sh, w, slice, cg, g8, ng, ek, eq, redK, redQ);
-    rowmix_column<1>(sh, w, slice, cg, g8, ng, ek, eq, redK, redQ);
-    rowmix_column<2>(sh, w, slice, cg, g8, ng, ek, eq, redK, redQ);
-    rowmix_column<3>(sh, w, slice, cg, g8, ng, ek, eq, redK, redQ);
+    // slot-0 views of the word group holding the width boundary (if any),
+    // formed once: there the width changes from one slice to the next
+    uint32_t vb[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if ((g8 >> 5) == j && (g8 & 31) != 0) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                vb[k] = slice + 8 * (4 * j + k) < g8 ? w[4 * j + k] : slot_top<4>(w[4 * j + k], 0);
+        }
+    rowmix_column<0>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+    rowmix_column<1>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+    rowmix_column<2>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+    rowmix_column<3>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
     // pivot row p = slice (kCompactPivots = 8 slices): its share of the
     // partials, added to this thread's own (the column phase multiplies by c_j)
     static_assert(PivotRegs<128, kCompactPivots>::M == 1, "one pivot row per thread");
@@ -251,22 +267,35 @@ __device__ __forceinline__ void decode_rowmix(const DecodeArgs &a, const TileCtx
                          fmaf(kp.y, sv[3], rq.w));
     }
 
-    column_sums<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, op.c, op.v);
+    column_sums<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, sh.cpiv[tid & 127], sh.bcol[tid & 127]);
 
     const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
     pivot_update<128, kCompactPivots>(t, slice, cg, pr, sh, bc);
+    // row-table slot of group g: g when 8-bit, c4 + 2 g (= g8 + 2 (g - g8))
+    // when 4-bit; word-steps wholly of one width and wholly present take a
+    // uniform path, the one straddling the width boundary or the head's last
+    // group a per-lane one
+    const int c4 = -g8;
+    const float al4 = t.alpha * (1.0f / 16.0f);
     float U[8];
 #pragma unroll
     for (int m = 0; m < 16; ++m) {
         const int g = slice + 8 * m;
-        if (g < g8) {
+        if (8 * m + 8 <= g8) {
             unpack_word<8>(w[m], U);
             cw.store(tid + 256 * m, requant_word<8, DIAG>(U, sh.av, sh.al, g, t.alpha, bc));
-        } else if (g < ng) {
+        } else if (8 * m >= g8 && 8 * m + 8 <= ng) {
             unpack_word<4>(w[m], U);
-            cw.store(tid + 256 * m, requant_word<4, DIAG>(U, sh.av, sh.al, g8 + 2 * (g - g8),
-                                                          t.alpha * (1.0f / 16.0f), bc));
+            cw.store(tid + 256 * m, requant_word<4, DIAG>(U, sh.av, sh.al, c4 + 2 * g, al4, bc));
+        } else if (8 * m < ng) {
+            if (g < g8) {
+                unpack_word<8>(w[m], U);
+                cw.store(tid + 256 * m, requant_word<8, DIAG>(U, sh.av, sh.al, g, t.alpha, bc));
+            } else if (g < ng) {
+                unpack_word<4>(w[m], U);
+                cw.store(tid + 256 * m, requant_word<4, DIAG>(U, sh.av, sh.al, c4 + 2 * g, al4, bc));
+            }
         }
     }
 }
