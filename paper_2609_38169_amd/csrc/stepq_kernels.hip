@@ -170,7 +170,8 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
 
 // Column E of the row-mix thread's two sums: one chain over the word groups
 // and their slot views (one accumulator live), written to LDS unscaled.
-// The views are recomputed per column rather than kept.
+// The slot-0 views of the group holding the width boundary (vb) come in
+// formed; the other views are formed again for each column rather than kept.
 template <int E>
 __device__ __forceinline__ void rowmix_column(const DecodeShared<128> &sh, const uint32_t (&w)[16],
                                               const uint32_t (&vb)[4], int slice, int cg, int g8, int ng, int ek,
