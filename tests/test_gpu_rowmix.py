@@ -183,3 +183,26 @@ def test_rowmix_lockstep_steps():
         PT.compare_pivots(n_pv.cpu().numpy().view(np.uint16).reshape(-1, 128, 128), npv, y, tb == 16,
                           f"row-mix lockstep pivots step {step}")
         PT.compare_out(o.cpu().numpy().reshape(-1, 128), o_ref)
+
+
+def test_rowmix_calibrated_pool_b512_sampled():
+    """The row-unit calibrated map that ``bench.py --calibrated row`` times
+    (per-head 8/4-bit splits, 24 FP16 pivot rows, from the calibration
+    pipeline on the workload's own draws) at full pool_b512 size, in the
+    same launch configuration: sampled requests lockstep with the oracle
+    over several frozen steps."""
+    from paper_2609_38169_amd import workloads as W
+    from paper_2609_38169_amd.calibrate import calibrate
+    w = W.workload(2)
+    draws = [W.step_inputs(w, 0, 1000 + t) for t in range(8)]          # calibration draws, not the test steps
+    g = w.n_v_heads // w.n_qk_heads
+    cat = lambda key: np.concatenate([d[key].float().numpy() for d in draws])
+    cal = calibrate(np.repeat(cat("q"), g, axis=1), np.repeat(cat("k"), g, axis=1), cat("beta"), cat("alpha"),
+                    W.initial_state(w, 0, range(4)).numpy(), budget=6.0, cand_bits=(4, 8), unit="row",
+                    n_pivots=24, horizon=1024)
+    bits = cal.row_bits
+    n16 = (bits == 16).sum(1)
+    assert n16.sum() == 24 and n16.max() <= 8 and not (bits == 2).any()
+    _say(f"row-unit calibrated pool_b512: {(bits == 8).sum()} rows @8, {(bits == 4).sum()} @4, 24 pivots")
+    PT.lockstep_run(w, 6, np.array([0, 1, 77, 255, 256, 400, 510, 511]), DEV, row_weight=cal.row_weight, say=_say,
+                    bits=bits)
