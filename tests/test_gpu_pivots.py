@@ -273,3 +273,27 @@ def test_calibrated_head_map_runs_lockstep():
     _say(f"calibrated head map: {int((bits[:, 0] == 8).sum())} heads @8, {int((bits[:, 0] == 4).sum())} @4, "
          f"{int(full16.sum())} FP16 heads")
     PT.lockstep_run(w, 4, np.array([0, 100, 255]), DEV, refit=True, row_weight=cal.row_weight, say=_say, bits=bits)
+
+
+def test_calibrated_head_map_pool_b512_sampled():
+    """The head-unit calibrated map that ``bench.py --calibrated head`` times
+    (whole heads at 8 or 4 bits and one whole FP16 head, from the
+    calibration pipeline on the workload's own draws) at full pool_b512
+    size with frozen scales: the decode step is one launch over the
+    compiled bodies of both widths and the FP16 body, and sampled requests
+    match the oracle lockstep."""
+    from paper_2609_38169_amd.calibrate import calibrate
+    w = W.workload(2)
+    steps = [W.step_inputs(w, 0, 1000 + t) for t in range(8)]        # calibration draws, not the test steps
+    g = w.n_v_heads // w.n_qk_heads
+    cat = lambda key: np.concatenate([s[key].float().numpy() for s in steps])
+    cal = calibrate(np.repeat(cat("q"), g, axis=1), np.repeat(cat("k"), g, axis=1), cat("beta"), cat("alpha"),
+                    W.initial_state(w, 0, range(4)).numpy(), budget=6.0, cand_bits=(4, 8), unit="head",
+                    n_pivots=1, horizon=1024)
+    bits = cal.row_bits
+    full16 = (bits == 16).all(axis=1)
+    assert full16.sum() == 1 and all(len(set(np.unique(b))) == 1 for b in bits)
+    _say(f"calibrated head map pool_b512: {int((bits[:, 0] == 8).sum())} heads @8, "
+         f"{int((bits[:, 0] == 4).sum())} @4, 1 FP16 head")
+    PT.lockstep_run(w, 6, np.array([0, 1, 77, 255, 256, 400, 510, 511]), DEV, row_weight=cal.row_weight, say=_say,
+                    bits=bits)
