@@ -297,3 +297,21 @@ def test_calibrated_head_map_pool_b512_sampled():
          f"{int((bits[:, 0] == 4).sum())} @4, 1 FP16 head")
     PT.lockstep_run(w, 6, np.array([0, 1, 77, 255, 256, 400, 510, 511]), DEV, row_weight=cal.row_weight, say=_say,
                     bits=bits)
+
+
+@pytest.mark.parametrize("kind", ["pivot_rows", "fp16_head"])
+def test_pivot_maps_pool_b512_sampled(kind):
+    """The maps of ``bench.py --pivots`` (1-3 FP16 pivot rows in a seeded
+    quarter of the heads, run by the padded uniform body) and
+    ``bench.py --fp16-heads 1`` (one whole FP16 head beside the uniform
+    heads, one combined launch) at full pool_b512 size with frozen scales:
+    sampled requests lockstep with the oracle."""
+    from paper_2609_38169_amd.pools import row_bits
+    w = W.workload(2)
+    bits = row_bits(w).copy()
+    if kind == "pivot_rows":
+        bits[W.pivot_mask_draw(w).numpy()] = 16
+    else:
+        bits[W.pivot_head_draw(w, 0, 1).numpy()] = 16
+    _say(f"{kind} pool_b512: {int((bits == 16).sum())} FP16 rows")
+    PT.lockstep_run(w, 6, np.array([0, 1, 77, 255, 256, 400, 510, 511]), DEV, say=_say, bits=bits)
