@@ -109,10 +109,12 @@ def fp32_step_bounds(codes, r, c, bits, q, k, v, alpha, beta, levels: int = 0):
 
 
 def compare_codes(gpu: np.ndarray, orc: np.ndarray, y: np.ndarray, what: str = "codes",
-                  frac: float = CODE_MISMATCH_FRAC, window=TIE_WINDOW):
+                  frac: float = CODE_MISMATCH_FRAC, window=TIE_WINDOW, total: int | None = None):
     """Apply the code tolerance to one comparison (at most ``frac`` of the
     entries mismatched, each within ``window`` of a rounding tie: a scalar
-    or a per-code array); returns the number of tie mismatches."""
+    or a per-code array); returns the number of tie mismatches.  ``total``:
+    the number of entries the fraction applies to, when the arrays passed
+    are the part of a larger comparison that holds every mismatch."""
     diff = gpu.astype(np.int16) - orc.astype(np.int16)
     bad = np.nonzero(diff)
     n_bad = bad[0].size
@@ -124,7 +126,8 @@ def compare_codes(gpu: np.ndarray, orc: np.ndarray, y: np.ndarray, what: str = "
     near_tie = np.abs(fpart - 0.5) <= win
     assert np.all(near_tie), (f"{what}: {int((~near_tie).sum())} mismatches away from a rounding tie, e.g. "
                               f"y={y[bad][~near_tie][:4]}")
-    assert n_bad <= frac * gpu.size, f"{what}: {n_bad} of {gpu.size} codes differ"
+    total = gpu.size if total is None else total
+    assert n_bad <= frac * total, f"{what}: {n_bad} of {total} codes differ"
     return n_bad
 
 
@@ -212,7 +215,14 @@ def compare_out(gpu: np.ndarray, orc: np.ndarray, what: str = "o", bound=None):
 
 class Lockstep:
     """One workload layer: a GPU pool plus the oracle's trajectory on
-    ``check_rows`` (batch rows whose slots are compared each step)."""
+    ``check_rows`` (batch rows whose slots are compared each step).
+
+    Every code compared is counted once in ``compared``; ``mismatches``
+    counts the codes that differ from the oracle's (ties).  ``finish``
+    applies the run-level limits.  Frozen steps without pivot rows or fp32
+    bounds take a fast path: the oracle's unrounded values are formed only
+    for the tiles that hold a mismatch, which keeps a check of every tile of
+    a 16,384-tile launch to about a second per step."""
 
     def __init__(self, w: W.Workload, pool, slots: torch.Tensor, bits: np.ndarray, check_rows: np.ndarray,
                  S0_check: np.ndarray, layer: int = 0, refit=False, row_weight=None, levels: int = 0,
@@ -231,6 +241,7 @@ class Lockstep:
         q = oracle.quantize(S.astype(np.float64), self.r, self.c, self.tile_bits, **self.lv)
         self.codes, self.pv = (q[0], q[1]) if self.pivots else (q, None)
         self.piv_mismatches = 0
+        self.piv_compared = 0
         dev = pool.device
         self.ids = slots.index_select(0, torch.as_tensor(self.rows, dtype=torch.long, device=slots.device)).to(dev)
         self.n_tiles = n
@@ -238,7 +249,15 @@ class Lockstep:
             np.asarray(row_weight, np.float64)[None], (len(self.rows),) + bits.shape).reshape(n, w.d_k)
         self.mismatches = 0
         self.compared = 0
-        self.saturated = 0.0
+        self.steps = 0
+
+    @property
+    def saturated(self) -> float:
+        """Fraction of the oracle's current integer codes at +-q_b."""
+        qb = (2 ** (np.minimum(self.tile_bits, 8).astype(np.int32) - 1) - 1).astype(np.int8)[:, :, None]
+        ints = np.broadcast_to((self.tile_bits != 16)[:, :, None], self.codes.shape)
+        sat = (np.abs(self.codes) == qb) & ints
+        return float(sat.sum()) / max(1, int(ints.sum()))
 
     def shaped(self, a, tail):
         return a.reshape((len(self.rows), self.w.n_v_heads) + tail)
@@ -266,8 +285,22 @@ class Lockstep:
             pv = torch.empty((n, w.n_v_heads, w.d_k, w.d_v), dtype=torch.int16, device=dev)
             self.pool.export_pivots(self.ids, pv)
             self.g_pv = pv.cpu().numpy().view(np.uint16).reshape(self.n_tiles, w.d_k, w.d_v)
-        torch.cuda.synchronize()
+        if codes.is_cuda:
+            torch.cuda.synchronize()
         return codes.cpu().numpy().reshape(self.n_tiles, w.d_k, w.d_v), r.cpu().numpy(), c.cpu().numpy()
+
+    def _frozen_fast(self, g_codes, q, k, v, a, b, step):
+        """Frozen step, every tile compared; y only where codes differ."""
+        new, o = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, **self.lv)
+        diff_tiles = np.nonzero(np.any((g_codes != new).reshape(self.n_tiles, -1), axis=1))[0]
+        nb = 0
+        if diff_tiles.size:
+            t = diff_tiles
+            _, _, y = oracle.decode_step(self.codes[t], self.r[t], self.c[t], self.tile_bits[t], q[t], k[t], v[t],
+                                         a[t], b[t], want_y=True, **self.lv)
+            nb = compare_codes(g_codes[t], new[t], y, f"layer {self.layer} step {step} codes",
+                               frac=STEP_MISMATCH_FRAC, total=g_codes.size)
+        return new, o, nb
 
     def check_step(self, inp: dict, o_gpu: torch.Tensor, step: int):
         """Oracle step on its own state, compare with the GPU's result."""
@@ -294,9 +327,7 @@ class Lockstep:
             nb, _ = compare_refit(g_codes, g_r.reshape(rn.shape), g_c, new, rn, cn, y, (ones, ones),
                                   self.tile_bits, f"layer {self.layer} step {step} row absmax",
                                   frac=STEP_MISMATCH_FRAC)
-            self.mismatches += nb
             self.r, self.c = rn, cn
-            self.compared += g_codes.size
         elif self.refit:
             res = oracle.decode_step_refit(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b,
                                            w=self.row_w, want=("y", "c_range"), tie_window=TIE_WINDOW, **pvk,
@@ -308,44 +339,60 @@ class Lockstep:
             nb, tc = compare_refit(g_codes, g_r.reshape(rn.shape), g_c.reshape(cn.shape), new, rn, cn,
                                    ex["y"], ex["c_range"], self.tile_bits, f"layer {self.layer} step {step} refit",
                                    frac=STEP_MISMATCH_FRAC)
-            self.mismatches += nb
             self.tie_cols += tc
             self.r, self.c = rn, cn
-            self.compared += g_codes.size
         else:
-            res = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True, **pvk,
-                                     **self.lv)
-            new, o, y = res[:3]
-            if self.pivots:
-                self.piv_mismatches += compare_pivots(self.g_pv, res[3], y, pmask, f"step {step} pivots")
-                self.pv = res[3]
             assert np.array_equal(g_r.reshape(self.r.shape), self.r), "row scales changed"
             assert np.array_equal(g_c.reshape(self.c.shape), self.c), "column scales changed"
-            win = TIE_WINDOW if dy is None else TIE_WINDOW + dy
-            self.mismatches += compare_codes(g_codes, new, y, f"layer {self.layer} step {step} codes",
-                                             frac=STEP_MISMATCH_FRAC, window=win)
+            if dy is None and not self.pivots:
+                new, o, nb = self._frozen_fast(g_codes, q, k, v, a, b, step)
+            else:
+                res = oracle.decode_step(self.codes, self.r, self.c, self.tile_bits, q, k, v, a, b, want_y=True,
+                                         **pvk, **self.lv)
+                new, o, y = res[:3]
+                if self.pivots:
+                    self.piv_mismatches += compare_pivots(self.g_pv, res[3], y, pmask, f"step {step} pivots")
+                    self.pv = res[3]
+                win = TIE_WINDOW if dy is None else TIE_WINDOW + dy
+                nb = compare_codes(g_codes, new, y, f"layer {self.layer} step {step} codes",
+                                   frac=STEP_MISMATCH_FRAC, window=win)
+        self.mismatches += nb
         self.compared += g_codes.size
+        if self.pivots:
+            self.piv_compared += int(np.count_nonzero(pmask)) * w.d_v
         rows_t = torch.as_tensor(self.rows, dtype=torch.long, device=o_gpu.device)
         og = o_gpu.index_select(0, rows_t).cpu().numpy().reshape(self.n_tiles, w.d_v)
         compare_out(og, o, f"layer {self.layer} step {step} o", bound=o_bound)
-        qb = (2 ** (self.tile_bits.astype(np.int32) - 1) - 1)[:, :, None]
-        self.saturated = float(np.mean(np.abs(new) == qb))
         self.codes = new
+        self.steps += 1
+
+    def finish(self, what: str = ""):
+        """Run-level limits: codes that differ from the oracle's at most
+        CODE_MISMATCH_FRAC of the codes compared over the run, pivot values at
+        most PIVOT_MISMATCH_FRAC (plus one)."""
+        assert self.compared > 0, f"{what}: nothing compared"
+        assert self.mismatches <= CODE_MISMATCH_FRAC * self.compared, \
+            f"{what}: {self.mismatches} of {self.compared} codes differ over the run"
+        if self.pivots:
+            assert self.piv_mismatches <= PIVOT_MISMATCH_FRAC * self.piv_compared + 1, \
+                f"{what}: {self.piv_mismatches} of {self.piv_compared} pivot values differ over the run"
+        return self
 
 
 def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, mutate=None, kda: bool = False,
                  refit=False, row_weight=None, say=print, bits=None, levels: int = 0, state_map=None,
-                 fp32_bounds: bool = False):
+                 fp32_bounds: bool = False, every: int = 16):
     """Full-size decode steps of one workload layer on the GPU, the rows
     ``check_rows`` compared lockstep with the oracle at every step.
     ``state_map`` (optional) transforms the checked slots' initial states
     [rows][Hv][d_k][d_v] before the oracle fits and quantizes them.
     ``fp32_bounds``: judge o (every mode) and, on frozen steps, the codes'
     distance from a rounding tie against the fp32 forward error bounds of
-    the step as well as the fixed limits."""
+    the step as well as the fixed limits.  A progress line every ``every``
+    steps."""
     from paper_2609_38169_amd.pools import build_pool, row_bits
     bits = row_bits(w, layer) if bits is None else bits
-    say(f"lockstep {w.name}: building pool ({w.n_slots} slots)")
+    say(f"lockstep {w.name}: building pool ({w.n_slots} slots), checking {len(check_rows)} of {w.batch} requests")
     pool = build_pool(w, layer, device=device, bits=bits, levels=levels)
     if row_weight is not None:
         pool.set_row_weight(row_weight)
@@ -356,6 +403,7 @@ def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, 
         S0 = np.ascontiguousarray(state_map(S0), dtype=np.float32)
     ls = Lockstep(w, pool, slots, bits, check_rows, S0, layer, refit=refit, row_weight=row_weight, levels=levels,
                   fp32_bounds=fp32_bounds)
+    del S0
     o = torch.empty((w.batch, w.n_v_heads, w.d_v), dtype=torch.float32, device=device)
     for t in range(steps):
         inp = W.step_inputs(w, layer, t, device=device)
@@ -370,15 +418,12 @@ def lockstep_run(w: W.Workload, steps: int, check_rows, device, layer: int = 0, 
             pool.step(slots, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o, refit=refit)
         torch.cuda.synchronize()
         ls.check_step(inp, o, t)
-    assert ls.mismatches <= CODE_MISMATCH_FRAC * ls.compared, \
-        f"{ls.mismatches} of {ls.compared} codes differ over the run"
-    if ls.pivots:
-        n_piv = int(np.count_nonzero(ls.tile_bits == 16)) * w.d_v * steps
-        assert ls.piv_mismatches <= PIVOT_MISMATCH_FRAC * n_piv + 1, \
-            f"{ls.piv_mismatches} of {n_piv} pivot values differ over the run"
+        if every and (t + 1) % every == 0 and t + 1 < steps:
+            say(f"lockstep {w.name}: {t + 1} steps ok ({ls.mismatches} code mismatches of {ls.compared})")
+    ls.finish(f"lockstep {w.name}")
     mode = {False: "", True: " refit", "row_absmax": " row-absmax"}[refit] + (" N2 levels" if levels else "")
     say(f"lockstep {w.name}{' kda' if kda else ''}{mode}: {steps} steps ok, "
-        f"code mismatches {ls.mismatches}, pivot mismatches {ls.piv_mismatches}, "
+        f"{ls.compared} codes compared, code mismatches {ls.mismatches}, pivot mismatches {ls.piv_mismatches}, "
         f"columns on another tie rounding {ls.tie_cols}, "
         f"saturated {ls.saturated:.3f}")
     return ls

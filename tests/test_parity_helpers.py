@@ -3,6 +3,7 @@ planted differences (the rules themselves must accept what the tolerances
 allow and reject everything else)."""
 import numpy as np
 import pytest
+import torch
 
 import _parity as PT
 import oracle
@@ -181,3 +182,110 @@ def test_fp32_step_bounds_cover_fp32_evaluations(spread):
         y, o = _fp32_step(codes, r, c, bits, q, k, v, alpha, beta, split)
         assert np.all(np.abs(y.astype(np.float64) - y64)[live] <= dy[live]), split
         assert np.all(np.abs(o.astype(np.float64) - o64) <= do), split
+
+
+# --- run-level counting of the lockstep (Lockstep.check_step / finish) ------
+
+class _HostPool:
+    """Stand-in for a pool in host memory: ``import_`` records what the
+    lockstep anchors; ``export`` returns the result the test planted."""
+
+    device = torch.device("cpu")
+
+    def __init__(self):
+        self.result = None
+
+    def import_(self, ids, codes, r, c):
+        self.anchored = (codes.numpy().copy(), r.numpy().copy(), c.numpy().copy())
+
+    def export(self, ids, codes, r, c):
+        g_codes, g_r, g_c = self.result
+        codes.copy_(torch.from_numpy(g_codes.reshape(codes.shape)))
+        r.copy_(torch.from_numpy(np.ascontiguousarray(g_r, np.float32).reshape(r.shape)))
+        c.copy_(torch.from_numpy(np.ascontiguousarray(g_c, np.float32).reshape(c.shape)))
+
+
+def _flip_ties(codes, y, bits, n_flip, rng):
+    """The other rounding of ``n_flip`` codes whose unrounded value lies
+    within the tie window (and away from the clip)."""
+    qb = (2.0 ** (bits.astype(np.int64) - 1) - 1)[:, :, None]
+    fpart = np.abs(y) - np.floor(np.abs(y))
+    cand = np.argwhere((np.abs(fpart - 0.5) <= PT.TIE_WINDOW) & (np.abs(y) < qb - 1))
+    assert len(cand) >= n_flip, "too few near-tie codes in the draw"
+    g = codes.copy()
+    for t, i, j in cand[rng.choice(len(cand), n_flip, replace=False)]:
+        lo = np.floor(y[t, i, j])
+        g[t, i, j] = int(lo + 1) if g[t, i, j] == lo else int(lo)
+    return g
+
+
+def _host_lockstep_run(mode, flips_per_step, steps=32):
+    """The tiny workload driven through Lockstep with the oracle's own step
+    standing in for the GPU's, plus planted tie flips."""
+    from paper_2609_38169_amd import workloads as W
+    from paper_2609_38169_amd.pools import row_bits
+    w = W.workload(0)
+    bits = row_bits(w)
+    rows = np.arange(w.batch)
+    S0 = W.initial_state(w, 0, [int(s) for s in W.active_slots(w)[rows]]).numpy()
+    pool = _HostPool()
+    ls = PT.Lockstep(w, pool, W.active_slots(w), bits, rows, S0, refit=mode)
+    rng = np.random.default_rng(5)
+    for t in range(steps):
+        inp = W.step_inputs(w, 0, t)
+        ls.anchor()
+        q, k, v, a, b = PT.oracle_inputs(w, inp, rows)
+        if mode == "refit":
+            new, rn, cn, o, ex = oracle.decode_step_refit(ls.codes, ls.r, ls.c, ls.tile_bits, q, k, v, a, b,
+                                                          want=("y",))
+            y = ex["y"]
+        elif mode == "row_absmax":
+            new, rn, cn, o, y = oracle.decode_step_rowmax(ls.codes, ls.r, ls.c, ls.tile_bits, q, k, v, a, b,
+                                                          want_y=True)
+        else:
+            new, o, y = oracle.decode_step(ls.codes, ls.r, ls.c, ls.tile_bits, q, k, v, a, b, want_y=True)
+            rn, cn = ls.r, ls.c
+        pool.result = (_flip_ties(new, y, ls.tile_bits, flips_per_step, rng), rn, cn)
+        o_gpu = torch.from_numpy(o.astype(np.float32).reshape(w.batch, w.n_v_heads, w.d_v))
+        ls.check_step(inp, o_gpu, t)
+    return ls
+
+
+@pytest.mark.parametrize("mode", ["refit", "row_absmax", False])
+def test_lockstep_counts_each_code_once(mode):
+    """1.5e-4 of the codes compared over a run differ at ties: each step is
+    within its 1e-3 limit, the run is beyond the 1e-4 limit and must fail
+    (each code counted once); 0.6e-4 passes."""
+    steps, per_tile = 32, 64 * 64
+    ls = _host_lockstep_run(mode, flips_per_step=3, steps=steps)
+    assert ls.compared == steps * 4 * per_tile
+    assert ls.mismatches == 3 * steps and ls.mismatches > 1.4e-4 * ls.compared
+    with pytest.raises(AssertionError, match="differ over the run"):
+        ls.finish()
+    ls = _host_lockstep_run(mode, flips_per_step=1, steps=steps)
+    assert ls.mismatches == steps and ls.mismatches < 0.7e-4 * ls.compared
+    ls.finish()
+
+
+def test_lockstep_fast_path_rejects_non_tie_mismatch():
+    """The frozen fast path forms the oracle's unrounded values only for
+    tiles with a mismatch; a mismatch away from a tie still fails."""
+    from paper_2609_38169_amd import workloads as W
+    from paper_2609_38169_amd.pools import row_bits
+    w = W.workload(0)
+    bits = row_bits(w)
+    rows = np.arange(w.batch)
+    S0 = W.initial_state(w, 0, [int(s) for s in W.active_slots(w)[rows]]).numpy()
+    pool = _HostPool()
+    ls = PT.Lockstep(w, pool, W.active_slots(w), bits, rows, S0)
+    inp = W.step_inputs(w, 0, 0)
+    ls.anchor()
+    q, k, v, a, b = PT.oracle_inputs(w, inp, rows)
+    new, o, y = oracle.decode_step(ls.codes, ls.r, ls.c, ls.tile_bits, q, k, v, a, b, want_y=True)
+    fpart = np.abs(y) - np.floor(np.abs(y))
+    t, i, j = np.argwhere((np.abs(fpart - 0.5) > 0.3) & (np.abs(y) < 3))[0]
+    g = new.copy()
+    g[t, i, j] += 1
+    pool.result = (g, ls.r, ls.c)
+    with pytest.raises(AssertionError, match="away from a rounding tie"):
+        ls.check_step(inp, torch.from_numpy(o.astype(np.float32).reshape(w.batch, w.n_v_heads, w.d_v)), 0)
