@@ -133,13 +133,36 @@ typedef struct {
  * record would exceed 4 GiB (tile offsets inside a record are 32-bit). */
 stepq_status stepq_pool_bytes(const stepq_pool_desc *desc, size_t *pool_bytes, size_t *slot_bytes);
 
+/* One launch of a decode step (stepq_pool_plan). */
+typedef struct {
+    int32_t body;             /* the kernel body it runs (library-internal launch code) */
+    int32_t first;            /* first position of head_order the launch covers */
+    int32_t n_heads;          /* value heads it covers: its grid is batch x n_heads workgroups */
+} stepq_launch_desc;
+
+/* The kernel launches of one decode step of a pool with this descriptor and
+ * these stepq_decode_step_ex flags, in launch order.  Host only, no device
+ * work.  Heads of one layout class share a launch (a frozen step of a pool
+ * whose classes all have a combined body is one launch); each launch covers
+ * positions [first, first + n_heads) of head_order [n_v_heads] (NULL: not
+ * written), which receives the value head at each position.  At most
+ * max_launches entries are written to launches; *n_launches receives the
+ * full count.  The plan is checked exactly as stepq_pool_create checks it:
+ * each tile's records lie inside the slot record, every head is listed once
+ * with its own tile offset, and each launch's body runs every head it gets.
+ * Errors as stepq_pool_create (a failed plan check is STEPQ_E_INVALID). */
+stepq_status stepq_pool_plan(const stepq_pool_desc *desc, uint32_t flags, stepq_launch_desc *launches,
+                             int32_t max_launches, int32_t *n_launches, int32_t *head_order);
+
 /* Create a pool.  device_mem: caller-owned device memory of at least
  * stepq_pool_bytes() bytes, 256-byte aligned, whose contents become the
  * pool; or NULL, in which case the library allocates (and later frees) it.
  * The pool contents are undefined until written by stepq_pool_load or
  * stepq_pool_import.  Allocates the small per-head layout tables on the
- * current device.  Blocks until they are copied.  STEPQ_E_NOMEM when an
- * allocation fails, STEPQ_E_HIP when a copy does. */
+ * current device.  Blocks until they are copied.  The decode launches are
+ * planned and checked on the host first (stepq_pool_plan); a plan that
+ * fails its check returns STEPQ_E_INVALID before any allocation.
+ * STEPQ_E_NOMEM when an allocation fails, STEPQ_E_HIP when a copy does. */
 stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, size_t device_mem_bytes,
                                stepq_pool **out);
 

@@ -21,7 +21,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libstepq.so")
 HIP_SOURCES = ["stepq_host.hip", "stepq_kernels.hip", "stepq_refit.hip", "stepq_rowmax.hip"]
-CXX_SOURCES = ["stepq_setup.cpp"]
+CXX_SOURCES = ["stepq_setup.cpp", "stepq_plan.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

@@ -768,6 +768,19 @@ __device__ __forceinline__ void unpack_row_pairs(const uint32_t (&w)[M8 + M4 + M
             Ub[3][g][h] = sbyte_pair_f16<3>(s0, s1);
         }
     }
+    // The converts are inline assembly, whose register writes the compiler's
+    // hazard checks do not see, and the matrix core reads these registers
+    // later.  An s_nop tied to every one of them comes after the last
+    // convert and before any read, whatever the schedule, and keeps the wait
+    // states a VALU write needs before a matrix-core read.
+    asm volatile("s_nop 4"
+                 : "+v"(Ub[0][0][0]), "+v"(Ub[0][0][1]), "+v"(Ub[0][1][0]), "+v"(Ub[0][1][1]), "+v"(Ub[0][2][0]),
+                   "+v"(Ub[0][2][1]), "+v"(Ub[0][3][0]), "+v"(Ub[0][3][1]), "+v"(Ub[1][0][0]), "+v"(Ub[1][0][1]),
+                   "+v"(Ub[1][1][0]), "+v"(Ub[1][1][1]), "+v"(Ub[1][2][0]), "+v"(Ub[1][2][1]), "+v"(Ub[1][3][0]),
+                   "+v"(Ub[1][3][1]), "+v"(Ub[2][0][0]), "+v"(Ub[2][0][1]), "+v"(Ub[2][1][0]), "+v"(Ub[2][1][1]),
+                   "+v"(Ub[2][2][0]), "+v"(Ub[2][2][1]), "+v"(Ub[2][3][0]), "+v"(Ub[2][3][1]), "+v"(Ub[3][0][0]),
+                   "+v"(Ub[3][0][1]), "+v"(Ub[3][1][0]), "+v"(Ub[3][1][1]), "+v"(Ub[3][2][0]), "+v"(Ub[3][2][1]),
+                   "+v"(Ub[3][3][0]), "+v"(Ub[3][3][1]));
 }
 
 // The thread's column partials of S^T k and S^T q (before the c_j factor)

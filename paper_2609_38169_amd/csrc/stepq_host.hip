@@ -10,6 +10,7 @@
 
 #include "stepq.h"
 #include "stepq_internal.h"
+#include "stepq_plan.h"
 
 using stepq::HeadInfo;
 
@@ -26,17 +27,8 @@ struct stepq_pool {
     float *d_roww = nullptr;          // [Hv][dk] row-impact factors, physical order
     int device = 0;
     int levels = STEPQ_LEVELS_ABSMAX; // level normalisation of the codes
-    int layout = 0;                   // uniform layout of every head, or 0
-    // Layout classes of a mixed pool at d_v = 128: heads grouped by their
-    // uniform layout (1-5), or the generic heads (0, or kCompactGeneric when
-    // all of them fit the compact body); one decode launch per class.  Empty
-    // when one launch covers every head.
-    std::vector<int> cls_layout, cls_off, cls_cnt;
-    // kMixedBase + L when the classes are uniform layout L (1 or 2) plus
-    // compact generic and/or whole FP16 heads: then a decode step (without
-    // refit) is one launch over the whole head list.  0 otherwise.
-    int mixed_code = 0;
-    stepq::LaunchHead *d_head_order = nullptr;  // [Hv] heads ordered by class, device
+    stepq::LaunchPlan plan;           // the decode launches of a step (stepq_plan.h)
+    stepq::LaunchHead *d_head_order = nullptr;  // plan.order on the device
 };
 
 namespace {
@@ -54,106 +46,16 @@ stepq_status hip_fail(hipError_t e, const char *what)
     return fail(STEPQ_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-size_t round128(size_t x) { return (x + 127) & ~static_cast<size_t>(127); }
-
 // Validate a descriptor and derive the layout tables (include/stepq.h).
 stepq_status build_layout(const stepq_pool_desc *d, std::vector<HeadInfo> *heads, std::vector<uint8_t> *perm,
                           size_t *slot_bytes)
 {
-    if (!d) return fail(STEPQ_E_INVALID, "descriptor is NULL");
-    if (d->n_slots < 1 || d->n_v_heads < 1 || d->n_qk_heads < 1)
-        return fail(STEPQ_E_INVALID, "n_slots, n_v_heads and n_qk_heads must be >= 1");
-    if (d->n_v_heads % d->n_qk_heads != 0)
-        return fail(STEPQ_E_INVALID, "n_v_heads must be a multiple of n_qk_heads");
-    if (d->d_k < 1 || d->d_k > stepq::kMaxDk) return fail(STEPQ_E_UNSUPPORTED, "d_k must be in 1..128");
-    if (d->d_v != 64 && d->d_v != 128) return fail(STEPQ_E_UNSUPPORTED, "d_v must be 64 or 128");
-    if (!d->row_bits) return fail(STEPQ_E_INVALID, "row_bits is NULL");
-    if (d->levels != STEPQ_LEVELS_ABSMAX && d->levels != STEPQ_LEVELS_POW2)
-        return fail(STEPQ_E_INVALID, "levels must be STEPQ_LEVELS_ABSMAX or STEPQ_LEVELS_POW2");
-    const int Hv = d->n_v_heads, dk = d->d_k, dv = d->d_v;
-    heads->assign(Hv, HeadInfo{});
-    perm->assign(static_cast<size_t>(Hv) * dk, 0);
-    size_t off = 0;
-    for (int h = 0; h < Hv; ++h) {
-        const uint8_t *b = d->row_bits + static_cast<size_t>(h) * dk;
-        int n16 = 0, n8 = 0, n4 = 0, n2 = 0;
-        for (int i = 0; i < dk; ++i) {
-            if (b[i] == 16) ++n16;
-            else if (b[i] == 8) ++n8;
-            else if (b[i] == 4) ++n4;
-            else if (b[i] == 2) ++n2;
-            else return fail(STEPQ_E_INVALID, "row_bits entries must be 2, 4, 8 or 16");
-        }
-        const bool f16_head = n16 == dk && dk == 128 && dv == 128;   // a whole FP16 head
-        if (n16 > stepq::kMaxPivots && !f16_head)
-            return fail(STEPQ_E_UNSUPPORTED, "at most 32 pivot (16) rows per head, or all rows of a 128x128 head");
-        int p = 0;
-        for (int width : {16, 8, 4, 2})
-            for (int i = 0; i < dk; ++i)
-                if (b[i] == width) (*perm)[static_cast<size_t>(h) * dk + p++] = static_cast<uint8_t>(i);
-        HeadInfo &hi = (*heads)[h];
-        hi.n16 = static_cast<uint16_t>(n16);
-        hi.n8 = static_cast<uint16_t>(n8);
-        hi.n4 = static_cast<uint16_t>(n4);
-        hi.n2 = static_cast<uint16_t>(n2);
-        hi.g8 = static_cast<uint16_t>(n8);
-        hi.g4 = static_cast<uint16_t>((n4 + 1) / 2);
-        hi.g2 = static_cast<uint16_t>((n2 + 3) / 4);
-        hi.layout = 0;
-        // At d = 128, integer rows that fit a uniform mix (first in table
-        // order) are stored in it: exactly, or, when pivot rows take some of
-        // the 128, with each width class padded by empty groups.
-        if (dv == 128 && dk == 128 && !f16_head)
-            for (int L = 0; L < stepq::kNumUniformLayouts; ++L) {
-                const stepq::UniformLayout &u = stepq::kUniformLayouts[L];
-                if (8 * u.m8 < n8 || 16 * u.m4 < n4 || 32 * u.m2 < n2) continue;
-                hi.g8 = static_cast<uint16_t>(8 * u.m8);
-                hi.g4 = static_cast<uint16_t>(8 * u.m4);
-                hi.g2 = static_cast<uint16_t>(8 * u.m2);
-                if (n16 == 0) hi.layout = L + 1;
-                else if (n16 <= stepq::kCompactPivots) hi.layout = stepq::kPivotUniformBase + L + 1;
-                break;
-            }
-        hi.groups = static_cast<uint32_t>(hi.g8 + hi.g4 + hi.g2);
-        if (f16_head) hi.layout = stepq::kF16HeadLayout;
-        const size_t creg = round128(static_cast<size_t>(hi.groups) * dv);
-        const size_t preg = round128(static_cast<size_t>(n16) * 2u * dv);
-        const size_t tb = round128(creg + preg + 4u * static_cast<size_t>(dk) + 4u * static_cast<size_t>(dv));
-        hi.piv_off = static_cast<uint32_t>(creg);
-        hi.r_off = static_cast<uint32_t>(creg + preg);
-        hi.tile_bytes = static_cast<uint32_t>(tb);
-        hi.tile_off = static_cast<uint32_t>(off);
-        // the compiled bodies address codes (or FP16 values), r and c from these sizes
-        if (hi.layout > 0 && static_cast<int>(hi.layout) <= stepq::kNumUniformLayouts) {
-            const stepq::UniformLayout &u = stepq::kUniformLayouts[hi.layout - 1];
-            const uint32_t m = static_cast<uint32_t>(u.m8 + u.m4 + u.m2);
-            if (hi.r_off != 1024u * m || hi.tile_bytes != 1024u * (m + 1))
-                return fail(STEPQ_E_INVALID, "internal: uniform head layout does not match its tile size");
-        }
-        if (static_cast<int>(hi.layout) > stepq::kPivotUniformBase) {
-            const stepq::UniformLayout &u = stepq::kUniformLayouts[hi.layout - stepq::kPivotUniformBase - 1];
-            const uint32_t m = static_cast<uint32_t>(u.m8 + u.m4 + u.m2);
-            if (hi.piv_off != 1024u * m || hi.r_off != 1024u * m + 256u * n16 || hi.tile_bytes != hi.r_off + 1024u)
-                return fail(STEPQ_E_INVALID, "internal: padded pivot head layout does not match its tile size");
-        }
-        if (static_cast<int>(hi.layout) == stepq::kF16HeadLayout &&
-            (hi.piv_off != 0 || hi.r_off != 128u * 256u || hi.tile_bytes != 128u * 256u + 1024u))
-            return fail(STEPQ_E_INVALID, "internal: FP16 head layout does not match its tile size");
-        off += tb;
-        // tile offsets inside a slot record are 32-bit
-        if (off > UINT32_MAX) return fail(STEPQ_E_UNSUPPORTED, "slot record over 4 GiB: too many heads");
-    }
-    *slot_bytes = off;
-    return STEPQ_OK;
+    std::string err;
+    const stepq_status st = stepq::derive_layout(d, heads, perm, slot_bytes, &err);
+    return st == STEPQ_OK ? st : fail(st, err);
 }
 
-stepq::FastDiv fast_div(uint32_t d)
-{
-    uint32_t sh = 0;
-    while ((1ull << sh) < d) ++sh;
-    const uint64_t m = ((1ull << 32) * ((1ull << sh) - d)) / d + 1;
-    return stepq::FastDiv{static_cast<uint32_t>(m), sh};
-}
+using stepq::fast_div;
 
 stepq::PoolView view(const stepq_pool *p)
 {
@@ -254,6 +156,41 @@ stepq_status stepq_pool_bytes(const stepq_pool_desc *desc, size_t *pool_bytes, s
     return STEPQ_OK;
 }
 
+stepq_status stepq_pool_plan(const stepq_pool_desc *desc, uint32_t flags, stepq_launch_desc *launches,
+                             int32_t max_launches, int32_t *n_launches, int32_t *head_order)
+{
+    if (!n_launches) return fail(STEPQ_E_INVALID, "n_launches is NULL");
+    *n_launches = 0;
+    if (max_launches < 0 || (max_launches > 0 && !launches)) return fail(STEPQ_E_INVALID, "bad launches buffer");
+    if (flags & ~static_cast<uint32_t>(STEPQ_STEP_KDA_GATE | STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX |
+                                       STEPQ_STEP_ADJACENT_SLOTS))
+        return fail(STEPQ_E_INVALID, "unknown decode-step flags");
+    std::vector<HeadInfo> heads;
+    std::vector<uint8_t> perm;
+    size_t sb = 0;
+    stepq_status st = build_layout(desc, &heads, &perm, &sb);
+    if (st != STEPQ_OK) return st;
+    stepq::LaunchPlan plan;
+    stepq::plan_launches(heads, desc->d_k, desc->d_v, &plan);
+    std::string why;
+    if (!stepq::check_plan(plan, heads, desc->d_k, desc->d_v, sb, &why))
+        return fail(STEPQ_E_INVALID, "internal: launch plan check failed: " + why);
+    const int Hv = desc->n_v_heads;
+    std::vector<stepq_launch_desc> out;
+    if (plan.mixed_code != 0 && !(flags & (STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX)))
+        out.push_back({plan.mixed_code, 0, Hv});
+    else if (plan.cls_code.empty())
+        out.push_back({plan.layout, 0, Hv});
+    else
+        for (size_t c = 0; c < plan.cls_code.size(); ++c)
+            out.push_back({plan.cls_code[c], plan.cls_off[c], plan.cls_cnt[c]});
+    for (size_t i = 0; i < out.size() && static_cast<int32_t>(i) < max_launches; ++i) launches[i] = out[i];
+    *n_launches = static_cast<int32_t>(out.size());
+    if (head_order)
+        for (int x = 0; x < Hv; ++x) head_order[x] = plan.order.empty() ? x : plan.order[x].h;
+    return STEPQ_OK;
+}
+
 stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, size_t device_mem_bytes,
                                stepq_pool **out)
 {
@@ -272,11 +209,15 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
     p->dk = desc->d_k;
     p->dv = desc->d_v;
     p->bits.assign(desc->row_bits, desc->row_bits + static_cast<size_t>(p->Hv) * p->dk);
-    p->layout = static_cast<int>(p->heads[0].layout);
-    for (const HeadInfo &hi : p->heads)
-        if (static_cast<int>(hi.layout) != p->layout) p->layout = 0;
-    // padded pivot heads differ in their row counts, which travel in the head list
-    if (p->layout > stepq::kPivotUniformBase) p->layout = 0;
+    // the decode launches, checked against the head records before any
+    // allocation or launch: a plan that would send a workgroup outside its
+    // tile, or a head to a body that does not run it, is refused here
+    stepq::plan_launches(p->heads, p->dk, p->dv, &p->plan);
+    std::string why;
+    if (!stepq::check_plan(p->plan, p->heads, p->dk, p->dv, p->slot_bytes, &why)) {
+        delete p;
+        return fail(STEPQ_E_INVALID, "internal: launch plan check failed: " + why);
+    }
     p->pool_bytes = p->slot_bytes * static_cast<size_t>(p->n_slots);
     hipError_t e = hipGetDevice(&p->device);
     if (e != hipSuccess) {
@@ -311,86 +252,8 @@ stepq_status stepq_pool_create(const stepq_pool_desc *desc, void *device_mem, si
         const std::vector<float> ones(p->perm.size(), 1.0f);
         e = hipMemcpy(p->d_roww, ones.data(), sizeof(float) * ones.size(), hipMemcpyHostToDevice);
     }
-    if (e == hipSuccess && p->layout == 0 && p->dv == 128) {
-        // one class per layout present; larger classes are launched first
-        std::vector<stepq::LaunchHead> order;
-        std::vector<std::pair<int, int>> cls;   // (-count, layout)
-        std::vector<int> codes;
-        for (int L = 0; L <= stepq::kF16HeadLayout; ++L) codes.push_back(L);
-        for (int L = 1; L <= stepq::kNumUniformLayouts; ++L) codes.push_back(stepq::kPivotUniformBase + L);
-        for (int L : codes) {
-            int n = 0;
-            for (const HeadInfo &hi : p->heads) n += static_cast<int>(hi.layout) == L;
-            if (n > 0) cls.emplace_back(-n, L);
-        }
-        std::sort(cls.begin(), cls.end());
-        for (const auto &c : cls) {
-            int code = c.second;
-            if (code == 0) {
-                // the generic heads take the row-mix body when every one of
-                // them is a compact 8/4-bit head with few pivot rows, else the
-                // compact generic body when all of them fit it
-                bool fits = true, rowmix = p->dk == 128;
-                for (const HeadInfo &hi : p->heads) {
-                    if (hi.layout != 0) continue;
-                    if (hi.groups > static_cast<uint32_t>(stepq::kCompactGroups) || hi.n16 > stepq::kCompactPivots)
-                        fits = false;
-                    if (hi.n2 != 0 || hi.n16 > stepq::kCompactPivots || hi.g8 != hi.n8 ||
-                        hi.g4 != (hi.n4 + 1) / 2 || hi.g2 != 0)
-                        rowmix = false;
-                }
-                if (rowmix) code = stepq::kRowMix;
-                else if (fits) code = stepq::kCompactGeneric;
-            }
-            p->cls_layout.push_back(code);
-            p->cls_off.push_back(static_cast<int>(order.size()));
-            p->cls_cnt.push_back(-c.first);
-            for (int h = 0; h < p->Hv; ++h) {
-                const HeadInfo &hi = p->heads[h];
-                if (static_cast<int>(hi.layout) != c.second) continue;
-                const int32_t counts = static_cast<int32_t>(hi.n16 | (hi.n8 << 8) | (hi.n4 << 16));
-                order.push_back({h, hi.tile_off, static_cast<int32_t>(hi.layout), counts});
-            }
-        }
-        // one uniform class of layout 1 or 2 whose other classes are its
-        // padded pivot heads, compact generic or whole FP16 heads: a decode
-        // step is one combined launch
-        int L = 0, others = 0, pivots = 0;
-        bool fits = true, f16 = false;
-        for (int code : p->cls_layout)
-            if (code == 1 || code == 2) {
-                if (L != 0) fits = false;
-                L = code;
-            }
-        for (int code : p->cls_layout) {
-            if (code == 1 || code == 2) continue;
-            if (code == stepq::kCompactGeneric || code == stepq::kF16HeadLayout ||
-                (L != 0 && code == stepq::kPivotUniformBase + L)) {
-                ++others;
-                f16 = f16 || code == stepq::kF16HeadLayout;
-                pivots += code == stepq::kPivotUniformBase + L;
-            } else {
-                fits = false;
-            }
-        }
-        // several classes that all have compiled bodies (uniform mixes,
-        // their padded pivot heads, whole FP16 heads): one launch of those
-        // bodies only, which fits fewer registers than the ones below.  The
-        // head list keeps the classes together: tiles of one kind in runs
-        // stream better than interleaved kinds.
-        bool compiled = p->cls_layout.size() > 1, piv = false;
-        for (int code : p->cls_layout) {
-            const bool pc = code > stepq::kPivotUniformBase &&
-                            code <= stepq::kPivotUniformBase + stepq::kNumUniformLayouts;
-            compiled = compiled && ((code >= 1 && code <= stepq::kF16HeadLayout) || pc);
-            piv = piv || pc;
-        }
-        if (fits && L != 0 && others > 0 && others == pivots)
-            p->mixed_code = stepq::kMixedPivotBase + L;       // one uniform mix and its pivot heads: one body
-        else if (compiled)
-            p->mixed_code = piv ? stepq::kMultiPivot : stepq::kMultiUniform;
-        else if (fits && L != 0 && others > 0)
-            p->mixed_code = (f16 ? stepq::kMixedF16Base : stepq::kMixedBase) + L;
+    if (e == hipSuccess && !p->plan.order.empty()) {
+        const auto &order = p->plan.order;
         e = hipMalloc(reinterpret_cast<void **>(&p->d_head_order), sizeof(stepq::LaunchHead) * order.size());
         if (e == hipSuccess)
             e = hipMemcpy(p->d_head_order, order.data(), sizeof(stepq::LaunchHead) * order.size(),
@@ -483,24 +346,25 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
                                                  : stepq::launch_decode(a, bf16, diag, layout, s);
     };
     hipError_t e = hipSuccess;
-    if (p->mixed_code != 0 && !(flags & (STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX))) {
+    const stepq::LaunchPlan &plan = p->plan;
+    if (plan.mixed_code != 0 && !(flags & (STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX))) {
         // uniform heads share one launch with compact generic and whole FP16 heads
         a.head_list = p->d_head_order;
         a.n_heads = p->Hv;
         a.div_heads = fast_div(static_cast<uint32_t>(p->Hv));
-        e = launch(p->mixed_code);
-    } else if (p->cls_layout.empty()) {
+        e = launch(plan.mixed_code);
+    } else if (plan.cls_code.empty()) {
         a.head_list = nullptr;
         a.n_heads = p->Hv;
         a.div_heads = fast_div(static_cast<uint32_t>(p->Hv));
-        e = launch(p->layout);
+        e = launch(plan.layout);
     } else {
         // a mixed pool: one launch per layout class, each with its own register budget
-        for (size_t c = 0; c < p->cls_layout.size() && e == hipSuccess; ++c) {
-            a.head_list = p->d_head_order + p->cls_off[c];
-            a.n_heads = p->cls_cnt[c];
-            a.div_heads = fast_div(static_cast<uint32_t>(p->cls_cnt[c]));
-            e = launch(p->cls_layout[c]);
+        for (size_t c = 0; c < plan.cls_code.size() && e == hipSuccess; ++c) {
+            a.head_list = p->d_head_order + plan.cls_off[c];
+            a.n_heads = plan.cls_cnt[c];
+            a.div_heads = fast_div(static_cast<uint32_t>(plan.cls_cnt[c]));
+            e = launch(plan.cls_code[c]);
         }
     }
     return e == hipSuccess ? STEPQ_OK : hip_fail(e, "decode launch");

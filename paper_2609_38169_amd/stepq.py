@@ -25,7 +25,7 @@ STEPQ_STEP_KDA_GATE, STEPQ_STEP_REFIT, STEPQ_STEP_ROW_ABSMAX, STEPQ_STEP_ADJACEN
 _STATUS = {0: "STEPQ_OK", 1: "STEPQ_E_INVALID", 2: "STEPQ_E_UNSUPPORTED", 3: "STEPQ_E_NOMEM", 4: "STEPQ_E_HIP"}
 
 EXPORTED = (
-    "stepq_pool_bytes", "stepq_pool_create", "stepq_pool_destroy", "stepq_pool_device_ptr",
+    "stepq_pool_bytes", "stepq_pool_plan", "stepq_pool_create", "stepq_pool_destroy", "stepq_pool_device_ptr",
     "stepq_pool_load", "stepq_decode_step", "stepq_decode_step_kda", "stepq_decode_step_ex",
     "stepq_pool_set_row_weight", "stepq_pool_dequant", "stepq_pool_export", "stepq_pool_import",
     "stepq_pool_export_pivots", "stepq_pool_import_pivots", "stepq_last_error", "stepq_setup_fit",
@@ -38,6 +38,10 @@ class StepqError(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"{_STATUS.get(status, status)}: {msg}")
         self.status = status
+
+
+class stepq_launch_desc(ctypes.Structure):
+    _fields_ = [("body", ctypes.c_int32), ("first", ctypes.c_int32), ("n_heads", ctypes.c_int32)]
 
 
 class stepq_pool_desc(ctypes.Structure):
@@ -60,6 +64,7 @@ def lib():
         st = ctypes.c_int
         sig = {
             "stepq_pool_bytes": ([P, P, P], st),
+            "stepq_pool_plan": ([P, ctypes.c_uint32, P, i32, P, P], st),
             "stepq_pool_create": ([P, P, ctypes.c_size_t, P], st),
             "stepq_pool_destroy": ([P], None),
             "stepq_pool_device_ptr": ([P], P),
@@ -134,6 +139,19 @@ def stepq_pool_bytes(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits, levels=
     pb, sb = ctypes.c_size_t(), ctypes.c_size_t()
     _check(lib().stepq_pool_bytes(ctypes.byref(d), ctypes.byref(pb), ctypes.byref(sb)))
     return pb.value, sb.value
+
+
+def stepq_pool_plan(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits, levels=STEPQ_LEVELS_ABSMAX, flags: int = 0):
+    """The launches of one decode step (host only): a list of (body,
+    first, n_heads) and the head order [n_v_heads] their head lists index."""
+    d, _keep = _desc(n_slots, n_v_heads, n_qk_heads, d_k, d_v, row_bits, levels)
+    n = ctypes.c_int32()
+    order = np.empty(n_v_heads, np.int32)
+    _check(lib().stepq_pool_plan(ctypes.byref(d), int(flags), None, 0, ctypes.byref(n), None))
+    buf = (stepq_launch_desc * max(1, n.value))()
+    _check(lib().stepq_pool_plan(ctypes.byref(d), int(flags), buf, n.value, ctypes.byref(n),
+                                 order.ctypes.data_as(ctypes.c_void_p)))
+    return [(x.body, x.first, x.n_heads) for x in buf[:n.value]], order
 
 
 class Pool:

@@ -12,6 +12,7 @@ import torch
 
 import oracle
 from paper_2609_38169_amd import stepq, workloads as W
+from paper_2609_38169_amd.pools import row_bits
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -316,3 +317,61 @@ def test_synthetic_pivot_draws():
         h = W.pivot_head_draw(w, 0, count)
         assert h.shape == (w.n_v_heads,) and int(h.sum()) == count and torch.equal(h, W.pivot_head_draw(w, 0, count))
     assert not torch.equal(W.pivot_head_draw(w, 0, 2), W.pivot_head_draw(w, 1, 2))
+
+
+def _plan_cases():
+    """Descriptors of every planning path: each workload's map, uniform mixes
+    side by side, padded pivot heads, whole FP16 heads, row-mix heads,
+    generic heads, d_v = 64 and ragged d_k."""
+    rng = np.random.default_rng(21)
+    cases = []
+    for i in range(5):
+        w = W.workload(i)
+        cases.append((w.name, w.n_v_heads, w.n_qk_heads, w.d_k, w.d_v, row_bits(w)))
+
+    def mix(m8, m4, m2, piv=0):
+        b = np.array([8] * m8 + [4] * m4 + [2] * m2, np.uint8)
+        b[rng.choice(128, piv, replace=False)] = 16
+        return rng.permutation(b)
+    heads = [mix(64, 64, 0), mix(128, 0, 0), mix(0, 128, 0), mix(64, 64, 0, 3), np.full(128, 16, np.uint8)]
+    cases.append(("compiled classes", 5, 5, 128, 128, np.stack(heads)))
+    cases.append(("rowmix", 6, 3, 128, 128, np.stack([mix(n8, 128 - n8, 0, p) for n8, p in
+                                                      [(50, 0), (70, 3), (61, 8), (88, 1), (40, 2), (99, 0)]])))
+    cases.append(("generic + uniform", 4, 2, 128, 128,
+                  np.stack([mix(64, 64, 0), rng.choice([2, 4, 8], 128).astype(np.uint8), mix(64, 64, 0),
+                            mix(30, 50, 48)])))
+    cases.append(("d_v 64", 3, 1, 37, 64, rng.choice([2, 4, 8, 16], (3, 37), p=[.3, .3, .3, .1]).astype(np.uint8)))
+    cases.append(("ragged d_k", 2, 2, 96, 128, rng.choice([2, 4, 8], (2, 96)).astype(np.uint8)))
+    return cases
+
+
+@pytest.mark.parametrize("flags", [0, stepq.STEPQ_STEP_REFIT, stepq.STEPQ_STEP_ROW_ABSMAX])
+def test_pool_plan_launches_cover_every_head_once(flags):
+    """stepq_pool_plan (host only): the launches of a decode step cut the
+    head order into consecutive slices that cover it, and the head order is
+    a permutation of the value heads; the library's own plan check (the one
+    stepq_pool_create runs) accepts every case."""
+    for name, Hv, Hqk, dk, dv, bits in _plan_cases():
+        launches, order = stepq.stepq_pool_plan(2, Hv, Hqk, dk, dv, bits, flags=flags)
+        assert sorted(order.tolist()) == list(range(Hv)), name
+        pos = 0
+        for body, first, n in launches:
+            assert first == pos and n >= 1, (name, launches)
+            pos += n
+        assert pos == Hv, (name, launches)
+
+
+def test_pool_plan_launch_counts():
+    """One launch for the uniform workloads, one combined launch for
+    layer_b64's two classes of whole 8- and 4-bit heads when frozen, one per
+    class when refitting."""
+    for i in (0, 2, 3, 4):
+        w = W.workload(i)
+        assert len(stepq.stepq_pool_plan(1, w.n_v_heads, w.n_qk_heads, w.d_k, w.d_v, row_bits(w))[0]) == 1
+    w = W.workload(1)
+    assert len(stepq.stepq_pool_plan(1, w.n_v_heads, w.n_qk_heads, w.d_k, w.d_v, row_bits(w))[0]) == 1
+    refit = stepq.stepq_pool_plan(1, w.n_v_heads, w.n_qk_heads, w.d_k, w.d_v, row_bits(w),
+                                  flags=stepq.STEPQ_STEP_REFIT)[0]
+    assert len(refit) == 2 and sum(n for _, _, n in refit) == w.n_v_heads
+    with pytest.raises(stepq.StepqError):
+        stepq.stepq_pool_plan(1, 2, 1, 128, 128, np.full((2, 128), 6, np.uint8))
