@@ -20,6 +20,13 @@ Prints one JSON line (rank 0):
              read + codes written + scales read) / its mean launch duration
              (HIP events around the K back-to-back timed launches, gaps
              included), against the 8 TB/s HBM peak
+  runs       the K timed steps split into --runs back-to-back runs (one
+             event at each boundary): per-run ms per step, median, min, max
+  bandwidth_refs  outside the timed region: a plain device copy of the
+             launch's state bytes, and the library's memory-only reference
+             of the decode launch (stepq_decode_stream_ref: same slots,
+             workgroup order and traffic, no arithmetic), with the decode
+             kernel's time over the reference's
   cpu_baseline  the fp64 oracle on the host cores on a bounded sample
 """
 from __future__ import annotations
@@ -235,6 +242,19 @@ def pool_case(args, w, mode, dev):
                                               adjacent=adjacent[key[1]])
         prepared[key]()
 
+    o_ref = torch.empty_like(o)
+    prepared_ref = {}
+
+    def ref(i):
+        # the memory-only reference launch of step i (same slots, order and traffic; scalar gate read)
+        j = i % len(subsets)
+        if j not in prepared_ref:
+            inp = W.step_inputs(w, 0, 0, device=dev)
+            prepared_ref[j] = (inp, pool.prepare_stream_ref(subsets[j], inp["q"], inp["k"], inp["v"], inp["alpha"],
+                                                            inp["beta"], o_ref, stream=torch.cuda.current_stream(),
+                                                            adjacent=adjacent[j]))
+        prepared_ref[j][1]()
+
     mix = {"pool_b512": "6-bit mixed {4,8}", "pool_4bit": "4-bit mixed {2,4,8}, heavy-tailed states"}[w.name]
     if args.calibrated:
         ints = bits[bits != 16]
@@ -245,7 +265,8 @@ def pool_case(args, w, mode, dev):
         rows = int((bits == 16).sum()) - full * w.d_k
         mix += f", {rows} FP16 pivot rows in {int(((bits == 16).any(1) & ~(bits == 16).all(1)).sum())} heads" if rows else ""
         mix += f", {full} of {w.n_v_heads} heads entirely FP16" if full else ""
-    return Case(w=w, bits=bits, step=step, launches_per_step=1, n_subsets=len(subsets), keep=(pool, inputs, o),
+    return Case(w=w, bits=bits, step=step, ref=ref, launches_per_step=1, n_subsets=len(subsets),
+                keep=(pool, inputs, o, o_ref),
                 tiles_per_step=w.batch * w.n_v_heads, layers=1,
                 workload=f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
                          f"d_k=d_v={w.d_k}, {mix}, fp32 scales, bf16 activations",
@@ -293,10 +314,22 @@ def stack_case(args, w, mode, dev):
     def step(i):
         graph.replay()
 
+    o_ref = torch.empty_like(bufs[0]["o"])
+    ref_call = []
+
+    def ref(i):
+        # the memory-only reference of one layer's launch (layer 0: same slots, order and traffic)
+        if not ref_call:
+            b = bufs[0]
+            alpha = b["alpha"] if b["alpha"].dim() == 2 else b["alpha"][:, :, 0].contiguous()
+            ref_call.append((alpha, pools[0].prepare_stream_ref(slots, b["q"], b["k"], b["v"], alpha, b["beta"], o_ref,
+                                                                stream=torch.cuda.current_stream(), adjacent=adjacent)))
+        ref_call[0][1]()
+
     pool_bytes = sum(p.pool_bytes for p in pools)
     fp32_bytes = w.layers * w.n_slots * w.n_v_heads * w.d_k * w.d_v * 4
-    return Case(w=w, bits=bits0, step=step, launches_per_step=w.layers, n_subsets=1,
-                keep=(pools, bufs, graph, calls, side), tiles_per_step=w.layers * w.batch * w.n_v_heads,
+    return Case(w=w, bits=bits0, step=step, ref=ref, launches_per_step=w.layers, n_subsets=1,
+                keep=(pools, bufs, graph, calls, side, o_ref, ref_call), tiles_per_step=w.layers * w.batch * w.n_v_heads,
                 layers=w.layers,
                 workload=f"{w.name}: {w.layers} layers x B={w.batch} requests x {w.n_v_heads} value heads "
                          f"({w.n_qk_heads} q/k heads), d_k=d_v={w.d_k}, 6-bit mixed {{4,8}}, fp32 scales, "
@@ -322,7 +355,12 @@ def main():
                     help="list each step's active requests in slot order (pool workloads; default: as drawn)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--copy-ref", action="store_true", help="also time a plain device copy of the same bytes")
+    ap.add_argument("--runs", type=int, default=3,
+                    help="the K timed steps are split into this many back-to-back runs; their median, min and max "
+                         "per-step times are reported beside the whole-region figures")
+    ap.add_argument("--no-copy-ref", action="store_true",
+                    help="skip the bandwidth references (a plain device copy of the step's state bytes, and the "
+                         "library's memory-only reference of the decode launch with the same slots and order)")
     ap.add_argument("--kda", action="store_true", help="channel-wise (KDA) gates [B][Hv][d_k] instead of alpha")
     ap.add_argument("--refit", action="store_true", help="online dual-axis refit of the scales in every step")
     ap.add_argument("--row-absmax", action="store_true",
@@ -398,15 +436,21 @@ def main():
         case.step(i)                    # prepare every call outside the timed region
     torch.cuda.synchronize()
     # timed region: K back-to-back steps between two events on the launch stream
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
-    t0.record(stream)
-    for i in range(K):
-        case.step(args.warmup + i)
-    t1.record(stream)
+    # (split into R back-to-back runs with an event at each boundary: the
+    # per-run times give the run-to-run spread; the region is still exactly
+    # K steps between its first and last event)
+    R = max(1, min(args.runs, K))
+    bounds = [K * j // R for j in range(R + 1)]
+    tev = [torch.cuda.Event(enable_timing=True) for _ in range(R + 1)]
+    tev[0].record(stream)
+    for j in range(R):
+        for i in range(bounds[j], bounds[j + 1]):
+            case.step(args.warmup + i)
+        tev[j + 1].record(stream)
     torch.cuda.synchronize()
-    total_ms = t0.elapsed_time(t1)
+    total_ms = tev[0].elapsed_time(tev[R])
     kern_ms = total_ms / (K * LPS)  # mean launch duration, gaps between launches included
+    run_ms = [tev[j].elapsed_time(tev[j + 1]) / (bounds[j + 1] - bounds[j]) for j in range(R)]
 
     # diagnostics outside the timed region: one event pair per step
     n_diag = min(K, 64)
@@ -445,10 +489,12 @@ def main():
         "steps": K,
         "warmup": args.warmup,
         "ms_per_step": total_ms / K,
+        "runs": {"n": R, "steps_each": [bounds[j + 1] - bounds[j] for j in range(R)], "ms_per_step": run_ms,
+                 "median": float(np.median(run_ms)), "min": float(np.min(run_ms)), "max": float(np.max(run_ms))},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32 (S^T k, S^T q: binary16 hi+lo matrix-core operands, fp32 accumulation)",
         "data": "synthetic",
         "config": dict({"workload": case.workload,
                         "gate": "channel-wise d [B][Hv][d_k] (KDA)" if args.kda else "scalar alpha [B][Hv] (GDN)",
@@ -491,7 +537,8 @@ def main():
         rl.update({"bound": "alu", "achieved": valu["achieved"], "peak": valu["peak"], "unit": valu["unit"],
                    "frac": valu["frac"], "ops_per_element": valu["ops_per_element"],
                    "matrix_core_ops_per_element": valu["matrix_core_ops_per_element"], "hbm": hbm})
-    if args.copy_ref:
+    if not args.no_copy_ref:
+        # achievable-bandwidth references, outside the timed region
         src = torch.empty(launch_bytes // 2, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
         for _ in range(3):
@@ -502,7 +549,26 @@ def main():
             dst.copy_(src)
         c1.record(stream)
         torch.cuda.synchronize()
-        line["copy_ref_GBps"] = 2 * src.numel() * 20 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+        del src, dst
+        refs = {"device_copy_GBps": 2 * (launch_bytes // 2) * 20 / (c0.elapsed_time(c1) * 1e-3) / 1e9,
+                "device_copy": "torch copy of half the launch's state bytes (read + write = the launch's bytes)"}
+        n_ref = 64
+        for i in range(8):
+            case.ref(i)
+        c0.record(stream)
+        for i in range(n_ref):
+            case.ref(i)
+        c1.record(stream)
+        torch.cuda.synchronize()
+        ref_ms = c0.elapsed_time(c1) / n_ref
+        # the frozen step's bytes (codes read and written, scales read): the reference writes no scales
+        ref_bytes = w.batch * sum(state_bytes_per_tile(bits[h], w.d_k, w.d_v, False) for h in range(w.n_v_heads))
+        refs.update({"memory_only_us": ref_ms * 1e3, "memory_only_GBps": ref_bytes / (ref_ms * 1e-3) / 1e9,
+                     "memory_only": "stepq_decode_stream_ref: the frozen decode launch's tiles, workgroup order and "
+                                    "memory traffic (codes read and written back, scales and activations read, o "
+                                    "written) without arithmetic, over the same slot subsets",
+                     "kernel_over_memory_only": kern_ms / ref_ms})
+        line["bandwidth_refs"] = refs
     if not args.no_cpu_baseline:
         log(f"GPU timing done ({total_ms / K * 1e3:.1f} us per step); oracle baseline on the host")
         line["cpu_baseline"] = cpu_baseline(w, bits, args.cpu_seconds)

@@ -173,8 +173,11 @@ void stepq_pool_destroy(stepq_pool *pool);
 /* Raw pool memory (layout above), for saving, restoring or inspecting it. */
 void *stepq_pool_device_ptr(const stepq_pool *pool);
 
-/* Quantize and pack full-precision states into slots (the boundary pack after
- * prefill).  For i < n: slot slot_ids[i] receives
+/* Quantize and pack full-precision states into slots: the pack of the
+ * boundary states after prefill, which hands a request's state to the
+ * decode pool (Appendix F.1, the packed-state integration: prefill runs on
+ * full-precision states and packs the states at its boundary).  For i < n:
+ * slot slot_ids[i] receives
  *   q_hj = clip(round(state[i][h][j][:] / (r c nu)), -q_b, q_b)
  * with scales r (logical row order) and c stored alongside, nu the level
  * step of the row's width (1/q_b under N1, 2^(8-b) under N2).
@@ -190,7 +193,12 @@ stepq_status stepq_pool_load(stepq_pool *pool, const int32_t *slot_ids, int32_t 
  *   alpha[b][h], beta[b][h]
  * in act_dtype (arrays [batch][Hqk][d_k], [batch][Hv][d_v], [batch][Hv]),
  * writes o[b][h][:] (fp32, [batch][Hv][d_v]) and rewrites its codes in
- * place.  All arithmetic is fp32.  batch == 0 is a no-op. */
+ * place.  The arithmetic is fp32, except that in the compiled bodies of the
+ * uniform row-width mixes S^T k and S^T q run on the matrix cores: each
+ * row weight (k_i r_i / q_b, q_i r_i / q_b, scaled by a power of two per
+ * tile) is split into binary16 hi + lo parts (22 significant bits), the
+ * codes are exact in binary16, and the products accumulate in fp32.
+ * batch == 0 is a no-op. */
 stepq_status stepq_decode_step(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
                                const void *k, const void *v, const void *alpha, const void *beta,
                                stepq_dtype act_dtype, float *o, void *stream);
@@ -247,6 +255,19 @@ enum {
 stepq_status stepq_decode_step_ex(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
                                   const void *k, const void *v, const void *gate, const void *beta,
                                   stepq_dtype act_dtype, uint32_t flags, float *o, void *stream);
+
+/* Memory-only reference of stepq_decode_step, a measurement aid and not
+ * part of the method: one launch over the same tiles, in the same workgroup
+ * order (STEPQ_STEP_ADJACENT_SLOTS as in stepq_decode_step_ex, the only flag
+ * taken), moving the same memory traffic with no arithmetic.  Each tile's
+ * codes (and pivot rows) are read with the decode kernels' access pattern
+ * and written back unchanged, its scales are read, q, k, v, alpha and beta
+ * are read (alpha as [batch][Hv]) and o is filled with zeros.  Its duration
+ * is the achievable time of the step's memory pattern.  Arguments and errors
+ * as stepq_decode_step; the pool's contents do not change. */
+stepq_status stepq_decode_stream_ref(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
+                                     const void *k, const void *v, const void *alpha, const void *beta,
+                                     stepq_dtype act_dtype, uint32_t flags, float *o, void *stream);
 
 /* Row-impact factors w of every head (Section 4.3 and its footnote's
  * normalisation; calibrated as in Appendices A.3 and C.1), used by

@@ -391,6 +391,39 @@ stepq_status stepq_decode_step_kda(stepq_pool *p, const int32_t *slot_ids, int32
     return decode_step_impl(p, slot_ids, batch, q, k, v, gate, beta, act_dtype, o, stream, STEPQ_STEP_KDA_GATE);
 }
 
+stepq_status stepq_decode_stream_ref(stepq_pool *p, const int32_t *slot_ids, int32_t batch, const void *q,
+                                     const void *k, const void *v, const void *alpha, const void *beta,
+                                     stepq_dtype act_dtype, uint32_t flags, float *o, void *stream)
+{
+    stepq_status st = common_checks(p, slot_ids, batch);
+    if (st != STEPQ_OK) return st;
+    if (act_dtype != STEPQ_F32 && act_dtype != STEPQ_BF16) return fail(STEPQ_E_INVALID, "unknown activation dtype");
+    if (flags & ~static_cast<uint32_t>(STEPQ_STEP_ADJACENT_SLOTS))
+        return fail(STEPQ_E_INVALID, "the memory-only reference takes STEPQ_STEP_ADJACENT_SLOTS only");
+    if (batch == 0) return STEPQ_OK;
+    if (!q || !k || !v || !alpha || !beta || !o) return fail(STEPQ_E_INVALID, "NULL activation or output pointer");
+    auto s = static_cast<hipStream_t>(stream);
+    st = check_slots(p, slot_ids, batch, s);
+    if (st != STEPQ_OK) return st;
+    stepq::DecodeArgs a{};
+    a.pool = view(p);
+    a.slot_ids = slot_ids;
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.alpha = alpha;
+    a.beta = beta;
+    a.o = o;
+    a.batch = batch;
+    a.launch_order = (flags & STEPQ_STEP_ADJACENT_SLOTS) ? 1 : 0;
+    // one launch over every head, in the order of the combined decode launch
+    a.head_list = p->plan.order.empty() ? nullptr : p->d_head_order;
+    a.n_heads = p->Hv;
+    a.div_heads = fast_div(static_cast<uint32_t>(p->Hv));
+    const hipError_t e = stepq::launch_stream_ref(a, act_dtype == STEPQ_BF16, s);
+    return e == hipSuccess ? STEPQ_OK : hip_fail(e, "reference launch");
+}
+
 static stepq_status tile_op(const stepq_pool *p, const int32_t *ids, int32_t n, stepq::TileArgs &a,
                             stepq::TileOp op, void *stream)
 {

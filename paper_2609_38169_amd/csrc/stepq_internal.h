@@ -84,6 +84,9 @@ hipError_t launch_decode_refit(const DecodeArgs &a, bool bf16, bool diag, int po
 // The decode step with the single-axis baseline's requantization: row
 // factors r'_i = max_j |X_ij|, column factors 1.
 hipError_t launch_decode_rowmax(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);
+// Memory-only reference of a decode launch: the same tiles, order and
+// memory traffic (codes rewritten unchanged, o zeroed), no arithmetic.
+hipError_t launch_stream_ref(const DecodeArgs &a, bool bf16, hipStream_t stream);
 hipError_t launch_tile_op(const TileArgs &a, TileOp op, hipStream_t stream);
 
 }  // namespace stepq

@@ -542,6 +542,46 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 }
 
 // ---------------------------------------------------------------------------
+// Memory-only reference of the decode step (a measurement aid, not part of
+// the method): the same tiles in the same workgroup order (tile_of), each
+// thread reading the same code words with the same policy (non-temporal
+// loads, all issued before any store) and writing them back unchanged
+// (sc1 nt stores), the scales read once, the activations read and o
+// written; no arithmetic.  `zero` is 0 at run time: the XOR keeps the
+// compiler from dropping a store of a value just loaded from the same
+// address, and o receives zeros.
+template <bool BF16>
+__global__ __launch_bounds__(256) void stream_ref_kernel(DecodeArgs a, uint32_t zero)
+{
+    const PoolView &P = a.pool;
+    TileCtx t;
+    tile_of(a, 0u, t);
+    const HeadInfo hi = P.heads[t.h];
+    const int slot = a.slot_ids[t.b];
+    uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + hi.tile_off;
+    const int tid = threadIdx.x;
+    // codes and pivot rows: everything before r
+    const CodeWords cw(rec, hi.r_off);
+    const int nw = static_cast<int>(hi.r_off / 4);
+    constexpr int kMaxWords = 32;          // a whole FP16 head: 32 KiB = 32 words per thread
+    uint32_t w[kMaxWords];
+#pragma unroll
+    for (int m = 0; m < kMaxWords; ++m) w[m] = 256 * m < nw ? cw.load(tid + 256 * m) : 0u;
+    const float *rr = reinterpret_cast<const float *>(rec + hi.r_off);
+    float acc = 0.f;
+    if (tid < P.dk) {
+        acc += rr[tid];
+        const size_t off = (static_cast<size_t>(t.b) * P.Hqk + t.hq) * P.dk + tid;
+        acc += act_ld<BF16>(a.k, off) + act_ld<BF16>(a.q, off);
+    }
+    if (tid < P.dv) acc += rr[P.dk + tid] + act_ld<BF16>(a.v, static_cast<size_t>(t.tile) * P.dv + tid);
+    acc += act_ld<BF16>(a.alpha, t.tile) + act_ld<BF16>(a.beta, t.tile);
+#pragma unroll
+    for (int m = 0; m < kMaxWords; ++m)
+        if (256 * m < nw) cw.store(tid + 256 * m, w[m] ^ zero);
+    if (tid < P.dv) a.o[static_cast<size_t>(t.tile) * P.dv + tid] = acc * __uint_as_float(zero);
+}
+
 template <TileOp OP>
 __global__ __launch_bounds__(256) void tile_kernel(TileArgs a)
 {
@@ -729,6 +769,15 @@ hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_lay
                           : launch_decode_any<true, false>(a, pool_layout, grid, stream);
     return diag ? launch_decode_any<false, true>(a, pool_layout, grid, stream)
                 : launch_decode_any<false, false>(a, pool_layout, grid, stream);
+}
+
+hipError_t launch_stream_ref(const DecodeArgs &a, bool bf16, hipStream_t stream)
+{
+    const unsigned grid = static_cast<unsigned>(a.batch) * static_cast<unsigned>(a.n_heads);
+    if (grid == 0) return hipSuccess;
+    if (bf16) hipLaunchKernelGGL(stream_ref_kernel<true>, dim3(grid), dim3(256), 0, stream, a, 0u);
+    else hipLaunchKernelGGL(stream_ref_kernel<false>, dim3(grid), dim3(256), 0, stream, a, 0u);
+    return hipGetLastError();
 }
 
 hipError_t launch_tile_op(const TileArgs &a, TileOp op, hipStream_t stream)

@@ -27,6 +27,7 @@ _STATUS = {0: "STEPQ_OK", 1: "STEPQ_E_INVALID", 2: "STEPQ_E_UNSUPPORTED", 3: "ST
 EXPORTED = (
     "stepq_pool_bytes", "stepq_pool_plan", "stepq_pool_create", "stepq_pool_destroy", "stepq_pool_device_ptr",
     "stepq_pool_load", "stepq_decode_step", "stepq_decode_step_kda", "stepq_decode_step_ex",
+    "stepq_decode_stream_ref",
     "stepq_pool_set_row_weight", "stepq_pool_dequant", "stepq_pool_export", "stepq_pool_import",
     "stepq_pool_export_pivots", "stepq_pool_import_pivots", "stepq_last_error", "stepq_setup_fit",
     "stepq_setup_fit_ex", "stepq_setup_fit_levels", "stepq_setup_lifetime_bits", "stepq_setup_row_impact", "stepq_setup_distortion",
@@ -72,6 +73,7 @@ def lib():
             "stepq_decode_step": ([P, P, i32, P, P, P, P, P, st, P, P], st),
             "stepq_decode_step_kda": ([P, P, i32, P, P, P, P, P, st, P, P], st),
             "stepq_decode_step_ex": ([P, P, i32, P, P, P, P, P, st, ctypes.c_uint32, P, P], st),
+            "stepq_decode_stream_ref": ([P, P, i32, P, P, P, P, P, st, ctypes.c_uint32, P, P], st),
             "stepq_pool_set_row_weight": ([P, P], st),
             "stepq_pool_dequant": ([P, P, i32, P, P], st),
             "stepq_pool_export": ([P, P, i32, P, P, P, P], st),
@@ -227,6 +229,23 @@ class Pool:
             args = args[:9] + (flags,) + args[9:]
         else:
             fn = lib().stepq_decode_step_kda if kda else lib().stepq_decode_step
+
+        def launch():
+            _ = keep
+            st = fn(*args)
+            if st != 0:
+                _check(st)
+        return launch
+
+    def prepare_stream_ref(self, slot_ids, q, k, v, alpha, beta, o, stream=None, adjacent=False):
+        """prepare_step for the memory-only reference of a decode step
+        (stepq_decode_stream_ref): same tiles, order and traffic, no
+        arithmetic; o receives zeros."""
+        args = _step_args(self, slot_ids, q, k, v, alpha, beta, o, stream, False)
+        keep = (slot_ids, q, k, v, alpha, beta, o)
+        flags = ctypes.c_uint32(STEPQ_STEP_ADJACENT_SLOTS if adjacent else 0)
+        args = args[:9] + (flags,) + args[9:]
+        fn = lib().stepq_decode_stream_ref
 
         def launch():
             _ = keep

@@ -181,3 +181,27 @@ def test_adjacent_slots_hint_changes_nothing(idx, refit):
         assert torch.equal(a.view(torch.uint8) if a.dtype == torch.int8 else a.view(torch.int32),
                            b.view(torch.uint8) if b.dtype == torch.int8 else b.view(torch.int32))
     _say(f"adjacent hint {w.name}: bit-identical")
+
+
+def test_stream_ref_moves_memory_only():
+    """The memory-only reference of a decode launch (a measurement aid)
+    leaves every byte of the pool as it was and writes zeros to o, on a
+    uniform pool (pool_b512) and on a pool with a head list (layer_b64's
+    two layout classes); it takes the adjacent-slots hint only."""
+    import ctypes
+    from paper_2609_38169_amd import stepq
+    from paper_2609_38169_amd.pools import build_pool, row_bits
+    for idx in (2, 1):
+        w = W.workload(idx)
+        pool = build_pool(w, device=DEV, bits=row_bits(w))
+        before = pool.memory.clone()
+        ids = W.active_slots(w).to(DEV)
+        inp = W.step_inputs(w, 0, 0, device=DEV)
+        o = torch.full((w.batch, w.n_v_heads, w.d_v), 7.0, dtype=torch.float32, device=DEV)
+        pool.prepare_stream_ref(ids, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o)()
+        torch.cuda.synchronize()
+        assert torch.equal(before, pool.memory), w.name
+        assert torch.count_nonzero(o).item() == 0, w.name
+    a = stepq._step_args(pool, ids, inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], o, None, False)
+    with pytest.raises(stepq.StepqError):
+        stepq._check(stepq.lib().stepq_decode_stream_ref(*a[:9], ctypes.c_uint32(stepq.STEPQ_STEP_REFIT), *a[9:]))
