@@ -221,8 +221,9 @@ def pool_case(args, w, mode, dev):
     if row_weight is not None:
         pool.set_row_weight(row_weight)
     subsets = [s.to(dev) for s in (W.rotation_slots(w)[:1] if args.resident else W.rotation_slots(w))]
-    if args.sorted_batch:
-        # the same requests, listed in slot order (a caller-side choice: any batch order is valid)
+    if args.batch_order == "slot":
+        # the same requests, listed in slot order: a request keeps its slot from step to step, so a
+        # caller orders its batch once per change of composition; any order gives identical results
         subsets = [torch.sort(s).values for s in subsets]
     adjacent = [adjacent_ids(s) for s in subsets]
     n_inp = min(w.steps, args.steps + args.warmup)
@@ -271,7 +272,8 @@ def pool_case(args, w, mode, dev):
                 workload=f"{w.name}: {w.n_slots}-slot pool, B={w.batch} active, {w.n_v_heads} heads, "
                          f"d_k=d_v={w.d_k}, {mix}, fp32 scales, bf16 activations",
                 extra={"slot_rotation": len(subsets), "cache_resident": bool(args.resident),
-                       "batch_order": "slot order" if args.sorted_batch else "as drawn",
+                       "batch_order": ("slot order (the drawn requests, listed by slot id)"
+                                       if args.batch_order == "slot" else "as drawn"),
                        "adjacent_slots_hint": bool(all(adjacent))},
                 pool_bytes=pool.pool_bytes)
 
@@ -351,8 +353,10 @@ def main():
     ap.add_argument("--calibrated", choices=["row", "head"], default=None,
                     help="pool workloads: the precision map from the calibration side of the setup step "
                          "(row units with 24 FP16 pivot rows, or head units with one FP16 head)")
-    ap.add_argument("--sorted-batch", action="store_true",
-                    help="list each step's active requests in slot order (pool workloads; default: as drawn)")
+    ap.add_argument("--batch-order", choices=["slot", "drawn"], default="slot",
+                    help="pool workloads: list each step's active requests in slot order (default; a caller-side "
+                         "choice, made once per batch composition: any order gives the same results), or in the "
+                         "order they were drawn")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--runs", type=int, default=3,

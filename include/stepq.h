@@ -385,6 +385,26 @@ stepq_status stepq_setup_distortion(int64_t C, int32_t H, int32_t d_k, int32_t d
  * from the mean log retention ell_u (Appendix A.3). */
 stepq_status stepq_setup_lifetime_weights(int32_t U, const double *ell, int32_t horizon, double *L);
 
+/* Mean log retention per unit, ell_u (Appendix A.3): the mean over the T
+ * calibration samples of log g, g the gate that decays the unit's entries
+ * (its own channel d_i under a channel-wise gate, gate_per_row 1, gate
+ * [T][H][d_k]; its head's alpha otherwise, gate [T][H]).  unit 0 (key rows):
+ * ell [H * d_k]; unit 1 (heads): ell [H], the mean over the head's rows.
+ * Gates must be finite and > 0 (STEPQ_E_INVALID otherwise). */
+stepq_status stepq_setup_mean_log_retention(int64_t T, int32_t H, int32_t d_k, const float *gate, int32_t gate_per_row,
+                                            int32_t unit, double *ell);
+
+/* The terms of Eq. 6's objective: cost[u][c] = L_u d_u(b_c) for the first
+ * n_cand candidates of each row of d [U][d_stride] (d_stride >= n_cand). */
+stepq_status stepq_setup_lifetime_costs(int32_t U, int32_t n_cand, const double *L, const double *d, int32_t d_stride,
+                                        double *cost);
+
+/* The pivot risk of Appendix C.2, the lifetime-weighted distortion an FP16
+ * unit removes: risk_u = L_u (d_u(b_int) - d_u(16)), with b_int and 16 in
+ * columns col_int and col_f16 of d [U][d_stride]. */
+stepq_status stepq_setup_pivot_risk(int32_t U, const double *L, const double *d, int32_t d_stride, int32_t col_int,
+                                    int32_t col_f16, double *risk);
+
 /* Bit allocation (Eq. 6): choose choice[u] in [0, n_cand) minimising
  * sum_u cost[u][choice[u]] (cost = L_u d_u(b), [U][n_cand]) subject to
  * sum_u n_u b_u <= budget * sum_u n_u.

@@ -84,6 +84,25 @@ def calib_distortion(states, cand_bits, unit: str, w=None, pivots=None):
     raise ValueError(unit)
 
 
+def mean_log_retention_units(gates, d_k: int, unit: str):
+    """l_u (Appendix A.3): mean over calibration samples of the log of the
+    gate that decays the unit, gates [T][H] (head gate) or [T][H][d_k]
+    (channel gate); key-row units [H*d_k] or head units [H] (the mean over
+    the head's rows).  Plain loops."""
+    g = np.asarray(gates, np.float64)
+    T, H = g.shape[:2]
+    rows = np.zeros((H, d_k))
+    for h in range(H):
+        for i in range(d_k):
+            s = 0.0
+            for t in range(T):
+                s += math.log(g[t, h, i] if g.ndim == 3 else g[t, h])
+            rows[h, i] = s / T
+    if unit == "row":
+        return rows.reshape(-1)
+    return np.array([sum(rows[h]) / d_k for h in range(H)])
+
+
 def lifetime_weights(ell, horizon: int):
     """L_u = sum_{j=0}^{H-1} exp(2 j l_u) (Section 3.2)."""
     return np.array([sum(math.exp(2.0 * j * e) for j in range(horizon)) for e in np.asarray(ell, np.float64)])

@@ -1,7 +1,8 @@
 """Calibration pipeline of the setup step, on libstepq's host functions:
 row-impact factors -> candidate distortions with the dual-axis codec ->
 lifetime weights -> FP16 pivots -> bit allocation (Section 3.2, Section 4.3,
-Appendices A.3, C.1, C.2).  Produces the precision map (widths 2/4/8, 16 for
+Appendices A.3, C.1, C.2).  Argument marshalling only: every step's
+arithmetic is a libstepq call.  Produces the precision map (widths 2/4/8, 16 for
 pivots) and the row-impact factors a pool is created and refit with."""
 from __future__ import annotations
 
@@ -31,14 +32,9 @@ def calibrate(q, k, beta, gates, states, budget: float, cand_bits=(2, 4, 8), uni
     the n_pivots units of largest L_u (d_u(b_max) - d_u(16)), chosen first;
     the remaining units are allocated under the budget (pivot bits are
     accounted separately, Table C1)."""
-    g = np.asarray(gates, np.float64)
     C, H, dk, dv = np.asarray(states).shape
     w, _ = stepq.stepq_setup_row_impact(q, k, beta, gates, gamma)
-    # mean log retention per unit (Appendix A.3): rows see their own gate
-    # (KDA) or their head's (GDN); heads average over their rows' gates
-    logg = np.log(g)
-    ell_rows = logg.mean(axis=0) if g.ndim == 3 else np.repeat(logg.mean(axis=0)[:, None], dk, axis=1)
-    ell = ell_rows.reshape(-1) if unit == "row" else ell_rows.mean(axis=1)
+    ell = stepq.stepq_setup_mean_log_retention(gates, dk, unit)
     L = stepq.stepq_setup_lifetime_weights(ell, horizon)
     cands = list(cand_bits) + ([16] if n_pivots > 0 else [])
     d = stepq.stepq_setup_distortion(states, cands, unit, row_weight=w, n_threads=n_threads)
@@ -46,7 +42,7 @@ def calibrate(q, k, beta, gates, states, budget: float, cand_bits=(2, 4, 8), uni
     piv = np.zeros(U, bool)
     if n_pivots > 0:
         ib = int(np.argmax(cand_bits))
-        piv = stepq.stepq_setup_select_pivots(L * (d[:, ib] - d[:, -1]), n_pivots)
+        piv = stepq.stepq_setup_select_pivots(stepq.stepq_setup_pivot_risk(L, d, ib, d.shape[1] - 1), n_pivots)
         # with the pivots fixed, the integer candidates are calibrated again
         # without them in the shared column fit
         pmask = piv.reshape(H, dk) if unit == "row" else np.repeat(piv[:, None], dk, axis=1)
@@ -57,7 +53,8 @@ def calibrate(q, k, beta, gates, states, budget: float, cand_bits=(2, 4, 8), uni
     idx = np.nonzero(~piv)[0]
     n_u = np.full(len(idx), dv if unit == "row" else dk * dv, np.int32)
     m = method or ("lagrangian" if unit == "row" else "dp")
-    choice = stepq.stepq_setup_allocate((L[:, None] * d_int)[idx], n_u, cand_bits, budget, m)
+    cost = stepq.stepq_setup_lifetime_costs(L, d_int, len(cand_bits))
+    choice = stepq.stepq_setup_allocate(cost[idx], n_u, cand_bits, budget, m)
     widths = np.full(U, 16, np.uint8)
     widths[idx] = np.asarray(cand_bits, np.uint8)[choice]
     bits = widths.reshape(H, dk) if unit == "row" else np.repeat(widths[:, None], dk, axis=1)

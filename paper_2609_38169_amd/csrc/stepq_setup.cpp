@@ -343,6 +343,58 @@ stepq_status stepq_setup_lifetime_weights(int32_t U, const double *ell, int32_t 
     return STEPQ_OK;
 }
 
+stepq_status stepq_setup_mean_log_retention(int64_t T, int32_t H, int32_t d_k, const float *gate, int32_t gate_per_row,
+                                            int32_t unit, double *ell)
+{
+    if (T < 1 || H < 1 || d_k < 1 || !gate || !ell || (gate_per_row != 0 && gate_per_row != 1) ||
+        (unit != 0 && unit != 1))
+        return STEPQ_E_INVALID;
+    const int64_t per_t = gate_per_row ? static_cast<int64_t>(H) * d_k : H;
+    for (int64_t e = 0; e < T * per_t; ++e)
+        if (!(gate[e] > 0.0f) || !std::isfinite(gate[e])) return STEPQ_E_INVALID;
+    // per key row: the mean over samples of log of the row's gate (its own
+    // channel under a channel-wise gate, its head's otherwise)
+    std::vector<double> rows(static_cast<size_t>(H) * d_k, 0.0);
+    for (int32_t h = 0; h < H; ++h)
+        for (int32_t i = 0; i < d_k; ++i) {
+            double s = 0.0;
+            for (int64_t t = 0; t < T; ++t)
+                s += std::log(static_cast<double>(gate_per_row ? gate[(t * H + h) * d_k + i] : gate[t * H + h]));
+            rows[static_cast<size_t>(h) * d_k + i] = s / static_cast<double>(T);
+        }
+    if (unit == 0) {
+        std::copy(rows.begin(), rows.end(), ell);
+    } else {
+        // a head unit: the mean over its rows
+        for (int32_t h = 0; h < H; ++h) {
+            double s = 0.0;
+            for (int32_t i = 0; i < d_k; ++i) s += rows[static_cast<size_t>(h) * d_k + i];
+            ell[h] = s / static_cast<double>(d_k);
+        }
+    }
+    return STEPQ_OK;
+}
+
+stepq_status stepq_setup_lifetime_costs(int32_t U, int32_t n_cand, const double *L, const double *d, int32_t d_stride,
+                                        double *cost)
+{
+    if (U < 1 || n_cand < 1 || d_stride < n_cand || !L || !d || !cost) return STEPQ_E_INVALID;
+    for (int32_t u = 0; u < U; ++u)
+        for (int32_t c = 0; c < n_cand; ++c)
+            cost[static_cast<size_t>(u) * n_cand + c] = L[u] * d[static_cast<size_t>(u) * d_stride + c];
+    return STEPQ_OK;
+}
+
+stepq_status stepq_setup_pivot_risk(int32_t U, const double *L, const double *d, int32_t d_stride, int32_t col_int,
+                                    int32_t col_f16, double *risk)
+{
+    if (U < 1 || !L || !d || !risk || col_int < 0 || col_f16 < 0 || col_int >= d_stride || col_f16 >= d_stride)
+        return STEPQ_E_INVALID;
+    for (int32_t u = 0; u < U; ++u)
+        risk[u] = L[u] * (d[static_cast<size_t>(u) * d_stride + col_int] - d[static_cast<size_t>(u) * d_stride + col_f16]);
+    return STEPQ_OK;
+}
+
 stepq_status stepq_setup_select_pivots(int32_t U, const double *risk, int32_t count, uint8_t *is_pivot)
 {
     if (U < 1 || !risk || !is_pivot || count < 0 || count > U) return STEPQ_E_INVALID;

@@ -32,6 +32,7 @@ EXPORTED = (
     "stepq_pool_export_pivots", "stepq_pool_import_pivots", "stepq_last_error", "stepq_setup_fit",
     "stepq_setup_fit_ex", "stepq_setup_fit_levels", "stepq_setup_lifetime_bits", "stepq_setup_row_impact", "stepq_setup_distortion",
     "stepq_setup_lifetime_weights", "stepq_setup_allocate", "stepq_setup_select_pivots",
+    "stepq_setup_mean_log_retention", "stepq_setup_lifetime_costs", "stepq_setup_pivot_risk",
 )
 
 
@@ -85,6 +86,9 @@ def lib():
             "stepq_setup_row_impact": ([i64, i32, i32, P, P, P, P, i32, ctypes.c_double, P, P], st),
             "stepq_setup_distortion": ([i64, i32, i32, i32, P, P, P, i32, P, i32, P, i32], st),
             "stepq_setup_lifetime_weights": ([i32, P, i32, P], st),
+            "stepq_setup_mean_log_retention": ([i64, i32, i32, P, i32, i32, P], st),
+            "stepq_setup_lifetime_costs": ([i32, i32, P, P, i32, P], st),
+            "stepq_setup_pivot_risk": ([i32, P, P, i32, i32, i32, P], st),
             "stepq_setup_allocate": ([i32, i32, P, P, P, ctypes.c_double, i32, P], st),
             "stepq_setup_select_pivots": ([i32, P, i32, P], st),
             "stepq_last_error": ([], ctypes.c_char_p),
@@ -491,6 +495,39 @@ def stepq_setup_lifetime_weights(ell, horizon: int):
     e = _host(ell, np.float64)
     out = np.empty(e.shape, np.float64)
     _setup_check(lib().stepq_setup_lifetime_weights(e.size, _vp(e), horizon, _vp(out)), "lifetime weights")
+    return out
+
+
+def stepq_setup_mean_log_retention(gates, d_k: int, unit: str):
+    """ell per unit (Appendix A.3) from calibration gates [T][H] (scalar,
+    GDN) or [T][H][d_k] (channel-wise, KDA): [H * d_k] for unit "row",
+    [H] for unit "head"."""
+    g = _host(gates, np.float32)
+    if g.ndim not in (2, 3) or (g.ndim == 3 and g.shape[2] != d_k):
+        raise ValueError("gates must be [T][H] or [T][H][d_k]")
+    T, H = g.shape[:2]
+    u = {"row": 0, "head": 1}[unit]
+    out = np.empty(H * d_k if u == 0 else H, np.float64)
+    _setup_check(lib().stepq_setup_mean_log_retention(T, H, d_k, _vp(g), int(g.ndim == 3), u, _vp(out)),
+                 "mean log retention")
+    return out
+
+
+def stepq_setup_lifetime_costs(L, d, n_cand: int):
+    """cost [U][n_cand] = L_u d_u(b) over the first n_cand columns of d [U][*]."""
+    Lh, dh = _host(L, np.float64), _host(d, np.float64)
+    U, stride = dh.shape
+    out = np.empty((U, n_cand), np.float64)
+    _setup_check(lib().stepq_setup_lifetime_costs(U, n_cand, _vp(Lh), _vp(dh), stride, _vp(out)), "lifetime costs")
+    return out
+
+
+def stepq_setup_pivot_risk(L, d, col_int: int, col_f16: int):
+    """risk_u = L_u (d_u[col_int] - d_u[col_f16]) for d [U][*]."""
+    Lh, dh = _host(L, np.float64), _host(d, np.float64)
+    U, stride = dh.shape
+    out = np.empty(U, np.float64)
+    _setup_check(lib().stepq_setup_pivot_risk(U, _vp(Lh), _vp(dh), stride, col_int, col_f16, _vp(out)), "pivot risk")
     return out
 
 

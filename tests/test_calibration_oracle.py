@@ -157,3 +157,22 @@ def test_pivot_choice_is_top_risk():
     risk[[3, 9]] = risk[4]                        # ties go to the lower index
     m = CAL.select_pivots(risk, 7)
     assert m.sum() == 7 and np.min(risk[m]) >= np.max(risk[~m])
+
+
+def test_mean_log_retention_units_closed_forms():
+    """l_u (Appendix A.3) of the oracle: gates a^t over T samples give
+    log(a) (T - 1) / 2 for every unit; a scalar gate gives each of its
+    head's rows the head's value; a head's value is the mean of its rows'."""
+    import math
+    import oracle.calibration as CAL
+    T, H, dk = 6, 2, 5
+    a = np.array([0.9, 0.5])
+    g = np.stack([a ** t for t in range(T)])                     # [T][H]
+    rows = CAL.mean_log_retention_units(g, dk, "row").reshape(H, dk)
+    np.testing.assert_allclose(rows, np.log(a)[:, None] * (T - 1) / 2 * np.ones((1, dk)), rtol=1e-13)
+    np.testing.assert_allclose(CAL.mean_log_retention_units(g, dk, "head"), np.log(a) * (T - 1) / 2, rtol=1e-13)
+    rng = np.random.default_rng(3)
+    gk = rng.uniform(0.2, 1.0, (T, H, dk))
+    r = CAL.mean_log_retention_units(gk, dk, "row").reshape(H, dk)
+    assert math.isclose(r[1, 3], sum(math.log(gk[t, 1, 3]) for t in range(T)) / T, rel_tol=1e-13)
+    np.testing.assert_allclose(CAL.mean_log_retention_units(gk, dk, "head"), r.mean(axis=1), rtol=1e-13)

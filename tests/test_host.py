@@ -263,6 +263,28 @@ def test_lifetime_weights_and_pivots_match_oracle():
     assert np.array_equal(stepq.stepq_setup_select_pivots(risk, 5), CAL.select_pivots(risk, 5))
 
 
+@pytest.mark.parametrize("kda", [False, True])
+def test_mean_log_retention_and_costs_match_oracle(kda):
+    """ell per key row and per head, the lifetime-weighted costs and the
+    pivot risk from libstepq against the oracle's loops; constant gates give
+    log g exactly (Appendix A.3)."""
+    import oracle.calibration as CAL
+    rng = np.random.default_rng(14)
+    T, H, dk = 9, 3, 7
+    g = rng.uniform(0.5, 1.0, (T, H, dk) if kda else (T, H)).astype(np.float32)
+    for unit in ("row", "head"):
+        np.testing.assert_allclose(stepq.stepq_setup_mean_log_retention(g, dk, unit),
+                                   CAL.mean_log_retention_units(g, dk, unit), rtol=1e-12, atol=1e-15)
+    const = np.full(g.shape, 0.75, np.float32)
+    np.testing.assert_allclose(stepq.stepq_setup_mean_log_retention(const, dk, "head"), np.log(0.75), rtol=1e-12)
+    L = rng.uniform(1, 50, H * dk)
+    d = rng.uniform(0, 1, (H * dk, 4))
+    np.testing.assert_allclose(stepq.stepq_setup_lifetime_costs(L, d, 3), L[:, None] * d[:, :3], rtol=1e-15)
+    np.testing.assert_allclose(stepq.stepq_setup_pivot_risk(L, d, 2, 3), L * (d[:, 2] - d[:, 3]), rtol=1e-15)
+    with pytest.raises(stepq.StepqError):
+        stepq.stepq_setup_mean_log_retention(np.zeros((2, H), np.float32), dk, "row")
+
+
 def test_allocators_match_oracle():
     import oracle.calibration as CAL
     rng = np.random.default_rng(13)
