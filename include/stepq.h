@@ -272,9 +272,12 @@ stepq_status stepq_decode_stream_ref(stepq_pool *pool, const int32_t *slot_ids, 
 /* Row-impact factors w of every head (Section 4.3 and its footnote's
  * normalisation; calibrated as in Appendices A.3 and C.1), used by
  * STEPQ_STEP_REFIT.  row_weight: host [Hv][d_k] in logical row order, each
- * finite and > 0; copied.  Synchronises the pool's device first, so no
- * decode step is in flight while the table changes.  A new pool has w = 1. */
-stepq_status stepq_pool_set_row_weight(stepq_pool *pool, const float *row_weight);
+ * finite and > 0; copied.  The upload is ordered on `stream` after the
+ * steps already enqueued there and before later ones, and the call returns
+ * once it is done (it waits for that stream only).  Steps on other streams
+ * must not be in flight on this pool.  The pool must be on the current
+ * device.  A new pool has w = 1. */
+stepq_status stepq_pool_set_row_weight(stepq_pool *pool, const float *row_weight, void *stream);
 
 /* Reconstruct S^_ij = r_i c_j z_ij (Section 4.3; z the level of the code in
  * the pool's normalisation, q / q_b under N1; pivot rows: their binary16

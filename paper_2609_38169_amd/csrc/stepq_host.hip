@@ -282,7 +282,7 @@ void stepq_pool_destroy(stepq_pool *p)
 
 void *stepq_pool_device_ptr(const stepq_pool *p) { return p ? p->mem : nullptr; }
 
-stepq_status stepq_pool_set_row_weight(stepq_pool *p, const float *row_weight)
+stepq_status stepq_pool_set_row_weight(stepq_pool *p, const float *row_weight, void *stream)
 {
     if (!p || !row_weight) return fail(STEPQ_E_INVALID, "NULL pool or row_weight");
     std::vector<float> phys(p->perm.size());
@@ -293,12 +293,13 @@ stepq_status stepq_pool_set_row_weight(stepq_pool *p, const float *row_weight)
             if (!(wv > 0.0f) || !std::isfinite(wv)) return fail(STEPQ_E_INVALID, "row weights must be finite and > 0");
             phys[pi] = wv;
         }
-    int cur = 0;
-    hipError_t e = hipGetDevice(&cur);
-    if (e == hipSuccess && cur != p->device) e = hipSetDevice(p->device);
-    if (e == hipSuccess) e = hipDeviceSynchronize();
-    if (e == hipSuccess) e = hipMemcpy(p->d_roww, phys.data(), sizeof(float) * phys.size(), hipMemcpyHostToDevice);
-    if (cur != p->device) (void)hipSetDevice(cur);
+    stepq_status st = check_device(p);
+    if (st != STEPQ_OK) return st;
+    // in stream order: after the steps already enqueued on the stream, before
+    // later ones; the host waits for this stream only (phys must outlive the copy)
+    auto s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(p->d_roww, phys.data(), sizeof(float) * phys.size(), hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
     return e == hipSuccess ? STEPQ_OK : hip_fail(e, "row weight upload");
 }
 

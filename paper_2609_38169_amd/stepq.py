@@ -75,7 +75,7 @@ def lib():
             "stepq_decode_step_kda": ([P, P, i32, P, P, P, P, P, st, P, P], st),
             "stepq_decode_step_ex": ([P, P, i32, P, P, P, P, P, st, ctypes.c_uint32, P, P], st),
             "stepq_decode_stream_ref": ([P, P, i32, P, P, P, P, P, st, ctypes.c_uint32, P, P], st),
-            "stepq_pool_set_row_weight": ([P, P], st),
+            "stepq_pool_set_row_weight": ([P, P, P], st),
             "stepq_pool_dequant": ([P, P, i32, P, P], st),
             "stepq_pool_export": ([P, P, i32, P, P, P, P], st),
             "stepq_pool_import": ([P, P, i32, P, P, P, P], st),
@@ -214,8 +214,8 @@ class Pool:
         else:
             stepq_decode_step_kda(self, slot_ids, q, k, v, gate, beta, o, stream)
 
-    def set_row_weight(self, w):
-        stepq_pool_set_row_weight(self, w)
+    def set_row_weight(self, w, stream=None):
+        stepq_pool_set_row_weight(self, w, stream)
 
     def prepare_step(self, slot_ids, q, k, v, alpha, beta, o, stream=None, refit=False, adjacent=False):
         """Validate the arguments of one decode step once and return a
@@ -345,13 +345,14 @@ def stepq_decode_step_ex(pool: Pool, slot_ids, q, k, v, gate, beta, o, flags: in
     _check(lib().stepq_decode_step_ex(*a[:9], ctypes.c_uint32(flags), *a[9:]))
 
 
-def stepq_pool_set_row_weight(pool: Pool, w):
-    """w: [Hv][d_k] row-impact factors (host array or tensor), logical row order."""
+def stepq_pool_set_row_weight(pool: Pool, w, stream=None):
+    """w: [Hv][d_k] row-impact factors (host array or tensor), logical row
+    order; uploaded in order on the stream (torch's current one by default)."""
     wt = np.ascontiguousarray(w.cpu().numpy() if isinstance(w, torch.Tensor) else w, dtype=np.float32)
     if wt.shape != (pool.Hv, pool.dk):
         raise ValueError(f"row weights have shape {wt.shape}, expected {(pool.Hv, pool.dk)}")
     with torch.cuda.device(pool.device):
-        _check(lib().stepq_pool_set_row_weight(pool.handle, wt.ctypes.data_as(ctypes.c_void_p)))
+        _check(lib().stepq_pool_set_row_weight(pool.handle, wt.ctypes.data_as(ctypes.c_void_p), _stream(stream)))
 
 
 def stepq_pool_dequant(pool: Pool, slot_ids, out, stream=None):

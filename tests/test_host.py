@@ -171,6 +171,51 @@ def test_setup_fit_matches_oracle(idx):
         stepq.stepq_pool_bytes(2, 4, 4, 16, 64, np.full((4, 16), 8, np.uint8), levels=7)
 
 
+@pytest.mark.parametrize("levels", [0, 1])
+def test_setup_fit_meets_its_definition(levels):
+    """The library's setup fit against Section 4.3's definitions directly,
+    not through the oracle: r_i is the fp32 rounding of (m_i / w_i)^(1/2),
+    m_i = mean_j |S_ij|; every integer entry lies within its row and column
+    factors, r_i c_j top_i >= |S_ij| (top_i = 1 under N1, 2^(8-b) q_b under
+    N2); each column's factor is the smallest fp32 value with that property
+    (the column's largest entry reaches the top level); pivot rows take no
+    part in the column factors; all-zero rows and columns get the floor
+    2^-60."""
+    rng = np.random.default_rng(31)
+    n, dk, dv = 6, 40, 64
+    S = (rng.standard_normal((n, dk, dv)) * np.exp(rng.standard_normal((n, dk, 1)))).astype(np.float32)
+    S[1, 3, :] = 0.0                      # a zero row
+    S[2, :, 5] = 0.0                      # a zero column
+    wts = np.exp(0.5 * rng.standard_normal((n, dk))).astype(np.float32)
+    bits = rng.choice([2, 4, 8, 16], size=(n, dk), p=[0.3, 0.3, 0.3, 0.1]).astype(np.uint8)
+    bits[2, :] = np.where(bits[2, :] == 16, 8, bits[2, :])
+    r, c = stepq.stepq_setup_fit(S, wts, row_bits=bits, levels=levels)
+    floor = 2.0 ** -60
+    m = np.abs(S.astype(np.float64)).mean(axis=2)
+    r_def = np.maximum(np.sqrt(m / wts.astype(np.float64)), floor)
+    assert np.all(np.abs(r.astype(np.float64) - r_def) <= np.spacing(r_def.astype(np.float32)).astype(np.float64)), \
+        "r is not the fp32 rounding of (m / w)^(1/2)"
+    assert r[1, 3] == np.float32(floor)
+    b = bits.astype(np.int64)
+    qb = 2.0 ** (b - 1) - 1
+    top = qb * 2.0 ** (8 - b) if levels else np.ones_like(qb)
+    ints = (bits != 16)[:, :, None]
+    bound = r.astype(np.float64)[:, :, None] * c.astype(np.float64)[:, None, :] * top[:, :, None]
+    assert np.all(np.where(ints, bound >= np.abs(S.astype(np.float64)), True)), "an entry exceeds r c top"
+    need = np.where(ints, np.abs(S.astype(np.float64)) / (r.astype(np.float64) * top)[:, :, None], 0.0).max(axis=1)
+    need = np.maximum(need, floor)
+    c64 = c.astype(np.float64)
+    assert np.all(c64 >= need)
+    below = np.nextafter(c, np.float32(0)).astype(np.float64)
+    assert np.all((below < need) | (c == np.float32(floor))), "a column factor is larger than it needs to be"
+    assert c[2, 5] == np.float32(floor)
+    # pivot rows do not move the column factors: scaling them changes nothing
+    S2 = S.copy()
+    S2[bits == 16] *= 1000.0
+    _, c2 = stepq.stepq_setup_fit(S2, wts, row_bits=bits, levels=levels)
+    assert np.array_equal(c, c2)
+
+
 def test_lifetime_bits_match_oracle():
     w = W.workload(1)
     g = W.calibration_gates(w)
