@@ -68,7 +68,7 @@ def traffic_file(mode, kda: bool, workload: str = "pool_b512", pivots: bool = Fa
 
 
 def kernel_sources(mode):
-    files = ["stepq_device.h", "stepq_internal.h"]
+    files = ["stepq_device.h", "stepq_internal.h", "stepq_layout.h"]
     files += {False: ["stepq_kernels.hip"], True: ["stepq_refit_body.h", "stepq_refit.hip"],
               "row_absmax": ["stepq_refit_body.h", "stepq_rowmax.hip"]}[mode]
     return [os.path.join(CSRC, f) for f in files]
