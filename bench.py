@@ -42,8 +42,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-# fp32 VALU operations without packed math: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
-VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# fp32 vector peak, an FMA counted as one operation: 256 CUs x 4 SIMDs x 32
+# lanes x 2.4 GHz = 78.6 Top/s (the published 157.3 TFLOP/s fp32 vector rate
+# counts an FMA as two).  On gfx950 only plain fp32 add, subtract, multiply
+# and FMA issue at that rate (a wave64 instruction every 2 cycles, without
+# packed math); conversions, clamps (med3, max, min), round-to-integer,
+# mixed-precision FMAs, byte packing, shifts and DPP moves issue at half of it
+# (measured), and the decode steps are mostly made of those.
+VALU_PEAK_TOPS = 256 * 4 * 32 * 2.4e9 / 1e12
 # fp32 operations per state element of one step, counted from the method in
 # its code-space form (each convert, add, multiply, FMA, max, round, clamp or
 # pack counts one): decode 1, S^T k and S^T q 2, new value 2, requantize 4;
@@ -531,10 +537,11 @@ def main():
                    "why": "untimed steps before warmup until the GPU clocks reach steady state under load"},
     }
     if rescale or w.name == "pool_4bit":
-        # Bound by fp32 VALU work, not by HBM, so that roofline is the primary one: the refitting
-        # steps, and the {2,4,8} pool, whose 2-bit rows carry four codes per byte (a copy of the
-        # frozen kernel with its arithmetic removed moves the pool_4bit bytes in ~52 us against
-        # ~72 us for the full kernel; on pool_b512 and stack48 the two are within a few percent).
+        # Bound by VALU issue, not by HBM, so that roofline is the primary one: the refitting
+        # steps, and the {2,4,8} pool, whose 2-bit rows carry four codes per byte (the library's
+        # memory-only reference of the pool_4bit launch takes ~54 us against ~64 us for the full
+        # kernel, and a copy of the kernel without the code-word traffic takes as long as the full
+        # one; on pool_b512 and stack48 the memory-only reference is within a few percent).
         rl = line["roofline"]
         hbm = {k: rl[k] for k in ("achieved", "peak", "unit", "frac")}
         valu = rl.pop("valu")

@@ -475,18 +475,19 @@ __device__ __forceinline__ float row_constants_mfma(float beta, const RowColOps 
         sh.av[p] = beta * ki * qb * __builtin_amdgcn_rcpf(op.r);
         if constexpr (DIAG) sh.al[p] = di * (p < X4 ? 1.0f : (p < X2 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
         kq = qi * ki;
-    }
-    kq = wave_sum(kq);
-    const float mk = wave_max(fabsf(kt)), mq = wave_max(fabsf(qt));
-    if ((tid & 63) == 0) {
-        sh.kap[tid >> 6] = kq;
-        sh.wmx[tid >> 6] = make_float2(mk, mq);
+        // the rows live in wavefronts 0 and 1 only: the others skip the reductions
+        kq = wave_sum(kq);
+        const float mk = wave_max(fabsf(kt)), mq = wave_max(fabsf(qt));
+        if ((tid & 63) == 0) {
+            sh.kap[tid >> 6] = kq;
+            sh.wmx[tid >> 6] = make_float2(mk, mq);
+        }
     }
     __syncthreads();
-    const float2 w0 = sh.wmx[0], w1 = sh.wmx[1];     // the rows live in wavefronts 0 and 1
+    const float2 w0 = sh.wmx[0], w1 = sh.wmx[1];
     ek = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(w0.x, w1.x)));
     eq = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(w0.y, w1.y)));
-    const float kappa = (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
+    const float kappa = sh.kap[0] + sh.kap[1];
     if (tid < 128) {
         const int p = tid;
         int slice, ridx;
@@ -566,18 +567,20 @@ __device__ __forceinline__ float row_constants_mfma_piv(const HeadInfo &hi, floa
         }
         sh.av[x] = av;
         if constexpr (DIAG) sh.al[x] = al;
-    }
-    kq = wave_sum(kq);
-    const float mk = wave_max(fabsf(kt)), mq = wave_max(fabsf(qt));
-    if ((tid & 63) == 0) {
-        sh.kap[tid >> 6] = kq;
-        sh.wmx[tid >> 6] = make_float2(mk, mq);
+        // the table slots and pivot rows live in wavefronts 0 and 1 only:
+        // the others skip the reductions
+        kq = wave_sum(kq);
+        const float mk = wave_max(fabsf(kt)), mq = wave_max(fabsf(qt));
+        if ((tid & 63) == 0) {
+            sh.kap[tid >> 6] = kq;
+            sh.wmx[tid >> 6] = make_float2(mk, mq);
+        }
     }
     __syncthreads();
-    const float2 w0 = sh.wmx[0], w1 = sh.wmx[1];     // the table slots live in wavefronts 0 and 1
+    const float2 w0 = sh.wmx[0], w1 = sh.wmx[1];
     ek = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(w0.x, w1.x)));
     eq = __builtin_amdgcn_readfirstlane(weight_scale_exp(fmaxf(w0.y, w1.y)));
-    const float kappa = (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
+    const float kappa = sh.kap[0] + sh.kap[1];
     if (tid < 128) {
         constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
         const int x = tid;
@@ -912,6 +915,68 @@ __device__ __forceinline__ uint32_t requant_word_p(const uint32_t (&Ub)[4][4][2]
         out |= P << (s * B);
     }
     return out ^ flip;
+}
+
+// Row r of the thread's 16 (row-pair register layout of unpack_row_pairs):
+// its row-table slot (= physical row in a uniform layout) and width.
+template <int M8, int M4>
+__device__ __forceinline__ constexpr int thread_row_width(int r)
+{
+    return r < M8 ? 8 : (r < M8 + 2 * M4 ? 4 : 2);
+}
+
+template <int M8, int M4>
+__device__ __forceinline__ int thread_row_slot(int r, int slice)
+{
+    constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
+    if (r < M8) return slice + 8 * r;
+    if (r < M8 + 2 * M4) {
+        const int k = r - M8;
+        return X4 + 2 * (slice + 8 * (k >> 1)) + (k & 1);
+    }
+    const int k = r - M8 - 2 * M4;
+    return X2 + 4 * (slice + 8 * (k >> 2)) + (k & 3);
+}
+
+// ---- the gate term of the refit's unrounded codes on the matrix cores.
+// Per field y = al U + av_i bc_j, U the old code as the converts left it.
+// A 4x4x4 binary16 block with A = al I (diagonal) and B = the 4 rows'
+// codes of a lane's column returns al U + C for those rows.  With al a
+// binary16 value the product al U (|U| <= 127) is exact in fp32 and the
+// other three products are zero; the block's addition of C is not always
+// the correctly rounded one, though: measured on gfx950 it equals the FMA
+// when C is of the magnitude of al U and is otherwise within one ulp of it.
+// al = alpha 2^(b-8) is a binary16 value when it is zero or a normal
+// binary16 number equal to alpha 2^(b-8) (a bf16 gate not far below 1, for
+// instance); otherwise the vector-unit FMA is used.  A 4x4x4 block costs the
+// SIMD about as much issue time as four vector FMAs (measured), so this pays
+// only where it also shortens the vector-unit work (the refitting body,
+// which then needs no separate product); the frozen-scale bodies keep the
+// gate term on the vector unit.
+
+// Exactly a normal binary16 value (or zero).
+__device__ __forceinline__ bool binary16_exact(float x)
+{
+    const float ax = fabsf(x);
+    return static_cast<float>(static_cast<_Float16>(x)) == x && (x == 0.f || (ax >= 0x1p-14f && ax <= 65504.f));
+}
+
+// A operand of the diagonal block: lane 4b + i supplies row i of A, al at
+// column i and zeros elsewhere.
+__device__ __forceinline__ u32x2 diag_operand(float al, int i)
+{
+    const uint32_t h = __builtin_bit_cast(uint16_t, static_cast<_Float16>(al));
+    const uint32_t v = (i & 1) ? (h << 16) : h;
+    return (i & 2) ? u32x2{0u, v} : u32x2{v, 0u};
+}
+
+// Whether the uniform layout's gate factors alpha, alpha / 16, alpha / 64
+// (of the widths it holds) are binary16 values.
+template <int M8, int M4, int M2>
+__device__ __forceinline__ bool gate_on_matrix_cores(float alpha)
+{
+    return (M8 == 0 || binary16_exact(alpha)) && (M4 == 0 || binary16_exact(alpha * (1.0f / 16.0f))) &&
+           (M2 == 0 || binary16_exact(alpha * (1.0f / 64.0f)));
 }
 
 // New word from the unpacked old fields: per field

@@ -37,6 +37,7 @@ namespace stepq {
 namespace {
 
 constexpr float kScaleFloor = 0x1p-60f;
+constexpr float kRoundMagic = 0x1.8p+23f;     // 1.5 2^23: x + this rounds x to an integer (|x| < 2^22)
 
 enum class Refit : int {
     DualAxis = 0,    // Key-Row-Aware Dual-Axis fit (Section 4.3, Appendix C.1)
@@ -195,6 +196,38 @@ __device__ __forceinline__ void word_y_p(const uint32_t (&Ub)[4][4][2], int r0, 
     }
 }
 
+// Pass 1 of a uniform body with the gate term of y on the matrix cores
+// (gate_on_matrix_cores must hold): per row group g and column e, one
+// diagonal 4x4x4 block gives y = al U + (av_i bc_j) for the group's 4 rows
+// (within one ulp of word_y_p's FMA); Y[4 r + e] for thread row r, and the
+// row partials to LDS.
+template <int M8, int M4, int M2, Refit MODE>
+__device__ __forceinline__ void refit_y_mfma(const uint32_t (&Ub)[4][4][2], RefitShared<128> &sh, int tid, int slice,
+                                             int cg, float alpha, const float (&bc)[4], const float (&cc)[4],
+                                             float (&Y)[64])
+{
+    constexpr int G4 = M8 / 4, G2 = (M8 + 2 * M4) / 4;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const float al = g < G4 ? alpha : (g < G2 ? alpha * (1.0f / 16.0f) : alpha * (1.0f / 64.0f));
+        const u32x2 A = diag_operand(al, tid & 3);
+        float as[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) as[k] = sh.d.av[thread_row_slot<M8, M4>(4 * g + k, slice)];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const f32x4 d = mfma4x4x4(A, Ub[e][g][0], Ub[e][g][1],
+                                      f32x4{as[0] * bc[e], as[1] * bc[e], as[2] * bc[e], as[3] * bc[e]});
+#pragma unroll
+            for (int k = 0; k < 4; ++k) Y[4 * (4 * g + k) + e] = d[k];
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+            put_row_partial<128>(sh, thread_row_slot<M8, M4>(4 * g + k, slice), cg,
+                                 row_partial<MODE>(&Y[4 * (4 * g + k)], cc));
+    }
+}
+
 template <int B>
 __device__ __forceinline__ void word_scale(float *Y, const float *hrow, int x0)
 {
@@ -230,7 +263,9 @@ __device__ __forceinline__ void word_fit(const float *Y, const float *wrow, int 
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const float yh = Y[4 * s + e];
-            const float z = __builtin_rintf(yh * ec[e]);
+            // round to nearest even by the fp32 grid at 1.5 2^23 (|z| <= q_b):
+            // one rounding of the exact product, in two full-rate operations
+            const float z = fmaf(yh, ec[e], kRoundMagic) - kRoundMagic;
             const float u = W * z;
             num[e] = fmaf(u, yh, num[e]);
             den[e] = fmaf(u, z, den[e]);
@@ -308,16 +343,26 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     ld4(&sh.d.bcol[4 * cg], bc);
     ld4(&sh.ccol[4 * cg], cc);
     float Y[NE];
+    bool y_done = false;
+    if constexpr (!DIAG) {
+        if (gate_on_matrix_cores<M8, M4, M2>(t.alpha)) {
+            refit_y_mfma<M8, M4, M2, MODE>(Ub, sh, tid, slice, cg, t.alpha, bc, cc, Y);
+            y_done = true;
+        }
+    }
+    if (!y_done) {
 #pragma unroll
-    for (int m = 0; m < M8; ++m) word_y_p<8, DIAG, MODE>(Ub, m, sh, slice + 8 * m, cg, t.alpha, bc, cc, &Y[4 * m]);
+        for (int m = 0; m < M8; ++m)
+            word_y_p<8, DIAG, MODE>(Ub, m, sh, slice + 8 * m, cg, t.alpha, bc, cc, &Y[4 * m]);
 #pragma unroll
-    for (int m = 0; m < M4; ++m)
-        word_y_p<4, DIAG, MODE>(Ub, M8 + 2 * m, sh, X4 + 2 * (slice + 8 * m), cg, t.alpha * (1.0f / 16.0f), bc, cc,
-                                &Y[Y4 + 8 * m]);
+        for (int m = 0; m < M4; ++m)
+            word_y_p<4, DIAG, MODE>(Ub, M8 + 2 * m, sh, X4 + 2 * (slice + 8 * m), cg, t.alpha * (1.0f / 16.0f), bc,
+                                    cc, &Y[Y4 + 8 * m]);
 #pragma unroll
-    for (int m = 0; m < M2; ++m)
-        word_y_p<2, DIAG, MODE>(Ub, M8 + 2 * M4 + 4 * m, sh, X2 + 4 * (slice + 8 * m), cg, t.alpha * (1.0f / 64.0f),
-                                bc, cc, &Y[Y2 + 16 * m]);
+        for (int m = 0; m < M2; ++m)
+            word_y_p<2, DIAG, MODE>(Ub, M8 + 2 * M4 + 4 * m, sh, X2 + 4 * (slice + 8 * m), cg,
+                                    t.alpha * (1.0f / 64.0f), bc, cc, &Y[Y2 + 16 * m]);
+    }
     __syncthreads();
     if (tid < 128) refit_row<128, MODE>(sh, tid, tid, tid < X4 ? 8 : (tid < X2 ? 4 : 2), op.r, rr_out, a.pool.lv);
     if constexpr (MODE == Refit::RowAbsmax) {

@@ -56,27 +56,6 @@ __device__ __forceinline__ void column_sums_rowmax(const DecodeArgs &a, int tile
     __syncthreads();
 }
 
-// Row r of the thread's 16 (row-pair register layout of unpack_row_pairs):
-// its row-table slot (= physical row in a uniform layout) and width.
-template <int M8, int M4>
-__device__ __forceinline__ constexpr int thread_row_width(int r)
-{
-    return r < M8 ? 8 : (r < M8 + 2 * M4 ? 4 : 2);
-}
-
-template <int M8, int M4>
-__device__ __forceinline__ int thread_row_slot(int r, int slice)
-{
-    constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
-    if (r < M8) return slice + 8 * r;
-    if (r < M8 + 2 * M4) {
-        const int k = r - M8;
-        return X4 + 2 * (slice + 8 * (k >> 1)) + (k & 1);
-    }
-    const int k = r - M8 - 2 * M4;
-    return X2 + 4 * (slice + 8 * (k >> 2)) + (k & 3);
-}
-
 // max(|a|, |b|, |c|) in one instruction.  Written out because the
 // compiler's own form would first quiet each input (the values come from
 // inline assembly, which it cannot prove free of signalling NaNs); finite
