@@ -448,7 +448,10 @@ __device__ __forceinline__ int weight_scale_exp(float m)
 // group], the thread's 16 rows being its 8-bit rows, then the two slots of
 // each 4-bit word, then the four slots of each 2-bit word (4 to a group).
 // Two barriers; the operand table is complete only after one more.
-template <bool DIAG, int M8, int M4, int M2, int DV>
+// SCALED: av and al of the 4- and 2-bit rows come divided by 2^B - 2, the
+// form the frozen-scale requantization of those rows works in
+// (requant_field_p).
+template <bool DIAG, int M8, int M4, int M2, int DV, bool SCALED = false>
 __device__ __forceinline__ float row_constants_mfma(float beta, const RowColOps &op, DecodeShared<DV> &sh,
                                                     const LevelTable &lv, int &ek, int &eq)
 {
@@ -472,8 +475,10 @@ __device__ __forceinline__ float row_constants_mfma(float beta, const RowColOps 
         const float rs = op.r * fq * di;
         kt = ki * rs;
         qt = qi * rs;
-        sh.av[p] = beta * ki * qb * __builtin_amdgcn_rcpf(op.r);
-        if constexpr (DIAG) sh.al[p] = di * (p < X4 ? 1.0f : (p < X2 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
+        const float sc = SCALED ? (p < X4 ? 1.0f : (p < X2 ? (1.0f / 14.0f) : 0.5f)) : 1.0f;
+        sh.av[p] = beta * ki * (qb * sc) * __builtin_amdgcn_rcpf(op.r);
+        if constexpr (DIAG)
+            sh.al[p] = di * (p < X4 ? 1.0f : (p < X2 ? (1.0f / 16.0f) * sc : (1.0f / 64.0f) * sc));
         kq = qi * ki;
         // the rows live in wavefronts 0 and 1 only: the others skip the reductions
         kq = wave_sum(kq);
@@ -522,7 +527,7 @@ __device__ __forceinline__ float row_constants_mfma(float beta, const RowColOps 
 // slot_row (empty slots get zero weights and update factors, so their zero
 // codes stay zero).  Also the pivot rows' constants (pvc) and c (cpiv), as
 // in row_constants.  Two barriers; the operand table needs one more.
-template <bool DIAG, int M8, int M4, int M2, int DV>
+template <bool DIAG, int M8, int M4, int M2, int DV, bool SCALED = false>
 __device__ __forceinline__ float row_constants_mfma_piv(const HeadInfo &hi, float alpha, float beta,
                                                         const RowColOps &op, DecodeShared<DV> &sh,
                                                         const LevelTable &lv, int &ek, int &eq)
@@ -561,8 +566,9 @@ __device__ __forceinline__ float row_constants_mfma_piv(const HeadInfo &hi, floa
             const float rs = r * lv.fq[wi] * di;
             kt = ki * rs;
             qt = qi * rs;
-            av = beta * ki * lv.iq[wi] * __builtin_amdgcn_rcpf(r);
-            al = di * (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
+            const float sc = SCALED ? (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 14.0f) : 0.5f)) : 1.0f;
+            av = beta * ki * (lv.iq[wi] * sc) * __builtin_amdgcn_rcpf(r);
+            al = di * (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 16.0f) * sc : (1.0f / 64.0f) * sc));
             kq += qi * ki;
         }
         sh.av[x] = av;
@@ -871,17 +877,42 @@ __device__ __forceinline__ f32x4 mfma_view(const _Float16 (&A)[4][4], const uint
     return mfma4x4x4(a, b0, b1, d);
 }
 
+// a * h + c clamped to [0, 1] by the instruction's clamp bit, h the low
+// (HI = 0) or high (HI = 1) binary16 half of hp.
+template <int HI>
+__device__ __forceinline__ float fma_mix_clamp(float a, uint32_t hp, float c)
+{
+    float r;
+    if constexpr (HI)
+        asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel:[0,1,0] op_sel_hi:[0,1,0] clamp" : "=v"(r) : "v"(a), "v"(hp), "v"(c));
+    else
+        asm("v_fma_mix_f32 %0, %1, %2, %3 op_sel_hi:[0,1,0] clamp" : "=v"(r) : "v"(a), "v"(hp), "v"(c));
+    return r;
+}
+
 // New field in byte E of P from the old field in half HALF of hp; the
-// arithmetic of requant_word below.
+// arithmetic of requant_word below.  For 4- and 2-bit fields the clamp to
+// [1, 2^B - 1] comes from the FMA's clamp bit: it forms
+// (y - 1) / (2^B - 2) = (al / (2^B - 2)) U + (a_s / (2^B - 2)) bc_j + 1/2
+// (a_s arrives divided), clamped to [0, 1], and one full-rate FMA scales it
+// back; on gfx950 that replaces a half-rate med3.  The scaling is exact for
+// 2-bit fields and costs a few ulp of the field value (at most 15) for
+// 4-bit ones.  8-bit fields, whose values reach 255, keep the med3 form.
 template <int B, int E, int HALF>
 __device__ __forceinline__ uint32_t requant_field_p(uint32_t hp, float al, float a_s, float bce, uint32_t P)
 {
     constexpr float bias = static_cast<float>(1 << (B - 1));
     constexpr float top = static_cast<float>((1 << B) - 1);
-    const float tt = fmaf(a_s, bce, bias);
-    float y = fma_mix<HALF>(al, hp, tt);
-    y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
-    return __builtin_amdgcn_cvt_pk_u8_f32(y, E, P);
+    if constexpr (B == 8) {
+        const float tt = fmaf(a_s, bce, bias);
+        float y = fma_mix<HALF>(al, hp, tt);
+        y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
+        return __builtin_amdgcn_cvt_pk_u8_f32(y, E, P);
+    } else {
+        const float tt = fmaf(a_s, bce, 0.5f);
+        const float y01 = fma_mix_clamp<HALF>(al, hp, tt);
+        return __builtin_amdgcn_cvt_pk_u8_f32(fmaf(y01, top - 1.0f, 1.0f), E, P);
+    }
 }
 
 template <int B, int HALF>
@@ -897,19 +928,24 @@ __device__ __forceinline__ uint32_t requant_slot_p(const uint32_t (&Ub)[4][4][2]
 }
 
 // New word of 8/B slots (row-table slots x0 + s, thread rows r0 + s) from
-// the row-pair registers; as requant_word otherwise.  r0 is a constant
+// the row-pair registers; as requant_word otherwise.  av and alt: the row
+// constants of row_constants_mfma with SCALED set.  r0 is a constant
 // once the caller's loops are unrolled, so every register index folds.
 template <int B, bool DIAG>
 __device__ __forceinline__ uint32_t requant_word_p(const uint32_t (&Ub)[4][4][2], int r0, const float *av,
                                                    const float *alt, int x0, float al_w, const float (&bc)[4])
 {
     constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
+    // 4- and 2-bit fields work on (y - 1) / (2^B - 2) (requant_field_p): av
+    // and the per-row gates come divided from the row constants, the scalar
+    // gate is divided here
+    constexpr float sc = B == 8 ? 1.0f : 1.0f / static_cast<float>((1 << B) - 2);
     uint32_t out = 0;
 #pragma unroll
     for (int s = 0; s < 8 / B; ++s) {
         const int r = r0 + s;
         const float a_s = av[x0 + s];
-        const float al = DIAG ? alt[x0 + s] : al_w;
+        const float al = DIAG ? alt[x0 + s] : al_w * sc;
         const uint32_t P = (r & 1) ? requant_slot_p<B, 1>(Ub, r >> 2, (r >> 1) & 1, al, a_s, bc)
                                    : requant_slot_p<B, 0>(Ub, r >> 2, (r >> 1) & 1, al, a_s, bc);
         out |= P << (s * B);

@@ -59,9 +59,9 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
     int ek, eq;
     float kappa;
     if constexpr (PIV)
-        kappa = row_constants_mfma_piv<DIAG, M8, M4, M2, 128>(t.hi, t.alpha, t.beta, op, sh, a.pool.lv, ek, eq);
+        kappa = row_constants_mfma_piv<DIAG, M8, M4, M2, 128, true>(t.hi, t.alpha, t.beta, op, sh, a.pool.lv, ek, eq);
     else
-        kappa = row_constants_mfma<DIAG, M8, M4, M2, 128>(t.beta, op, sh, a.pool.lv, ek, eq);
+        kappa = row_constants_mfma<DIAG, M8, M4, M2, 128, true>(t.beta, op, sh, a.pool.lv, ek, eq);
 
     uint32_t Ub[4][4][2];
     unpack_row_pairs<M8, M4, M2>(w, Ub);
