@@ -283,7 +283,9 @@ __device__ __forceinline__ RowColOps load_ops(const DecodeArgs &a, int tile, int
 // Row constants into LDS, indexed by row-table slot, and q.k.  Two barriers;
 // returns q.k.  Rows are read through the physical -> logical permutation
 // from the LDS copy of k and q.
-template <bool DIAG, int DV>
+// SCALED: av and al come divided by the row width's clamp_scale, the form
+// the frozen-scale requantization works in (requant_word).
+template <bool DIAG, int DV, bool SCALED = false>
 __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float alpha, float beta,
                                                const RowColOps &op, DecodeShared<DV> &sh, const LevelTable &lv)
 {
@@ -327,8 +329,9 @@ __device__ __forceinline__ float row_constants(const HeadInfo &hi, int dk, float
             const float rs = rp * fq * di;
             kt = ki * rs;
             qt = qi * rs;
-            av = beta * ki * qb * __builtin_amdgcn_rcpf(rp);
-            al = di * (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 16.0f) : (1.0f / 64.0f)));
+            const float sc = SCALED ? (bw == 8 ? 1.0f / 256.0f : (bw == 4 ? (1.0f / 14.0f) : 0.5f)) : 1.0f;
+            av = beta * ki * (qb * sc) * __builtin_amdgcn_rcpf(rp);
+            al = di * (bw == 8 ? sc : (bw == 4 ? (1.0f / 16.0f) * sc : (1.0f / 64.0f) * sc));
             kq += qi * ki;
         }
         sh.kq[x] = make_float2(kt, qt);
@@ -448,9 +451,8 @@ __device__ __forceinline__ int weight_scale_exp(float m)
 // group], the thread's 16 rows being its 8-bit rows, then the two slots of
 // each 4-bit word, then the four slots of each 2-bit word (4 to a group).
 // Two barriers; the operand table is complete only after one more.
-// SCALED: av and al of the 4- and 2-bit rows come divided by 2^B - 2, the
-// form the frozen-scale requantization of those rows works in
-// (requant_field_p).
+// SCALED: av and al come divided by the row width's clamp_scale, the form
+// the frozen-scale requantization works in (requant_field_p).
 template <bool DIAG, int M8, int M4, int M2, int DV, bool SCALED = false>
 __device__ __forceinline__ float row_constants_mfma(float beta, const RowColOps &op, DecodeShared<DV> &sh,
                                                     const LevelTable &lv, int &ek, int &eq)
@@ -475,10 +477,10 @@ __device__ __forceinline__ float row_constants_mfma(float beta, const RowColOps 
         const float rs = op.r * fq * di;
         kt = ki * rs;
         qt = qi * rs;
-        const float sc = SCALED ? (p < X4 ? 1.0f : (p < X2 ? (1.0f / 14.0f) : 0.5f)) : 1.0f;
+        const float sc = SCALED ? (p < X4 ? 1.0f / 256.0f : (p < X2 ? (1.0f / 14.0f) : 0.5f)) : 1.0f;
         sh.av[p] = beta * ki * (qb * sc) * __builtin_amdgcn_rcpf(op.r);
         if constexpr (DIAG)
-            sh.al[p] = di * (p < X4 ? 1.0f : (p < X2 ? (1.0f / 16.0f) * sc : (1.0f / 64.0f) * sc));
+            sh.al[p] = di * (p < X4 ? sc : (p < X2 ? (1.0f / 16.0f) * sc : (1.0f / 64.0f) * sc));
         kq = qi * ki;
         // the rows live in wavefronts 0 and 1 only: the others skip the reductions
         kq = wave_sum(kq);
@@ -566,9 +568,9 @@ __device__ __forceinline__ float row_constants_mfma_piv(const HeadInfo &hi, floa
             const float rs = r * lv.fq[wi] * di;
             kt = ki * rs;
             qt = qi * rs;
-            const float sc = SCALED ? (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 14.0f) : 0.5f)) : 1.0f;
+            const float sc = SCALED ? (bw == 8 ? 1.0f / 256.0f : (bw == 4 ? (1.0f / 14.0f) : 0.5f)) : 1.0f;
             av = beta * ki * (lv.iq[wi] * sc) * __builtin_amdgcn_rcpf(r);
-            al = di * (bw == 8 ? 1.0f : (bw == 4 ? (1.0f / 16.0f) * sc : (1.0f / 64.0f) * sc));
+            al = di * (bw == 8 ? sc : (bw == 4 ? (1.0f / 16.0f) * sc : (1.0f / 64.0f) * sc));
             kq += qi * ki;
         }
         sh.av[x] = av;
@@ -890,29 +892,34 @@ __device__ __forceinline__ float fma_mix_clamp(float a, uint32_t hp, float c)
     return r;
 }
 
+// Scale of the clamped form of a B-bit field (requant_field_p): the field
+// value y in [1, 2^B - 1] is handled as (y - 1) / S clamped to [0, 1].
+// S = 2^B - 2 for 4- and 2-bit fields, where the top of the clamp is the
+// top level; S = 256 for 8-bit fields, whose clamp then tops at 257 and
+// v_cvt_pk_u8_f32's saturation at 255 does the rest.  2- and 8-bit scales
+// are powers of two.
+template <int B>
+__device__ __forceinline__ constexpr float clamp_scale()
+{
+    return B == 8 ? 256.0f : static_cast<float>((1 << B) - 2);
+}
+
 // New field in byte E of P from the old field in half HALF of hp; the
-// arithmetic of requant_word below.  For 4- and 2-bit fields the clamp to
-// [1, 2^B - 1] comes from the FMA's clamp bit: it forms
-// (y - 1) / (2^B - 2) = (al / (2^B - 2)) U + (a_s / (2^B - 2)) bc_j + 1/2
-// (a_s arrives divided), clamped to [0, 1], and one full-rate FMA scales it
-// back; on gfx950 that replaces a half-rate med3.  The scaling is exact for
-// 2-bit fields and costs a few ulp of the field value (at most 15) for
-// 4-bit ones.  8-bit fields, whose values reach 255, keep the med3 form.
+// arithmetic of requant_word below, with the clamp to [1, 2^B - 1] from the
+// FMA's clamp bit: it forms
+//     (y - 1) / S = (al / S) U + (a_s / S) bc_j + (2^(B-1) - 1) / S
+// (al and a_s arrive divided by S) clamped to [0, 1], and one full-rate FMA
+// scales it back; on gfx950 that replaces a half-rate med3.  The scalings
+// are exact for 8- and 2-bit fields and cost a few ulp of the field value
+// (at most 15) for 4-bit ones.
 template <int B, int E, int HALF>
 __device__ __forceinline__ uint32_t requant_field_p(uint32_t hp, float al, float a_s, float bce, uint32_t P)
 {
-    constexpr float bias = static_cast<float>(1 << (B - 1));
-    constexpr float top = static_cast<float>((1 << B) - 1);
-    if constexpr (B == 8) {
-        const float tt = fmaf(a_s, bce, bias);
-        float y = fma_mix<HALF>(al, hp, tt);
-        y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
-        return __builtin_amdgcn_cvt_pk_u8_f32(y, E, P);
-    } else {
-        const float tt = fmaf(a_s, bce, 0.5f);
-        const float y01 = fma_mix_clamp<HALF>(al, hp, tt);
-        return __builtin_amdgcn_cvt_pk_u8_f32(fmaf(y01, top - 1.0f, 1.0f), E, P);
-    }
+    constexpr float S = clamp_scale<B>();
+    constexpr float c0 = static_cast<float>((1 << (B - 1)) - 1) / S;
+    const float tt = fmaf(a_s, bce, c0);
+    const float y01 = fma_mix_clamp<HALF>(al, hp, tt);
+    return __builtin_amdgcn_cvt_pk_u8_f32(fmaf(y01, S, 1.0f), E, P);
 }
 
 template <int B, int HALF>
@@ -936,10 +943,10 @@ __device__ __forceinline__ uint32_t requant_word_p(const uint32_t (&Ub)[4][4][2]
                                                    const float *alt, int x0, float al_w, const float (&bc)[4])
 {
     constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
-    // 4- and 2-bit fields work on (y - 1) / (2^B - 2) (requant_field_p): av
-    // and the per-row gates come divided from the row constants, the scalar
+    // the fields are handled as (y - 1) / S (requant_field_p): av and the
+    // per-row gates come divided by S from the row constants, the scalar
     // gate is divided here
-    constexpr float sc = B == 8 ? 1.0f : 1.0f / static_cast<float>((1 << B) - 2);
+    constexpr float sc = 1.0f / clamp_scale<B>();
     uint32_t out = 0;
 #pragma unroll
     for (int s = 0; s < 8 / B; ++s) {
@@ -1015,30 +1022,41 @@ __device__ __forceinline__ bool gate_on_matrix_cores(float alpha)
            (M2 == 0 || binary16_exact(alpha * (1.0f / 64.0f)));
 }
 
+// a * b + c clamped to [0, 1] by the instruction's clamp bit.
+__device__ __forceinline__ float fma_clamp(float a, float b, float c)
+{
+    float r;
+    asm("v_fma_f32 %0, %1, %2, %3 clamp" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
 // New word from the unpacked old fields: per field
 //   y = al U + av_i bc_j + 2^(B-1)        (code + bias, Eq. 3 argument)
 // clamped to [1, 2^B - 1] (i.e. code in [-q_b, q_b]), rounded to nearest
 // even and packed to a byte by v_cvt_pk_u8_f32, then the bias is removed
-// from all fields at once by flipping each field's top bit.
+// from all fields at once by flipping each field's top bit.  The clamp is
+// the FMA's clamp bit on (y - 1) / S, scaled back by one more FMA
+// (requant_field_p, clamp_scale): av and the per-row gates alt come
+// divided by S (row_constants with SCALED set), the scalar gate al_w is
+// divided here.
 template <int B, bool DIAG>
 __device__ __forceinline__ uint32_t requant_word(const float *U, const float *av, const float *alt, int x0,
                                                  float al_w, const float (&bc)[4])
 {
-    constexpr float bias = static_cast<float>(1 << (B - 1));
-    constexpr float top = static_cast<float>((1 << B) - 1);
+    constexpr float S = clamp_scale<B>();
+    constexpr float c0 = static_cast<float>((1 << (B - 1)) - 1) / S;
     constexpr uint32_t flip = B == 8 ? 0x80808080u : (B == 4 ? 0x88888888u : 0xAAAAAAAAu);
     uint32_t out = 0;
 #pragma unroll
     for (int s = 0; s < 8 / B; ++s) {
         const float a_s = av[x0 + s];
-        const float al = DIAG ? alt[x0 + s] : al_w;
+        const float al = DIAG ? alt[x0 + s] : al_w * (1.0f / S);
         uint32_t P = 0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            const float tt = fmaf(a_s, bc[e], bias);
-            float y = fmaf(al, U[4 * s + e], tt);
-            y = __builtin_amdgcn_fmed3f(y, 1.0f, top);
-            P = __builtin_amdgcn_cvt_pk_u8_f32(y, e, P);
+            const float tt = fmaf(a_s, bc[e], c0);
+            const float y01 = fma_clamp(al, U[4 * s + e], tt);
+            P = __builtin_amdgcn_cvt_pk_u8_f32(fmaf(y01, S, 1.0f), e, P);
         }
         out |= P << (s * B);
     }

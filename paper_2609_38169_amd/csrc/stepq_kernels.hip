@@ -127,7 +127,7 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
     PivotRegs<DV, PMAX> pr;
     pivot_load(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    const float kappa = row_constants<DIAG, DV>(t.hi, a.pool.dk, t.alpha, t.beta, op, sh, a.pool.lv);
+    const float kappa = row_constants<DIAG, DV, true>(t.hi, a.pool.dk, t.alpha, t.beta, op, sh, a.pool.lv);
 
     float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
     float U[16];
@@ -232,7 +232,7 @@ __device__ __forceinline__ void decode_rowmix(const DecodeArgs &a, const TileCtx
     // v_j waits in LDS for the column phase (c_j is kept there for the pivot
     // rows), so neither is held in registers through the row sums
     if (tid < 128) sh.bcol[tid] = op.v;
-    const float kappa = uniform_f(row_constants<DIAG, 128>(t.hi, 128, t.alpha, t.beta, op, sh, a.pool.lv));
+    const float kappa = uniform_f(row_constants<DIAG, 128, true>(t.hi, 128, t.alpha, t.beta, op, sh, a.pool.lv));
     int ek, eq;
     row_operands_rowmix(t.hi, sh, ek, eq);
 
