@@ -129,6 +129,19 @@ def test_tiles_at_extreme_magnitudes(refit, kda):
                     fp32_bounds=True)
 
 
+@pytest.mark.parametrize("idx", [2, 3])
+def test_saturating_updates(idx):
+    """v scaled by 64 (exact in bf16): the rank-one write drives a large share
+    of the new codes past +-q_b in both directions, on every row width of the
+    workload's mix (8/4 for pool_b512, 8/4/2 for pool_4bit), so the clamp of
+    the requantization (the FMA clamp bit on (y - 1)/S, and for 8-bit fields
+    the convert's saturation at 255) decides them; lockstep with the oracle,
+    which clips in fp64."""
+    w = W.workload(idx)
+    ls = PT.lockstep_run(w, 2, np.array([0, 255, 511]), DEV, mutate=_set("v", lambda v: v * 64), say=_say)
+    assert ls.saturated > 0.05, f"only {ls.saturated:.3f} of the checked codes saturated"
+
+
 def test_zero_keys_and_queries():
     """All-zero k on some q/k heads and all-zero q on others: a tile whose
     largest k (or q) weight is 0.  With k = 0 the step is a pure decay,
