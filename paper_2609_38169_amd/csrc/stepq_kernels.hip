@@ -117,13 +117,12 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
     const int tid = threadIdx.x;
     const int cg = tid % CG, slice = tid / CG;
     const int ngroups = static_cast<int>(t.hi.groups);
+    // words of groups past the head's last lie in the zeroed tail of the
+    // codes region or past it (read as 0): one uniform check per word-step
     const CodeWords cw(t.codes, t.hi.piv_off);
     uint32_t w[MMAX];
 #pragma unroll
-    for (int m = 0; m < MMAX; ++m) {
-        const int g = slice + NSL * m;
-        w[m] = g < ngroups ? cw.load(tid + 256 * m) : 0u;
-    }
+    for (int m = 0; m < MMAX; ++m) w[m] = NSL * m < ngroups ? cw.load(tid + 256 * m) : 0u;
     PivotRegs<DV, PMAX> pr;
     pivot_load(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, DV>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
@@ -219,13 +218,13 @@ __device__ __forceinline__ void decode_rowmix(const DecodeArgs &a, const TileCtx
     const int cg = tid & 31, slice = tid >> 5;
     const int g8 = __builtin_amdgcn_readfirstlane(static_cast<int>(t.hi.g8));
     const int ng = __builtin_amdgcn_readfirstlane(static_cast<int>(t.hi.groups));
+    // the buffer covers the codes region only (piv_off = 128 ng): the words
+    // of groups past the head's last read 0 and their stores are dropped, so
+    // each word-step needs one uniform check and no per-lane one
     const CodeWords cw(t.codes, t.hi.piv_off);
     uint32_t w[16];
 #pragma unroll
-    for (int m = 0; m < 16; ++m) {
-        if (8 * m + 8 <= ng) w[m] = cw.load(tid + 256 * m);
-        else w[m] = slice + 8 * m < ng ? cw.load(tid + 256 * m) : 0u;
-    }
+    for (int m = 0; m < 16; ++m) w[m] = 8 * m < ng ? cw.load(tid + 256 * m) : 0u;
     PivotRegs<128, kCompactPivots> pr;
     pivot_load<128, kCompactPivots>(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
@@ -274,29 +273,29 @@ __device__ __forceinline__ void decode_rowmix(const DecodeArgs &a, const TileCtx
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
     pivot_update<128, kCompactPivots>(t, slice, cg, pr, sh, bc);
     // row-table slot of group g: g when 8-bit, c4 + 2 g (= g8 + 2 (g - g8))
-    // when 4-bit; word-steps wholly of one width and wholly present take a
-    // uniform path, the one straddling the width boundary or the head's last
-    // group a per-lane one
+    // when 4-bit; word-steps wholly of one width take a uniform path, the one
+    // straddling the width boundary a per-lane one
     const int c4 = -g8;
     const float al4 = t.alpha * (1.0f / 16.0f);
     float U[8];
 #pragma unroll
     for (int m = 0; m < 16; ++m) {
         const int g = slice + 8 * m;
+        if (8 * m >= ng) break;
         if (8 * m + 8 <= g8) {
             unpack_word<8>(w[m], U);
             cw.store(tid + 256 * m, requant_word<8, DIAG>(U, sh.av, sh.al, g, t.alpha, bc));
-        } else if (8 * m >= g8 && 8 * m + 8 <= ng) {
+        } else if (8 * m >= g8) {
+            // lanes past the head's last group read table entries of other
+            // rows, and their stores are dropped
             unpack_word<4>(w[m], U);
             cw.store(tid + 256 * m, requant_word<4, DIAG>(U, sh.av, sh.al, c4 + 2 * g, al4, bc));
-        } else if (8 * m < ng) {
-            if (g < g8) {
-                unpack_word<8>(w[m], U);
-                cw.store(tid + 256 * m, requant_word<8, DIAG>(U, sh.av, sh.al, g, t.alpha, bc));
-            } else if (g < ng) {
-                unpack_word<4>(w[m], U);
-                cw.store(tid + 256 * m, requant_word<4, DIAG>(U, sh.av, sh.al, c4 + 2 * g, al4, bc));
-            }
+        } else if (g < g8) {
+            unpack_word<8>(w[m], U);
+            cw.store(tid + 256 * m, requant_word<8, DIAG>(U, sh.av, sh.al, g, t.alpha, bc));
+        } else {
+            unpack_word<4>(w[m], U);
+            cw.store(tid + 256 * m, requant_word<4, DIAG>(U, sh.av, sh.al, c4 + 2 * g, al4, bc));
         }
     }
 }
