@@ -275,13 +275,14 @@ def test_calibrated_head_map_runs_lockstep():
     PT.lockstep_run(w, 4, np.array([0, 100, 255]), DEV, refit=True, row_weight=cal.row_weight, say=_say, bits=bits)
 
 
-def test_calibrated_head_map_pool_b512_sampled():
+@pytest.mark.timeout(900)
+def test_calibrated_head_map_pool_b512_every_tile():
     """The head-unit calibrated map that ``bench.py --calibrated head`` times
     (whole heads at 8 or 4 bits and one whole FP16 head, from the
     calibration pipeline on the workload's own draws) at full pool_b512
     size with frozen scales: the decode step is one launch over the
-    compiled bodies of both widths and the FP16 body, and sampled requests
-    match the oracle lockstep."""
+    compiled bodies of both widths and the FP16 body, and every tile
+    matches the oracle lockstep."""
     from paper_2609_38169_amd.calibrate import calibrate
     w = W.workload(2)
     steps = [W.step_inputs(w, 0, 1000 + t) for t in range(8)]        # calibration draws, not the test steps
@@ -295,17 +296,17 @@ def test_calibrated_head_map_pool_b512_sampled():
     assert full16.sum() == 1 and all(len(set(np.unique(b))) == 1 for b in bits)
     _say(f"calibrated head map pool_b512: {int((bits[:, 0] == 8).sum())} heads @8, "
          f"{int((bits[:, 0] == 4).sum())} @4, 1 FP16 head")
-    PT.lockstep_run(w, 6, np.array([0, 1, 77, 255, 256, 400, 510, 511]), DEV, row_weight=cal.row_weight, say=_say,
-                    bits=bits)
+    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, row_weight=cal.row_weight, say=_say, bits=bits)
 
 
 @pytest.mark.parametrize("kind", ["pivot_rows", "fp16_head"])
-def test_pivot_maps_pool_b512_sampled(kind):
+@pytest.mark.timeout(900)
+def test_pivot_maps_pool_b512_every_tile(kind):
     """The maps of ``bench.py --pivots`` (1-3 FP16 pivot rows in a seeded
     quarter of the heads, run by the padded uniform body) and
     ``bench.py --fp16-heads 1`` (one whole FP16 head beside the uniform
     heads, one combined launch) at full pool_b512 size with frozen scales:
-    sampled requests lockstep with the oracle."""
+    every tile lockstep with the oracle."""
     from paper_2609_38169_amd.pools import row_bits
     w = W.workload(2)
     bits = row_bits(w).copy()
@@ -314,4 +315,4 @@ def test_pivot_maps_pool_b512_sampled(kind):
     else:
         bits[W.pivot_head_draw(w, 0, 1).numpy()] = 16
     _say(f"{kind} pool_b512: {int((bits == 16).sum())} FP16 rows")
-    PT.lockstep_run(w, 6, np.array([0, 1, 77, 255, 256, 400, 510, 511]), DEV, say=_say, bits=bits)
+    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, say=_say, bits=bits)

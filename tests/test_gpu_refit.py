@@ -40,17 +40,22 @@ def test_refit_layer_b64_64_steps():
     assert ls.saturated < 0.05
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("idx", [2, 3])
-def test_refit_pool_sized_sampled(idx):
+def test_refit_pool_sized_every_tile(idx):
+    """pool_b512 / pool_4bit with the online refit: all 16,384 tiles of the
+    full launch compared at every one of 16 steps."""
     w = W.workload(idx)
-    rows = np.array([0, 1, 77, 255, 256, 400, 510, 511])
-    _run(w, 12, rows)
+    ls = _run(w, 16, np.arange(w.batch))
+    assert ls.compared == 16 * w.batch * w.n_v_heads * w.d_k * w.d_v
 
 
-def test_refit_pool_b512_kda_sampled():
+@pytest.mark.timeout(900)
+def test_refit_pool_b512_kda_every_tile():
+    """Channel-wise gates and row weights with the online refit on the full
+    pool_b512 launch, every tile compared for 8 steps."""
     w = W.workload(2)
-    rows = np.array([2, 130, 300, 508])
-    _run(w, 8, rows, kda=True, row_weight=W.row_weight_draw(w).numpy())
+    _run(w, 8, np.arange(w.batch), kda=True, row_weight=W.row_weight_draw(w).numpy())
 
 
 def _ragged():

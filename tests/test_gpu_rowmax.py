@@ -31,15 +31,20 @@ def test_rowmax_layer_b64_64_steps():
     _run(w, 64, np.arange(w.batch))
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("idx", [2, 3])
-def test_rowmax_pool_sized_sampled(idx):
+def test_rowmax_pool_sized_every_tile(idx):
+    """pool_b512 / pool_4bit with the row-absmax step: all 16,384 tiles of
+    the full launch compared at every one of 16 steps."""
     w = W.workload(idx)
-    _run(w, 12, np.array([0, 1, 77, 255, 256, 400, 510, 511]))
+    ls = _run(w, 16, np.arange(w.batch))
+    assert ls.compared == 16 * w.batch * w.n_v_heads * w.d_k * w.d_v
 
 
-def test_rowmax_pool_b512_kda_sampled():
+@pytest.mark.timeout(900)
+def test_rowmax_pool_b512_kda_every_tile():
     w = W.workload(2)
-    _run(w, 8, np.array([5, 131, 333, 507]), kda=True)
+    _run(w, 8, np.arange(w.batch), kda=True)
 
 
 @pytest.mark.parametrize("case", range(5))

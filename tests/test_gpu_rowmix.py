@@ -185,14 +185,15 @@ def test_rowmix_lockstep_steps():
         PT.compare_out(o.cpu().numpy().reshape(-1, 128), o_ref)
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("kda", [False, True])
-def test_rowmix_calibrated_pool_b512_sampled(kda):
+def test_rowmix_calibrated_pool_b512_every_tile(kda):
     """The row-unit calibrated map that ``bench.py --calibrated row`` times
     (per-head 8/4-bit splits, 24 FP16 pivot rows, from the calibration
     pipeline on the workload's own draws) at full pool_b512 size, in the
     same launch configuration, with the scalar gate and with channel-wise
-    (KDA) gates: sampled requests lockstep with the oracle over several
-    frozen steps."""
+    (KDA) gates: every tile lockstep with the oracle over several frozen
+    steps."""
     from paper_2609_38169_amd import workloads as W
     from paper_2609_38169_amd.calibrate import calibrate
     w = W.workload(2)
@@ -206,5 +207,4 @@ def test_rowmix_calibrated_pool_b512_sampled(kda):
     n16 = (bits == 16).sum(1)
     assert n16.sum() == 24 and n16.max() <= 8 and not (bits == 2).any()
     _say(f"row-unit calibrated pool_b512: {(bits == 8).sum()} rows @8, {(bits == 4).sum()} @4, 24 pivots")
-    PT.lockstep_run(w, 6, np.array([0, 1, 77, 255, 256, 400, 510, 511]), DEV, row_weight=cal.row_weight, say=_say,
-                    bits=bits, kda=kda)
+    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, row_weight=cal.row_weight, say=_say, bits=bits, kda=kda)
