@@ -197,7 +197,13 @@ stepq_status stepq_pool_load(stepq_pool *pool, const int32_t *slot_ids, int32_t 
  * uniform row-width mixes S^T k and S^T q run on the matrix cores: each
  * row weight (k_i r_i / q_b, q_i r_i / q_b, scaled by a power of two per
  * tile) is split into binary16 hi + lo parts (22 significant bits), the
- * codes are exact in binary16, and the products accumulate in fp32.
+ * codes are exact in binary16, and the products accumulate in fp32.  The
+ * new code's field value y = code + 2^(b-1) is formed as (y - 1) / S,
+ * clamped to [0, 1] and scaled back (S = 256, 14 or 2 for 8-, 4- and 2-bit
+ * fields; exact scalings except for 4-bit fields, a few ulp of values at
+ * most 15), then rounded to nearest even.  With STEPQ_STEP_REFIT the gate
+ * term of the unrounded code may run on a matrix-core block, within one
+ * ulp of the fp32 FMA.
  * batch == 0 is a no-op. */
 stepq_status stepq_decode_step(stepq_pool *pool, const int32_t *slot_ids, int32_t batch, const void *q,
                                const void *k, const void *v, const void *alpha, const void *beta,
