@@ -22,11 +22,12 @@
 // denominator.  The new r' and c' overwrite the tile's scales; a zero
 // denominator keeps c_j.
 //
-// The same body also runs the single-axis baseline the paper compares
+// The generic body also runs the single-axis baseline the paper compares
 // against (Section 5.1: symmetric row-wise absmax INT-b): every step
 //     r'_i = max_j |X_ij| = (r_i / q_b) max_j c_j |y_ij|,   c'_j = 1,
 //     q'_ij = clip(round(y_ij c_j r_i / r'_i), -q_b, q_b),
-// i.e. pass 1 with a row maximum instead of a row sum, then pass 4.
+// i.e. pass 1 with a row maximum instead of a row sum, then pass 4; the
+// uniform layouts have a lean body of their own for it (stepq_rowmax.hip).
 #pragma once
 
 #include "stepq_device.h"
@@ -310,6 +311,8 @@ __device__ __forceinline__ void ld4(const float *p, float (&v)[4])
 template <bool BF16, bool DIAG, int M8, int M4, int M2, Refit MODE>
 __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx &t, RefitShared<128> &sh)
 {
+    // uniform layouts take the lean row-absmax body of stepq_rowmax.hip
+    static_assert(MODE == Refit::DualAxis, "the uniform refitting body runs the dual-axis fit");
     constexpr int M = M8 + M4 + M2;
     constexpr int NE = 4 * (M8 + 2 * M4 + 4 * M2);
     constexpr int X4 = 8 * M8, X2 = 8 * M8 + 16 * M4;
@@ -365,30 +368,7 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     }
     __syncthreads();
     if (tid < 128) refit_row<128, MODE>(sh, tid, tid, tid < X4 ? 8 : (tid < X2 ? 4 : 2), op.r, rr_out, a.pool.lv);
-    if constexpr (MODE == Refit::RowAbsmax) {
-        if (tid < 128) cc_out[tid] = 1.0f;
-    }
     __syncthreads();
-
-    if constexpr (MODE == Refit::RowAbsmax) {
-        // yh = y r / r', then q' = round(yh c_j): the column factors become 1
-#pragma unroll
-        for (int m = 0; m < M8; ++m) word_scale<8>(&Y[4 * m], sh.hrow, slice + 8 * m);
-#pragma unroll
-        for (int m = 0; m < M4; ++m) word_scale<4>(&Y[Y4 + 8 * m], sh.hrow, X4 + 2 * (slice + 8 * m));
-#pragma unroll
-        for (int m = 0; m < M2; ++m) word_scale<2>(&Y[Y2 + 16 * m], sh.hrow, X2 + 4 * (slice + 8 * m));
-#pragma unroll
-        for (int m = 0; m < M8; ++m)
-            cw.store_m(tid, m, word_requant<8>(&Y[4 * m], cc));
-#pragma unroll
-        for (int m = 0; m < M4; ++m)
-            cw.store_m(tid, M8 + m, word_requant<4>(&Y[Y4 + 8 * m], cc));
-#pragma unroll
-        for (int m = 0; m < M2; ++m)
-            cw.store_m(tid, M8 + M4 + m, word_requant<2>(&Y[Y2 + 16 * m], cc));
-        return;
-    }
 
     // pass 2: yh = y r / r' and the column maxima per width
     {
@@ -647,7 +627,11 @@ __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
 template <bool BF16, bool DIAG, Refit MODE>
 hipError_t launch_refit_any(const DecodeArgs &a, int layout, unsigned grid, hipStream_t s)
 {
-    if (a.pool.dv == 128) {
+    if constexpr (MODE == Refit::RowAbsmax) {
+        // uniform layouts are launched on the lean body (launch_decode_rowmax)
+        if (a.pool.dv == 128) hipLaunchKernelGGL((refit_kernel<128, BF16, 0, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+        else hipLaunchKernelGGL((refit_kernel<64, BF16, 0, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+    } else if (a.pool.dv == 128) {
         switch (layout) {
         case 1: hipLaunchKernelGGL((refit_kernel<128, BF16, 1, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a); break;
         case 2: hipLaunchKernelGGL((refit_kernel<128, BF16, 2, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a); break;
