@@ -49,7 +49,7 @@ template <int DV>
 struct RefitShared {
     DecodeShared<DV> d;
     union {
-        float rowp[kSlotTable][DV / 4];            // partials of sum_j c_j |y_ij| by row slot, per column lane
+        float rowp[kSlotTable][DV / 8];            // partials of sum_j c_j |y_ij| by row slot, per column-lane pair
         float4 cmax[256 / (DV / 4)][DV / 4];       // per slice column maxima of |yh| / q_b
     } u;
     float hrow[kSlotTable];                        // r_i / r'_i by row slot (0 for empty slots)
@@ -60,11 +60,16 @@ struct RefitShared {
     float gcol[DV];                                // c_j / c'_j
 };
 
-// One row partial of a thread (4 columns of one row slot).
-template <int DV>
+// One row partial of a thread (4 columns of one row slot), combined with
+// that of the neighbouring lane (the next 4 columns of the same row) before
+// it goes to LDS: sums for the dual-axis fit, maxima (of non-negative
+// values) for the row absmax.  Both lanes of a pair write the same value.
+template <int DV, Refit MODE>
 __device__ __forceinline__ void put_row_partial(RefitShared<DV> &sh, int x, int cg, float acc)
 {
-    sh.u.rowp[x][cg] = acc;
+    if constexpr (MODE == Refit::DualAxis) acc += dpp_term<0xB1, 0xF>(acc);    // quad_perm [1,0,3,2]
+    else acc = __uint_as_float(max(__float_as_uint(acc), dpp_bits<0xB1, 0xF>(__float_as_uint(acc))));
+    sh.u.rowp[x][cg >> 1] = acc;
 }
 
 // Row partial over the thread's 4 columns: sum_e c_e |y_e| (dual axis) or
@@ -100,7 +105,7 @@ __device__ __forceinline__ void refit_row(RefitShared<DV> &sh, int x, int p, int
     if constexpr (MODE == Refit::RowAbsmax) {
         float mx = 0.f;
 #pragma unroll
-        for (int l = 0; l < DV / 4; l += 4) {
+        for (int l = 0; l < DV / 8; l += 4) {
             const float4 v4 = *reinterpret_cast<const float4 *>(&sh.u.rowp[x][l]);
             mx = fmaxf(mx, fmaxf(fmaxf(v4.x, v4.y), fmaxf(v4.z, v4.w)));
         }
@@ -111,7 +116,7 @@ __device__ __forceinline__ void refit_row(RefitShared<DV> &sh, int x, int p, int
     }
     float sum = 0.f;
 #pragma unroll
-    for (int l = 0; l < DV / 4; l += 4) {
+    for (int l = 0; l < DV / 8; l += 4) {
         const float4 v4 = *reinterpret_cast<const float4 *>(&sh.u.rowp[x][l]);
         sum += (v4.x + v4.y) + (v4.z + v4.w);
     }
@@ -193,7 +198,7 @@ __device__ __forceinline__ void word_y_p(const uint32_t (&Ub)[4][4][2], int r0, 
             y[2] = fma_mix<0>(al, Ub[2][g][h], a_s * bc[2]);
             y[3] = fma_mix<0>(al, Ub[3][g][h], a_s * bc[3]);
         }
-        put_row_partial<128>(sh, x0 + s, cg, row_partial<MODE>(y, cc));
+        put_row_partial<128, MODE>(sh, x0 + s, cg, row_partial<MODE>(y, cc));
     }
 }
 
@@ -224,7 +229,7 @@ __device__ __forceinline__ void refit_y_mfma(const uint32_t (&Ub)[4][4][2], Refi
         }
 #pragma unroll
         for (int k = 0; k < 4; ++k)
-            put_row_partial<128>(sh, thread_row_slot<M8, M4>(4 * g + k, slice), cg,
+            put_row_partial<128, MODE>(sh, thread_row_slot<M8, M4>(4 * g + k, slice), cg,
                                  row_partial<MODE>(&Y[4 * (4 * g + k)], cc));
     }
 }
@@ -500,7 +505,7 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
         float Y[16];
         gen_word_y<B, DIAG, DV>(w[m], sh.d, gr.x0, t.alpha, bc, Y);
 #pragma unroll
-        for (int s = 0; s < 8 / B; ++s) put_row_partial<DV>(sh, gr.x0 + s, cg, row_partial<MODE>(&Y[4 * s], cc));
+        for (int s = 0; s < 8 / B; ++s) put_row_partial<DV, MODE>(sh, gr.x0 + s, cg, row_partial<MODE>(&Y[4 * s], cc));
     });
     __syncthreads();
     if (tid < kSlotTable) {
