@@ -499,7 +499,7 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
     ld4(&sh.ccol[4 * cg], cc);
     pivot_update(t, slice, cg, pr, sh.d, bc);      // pivot rows take no part in the fits
 
-    // pass 1: row partials straight to LDS (each (lane, slot) has one writer)
+    // pass 1: row partials straight to LDS (one entry per lane pair and slot)
     each_word<DV>(t, slice, [&](auto bw, const GroupRows &gr, int m) {
         constexpr int B = decltype(bw)::value;
         float Y[16];
