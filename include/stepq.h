@@ -194,10 +194,13 @@ stepq_status stepq_pool_load(stepq_pool *pool, const int32_t *slot_ids, int32_t 
  * in act_dtype (arrays [batch][Hqk][d_k], [batch][Hv][d_v], [batch][Hv]),
  * writes o[b][h][:] (fp32, [batch][Hv][d_v]) and rewrites its codes in
  * place.  The arithmetic is fp32, except that in the compiled bodies of the
- * uniform row-width mixes S^T k and S^T q run on the matrix cores: each
- * row weight (k_i r_i / q_b, q_i r_i / q_b, scaled by a power of two per
- * tile) is split into binary16 hi + lo parts (22 significant bits), the
- * codes are exact in binary16, and the products accumulate in fp32.  The
+ * uniform row-width mixes, and of heads at d_k = d_v = 128 whose integer
+ * rows are 8- and 4-bit in any split with at most 8 FP16 pivot rows (the
+ * per-row maps of a row-unit calibration), S^T k and S^T q run on the
+ * matrix cores: each row weight (k_i r_i / q_b, q_i r_i / q_b, scaled by a
+ * power of two per tile) is split into binary16 hi + lo parts (22
+ * significant bits), the codes are exact in binary16, and the products
+ * accumulate in fp32.  The
  * new code's field value y = code + 2^(b-1) is formed as (y - 1) / S,
  * clamped to [0, 1] and scaled back (S = 256, 14 or 2 for 8-, 4- and 2-bit
  * fields; exact scalings except for 4-bit fields, a few ulp of values at

@@ -167,42 +167,6 @@ __device__ __forceinline__ void decode_generic(const DecodeArgs &a, const TileCt
     }
 }
 
-// Column E of the row-mix thread's two sums: one chain over the word groups
-// and their slot views (one accumulator live), written to LDS unscaled.
-// The slot-0 views of the group holding the width boundary (vb) come in
-// formed; the other views are formed again for each column rather than kept.
-template <int E>
-__device__ __forceinline__ void rowmix_column(const DecodeShared<128> &sh, const uint32_t (&w)[16],
-                                              const uint32_t (&vb)[4], int slice, int cg, int g8, int ng, int ek,
-                                              int eq, float *redK, float *redQ)
-{
-    f32x4 d = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        if (32 * j >= ng) break;
-        if (32 * j + 32 <= g8) {
-            // 8-bit words only: their bytes are the codes
-            const uint32_t v[4] = {w[4 * j], w[4 * j + 1], w[4 * j + 2], w[4 * j + 3]};
-            d = mfma_view<E>(sh.aopv[slice][j][0], v, cg, d);
-        } else {
-            uint32_t v[4];
-            if (32 * j >= g8) {
-#pragma unroll
-                for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 0);
-                d = mfma_view<E>(sh.aopv[slice][j][0], v, cg, d);
-            } else {
-                d = mfma_view<E>(sh.aopv[slice][j][0], vb, cg, d);    // the group of the width boundary
-            }
-#pragma unroll
-            for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 1);
-            d = mfma_view<E>(sh.aopv[slice][j][1], v, cg, d);
-        }
-    }
-    redK[E] = __builtin_amdgcn_ldexpf(d[0] + d[1], -ek);
-    redQ[E] = __builtin_amdgcn_ldexpf(d[2] + d[3], -eq);
-    __builtin_amdgcn_sched_barrier(0);
-}
-
 // A head at d = 128 whose integer rows are 8- and 4-bit in any split, in the
 // compact layout, with up to kCompactPivots FP16 pivot rows (the per-row
 // maps of a row-unit calibration).  Groups below hi.g8 are 8-bit, the rest
@@ -228,46 +192,7 @@ __device__ __forceinline__ void decode_rowmix(const DecodeArgs &a, const TileCtx
     PivotRegs<128, kCompactPivots> pr;
     pivot_load<128, kCompactPivots>(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    // v_j waits in LDS for the column phase (c_j is kept there for the pivot
-    // rows), so neither is held in registers through the row sums
-    if (tid < 128) sh.bcol[tid] = op.v;
-    const float kappa = uniform_f(row_constants<DIAG, 128, true>(t.hi, 128, t.alpha, t.beta, op, sh, a.pool.lv));
-    int ek, eq;
-    row_operands_rowmix(t.hi, sh, ek, eq);
-
-    float *redK = &sh.red[0][slice][cg].x, *redQ = &sh.red[1][slice][cg].x;
-    // slot-0 views of the word group holding the width boundary (if any),
-    // formed once: there the width changes from one slice to the next
-    uint32_t vb[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        if ((g8 >> 5) == j && (g8 & 31) != 0) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                vb[k] = slice + 8 * (4 * j + k) < g8 ? w[4 * j + k] : slot_top<4>(w[4 * j + k], 0);
-        }
-    rowmix_column<0>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
-    rowmix_column<1>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
-    rowmix_column<2>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
-    rowmix_column<3>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
-    // pivot row p = slice (kCompactPivots = 8 slices): its share of the
-    // partials, added to this thread's own (the column phase multiplies by c_j)
-    static_assert(PivotRegs<128, kCompactPivots>::M == 1, "one pivot row per thread");
-    if (slice < t.hi.n16) {
-        const float4 c4 = *reinterpret_cast<const float4 *>(&sh.cpiv[4 * cg]);
-        const uint32_t lo = pr.v[0].x, hi = pr.v[0].y;
-        const float sv[4] = {half_lo(lo) * __builtin_amdgcn_rcpf(c4.x), half_hi(lo) * __builtin_amdgcn_rcpf(c4.y),
-                             half_lo(hi) * __builtin_amdgcn_rcpf(c4.z), half_hi(hi) * __builtin_amdgcn_rcpf(c4.w)};
-        const float4 kp = sh.pvc[slice];
-        float4 &rk = sh.red[0][slice][cg];
-        rk = make_float4(fmaf(kp.x, sv[0], rk.x), fmaf(kp.x, sv[1], rk.y), fmaf(kp.x, sv[2], rk.z),
-                         fmaf(kp.x, sv[3], rk.w));
-        float4 &rq = sh.red[1][slice][cg];
-        rq = make_float4(fmaf(kp.y, sv[0], rq.x), fmaf(kp.y, sv[1], rq.y), fmaf(kp.y, sv[2], rq.z),
-                         fmaf(kp.y, sv[3], rq.w));
-    }
-
-    column_sums<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, sh.cpiv[tid & 127], sh.bcol[tid & 127]);
+    rowmix_sums<DIAG, true>(a, t, sh, w, pr, op, g8, ng);
 
     const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};

@@ -261,10 +261,13 @@ bool decode_body_runs(int code, const HeadInfo &hi, int dk)
     return false;
 }
 
-bool refit_body_runs(int code, const HeadInfo &hi)
+bool refit_body_runs(int code, const HeadInfo &hi, int dk)
 {
     const int L = static_cast<int>(hi.layout);
     if (compiled(code)) return L == code;    // whole FP16 heads take their decode body in every mode
+    // the row-mix class has a refitting body of its own (the dual-axis fit;
+    // the row-absmax step takes the generic body, which runs these heads too)
+    if (code == kRowMix) return rowmix_head(hi, dk);
     // every other code runs the generic refitting body, which reads the
     // head's own record (the tight layout, or a padded uniform mix)
     return !compiled(L);
@@ -305,7 +308,7 @@ bool check_plan(const LaunchPlan &plan, const std::vector<HeadInfo> &heads, int 
                 return fail_check(err, at + "layout differs from the single launch's");
             if (tb != 0 && (hi.tile_bytes != tb || hi.tile_off != static_cast<uint64_t>(tb) * h))
                 return fail_check(err, at + "not where the body's fixed tile size puts it");
-            if (!decode_body_runs(plan.layout, hi, dk) || !refit_body_runs(plan.layout, hi))
+            if (!decode_body_runs(plan.layout, hi, dk) || !refit_body_runs(plan.layout, hi, dk))
                 return fail_check(err, at + "the single launch's body does not run it");
         }
         if (plan.layout == 0 && dv == 128) return fail_check(err, "a generic pool at d_v = 128 needs a head list");
@@ -341,7 +344,7 @@ bool check_plan(const LaunchPlan &plan, const std::vector<HeadInfo> &heads, int 
             const HeadInfo &hi = heads[plan.order[e].h];
             if (!decode_body_runs(plan.cls_code[c], hi, dk))
                 return fail_check(err, at + "its decode body does not run head " + std::to_string(plan.order[e].h));
-            if (!refit_body_runs(plan.cls_code[c], hi))
+            if (!refit_body_runs(plan.cls_code[c], hi, dk))
                 return fail_check(err, at + "its refitting body does not run head " + std::to_string(plan.order[e].h));
         }
     }

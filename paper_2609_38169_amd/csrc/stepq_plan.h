@@ -44,7 +44,7 @@ void plan_launches(const std::vector<HeadInfo> &heads, int dk, int dv, LaunchPla
 // Whether the frozen-step decode body of launch code `code` handles head
 // `hi`, and the same for the refitting bodies (refit and row-absmax).
 bool decode_body_runs(int code, const HeadInfo &hi, int dk);
-bool refit_body_runs(int code, const HeadInfo &hi);
+bool refit_body_runs(int code, const HeadInfo &hi, int dk);
 
 // Tile size that the compiled body of layout code L (1 .. kF16HeadLayout)
 // assumes for every head when it runs without a head list; 0 otherwise.

@@ -596,6 +596,184 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
     });
 }
 
+// ---- row-mix heads (kRowMix: 8- and 4-bit rows in any split, at most
+// kCompactPivots FP16 pivot rows, d = 128: the per-row maps of a row-unit
+// calibration).  The first half is the frozen row-mix body's (rowmix_sums:
+// both sums over rows on the matrix cores).  Then, as in the uniform body, y
+// stays in registers through the four passes, indexed by word-step: Y[m]
+// holds word-step m's row (an 8-bit word) or the slot-0 row of its 4-bit
+// word, at most 64 values; the slot-1 row of a 4-bit word is formed again
+// from the packed word in each pass after the first.  The per-element
+// arithmetic is the generic body's (gen_word_y, word_fit, word_requant) in
+// the same order, so the two bodies give the same codes and scales.
+// The width of a word-step is a per-lane test (it differs between slices in
+// at most one word-step); lanes past the head's last group (in the last
+// word-step) take no part in the sums and store nothing.
+
+// y of the 4 fields of view W (each at the top of its byte) of row slot x,
+// as gen_word_y forms it.
+template <bool DIAG>
+__device__ __forceinline__ void rm_row_y(uint32_t W, const DecodeShared<128> &d, int x, float al_w,
+                                         const float (&bc)[4], float *y)
+{
+    const float a_s = d.av[x];
+    const float al = DIAG ? d.al[x] : al_w;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) y[e] = fmaf(al, sbyte(W, e), a_s * bc[e]);
+}
+
+// Calls f8(g) for an 8-bit word-step of group g and f4(g) for a 4-bit one
+// whose group holds codes, over the thread's word-steps m (group g = slice
+// + 8 m), for every m while 8 m < ng.
+template <class F8, class F4>
+__device__ __forceinline__ void rm_each_step(int slice, int g8, int ng, F8 &&f8, F4 &&f4)
+{
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+        if (8 * m >= ng) break;
+        const int g = slice + 8 * m;
+        if (g < g8) f8(m, g);
+        else if (g < ng) f4(m, g);
+    }
+}
+
+template <bool BF16, bool DIAG>
+__device__ __forceinline__ void refit_rowmix(const DecodeArgs &a, const TileCtx &t, RefitShared<128> &sh)
+{
+    constexpr Refit DA = Refit::DualAxis;
+    const int tid = threadIdx.x;
+    const int cg = tid & 31, slice = tid >> 5;
+    const int g8 = __builtin_amdgcn_readfirstlane(static_cast<int>(t.hi.g8));
+    const int ng = __builtin_amdgcn_readfirstlane(static_cast<int>(t.hi.groups));
+    float *rr_out = const_cast<float *>(t.rr);
+    float *cc_out = const_cast<float *>(t.cc);
+    // the buffer covers the codes region only (piv_off = 128 ng): words of
+    // groups past the head's last read 0
+    const CodeWords cw(t.codes, t.hi.piv_off);
+    uint32_t w[16];
+#pragma unroll
+    for (int m = 0; m < 16; ++m) w[m] = 8 * m < ng ? cw.load(tid + 256 * m) : 0u;
+    PivotRegs<128, kCompactPivots> pr;
+    pivot_load<128, kCompactPivots>(t, slice, cg, pr);
+    const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
+    if (tid < 128) {
+        sh.ccol[tid] = op.c;
+        sh.wphys[tid] = a.pool.roww[t.h * 128 + tid];
+    }
+    rowmix_sums<DIAG, false>(a, t, sh.d, w, pr, op, g8, ng);
+
+    float bc[4], cc[4];
+    ld4(&sh.d.bcol[4 * cg], bc);
+    ld4(&sh.ccol[4 * cg], cc);
+    pivot_update<128, kCompactPivots>(t, slice, cg, pr, sh.d, bc);    // pivot rows take no part in the fits
+    const float al8 = t.alpha, al4 = t.alpha * (1.0f / 16.0f);
+
+    // pass 1: y on the old scales, the row partials (row slot g of an 8-bit
+    // group, 2 g - g8 and the next of a 4-bit one)
+    float Y[16][4];
+    rm_each_step(
+        slice, g8, ng,
+        [&](int m, int g) {
+            rm_row_y<DIAG>(w[m], sh.d, g, al8, bc, Y[m]);
+            put_row_partial<128, DA>(sh, g, cg, row_partial<DA>(Y[m], cc));
+        },
+        [&](int m, int g) {
+            const int x0 = 2 * g - g8;
+            float y1[4];
+            rm_row_y<DIAG>(slot_top<4>(w[m], 0), sh.d, x0, al4, bc, Y[m]);
+            rm_row_y<DIAG>(slot_top<4>(w[m], 1), sh.d, x0 + 1, al4, bc, y1);
+            put_row_partial<128, DA>(sh, x0, cg, row_partial<DA>(Y[m], cc));
+            put_row_partial<128, DA>(sh, x0 + 1, cg, row_partial<DA>(y1, cc));
+        });
+    __syncthreads();
+    if (tid < kSlotTable) {
+        int bw;
+        const int p = slot_row(t.hi, tid, bw);
+        if (p >= 0) {
+            refit_row<128, DA>(sh, tid, p, bw, sh.d.sr[p], rr_out, a.pool.lv);
+        } else {
+            sh.hrow[tid] = 0.f;
+            sh.wrow[tid] = 0.f;
+        }
+    }
+    __syncthreads();
+
+    // yh of the slot-1 row of the 4-bit word of word-step m, group g
+    auto slot1_yh = [&](int m, int g, float (&y1)[4]) {
+        const int x1 = 2 * g - g8 + 1;
+        rm_row_y<DIAG>(slot_top<4>(w[m], 1), sh.d, x1, al4, bc, y1);
+        const float h = sh.hrow[x1];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) y1[e] *= h;
+    };
+
+    // pass 2: yh = y r / r' (in place for the kept rows) and the column
+    // maxima per width
+    {
+        float mx8[4] = {0.f, 0.f, 0.f, 0.f}, mx4[4] = {0.f, 0.f, 0.f, 0.f};
+        const float mx2[4] = {0.f, 0.f, 0.f, 0.f};
+        rm_each_step(
+            slice, g8, ng,
+            [&](int m, int g) {
+                const float h = sh.hrow[g];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    Y[m][e] *= h;
+                    mx8[e] = fmaxf(mx8[e], fabsf(Y[m][e]));
+                }
+            },
+            [&](int m, int g) {
+                const float h = sh.hrow[2 * g - g8];
+                float y1[4];
+                slot1_yh(m, g, y1);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    Y[m][e] *= h;
+                    mx4[e] = fmaxf(mx4[e], fabsf(Y[m][e]));
+                    mx4[e] = fmaxf(mx4[e], fabsf(y1[e]));
+                }
+            });
+        sh.u.cmax[slice][cg] = width_max(mx8, mx4, mx2);
+    }
+    __syncthreads();
+    if (tid < 128) refit_colmax<128>(sh, tid);
+    __syncthreads();
+
+    // pass 3: fixed codes and the least-squares sums
+    {
+        float ec[4];
+        ld4(&sh.ecol[4 * cg], ec);
+        float num[4] = {0.f, 0.f, 0.f, 0.f}, den[4] = {0.f, 0.f, 0.f, 0.f};
+        rm_each_step(
+            slice, g8, ng, [&](int m, int g) { word_fit<8>(Y[m], sh.wrow, g, ec, num, den); },
+            [&](int m, int g) {
+                float y8[8];
+                slot1_yh(m, g, *reinterpret_cast<float(*)[4]>(&y8[4]));
+#pragma unroll
+                for (int e = 0; e < 4; ++e) y8[e] = Y[m][e];
+                word_fit<4>(y8, sh.wrow, 2 * g - g8, ec, num, den);
+            });
+        sh.d.red[0][slice][cg] = make_float4(num[0], num[1], num[2], num[3]);
+        sh.d.red[1][slice][cg] = make_float4(den[0], den[1], den[2], den[3]);
+    }
+    __syncthreads();
+    if (tid < 128) refit_colfit<128>(sh, tid, cc_out);
+    __syncthreads();
+
+    // pass 4: requantize on the new scales, store in place
+    float gc[4];
+    ld4(&sh.gcol[4 * cg], gc);
+    rm_each_step(
+        slice, g8, ng, [&](int m, int) { cw.store(tid + 256 * m, word_requant<8>(Y[m], gc)); },
+        [&](int m, int g) {
+            float y8[8];
+            slot1_yh(m, g, *reinterpret_cast<float(*)[4]>(&y8[4]));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) y8[e] = Y[m][e];
+            cw.store(tid + 256 * m, word_requant<4>(y8, gc));
+        });
+}
+
 template <int DV, bool BF16, int LAYOUT, bool DIAG, Refit MODE>
 __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
 {
@@ -603,7 +781,8 @@ __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
     const PoolView &P = a.pool;
     TileCtx t;
     uint32_t tile_bytes = 0;
-    if constexpr (DV == 128 && LAYOUT > 0) {
+    constexpr bool UNIFORM = DV == 128 && LAYOUT > 0 && LAYOUT <= kNumUniformLayouts;
+    if constexpr (UNIFORM) {
         constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
         tile_bytes = 1024u * (u.m8 + u.m4 + u.m2 + 1);
     }
@@ -611,7 +790,7 @@ __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
     const int slot = a.slot_ids[t.b];
     t.alpha = DIAG ? 1.0f : act_ld<BF16>(a.alpha, t.tile);
     t.beta = act_ld<BF16>(a.beta, t.tile);
-    if constexpr (DV == 128 && LAYOUT > 0) {
+    if constexpr (UNIFORM) {
         constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
         constexpr uint32_t r_off = 1024u * (u.m8 + u.m4 + u.m2);
         uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.off;
@@ -625,7 +804,12 @@ __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
         t.codes = reinterpret_cast<uint32_t *>(rec);
         t.rr = reinterpret_cast<const float *>(rec + t.hi.r_off);
         t.cc = t.rr + P.dk;
-        refit_generic<BF16, DIAG, DV, MODE>(a, t, sh);
+        if constexpr (DV == 128 && LAYOUT == kRowMix) {
+            static_assert(MODE == Refit::DualAxis, "the row-mix refitting body runs the dual-axis fit");
+            refit_rowmix<BF16, DIAG>(a, t, sh);
+        } else {
+            refit_generic<BF16, DIAG, DV, MODE>(a, t, sh);
+        }
     }
 }
 
@@ -643,6 +827,9 @@ hipError_t launch_refit_any(const DecodeArgs &a, int layout, unsigned grid, hipS
         case 3: hipLaunchKernelGGL((refit_kernel<128, BF16, 3, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a); break;
         case 4: hipLaunchKernelGGL((refit_kernel<128, BF16, 4, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a); break;
         case 5: hipLaunchKernelGGL((refit_kernel<128, BF16, 5, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a); break;
+        case kRowMix:
+            hipLaunchKernelGGL((refit_kernel<128, BF16, kRowMix, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+            break;
         default: hipLaunchKernelGGL((refit_kernel<128, BF16, 0, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a); break;
         }
     } else {

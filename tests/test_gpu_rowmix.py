@@ -5,7 +5,8 @@ KDA, fp32 and bf16 activations, against the fp64 oracle through the C ABI.
 
 No uniform mix holds these heads, so the frozen step runs them on the
 row-mix body, whose matrix-core blocks read each word through its slot
-views.  The split between the 8- and 4-bit row groups is swept across every
+views, and the refit on the row-mix refitting body (the same first half,
+then the values kept in registers by word-step through the fits).  The split between the 8- and 4-bit row groups is swept across every
 position inside a word-step (the groups of one word-step then have
 different widths from slice to slice) and across the boundaries of the
 4-word groups that form the blocks' K dimension; odd 4-bit row counts leave
@@ -185,15 +186,10 @@ def test_rowmix_lockstep_steps():
         PT.compare_out(o.cpu().numpy().reshape(-1, 128), o_ref)
 
 
-@pytest.mark.timeout(900)
-@pytest.mark.parametrize("kda", [False, True])
-def test_rowmix_calibrated_pool_b512_every_tile(kda):
+def _calibrated_row_map():
     """The row-unit calibrated map that ``bench.py --calibrated row`` times
     (per-head 8/4-bit splits, 24 FP16 pivot rows, from the calibration
-    pipeline on the workload's own draws) at full pool_b512 size, in the
-    same launch configuration, with the scalar gate and with channel-wise
-    (KDA) gates: every tile lockstep with the oracle over several frozen
-    steps."""
+    pipeline on the workload's own draws) and its row-impact factors."""
     from paper_2609_38169_amd import workloads as W
     from paper_2609_38169_amd.calibrate import calibrate
     w = W.workload(2)
@@ -207,4 +203,30 @@ def test_rowmix_calibrated_pool_b512_every_tile(kda):
     n16 = (bits == 16).sum(1)
     assert n16.sum() == 24 and n16.max() <= 8 and not (bits == 2).any()
     _say(f"row-unit calibrated pool_b512: {(bits == 8).sum()} rows @8, {(bits == 4).sum()} @4, 24 pivots")
-    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, row_weight=cal.row_weight, say=_say, bits=bits, kda=kda)
+    return w, bits, cal.row_weight
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("kda", [False, True])
+def test_rowmix_calibrated_pool_b512_every_tile(kda):
+    """The row-unit calibrated map at full pool_b512 size, in the launch
+    configuration ``bench.py --calibrated row`` times, with the scalar gate
+    and with channel-wise (KDA) gates: every tile lockstep with the oracle
+    over several frozen steps."""
+    w, bits, row_weight = _calibrated_row_map()
+    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, row_weight=row_weight, say=_say, bits=bits, kda=kda)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("kda,levels", [(True, 1), (False, 0)])
+def test_rowmix_calibrated_refit_pool_b512_every_tile(kda, levels):
+    """The decode step with the online dual-axis refit on the row-unit
+    calibrated map at full pool_b512 size (the row-mix refitting body), as
+    ``bench.py --calibrated row --refit`` times it: channel-wise gates on the
+    2^(8-b) q codebook (the paper's KDA setting: row-level allocation, FP16
+    pivot rows, the shared column fit over the mixed-width integer rows) and
+    the scalar gate on q / q_b levels.  Every tile lockstep with the oracle
+    over several steps."""
+    w, bits, row_weight = _calibrated_row_map()
+    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, refit=True, row_weight=row_weight, say=_say, bits=bits,
+                    kda=kda, levels=levels)
