@@ -915,13 +915,60 @@ __device__ __forceinline__ void rowmix_column(const DecodeShared<128> &sh, const
     __builtin_amdgcn_sched_barrier(0);
 }
 
+// All four columns of the row-mix thread's two sums in one pass over the
+// word groups (four accumulators live): each group's slot views are formed
+// once rather than once per column.  For bodies whose register peak lies
+// after the column phase (the refitting body).
+__device__ __forceinline__ void rowmix_columns4(const DecodeShared<128> &sh, const uint32_t (&w)[16],
+                                                const uint32_t (&vb)[4], int slice, int cg, int g8, int ng, int ek,
+                                                int eq, float *redK, float *redQ)
+{
+    f32x4 d0 = {0.f, 0.f, 0.f, 0.f}, d1 = d0, d2 = d0, d3 = d0;
+    auto all = [&](const _Float16 (&A)[4][4], const uint32_t (&v)[4]) {
+        d0 = mfma_view<0>(A, v, cg, d0);
+        d1 = mfma_view<1>(A, v, cg, d1);
+        d2 = mfma_view<2>(A, v, cg, d2);
+        d3 = mfma_view<3>(A, v, cg, d3);
+    };
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (32 * j >= ng) break;
+        if (32 * j + 32 <= g8) {
+            const uint32_t v[4] = {w[4 * j], w[4 * j + 1], w[4 * j + 2], w[4 * j + 3]};
+            all(sh.aopv[slice][j][0], v);
+        } else {
+            uint32_t v[4];
+            if (32 * j >= g8) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 0);
+                all(sh.aopv[slice][j][0], v);
+            } else {
+                all(sh.aopv[slice][j][0], vb);    // the group of the width boundary
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 1);
+            all(sh.aopv[slice][j][1], v);
+        }
+    }
+    redK[0] = __builtin_amdgcn_ldexpf(d0[0] + d0[1], -ek);
+    redQ[0] = __builtin_amdgcn_ldexpf(d0[2] + d0[3], -eq);
+    redK[1] = __builtin_amdgcn_ldexpf(d1[0] + d1[1], -ek);
+    redQ[1] = __builtin_amdgcn_ldexpf(d1[2] + d1[3], -eq);
+    redK[2] = __builtin_amdgcn_ldexpf(d2[0] + d2[1], -ek);
+    redQ[2] = __builtin_amdgcn_ldexpf(d2[2] + d2[3], -eq);
+    redK[3] = __builtin_amdgcn_ldexpf(d3[0] + d3[1], -ek);
+    redQ[3] = __builtin_amdgcn_ldexpf(d3[2] + d3[3], -eq);
+}
+
 // The first half of the row-mix bodies (decode_rowmix and the refitting
 // body's refit_rowmix): row constants (divided by the widths' clamp scales
 // when SCALED, the form the frozen-scale requantization works in), both sums
 // over rows on the matrix cores, the pivot rows' share, and the column
 // phase: o is written and delta_j / c_j is left in sh.bcol.  w: the
 // thread's 16 code words (0 past the head's last group); pr: its pivot row.
-template <bool DIAG, bool SCALED>
+// ALLCOLS: the four columns in one pass (rowmix_columns4), else one at a
+// time (fewer registers).
+template <bool DIAG, bool SCALED, bool ALLCOLS = false>
 __device__ __forceinline__ void rowmix_sums(const DecodeArgs &a, const TileCtx &t, DecodeShared<128> &sh,
                                             const uint32_t (&w)[16], const PivotRegs<128, kCompactPivots> &pr,
                                             const RowColOps &op, int g8, int ng)
@@ -946,10 +993,14 @@ __device__ __forceinline__ void rowmix_sums(const DecodeArgs &a, const TileCtx &
             for (int k = 0; k < 4; ++k)
                 vb[k] = slice + 8 * (4 * j + k) < g8 ? w[4 * j + k] : slot_top<4>(w[4 * j + k], 0);
         }
-    rowmix_column<0>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
-    rowmix_column<1>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
-    rowmix_column<2>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
-    rowmix_column<3>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+    if constexpr (ALLCOLS) {
+        rowmix_columns4(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+    } else {
+        rowmix_column<0>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+        rowmix_column<1>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+        rowmix_column<2>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+        rowmix_column<3>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+    }
     // pivot row p = slice (kCompactPivots = 8 slices): its share of the
     // partials, added to this thread's own (the column phase multiplies by c_j)
     static_assert(PivotRegs<128, kCompactPivots>::M == 1, "one pivot row per thread");

@@ -599,7 +599,8 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
 // ---- row-mix heads (kRowMix: 8- and 4-bit rows in any split, at most
 // kCompactPivots FP16 pivot rows, d = 128: the per-row maps of a row-unit
 // calibration).  The first half is the frozen row-mix body's (rowmix_sums:
-// both sums over rows on the matrix cores).  Then, as in the uniform body, y
+// both sums over rows on the matrix cores, here all four columns in one
+// pass: the register peak comes later).  Then, as in the uniform body, y
 // stays in registers through the four passes, indexed by word-step: Y[m]
 // holds word-step m's row (an 8-bit word) or the slot-0 row of its 4-bit
 // word, at most 64 values; the slot-1 row of a 4-bit word is formed again
@@ -607,8 +608,9 @@ __device__ __forceinline__ void refit_generic(const DecodeArgs &a, const TileCtx
 // arithmetic is the generic body's (gen_word_y, word_fit, word_requant) in
 // the same order, so the two bodies give the same codes and scales.
 // The width of a word-step is a per-lane test (it differs between slices in
-// at most one word-step); lanes past the head's last group (in the last
-// word-step) take no part in the sums and store nothing.
+// at most one word-step): measured faster than a uniform branch for the
+// word-steps wholly of one width.  Lanes past the head's last group (in the
+// last word-step) take no part in the sums and store nothing.
 
 // y of the 4 fields of view W (each at the top of its byte) of row slot x,
 // as gen_word_y forms it.
@@ -660,7 +662,7 @@ __device__ __forceinline__ void refit_rowmix(const DecodeArgs &a, const TileCtx 
         sh.ccol[tid] = op.c;
         sh.wphys[tid] = a.pool.roww[t.h * 128 + tid];
     }
-    rowmix_sums<DIAG, false>(a, t, sh.d, w, pr, op, g8, ng);
+    rowmix_sums<DIAG, false, true>(a, t, sh.d, w, pr, op, g8, ng);
 
     float bc[4], cc[4];
     ld4(&sh.d.bcol[4 * cg], bc);
