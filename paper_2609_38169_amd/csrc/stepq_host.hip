@@ -348,8 +348,11 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     };
     hipError_t e = hipSuccess;
     const stepq::LaunchPlan &plan = p->plan;
-    if (plan.mixed_code != 0 && !(flags & (STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX))) {
-        // uniform heads share one launch with compact generic and whole FP16 heads
+    const bool refit_multi = (flags & STEPQ_STEP_REFIT) && plan.mixed_code == stepq::kMultiUniform;
+    if ((plan.mixed_code != 0 && !(flags & (STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX))) || refit_multi) {
+        // uniform heads share one launch with compact generic and whole FP16
+        // heads; with the refit, heads of several uniform layouts and whole
+        // FP16 heads share one launch of the refitting bodies
         a.head_list = p->d_head_order;
         a.n_heads = p->Hv;
         a.div_heads = fast_div(static_cast<uint32_t>(p->Hv));

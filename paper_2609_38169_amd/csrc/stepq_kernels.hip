@@ -225,95 +225,6 @@ __device__ __forceinline__ void decode_rowmix(const DecodeArgs &a, const TileCtx
     }
 }
 
-// A head whose every row is an FP16 pivot (d = 128).  Thread (slice, cg)
-// holds columns 4 cg .. 4 cg + 3 of rows p = slice + 8 m as two binary16
-// pairs; the FMAs read the halves directly (v_fma_mix), so nothing is
-// unpacked.  The column phase runs with unit column factors.  Each value
-// becomes X = d_i S + beta k_i delta_j rounded to binary16 (nearest even),
-// stored in place; r and c are left alone (no integer rows to fit).
-template <bool BF16, bool DIAG>
-__device__ __forceinline__ void decode_f16head(const DecodeArgs &a, const TileCtx &t, DecodeShared<128> &sh)
-{
-    const int tid = threadIdx.x;
-    const int cg = tid & 31, slice = tid >> 5;
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(t.codes, 0, 128 * 256, 0x00020000);
-    // one 8-byte access per row and thread: a half-wavefront covers a whole
-    // 256-byte row
-    u32x2 S[16];
-#pragma unroll
-    for (int m = 0; m < 16; ++m)
-        S[m] = __builtin_amdgcn_raw_buffer_load_b64(rs, (slice + 8 * m) * 256 + 8 * cg, 0, CodeWords::kLoad);
-    // k, q, the gate and the permutation by row, v by column (the r and c
-    // slots of the record are not read)
-    const PoolView &P = a.pool;
-    float vj = 0.f;
-    int perm = 0;
-    if (tid < 128) {
-        const size_t off = (static_cast<size_t>(t.b) * P.Hqk + t.hq) * 128 + tid;
-        sh.sk[tid] = act_ld<BF16>(a.k, off);
-        sh.sq[tid] = act_ld<BF16>(a.q, off);
-        if constexpr (DIAG) sh.sd[tid] = act_ld<BF16>(a.alpha, static_cast<size_t>(t.tile) * 128 + tid);
-        perm = P.perm[t.h * 128 + tid];
-        vj = act_ld<BF16>(a.v, static_cast<size_t>(t.tile) * 128 + tid);
-    }
-    __syncthreads();
-    float kq = 0.f;
-    if (tid < 128) {
-        // physical row p = tid holds logical row perm[p]
-        const int i = perm;
-        const float ki = sh.sk[i], qi = sh.sq[i];
-        const float di = DIAG ? sh.sd[i] : 1.0f;       // the scalar gate is applied with the columns
-        sh.kq[tid] = make_float2(ki * di, qi * di);
-        sh.av[tid] = t.beta * ki;
-        if constexpr (DIAG) sh.al[tid] = di;
-        kq = qi * ki;
-    }
-    kq = wave_sum(kq);
-    if ((tid & 63) == 0) sh.kap[tid >> 6] = kq;
-    __syncthreads();
-    const float kappa = (sh.kap[0] + sh.kap[1]) + (sh.kap[2] + sh.kap[3]);
-
-    float acK[4] = {0.f, 0.f, 0.f, 0.f}, acQ[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int m = 0; m < 16; ++m) {
-        const float2 c = sh.kq[slice + 8 * m];
-        acK[0] = fma_mix<0>(c.x, S[m].x, acK[0]);
-        acQ[0] = fma_mix<0>(c.y, S[m].x, acQ[0]);
-        acK[1] = fma_mix<1>(c.x, S[m].x, acK[1]);
-        acQ[1] = fma_mix<1>(c.y, S[m].x, acQ[1]);
-        acK[2] = fma_mix<0>(c.x, S[m].y, acK[2]);
-        acQ[2] = fma_mix<0>(c.y, S[m].y, acQ[2]);
-        acK[3] = fma_mix<1>(c.x, S[m].y, acK[3]);
-        acQ[3] = fma_mix<1>(c.y, S[m].y, acQ[3]);
-    }
-    column_phase<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, acK, acQ, 1.0f, vj);
-    if (a.f16_c_one && tid < 128) const_cast<float *>(t.cc)[tid] = 1.0f;
-
-    const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);   // delta_j
-    const float dl[4] = {b4.x, b4.y, b4.z, b4.w};
-#pragma unroll
-    for (int m = 0; m < 16; ++m) {
-        const int p = slice + 8 * m;
-        const float bk = sh.av[p];
-        const float dg = DIAG ? sh.al[p] : t.alpha;
-        const float x0 = fmaf(bk, dl[0], dg * half_lo(S[m].x)), x1 = fmaf(bk, dl[1], dg * half_hi(S[m].x));
-        const float x2 = fmaf(bk, dl[2], dg * half_lo(S[m].y)), x3 = fmaf(bk, dl[3], dg * half_hi(S[m].y));
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{pack_halves(x0, x1), pack_halves(x2, x3)}, rs, p * 256 + 8 * cg, 0,
-                                              CodeWords::kStore);
-    }
-}
-
-template <bool BF16, bool DIAG>
-__device__ __forceinline__ void run_f16head(const DecodeArgs &a, TileCtx &t, int slot, DecodeShared<128> &sh)
-{
-    // the tile record is 128 rows x 128 binary16 values, then the unused r and c
-    uint8_t *rec = a.pool.base + static_cast<uint64_t>(slot) * a.pool.slot_bytes + t.off;
-    t.codes = reinterpret_cast<uint32_t *>(rec);
-    t.rr = reinterpret_cast<const float *>(rec + 128 * 256);
-    t.cc = t.rr + 128;
-    decode_f16head<BF16, DIAG>(a, t, sh);
-}
-
 template <bool BF16, bool DIAG, int L>
 __device__ __forceinline__ void run_uniform(const DecodeArgs &a, TileCtx &t, int slot, DecodeShared<128> &sh)
 {

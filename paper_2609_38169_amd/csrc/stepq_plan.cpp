@@ -268,6 +268,8 @@ bool refit_body_runs(int code, const HeadInfo &hi, int dk)
     // the row-mix class has a refitting body of its own (the dual-axis fit;
     // the row-absmax step takes the generic body, which runs these heads too)
     if (code == kRowMix) return rowmix_head(hi, dk);
+    // the combined launch of the uniform refitting bodies and whole FP16 heads
+    if (code == kMultiUniform) return compiled(L);
     // every other code runs the generic refitting body, which reads the
     // head's own record (the tight layout, or a padded uniform mix)
     return !compiled(L);
@@ -350,9 +352,13 @@ bool check_plan(const LaunchPlan &plan, const std::vector<HeadInfo> &heads, int 
     }
     if (next != Hv) return fail_check(err, "the classes do not cover the head list");
     if (plan.mixed_code != 0)
-        for (const LaunchHead &lh : plan.order)
+        for (const LaunchHead &lh : plan.order) {
             if (!decode_body_runs(plan.mixed_code, heads[lh.h], dk))
                 return fail_check(err, "the combined launch's body does not run head " + std::to_string(lh.h));
+            // the refit takes the combined launch only for kMultiUniform
+            if (plan.mixed_code == kMultiUniform && !refit_body_runs(plan.mixed_code, heads[lh.h], dk))
+                return fail_check(err, "the combined refitting launch does not run head " + std::to_string(lh.h));
+        }
     return true;
 }
 

@@ -776,6 +776,19 @@ __device__ __forceinline__ void refit_rowmix(const DecodeArgs &a, const TileCtx 
         });
 }
 
+// A tile of uniform layout L: codes (1024 bytes per word-step), then r, c.
+template <bool BF16, bool DIAG, int L, Refit MODE>
+__device__ __forceinline__ void run_refit_uniform(const DecodeArgs &a, TileCtx &t, int slot, RefitShared<128> &sh)
+{
+    constexpr UniformLayout u = kUniformLayouts[L - 1];
+    constexpr uint32_t r_off = 1024u * (u.m8 + u.m4 + u.m2);
+    uint8_t *rec = a.pool.base + static_cast<uint64_t>(slot) * a.pool.slot_bytes + t.off;
+    t.codes = reinterpret_cast<uint32_t *>(rec);
+    t.rr = reinterpret_cast<const float *>(rec + r_off);
+    t.cc = t.rr + 128;
+    refit_uniform<BF16, DIAG, u.m8, u.m4, u.m2, MODE>(a, t, sh);
+}
+
 template <int DV, bool BF16, int LAYOUT, bool DIAG, Refit MODE>
 __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
 {
@@ -793,13 +806,19 @@ __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
     t.alpha = DIAG ? 1.0f : act_ld<BF16>(a.alpha, t.tile);
     t.beta = act_ld<BF16>(a.beta, t.tile);
     if constexpr (UNIFORM) {
-        constexpr UniformLayout u = kUniformLayouts[LAYOUT - 1];
-        constexpr uint32_t r_off = 1024u * (u.m8 + u.m4 + u.m2);
-        uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.off;
-        t.codes = reinterpret_cast<uint32_t *>(rec);
-        t.rr = reinterpret_cast<const float *>(rec + r_off);
-        t.cc = t.rr + 128;
-        refit_uniform<BF16, DIAG, u.m8, u.m4, u.m2, MODE>(a, t, sh);
+        run_refit_uniform<BF16, DIAG, LAYOUT, MODE>(a, t, slot, sh);
+    } else if constexpr (DV == 128 && LAYOUT == kMultiUniform) {
+        // heads of several uniform layouts and whole FP16 heads in one launch
+        // (the head list), each tile on its own body; a whole FP16 head has
+        // no integer rows to fit and takes the frozen-step body
+        switch (t.layout) {
+        case 1: run_refit_uniform<BF16, DIAG, 1, MODE>(a, t, slot, sh); break;
+        case 2: run_refit_uniform<BF16, DIAG, 2, MODE>(a, t, slot, sh); break;
+        case 3: run_refit_uniform<BF16, DIAG, 3, MODE>(a, t, slot, sh); break;
+        case 4: run_refit_uniform<BF16, DIAG, 4, MODE>(a, t, slot, sh); break;
+        case 5: run_refit_uniform<BF16, DIAG, 5, MODE>(a, t, slot, sh); break;
+        default: run_f16head<BF16, DIAG>(a, t, slot, sh.d); break;
+        }
     } else {
         t.hi = P.heads[t.h];
         uint8_t *rec = P.base + static_cast<uint64_t>(slot) * P.slot_bytes + t.hi.tile_off;
@@ -831,6 +850,9 @@ hipError_t launch_refit_any(const DecodeArgs &a, int layout, unsigned grid, hipS
         case 5: hipLaunchKernelGGL((refit_kernel<128, BF16, 5, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a); break;
         case kRowMix:
             hipLaunchKernelGGL((refit_kernel<128, BF16, kRowMix, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+            break;
+        case kMultiUniform:
+            hipLaunchKernelGGL((refit_kernel<128, BF16, kMultiUniform, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
             break;
         default: hipLaunchKernelGGL((refit_kernel<128, BF16, 0, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a); break;
         }

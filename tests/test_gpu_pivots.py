@@ -217,8 +217,9 @@ def test_pivot_pool_b512_lockstep(mode):
 def test_fp16_heads_pool_b512_lockstep(mode):
     """The B=512 pool with two value heads kept entirely in FP16 (the
     frozen step takes one launch holding the 6-bit, FP16-head and generic
-    bodies; the refitting steps one launch per class), sampled slots
-    compared lockstep."""
+    bodies, the refit one launch of the 6-bit refitting body and the
+    FP16-head body, the row-absmax step one launch per class), sampled
+    slots compared lockstep."""
     w = W.workload(2)
     bits = row_bits(w)
     bits[W.pivot_head_draw(w, 0, 2).numpy()] = 16
@@ -276,12 +277,14 @@ def test_calibrated_head_map_runs_lockstep():
 
 
 @pytest.mark.timeout(900)
-def test_calibrated_head_map_pool_b512_every_tile():
+@pytest.mark.parametrize("refit", [False, True])
+def test_calibrated_head_map_pool_b512_every_tile(refit):
     """The head-unit calibrated map that ``bench.py --calibrated head`` times
     (whole heads at 8 or 4 bits and one whole FP16 head, from the
-    calibration pipeline on the workload's own draws) at full pool_b512
-    size with frozen scales: the decode step is one launch over the
-    compiled bodies of both widths and the FP16 body, and every tile
+    calibration pipeline on the workload's own draws: the paper's GDN
+    setting) at full pool_b512 size, with frozen scales and with the online
+    refit: either step is one launch over the compiled bodies of both
+    widths (frozen-step or refitting) and the FP16 body, and every tile
     matches the oracle lockstep."""
     from paper_2609_38169_amd.calibrate import calibrate
     w = W.workload(2)
@@ -296,7 +299,7 @@ def test_calibrated_head_map_pool_b512_every_tile():
     assert full16.sum() == 1 and all(len(set(np.unique(b))) == 1 for b in bits)
     _say(f"calibrated head map pool_b512: {int((bits[:, 0] == 8).sum())} heads @8, "
          f"{int((bits[:, 0] == 4).sum())} @4, 1 FP16 head")
-    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, row_weight=cal.row_weight, say=_say, bits=bits)
+    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, refit=refit, row_weight=cal.row_weight, say=_say, bits=bits)
 
 
 @pytest.mark.parametrize("kind", ["pivot_rows", "fp16_head"])
