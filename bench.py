@@ -68,8 +68,9 @@ def mode_name(mode) -> str:
     return {False: "decode", True: "refit", "row_absmax": "rowmax"}[mode]
 
 
-def traffic_file(mode, kda: bool, workload: str = "pool_b512", pivots: bool = False) -> str:
-    name = mode_name(mode) + ("_kda" if kda else "") + ("_pivots" if pivots else "")
+def traffic_file(mode, kda: bool, workload: str = "pool_b512", pivots: bool = False, calibrated=None) -> str:
+    name = (mode_name(mode) + ("_kda" if kda else "") + ("_pivots" if pivots else "")
+            + (f"_calibrated_{calibrated}" if calibrated else ""))
     return os.path.join(ROOT, "profiles", f"traffic_{name}_{workload}.json")
 
 
@@ -162,13 +163,13 @@ def cpu_baseline(w, bits, seconds: float):
                             "sample": f"{step1} decode steps of the same tiles, {elapsed1:.1f} s"}}
 
 
-def traffic_entry(mode, kda: bool, workload: str = "pool_b512", pivots: bool = False):
+def traffic_entry(mode, kda: bool, workload: str = "pool_b512", pivots: bool = False, calibrated=None):
     """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, scaled by a plain
     copy's counters) from the committed rocprofv3 summary of this kernel,
     mode and workload, if it was taken on the current kernel source; else
     None."""
     try:
-        t = json.load(open(traffic_file(mode, kda, workload, pivots)))
+        t = json.load(open(traffic_file(mode, kda, workload, pivots, calibrated)))
     except (OSError, ValueError):
         return None
     if t.get("kernel_sha") != kernel_hash(mode):
@@ -519,8 +520,8 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic_entry(mode, args.kda, w.name, args.pivots)
-                       if not (args.fp16_heads or args.calibrated) else None,
+            "traffic": traffic_entry(mode, args.kda, w.name, args.pivots, args.calibrated)
+                       if not args.fp16_heads else None,
             "valu": {"achieved": valu_tops, "peak": VALU_PEAK_TOPS, "unit": "Top/s", "frac": valu_tops / VALU_PEAK_TOPS,
                      "ops_per_element": valu_ops, "matrix_core_ops_per_element": MATRIX_CORE_OPS[mode]},
             "kernel": kern_name,
