@@ -85,12 +85,23 @@ def log(msg: str):
     print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
+def source_code(path: str) -> bytes:
+    """A C++ source without its comments and blank lines (string literals
+    in these sources hold no comment markers)."""
+    import re
+    text = open(path, encoding="utf-8").read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(line.rstrip() for line in text.splitlines() if line.strip()).encode()
+
+
 def kernel_hash(mode=False) -> str:
-    """Hash of the sources of the timed kernel, to tell whether committed
-    counter summaries were taken on it."""
+    """Hash of the code of the timed kernel's sources (comments and blank
+    lines left out), to tell whether committed counter summaries were taken
+    on it."""
     h = hashlib.sha256()
     for f in kernel_sources(mode):
-        h.update(open(f, "rb").read())
+        h.update(source_code(f))
     return h.hexdigest()[:16]
 
 

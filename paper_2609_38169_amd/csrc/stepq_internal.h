@@ -73,7 +73,9 @@ struct TileArgs {
 // kMixedBase + L / kMixedF16Base + L (decode step only) for uniform layout-L
 // heads mixed with such pivot heads, compact generic (and whole FP16) heads.
 // The refitting steps take their generic body for kCompactGeneric and
-// kPivotUniformBase + L.
+// kPivotUniformBase + L; the refit takes its row-mix body for kRowMix and
+// one launch over the uniform refitting bodies and the FP16-head body for
+// kMultiUniform (the row-absmax step launches such pools per class).
 // diag: a.alpha holds the channel-wise gate [batch][Hv][d_k] instead of the
 // scalar gate [batch][Hv].
 hipError_t launch_decode(const DecodeArgs &a, bool bf16, bool diag, int pool_layout, hipStream_t stream);
