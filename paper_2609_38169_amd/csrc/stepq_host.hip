@@ -348,11 +348,13 @@ static stepq_status decode_step_impl(stepq_pool *p, const int32_t *slot_ids, int
     };
     hipError_t e = hipSuccess;
     const stepq::LaunchPlan &plan = p->plan;
-    const bool refit_multi = (flags & STEPQ_STEP_REFIT) && plan.mixed_code == stepq::kMultiUniform;
+    // the combined launches the refit has bodies for: several uniform layouts
+    // and whole FP16 heads, or one uniform layout and its padded pivot heads
+    const bool refit_multi = (flags & STEPQ_STEP_REFIT) && stepq::refit_combined(plan.mixed_code);
     if ((plan.mixed_code != 0 && !(flags & (STEPQ_STEP_REFIT | STEPQ_STEP_ROW_ABSMAX))) || refit_multi) {
         // uniform heads share one launch with compact generic and whole FP16
-        // heads; with the refit, heads of several uniform layouts and whole
-        // FP16 heads share one launch of the refitting bodies
+        // heads; with the refit, the heads of refit_combined's launches share
+        // one launch of the refitting bodies
         a.head_list = p->d_head_order;
         a.n_heads = p->Hv;
         a.div_heads = fast_div(static_cast<uint32_t>(p->Hv));

@@ -67,25 +67,7 @@ __device__ __forceinline__ void decode_uniform(const DecodeArgs &a, const TileCt
     unpack_row_pairs<M8, M4, M2>(w, Ub);
     __syncthreads();    // operand table written
     matvec_partials(sh, slice, cg, Ub, ek, eq);
-    if constexpr (PIV) {
-        // pivot row p = slice (at most one per thread: kCompactPivots = 8
-        // slices): its share k_i S_pj / c_j and q_i S_pj / c_j (the column
-        // phase multiplies by c_j), added to this thread's own partials
-        static_assert(PivotRegs<128, kCompactPivots>::M == 1, "one pivot row per thread");
-        if (slice < t.hi.n16) {
-            const float4 c4 = *reinterpret_cast<const float4 *>(&sh.cpiv[4 * cg]);
-            const uint32_t lo = pr.v[0].x, hi = pr.v[0].y;
-            const float sv[4] = {half_lo(lo) * __builtin_amdgcn_rcpf(c4.x), half_hi(lo) * __builtin_amdgcn_rcpf(c4.y),
-                                 half_lo(hi) * __builtin_amdgcn_rcpf(c4.z), half_hi(hi) * __builtin_amdgcn_rcpf(c4.w)};
-            const float4 kp = sh.pvc[slice];
-            float4 &rk = sh.red[0][slice][cg];
-            rk = make_float4(fmaf(kp.x, sv[0], rk.x), fmaf(kp.x, sv[1], rk.y), fmaf(kp.x, sv[2], rk.z),
-                             fmaf(kp.x, sv[3], rk.w));
-            float4 &rq = sh.red[1][slice][cg];
-            rq = make_float4(fmaf(kp.y, sv[0], rq.x), fmaf(kp.y, sv[1], rq.y), fmaf(kp.y, sv[2], rq.z),
-                             fmaf(kp.y, sv[3], rq.w));
-        }
-    }
+    if constexpr (PIV) pivot_partials_slice(t, slice, cg, pr, sh);
 
     column_sums<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh, kappa, op.c, op.v);
 
@@ -245,20 +227,7 @@ template <bool BF16, bool DIAG, int L>
 __device__ __forceinline__ void run_uniform_piv(const DecodeArgs &a, TileCtx &t, int slot, DecodeShared<128> &sh)
 {
     constexpr UniformLayout u = kUniformLayouts[L - 1];
-    constexpr uint32_t piv_off = 1024u * (u.m8 + u.m4 + u.m2);
-    const int n16 = t.counts & 0xff, n8 = (t.counts >> 8) & 0xff, n4 = (t.counts >> 16) & 0xff;
-    t.hi.n16 = static_cast<uint16_t>(n16);
-    t.hi.n8 = static_cast<uint16_t>(n8);
-    t.hi.n4 = static_cast<uint16_t>(n4);
-    t.hi.n2 = static_cast<uint16_t>(128 - n16 - n8 - n4);
-    t.hi.g8 = static_cast<uint16_t>(8 * u.m8);
-    t.hi.g4 = static_cast<uint16_t>(8 * u.m4);
-    t.hi.g2 = static_cast<uint16_t>(8 * u.m2);
-    t.hi.piv_off = piv_off;
-    uint8_t *rec = a.pool.base + static_cast<uint64_t>(slot) * a.pool.slot_bytes + t.off;
-    t.codes = reinterpret_cast<uint32_t *>(rec);
-    t.rr = reinterpret_cast<const float *>(rec + piv_off + 256u * static_cast<uint32_t>(n16));
-    t.cc = t.rr + 128;
+    padded_pivot_tile<L>(a, t, slot);
     decode_uniform<BF16, DIAG, u.m8, u.m4, u.m2, true>(a, t, sh);
 }
 

@@ -261,6 +261,11 @@ bool decode_body_runs(int code, const HeadInfo &hi, int dk)
     return false;
 }
 
+bool refit_combined(int mixed_code)
+{
+    return mixed_code == kMultiUniform || (mixed_code > kMixedPivotBase && mixed_code <= kMixedPivotBase + 2);
+}
+
 bool refit_body_runs(int code, const HeadInfo &hi, int dk)
 {
     const int L = static_cast<int>(hi.layout);
@@ -270,6 +275,14 @@ bool refit_body_runs(int code, const HeadInfo &hi, int dk)
     if (code == kRowMix) return rowmix_head(hi, dk);
     // the combined launch of the uniform refitting bodies and whole FP16 heads
     if (code == kMultiUniform) return compiled(L);
+    // padded pivot heads have a refitting body of their own (the dual-axis
+    // fit; the row-absmax step takes the generic body, which runs them too),
+    // which also runs the heads of their uniform layout in one launch
+    if (pivot_uniform(code)) return L == code;
+    if (code > kMixedPivotBase && code <= kMixedPivotBase + 2) {
+        const int u = code - kMixedPivotBase;
+        return L == u || L == kPivotUniformBase + u;
+    }
     // every other code runs the generic refitting body, which reads the
     // head's own record (the tight layout, or a padded uniform mix)
     return !compiled(L);
@@ -355,8 +368,8 @@ bool check_plan(const LaunchPlan &plan, const std::vector<HeadInfo> &heads, int 
         for (const LaunchHead &lh : plan.order) {
             if (!decode_body_runs(plan.mixed_code, heads[lh.h], dk))
                 return fail_check(err, "the combined launch's body does not run head " + std::to_string(lh.h));
-            // the refit takes the combined launch only for kMultiUniform
-            if (plan.mixed_code == kMultiUniform && !refit_body_runs(plan.mixed_code, heads[lh.h], dk))
+            // the refit takes the combined launches that refit_combined names
+            if (refit_combined(plan.mixed_code) && !refit_body_runs(plan.mixed_code, heads[lh.h], dk))
                 return fail_check(err, "the combined refitting launch does not run head " + std::to_string(lh.h));
         }
     return true;

@@ -45,6 +45,9 @@ void plan_launches(const std::vector<HeadInfo> &heads, int dk, int dv, LaunchPla
 // `hi`, and the same for the refitting bodies (refit and row-absmax).
 bool decode_body_runs(int code, const HeadInfo &hi, int dk);
 bool refit_body_runs(int code, const HeadInfo &hi, int dk);
+// Whether the refit runs a plan's combined launch (mixed_code) as one
+// launch of its refitting bodies (else it launches per class).
+bool refit_combined(int mixed_code);
 
 // Tile size that the compiled body of layout code L (1 .. kF16HeadLayout)
 // assumes for every head when it runs without a head list; 0 otherwise.

@@ -312,8 +312,13 @@ __device__ __forceinline__ void ld4(const float *p, float (&v)[4])
 }
 
 // Uniform layouts at d_v = 128: widths known at compile time, all 64 values
-// of the thread kept in registers across the four passes.
-template <bool BF16, bool DIAG, int M8, int M4, int M2, Refit MODE>
+// of the thread kept in registers across the four passes.  PIV: a padded
+// pivot head (up to kCompactPivots FP16 pivot rows beside the padded mix,
+// t.hi from the head list): its pivot rows join the sums over rows and are
+// updated in binary16, and take no part in the fits; the padded mix's empty
+// slots (zero codes, no row) get h = W = 0, so they add nothing to the fits
+// and keep zero codes.
+template <bool BF16, bool DIAG, int M8, int M4, int M2, Refit MODE, bool PIV = false>
 __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx &t, RefitShared<128> &sh)
 {
     // uniform layouts take the lean row-absmax body of stepq_rowmax.hip
@@ -330,6 +335,8 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     uint32_t w[M];
 #pragma unroll
     for (int m = 0; m < M; ++m) w[m] = cw.load_m(tid, m);
+    PivotRegs<128, kCompactPivots> pr;
+    if constexpr (PIV) pivot_load<128, kCompactPivots>(t, slice, cg, pr);
 
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
     if (tid < 128) {
@@ -338,11 +345,16 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     }
     // S^T k and S^T q on the matrix cores, as in the frozen-scale body
     int ek, eq;
-    const float kappa = row_constants_mfma<DIAG, M8, M4, M2, 128>(t.beta, op, sh.d, a.pool.lv, ek, eq);
+    float kappa;
+    if constexpr (PIV)
+        kappa = row_constants_mfma_piv<DIAG, M8, M4, M2, 128>(t.hi, t.alpha, t.beta, op, sh.d, a.pool.lv, ek, eq);
+    else
+        kappa = row_constants_mfma<DIAG, M8, M4, M2, 128>(t.beta, op, sh.d, a.pool.lv, ek, eq);
     uint32_t Ub[4][4][2];
     unpack_row_pairs<M8, M4, M2>(w, Ub);
     __syncthreads();    // operand table written
     matvec_partials(sh.d, slice, cg, Ub, ek, eq);
+    if constexpr (PIV) pivot_partials_slice(t, slice, cg, pr, sh.d);
 
     column_sums<128>(a, t.tile, DIAG ? 1.0f : t.alpha, t.beta, sh.d, kappa, op.c, op.v);
 
@@ -350,6 +362,7 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
     float bc[4], cc[4];
     ld4(&sh.d.bcol[4 * cg], bc);
     ld4(&sh.ccol[4 * cg], cc);
+    if constexpr (PIV) pivot_update<128, kCompactPivots>(t, slice, cg, pr, sh.d, bc);
     float Y[NE];
     bool y_done = false;
     if constexpr (!DIAG) {
@@ -372,7 +385,21 @@ __device__ __forceinline__ void refit_uniform(const DecodeArgs &a, const TileCtx
                                     t.alpha * (1.0f / 64.0f), bc, cc, &Y[Y2 + 16 * m]);
     }
     __syncthreads();
-    if (tid < 128) refit_row<128, MODE>(sh, tid, tid, tid < X4 ? 8 : (tid < X2 ? 4 : 2), op.r, rr_out, a.pool.lv);
+    if (tid < 128) {
+        if constexpr (PIV) {
+            // row-table slot tid holds physical row p, or no row
+            int bw;
+            const int p = slot_row(t.hi, tid, bw);
+            if (p >= 0) {
+                refit_row<128, MODE>(sh, tid, p, bw, sh.d.sr[p], rr_out, a.pool.lv);
+            } else {
+                sh.hrow[tid] = 0.f;
+                sh.wrow[tid] = 0.f;
+            }
+        } else {
+            refit_row<128, MODE>(sh, tid, tid, tid < X4 ? 8 : (tid < X2 ? 4 : 2), op.r, rr_out, a.pool.lv);
+        }
+    }
     __syncthreads();
 
     // pass 2: yh = y r / r' and the column maxima per width
@@ -789,6 +816,16 @@ __device__ __forceinline__ void run_refit_uniform(const DecodeArgs &a, TileCtx &
     refit_uniform<BF16, DIAG, u.m8, u.m4, u.m2, MODE>(a, t, sh);
 }
 
+// A padded pivot head of uniform layout L (its row counts from the head
+// list), or a layout-L head taken as one with no pivot rows.
+template <bool BF16, bool DIAG, int L, Refit MODE>
+__device__ __forceinline__ void run_refit_uniform_piv(const DecodeArgs &a, TileCtx &t, int slot, RefitShared<128> &sh)
+{
+    constexpr UniformLayout u = kUniformLayouts[L - 1];
+    padded_pivot_tile<L>(a, t, slot);
+    refit_uniform<BF16, DIAG, u.m8, u.m4, u.m2, MODE, true>(a, t, sh);
+}
+
 template <int DV, bool BF16, int LAYOUT, bool DIAG, Refit MODE>
 __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
 {
@@ -807,6 +844,12 @@ __global__ __launch_bounds__(256) void refit_kernel(DecodeArgs a)
     t.beta = act_ld<BF16>(a.beta, t.tile);
     if constexpr (UNIFORM) {
         run_refit_uniform<BF16, DIAG, LAYOUT, MODE>(a, t, slot, sh);
+    } else if constexpr (DV == 128 && LAYOUT > kPivotUniformBase && LAYOUT <= kPivotUniformBase + kNumUniformLayouts) {
+        run_refit_uniform_piv<BF16, DIAG, LAYOUT - kPivotUniformBase, MODE>(a, t, slot, sh);
+    } else if constexpr (DV == 128 && LAYOUT > kMixedPivotBase && LAYOUT <= kMixedPivotBase + 2) {
+        // layout-L heads and layout-L padded pivot heads in one launch of one
+        // body: a layout-L head is a padded pivot head with no pivot rows
+        run_refit_uniform_piv<BF16, DIAG, LAYOUT - kMixedPivotBase, MODE>(a, t, slot, sh);
     } else if constexpr (DV == 128 && LAYOUT == kMultiUniform) {
         // heads of several uniform layouts and whole FP16 heads in one launch
         // (the head list), each tile on its own body; a whole FP16 head has
@@ -853,6 +896,27 @@ hipError_t launch_refit_any(const DecodeArgs &a, int layout, unsigned grid, hipS
             break;
         case kMultiUniform:
             hipLaunchKernelGGL((refit_kernel<128, BF16, kMultiUniform, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+            break;
+        case kPivotUniformBase + 1:
+            hipLaunchKernelGGL((refit_kernel<128, BF16, kPivotUniformBase + 1, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+            break;
+        case kPivotUniformBase + 2:
+            hipLaunchKernelGGL((refit_kernel<128, BF16, kPivotUniformBase + 2, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+            break;
+        case kPivotUniformBase + 3:
+            hipLaunchKernelGGL((refit_kernel<128, BF16, kPivotUniformBase + 3, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+            break;
+        case kPivotUniformBase + 4:
+            hipLaunchKernelGGL((refit_kernel<128, BF16, kPivotUniformBase + 4, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+            break;
+        case kPivotUniformBase + 5:
+            hipLaunchKernelGGL((refit_kernel<128, BF16, kPivotUniformBase + 5, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+            break;
+        case kMixedPivotBase + 1:
+            hipLaunchKernelGGL((refit_kernel<128, BF16, kMixedPivotBase + 1, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
+            break;
+        case kMixedPivotBase + 2:
+            hipLaunchKernelGGL((refit_kernel<128, BF16, kMixedPivotBase + 2, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a);
             break;
         default: hipLaunchKernelGGL((refit_kernel<128, BF16, 0, DIAG, MODE>), dim3(grid), dim3(256), 0, s, a); break;
         }

@@ -204,9 +204,10 @@ def test_pivot_decode_step(case, kda, mode):
 
 @pytest.mark.parametrize("mode", [False, True, "row_absmax"])
 def test_pivot_pool_b512_lockstep(mode):
-    """The B=512 pool with pivot rows in a quarter of the heads (those heads
-    take the generic body, the rest the compiled 6-bit one), all slots
-    stepped, sampled slots compared lockstep."""
+    """The B=512 pool with pivot rows in a quarter of the heads (the frozen
+    and refitting steps run them on the padded uniform bodies in one launch
+    with the other heads, the row-absmax step on the generic body), all
+    slots stepped, sampled slots compared lockstep."""
     w = W.workload(2)
     bits = row_bits(w)
     bits[W.pivot_mask_draw(w).numpy()] = 16
@@ -302,14 +303,16 @@ def test_calibrated_head_map_pool_b512_every_tile(refit):
     PT.lockstep_run(w, 6, np.arange(w.batch), DEV, refit=refit, row_weight=cal.row_weight, say=_say, bits=bits)
 
 
+@pytest.mark.parametrize("refit", [False, True])
 @pytest.mark.parametrize("kind", ["pivot_rows", "fp16_head"])
 @pytest.mark.timeout(900)
-def test_pivot_maps_pool_b512_every_tile(kind):
+def test_pivot_maps_pool_b512_every_tile(kind, refit):
     """The maps of ``bench.py --pivots`` (1-3 FP16 pivot rows in a seeded
-    quarter of the heads, run by the padded uniform body) and
-    ``bench.py --fp16-heads 1`` (one whole FP16 head beside the uniform
-    heads, one combined launch) at full pool_b512 size with frozen scales:
-    every tile lockstep with the oracle."""
+    quarter of the heads, run by the padded uniform body, frozen-step or
+    refitting) and ``bench.py --fp16-heads 1`` (one whole FP16 head beside
+    the uniform heads, one combined launch) at full pool_b512 size, with
+    frozen scales and with the online refit: every tile lockstep with the
+    oracle."""
     from paper_2609_38169_amd.pools import row_bits
     w = W.workload(2)
     bits = row_bits(w).copy()
@@ -317,5 +320,5 @@ def test_pivot_maps_pool_b512_every_tile(kind):
         bits[W.pivot_mask_draw(w).numpy()] = 16
     else:
         bits[W.pivot_head_draw(w, 0, 1).numpy()] = 16
-    _say(f"{kind} pool_b512: {int((bits == 16).sum())} FP16 rows")
-    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, say=_say, bits=bits)
+    _say(f"{kind} pool_b512{' refit' if refit else ''}: {int((bits == 16).sum())} FP16 rows")
+    PT.lockstep_run(w, 6, np.arange(w.batch), DEV, refit=refit, say=_say, bits=bits)
