@@ -174,7 +174,7 @@ __device__ __forceinline__ void decode_rowmix(const DecodeArgs &a, const TileCtx
     PivotRegs<128, kCompactPivots> pr;
     pivot_load<128, kCompactPivots>(t, slice, cg, pr);
     const RowColOps op = load_ops<BF16, DIAG, 128>(a, t.tile, t.b, t.hq, t.h, t.rr, t.cc);
-    rowmix_sums<DIAG, true>(a, t, sh, w, pr, op, g8, ng);
+    rowmix_sums<DIAG, true, true>(a, t, sh, w, pr, op, g8, ng);
 
     const float4 b4 = *reinterpret_cast<const float4 *>(&sh.bcol[4 * cg]);
     const float bc[4] = {b4.x, b4.y, b4.z, b4.w};
