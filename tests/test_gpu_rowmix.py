@@ -52,10 +52,19 @@ def _cases():
     b[3] = 16
     b = np.concatenate([b, np.stack([_head(rng, 64, 0), _head(rng, 77, 2), _head(rng, 88, 0), _head(rng, 50, 2)])])
     cases.append((8, 4, 3, b))
+    # 3: 32 heads of seeded random splits (8-bit rows anywhere in 0..128, 0
+    # to 8 pivot rows), GQA 4:1: the width boundary and the last group fall
+    # at many offsets, and heads that happen to fit a uniform mix take their
+    # own class
+    hs = []
+    for _ in range(32):
+        npiv = int(rng.integers(0, 9))
+        hs.append(_head(rng, int(rng.integers(0, 129 - npiv)), npiv))
+    cases.append((32, 8, 3, np.stack(hs)))
     return cases
 
 
-N_CASES = 3
+N_CASES = 4
 
 
 def _state(case, seed):
