@@ -239,3 +239,14 @@ def test_rowmix_calibrated_refit_pool_b512_every_tile(kda, levels):
     w, bits, row_weight = _calibrated_row_map()
     PT.lockstep_run(w, 6, np.arange(w.batch), DEV, refit=True, row_weight=row_weight, say=_say, bits=bits,
                     kda=kda, levels=levels)
+
+
+@pytest.mark.timeout(900)
+def test_rowmix_kda_setting_refit_64_steps():
+    """The paper's KDA decode step (row-unit calibrated map with FP16 pivot
+    rows, channel-wise gates on the 2^(8-b) q codebook, the dual-axis refit
+    every step) over 64 steps of the full pool_b512 launch: a third of the
+    requests (every head) lockstep with the oracle at every step."""
+    w, bits, row_weight = _calibrated_row_map()
+    PT.lockstep_run(w, 64, np.arange(0, w.batch, 3), DEV, refit=True, row_weight=row_weight, say=_say, bits=bits,
+                    kda=True, levels=1)
