@@ -651,9 +651,9 @@ __device__ __forceinline__ void rm_row_y(uint32_t W, const DecodeShared<128> &d,
     for (int e = 0; e < 4; ++e) y[e] = fmaf(al, sbyte(W, e), a_s * bc[e]);
 }
 
-// Calls f8(g) for an 8-bit word-step of group g and f4(g) for a 4-bit one
-// whose group holds codes, over the thread's word-steps m (group g = slice
-// + 8 m), for every m while 8 m < ng.
+// Calls f8(m, g) for word-step m of the thread if its group g = slice + 8 m
+// is 8-bit, or f4(m, g) if it is a 4-bit group that holds codes (g < ng),
+// for every m while 8 m < ng.
 template <class F8, class F4>
 __device__ __forceinline__ void rm_each_step(int slice, int g8, int ng, F8 &&f8, F4 &&f4)
 {
