@@ -83,11 +83,16 @@ __device__ __forceinline__ float row_z(uint32_t hp, int half, float coef, float 
 // requantized from z.  Two barriers.
 template <bool DIAG, int M8, int M4, int M2, int H>
 __device__ __forceinline__ void rowmax_half(const TileCtx &t, RowmaxShared &sh, const uint32_t (&Ub)[4][4][2],
-                                            const float (&dl)[4], const float (&cl)[4], float *part,
-                                            const CodeWords &cw)
+                                            float *part, const CodeWords &cw)
 {
     const int tid = threadIdx.x;
     const int cg = tid & 31, slice = tid >> 5;
+    // delta_j and c_j of the thread's columns, read for each half: they are
+    // not held through the other half's reduction
+    const float4 d4 = *reinterpret_cast<const float4 *>(&sh.dcol[4 * cg]);
+    const float4 c4 = *reinterpret_cast<const float4 *>(&sh.ccol[4 * cg]);
+    const float dl[4] = {d4.x, d4.y, d4.z, d4.w};
+    const float cl[4] = {c4.x, c4.y, c4.z, c4.w};
     float z[8][4];
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -181,14 +186,10 @@ __device__ __forceinline__ void rowmax_uniform(const DecodeArgs &a, const TileCt
     // The thread's 16 rows in two halves of 8: each half forms its z,
     // reduces its row maxima and is requantized before the next half's z
     // exist, so at most 32 z values are live
-    const float4 d4 = *reinterpret_cast<const float4 *>(&sh.dcol[4 * cg]);
-    const float4 c4 = *reinterpret_cast<const float4 *>(&sh.ccol[4 * cg]);
-    const float dl[4] = {d4.x, d4.y, d4.z, d4.w};
-    const float cl[4] = {c4.x, c4.y, c4.z, c4.w};
     float *part = reinterpret_cast<float *>(&sh.d.red[0][0][0]);    // [128 rows][16 lane pairs]
     if (tid < 128) const_cast<float *>(t.cc)[tid] = 1.0f;    // c' = 1 (c was read at the start)
-    rowmax_half<DIAG, M8, M4, M2, 0>(t, sh, Ub, dl, cl, part, cw);
-    rowmax_half<DIAG, M8, M4, M2, 1>(t, sh, Ub, dl, cl, part, cw);
+    rowmax_half<DIAG, M8, M4, M2, 0>(t, sh, Ub, part, cw);
+    rowmax_half<DIAG, M8, M4, M2, 1>(t, sh, Ub, part, cw);
 }
 
 template <bool BF16, int LAYOUT, bool DIAG>
