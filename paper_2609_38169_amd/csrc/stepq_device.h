@@ -966,9 +966,8 @@ __device__ __forceinline__ void rowmix_column(const DecodeShared<128> &sh, const
 // word groups (four accumulators live): each group's slot views are formed
 // once rather than once per column.  For bodies whose register peak lies
 // after the column phase (the refitting body).
-__device__ __forceinline__ void rowmix_columns4(const DecodeShared<128> &sh, const uint32_t (&w)[16],
-                                                const uint32_t (&vb)[4], int slice, int cg, int g8, int ng, int ek,
-                                                int eq, float *redK, float *redQ)
+__device__ __forceinline__ void rowmix_columns4(const DecodeShared<128> &sh, const uint32_t (&w)[16], int slice,
+                                                int cg, int g8, int ng, int ek, int eq, float *redK, float *redQ)
 {
     f32x4 d0 = {0.f, 0.f, 0.f, 0.f}, d1 = d0, d2 = d0, d3 = d0;
     auto all = [&](const _Float16 (&A)[4][4], const uint32_t (&v)[4]) {
@@ -990,7 +989,11 @@ __device__ __forceinline__ void rowmix_columns4(const DecodeShared<128> &sh, con
                 for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 0);
                 all(sh.aopv[slice][j][0], v);
             } else {
-                all(sh.aopv[slice][j][0], vb);    // the group of the width boundary
+                // the group of the width boundary: 8-bit below g8, slot 0 of a 4-bit group above
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    v[k] = slice + 8 * (4 * j + k) < g8 ? w[4 * j + k] : slot_top<4>(w[4 * j + k], 0);
+                all(sh.aopv[slice][j][0], v);
             }
 #pragma unroll
             for (int k = 0; k < 4; ++k) v[k] = slot_top<4>(w[4 * j + k], 1);
@@ -1032,17 +1035,17 @@ __device__ __forceinline__ void rowmix_sums(const DecodeArgs &a, const TileCtx &
     float *redK = &sh.red[0][slice][cg].x, *redQ = &sh.red[1][slice][cg].x;
     // slot-0 views of the word group holding the width boundary (if any),
     // formed once: there the width changes from one slice to the next
-    uint32_t vb[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        if ((g8 >> 5) == j && (g8 & 31) != 0) {
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                vb[k] = slice + 8 * (4 * j + k) < g8 ? w[4 * j + k] : slot_top<4>(w[4 * j + k], 0);
-        }
     if constexpr (ALLCOLS) {
-        rowmix_columns4(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
+        rowmix_columns4(sh, w, slice, cg, g8, ng, ek, eq, redK, redQ);
     } else {
+        uint32_t vb[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if ((g8 >> 5) == j && (g8 & 31) != 0) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    vb[k] = slice + 8 * (4 * j + k) < g8 ? w[4 * j + k] : slot_top<4>(w[4 * j + k], 0);
+            }
         rowmix_column<0>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
         rowmix_column<1>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
         rowmix_column<2>(sh, w, vb, slice, cg, g8, ng, ek, eq, redK, redQ);
